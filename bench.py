@@ -1,0 +1,178 @@
+"""Throughput of one pipeline stage's work per mini-batch on one MI355X.
+
+Workload (default): partition 1 of the 4-way split of a 5-level U-Net
+(base 64 -> 1024 channels), input 32x64x192x192 bf16 ~ N(0,1), m = 8
+micro-batches, checkpoint = always.  A step is the whole stage: the m
+forwards F_{i,1} (keeping only their inputs), then for i = m..1 the
+recompute F'_{i,1}, the backward B_{i,1} (data gradient of the stage input
+included) and the accumulation of g_i.  Upstream gradients of the stage's
+output and of its three exported skips are seeded inputs, resident in HBM
+with everything else before timing starts.
+
+Prints one JSON line.  `--gpus N` with N > 1 is not supported: this build
+runs on a single GPU.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+
+BF16_PEAK = 2.5e15      # MI355X dense bf16 MFMA, FLOP/s
+HBM_PEAK = 8.0e12       # MI355X HBM3E, B/s
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(wl, lo, hi, samples, dtype):
+    """The oracle (float64 CPU, bf16 storage points) on a bounded sample of the
+    same workload: `samples` single-sample forward + backward passes of the
+    stage at full per-sample shape."""
+    import numpy as np
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count()
+    import oracle
+    from oracle import network
+    from workloads import synth
+    net = wl.net
+    P = oracle.net_params(net, dtype)
+    ex = network.exported_stashes(net, lo, hi)
+    shapes = net.shapes()
+    out_shapes = [(net.layers[hi - 1].cout,) + tuple(shapes[hi - 1])]
+    for sid in ex:
+        k = [q for q, L in enumerate(net.layers) if L.stash_id == sid][0]
+        out_shapes.append((net.layers[k].cout,) + tuple(shapes[k]))
+    xs = synth.quantize(synth.normal(101, (samples, net.in_channels, net.height, net.width)), dtype)[0]
+    Gs = [synth.quantize(synth.normal(102 + k, (samples,) + s), dtype)[0] for k, s in enumerate(out_shapes)]
+    t0 = time.perf_counter()
+    for s in range(samples):
+        network.run(net, P, xs[s:s + 1], lo=lo, hi=hi, out_grads=[g[s:s + 1] for g in Gs],
+                    storage="bf16")
+    dt = time.perf_counter() - t0
+    return {"value": samples / dt, "unit": "samples/s", "cores": cores, "kind": "oracle",
+            "sample": f"{samples} single-sample forward+backward passes of the stage at full "
+                      f"per-sample shape (no recompute, float64 with bf16 storage rounding), "
+                      f"{dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-samples", type=int, default=6)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--mode", default="always", choices=["always", "except_last", "never"])
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); this build has no "
+              f"multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2004_09910_amd as tgp
+    from paper_2004_09910_amd.harness import Session, nchw_to_device_nhwc
+    from workloads import specs, synth
+    from workloads.specs import BF16, CKPT_NAMES
+
+    wl = specs.unet_stage()
+    net = wl.net
+    mode = CKPT_NAMES[args.mode]
+    log("setting up", wl.name)
+    sess = Session(net, BF16, n=wl.n, bind_layers=None)
+    lo, hi = sess.bounds[0]
+    sess.plan(wl.batch, wl.m, mode)
+    B, m = wl.batch, wl.m
+    _, xraw = synth.input_x(net, B, BF16)
+    x = nchw_to_device_nhwc(xraw, BF16)
+    C, H, W = sess.part_out_shape(1)
+    y = torch.empty((B, H, W, C), dtype=torch.bfloat16, device="cuda")
+    _, g0 = synth.target_like((B, C, H, W), BF16, 0)
+    dy = nchw_to_device_nhwc(g0, BF16)
+    dx = torch.empty_like(x)
+    b = B // m
+    for k, sid in enumerate(sess.exported_stashes(1)):
+        _, gk = synth.target_like((B,) + sess.stash_shape(sid), BF16, 1 + k)
+        gd = nchw_to_device_nhwc(gk, BF16)
+        for i in range(1, m + 1):
+            sess.stash_view(i, sid, True).copy_(gd[(i - 1) * b:i * b])
+    del xraw
+    stream = torch.cuda.current_stream().cuda_stream
+    torch.cuda.synchronize()
+
+    log("warmup", args.warmup)
+    for _ in range(args.warmup):
+        sess.stage_step(1, x, y, dy, dx, stream)
+    torch.cuda.synchronize()
+
+    # timed region, with per-kernel HIP events on the launch stream
+    tgp.profile_enable(True)
+    tgp.profile_read()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        sess.stage_step(1, x, y, dy, dx, stream)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    stats = tgp.profile_read()
+    tgp.profile_enable(False)
+    elapsed = t1 - t0
+    ms_step = 1e3 * elapsed / args.steps
+    log(f"timed {args.steps} steps: {ms_step:.3f} ms/step")
+
+    fwd_flops = sum(net.flops_per_sample()[lo:hi]) * B
+    recompute = {specs.CKPT_ALWAYS: 1.0, specs.CKPT_EXCEPT_LAST: (m - 1) / m,
+                 specs.CKPT_NEVER: 0.0}[mode]
+    step_flops = fwd_flops * (3.0 + recompute)    # forward, recompute, dgrad, wgrad
+    samples_s = B * args.steps / elapsed
+
+    stats.sort(key=lambda r: -r["ms"])
+    for r in stats:
+        log(f"  {r['name']:32s} n={r['launches']:6d} {r['ms']:9.3f} ms "
+            f"{(r['flops'] / (r['ms'] * 1e-3) / 1e12) if r['ms'] > 0 else 0:8.1f} TF/s "
+            f"{(r['bytes'] / (r['ms'] * 1e-3) / 1e9) if r['ms'] > 0 else 0:8.1f} GB/s")
+    dom = stats[0]
+    per_launch_ms = dom["ms"] / dom["launches"]
+    if dom["flops"] > 0:
+        achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": achieved, "peak": BF16_PEAK / 1e12,
+                "unit": "TFLOP/s", "frac": achieved / (BF16_PEAK / 1e12), "traffic": None}
+    else:
+        achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                "frac": achieved / (HBM_PEAK / 1e9), "traffic": None}
+    roof["kernel"] = dom["name"]
+    roof["launches_per_step"] = dom["launches"] / args.steps
+    roof["avg_launch_us"] = 1e3 * per_launch_ms
+    kernel_ms = sum(r["ms"] for r in stats) / args.steps
+
+    out = {
+        "metric": "stage fwd+recompute+bwd samples/sec at 1 MI355X; MFMA util % of bf16 peak",
+        "value": samples_s, "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "network": net.name, "partition": f"1 of {wl.n}",
+                   "layers": hi - lo, "global_batch": B, "micro_batches": m,
+                   "checkpoint": args.mode, "input": f"{B}x{net.in_channels}x{net.height}x{net.width}",
+                   "dx_in": True},
+        "mfma_util_pct": 100.0 * step_flops / (ms_step * 1e-3) / BF16_PEAK,
+        "step_tflop": step_flops / 1e12,
+        "kernel_busy_ms_per_step": kernel_ms,
+        "roofline": roof,
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline")
+        out["cpu_baseline"] = cpu_baseline(wl, lo, hi, args.cpu_samples, BF16)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,210 @@
+/*
+ * tgp.h -- C ABI of an MI355X (gfx950) micro-batch pipeline stage with
+ * checkpointing: the GPipe method of torchgpipe (Kim et al., arXiv
+ * 2004.09910) taken at the scale of one GPU.
+ *
+ * The network is a sequence of black-box, referentially transparent layers
+ * (Sec. 3) cut into n contiguous partitions f^1..f^n (Sec. 2).  A mini-batch
+ * of B samples is split into m micro-batches of b = B/m samples.  The four
+ * entry points the method is built from are
+ *
+ *   tgp_stage_forward            task F_{i,j}   (eq. (F_ij); Sec. 2.1 checkpointing)
+ *   tgp_stage_backward_recompute F'_{i,j} then B_{i,j}  (eq. (B_ij); Sec. 2.1)
+ *   tgp_grad_accumulate          g^j += g_i^j   (Sec. 2, sum of g_i^j over i)
+ *   tgp_pipeline_step            all tasks in deterministic clock-cycle order
+ *                                (Algorithm 1, Sec. 3.2.1) and its reverse
+ *
+ * Conventions for every call
+ *   - Tensors are NHWC.  Activations, activation gradients and weights are
+ *     bfloat16 (raw 16-bit storage) for TGP_BF16 nets and float32 for
+ *     TGP_FP32 nets.  Biases, weight-gradient accumulators and the loss are
+ *     float32 in both.  Weights are KRSC: [cout][kh][kw][cin] for 3x3 and 1x1
+ *     convolutions, [c][3][3] for depthwise.
+ *   - Device pointers are plain device addresses owned by the caller.  The
+ *     library never allocates device memory: the caller sizes a workspace with
+ *     tgp_plan and binds it with tgp_bind_workspace.  Pointers must stay
+ *     valid for as long as the calls that use them may run.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Calls enqueue work and return without synchronising; kernel faults
+ *     surface at the caller's next synchronisation.
+ *   - All argument and state checks run on the host before anything is
+ *     enqueued.  A call that returns an error has enqueued nothing, except
+ *     TGP_EHIP, which reports a failed launch (tgp_last_error names it).
+ *   - A tgp_net is not thread safe.  Results are deterministic: every
+ *     reduction has a fixed order, no kernel uses floating-point atomics, and
+ *     kernel choice and launch shape depend only on tensor shapes.
+ */
+#ifndef TGP_H
+#define TGP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct tgp_net tgp_net;
+
+typedef enum {
+  TGP_OK = 0,
+  TGP_EINVAL = 1,       /* bad argument (shape, index, NULL pointer, mismatch) */
+  TGP_ESTATE = 2,       /* call out of the order the method requires */
+  TGP_ENOSPACE = 3,     /* bound workspace smaller than tgp_plan asked for */
+  TGP_EHIP = 4,         /* a HIP launch failed */
+  TGP_EUNSUPPORTED = 5  /* layer/dtype combination not built */
+} tgp_status;
+
+typedef enum { TGP_BF16 = 0, TGP_FP32 = 1 } tgp_dtype;
+
+/* Checkpoint policy (Sec. 2.1): ALWAYS checkpoints every micro-batch,
+ * EXCEPT_LAST skips F'_{m,j} (the last micro-batch keeps its activations),
+ * NEVER stores all activations.  EXCEPT_LAST with m = 1 is NEVER. */
+typedef enum { TGP_CKPT_ALWAYS = 0, TGP_CKPT_EXCEPT_LAST = 1, TGP_CKPT_NEVER = 2 } tgp_ckpt;
+
+typedef enum { TGP_CONV3X3 = 0, TGP_CONV1X1 = 1, TGP_DWCONV3X3 = 2 } tgp_kind;
+
+/* Input transform applied before a layer's convolution:
+ * MAXPOOL2: 2x2 stride-2 max-pool of the previous output (argmax ties go to
+ *           the first element in row-major window order);
+ * UPCAT2:   channel concat [nearest 2x upsample of the previous output,
+ *           skip tensor `pop_id`] (Sec. 3.3 skip connections). */
+typedef enum { TGP_PRO_NONE = 0, TGP_PRO_MAXPOOL2 = 1, TGP_PRO_UPCAT2 = 2 } tgp_prologue;
+
+/* One layer: y = act(conv(prologue(x)) + b), act = ReLU if relu != 0.
+ * Convolutions are cross-correlations, stride 1, zero padding 1 (3x3) or 0
+ * (1x1).  stash_id >= 0 stashes the output as skip `stash_id` for a later
+ * UPCAT2 layer (Sec. 3.3); pop_id names the skip an UPCAT2 layer consumes. */
+typedef struct {
+  int32_t kind;      /* tgp_kind */
+  int32_t cin;       /* channels after the prologue */
+  int32_t cout;
+  int32_t relu;      /* 0/1 */
+  int32_t bias;      /* 0/1 */
+  int32_t prologue;  /* tgp_prologue */
+  int32_t stash_id;  /* -1 or 0..63 */
+  int32_t pop_id;    /* -1 or 0..63 (UPCAT2 only) */
+} tgp_layer;
+
+/* Schedule-trace opcodes (tgp_schedule_trace). */
+enum { TGP_OP_FORWARD = 0, TGP_OP_RECOMPUTE = 1, TGP_OP_BACKWARD = 2,
+       TGP_OP_ACCUMULATE = 3, TGP_OP_LOSS = 4 };
+
+/* Creates a network description (host memory only; no device work).
+ * `layers` is copied.  in_c/H/W describe one sample of the network input.
+ * Errors: EINVAL for inconsistent channels or sizes, odd sizes under a pool,
+ * an UPCAT2 whose skip is missing or of the wrong size, n_layers < 1;
+ * EUNSUPPORTED for a kind/dtype the library does not build. */
+tgp_status tgp_net_create(const tgp_layer* layers, int n_layers, int in_c, int H, int W,
+                          int dtype, tgp_net** out);
+void tgp_net_destroy(tgp_net* net);
+
+/* Forward FLOPs of one sample through layer `layer` (2 per multiply-add). */
+tgp_status tgp_layer_flops(const tgp_net* net, int layer, int64_t* flops);
+
+/* Partition into n contiguous parts (Sec. 2: f = f^n o ... o f^1).
+ * balance[j] = number of layers of partition j+1 (sum = n_layers, each >= 1).
+ * balance == NULL picks the split that minimises the largest per-partition
+ * forward FLOP count (exact dynamic programme); among such splits, the one
+ * with the smallest sum of squared partition costs; then the earliest cut
+ * points (Sec. 3: a partition with small pairwise resource discrepancy).
+ * A later tgp_plan is required. */
+tgp_status tgp_set_partition(tgp_net* net, int n, const int* balance);
+tgp_status tgp_get_partition(const tgp_net* net, int* n, int* balance /* >= n entries */);
+
+/* The same split rule as a pure function of per-layer costs: cost[L], n
+ * parts; writes balance[n].  Host only. */
+tgp_status tgp_balance_minmax(const int64_t* cost, int L, int n, int* balance);
+
+/* Binds layer parameters (device pointers, caller-owned):
+ * w: weights (net dtype, KRSC); b: float32 bias (NULL iff the layer has no
+ * bias); dw_acc, db_acc: float32 gradient accumulators g^j, same layouts
+ * (db_acc NULL iff no bias).  Every layer must be bound before any step. */
+tgp_status tgp_bind_params(tgp_net* net, int layer, const void* w, const float* b,
+                           float* dw_acc, float* db_acc);
+
+/* Fixes the mini-batch size B, the micro-batch count m (B % m == 0) and the
+ * checkpoint policy for the following calls, and returns the workspace size
+ * in bytes.  Resets the per-task state.  Requires a partition. */
+tgp_status tgp_plan(tgp_net* net, int B, int m, int ckpt_mode, size_t* workspace_bytes);
+
+/* Binds caller-owned device memory of at least the planned size (ENOSPACE
+ * otherwise).  Base address must be 256-byte aligned. */
+tgp_status tgp_bind_workspace(tgp_net* net, void* dev, size_t bytes);
+
+/* Device address of micro-batch i's (1-based) slot of skip `stash_id`
+ * (grad = 0) or of the gradient flowing back into it (grad = 1); NHWC,
+ * b x H x W x C of the stashing layer, net dtype.  Stage runs read exported
+ * skips here and write the upstream gradients of exported skips here before
+ * tgp_stage_backward_recompute.  Requires a bound workspace. */
+tgp_status tgp_stash_ptr(tgp_net* net, int i, int stash_id, int grad, void** p);
+
+/* Task F_{i,j} (eq. (F_ij)), 1-based i in 1..m and j in 1..n, for
+ * micro-batch i: runs partition j's layers on x_in (b x H x W x C of the
+ * partition input) and writes its output to y_out.  Skips popped here are
+ * read from their stash slots; skips stashed here are written to theirs.
+ * checkpoint = 1 keeps only x_in (and the popped skips) for the backward
+ * (Sec. 2.1); checkpoint = 0 keeps every activation in the workspace.  The
+ * flag must equal the planned policy's decision for i (EINVAL otherwise).
+ * x_in and y_out must stay untouched until B_{i,j} has run.
+ * ESTATE if F_{i,j} already ran in this step. */
+tgp_status tgp_stage_forward(tgp_net* net, int j, int i, int checkpoint, const void* x_in,
+                             void* y_out, void* stream);
+
+/* F'_{i,j} (when F_{i,j} was checkpointed: the forward rerun from the saved
+ * input with the same kernels, so bit-identical) followed by B_{i,j} (eq.
+ * (B_ij)): dy_out is the gradient of the partition output (shape of y_out);
+ * writes dx_in, the gradient of the partition input, unless dx_in is NULL
+ * (then the first layer's data gradient is skipped).  Gradients of skips
+ * popped here go to their gradient slots; skips stashed here add the
+ * gradient found in theirs.  The weight gradient g_i^j is left for
+ * tgp_grad_accumulate.  Order (Sec. 2.1): for a given j, i = m, m-1, .., 1,
+ * each after F_{i,j} and after tgp_grad_accumulate(j, i+1); ESTATE otherwise. */
+tgp_status tgp_stage_backward_recompute(tgp_net* net, int j, int i, const void* dy_out,
+                                        void* dx_in, void* stream);
+
+/* g^j (+)= g_i^j into the bound float32 accumulators of partition j's layers
+ * (Sec. 2: the gradient is the sum of g_i^j over i).  overwrite must be 1
+ * exactly for i = m (the first backward of a step), else 0.  Requires
+ * B_{i,j}; ESTATE otherwise. */
+tgp_status tgp_grad_accumulate(tgp_net* net, int j, int i, int overwrite, void* stream);
+
+/* One training step over the whole network: scatter x (B samples) into m
+ * micro-batches; forward clocks k = 1..m+n-1 running F_{i,j} for i+j-1 = k
+ * with j ascending (Algorithm 1); MSE loss sum (y-t)^2 / numel(target) of
+ * each micro-batch's final output against its slice of `target`, with no
+ * 1/2 factor; backward clocks k = m+n-1..1 with j descending, each task
+ * F'_{i,j} (if checkpointed) + B_{i,j} + grad accumulate.  Writes the loss
+ * (float32) to *loss_dev and the network output to y_out (may be NULL).
+ * B, m, n and ckpt_mode must match tgp_plan and tgp_set_partition. */
+tgp_status tgp_pipeline_step(tgp_net* net, const void* x, const void* target, int B, int m,
+                             int n, int ckpt_mode, float* loss_dev, void* y_out, void* stream);
+
+/* Host-only: the (op, i, j) sequence tgp_pipeline_step issues for (m, n,
+ * ckpt_mode), as 3 int32 per op in `ops` (capacity `cap` ops); *count gets
+ * the number of ops.  EINVAL if cap is too small (count still set). */
+tgp_status tgp_schedule_trace(int m, int n, int ckpt_mode, int32_t* ops, int cap, int* count);
+
+/* Measurement hooks (outside the method).  While enabled on the calling
+ * thread, each kernel launch is bracketed by two HIP events on its stream.
+ * tgp_profile_read waits for the recorded events, returns one entry per
+ * kernel (launch count, summed duration in ms, and the algorithmic FLOPs and
+ * HBM bytes the launcher attributes to those launches) and clears the record.
+ * EINVAL if cap is too small (count still set). */
+typedef struct {
+  char name[96];
+  int64_t launches;
+  double ms;
+  double flops;
+  double bytes;
+} tgp_kernel_stat;
+tgp_status tgp_profile_enable(int enable);
+tgp_status tgp_profile_read(tgp_kernel_stat* out, int cap, int* count);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* tgp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TGP_H */

@@ -1,0 +1,514 @@
+// bf16 implicit-GEMM convolutions on gfx950 MFMA (v_mfma_f32_32x32x16_bf16),
+// fp32 accumulation, NHWC activations, KRSC weights.
+//
+// Forward (and data gradient, which is the same contraction on the rotated,
+// transposed weight):  Y^T[co][p] = sum_k W[co][k] * im2col(X)[p][k],
+// k = (tap, ci) so that every 64-wide K slice is one filter tap and 64
+// contiguous channels: both operands are K-contiguous 128-byte rows that are
+// staged into LDS with 16-byte loads.  Each block computes a BN x BM
+// (channels x pixels) tile with 4 waves; bias + ReLU + bf16 rounding are fused
+// into the epilogue.
+//
+// Weight gradient:  dW[co][tap][ci] = sum_p dZ[p][co] * X[p + off(tap)][ci],
+// K = pixels.  In NHWC both operands are channel-contiguous, so each thread
+// loads an 8-pixel x 8-channel block with 16-byte loads and transposes it in
+// registers before writing pixel-contiguous rows to LDS.  The pixel range is
+// split over grid.z; each split writes its fp32 partial tile and a second
+// kernel sums the splits in fixed order (deterministic, no atomics).
+#include "common.h"
+#include "kernels.h"
+#include "prof.h"
+
+namespace tgpk {
+namespace {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+// 16-byte chunk as a native vector (HIP's u32x4 wraps a union that keeps
+// arrays of it out of registers)
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// XOR swizzle of the eight 16-byte chunks of a 128-byte LDS row, so that
+// eight consecutive rows read at the same logical chunk, and rows eight apart
+// written at the same chunk, hit distinct banks.
+__device__ __forceinline__ int swz(int row, int q) { return q ^ ((row ^ (row >> 3)) & 7); }
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8_t, v); }
+
+__device__ __forceinline__ f32x16_t mfma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// Global -> register prefetch of one 64-wide K step of the forward GEMM:
+// A = weight rows (16-byte chunk q of each of A_CH rows), B = im2col rows
+// (the pixel's neighbour at this step's tap, zero outside the image).
+template <int A_CH, int B_CH, int TAPS>
+__device__ __forceinline__ void fwd_gload(u32x4 (&ra)[A_CH], u32x4 (&rb)[B_CH], int ks, int cpt,
+                                          int Cin, int K, int W, int H,
+                                          const bf16_t* __restrict__ wbase,
+                                          const bf16_t* __restrict__ xbase,
+                                          const int (&ph)[B_CH], const int (&pw)[B_CH],
+                                          const bool (&pok)[B_CH]) {
+  const int tap = ks / cpt;
+  const int c0 = (ks - tap * cpt) * 64;
+  const int dr = (TAPS == 9) ? tap / 3 - 1 : 0;
+  const int dc = (TAPS == 9) ? tap % 3 - 1 : 0;
+#pragma unroll
+  for (int u = 0; u < A_CH; ++u)
+    ra[u] = *(const u32x4*)(wbase + (long)32 * u * K + tap * Cin + c0);
+  const long shift = ((long)dr * W + dc) * Cin + c0;
+#pragma unroll
+  for (int u = 0; u < B_CH; ++u) {
+    const int hh = ph[u] + dr, ww = pw[u] + dc;
+    const bool ok = pok[u] && (unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W;
+    u32x4 v = u32x4{0, 0, 0, 0};
+    if (ok) v = *(const u32x4*)(xbase + (long)32 * u * Cin + shift);
+    rb[u] = v;
+  }
+}
+
+template <int A_CH, int B_CH>
+__device__ __forceinline__ void fwd_lstore(const u32x4 (&ra)[A_CH], const u32x4 (&rb)[B_CH],
+                                           u32x4* As, u32x4* Bs, int tid, int q) {
+#pragma unroll
+  for (int u = 0; u < A_CH; ++u) {
+    const int row = (tid >> 3) + 32 * u;
+    As[row * 8 + swz(row, q)] = ra[u];
+  }
+#pragma unroll
+  for (int u = 0; u < B_CH; ++u) {
+    const int row = (tid >> 3) + 32 * u;
+    Bs[row * 8 + swz(row, q)] = rb[u];
+  }
+}
+
+// ---------------------------------------------------------------- forward
+
+// WCO x WP waves; each wave owns TM x TN MFMA tiles of 32 x 32.
+template <int WCO, int WP, int TM, int TN, int TAPS>
+__global__ __launch_bounds__(256) void conv_fwd_mfma(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
+    const float* __restrict__ bias, bf16_t* __restrict__ Y, int P, int H, int W, int Cin,
+    int Cout, int relu) {
+  static_assert(WCO * WP == 4, "4 waves");
+  constexpr int BN = WCO * TM * 32;  // output channels per block
+  constexpr int BM = WP * TN * 32;   // pixels per block
+  constexpr int BK = 64;
+  constexpr int A_CH = BN * 8 / 256;  // 16-byte chunks per thread per K step
+  constexpr int B_CH = BM * 8 / 256;
+  static_assert(A_CH >= 1 && B_CH >= 1, "tile too small");
+  __shared__ u32x4 smem[2][(BN + BM) * 8];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wco = wave / WP, wp = wave % WP;
+  const int p0 = blockIdx.x * BM, co0 = blockIdx.y * BN;
+  const int K = TAPS * Cin;
+  const int cpt = Cin / BK;
+  const int nk = TAPS * cpt;
+  const int q = tid & 7;
+  const int HW = H * W;
+
+  int ph[B_CH], pw[B_CH];
+  bool pok[B_CH];
+#pragma unroll
+  for (int u = 0; u < B_CH; ++u) {
+    int p = p0 + (tid >> 3) + 32 * u;
+    pok[u] = p < P;
+    int pp = pok[u] ? p : 0;
+    int rem = pp % HW;
+    ph[u] = rem / W;
+    pw[u] = rem - ph[u] * W;
+  }
+  const bf16_t* xbase = X + (long)(p0 + (tid >> 3)) * Cin + q * 8;
+  const bf16_t* wbase = Wt + (long)(co0 + (tid >> 3)) * K + q * 8;
+
+  u32x4 ra[A_CH], rb[B_CH];
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
+
+  fwd_gload<A_CH, B_CH, TAPS>(ra, rb, 0, cpt, Cin, K, W, H, wbase, xbase, ph, pw, pok);
+  fwd_lstore<A_CH, B_CH>(ra, rb, smem[0], smem[0] + BN * 8, tid, q);
+  __syncthreads();
+  for (int ks = 0; ks < nk; ++ks) {
+    const int buf = ks & 1;
+    if (ks + 1 < nk)
+      fwd_gload<A_CH, B_CH, TAPS>(ra, rb, ks + 1, cpt, Cin, K, W, H, wbase, xbase, ph, pw, pok);
+    const u32x4* As = smem[buf];
+    const u32x4* Bs = smem[buf] + BN * 8;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int qq = 2 * kk + (lane >> 5);
+      bf16x8_t a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        int row = wco * TM * 32 + i * 32 + (lane & 31);
+        a[i] = as_bf16x8(As[row * 8 + swz(row, qq)]);
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        int row = wp * TN * 32 + j * 32 + (lane & 31);
+        b[j] = as_bf16x8(Bs[row * 8 + swz(row, qq)]);
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
+    }
+    if (ks + 1 < nk) fwd_lstore<A_CH, B_CH>(ra, rb, smem[buf ^ 1], smem[buf ^ 1] + BN * 8, tid, q);
+    __syncthreads();
+  }
+
+  // Epilogue: lane holds pixel (lane & 31) of each 32x32 tile and, per group
+  // g, four consecutive channels 8g + 4*(lane>>5) + 0..3.
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      int p = p0 + wp * TN * 32 + j * 32 + (lane & 31);
+      if (p >= P) continue;
+      bf16_t* yrow = Y + (long)p * Cout;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        int co = co0 + wco * TM * 32 + i * 32 + 8 * g + 4 * (lane >> 5);
+        float v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          v[t] = acc[i][j][4 * g + t];
+          if (bias) v[t] += bias[co + t];
+          if (relu) v[t] = fmaxf(v[t], 0.0f);
+        }
+        uint2 o;
+        o.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
+        o.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+        *(uint2*)(yrow + co) = o;
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------- wgrad
+
+// 8x8 transpose of bfloat16: in[j] holds 8 channels of pixel j; out[c] gets
+// 8 pixels of channel c.
+__device__ __forceinline__ void transpose8x8(const u32x4 (&in)[8], u32x4 (&out)[8]) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    uint32_t d[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      uint32_t lo = in[2 * e][c >> 1];
+      uint32_t hi = in[2 * e + 1][c >> 1];
+      d[e] = (c & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+    }
+    out[c] = u32x4{d[0], d[1], d[2], d[3]};
+  }
+}
+
+template <int WM, int WN, int TM, int TN, int TAPS>
+__global__ __launch_bounds__(256) void conv_wgrad_mfma(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ dZ, float* __restrict__ part,
+    int P, int H, int W, int Cin, int Cout, int pix_per_split) {
+  static_assert(WM * WN == 4, "4 waves");
+  constexpr int BMc = WM * TM * 32;  // output channels (co) per block
+  constexpr int BNc = WN * TN * 32;  // input channels (ci) per block
+  constexpr int BK = 64;             // pixels per K step
+  static_assert(BMc + BNc <= 256, "one 8x8 block per thread");
+  __shared__ u32x4 smem[2][(BMc + BNc) * 8];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int ncb = Cin / BNc;
+  const int tap = blockIdx.x / ncb;
+  const int ci0 = (blockIdx.x - tap * ncb) * BNc;
+  const int co0 = blockIdx.y * BMc;
+  const int split = blockIdx.z;
+  const int ps = split * pix_per_split;
+  const int pe = min(P, ps + pix_per_split);
+  const int nk = (pe - ps + BK - 1) / BK;
+  const int dr = (TAPS == 9) ? tap / 3 - 1 : 0;
+  const int dc = (TAPS == 9) ? tap % 3 - 1 : 0;
+
+  // Load role: threads [0, BMc) load dZ blocks, [BMc, BMc+BNc) load X blocks.
+  const bool isA = tid < BMc;
+  const bool active = tid < BMc + BNc;
+  const int t2 = isA ? tid : tid - BMc;
+  const int nchunk = isA ? BMc / 8 : BNc / 8;
+  const int cc = t2 % nchunk;      // 8-channel chunk
+  const int pc = t2 / nchunk;      // 8-pixel chunk within the K step (0..7)
+
+  u32x4 v[8];
+  auto gload = [&](int ks) {
+    int pbase = ps + ks * BK + pc * 8;
+    if (!active) return;
+    if (isA) {
+      const bf16_t* src = dZ + (long)pbase * Cout + co0 + cc * 8;
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        v[j] = (pbase + j < pe) ? *(const u32x4*)(src + (long)j * Cout) : u32x4{0, 0, 0, 0};
+    } else {
+      int HW = H * W;
+      int pp = pbase < P ? pbase : 0;
+      int rem = pp % HW;
+      int h = rem / W, w = rem - h * W;
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        int hh = h + dr, ww = w + dc;
+        bool ok = (pbase + j < pe) && (unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W;
+        v[j] = ok ? *(const u32x4*)(X + ((long)(pbase + j) + (long)dr * W + dc) * Cin + ci0 + cc * 8)
+                  : u32x4{0, 0, 0, 0};
+        if (++w == W) { w = 0; if (++h == H) h = 0; }
+      }
+    }
+  };
+  auto lstore = [&](int buf) {
+    if (!active) return;
+    u32x4 o[8];
+    transpose8x8(v, o);
+    u32x4* dst = smem[buf] + (isA ? 0 : BMc * 8);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      int row = cc * 8 + c;
+      dst[row * 8 + swz(row, pc)] = o[c];
+    }
+  };
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
+
+  if (nk > 0) {
+    gload(0);
+    lstore(0);
+  }
+  __syncthreads();
+  for (int ks = 0; ks < nk; ++ks) {
+    const int buf = ks & 1;
+    if (ks + 1 < nk) gload(ks + 1);
+    const u32x4* As = smem[buf];
+    const u32x4* Bs = smem[buf] + BMc * 8;
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int qq = 2 * kk + (lane >> 5);
+      bf16x8_t a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        int row = wm * TM * 32 + i * 32 + (lane & 31);
+        a[i] = as_bf16x8(As[row * 8 + swz(row, qq)]);
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        int row = wn * TN * 32 + j * 32 + (lane & 31);
+        b[j] = as_bf16x8(Bs[row * 8 + swz(row, qq)]);
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
+    }
+    if (ks + 1 < nk) lstore(buf ^ 1);
+    __syncthreads();
+  }
+
+  float* out = part + (long)split * Cout * TAPS * Cin;
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      int ci = ci0 + wn * TN * 32 + j * 32 + (lane & 31);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        int co = co0 + wm * TM * 32 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        out[((long)co * TAPS + tap) * Cin + ci] = acc[i][j][r];
+      }
+    }
+}
+
+// dw[e] = sum_{s < S} part[s][e] in a fixed order: split-lane l of a block
+// sums s = l, l + 16, l + 32, ... serially, then lanes 0..15 are added in
+// order.  Each block covers 16 float4 columns (64 elements).
+__global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ part,
+                                                     float* __restrict__ dw, long E, int S) {
+  __shared__ float4 red[16][16];
+  const int col = threadIdx.x & 15, lane = threadIdx.x >> 4;
+  const long e4 = ((long)blockIdx.x * 16 + col) * 4;
+  const bool vec = (E & 3) == 0;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (e4 < E) {
+    for (int k = lane; k < S; k += 16) {
+      const float* p = part + (long)k * E + e4;
+      if (vec) {
+        float4 t = *(const float4*)p;
+        acc.x += t.x; acc.y += t.y; acc.z += t.z; acc.w += t.w;
+      } else {
+        acc.x += p[0];
+        if (e4 + 1 < E) acc.y += p[1];
+        if (e4 + 2 < E) acc.z += p[2];
+        if (e4 + 3 < E) acc.w += p[3];
+      }
+    }
+  }
+  red[lane][col] = acc;
+  __syncthreads();
+  if (lane == 0 && e4 < E) {
+    float4 s = red[0][col];
+    for (int l = 1; l < 16; ++l) {
+      float4 t = red[l][col];
+      s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
+    }
+    if (vec) {
+      *(float4*)(dw + e4) = s;
+    } else {
+      dw[e4] = s.x;
+      if (e4 + 1 < E) dw[e4 + 1] = s.y;
+      if (e4 + 2 < E) dw[e4 + 2] = s.z;
+      if (e4 + 3 < E) dw[e4 + 3] = s.w;
+    }
+  }
+}
+
+// wt[ci][tap'][co] = w[co][taps-1-tap'][ci]: the data gradient of a
+// cross-correlation is a cross-correlation with the 180-degree rotated,
+// channel-transposed filter.
+template <typename T>
+__global__ void wtransform_kernel(const T* __restrict__ w, T* __restrict__ wt, int cout, int cin,
+                                  int taps) {
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  long n = (long)cout * cin * taps;
+  if (e >= n) return;
+  int co = e % cout;
+  long r = e / cout;
+  int tp = r % taps;
+  int ci = r / taps;
+  wt[e] = w[((long)co * taps + (taps - 1 - tp)) * cin + ci];
+}
+
+struct WgradPlan {
+  int S, pix_per_split;
+};
+
+template <int TM, int TN>
+WgradPlan wgrad_plan(long P, int tiles) {
+  const int BK = 64;
+  int S = cdiv(512, tiles);
+  int maxS = cdiv(P, 256);
+  if (S > maxS) S = maxS;
+  if (S < 1) S = 1;
+  int pps = cdiv(cdiv(P, S), BK) * BK;
+  S = cdiv(P, pps);
+  return {S, pps};
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- dispatch
+
+hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st);
+
+bool mfma_conv_ok(int dt, int cin, int cout) {
+  return dt == 0 && cin % 64 == 0 && cout % 64 == 0;
+}
+
+hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void* y,
+                             const ConvShape& s, int relu, hipStream_t st) {
+  long P = s.pixels();
+  const bf16_t* X = (const bf16_t*)x;
+  const bf16_t* Wt = (const bf16_t*)w;
+  bf16_t* Y = (bf16_t*)y;
+  double flops = 2.0 * P * s.cout * s.taps * s.cin;
+  double bytes = 2.0 * ((double)P * s.cin + (double)s.cout * s.taps * s.cin + (double)P * s.cout);
+  if (s.cout % 128 == 0) {
+    dim3 grid(cdiv(P, 128), s.cout / 128);
+    if (s.taps == 9) {
+      ProfScope ps("conv_fwd_mfma<2,2,2,2,9>", flops, bytes, st);
+      hipLaunchKernelGGL((conv_fwd_mfma<2, 2, 2, 2, 9>), grid, dim3(256), 0, st, X, Wt, b, Y,
+                         (int)P, s.H, s.W, s.cin, s.cout, relu);
+    } else {
+      ProfScope ps("conv_fwd_mfma<2,2,2,2,1>", flops, bytes, st);
+      hipLaunchKernelGGL((conv_fwd_mfma<2, 2, 2, 2, 1>), grid, dim3(256), 0, st, X, Wt, b, Y,
+                         (int)P, s.H, s.W, s.cin, s.cout, relu);
+    }
+  } else {
+    dim3 grid(cdiv(P, 256), s.cout / 64);
+    if (s.taps == 9) {
+      ProfScope ps("conv_fwd_mfma<1,4,2,2,9>", flops, bytes, st);
+      hipLaunchKernelGGL((conv_fwd_mfma<1, 4, 2, 2, 9>), grid, dim3(256), 0, st, X, Wt, b, Y,
+                         (int)P, s.H, s.W, s.cin, s.cout, relu);
+    } else {
+      ProfScope ps("conv_fwd_mfma<1,4,2,2,1>", flops, bytes, st);
+      hipLaunchKernelGGL((conv_fwd_mfma<1, 4, 2, 2, 1>), grid, dim3(256), 0, st, X, Wt, b, Y,
+                         (int)P, s.H, s.W, s.cin, s.cout, relu);
+    }
+  }
+  return hipGetLastError();
+}
+
+hipError_t weight_transform(int dt, const void* w, void* wt, int cout, int cin, int taps,
+                            hipStream_t st) {
+  long n = (long)cout * cin * taps;
+  ProfScope ps("wtransform", 0.0, 2.0 * n * (dt == 0 ? 2 : 4), st);
+  if (dt == 0)
+    hipLaunchKernelGGL(wtransform_kernel<bf16_t>, dim3(cdiv(n, 256)), dim3(256), 0, st,
+                       (const bf16_t*)w, (bf16_t*)wt, cout, cin, taps);
+  else
+    hipLaunchKernelGGL(wtransform_kernel<float>, dim3(cdiv(n, 256)), dim3(256), 0, st,
+                       (const float*)w, (float*)wt, cout, cin, taps);
+  return hipGetLastError();
+}
+
+size_t wgrad_mfma_partial_floats(const ConvShape& s) {
+  int tiles = s.taps * (s.cin / 64) * (s.cout / 64);
+  if (s.cin % 128 == 0 && s.cout % 128 == 0) tiles = s.taps * (s.cin / 128) * (s.cout / 128);
+  WgradPlan pl = wgrad_plan<2, 2>(s.pixels(), tiles);
+  return (size_t)pl.S * s.cout * s.taps * s.cin;
+}
+
+hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
+                           const ConvShape& s, hipStream_t st) {
+  long P = s.pixels();
+  const bf16_t* X = (const bf16_t*)x;
+  const bf16_t* DZ = (const bf16_t*)dz;
+  bool big = s.cin % 128 == 0 && s.cout % 128 == 0;
+  int bm = big ? 128 : 64, bn = big ? 128 : 64;
+  int tiles = s.taps * (s.cin / bn) * (s.cout / bm);
+  WgradPlan pl = wgrad_plan<2, 2>(P, tiles);
+  dim3 grid(s.taps * (s.cin / bn), s.cout / bm, pl.S);
+  long E = (long)s.cout * s.taps * s.cin;
+  double flops = 2.0 * P * E;
+  double bytes = 2.0 * ((double)P * s.cin + (double)P * s.cout) + 4.0 * pl.S * E;
+  {
+    const char* nm = big ? (s.taps == 9 ? "conv_wgrad_mfma<2,2,2,2,9>" : "conv_wgrad_mfma<2,2,2,2,1>")
+                         : (s.taps == 9 ? "conv_wgrad_mfma<2,2,1,1,9>" : "conv_wgrad_mfma<2,2,1,1,1>");
+    ProfScope ps(nm, flops, bytes, st);
+    if (big) {
+      if (s.taps == 9)
+        hipLaunchKernelGGL((conv_wgrad_mfma<2, 2, 2, 2, 9>), grid, dim3(256), 0, st, X, DZ,
+                           partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+      else
+        hipLaunchKernelGGL((conv_wgrad_mfma<2, 2, 2, 2, 1>), grid, dim3(256), 0, st, X, DZ,
+                           partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+    } else {
+      if (s.taps == 9)
+        hipLaunchKernelGGL((conv_wgrad_mfma<2, 2, 1, 1, 9>), grid, dim3(256), 0, st, X, DZ,
+                           partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+      else
+        hipLaunchKernelGGL((conv_wgrad_mfma<2, 2, 1, 1, 1>), grid, dim3(256), 0, st, X, DZ,
+                           partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+    }
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return splitk_reduce_launch(partial, dw, E, pl.S, st);
+}
+
+hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st) {
+  ProfScope ps("splitk_reduce", 0.0, 4.0 * E * (S + 1), st);
+  hipLaunchKernelGGL(splitk_reduce, dim3(cdiv(E, 64)), dim3(256), 0, st, part, out, E, S);
+  return hipGetLastError();
+}
+
+}  // namespace tgpk

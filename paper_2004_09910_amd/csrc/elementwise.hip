@@ -1,0 +1,812 @@
+// Non-MFMA kernels: direct convolutions for float32 runs and for shapes the
+// MFMA tiles do not cover (e.g. a 1-channel head), depthwise 3x3, ReLU
+// backward, bias gradient, max-pool, upsample-concat, MSE and gradient
+// accumulation.  All reductions run in a fixed order (per-thread serial sums,
+// fixed LDS trees, fixed split order), so results are bit-reproducible.
+#include "common.h"
+#include "kernels.h"
+#include "prof.h"
+
+namespace tgpk {
+
+bool mfma_conv_ok(int dt, int cin, int cout);
+hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void* y,
+                             const ConvShape& s, int relu, hipStream_t st);
+size_t wgrad_mfma_partial_floats(const ConvShape& s);
+hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
+                           const ConvShape& s, hipStream_t st);
+hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st);
+
+namespace {
+
+// ---------------------------------------------------------------- 16-byte packs
+
+template <typename T> struct Pk;
+template <> struct Pk<bf16_t> {
+  static constexpr int N = 8;
+  static __device__ __forceinline__ void un(uint4 v, float* f) {
+    const uint32_t* d = &v.x;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) { f[2 * i] = bf2f(d[i] & 0xffffu); f[2 * i + 1] = bf2f(d[i] >> 16); }
+  }
+  static __device__ __forceinline__ uint4 pk(const float* f) {
+    uint4 v;
+    uint32_t* d = &v.x;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) d[i] = f2bf(f[2 * i]) | (f2bf(f[2 * i + 1]) << 16);
+    return v;
+  }
+};
+template <> struct Pk<float> {
+  static constexpr int N = 4;
+  static __device__ __forceinline__ void un(uint4 v, float* f) {
+    f[0] = __uint_as_float(v.x); f[1] = __uint_as_float(v.y);
+    f[2] = __uint_as_float(v.z); f[3] = __uint_as_float(v.w);
+  }
+  static __device__ __forceinline__ uint4 pk(const float* f) {
+    return make_uint4(__float_as_uint(f[0]), __float_as_uint(f[1]), __float_as_uint(f[2]),
+                      __float_as_uint(f[3]));
+  }
+};
+
+template <typename T> __device__ __forceinline__ uint4 ld16(const T* p) { return *(const uint4*)p; }
+template <typename T> __device__ __forceinline__ void st16(T* p, uint4 v) { *(uint4*)p = v; }
+
+// ---------------------------------------------------------------- direct conv
+
+template <typename T>
+__global__ __launch_bounds__(256) void conv_fwd_direct(const T* __restrict__ x,
+                                                       const T* __restrict__ w,
+                                                       const float* __restrict__ b,
+                                                       T* __restrict__ y, long P, int H, int W,
+                                                       int Cin, int Cout, int taps, int relu) {
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= P * Cout) return;
+  int co = e % Cout;
+  long p = e / Cout;
+  int HW = H * W;
+  int rem = p % HW, h = rem / W, wq = rem - h * W;
+  float acc = 0.f;
+  for (int t = 0; t < taps; ++t) {
+    int dr = taps == 9 ? t / 3 - 1 : 0, dc = taps == 9 ? t % 3 - 1 : 0;
+    int hh = h + dr, ww = wq + dc;
+    if ((unsigned)hh >= (unsigned)H || (unsigned)ww >= (unsigned)W) continue;
+    const T* xr = x + (p + (long)dr * W + dc) * Cin;
+    const T* wr = w + ((long)co * taps + t) * Cin;
+    for (int ci = 0; ci < Cin; ++ci) acc += Elt<T>::ld(xr + ci) * Elt<T>::ld(wr + ci);
+  }
+  if (b) acc += b[co];
+  if (relu) acc = fmaxf(acc, 0.f);
+  Elt<T>::st(y + e, acc);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void conv_dgrad_direct(const T* __restrict__ dz,
+                                                         const T* __restrict__ w,
+                                                         T* __restrict__ dx, long P, int H,
+                                                         int W, int Cin, int Cout, int taps) {
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= P * Cin) return;
+  int ci = e % Cin;
+  long p = e / Cin;
+  int HW = H * W;
+  int rem = p % HW, h = rem / W, wq = rem - h * W;
+  float acc = 0.f;
+  for (int t = 0; t < taps; ++t) {
+    int dr = taps == 9 ? t / 3 - 1 : 0, dc = taps == 9 ? t % 3 - 1 : 0;
+    // output pixel (h - dr, w - dc) read input pixel (h, w) through tap t
+    int hh = h - dr, ww = wq - dc;
+    if ((unsigned)hh >= (unsigned)H || (unsigned)ww >= (unsigned)W) continue;
+    const T* dr_ = dz + (p - (long)dr * W - dc) * Cout;
+    for (int co = 0; co < Cout; ++co)
+      acc += Elt<T>::ld(dr_ + co) * Elt<T>::ld(w + ((long)co * taps + t) * Cin + ci);
+  }
+  Elt<T>::st(dx + e, acc);
+}
+
+// partial[s][co][tap][ci] = sum over pixels of split s of dz[p][co] * x[p+off][ci]
+template <typename T>
+__global__ __launch_bounds__(256) void conv_wgrad_direct(const T* __restrict__ x,
+                                                         const T* __restrict__ dz,
+                                                         float* __restrict__ part, long P,
+                                                         int H, int W, int Cin, int Cout,
+                                                         int taps, long pps) {
+  long E = (long)Cout * taps * Cin;
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= E) return;
+  int ci = e % Cin;
+  long r = e / Cin;
+  int t = r % taps;
+  int co = r / taps;
+  int dr = taps == 9 ? t / 3 - 1 : 0, dc = taps == 9 ? t % 3 - 1 : 0;
+  long ps = (long)blockIdx.y * pps, pe = ps + pps < P ? ps + pps : P;
+  int HW = H * W;
+  float acc = 0.f;
+  for (long p = ps; p < pe; ++p) {
+    int rem = p % HW, h = rem / W, wq = rem - h * W;
+    int hh = h + dr, ww = wq + dc;
+    if ((unsigned)hh >= (unsigned)H || (unsigned)ww >= (unsigned)W) continue;
+    acc += Elt<T>::ld(dz + p * Cout + co) * Elt<T>::ld(x + (p + (long)dr * W + dc) * Cin + ci);
+  }
+  part[(long)blockIdx.y * E + e] = acc;
+}
+
+long direct_wgrad_pps(long P) { return P < 256 ? 256 : (P + 63) / 64; }
+int direct_wgrad_splits(long P) { return (int)((P + direct_wgrad_pps(P) - 1) / direct_wgrad_pps(P)); }
+
+// ---------------------------------------------------------------- depthwise
+
+template <typename T>
+__global__ __launch_bounds__(256) void dw_fwd(const T* __restrict__ x, const T* __restrict__ w,
+                                              const float* __restrict__ b, T* __restrict__ y,
+                                              long P, int H, int W, int C, int relu) {
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= P * C) return;
+  int c = e % C;
+  long p = e / C;
+  int HW = H * W, rem = p % HW, h = rem / W, wq = rem - h * W;
+  float acc = 0.f;
+#pragma unroll
+  for (int t = 0; t < 9; ++t) {
+    int hh = h + t / 3 - 1, ww = wq + t % 3 - 1;
+    if ((unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W)
+      acc += Elt<T>::ld(w + c * 9 + t) * Elt<T>::ld(x + (p + (long)(t / 3 - 1) * W + (t % 3 - 1)) * C + c);
+  }
+  if (b) acc += b[c];
+  if (relu) acc = fmaxf(acc, 0.f);
+  Elt<T>::st(y + e, acc);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void dw_dgrad_k(const T* __restrict__ dz, const T* __restrict__ w,
+                                                  T* __restrict__ dx, long P, int H, int W, int C) {
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= P * C) return;
+  int c = e % C;
+  long p = e / C;
+  int HW = H * W, rem = p % HW, h = rem / W, wq = rem - h * W;
+  float acc = 0.f;
+#pragma unroll
+  for (int t = 0; t < 9; ++t) {
+    int dr = t / 3 - 1, dc = t % 3 - 1;
+    int hh = h - dr, ww = wq - dc;
+    if ((unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W)
+      acc += Elt<T>::ld(w + c * 9 + t) * Elt<T>::ld(dz + (p - (long)dr * W - dc) * C + c);
+  }
+  Elt<T>::st(dx + e, acc);
+}
+
+// ---------------------------------------------------------------- elementwise
+
+template <typename T>
+__global__ __launch_bounds__(256) void relu_bwd_k(const T* __restrict__ dy, const T* __restrict__ ds,
+                                                  const T* __restrict__ y, T* __restrict__ dz,
+                                                  int relu, long n, int vec) {
+  constexpr int N = Pk<T>::N;
+  long e0 = ((long)blockIdx.x * 256 + threadIdx.x) * N;
+  if (e0 >= n) return;
+  if (vec && e0 + N <= n) {
+    float a[N], s[N], m[N];
+    Pk<T>::un(ld16(dy + e0), a);
+    if (ds) {
+      Pk<T>::un(ld16(ds + e0), s);
+#pragma unroll
+      for (int i = 0; i < N; ++i) a[i] += s[i];
+    }
+    if (relu) {
+      Pk<T>::un(ld16(y + e0), m);
+#pragma unroll
+      for (int i = 0; i < N; ++i) a[i] = m[i] > 0.f ? a[i] : 0.f;
+    }
+    st16(dz + e0, Pk<T>::pk(a));
+  } else {
+    for (long e = e0; e < n && e < e0 + N; ++e) {
+      float a = Elt<T>::ld(dy + e);
+      if (ds) a += Elt<T>::ld(ds + e);
+      if (relu && !(Elt<T>::ld(y + e) > 0.f)) a = 0.f;
+      Elt<T>::st(dz + e, a);
+    }
+  }
+}
+
+// dz = (dy [+ dskip]) * [y > 0] with the bias gradient's column partial sums
+// fused in: block b covers rows [b*rows, (b+1)*rows); thread t handles the
+// 16-byte channel pack t % CP for rows t / CP, t / CP + 256 / CP, ...
+// (serial, fixed order); row lanes are then added in order in LDS and
+// part[b][c] is written.  Needs 256 % CP == 0 (CP = C / pack).
+template <typename T>
+__global__ __launch_bounds__(256) void relu_bwd_bias_k(const T* __restrict__ dy,
+                                                       const T* __restrict__ ds,
+                                                       const T* __restrict__ y,
+                                                       T* __restrict__ dz, float* __restrict__ part,
+                                                       int relu, long P, int C, long rows) {
+  constexpr int N = Pk<T>::N;
+  __shared__ float red[256 * N];
+  const int CP = C / N;
+  const int cp = threadIdx.x % CP, rl = threadIdx.x / CP, nl = 256 / CP;
+  const long p0 = (long)blockIdx.x * rows, p1 = p0 + rows < P ? p0 + rows : P;
+  float sum[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) sum[i] = 0.f;
+  for (long p = p0 + rl; p < p1; p += nl) {
+    const long e = p * C + cp * N;
+    float a[N], s2[N], m[N];
+    Pk<T>::un(ld16(dy + e), a);
+    if (ds) {
+      Pk<T>::un(ld16(ds + e), s2);
+#pragma unroll
+      for (int i = 0; i < N; ++i) a[i] += s2[i];
+    }
+    if (relu) {
+      Pk<T>::un(ld16(y + e), m);
+#pragma unroll
+      for (int i = 0; i < N; ++i) a[i] = m[i] > 0.f ? a[i] : 0.f;
+    }
+    uint4 o = Pk<T>::pk(a);
+    st16(dz + e, o);
+    Pk<T>::un(o, a);   // the bias gradient sums the stored (rounded) dz
+#pragma unroll
+    for (int i = 0; i < N; ++i) sum[i] += a[i];
+  }
+#pragma unroll
+  for (int i = 0; i < N; ++i) red[threadIdx.x * N + i] = sum[i];
+  __syncthreads();
+  if (rl == 0) {
+    for (int l = 1; l < nl; ++l)
+#pragma unroll
+      for (int i = 0; i < N; ++i) sum[i] += red[(l * CP + cp) * N + i];
+#pragma unroll
+    for (int i = 0; i < N; ++i) part[(long)blockIdx.x * C + cp * N + i] = sum[i];
+  }
+}
+
+// Column sums of a P x C matrix: block (cg, pb) sums rows [pb*rows, ...) for
+// channels cg*64 .. +63; 4 row lanes, combined in fixed order.
+template <typename T>
+__global__ __launch_bounds__(256) void colsum_k(const T* __restrict__ a, float* __restrict__ part,
+                                                long P, int C, long rows) {
+  __shared__ float red[4][64];
+  int c = blockIdx.x * 64 + (threadIdx.x & 63);
+  int lane = threadIdx.x >> 6;
+  long p0 = (long)blockIdx.y * rows, p1 = p0 + rows < P ? p0 + rows : P;
+  float s = 0.f;
+  if (c < C)
+    for (long p = p0 + lane; p < p1; p += 4) s += Elt<T>::ld(a + p * C + c);
+  red[lane][threadIdx.x & 63] = s;
+  __syncthreads();
+  if (lane == 0 && c < C) {
+    int k = threadIdx.x & 63;
+    part[(long)blockIdx.y * C + c] = ((red[0][k] + red[1][k]) + red[2][k]) + red[3][k];
+  }
+}
+
+// depthwise wgrad partials: thread (c, tap) of split s
+template <typename T>
+__global__ __launch_bounds__(256) void dw_wgrad_k(const T* __restrict__ x, const T* __restrict__ dz,
+                                                  float* __restrict__ part, long P, int H, int W,
+                                                  int C, long pps) {
+  long E = (long)C * 9;
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= E) return;
+  int t = e % 9, c = e / 9;
+  int dr = t / 3 - 1, dc = t % 3 - 1;
+  long ps = (long)blockIdx.y * pps, pe = ps + pps < P ? ps + pps : P;
+  int HW = H * W;
+  float acc = 0.f;
+  for (long p = ps; p < pe; ++p) {
+    int rem = p % HW, h = rem / W, wq = rem - h * W;
+    int hh = h + dr, ww = wq + dc;
+    if ((unsigned)hh >= (unsigned)H || (unsigned)ww >= (unsigned)W) continue;
+    acc += Elt<T>::ld(dz + p * C + c) * Elt<T>::ld(x + (p + (long)dr * W + dc) * C + c);
+  }
+  part[(long)blockIdx.y * E + e] = acc;
+}
+
+// ---------------------------------------------------------------- pool
+
+template <typename T>
+__global__ __launch_bounds__(256) void maxpool_fwd_k(const T* __restrict__ x, T* __restrict__ y,
+                                                     int nb, int H, int W, int C) {
+  constexpr int N = Pk<T>::N;
+  int CP = C / N, H2 = H / 2, W2 = W / 2;
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  long total = (long)nb * H2 * W2 * CP;
+  if (e >= total) return;
+  int cp = e % CP;
+  long r = e / CP;
+  int w2 = r % W2;
+  r /= W2;
+  int h2 = r % H2;
+  int n = r / H2;
+  const T* base = x + (((long)n * H + 2 * h2) * W + 2 * w2) * C + cp * N;
+  float m[N], v[N];
+  Pk<T>::un(ld16(base), m);
+  const long off[3] = {C, (long)W * C, (long)W * C + C};
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    Pk<T>::un(ld16(base + off[k]), v);
+#pragma unroll
+    for (int i = 0; i < N; ++i) m[i] = v[i] > m[i] ? v[i] : m[i];
+  }
+  st16(y + e * N, Pk<T>::pk(m));
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void maxpool_bwd_k(const T* __restrict__ x, const T* __restrict__ dy,
+                                                     T* __restrict__ dx, int nb, int H, int W, int C) {
+  constexpr int N = Pk<T>::N;
+  int CP = C / N, H2 = H / 2, W2 = W / 2;
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  long total = (long)nb * H2 * W2 * CP;
+  if (e >= total) return;
+  int cp = e % CP;
+  long r = e / CP;
+  int w2 = r % W2;
+  r /= W2;
+  int h2 = r % H2;
+  int n = r / H2;
+  long o = (((long)n * H + 2 * h2) * W + 2 * w2) * C + cp * N;
+  const long off[4] = {0, C, (long)W * C, (long)W * C + C};
+  float v[4][N], g[N];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) Pk<T>::un(ld16(x + o + off[k]), v[k]);
+  Pk<T>::un(ld16(dy + e * N), g);
+  float out[4][N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) {
+    int arg = 0;
+    float best = v[0][i];
+#pragma unroll
+    for (int k = 1; k < 4; ++k)
+      if (v[k][i] > best) { best = v[k][i]; arg = k; }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) out[k][i] = (k == arg) ? g[i] : 0.f;
+  }
+#pragma unroll
+  for (int k = 0; k < 4; ++k) st16(dx + o + off[k], Pk<T>::pk(out[k]));
+}
+
+// ---------------------------------------------------------------- upsample-concat
+
+template <typename T>
+__global__ __launch_bounds__(256) void upcat_fwd_k(const T* __restrict__ prev, const T* __restrict__ skip,
+                                                   T* __restrict__ out, int nb, int H, int W, int C1,
+                                                   int C2) {
+  constexpr int N = Pk<T>::N;
+  int C = C1 + C2, CP = C / N;
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  long total = (long)nb * H * W * CP;
+  if (e >= total) return;
+  int cp = e % CP;
+  long p = e / CP;
+  int w = p % W;
+  long r = p / W;
+  int h = r % H;
+  int n = r / H;
+  int c = cp * N;
+  uint4 v;
+  if (c < C1)
+    v = ld16(prev + (((long)n * (H / 2) + h / 2) * (W / 2) + w / 2) * C1 + c);
+  else
+    v = ld16(skip + p * C2 + (c - C1));
+  st16(out + p * C + c, v);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void upcat_bwd_prev_k(const T* __restrict__ dcat, T* __restrict__ dprev,
+                                                        int nb, int H, int W, int C1, int C2) {
+  constexpr int N = Pk<T>::N;
+  int C = C1 + C2, CP = C1 / N, H2 = H / 2, W2 = W / 2;
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  long total = (long)nb * H2 * W2 * CP;
+  if (e >= total) return;
+  int cp = e % CP;
+  long r = e / CP;
+  int w2 = r % W2;
+  r /= W2;
+  int h2 = r % H2;
+  int n = r / H2;
+  long o = (((long)n * H + 2 * h2) * W + 2 * w2) * C + cp * N;
+  const long off[4] = {0, C, (long)W * C, (long)W * C + C};
+  float s[N], v[N];
+  Pk<T>::un(ld16(dcat + o), s);
+#pragma unroll
+  for (int k = 1; k < 4; ++k) {
+    Pk<T>::un(ld16(dcat + o + off[k]), v);
+#pragma unroll
+    for (int i = 0; i < N; ++i) s[i] += v[i];
+  }
+  st16(dprev + e * N, Pk<T>::pk(s));
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void upcat_bwd_skip_k(const T* __restrict__ dcat, T* __restrict__ dskip,
+                                                        long P, int C1, int C2) {
+  constexpr int N = Pk<T>::N;
+  int CP = C2 / N;
+  long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= P * CP) return;
+  int cp = e % CP;
+  long p = e / CP;
+  st16(dskip + p * C2 + cp * N, ld16(dcat + p * (C1 + C2) + C1 + cp * N));
+}
+
+// ---------------------------------------------------------------- loss / accumulate
+
+template <typename T>
+__global__ __launch_bounds__(256) void mse_k(const T* __restrict__ y, const T* __restrict__ t,
+                                             T* __restrict__ dy, float* __restrict__ part, long n,
+                                             float inv_numel, long per_block) {
+  __shared__ float red[256];
+  long b0 = (long)blockIdx.x * per_block, b1 = b0 + per_block < n ? b0 + per_block : n;
+  float s = 0.f;
+  for (long e = b0 + threadIdx.x; e < b1; e += 256) {
+    float d = Elt<T>::ld(y + e) - Elt<T>::ld(t + e);
+    s += d * d;
+    Elt<T>::st(dy + e, 2.0f * d * inv_numel);
+  }
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int k = 128; k > 0; k >>= 1) {
+    if (threadIdx.x < k) red[threadIdx.x] += red[threadIdx.x + k];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) part[blockIdx.x] = red[0];
+}
+
+__global__ void serial_sum_k(const float* __restrict__ a, int n, float scale,
+                             float* __restrict__ out) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  float s = 0.f;
+  for (int i = 0; i < n; ++i) s += a[i];
+  *out = s * scale;
+}
+
+__global__ __launch_bounds__(256) void accumulate_k(float* __restrict__ acc, const float* __restrict__ g,
+                                                    long n, int overwrite) {
+  long e0 = ((long)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (e0 >= n) return;
+  if (e0 + 4 <= n) {
+    float4 v = *(const float4*)(g + e0);
+    if (!overwrite) {
+      float4 a = *(const float4*)(acc + e0);
+      v.x = a.x + v.x; v.y = a.y + v.y; v.z = a.z + v.z; v.w = a.w + v.w;
+    }
+    *(float4*)(acc + e0) = v;
+  } else {
+    for (long e = e0; e < n; ++e) acc[e] = overwrite ? g[e] : acc[e] + g[e];
+  }
+}
+
+// acc_k (+)= g_k for up to kMaxAcc (acc, g, n) entries in one launch; block
+// b covers float4 column range [b*1024, (b+1)*1024) of every entry.
+__global__ __launch_bounds__(256) void accumulate_multi_k(AccBatch batch, int overwrite) {
+  for (int k = 0; k < batch.count; ++k) {
+    const long n = batch.n[k];
+    const long e0 = ((long)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (e0 >= n) continue;
+    float* acc = batch.acc[k];
+    const float* g = batch.g[k];
+    if (e0 + 4 <= n) {
+      float4 v = *(const float4*)(g + e0);
+      if (!overwrite) {
+        float4 a = *(const float4*)(acc + e0);
+        v.x = a.x + v.x; v.y = a.y + v.y; v.z = a.z + v.z; v.w = a.w + v.w;
+      }
+      *(float4*)(acc + e0) = v;
+    } else {
+      for (long e = e0; e < n; ++e) acc[e] = overwrite ? g[e] : acc[e] + g[e];
+    }
+  }
+}
+
+inline bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+}  // namespace
+
+// ---------------------------------------------------------------- dispatch
+
+hipError_t conv_forward(int dt, const void* x, const void* w, const float* b, void* y,
+                        const ConvShape& s, int relu, hipStream_t st) {
+  if (mfma_conv_ok(dt, s.cin, s.cout)) return conv_forward_mfma(x, w, b, y, s, relu, st);
+  long P = s.pixels();
+  dim3 g(cdiv(P * s.cout, 256));
+  int esz = dt == 0 ? 2 : 4;
+  ProfScope ps("conv_fwd_direct", 2.0 * P * s.cout * s.taps * s.cin,
+               (double)esz * (P * s.cin + (double)s.cout * s.taps * s.cin + P * s.cout), st);
+  if (dt == 0)
+    hipLaunchKernelGGL(conv_fwd_direct<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
+                       (const bf16_t*)w, b, (bf16_t*)y, P, s.H, s.W, s.cin, s.cout, s.taps, relu);
+  else
+    hipLaunchKernelGGL(conv_fwd_direct<float>, g, dim3(256), 0, st, (const float*)x,
+                       (const float*)w, b, (float*)y, P, s.H, s.W, s.cin, s.cout, s.taps, relu);
+  return hipGetLastError();
+}
+
+bool conv_dgrad_uses_wt(int dt, const ConvShape& s) { return mfma_conv_ok(dt, s.cout, s.cin); }
+
+hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, void* dx,
+                      const ConvShape& s, hipStream_t st) {
+  if (conv_dgrad_uses_wt(dt, s)) {
+    ConvShape t{s.nb, s.H, s.W, s.cout, s.cin, s.taps};
+    return conv_forward_mfma(dz, wt, nullptr, dx, t, 0, st);
+  }
+  long P = s.pixels();
+  dim3 g(cdiv(P * s.cin, 256));
+  int esz = dt == 0 ? 2 : 4;
+  ProfScope ps("conv_dgrad_direct", 2.0 * P * s.cout * s.taps * s.cin,
+               (double)esz * (P * s.cin + (double)s.cout * s.taps * s.cin + P * s.cout), st);
+  if (dt == 0)
+    hipLaunchKernelGGL(conv_dgrad_direct<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dz,
+                       (const bf16_t*)w, (bf16_t*)dx, P, s.H, s.W, s.cin, s.cout, s.taps);
+  else
+    hipLaunchKernelGGL(conv_dgrad_direct<float>, g, dim3(256), 0, st, (const float*)dz,
+                       (const float*)w, (float*)dx, P, s.H, s.W, s.cin, s.cout, s.taps);
+  return hipGetLastError();
+}
+
+size_t conv_wgrad_partial_floats(int dt, const ConvShape& s) {
+  if (mfma_conv_ok(dt, s.cin, s.cout)) return wgrad_mfma_partial_floats(s);
+  return (size_t)direct_wgrad_splits(s.pixels()) * s.cout * s.taps * s.cin;
+}
+
+hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial,
+                      const ConvShape& s, hipStream_t st) {
+  if (mfma_conv_ok(dt, s.cin, s.cout)) return conv_wgrad_mfma(x, dz, dw, partial, s, st);
+  long P = s.pixels();
+  long E = (long)s.cout * s.taps * s.cin;
+  long pps = direct_wgrad_pps(P);
+  int S = direct_wgrad_splits(P);
+  dim3 g(cdiv(E, 256), S);
+  {
+  int esz = dt == 0 ? 2 : 4;
+  ProfScope ps("conv_wgrad_direct", 2.0 * P * E, (double)esz * P * (s.cin + s.cout) + 4.0 * S * E, st);
+  if (dt == 0)
+    hipLaunchKernelGGL(conv_wgrad_direct<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
+                       (const bf16_t*)dz, partial, P, s.H, s.W, s.cin, s.cout, s.taps, pps);
+  else
+    hipLaunchKernelGGL(conv_wgrad_direct<float>, g, dim3(256), 0, st, (const float*)x,
+                       (const float*)dz, partial, P, s.H, s.W, s.cin, s.cout, s.taps, pps);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return splitk_reduce_launch(partial, dw, E, S, st);
+}
+
+hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
+                      int H, int W, int C, int relu, hipStream_t st) {
+  long P = (long)nb * H * W;
+  dim3 g(cdiv(P * C, 256));
+  ProfScope ps("dw_forward", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
+  if (dt == 0)
+    hipLaunchKernelGGL(dw_fwd<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, (const bf16_t*)w,
+                       b, (bf16_t*)y, P, H, W, C, relu);
+  else
+    hipLaunchKernelGGL(dw_fwd<float>, g, dim3(256), 0, st, (const float*)x, (const float*)w, b,
+                       (float*)y, P, H, W, C, relu);
+  return hipGetLastError();
+}
+
+hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int H, int W,
+                    int C, hipStream_t st) {
+  long P = (long)nb * H * W;
+  dim3 g(cdiv(P * C, 256));
+  ProfScope ps("dw_dgrad", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
+  if (dt == 0)
+    hipLaunchKernelGGL(dw_dgrad_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dz,
+                       (const bf16_t*)w, (bf16_t*)dx, P, H, W, C);
+  else
+    hipLaunchKernelGGL(dw_dgrad_k<float>, g, dim3(256), 0, st, (const float*)dz,
+                       (const float*)w, (float*)dx, P, H, W, C);
+  return hipGetLastError();
+}
+
+size_t dw_wgrad_partial_floats(int nb, int H, int W, int C) {
+  long P = (long)nb * H * W;
+  return (size_t)direct_wgrad_splits(P) * C * 9;
+}
+
+hipError_t dw_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial, int nb,
+                    int H, int W, int C, hipStream_t st) {
+  long P = (long)nb * H * W;
+  long E = (long)C * 9;
+  long pps = direct_wgrad_pps(P);
+  int S = direct_wgrad_splits(P);
+  dim3 g(cdiv(E, 256), S);
+  {
+  ProfScope ps("dw_wgrad", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C + 4.0 * S * E, st);
+  if (dt == 0)
+    hipLaunchKernelGGL(dw_wgrad_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
+                       (const bf16_t*)dz, partial, P, H, W, C, pps);
+  else
+    hipLaunchKernelGGL(dw_wgrad_k<float>, g, dim3(256), 0, st, (const float*)x,
+                       (const float*)dz, partial, P, H, W, C, pps);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return splitk_reduce_launch(partial, dw, E, S, st);
+}
+
+hipError_t relu_backward(int dt, const void* dy, const void* dskip, const void* y, void* dz,
+                         int relu, long n, hipStream_t st) {
+  int N = dt == 0 ? 8 : 4;
+  int vec = al16(dy) && al16(dz) && (!dskip || al16(dskip)) && (!relu || al16(y)) ? 1 : 0;
+  dim3 g(cdiv(n, 256L * N));
+  ProfScope ps("relu_backward", 0.0, (dt == 0 ? 2.0 : 4.0) * n * (3 + (dskip ? 1 : 0) - (relu ? 0 : 1)), st);
+  if (dt == 0)
+    hipLaunchKernelGGL(relu_bwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dy,
+                       (const bf16_t*)dskip, (const bf16_t*)y, (bf16_t*)dz, relu, n, vec);
+  else
+    hipLaunchKernelGGL(relu_bwd_k<float>, g, dim3(256), 0, st, (const float*)dy,
+                       (const float*)dskip, (const float*)y, (float*)dz, relu, n, vec);
+  return hipGetLastError();
+}
+
+static long colsum_rows(long P) { return P < 1024 ? (P < 1 ? 1 : P) : 1024; }
+size_t colsum_partial_floats(long P, int C) {
+  return (size_t)cdiv(P, colsum_rows(P)) * C;
+}
+
+static long relu_bias_rows(long P) { return 256; }
+bool relu_bias_fusable(int dt, int C, const void* dy, const void* dskip, const void* y,
+                       const void* dz) {
+  int N = dt == 0 ? 8 : 4;
+  if (C % N) return false;
+  int CP = C / N;
+  return CP <= 256 && 256 % CP == 0 && al16(dy) && al16(dz) && (!dskip || al16(dskip)) &&
+         al16(y);
+}
+size_t relu_bias_partial_floats(long P, int C) { return (size_t)cdiv(P, relu_bias_rows(P)) * C; }
+
+hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
+                              int relu, float* db, float* partial, long P, int C,
+                              hipStream_t st) {
+  long rows = relu_bias_rows(P);
+  int nb = cdiv(P, rows);
+  {
+    ProfScope ps("relu_backward_bias", 0.0,
+                 (dt == 0 ? 2.0 : 4.0) * P * C * (3 + (dskip ? 1 : 0) - (relu ? 0 : 1)) + 4.0 * nb * C, st);
+    if (dt == 0)
+      hipLaunchKernelGGL(relu_bwd_bias_k<bf16_t>, dim3(nb), dim3(256), 0, st, (const bf16_t*)dy,
+                         (const bf16_t*)dskip, (const bf16_t*)y, (bf16_t*)dz, partial, relu, P, C,
+                         rows);
+    else
+      hipLaunchKernelGGL(relu_bwd_bias_k<float>, dim3(nb), dim3(256), 0, st, (const float*)dy,
+                         (const float*)dskip, (const float*)y, (float*)dz, partial, relu, P, C,
+                         rows);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return splitk_reduce_launch(partial, db, C, nb, st);
+}
+
+hipError_t bias_grad(int dt, const void* dz, float* db, float* partial, long P, int C,
+                     hipStream_t st) {
+  long rows = colsum_rows(P);
+  int nb = cdiv(P, rows);
+  dim3 g(cdiv(C, 64), nb);
+  {
+  ProfScope ps("bias_colsum", 0.0, (dt == 0 ? 2.0 : 4.0) * P * C + 4.0 * nb * C, st);
+  if (dt == 0)
+    hipLaunchKernelGGL(colsum_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dz, partial, P, C, rows);
+  else
+    hipLaunchKernelGGL(colsum_k<float>, g, dim3(256), 0, st, (const float*)dz, partial, P, C, rows);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return splitk_reduce_launch(partial, db, C, nb, st);
+}
+
+hipError_t maxpool_forward(int dt, const void* x, void* y, int nb, int H, int W, int C,
+                           hipStream_t st) {
+  int N = dt == 0 ? 8 : 4;
+  long total = (long)nb * (H / 2) * (W / 2) * (C / N);
+  dim3 g(cdiv(total, 256));
+  ProfScope ps("maxpool_forward", 0.0, (dt == 0 ? 2.0 : 4.0) * nb * H * W * C * 1.25, st);
+  if (dt == 0)
+    hipLaunchKernelGGL(maxpool_fwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)y, nb, H, W, C);
+  else
+    hipLaunchKernelGGL(maxpool_fwd_k<float>, g, dim3(256), 0, st, (const float*)x, (float*)y, nb, H, W, C);
+  return hipGetLastError();
+}
+
+hipError_t maxpool_backward(int dt, const void* x, const void* dy, void* dx, int nb, int H,
+                            int W, int C, hipStream_t st) {
+  int N = dt == 0 ? 8 : 4;
+  long total = (long)nb * (H / 2) * (W / 2) * (C / N);
+  dim3 g(cdiv(total, 256));
+  ProfScope ps("maxpool_backward", 0.0, (dt == 0 ? 2.0 : 4.0) * nb * H * W * C * 2.25, st);
+  if (dt == 0)
+    hipLaunchKernelGGL(maxpool_bwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
+                       (const bf16_t*)dy, (bf16_t*)dx, nb, H, W, C);
+  else
+    hipLaunchKernelGGL(maxpool_bwd_k<float>, g, dim3(256), 0, st, (const float*)x,
+                       (const float*)dy, (float*)dx, nb, H, W, C);
+  return hipGetLastError();
+}
+
+hipError_t upcat_forward(int dt, const void* prev, const void* skip, void* out, int nb, int H,
+                         int W, int C1, int C2, hipStream_t st) {
+  int N = dt == 0 ? 8 : 4;
+  long total = (long)nb * H * W * ((C1 + C2) / N);
+  dim3 g(cdiv(total, 256));
+  ProfScope ps("upcat_forward", 0.0, (dt == 0 ? 2.0 : 4.0) * nb * H * W * (0.25 * C1 + C2 + C1 + C2), st);
+  if (dt == 0)
+    hipLaunchKernelGGL(upcat_fwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)prev,
+                       (const bf16_t*)skip, (bf16_t*)out, nb, H, W, C1, C2);
+  else
+    hipLaunchKernelGGL(upcat_fwd_k<float>, g, dim3(256), 0, st, (const float*)prev,
+                       (const float*)skip, (float*)out, nb, H, W, C1, C2);
+  return hipGetLastError();
+}
+
+hipError_t upcat_backward(int dt, const void* dcat, void* dprev, void* dskip, int nb, int H,
+                          int W, int C1, int C2, hipStream_t st) {
+  int N = dt == 0 ? 8 : 4;
+  long t1 = (long)nb * (H / 2) * (W / 2) * (C1 / N);
+  long P = (long)nb * H * W;
+  ProfScope ps("upcat_backward", 0.0, (dt == 0 ? 2.0 : 4.0) * P * (C1 + 0.25 * C1 + 2.0 * C2), st);
+  if (dt == 0) {
+    hipLaunchKernelGGL(upcat_bwd_prev_k<bf16_t>, dim3(cdiv(t1, 256)), dim3(256), 0, st,
+                       (const bf16_t*)dcat, (bf16_t*)dprev, nb, H, W, C1, C2);
+    hipLaunchKernelGGL(upcat_bwd_skip_k<bf16_t>, dim3(cdiv(P * (C2 / N), 256)), dim3(256), 0, st,
+                       (const bf16_t*)dcat, (bf16_t*)dskip, P, C1, C2);
+  } else {
+    hipLaunchKernelGGL(upcat_bwd_prev_k<float>, dim3(cdiv(t1, 256)), dim3(256), 0, st,
+                       (const float*)dcat, (float*)dprev, nb, H, W, C1, C2);
+    hipLaunchKernelGGL(upcat_bwd_skip_k<float>, dim3(cdiv(P * (C2 / N), 256)), dim3(256), 0, st,
+                       (const float*)dcat, (float*)dskip, P, C1, C2);
+  }
+  return hipGetLastError();
+}
+
+static long mse_per_block(long n) { return n < 4096 ? 4096 : 16384; }
+size_t mse_partial_floats(long n) { return (size_t)cdiv(n, mse_per_block(n)); }
+
+hipError_t mse_forward_backward(int dt, const void* y, const void* t, void* dy,
+                                float* loss_part, float* partial, long n, float inv_numel,
+                                hipStream_t st) {
+  long pb = mse_per_block(n);
+  int nb = cdiv(n, pb);
+  {
+  ProfScope ps("mse", 3.0 * n, (dt == 0 ? 6.0 : 12.0) * n, st);
+  if (dt == 0)
+    hipLaunchKernelGGL(mse_k<bf16_t>, dim3(nb), dim3(256), 0, st, (const bf16_t*)y,
+                       (const bf16_t*)t, (bf16_t*)dy, partial, n, inv_numel, pb);
+  else
+    hipLaunchKernelGGL(mse_k<float>, dim3(nb), dim3(256), 0, st, (const float*)y,
+                       (const float*)t, (float*)dy, partial, n, inv_numel, pb);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(serial_sum_k, dim3(1), dim3(64), 0, st, (const float*)partial, nb, 1.0f,
+                     loss_part);
+  return hipGetLastError();
+}
+
+hipError_t loss_finalize(const float* parts, int m, float inv_numel, float* loss,
+                         hipStream_t st) {
+  hipLaunchKernelGGL(serial_sum_k, dim3(1), dim3(64), 0, st, parts, m, inv_numel, loss);
+  return hipGetLastError();
+}
+
+hipError_t grad_accumulate_batch(const AccBatch& b, int overwrite, hipStream_t st) {
+  long maxn = 0;
+  double bytes = 0;
+  for (int k = 0; k < b.count; ++k) {
+    maxn = b.n[k] > maxn ? b.n[k] : maxn;
+    bytes += (overwrite ? 8.0 : 12.0) * b.n[k];
+  }
+  if (maxn == 0) return hipSuccess;
+  ProfScope ps("grad_accumulate", 0.0, bytes, st);
+  hipLaunchKernelGGL(accumulate_multi_k, dim3(cdiv(maxn, 1024)), dim3(256), 0, st, b, overwrite);
+  return hipGetLastError();
+}
+
+hipError_t grad_accumulate(float* acc, const float* g, long n, int overwrite, hipStream_t st) {
+  ProfScope ps("grad_accumulate", (double)n, (overwrite ? 8.0 : 12.0) * n, st);
+  hipLaunchKernelGGL(accumulate_k, dim3(cdiv(n, 1024)), dim3(256), 0, st, acc, g, n, overwrite);
+  return hipGetLastError();
+}
+
+}  // namespace tgpk

@@ -1,0 +1,98 @@
+// Internal launcher interface between the host runtime and the HIP kernels.
+// Every launcher enqueues on `st` and returns the launch status.  dt selects
+// the storage type of activations and weights: 0 = bfloat16, 1 = float32.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tgpk {
+
+// One convolution at one micro-batch: nb samples of H x W, NHWC.
+struct ConvShape {
+  int nb, H, W, cin, cout, taps;  // taps = 9 (3x3, pad 1) or 1 (1x1)
+  long pixels() const { return (long)nb * H * W; }
+};
+
+// y = act(conv(x, w) + b); w is KRSC [cout][taps][cin].
+hipError_t conv_forward(int dt, const void* x, const void* w, const float* b, void* y,
+                        const ConvShape& s, int relu, hipStream_t st);
+// Whether the data-gradient kernel for this shape reads the transformed
+// weight wt = [cin][taps][cout] (taps rotated by 180 degrees).
+bool conv_dgrad_uses_wt(int dt, const ConvShape& s);
+hipError_t weight_transform(int dt, const void* w, void* wt, int cout, int cin, int taps,
+                            hipStream_t st);
+// dx[p][ci] = sum_{co,tap} dz[p - off(tap)][co] w[co][tap][ci]
+hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, void* dx,
+                      const ConvShape& s, hipStream_t st);
+// Weight gradient of one micro-batch into dw (float32, KRSC), via split-K
+// partials in `partial` (conv_wgrad_partial_floats floats) reduced in fixed
+// split order.
+size_t conv_wgrad_partial_floats(int dt, const ConvShape& s);
+hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial,
+                      const ConvShape& s, hipStream_t st);
+
+// Depthwise 3x3 (pad 1), w = [c][9].
+hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
+                      int H, int W, int C, int relu, hipStream_t st);
+hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int H, int W,
+                    int C, hipStream_t st);
+size_t dw_wgrad_partial_floats(int nb, int H, int W, int C);
+hipError_t dw_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial, int nb,
+                    int H, int W, int C, hipStream_t st);
+
+// dz = (dy [+ dskip]) * [y > 0] (mask only when relu), stored in dt.
+hipError_t relu_backward(int dt, const void* dy, const void* dskip, const void* y, void* dz,
+                         int relu, long n, hipStream_t st);
+// db[c] = sum_p dz[p][c] over P rows, fixed-order two-stage reduction.
+size_t colsum_partial_floats(long P, int C);
+hipError_t bias_grad(int dt, const void* dz, float* db, float* partial, long P, int C,
+                     hipStream_t st);
+
+// 2x2/2 max-pool of x (nb x H x W x C) into y; backward routes dy to the first
+// maximal element of each window (row-major).
+hipError_t maxpool_forward(int dt, const void* x, void* y, int nb, int H, int W, int C,
+                           hipStream_t st);
+hipError_t maxpool_backward(int dt, const void* x, const void* dy, void* dx, int nb, int H,
+                            int W, int C, hipStream_t st);
+
+// out (nb x H x W x (C1+C2)) = [nearest 2x upsample of prev (H/2 x W/2 x C1), skip].
+hipError_t upcat_forward(int dt, const void* prev, const void* skip, void* out, int nb, int H,
+                         int W, int C1, int C2, hipStream_t st);
+// dprev = sum of 2x2 blocks of dcat[..., :C1]; dskip = dcat[..., C1:].
+hipError_t upcat_backward(int dt, const void* dcat, void* dprev, void* dskip, int nb, int H,
+                          int W, int C1, int C2, hipStream_t st);
+
+// Squared-error part of one micro-batch: *loss_part = sum (y-t)^2 and
+// dy = 2 (y-t) * inv_numel, fixed-order reduction.
+size_t mse_partial_floats(long n);
+hipError_t mse_forward_backward(int dt, const void* y, const void* t, void* dy,
+                                float* loss_part, float* partial, long n, float inv_numel,
+                                hipStream_t st);
+// *loss = (sum_{i<m} parts[i]) * inv_numel, in order.
+hipError_t loss_finalize(const float* parts, int m, float inv_numel, float* loss,
+                         hipStream_t st);
+
+// acc = g (overwrite) or acc + g, float32.
+hipError_t grad_accumulate(float* acc, const float* g, long n, int overwrite, hipStream_t st);
+
+// The same for up to kMaxAcc tensors in one launch (passed by value).
+constexpr int kMaxAcc = 64;
+struct AccBatch {
+  int count;
+  float* acc[kMaxAcc];
+  const float* g[kMaxAcc];
+  long n[kMaxAcc];
+};
+hipError_t grad_accumulate_batch(const AccBatch& b, int overwrite, hipStream_t st);
+
+// relu_backward fused with the bias gradient's column sums (fixed-order
+// two-stage reduction), for layers where relu_bias_fusable() holds.
+bool relu_bias_fusable(int dt, int C, const void* dy, const void* dskip, const void* y,
+                       const void* dz);
+size_t relu_bias_partial_floats(long P, int C);
+hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
+                              int relu, float* db, float* partial, long P, int C,
+                              hipStream_t st);
+
+}  // namespace tgpk

@@ -1,0 +1,91 @@
+#include "prof.h"
+
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "tgp.h"
+
+namespace tgpk {
+namespace {
+
+struct Rec {
+  std::string name;
+  double flops, bytes;
+  hipEvent_t a, b;
+};
+
+struct State {
+  bool on = false;
+  std::vector<Rec> recs;
+  std::vector<hipEvent_t> pool;
+  hipEvent_t get() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+};
+
+thread_local State g;
+
+}  // namespace
+
+bool prof_enabled() { return g.on; }
+
+ProfScope::ProfScope(const char* name, double flops, double bytes, hipStream_t st) : st_(st) {
+  if (!g.on) return;
+  hipEvent_t a = g.get(), b = g.get();
+  if (!a || !b) return;
+  hipEventRecord(a, st);
+  g.recs.push_back({name, flops, bytes, a, b});
+  rec_ = (int)g.recs.size() - 1;
+}
+
+ProfScope::~ProfScope() {
+  if (rec_ >= 0) hipEventRecord(g.recs[rec_].b, st_);
+}
+
+}  // namespace tgpk
+
+extern "C" {
+
+tgp_status tgp_profile_enable(int enable) {
+  tgpk::g.on = enable != 0;
+  return TGP_OK;
+}
+
+tgp_status tgp_profile_read(tgp_kernel_stat* out, int cap, int* count) {
+  using tgpk::g;
+  if (!count) return TGP_EINVAL;
+  std::vector<tgp_kernel_stat> agg;
+  for (auto& r : g.recs) {
+    if (hipEventSynchronize(r.b) != hipSuccess) return TGP_EHIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return TGP_EHIP;
+    tgp_kernel_stat* s = nullptr;
+    for (auto& a : agg)
+      if (r.name == a.name) s = &a;
+    if (!s) {
+      agg.push_back(tgp_kernel_stat{});
+      s = &agg.back();
+      strncpy(s->name, r.name.c_str(), sizeof(s->name) - 1);
+    }
+    s->launches += 1;
+    s->ms += ms;
+    s->flops += r.flops;
+    s->bytes += r.bytes;
+    g.pool.push_back(r.a);
+    g.pool.push_back(r.b);
+  }
+  g.recs.clear();
+  *count = (int)agg.size();
+  for (int k = 0; k < (int)agg.size() && k < cap; ++k) out[k] = agg[k];
+  return *count <= cap ? TGP_OK : TGP_EINVAL;
+}
+
+}  // extern "C"

@@ -1,0 +1,820 @@
+// Host runtime behind the tgp C ABI: network description, FLOP partitioner,
+// workspace planner, per-task state machine, the stage tasks F_{i,j},
+// F'_{i,j} + B_{i,j} and the gradient accumulation, and the clock-cycle
+// scheduler that issues them (Algorithm 1 and its reverse).  It owns no
+// device memory: every buffer is a slice of caller-owned memory.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "tgp.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+tgp_status fail(tgp_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return s;
+}
+
+inline size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
+enum CellState : uint8_t { IDLE = 0, FWD = 1, BWD = 2, ACC = 3 };
+
+struct LayerRt {
+  tgp_layer d;
+  int H = 0, W = 0;            // output size == conv input size (after prologue)
+  int inH = 0, inW = 0, inC = 0;  // pre-prologue input (previous output / net input)
+  int taps = 9;
+  long w_elems = 0;
+  int part = 0;                // 0-based partition
+  const void* w = nullptr;
+  const float* b = nullptr;
+  float* dw_acc = nullptr;
+  float* db_acc = nullptr;
+  bool bound = false;
+  // per micro-batch byte sizes
+  size_t out_bytes = 0, pro_bytes = 0;
+  // workspace offsets
+  size_t o_scr_out = 0, o_scr_pro = 0, o_gw = 0, o_gb = 0, o_wt = 0;
+  std::vector<size_t> o_sto_out, o_sto_pro;  // per stored set
+  bool has_wt = false;
+};
+
+}  // namespace
+
+struct tgp_net {
+  std::vector<LayerRt> L;
+  int in_c = 0, H = 0, W = 0, dt = 0, esz = 2;
+  int n = 0;
+  std::vector<int> lo, hi;
+  std::map<int, int> stash_layer;  // stash id -> layer
+  // plan
+  bool planned = false;
+  int B = 0, m = 0, b = 0, mode = 0;
+  size_t ws_need = 0;
+  char* ws = nullptr;
+  size_t ws_size = 0;
+  int nsets = 0;
+  std::map<int, size_t> o_stash, o_stash_grad;  // offsets for micro-batch 1
+  size_t stash_stride = 0;                      // bytes per micro-batch of stash area
+  size_t o_g0 = 0, o_g1 = 0, o_dinp = 0, o_dz = 0, o_part = 0, o_colpart = 0, o_msepart = 0,
+         o_loss = 0;
+  std::vector<size_t> o_bnd, o_gbnd;  // per (i, j) pipeline boundaries, [i*n + j]
+  size_t o_out = 0, o_dy = 0, out_bytes_mb = 0;
+  // state per (i, j): index (i-1)*n + (j-1)
+  std::vector<uint8_t> st;
+  std::vector<const void*> saved_x;
+  std::vector<void*> saved_y;
+  std::vector<uint8_t> saved_ckpt;
+};
+
+namespace {
+
+long out_elems_mb(const tgp_net* N, const LayerRt& l) { return (long)N->b * l.H * l.W * l.d.cout; }
+
+int64_t layer_flops(const LayerRt& l) {
+  if (l.d.kind == TGP_DWCONV3X3) return 2LL * l.H * l.W * l.d.cout * 9;
+  return 2LL * l.H * l.W * l.d.cout * l.d.cin * l.taps;
+}
+
+// Contiguous split of per-layer costs into n parts: the largest part cost is
+// minimised exactly; among such splits the sum of squared part costs (how
+// uneven the parts are) is minimised; remaining ties go to the earliest cut
+// points.  O(n L^2) dynamic programmes, exact integer arithmetic.
+bool balance_dp(const std::vector<int64_t>& c, int n, std::vector<int>& bal) {
+  typedef unsigned __int128 u128;
+  int L = (int)c.size();
+  if (n < 1 || n > L) return false;
+  std::vector<int64_t> pre(L + 1, 0);
+  for (int i = 0; i < L; ++i) pre[i + 1] = pre[i] + c[i];
+  const int64_t INF = INT64_MAX;
+  // best[k][s]: smallest achievable max part cost splitting layers s..L-1 into k parts
+  std::vector<std::vector<int64_t>> best(n + 1, std::vector<int64_t>(L + 1, INF));
+  best[0][L] = 0;
+  for (int k = 1; k <= n; ++k)
+    for (int s = L - k; s >= 0; --s)
+      for (int e = s + 1; e <= L - (k - 1); ++e) {
+        if (best[k - 1][e] == INF) continue;
+        int64_t v = std::max(best[k - 1][e], pre[e] - pre[s]);
+        if (v < best[k][s]) best[k][s] = v;
+      }
+  const int64_t opt = best[n][0];
+  // sq[k][s]: smallest sum of squared part costs splitting s..L-1 into k parts
+  // with every part <= opt.
+  const u128 UINF = ~(u128)0;
+  std::vector<std::vector<u128>> sq(n + 1, std::vector<u128>(L + 1, UINF));
+  sq[0][L] = 0;
+  for (int k = 1; k <= n; ++k)
+    for (int s = L - k; s >= 0; --s)
+      for (int e = s + 1; e <= L - (k - 1); ++e) {
+        int64_t part = pre[e] - pre[s];
+        if (part > opt || sq[k - 1][e] == UINF) continue;
+        u128 v = sq[k - 1][e] + (u128)part * (u128)part;
+        if (v < sq[k][s]) sq[k][s] = v;
+      }
+  bal.assign(n, 0);
+  int s = 0;
+  for (int k = n; k >= 1; --k) {
+    int chosen = -1;
+    for (int e = s + 1; e <= L - (k - 1); ++e) {
+      int64_t part = pre[e] - pre[s];
+      if (part > opt || sq[k - 1][e] == UINF) continue;
+      if (sq[k - 1][e] + (u128)part * (u128)part == sq[k][s]) { chosen = e; break; }
+    }
+    if (chosen < 0) return false;
+    bal[n - k] = chosen - s;
+    s = chosen;
+  }
+  return s == L;
+}
+
+int vecN(int dt) { return dt == TGP_BF16 ? 8 : 4; }
+
+bool ckpt_of(int mode, int i, int m) {
+  return mode == TGP_CKPT_ALWAYS || (mode == TGP_CKPT_EXCEPT_LAST && i < m);
+}
+
+int cell(const tgp_net* N, int i, int j) { return (i - 1) * N->n + (j - 1); }
+
+hipStream_t S(void* s) { return (hipStream_t)s; }
+
+#define HIPCHK(expr, name)                                                         \
+  do {                                                                             \
+    hipError_t e_ = (expr);                                                        \
+    if (e_ != hipSuccess)                                                          \
+      return fail(TGP_EHIP, "%s: %s", name, hipGetErrorString(e_));                \
+  } while (0)
+
+char* W_(tgp_net* N, size_t off) { return N->ws + off; }
+
+// ------------------------------------------------------------ per-layer device work
+
+struct ActView {
+  const void* in0;              // partition input
+  std::vector<const void*> out; // per layer in partition
+  std::vector<const void*> pro; // per layer in partition (nullptr if none)
+};
+
+size_t stash_off(const tgp_net* N, int i, int sid, bool grad) {
+  auto& m = grad ? N->o_stash_grad : N->o_stash;
+  return m.at(sid) + (size_t)(i - 1) * N->stash_stride;
+}
+
+// Forward over partition j for micro-batch i.  phase: 0 = checkpointed
+// forward, 1 = storing forward, 2 = recompute.
+tgp_status run_forward(tgp_net* N, int j, int i, int phase, const void* x_in, void* y_out,
+                       hipStream_t st) {
+  const int lo = N->lo[j - 1], hi = N->hi[j - 1];
+  int set = (phase == 1) ? (N->mode == TGP_CKPT_NEVER ? i - 1 : 0) : -1;
+  const void* src = x_in;
+  for (int l = lo; l < hi; ++l) {
+    LayerRt& Lr = N->L[l];
+    const tgp_layer& d = Lr.d;
+    void* out;
+    if (phase == 2) out = W_(N, Lr.o_scr_out);
+    else if (l == hi - 1) out = y_out;
+    else if (d.stash_id >= 0) out = W_(N, stash_off(N, i, d.stash_id, false));
+    else if (phase == 1) out = W_(N, Lr.o_sto_out[set]);
+    else out = W_(N, Lr.o_scr_out);
+    const void* cin_ptr = src;
+    if (d.prologue != TGP_PRO_NONE) {
+      void* pro = (phase == 1) ? W_(N, Lr.o_sto_pro[set]) : W_(N, Lr.o_scr_pro);
+      if (d.prologue == TGP_PRO_MAXPOOL2) {
+        HIPCHK(tgpk::maxpool_forward(N->dt, src, pro, N->b, Lr.inH, Lr.inW, Lr.inC, st),
+               "maxpool_forward");
+      } else {
+        const LayerRt& sl = N->L[N->stash_layer.at(d.pop_id)];
+        HIPCHK(tgpk::upcat_forward(N->dt, src, W_(N, stash_off(N, i, d.pop_id, false)), pro,
+                                   N->b, Lr.H, Lr.W, Lr.inC, sl.d.cout, st),
+               "upcat_forward");
+      }
+      cin_ptr = pro;
+    }
+    if (d.kind == TGP_DWCONV3X3) {
+      HIPCHK(tgpk::dw_forward(N->dt, cin_ptr, Lr.w, d.bias ? Lr.b : nullptr, out, N->b, Lr.H,
+                              Lr.W, d.cout, d.relu, st),
+             "dw_forward");
+    } else {
+      tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
+      HIPCHK(tgpk::conv_forward(N->dt, cin_ptr, Lr.w, d.bias ? Lr.b : nullptr, out, s, d.relu,
+                                st),
+             "conv_forward");
+    }
+    src = out;
+  }
+  return TGP_OK;
+}
+
+// Pointers the backward of (i, j) reads: layer outputs and prologue outputs.
+void activation_view(tgp_net* N, int j, int i, bool ckpt, ActView& v) {
+  const int lo = N->lo[j - 1], hi = N->hi[j - 1];
+  int c = cell(N, i, j);
+  v.in0 = N->saved_x[c];
+  v.out.assign(hi - lo, nullptr);
+  v.pro.assign(hi - lo, nullptr);
+  int set = N->mode == TGP_CKPT_NEVER ? i - 1 : 0;
+  for (int l = lo; l < hi; ++l) {
+    LayerRt& Lr = N->L[l];
+    if (ckpt) {
+      v.out[l - lo] = W_(N, Lr.o_scr_out);
+      if (Lr.d.prologue != TGP_PRO_NONE) v.pro[l - lo] = W_(N, Lr.o_scr_pro);
+    } else {
+      if (l == hi - 1) v.out[l - lo] = N->saved_y[c];
+      else if (Lr.d.stash_id >= 0) v.out[l - lo] = W_(N, stash_off(N, i, Lr.d.stash_id, false));
+      else v.out[l - lo] = W_(N, Lr.o_sto_out[set]);
+      if (Lr.d.prologue != TGP_PRO_NONE) v.pro[l - lo] = W_(N, Lr.o_sto_pro[set]);
+    }
+  }
+}
+
+tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_in,
+                        hipStream_t st) {
+  const int lo = N->lo[j - 1], hi = N->hi[j - 1];
+  bool ckpt = N->saved_ckpt[cell(N, i, j)];
+  if (ckpt) {
+    tgp_status r = run_forward(N, j, i, 2, N->saved_x[cell(N, i, j)], nullptr, st);
+    if (r != TGP_OK) return r;
+  }
+  if (i == N->m) {
+    // first backward of partition j in this step: refresh the transformed
+    // weights used by the data-gradient kernels
+    for (int l = lo; l < hi; ++l) {
+      LayerRt& Lr = N->L[l];
+      if (Lr.has_wt)
+        HIPCHK(tgpk::weight_transform(N->dt, Lr.w, W_(N, Lr.o_wt), Lr.d.cout, Lr.d.cin, Lr.taps,
+                                      st),
+               "weight_transform");
+    }
+  }
+  ActView v;
+  activation_view(N, j, i, ckpt, v);
+  void* gcur = W_(N, N->o_g0);
+  void* gnext = W_(N, N->o_g1);
+  void* dz = W_(N, N->o_dz);
+  void* dinp = W_(N, N->o_dinp);
+  float* part = (float*)W_(N, N->o_part);
+  float* colpart = (float*)W_(N, N->o_colpart);
+  const void* dy = dy_out;
+  for (int l = hi - 1; l >= lo; --l) {
+    LayerRt& Lr = N->L[l];
+    const tgp_layer& d = Lr.d;
+    const void* y = v.out[l - lo];
+    const void* src = (l == lo) ? v.in0 : v.out[l - 1 - lo];  // pre-prologue input
+    const void* cin_ptr = d.prologue != TGP_PRO_NONE ? v.pro[l - lo] : src;
+    const void* dskip = d.stash_id >= 0 ? W_(N, stash_off(N, i, d.stash_id, true)) : nullptr;
+    long nout = out_elems_mb(N, Lr);
+    long P = (long)N->b * Lr.H * Lr.W;
+    if (d.bias && tgpk::relu_bias_fusable(N->dt, d.cout, dy, dskip, y, dz)) {
+      HIPCHK(tgpk::relu_backward_bias(N->dt, dy, dskip, y, dz, d.relu, (float*)W_(N, Lr.o_gb),
+                                      colpart, P, d.cout, st),
+             "relu_backward_bias");
+    } else {
+      HIPCHK(tgpk::relu_backward(N->dt, dy, dskip, y, dz, d.relu, nout, st), "relu_backward");
+      if (d.bias)
+        HIPCHK(tgpk::bias_grad(N->dt, dz, (float*)W_(N, Lr.o_gb), colpart, P, d.cout, st),
+               "bias_grad");
+    }
+    float* gw = (float*)W_(N, Lr.o_gw);
+    if (d.kind == TGP_DWCONV3X3) {
+      HIPCHK(tgpk::dw_wgrad(N->dt, cin_ptr, dz, gw, part, N->b, Lr.H, Lr.W, d.cout, st),
+             "dw_wgrad");
+    } else {
+      tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
+      HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr, dz, gw, part, s, st), "conv_wgrad");
+    }
+    if (l == lo && dx_in == nullptr) break;
+    void* dest_prev = (l == lo) ? dx_in : gnext;  // gradient of the pre-prologue input
+    void* dgrad_out = d.prologue == TGP_PRO_NONE ? dest_prev : dinp;
+    if (d.kind == TGP_DWCONV3X3) {
+      HIPCHK(tgpk::dw_dgrad(N->dt, dz, Lr.w, dgrad_out, N->b, Lr.H, Lr.W, d.cout, st),
+             "dw_dgrad");
+    } else {
+      tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
+      HIPCHK(tgpk::conv_dgrad(N->dt, dz, Lr.w, Lr.has_wt ? W_(N, Lr.o_wt) : nullptr, dgrad_out,
+                              s, st),
+             "conv_dgrad");
+    }
+    if (d.prologue == TGP_PRO_MAXPOOL2) {
+      HIPCHK(tgpk::maxpool_backward(N->dt, src, dinp, dest_prev, N->b, Lr.inH, Lr.inW, Lr.inC,
+                                    st),
+             "maxpool_backward");
+    } else if (d.prologue == TGP_PRO_UPCAT2) {
+      const LayerRt& sl = N->L[N->stash_layer.at(d.pop_id)];
+      HIPCHK(tgpk::upcat_backward(N->dt, dinp, dest_prev,
+                                  W_(N, stash_off(N, i, d.pop_id, true)), N->b, Lr.H, Lr.W,
+                                  Lr.inC, sl.d.cout, st),
+             "upcat_backward");
+    }
+    dy = gnext;
+    std::swap(gcur, gnext);
+  }
+  return TGP_OK;
+}
+
+tgp_status run_accumulate(tgp_net* N, int j, int overwrite, hipStream_t st) {
+  tgpk::AccBatch batch;
+  batch.count = 0;
+  auto flush = [&]() -> tgp_status {
+    if (batch.count == 0) return TGP_OK;
+    HIPCHK(tgpk::grad_accumulate_batch(batch, overwrite, st), "grad_accumulate");
+    batch.count = 0;
+    return TGP_OK;
+  };
+  auto add = [&](float* acc, const float* g, long n) -> tgp_status {
+    if (batch.count == tgpk::kMaxAcc) {
+      tgp_status r = flush();
+      if (r != TGP_OK) return r;
+    }
+    batch.acc[batch.count] = acc;
+    batch.g[batch.count] = g;
+    batch.n[batch.count] = n;
+    ++batch.count;
+    return TGP_OK;
+  };
+  for (int l = N->lo[j - 1]; l < N->hi[j - 1]; ++l) {
+    LayerRt& Lr = N->L[l];
+    tgp_status r = add(Lr.dw_acc, (const float*)W_(N, Lr.o_gw), Lr.w_elems);
+    if (r == TGP_OK && Lr.d.bias) r = add(Lr.db_acc, (const float*)W_(N, Lr.o_gb), Lr.d.cout);
+    if (r != TGP_OK) return r;
+  }
+  return flush();
+}
+
+// Plan and workspace present, and the layers of partition j (all partitions
+// for j = 0) bound.
+tgp_status check_ready(const tgp_net* N, int j = 0) {
+  if (!N) return fail(TGP_EINVAL, "net is NULL");
+  if (!N->planned) return fail(TGP_ESTATE, "tgp_plan has not been called");
+  if (!N->ws) return fail(TGP_ESTATE, "no workspace bound");
+  int lo = 0, hi = (int)N->L.size();
+  if (j >= 1 && j <= N->n) { lo = N->lo[j - 1]; hi = N->hi[j - 1]; }
+  for (int l = lo; l < hi; ++l)
+    if (!N->L[l].bound) return fail(TGP_ESTATE, "layer %d has no bound parameters", l);
+  return TGP_OK;
+}
+
+// ------------------------------------------------------------ schedule
+
+struct Exec {
+  virtual ~Exec() {}
+  virtual tgp_status forward(int i, int j, bool ckpt) = 0;
+  virtual tgp_status loss(int i) = 0;
+  virtual tgp_status backward(int i, int j, bool recompute) = 0;
+  virtual tgp_status accumulate(int i, int j, bool overwrite) = 0;
+};
+
+// Forward clocks k = 1..m+n-1 run every F_{i,j} with i + j - 1 = k, j
+// ascending (Algorithm 1; tasks of one clock are independent).  The loss of
+// micro-batch i is taken right after F_{i,n}.  Backward clocks run in the
+// reverse order with j descending, which keeps B_{i,j+1} before B_{i,j} and
+// B_{i+1,j} before B_{i,j} (Sec. 2.1); each B_{i,j} is preceded by its
+// recompute when F_{i,j} was checkpointed and followed by the accumulation of
+// g_i^j.
+tgp_status run_schedule(int m, int n, int mode, Exec& ex) {
+  for (int k = 1; k <= m + n - 1; ++k)
+    for (int j = 1; j <= n; ++j) {
+      int i = k - j + 1;
+      if (i < 1 || i > m) continue;
+      tgp_status r = ex.forward(i, j, ckpt_of(mode, i, m));
+      if (r != TGP_OK) return r;
+      if (j == n && (r = ex.loss(i)) != TGP_OK) return r;
+    }
+  for (int k = m + n - 1; k >= 1; --k)
+    for (int j = n; j >= 1; --j) {
+      int i = k - j + 1;
+      if (i < 1 || i > m) continue;
+      tgp_status r = ex.backward(i, j, ckpt_of(mode, i, m));
+      if (r != TGP_OK) return r;
+      if ((r = ex.accumulate(i, j, i == m)) != TGP_OK) return r;
+    }
+  return TGP_OK;
+}
+
+struct TraceExec : Exec {
+  std::vector<int32_t> ops;
+  void put(int op, int i, int j) { ops.push_back(op); ops.push_back(i); ops.push_back(j); }
+  tgp_status forward(int i, int j, bool) override { put(TGP_OP_FORWARD, i, j); return TGP_OK; }
+  tgp_status loss(int i) override { put(TGP_OP_LOSS, i, 0); return TGP_OK; }
+  tgp_status backward(int i, int j, bool rc) override {
+    if (rc) put(TGP_OP_RECOMPUTE, i, j);
+    put(TGP_OP_BACKWARD, i, j);
+    return TGP_OK;
+  }
+  tgp_status accumulate(int i, int j, bool) override { put(TGP_OP_ACCUMULATE, i, j); return TGP_OK; }
+};
+
+size_t slot_bytes_mb(const tgp_net* N, int l) {  // output of layer l for one micro-batch
+  return al256((size_t)N->b * N->L[l].H * N->L[l].W * N->L[l].d.cout * N->esz);
+}
+
+struct GpuExec : Exec {
+  tgp_net* N;
+  const char* x;
+  const char* target;
+  float* loss_dev;
+  char* y_out;
+  hipStream_t st;
+  size_t in_mb_bytes, out_mb_bytes;
+  const void* bnd(int i, int j) {  // output of partition j for micro-batch i (j = 0: input)
+    if (j == 0) return x + (size_t)(i - 1) * in_mb_bytes;
+    if (j == N->n) return y_out ? (const void*)(y_out + (size_t)(i - 1) * out_mb_bytes)
+                                : (const void*)W_(N, N->o_out + (size_t)(i - 1) * al256(out_mb_bytes));
+    return W_(N, N->o_bnd[(i - 1) * N->n + j]);
+  }
+  void* gbnd(int i, int j) {  // gradient of the output of partition j
+    if (j == N->n) return W_(N, N->o_dy + (size_t)(i - 1) * al256(out_mb_bytes));
+    return W_(N, N->o_gbnd[(i - 1) * N->n + j]);
+  }
+  tgp_status forward(int i, int j, bool ckpt) override {
+    return tgp_stage_forward(N, j, i, ckpt ? 1 : 0, bnd(i, j - 1), (void*)bnd(i, j), st);
+  }
+  tgp_status loss(int i) override {
+    const LayerRt& last = N->L.back();
+    long n_mb = (long)N->b * last.H * last.W * last.d.cout;
+    long numel = n_mb * N->m;
+    HIPCHK(tgpk::mse_forward_backward(N->dt, bnd(i, N->n),
+                                      target + (size_t)(i - 1) * out_mb_bytes, gbnd(i, N->n),
+                                      (float*)W_(N, N->o_loss) + (i - 1),
+                                      (float*)W_(N, N->o_msepart), n_mb, 1.0f / (float)numel,
+                                      st),
+           "mse_forward_backward");
+    return TGP_OK;
+  }
+  tgp_status backward(int i, int j, bool) override {
+    return tgp_stage_backward_recompute(N, j, i, gbnd(i, j), j > 1 ? gbnd(i, j - 1) : nullptr,
+                                        st);
+  }
+  tgp_status accumulate(int i, int j, bool ow) override {
+    return tgp_grad_accumulate(N, j, i, ow ? 1 : 0, st);
+  }
+};
+
+}  // namespace
+
+// ============================================================ C ABI
+
+extern "C" {
+
+const char* tgp_last_error(void) { return g_err.c_str(); }
+
+tgp_status tgp_net_create(const tgp_layer* layers, int n_layers, int in_c, int H, int W,
+                          int dtype, tgp_net** out) {
+  g_err.clear();
+  if (!out) return fail(TGP_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!layers || n_layers < 1) return fail(TGP_EINVAL, "need at least one layer");
+  if (in_c < 1 || H < 1 || W < 1) return fail(TGP_EINVAL, "bad input shape");
+  if (dtype != TGP_BF16 && dtype != TGP_FP32) return fail(TGP_EINVAL, "bad dtype %d", dtype);
+  tgp_net* N = new tgp_net;
+  N->in_c = in_c; N->H = H; N->W = W; N->dt = dtype; N->esz = dtype == TGP_BF16 ? 2 : 4;
+  int c = in_c, h = H, w = W;
+  std::map<int, std::pair<int, std::pair<int, int>>> stashed;  // id -> (C, (H, W))
+  const int V = vecN(dtype);
+  for (int l = 0; l < n_layers; ++l) {
+    LayerRt Lr;
+    Lr.d = layers[l];
+    const tgp_layer& d = Lr.d;
+    auto bad = [&](tgp_status s, const char* why) {
+      delete N;
+      return fail(s, "layer %d: %s", l, why);
+    };
+    if (d.kind < 0 || d.kind > 2) return bad(TGP_EINVAL, "bad kind");
+    if (d.cin < 1 || d.cout < 1) return bad(TGP_EINVAL, "bad channel count");
+    if (d.prologue < 0 || d.prologue > 2) return bad(TGP_EINVAL, "bad prologue");
+    if (d.stash_id < -1 || d.stash_id > 63 || d.pop_id < -1 || d.pop_id > 63)
+      return bad(TGP_EINVAL, "skip id out of range");
+    Lr.inH = h; Lr.inW = w; Lr.inC = c;
+    int want = c;
+    if (d.prologue == TGP_PRO_MAXPOOL2) {
+      if (h % 2 || w % 2) return bad(TGP_EINVAL, "max-pool of an odd size");
+      if (c % V) return bad(TGP_EUNSUPPORTED, "max-pool channels must be a multiple of 8 (bf16) / 4 (fp32)");
+      h /= 2; w /= 2;
+    } else if (d.prologue == TGP_PRO_UPCAT2) {
+      auto it = stashed.find(d.pop_id);
+      if (it == stashed.end()) return bad(TGP_EINVAL, "pops a skip no earlier layer stashed");
+      h *= 2; w *= 2;
+      if (it->second.second != std::make_pair(h, w)) return bad(TGP_EINVAL, "skip size mismatch");
+      if (c % V || it->second.first % V)
+        return bad(TGP_EUNSUPPORTED, "upsample-concat channels must be a multiple of 8 (bf16) / 4 (fp32)");
+      want = c + it->second.first;
+      stashed.erase(it);
+    } else if (d.pop_id >= 0) {
+      return bad(TGP_EINVAL, "pop_id set without an UPCAT2 prologue");
+    }
+    if (d.cin != want) return bad(TGP_EINVAL, "cin does not match the incoming channels");
+    if (d.kind == TGP_DWCONV3X3 && d.cin != d.cout) return bad(TGP_EINVAL, "depthwise needs cin == cout");
+    Lr.H = h; Lr.W = w;
+    Lr.taps = d.kind == TGP_CONV1X1 ? 1 : 9;
+    Lr.w_elems = d.kind == TGP_DWCONV3X3 ? (long)d.cout * 9 : (long)d.cout * d.cin * Lr.taps;
+    c = d.cout;
+    if (d.stash_id >= 0) {
+      if (N->stash_layer.count(d.stash_id)) return bad(TGP_EINVAL, "stash id used twice");
+      N->stash_layer[d.stash_id] = l;
+      stashed[d.stash_id] = {c, {h, w}};
+    }
+    N->L.push_back(Lr);
+  }
+  N->n = 1;
+  N->lo = {0};
+  N->hi = {n_layers};
+  *out = N;
+  return TGP_OK;
+}
+
+void tgp_net_destroy(tgp_net* net) { delete net; }
+
+tgp_status tgp_layer_flops(const tgp_net* N, int layer, int64_t* flops) {
+  if (!N || !flops) return fail(TGP_EINVAL, "NULL argument");
+  if (layer < 0 || layer >= (int)N->L.size()) return fail(TGP_EINVAL, "bad layer %d", layer);
+  *flops = layer_flops(N->L[layer]);
+  return TGP_OK;
+}
+
+tgp_status tgp_balance_minmax(const int64_t* cost, int L, int n, int* balance) {
+  if (!cost || !balance || L < 1) return fail(TGP_EINVAL, "bad arguments");
+  if (n < 1 || n > L) return fail(TGP_EINVAL, "n=%d must be in 1..%d", n, L);
+  std::vector<int64_t> c(cost, cost + L);
+  for (auto v : c)
+    if (v < 0) return fail(TGP_EINVAL, "negative cost");
+  std::vector<int> bal;
+  if (!balance_dp(c, n, bal)) return fail(TGP_EINVAL, "no split");
+  std::copy(bal.begin(), bal.end(), balance);
+  return TGP_OK;
+}
+
+tgp_status tgp_set_partition(tgp_net* N, int n, const int* balance) {
+  if (!N) return fail(TGP_EINVAL, "net is NULL");
+  int L = (int)N->L.size();
+  if (n < 1 || n > L) return fail(TGP_EINVAL, "n=%d must be in 1..%d", n, L);
+  std::vector<int> bal;
+  if (balance) {
+    int sum = 0;
+    for (int k = 0; k < n; ++k) {
+      if (balance[k] < 1) return fail(TGP_EINVAL, "empty partition %d", k + 1);
+      sum += balance[k];
+    }
+    if (sum != L) return fail(TGP_EINVAL, "balance sums to %d, need %d", sum, L);
+    bal.assign(balance, balance + n);
+  } else {
+    std::vector<int64_t> c;
+    for (auto& l : N->L) c.push_back(layer_flops(l));
+    if (!balance_dp(c, n, bal)) return fail(TGP_EINVAL, "no split");
+  }
+  N->n = n;
+  N->lo.assign(n, 0);
+  N->hi.assign(n, 0);
+  int s = 0;
+  for (int k = 0; k < n; ++k) {
+    N->lo[k] = s;
+    s += bal[k];
+    N->hi[k] = s;
+    for (int l = N->lo[k]; l < N->hi[k]; ++l) N->L[l].part = k;
+  }
+  N->planned = false;
+  N->ws = nullptr;
+  return TGP_OK;
+}
+
+tgp_status tgp_get_partition(const tgp_net* N, int* n, int* balance) {
+  if (!N || !n) return fail(TGP_EINVAL, "NULL argument");
+  *n = N->n;
+  if (balance)
+    for (int k = 0; k < N->n; ++k) balance[k] = N->hi[k] - N->lo[k];
+  return TGP_OK;
+}
+
+tgp_status tgp_bind_params(tgp_net* N, int layer, const void* w, const float* b, float* dw_acc,
+                           float* db_acc) {
+  if (!N) return fail(TGP_EINVAL, "net is NULL");
+  if (layer < 0 || layer >= (int)N->L.size()) return fail(TGP_EINVAL, "bad layer %d", layer);
+  LayerRt& Lr = N->L[layer];
+  if (!w || !dw_acc) return fail(TGP_EINVAL, "layer %d: NULL weight or accumulator", layer);
+  if (Lr.d.bias && (!b || !db_acc)) return fail(TGP_EINVAL, "layer %d: bias pointers missing", layer);
+  if (!Lr.d.bias && (b || db_acc)) return fail(TGP_EINVAL, "layer %d has no bias", layer);
+  Lr.w = w; Lr.b = b; Lr.dw_acc = dw_acc; Lr.db_acc = db_acc; Lr.bound = true;
+  return TGP_OK;
+}
+
+tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
+  if (!N || !bytes) return fail(TGP_EINVAL, "NULL argument");
+  if (m < 1 || B < 1) return fail(TGP_EINVAL, "B and m must be positive");
+  if (B % m) return fail(TGP_EINVAL, "B=%d is not divisible by m=%d", B, m);
+  if (mode < 0 || mode > 2) return fail(TGP_EINVAL, "bad checkpoint mode %d", mode);
+  N->B = B; N->m = m; N->b = B / m; N->mode = mode;
+  const int n = N->n;
+  for (auto& l : N->L)
+    if ((long)N->b * l.H * l.W >= (1L << 31) / 4 || (long)N->b * l.inH * l.inW >= (1L << 31) / 4)
+      return fail(TGP_EINVAL, "micro-batch too large for 32-bit pixel indices");
+  size_t off = 0;
+  auto take = [&](size_t bytes_) { size_t o = off; off += al256(bytes_); return o; };
+  // skips and their gradients, one slot per micro-batch
+  N->o_stash.clear(); N->o_stash_grad.clear();
+  size_t stride = 0;
+  for (auto& kv : N->stash_layer) stride += slot_bytes_mb(N, kv.second);
+  N->stash_stride = stride;
+  size_t base = take(stride * m), acc = 0;
+  for (auto& kv : N->stash_layer) { N->o_stash[kv.first] = base + acc; acc += slot_bytes_mb(N, kv.second); }
+  base = take(stride * m); acc = 0;
+  for (auto& kv : N->stash_layer) { N->o_stash_grad[kv.first] = base + acc; acc += slot_bytes_mb(N, kv.second); }
+  // transient activations (checkpointed forward and recompute)
+  size_t max_act = 0, max_pro = 0;
+  for (size_t l = 0; l < N->L.size(); ++l) {
+    LayerRt& Lr = N->L[l];
+    Lr.out_bytes = (size_t)N->b * Lr.H * Lr.W * Lr.d.cout * N->esz;
+    Lr.pro_bytes = Lr.d.prologue != TGP_PRO_NONE ? (size_t)N->b * Lr.H * Lr.W * Lr.d.cin * N->esz : 0;
+    size_t in_bytes = (size_t)N->b * Lr.inH * Lr.inW * Lr.inC * N->esz;
+    max_act = std::max({max_act, Lr.out_bytes, in_bytes});
+    max_pro = std::max(max_pro, Lr.pro_bytes);
+    Lr.o_scr_out = take(Lr.out_bytes);
+    Lr.o_scr_pro = Lr.pro_bytes ? take(Lr.pro_bytes) : 0;
+  }
+  // stored activations of non-checkpointed micro-batches
+  N->nsets = mode == TGP_CKPT_NEVER ? m : (mode == TGP_CKPT_EXCEPT_LAST ? 1 : 0);
+  for (size_t l = 0; l < N->L.size(); ++l) {
+    LayerRt& Lr = N->L[l];
+    Lr.o_sto_out.assign(N->nsets, 0);
+    Lr.o_sto_pro.assign(N->nsets, 0);
+    bool last_of_part = (int)l == N->hi[Lr.part] - 1;
+    for (int s = 0; s < N->nsets; ++s) {
+      if (!last_of_part && Lr.d.stash_id < 0) Lr.o_sto_out[s] = take(Lr.out_bytes);
+      if (Lr.pro_bytes) Lr.o_sto_pro[s] = take(Lr.pro_bytes);
+    }
+  }
+  // per-micro-batch gradients g_i and transformed weights
+  size_t max_part = 0, max_col = 0;
+  for (auto& Lr : N->L) {
+    Lr.o_gw = take(Lr.w_elems * 4);
+    Lr.o_gb = Lr.d.bias ? take(Lr.d.cout * 4) : 0;
+    tgpk::ConvShape s{N->b, Lr.H, Lr.W, Lr.d.cin, Lr.d.cout, Lr.taps};
+    Lr.has_wt = Lr.d.kind != TGP_DWCONV3X3 && tgpk::conv_dgrad_uses_wt(N->dt, s);
+    Lr.o_wt = Lr.has_wt ? take(Lr.w_elems * N->esz) : 0;
+    size_t pf = Lr.d.kind == TGP_DWCONV3X3 ? tgpk::dw_wgrad_partial_floats(N->b, Lr.H, Lr.W, Lr.d.cout)
+                                           : tgpk::conv_wgrad_partial_floats(N->dt, s);
+    max_part = std::max(max_part, pf);
+    max_col = std::max({max_col, tgpk::colsum_partial_floats((long)N->b * Lr.H * Lr.W, Lr.d.cout),
+                        tgpk::relu_bias_partial_floats((long)N->b * Lr.H * Lr.W, Lr.d.cout)});
+  }
+  N->o_g0 = take(max_act);
+  N->o_g1 = take(max_act);
+  N->o_dz = take(max_act);
+  N->o_dinp = take(std::max<size_t>(max_pro, 16));
+  N->o_part = take(max_part * 4);
+  N->o_colpart = take(max_col * 4);
+  const LayerRt& last = N->L.back();
+  long out_mb = (long)N->b * last.H * last.W * last.d.cout;
+  N->out_bytes_mb = out_mb * N->esz;
+  N->o_msepart = take(tgpk::mse_partial_floats(out_mb) * 4);
+  N->o_loss = take(m * 4);
+  // pipeline boundaries
+  N->o_bnd.assign((size_t)m * n + n, 0);
+  N->o_gbnd.assign((size_t)m * n + n, 0);
+  for (int i = 1; i <= m; ++i)
+    for (int j = 1; j < n; ++j) {
+      N->o_bnd[(i - 1) * n + j] = take(N->L[N->hi[j - 1] - 1].out_bytes);
+      N->o_gbnd[(i - 1) * n + j] = take(N->L[N->hi[j - 1] - 1].out_bytes);
+    }
+  N->o_out = take(al256(N->out_bytes_mb) * m);
+  N->o_dy = take(al256(N->out_bytes_mb) * m);
+  N->ws_need = off;
+  N->planned = true;
+  N->ws = nullptr;
+  N->ws_size = 0;
+  N->st.assign((size_t)m * n, IDLE);
+  N->saved_x.assign((size_t)m * n, nullptr);
+  N->saved_y.assign((size_t)m * n, nullptr);
+  N->saved_ckpt.assign((size_t)m * n, 0);
+  *bytes = off;
+  return TGP_OK;
+}
+
+tgp_status tgp_bind_workspace(tgp_net* N, void* dev, size_t bytes) {
+  if (!N) return fail(TGP_EINVAL, "net is NULL");
+  if (!N->planned) return fail(TGP_ESTATE, "tgp_plan has not been called");
+  if (!dev) return fail(TGP_EINVAL, "workspace is NULL");
+  if ((uintptr_t)dev & 255) return fail(TGP_EINVAL, "workspace must be 256-byte aligned");
+  if (bytes < N->ws_need)
+    return fail(TGP_ENOSPACE, "workspace of %zu bytes, need %zu", bytes, N->ws_need);
+  N->ws = (char*)dev;
+  N->ws_size = bytes;
+  return TGP_OK;
+}
+
+tgp_status tgp_stash_ptr(tgp_net* N, int i, int stash_id, int grad, void** p) {
+  if (!N || !p) return fail(TGP_EINVAL, "NULL argument");
+  if (!N->planned || !N->ws) return fail(TGP_ESTATE, "no plan or workspace");
+  if (i < 1 || i > N->m) return fail(TGP_EINVAL, "micro-batch %d out of 1..%d", i, N->m);
+  if (!N->stash_layer.count(stash_id)) return fail(TGP_EINVAL, "no skip %d", stash_id);
+  *p = W_(N, stash_off(N, i, stash_id, grad != 0));
+  return TGP_OK;
+}
+
+tgp_status tgp_stage_forward(tgp_net* N, int j, int i, int checkpoint, const void* x_in,
+                             void* y_out, void* stream) {
+  tgp_status r = check_ready(N, j);
+  if (r != TGP_OK) return r;
+  if (j < 1 || j > N->n) return fail(TGP_EINVAL, "partition %d out of 1..%d", j, N->n);
+  if (i < 1 || i > N->m) return fail(TGP_EINVAL, "micro-batch %d out of 1..%d", i, N->m);
+  if (!x_in || !y_out) return fail(TGP_EINVAL, "NULL x_in or y_out");
+  if ((checkpoint != 0) != ckpt_of(N->mode, i, N->m))
+    return fail(TGP_EINVAL, "checkpoint=%d disagrees with the planned policy for i=%d", checkpoint, i);
+  int c = cell(N, i, j);
+  if (N->st[c] == FWD || N->st[c] == BWD)
+    return fail(TGP_ESTATE, "F_{%d,%d} already ran in this step", i, j);
+  r = run_forward(N, j, i, checkpoint ? 0 : 1, x_in, y_out, S(stream));
+  if (r != TGP_OK) return r;
+  N->st[c] = FWD;
+  N->saved_x[c] = x_in;
+  N->saved_y[c] = y_out;
+  N->saved_ckpt[c] = checkpoint ? 1 : 0;
+  return TGP_OK;
+}
+
+tgp_status tgp_stage_backward_recompute(tgp_net* N, int j, int i, const void* dy_out,
+                                        void* dx_in, void* stream) {
+  tgp_status r = check_ready(N, j);
+  if (r != TGP_OK) return r;
+  if (j < 1 || j > N->n) return fail(TGP_EINVAL, "partition %d out of 1..%d", j, N->n);
+  if (i < 1 || i > N->m) return fail(TGP_EINVAL, "micro-batch %d out of 1..%d", i, N->m);
+  if (!dy_out) return fail(TGP_EINVAL, "NULL dy_out");
+  int c = cell(N, i, j);
+  if (N->st[c] != FWD) return fail(TGP_ESTATE, "B_{%d,%d} needs F_{%d,%d} first", i, j, i, j);
+  if (i < N->m && N->st[cell(N, i + 1, j)] != ACC)
+    return fail(TGP_ESTATE, "B_{%d,%d} must follow B_{%d,%d} and its accumulation", i, j, i + 1, j);
+  r = run_backward(N, j, i, dy_out, dx_in, S(stream));
+  if (r != TGP_OK) return r;
+  N->st[c] = BWD;
+  return TGP_OK;
+}
+
+tgp_status tgp_grad_accumulate(tgp_net* N, int j, int i, int overwrite, void* stream) {
+  tgp_status r = check_ready(N, j);
+  if (r != TGP_OK) return r;
+  if (j < 1 || j > N->n) return fail(TGP_EINVAL, "partition %d out of 1..%d", j, N->n);
+  if (i < 1 || i > N->m) return fail(TGP_EINVAL, "micro-batch %d out of 1..%d", i, N->m);
+  if ((overwrite != 0) != (i == N->m))
+    return fail(TGP_EINVAL, "overwrite must be 1 exactly for i = m");
+  int c = cell(N, i, j);
+  if (N->st[c] != BWD) return fail(TGP_ESTATE, "accumulate (%d,%d) needs B_{%d,%d} first", i, j, i, j);
+  r = run_accumulate(N, j, overwrite, S(stream));
+  if (r != TGP_OK) return r;
+  N->st[c] = ACC;
+  return TGP_OK;
+}
+
+tgp_status tgp_pipeline_step(tgp_net* N, const void* x, const void* target, int B, int m, int n,
+                             int mode, float* loss_dev, void* y_out, void* stream) {
+  tgp_status r = check_ready(N);
+  if (r != TGP_OK) return r;
+  if (!x || !target || !loss_dev) return fail(TGP_EINVAL, "NULL x, target or loss");
+  if (B != N->B || m != N->m || mode != N->mode)
+    return fail(TGP_EINVAL, "B/m/mode differ from tgp_plan (%d/%d/%d)", N->B, N->m, N->mode);
+  if (n != N->n) return fail(TGP_EINVAL, "n=%d differs from the partition (%d)", n, N->n);
+  for (int c = 0; c < m * n; ++c)
+    if (N->st[c] == FWD || N->st[c] == BWD)
+      return fail(TGP_ESTATE, "a stage step is in progress");
+  GpuExec ex;
+  ex.N = N;
+  ex.x = (const char*)x;
+  ex.target = (const char*)target;
+  ex.loss_dev = loss_dev;
+  ex.y_out = (char*)y_out;
+  ex.st = S(stream);
+  ex.in_mb_bytes = (size_t)N->b * N->H * N->W * N->in_c * N->esz;
+  ex.out_mb_bytes = N->out_bytes_mb;
+  r = run_schedule(m, n, mode, ex);
+  if (r != TGP_OK) return r;
+  const LayerRt& last = N->L.back();
+  long numel = (long)N->B * last.H * last.W * last.d.cout;
+  HIPCHK(tgpk::loss_finalize((const float*)W_(N, N->o_loss), m, 1.0f / (float)numel, loss_dev,
+                             S(stream)),
+         "loss_finalize");
+  return TGP_OK;
+}
+
+tgp_status tgp_schedule_trace(int m, int n, int mode, int32_t* ops, int cap, int* count) {
+  if (!count) return fail(TGP_EINVAL, "count is NULL");
+  if (m < 1 || n < 1) return fail(TGP_EINVAL, "m and n must be positive");
+  if (mode < 0 || mode > 2) return fail(TGP_EINVAL, "bad checkpoint mode %d", mode);
+  TraceExec t;
+  run_schedule(m, n, mode, t);
+  *count = (int)(t.ops.size() / 3);
+  if (*count > cap || (!ops && *count > 0)) return fail(TGP_EINVAL, "capacity %d < %d ops", cap, *count);
+  std::copy(t.ops.begin(), t.ops.end(), ops);
+  return TGP_OK;
+}
+
+}  // extern "C"

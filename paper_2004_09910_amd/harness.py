@@ -1,0 +1,188 @@
+"""Torch-side harness around the C ABI: device memory, seeded parameters and
+layout conversion for tests, the benchmark and the smoke check.
+
+Torch provides device memory, streams and exact layout permutations only;
+every step of the method runs in libtgp.so.
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+import paper_2004_09910_amd as tgp
+from workloads import specs, synth
+from workloads.specs import BF16, CONV1X1, DWCONV3X3, FP32
+
+TORCH_DT = {BF16: torch.bfloat16, FP32: torch.float32}
+
+
+def raw_to_torch(raw: np.ndarray, dtype: int) -> torch.Tensor:
+    """Raw storage (float32 array, or uint16 bfloat16 bits) -> CPU tensor."""
+    if dtype == FP32:
+        return torch.from_numpy(np.ascontiguousarray(raw, dtype=np.float32))
+    return torch.from_numpy(np.ascontiguousarray(raw).view(np.int16)).view(torch.bfloat16)
+
+
+def nchw_to_device_nhwc(raw: np.ndarray, dtype: int, device="cuda") -> torch.Tensor:
+    t = raw_to_torch(raw, dtype)
+    return t.permute(0, 2, 3, 1).contiguous().to(device)
+
+
+def nhwc_to_nchw64(t: torch.Tensor) -> np.ndarray:
+    return t.detach().float().cpu().permute(0, 3, 1, 2).contiguous().numpy().astype(np.float64)
+
+
+class _CAI:
+    """Exposes a raw device address to torch.as_tensor (no copy)."""
+
+    def __init__(self, ptr: int, shape, typestr: str):
+        self.__cuda_array_interface__ = {"shape": tuple(shape), "typestr": typestr,
+                                         "data": (int(ptr), False), "version": 2,
+                                         "strides": None}
+
+
+def wrap(ptr: int, shape, dtype: int, device="cuda") -> torch.Tensor:
+    if dtype == FP32:
+        return torch.as_tensor(_CAI(ptr, shape, "<f4"), device=device)
+    return torch.as_tensor(_CAI(ptr, shape, "<i2"), device=device).view(torch.bfloat16)
+
+
+def layer_tuple(L: specs.Layer):
+    return (L.kind, L.cin, L.cout, int(L.relu), int(L.bias), L.prologue, L.stash_id, L.pop_id)
+
+
+class Session:
+    """One network on one device with seeded parameters bound."""
+
+    def __init__(self, net: specs.Net, dtype: int, n: int = 1,
+                 balance: Optional[Sequence[int]] = None, device: str = "cuda",
+                 seed_offset: int = 0, bind_layers: Optional[Sequence[int]] = None):
+        self.net, self.dtype, self.device = net, dtype, device
+        self.h = tgp.net_create([layer_tuple(L) for L in net.layers], net.in_channels,
+                                net.height, net.width, dtype)
+        tgp.set_partition(self.h, n, balance)
+        self.n = n
+        self.balance = tgp.get_partition(self.h)
+        self.bounds = []
+        lo = 0
+        for c in self.balance:
+            self.bounds.append((lo, lo + c))
+            lo += c
+        self.shapes = net.shapes()
+        self.params: Dict[int, dict] = {}
+        layers = range(len(net.layers)) if bind_layers is None else bind_layers
+        for idx in layers:
+            self._bind_layer(idx, seed_offset)
+        self.ws = None
+        self.B = self.m = self.b = self.mode = None
+
+    def _bind_layer(self, idx: int, seed_offset: int):
+        L = self.net.layers[idx]
+        (w64, wraw), b = synth.layer_params(self.net, idx, self.dtype, seed_offset)
+        wt = raw_to_torch(wraw, self.dtype)
+        if L.kind == DWCONV3X3:
+            wk = wt.reshape(L.cout, 9)
+        else:
+            wk = wt.permute(0, 2, 3, 1)   # OIHW -> KRSC
+        wk = wk.contiguous().to(self.device)
+        bt = None if b is None else torch.from_numpy(b[1]).to(self.device)
+        dw = torch.zeros(wk.shape, dtype=torch.float32, device=self.device)
+        db = None if b is None else torch.zeros(L.cout, dtype=torch.float32, device=self.device)
+        tgp.bind_params(self.h, idx, wk.data_ptr(), None if bt is None else bt.data_ptr(),
+                        dw.data_ptr(), None if db is None else db.data_ptr())
+        self.params[idx] = {"w": wk, "b": bt, "dw": dw, "db": db, "w64": w64,
+                            "b64": None if b is None else b[0]}
+
+    def plan(self, B: int, m: int, mode: int) -> int:
+        nbytes = tgp.plan(self.h, B, m, mode)
+        self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        tgp.bind_workspace(self.h, self.ws.data_ptr(), self.ws.numel())
+        self.B, self.m, self.b, self.mode = B, m, B // m, mode
+        return nbytes
+
+    def close(self):
+        if self.h:
+            tgp.net_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ---------------------------------------------------------------- shapes
+
+    def part_in_shape(self, j: int):
+        """(C, H, W) of partition j's input (pre-prologue)."""
+        lo, _ = self.bounds[j - 1]
+        if lo == 0:
+            return (self.net.in_channels, self.net.height, self.net.width)
+        h, w = self.shapes[lo - 1]
+        return (self.net.layers[lo - 1].cout, h, w)
+
+    def part_out_shape(self, j: int):
+        _, hi = self.bounds[j - 1]
+        h, w = self.shapes[hi - 1]
+        return (self.net.layers[hi - 1].cout, h, w)
+
+    def exported_stashes(self, j: int) -> List[int]:
+        lo, hi = self.bounds[j - 1]
+        made = [L.stash_id for L in self.net.layers[lo:hi] if L.stash_id >= 0]
+        popped = {L.pop_id for L in self.net.layers[lo:hi] if L.pop_id >= 0}
+        return sorted(s for s in made if s not in popped)
+
+    def stash_shape(self, sid: int):
+        idx = [k for k, L in enumerate(self.net.layers) if L.stash_id == sid][0]
+        h, w = self.shapes[idx]
+        return (self.net.layers[idx].cout, h, w)
+
+    def stash_view(self, i: int, sid: int, grad: bool) -> torch.Tensor:
+        c, h, w = self.stash_shape(sid)
+        return wrap(tgp.stash_ptr(self.h, i, sid, grad), (self.b, h, w, c), self.dtype,
+                    self.device)
+
+    def esz(self) -> int:
+        return 2 if self.dtype == BF16 else 4
+
+    # ---------------------------------------------------------------- runs
+
+    def checkpointed(self, i: int) -> bool:
+        return self.mode == specs.CKPT_ALWAYS or (self.mode == specs.CKPT_EXCEPT_LAST and i < self.m)
+
+    def stage_step(self, j: int, x: torch.Tensor, y: torch.Tensor, dy: torch.Tensor,
+                   dx: Optional[torch.Tensor], stream: int = 0):
+        """All m forwards of partition j, then backward + accumulate for
+        i = m..1 (one stage's work per mini-batch).  Tensors are full-batch
+        NHWC; micro-batch slices are pointer offsets."""
+        def sl(t, i):
+            return t.data_ptr() + (i - 1) * (t.numel() // self.m) * t.element_size()
+        for i in range(1, self.m + 1):
+            tgp.stage_forward(self.h, j, i, self.checkpointed(i), sl(x, i), sl(y, i), stream)
+        for i in range(self.m, 0, -1):
+            tgp.stage_backward_recompute(self.h, j, i, sl(dy, i),
+                                         None if dx is None else sl(dx, i), stream)
+            tgp.grad_accumulate(self.h, j, i, i == self.m, stream)
+
+    def pipeline_step(self, x: torch.Tensor, target: torch.Tensor, loss: torch.Tensor,
+                      y: Optional[torch.Tensor] = None, stream: int = 0):
+        tgp.pipeline_step(self.h, x.data_ptr(), target.data_ptr(), self.B, self.m, self.n,
+                          self.mode, loss.data_ptr(), None if y is None else y.data_ptr(),
+                          stream)
+
+    def grads64(self, layers: Optional[Sequence[int]] = None):
+        """{idx: (dW as float64 OIHW, db as float64 or None)}"""
+        out = {}
+        for idx in (layers if layers is not None else sorted(self.params)):
+            L = self.net.layers[idx]
+            p = self.params[idx]
+            dw = p["dw"].double().cpu()
+            if L.kind == DWCONV3X3:
+                dw = dw.reshape(L.cout, 1, 3, 3)
+            else:
+                dw = dw.permute(0, 3, 1, 2)
+            out[idx] = (dw.contiguous().numpy(),
+                        None if p["db"] is None else p["db"].double().cpu().numpy())
+        return out

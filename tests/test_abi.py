@@ -1,0 +1,193 @@
+"""Host-side tests of the C ABI (no GPU needed): exported symbols, the
+clock-cycle schedule against the oracle's Algorithm 1 enumeration, the FLOP
+partitioner against brute force, and argument / state validation, none of
+which enqueues device work."""
+import itertools
+import os
+import random
+import re
+
+import pytest
+
+import paper_2004_09910_amd as tgp
+from oracle import pipeline as opipe
+from paper_2004_09910_amd.harness import layer_tuple
+from workloads import specs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    hdr = open(os.path.join(ROOT, "include", "tgp.h")).read()
+    hdr = re.sub(r"/\*.*?\*/", "", hdr, flags=re.S)
+    names = set(re.findall(r"\b(tgp_[a-z_]+)\s*\(", hdr))
+    assert len(names) >= 16
+    for nm in sorted(names):
+        assert hasattr(tgp._lib, nm), nm
+
+
+@pytest.mark.parametrize("mode", [0, 1, 2])
+@pytest.mark.parametrize("m", range(1, 7))
+@pytest.mark.parametrize("n", range(1, 6))
+def test_schedule_trace_follows_clock_cycle(m, n, mode):
+    ops = tgp.schedule_trace(m, n, mode)
+    fwd = [(i, j) for op, i, j in ops if op == tgp.OP_FORWARD]
+    bwd = [(i, j) for op, i, j in ops if op == tgp.OP_BACKWARD]
+    assert fwd == [t for c in opipe.forward_clocks(m, n) for t in c]
+    assert bwd == [t for c in opipe.backward_clocks(m, n) for t in c]
+    # every forward precedes every backward; the loss of micro-batch i comes
+    # right after F_{i,n}
+    last_f = max(k for k, o in enumerate(ops) if o[0] == tgp.OP_FORWARD)
+    first_b = min(k for k, o in enumerate(ops) if o[0] in (tgp.OP_BACKWARD, tgp.OP_RECOMPUTE))
+    assert last_f < first_b
+    for k, (op, i, j) in enumerate(ops):
+        if op == tgp.OP_FORWARD and j == n:
+            assert ops[k + 1] == (tgp.OP_LOSS, i, 0)
+        if op == tgp.OP_RECOMPUTE:
+            assert ops[k + 1] == (tgp.OP_BACKWARD, i, j)
+            assert opipe.checkpointed(mode, i, m)
+        if op == tgp.OP_BACKWARD:
+            assert ops[k + 1] == (tgp.OP_ACCUMULATE, i, j)
+            assert (ops[k - 1] == (tgp.OP_RECOMPUTE, i, j)) == opipe.checkpointed(mode, i, m)
+    assert sum(op == tgp.OP_RECOMPUTE for op, _, _ in ops) == \
+        n * sum(opipe.checkpointed(mode, i, m) for i in range(1, m + 1))
+
+
+def test_schedule_trace_m4_n3_written_out():
+    ops = tgp.schedule_trace(4, 3, 1)   # except-last
+    want_f = [(1, 1), (2, 1), (1, 2), (3, 1), (2, 2), (1, 3), (4, 1), (3, 2), (2, 3), (4, 2),
+              (3, 3), (4, 3)]
+    assert [(i, j) for op, i, j in ops if op == tgp.OP_FORWARD] == want_f
+    assert [(i, j) for op, i, j in ops if op == tgp.OP_RECOMPUTE] == \
+        [(3, 3), (2, 3), (3, 2), (1, 3), (2, 2), (3, 1), (1, 2), (2, 1), (1, 1)]
+
+
+def _brute_balance(cost, n):
+    L = len(cost)
+    best = None
+    for cuts in itertools.combinations(range(1, L), n - 1):
+        edges = (0,) + cuts + (L,)
+        parts = [sum(cost[edges[k]:edges[k + 1]]) for k in range(n)]
+        key = (max(parts), sum(p * p for p in parts), cuts)
+        if best is None or key < best[0]:
+            best = (key, [edges[k + 1] - edges[k] for k in range(n)])
+    return best[1]
+
+
+def test_partitioner_matches_brute_force():
+    rnd = random.Random(5)
+    for _ in range(300):
+        L = rnd.randint(1, 10)
+        n = rnd.randint(1, min(L, 4))
+        cost = [rnd.choice([0, 1, 2, 3, 5, 8, 13, 10 ** 12]) for _ in range(L)]
+        assert tgp.balance_minmax(cost, n) == _brute_balance(cost, n), (cost, n)
+
+
+def _net(net, dtype=0):
+    return tgp.net_create([layer_tuple(L) for L in net.layers], net.in_channels, net.height,
+                          net.width, dtype)
+
+
+def test_unet_partition_and_flops():
+    net = specs.unet(5, 64, 64, 192)
+    h = _net(net)
+    try:
+        assert [tgp.layer_flops(h, k) for k in range(len(net.layers))] == net.flops_per_sample()
+        tgp.set_partition(h, 4)
+        assert tgp.get_partition(h) == [7, 5, 3, 4]
+        tgp.set_partition(h, 2, [10, 9])
+        assert tgp.get_partition(h) == [10, 9]
+        with pytest.raises(tgp.TgpError):
+            tgp.set_partition(h, 2, [10, 10])
+        with pytest.raises(tgp.TgpError):
+            tgp.set_partition(h, 20)
+    finally:
+        tgp.net_destroy(h)
+    h = _net(specs.unet(6, 128, 128, 256))
+    tgp.set_partition(h, 8)
+    assert tgp.get_partition(h) == [4, 4, 4, 2, 2, 2, 2, 3]
+    tgp.net_destroy(h)
+
+
+def _status(layers, in_c=8, H=8, W=8, dtype=0):
+    return tgp.call_status("tgp_net_create", (tgp.Layer * len(layers))(*[tgp.Layer(*l) for l in layers]),
+                           len(layers), in_c, H, W, dtype, tgp.ctypes.byref(tgp.ctypes.c_void_p()))
+
+
+def test_net_create_validation():
+    C3, C1, DW = 0, 1, 2
+    ok = [(C3, 8, 8, 1, 1, 0, 0, -1), (C3, 8, 16, 1, 1, 1, -1, -1), (C3, 24, 8, 1, 1, 2, -1, 0)]
+    assert _status(ok) == tgp.OK
+    assert _status([(C3, 4, 8, 1, 1, 0, -1, -1)]) == tgp.EINVAL          # cin mismatch
+    assert _status([(C3, 8, 8, 1, 1, 2, -1, 3)]) == tgp.EINVAL           # pop of missing skip
+    assert _status([(C3, 8, 8, 1, 1, 1, -1, -1)], H=7) == tgp.EINVAL     # odd pool
+    assert _status([(DW, 8, 16, 0, 0, 0, -1, -1)]) == tgp.EINVAL         # depthwise cin != cout
+    assert _status([(C3, 8, 8, 1, 1, 0, 0, -1), (C3, 8, 8, 1, 1, 0, 0, -1)]) == tgp.EINVAL
+    assert _status([(9, 8, 8, 1, 1, 0, -1, -1)]) == tgp.EINVAL           # bad kind
+    assert _status([(C3, 4, 4, 1, 1, 1, -1, -1)], in_c=4) == tgp.EUNSUPPORTED  # bf16 pool, 4 ch
+    assert _status([(C3, 4, 4, 1, 1, 1, -1, -1)], in_c=4, dtype=1) == tgp.OK
+    assert _status([]) == tgp.EINVAL
+
+
+FAKE = 1 << 20   # a non-null address; never dereferenced by these tests
+
+
+def _bound_net(mode=0, B=4, m=2, n=2):
+    net = specs.plain_stack(4, 8, 8, 8)
+    h = _net(net, dtype=1)
+    tgp.set_partition(h, n)
+    for k in range(4):
+        tgp.bind_params(h, k, FAKE, FAKE, FAKE, FAKE)
+    nbytes = tgp.plan(h, B, m, mode)
+    return h, nbytes
+
+
+def test_plan_and_workspace_validation():
+    h, nbytes = _bound_net()
+    assert nbytes > 0
+    sz = tgp.ctypes.c_size_t()
+    assert tgp.call_status("tgp_plan", h, 5, 2, 0, tgp.ctypes.byref(sz)) == tgp.EINVAL
+    assert tgp.call_status("tgp_plan", h, 4, 2, 7, tgp.ctypes.byref(sz)) == tgp.EINVAL
+    assert tgp.call_status("tgp_plan", h, 4, 2, 0, tgp.ctypes.byref(sz)) == tgp.OK
+    assert tgp.call_status("tgp_bind_workspace", h, FAKE, sz.value - 1) == tgp.ENOSPACE
+    assert tgp.call_status("tgp_bind_workspace", h, FAKE + 16, sz.value) == tgp.EINVAL
+    assert tgp.call_status("tgp_bind_workspace", h, None, sz.value) == tgp.EINVAL
+    # no workspace bound yet
+    assert tgp.call_status("tgp_stage_forward", h, 1, 1, 1, FAKE, FAKE, None) == tgp.ESTATE
+    # checkpoint memory: never > except_last > always for m > 1
+    sizes = [_bound_net(mode)[1] for mode in (0, 1, 2)]
+    assert sizes[0] < sizes[1] < sizes[2]
+    tgp.net_destroy(h)
+
+
+def test_stage_state_machine_rejects_out_of_order_calls():
+    h, nbytes = _bound_net(mode=1, B=4, m=2, n=2)
+    tgp.bind_workspace(h, FAKE, nbytes)
+    st = lambda name, *a: tgp.call_status(name, h, *a)
+    # checkpoint flag must match the planned policy (except-last: i=1 yes, i=2 no)
+    assert st("tgp_stage_forward", 1, 1, 0, FAKE, FAKE, None) == tgp.EINVAL
+    assert st("tgp_stage_forward", 1, 2, 1, FAKE, FAKE, None) == tgp.EINVAL
+    assert st("tgp_stage_forward", 3, 1, 1, FAKE, FAKE, None) == tgp.EINVAL   # bad j
+    assert st("tgp_stage_forward", 1, 3, 1, FAKE, FAKE, None) == tgp.EINVAL   # bad i
+    assert st("tgp_stage_forward", 1, 1, 1, None, FAKE, None) == tgp.EINVAL   # NULL x
+    # backward before forward, accumulate before backward
+    assert st("tgp_stage_backward_recompute", 1, 2, FAKE, None, None) == tgp.ESTATE
+    assert st("tgp_grad_accumulate", 1, 2, 1, None) == tgp.ESTATE
+    assert st("tgp_grad_accumulate", 1, 1, 1, None) == tgp.EINVAL             # overwrite only at i=m
+    # pipeline step arguments must match the plan
+    assert st("tgp_pipeline_step", FAKE, FAKE, 8, 2, 2, 1, FAKE, None, None) == tgp.EINVAL
+    assert st("tgp_pipeline_step", FAKE, FAKE, 4, 2, 1, 1, FAKE, None, None) == tgp.EINVAL
+    assert st("tgp_pipeline_step", FAKE, FAKE, 4, 2, 2, 0, FAKE, None, None) == tgp.EINVAL
+    assert st("tgp_pipeline_step", None, FAKE, 4, 2, 2, 1, FAKE, None, None) == tgp.EINVAL
+    assert "match" in tgp.last_error() or "NULL" in tgp.last_error()
+    tgp.net_destroy(h)
+
+
+def test_unbound_layers_are_rejected():
+    net = specs.plain_stack(2, 8, 8, 8)
+    h = _net(net, dtype=1)
+    nbytes = tgp.plan(h, 2, 1, 0)
+    tgp.bind_workspace(h, FAKE, nbytes)
+    assert tgp.call_status("tgp_stage_forward", h, 1, 1, 1, FAKE, FAKE, None) == tgp.ESTATE
+    assert "bound" in tgp.last_error()
+    tgp.net_destroy(h)

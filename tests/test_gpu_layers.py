@@ -1,0 +1,96 @@
+"""Single-layer parity: each kernel family through the C ABI, as a one-layer
+stage with an injected upstream gradient.  Both sides start from identical
+bf16 inputs, so no ReLU or pool decision can differ and every output (y, dx,
+dW, db) is held to the benchmark spec's tolerance directly: 2e-2 max-rel for bf16,
+1e-4 for fp32.  Shapes include ragged pixel tiles and the benchmark's own
+level-0 and deepest layer shapes at its micro-batch size."""
+import pytest
+
+from gpu_util import (TOL, check_grad, gpu_stage, gpu_stage_with_popped, maxrel,
+                      oracle_stage_variants, report, say)
+from paper_2004_09910_amd.harness import nhwc_to_nchw64
+from workloads import specs
+from workloads.specs import (BF16, CONV1X1, CONV3X3, DWCONV3X3, FP32, PRO_MAXPOOL2,
+                             PRO_UPCAT2, Layer, Net)
+
+pytestmark = pytest.mark.gpu
+
+
+def one_layer(L, h, w, name="one"):
+    return Net(name, (L,), L.cin, h, w)
+
+
+def run_and_check(net, bal, j, dtype, B, m, what, popped=False):
+    say(what)
+    if popped:
+        got = gpu_stage_with_popped(net, bal, j, dtype=dtype, B=B, m=m)
+    else:
+        got = gpu_stage(net, dtype, B, m, 0, bal, j)
+    ref, alts = oracle_stage_variants(net, dtype, got["lo"], got["hi"], got["xv"], got["G"],
+                                 stash_in=got.get("stash_in"))
+    errs = {}
+    ok = check_grad("y", nhwc_to_nchw64(got["y"]), ref["y"], [a["y"] for a in alts], dtype, errs, strict=True)
+    ok &= check_grad("dx", nhwc_to_nchw64(got["dx"]), ref["dx"], [a["dx"] for a in alts], dtype, errs, strict=True)
+    for idx, (dW, db) in ref["grads"].items():
+        ok &= check_grad(f"dW{idx}", got["grads"][idx][0], dW, [a["grads"][idx][0] for a in alts], dtype, errs,
+                         strict=True)
+        if db is not None:
+            ok &= check_grad(f"db{idx}", got["grads"][idx][1], db, [a["grads"][idx][1] for a in alts], dtype,
+                             errs, strict=True)
+    report(what, errs)
+    assert ok, errs
+
+
+@pytest.mark.parametrize("cin,cout,h,w,B,m", [
+    (64, 64, 32, 32, 4, 2),      # 64-channel tile (BN = 64, BM = 256)
+    (64, 128, 20, 12, 6, 3),     # ragged pixel tile, 128-channel tile
+    (128, 256, 10, 10, 4, 4),    # b = 1
+    (512, 512, 6, 6, 2, 1),      # deep K, one partial tile
+])
+def test_conv3x3(cin, cout, h, w, B, m):
+    net = one_layer(Layer(CONV3X3, cin, cout), h, w)
+    run_and_check(net, (1,), 1, BF16, B, m, f"conv3x3 {cin}->{cout} @{h}x{w} B={B} m={m}")
+
+
+def test_conv1x1_and_depthwise():
+    net = one_layer(Layer(CONV1X1, 256, 256), 14, 14)
+    run_and_check(net, (1,), 1, BF16, 4, 2, "conv1x1 256->256 @14x14")
+    net = one_layer(Layer(DWCONV3X3, 256, 256, relu=False, bias=False), 14, 14)
+    run_and_check(net, (1,), 1, BF16, 4, 2, "dwconv3x3 256 @14x14")
+
+
+def test_head_without_relu():
+    net = one_layer(Layer(CONV1X1, 64, 1, relu=False), 16, 16)
+    run_and_check(net, (1,), 1, BF16, 4, 2, "head 1x1 64->1")
+
+
+def test_maxpool_prologue():
+    net = Net("pool", (Layer(CONV3X3, 64, 64), Layer(CONV3X3, 64, 128, prologue=PRO_MAXPOOL2)),
+              64, 24, 20)
+    run_and_check(net, (1, 1), 2, BF16, 4, 2, "maxpool prologue + conv 64->128")
+
+
+def test_upcat_prologue():
+    net = Net("upcat", (Layer(CONV3X3, 64, 64, stash_id=0),
+                        Layer(CONV3X3, 64, 128, prologue=PRO_MAXPOOL2),
+                        Layer(CONV3X3, 192, 64, prologue=PRO_UPCAT2, pop_id=0)), 64, 16, 24)
+    run_and_check(net, (1, 1, 1), 3, BF16, 4, 2, "upsample-concat prologue + conv 192->64",
+                  popped=True)
+
+
+def test_fp32_direct_conv():
+    net = one_layer(Layer(CONV3X3, 16, 16), 32, 32)
+    run_and_check(net, (1,), 1, FP32, 8, 4, "fp32 conv3x3 16->16")
+    net = Net("pool32", (Layer(CONV3X3, 16, 16, stash_id=0),
+                         Layer(CONV3X3, 16, 32, prologue=PRO_MAXPOOL2),
+                         Layer(CONV3X3, 48, 16, prologue=PRO_UPCAT2, pop_id=0)), 16, 8, 8)
+    run_and_check(net, (1, 1, 1), 3, FP32, 4, 2, "fp32 upcat", popped=True)
+    run_and_check(net, (1, 2), 2, FP32, 4, 2, "fp32 pool + upcat", popped=True)
+
+
+@pytest.mark.parametrize("cin,cout,h", [(64, 64, 192), (256, 512, 24)])
+def test_benchmark_layer_shapes(cin, cout, h):
+    """The stage's level-0 layer (147456 x 64 x 576 per micro-batch) and its
+    deepest layer (2304 x 512 x 2304) at the benchmark's micro-batch size 4."""
+    net = one_layer(Layer(CONV3X3, cin, cout), h, h)
+    run_and_check(net, (1,), 1, BF16, 4, 1, f"bench layer {cin}->{cout} @{h}x{h} b=4")
