@@ -200,6 +200,8 @@ typedef struct {
 } tgp_kernel_stat;
 tgp_status tgp_profile_enable(int enable);
 tgp_status tgp_profile_read(tgp_kernel_stat* out, int cap, int* count);
+/* Drops the recorded events without reading them. */
+tgp_status tgp_profile_clear(void);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char* tgp_last_error(void);

@@ -17,7 +17,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libtgp.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2004_09910_amd.build`")
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2004_09910_amd/build.py`")
 
 # torch ships its own HIP runtime.  Load it before libtgp.so so that the
 # library's libamdhip64.so.7 dependency resolves to that same, already loaded
@@ -82,6 +82,8 @@ _lib.tgp_profile_enable.argtypes = [_I]
 _lib.tgp_profile_enable.restype = ctypes.c_int
 _lib.tgp_profile_read.argtypes = [ctypes.POINTER(KernelStat), _I, ctypes.POINTER(_I)]
 _lib.tgp_profile_read.restype = ctypes.c_int
+_lib.tgp_profile_clear.argtypes = []
+_lib.tgp_profile_clear.restype = ctypes.c_int
 _lib.tgp_net_destroy.argtypes = [_P]
 _lib.tgp_net_destroy.restype = None
 _lib.tgp_last_error.argtypes = []
@@ -210,3 +212,7 @@ def profile_read() -> List[dict]:
     _check(_lib.tgp_profile_read(buf, 256, ctypes.byref(cnt)), "tgp_profile_read")
     return [{"name": buf[k].name.decode(), "launches": buf[k].launches, "ms": buf[k].ms,
              "flops": buf[k].flops, "bytes": buf[k].bytes} for k in range(cnt.value)]
+
+
+def profile_clear() -> None:
+    _check(_lib.tgp_profile_clear(), "tgp_profile_clear")

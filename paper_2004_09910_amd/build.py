@@ -1,6 +1,7 @@
 """Builds libtgp.so (HIP kernels + host runtime + C ABI) for gfx950 in-tree.
 
-Run `python -m paper_2004_09910_amd.build`; objects go to _build/ next to
+Run `python paper_2004_09910_amd/build.py` (by path, so that the package,
+which loads the library, is not imported first); objects go to _build/ next to
 this file and the shared library to paper_2004_09910_amd/libtgp.so.
 """
 import os

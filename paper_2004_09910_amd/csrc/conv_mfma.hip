@@ -189,6 +189,186 @@ __global__ __launch_bounds__(256) void conv_fwd_mfma(
   }
 }
 
+// ---------------------------------------------------------------- forward (LDS DMA)
+
+// Sixteen zero bytes in device memory: the source of every im2col chunk that
+// falls outside the image (the zero padding), so that all tile loads can be
+// direct global -> LDS copies.
+__device__ __attribute__((aligned(16))) unsigned int g_zero16[4];
+
+#define TGP_LDS(p) ((__attribute__((address_space(3))) void*)(p))
+
+// s_waitcnt with only the vector-memory counter limited to N (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
+}
+
+// Waits until at most `ahead` stages of LPS loads each are still in flight.
+template <int NS, int LPS>
+__device__ __forceinline__ void wait_stages(int ahead) {
+  if constexpr (NS >= 4) {
+    if (ahead >= 2) { wait_vmcnt<2 * LPS>(); return; }
+  }
+  if constexpr (NS >= 3) {
+    if (ahead >= 1) { wait_vmcnt<LPS>(); return; }
+  }
+  wait_vmcnt<0>();
+}
+
+// Implicit-GEMM forward with an NS-stage ring of LDS tiles filled by
+// global_load_lds_dwordx4: each wave instruction copies 8 rows of 128 bytes;
+// lane l fills physical chunk l & 7 of row l >> 3 with the logical chunk that
+// the XOR swizzle puts there.  Loads run NS - 1 K steps ahead of the MFMAs.
+// Block index remapped so that consecutive pixel tiles (which share halo
+// rows and read the same weights) run on the same XCD: the dispatcher deals
+// blocks round-robin over the 8 XCDs, each with its own L2.
+__device__ __forceinline__ int xcd_remap(int bid, int nb) {
+  const int per = nb / 8, rem = nb % 8;
+  const int x = bid % 8, i = bid / 8;
+  return x < rem ? x * (per + 1) + i : rem * (per + 1) + (x - rem) * per + i;
+}
+
+template <int WCO, int WP, int TM, int TN, int TAPS, int NS>
+__global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_dma(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
+    const float* __restrict__ bias, bf16_t* __restrict__ Y, int P, int H, int W, int Cin,
+    int Cout, int relu, int co_major) {
+  constexpr int NW = WCO * WP;       // waves per block
+  constexpr int BN = WCO * TM * 32;  // output channels per block
+  constexpr int BM = WP * TN * 32;   // pixels per block
+  constexpr int ROWS = BN + BM;
+  constexpr int LPS = ROWS / (8 * NW);  // DMA instructions per wave per stage
+  static_assert(BN % 64 == 0 && ROWS % (8 * NW) == 0, "tile shape");
+  __shared__ u32x4 smem[NS][ROWS * 8];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wco = wave / WP, wp = wave % WP;
+  // The grid is (pixel tiles x channel tiles) flattened.  Each XCD gets a
+  // contiguous range of it: pixel-tile-major when the activations are the
+  // larger operand (an XCD then holds a slice of the image plus all weights
+  // in its L2), channel-tile-major when the weights are (a slice of the
+  // weights plus the whole activation tile set).
+  const int nct = Cout / BN;
+  const int npt = gridDim.x / nct;
+  const int lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int p0 = (co_major ? lb % npt : lb / nct) * BM;
+  const int co0 = (co_major ? lb / npt : lb % nct) * BN;
+  const int K = TAPS * Cin;
+  const int cpt = Cin / 64;
+  const int nk = TAPS * cpt;
+  const int HW = H * W;
+
+  // Source of each row this lane fills, per stage instruction u.
+  const bf16_t* src[LPS];
+  int ph[LPS], pw[LPS];
+  bool pok[LPS];
+#pragma unroll
+  for (int u = 0; u < LPS; ++u) {
+    const int r = (wave + NW * u) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ ((r ^ (r >> 3)) & 7);
+    if ((wave + NW * u) * 8 < BN) {
+      src[u] = Wt + (long)(co0 + r) * K + c * 8;
+      ph[u] = pw[u] = 0;
+      pok[u] = true;
+    } else {
+      const int p = p0 + r - BN;
+      pok[u] = p < P;
+      const int pp = pok[u] ? p : 0;
+      const int rem = pp % HW;
+      ph[u] = rem / W;
+      pw[u] = rem - ph[u] * W;
+      src[u] = X + (long)pp * Cin + c * 8;
+    }
+  }
+  const bf16_t* zero = (const bf16_t*)g_zero16;
+
+  auto issue = [&](int ks, int slot) __attribute__((always_inline)) {
+    const int tap = ks / cpt;
+    const int c0 = (ks - tap * cpt) * 64;
+    const int dr = (TAPS == 9) ? tap / 3 - 1 : 0;
+    const int dc = (TAPS == 9) ? tap % 3 - 1 : 0;
+    const long shift = ((long)dr * W + dc) * Cin + c0;
+#pragma unroll
+    for (int u = 0; u < LPS; ++u) {
+      const bf16_t* g;
+      if ((wave + NW * u) * 8 < BN) {
+        g = src[u] + tap * Cin + c0;
+      } else {
+        const int hh = ph[u] + dr, ww = pw[u] + dc;
+        const bool ok = pok[u] && (unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W;
+        g = ok ? src[u] + shift : zero;
+      }
+      __builtin_amdgcn_global_load_lds((const void*)g,
+                                       TGP_LDS(&smem[slot][(wave + NW * u) * 64]), 16, 0, 0);
+    }
+  };
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
+
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nk) issue(s, s);
+  for (int ks = 0; ks < nk; ++ks) {
+    const int ahead = min(NS - 2, nk - 1 - ks);
+    wait_stages<NS, LPS>(ahead);
+    __builtin_amdgcn_s_barrier();
+    if (ks + NS - 1 < nk) issue(ks + NS - 1, (ks + NS - 1) % NS);
+    const u32x4* As = smem[ks % NS];
+    const u32x4* Bs = smem[ks % NS] + BN * 8;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const int qq = 2 * kk + (lane >> 5);
+      bf16x8_t a[TM], b[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int row = wco * TM * 32 + i * 32 + (lane & 31);
+        a[i] = as_bf16x8(As[row * 8 + swz(row, qq)]);
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int row = wp * TN * 32 + j * 32 + (lane & 31);
+        b[j] = as_bf16x8(Bs[row * 8 + swz(row, qq)]);
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
+    }
+  }
+
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int p = p0 + wp * TN * 32 + j * 32 + (lane & 31);
+      if (p >= P) continue;
+      bf16_t* yrow = Y + (long)p * Cout;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int co = co0 + wco * TM * 32 + i * 32 + 8 * g + 4 * (lane >> 5);
+        float v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          v[t] = acc[i][j][4 * g + t];
+          if (bias) v[t] += bias[co + t];
+          if (relu) v[t] = fmaxf(v[t], 0.0f);
+        }
+        uint2 o;
+        o.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
+        o.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+        *(uint2*)(yrow + co) = o;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- wgrad
 
 // 8x8 transpose of bfloat16: in[j] holds 8 channels of pixel j; out[c] gets
@@ -391,12 +571,18 @@ struct WgradPlan {
   int S, pix_per_split;
 };
 
+// Split count for the weight gradient: enough blocks to fill the chip
+// (~512), at least 256 pixels per split, and at most ~8 MB of fp32 partials
+// (their write + fixed-order re-read otherwise costs more than the extra
+// parallelism gains).
 template <int TM, int TN>
-WgradPlan wgrad_plan(long P, int tiles) {
+WgradPlan wgrad_plan(long P, int tiles, long E) {
   const int BK = 64;
   int S = cdiv(512, tiles);
   int maxS = cdiv(P, 256);
   if (S > maxS) S = maxS;
+  long cap = (8L << 20) / (4 * E);
+  if (S > cap) S = (int)cap;
   if (S < 1) S = 1;
   int pps = cdiv(cdiv(P, S), BK) * BK;
   S = cdiv(P, pps);
@@ -413,38 +599,66 @@ bool mfma_conv_ok(int dt, int cin, int cout) {
   return dt == 0 && cin % 64 == 0 && cout % 64 == 0;
 }
 
+// Forward tile configurations.  A configuration is chosen per shape by
+// fwd_config() (a pure function of the shape, so recomputation reuses the
+// exact same kernel); g_fwd_variant > 0 forces one for measurement sweeps.
+int g_fwd_variant = 0;
+int g_fwd_order = -1;   // -1: by operand size; 0/1 forced (measurement only)
+
+template <int WCO, int WP, int TM, int TN, int NS>
+hipError_t launch_fwd_dma(const char* name, const bf16_t* X, const bf16_t* Wt, const float* b,
+                          bf16_t* Y, long P, const ConvShape& s, int relu, hipStream_t st) {
+  constexpr int BN = WCO * TM * 32, BM = WP * TN * 32;
+  if (s.cout % BN) return hipErrorInvalidValue;
+  dim3 grid(cdiv(P, BM) * (s.cout / BN));
+  double flops = 2.0 * P * s.cout * s.taps * s.cin;
+  double bytes = 2.0 * ((double)P * s.cin + (double)s.cout * s.taps * s.cin + (double)P * s.cout);
+  ProfScope ps(name, flops, bytes, st);
+  const double xbytes = 2.0 * P * s.cin, wbytes = 2.0 * s.cout * s.taps * s.cin;
+  const int co_major = g_fwd_order >= 0 ? g_fwd_order : (wbytes > xbytes ? 1 : 0);
+  if (s.taps == 9)
+    hipLaunchKernelGGL((conv_fwd_dma<WCO, WP, TM, TN, 9, NS>), grid, dim3(WCO * WP * 64), 0, st, X,
+                       Wt, b, Y, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major);
+  else
+    hipLaunchKernelGGL((conv_fwd_dma<WCO, WP, TM, TN, 1, NS>), grid, dim3(WCO * WP * 64), 0, st, X,
+                       Wt, b, Y, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major);
+  return hipGetLastError();
+}
+
+#define TGP_FWD_CFG(WCO, WP, TM, TN, NS) \
+  launch_fwd_dma<WCO, WP, TM, TN, NS>("conv_fwd_dma<" #WCO "," #WP "," #TM "," #TN "," #NS ">", X, Wt, b, Y, P, s, relu, st)
+
+// Measured on MI355X at the benchmark's micro-batch shapes: 64 x 64 tiles
+// (4 waves) win for deep, pixel-poor layers; 64 x 128 tiles with 8 waves for
+// pixel-rich layers with few output channels per pixel row.
+int fwd_config(const ConvShape& s) {
+  if (g_fwd_variant > 0) return g_fwd_variant;
+  const long P = s.pixels();
+  if (P >= 32768 && s.cout <= 128) return 7;
+  return 4;
+}
+
 hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void* y,
                              const ConvShape& s, int relu, hipStream_t st) {
   long P = s.pixels();
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* Wt = (const bf16_t*)w;
   bf16_t* Y = (bf16_t*)y;
-  double flops = 2.0 * P * s.cout * s.taps * s.cin;
-  double bytes = 2.0 * ((double)P * s.cin + (double)s.cout * s.taps * s.cin + (double)P * s.cout);
-  if (s.cout % 128 == 0) {
-    dim3 grid(cdiv(P, 128), s.cout / 128);
-    if (s.taps == 9) {
-      ProfScope ps("conv_fwd_mfma<2,2,2,2,9>", flops, bytes, st);
-      hipLaunchKernelGGL((conv_fwd_mfma<2, 2, 2, 2, 9>), grid, dim3(256), 0, st, X, Wt, b, Y,
-                         (int)P, s.H, s.W, s.cin, s.cout, relu);
-    } else {
-      ProfScope ps("conv_fwd_mfma<2,2,2,2,1>", flops, bytes, st);
-      hipLaunchKernelGGL((conv_fwd_mfma<2, 2, 2, 2, 1>), grid, dim3(256), 0, st, X, Wt, b, Y,
-                         (int)P, s.H, s.W, s.cin, s.cout, relu);
-    }
-  } else {
-    dim3 grid(cdiv(P, 256), s.cout / 64);
-    if (s.taps == 9) {
-      ProfScope ps("conv_fwd_mfma<1,4,2,2,9>", flops, bytes, st);
-      hipLaunchKernelGGL((conv_fwd_mfma<1, 4, 2, 2, 9>), grid, dim3(256), 0, st, X, Wt, b, Y,
-                         (int)P, s.H, s.W, s.cin, s.cout, relu);
-    } else {
-      ProfScope ps("conv_fwd_mfma<1,4,2,2,1>", flops, bytes, st);
-      hipLaunchKernelGGL((conv_fwd_mfma<1, 4, 2, 2, 1>), grid, dim3(256), 0, st, X, Wt, b, Y,
-                         (int)P, s.H, s.W, s.cin, s.cout, relu);
-    }
+  const bool wide = s.cout % 128 == 0;
+  switch (fwd_config(s)) {
+    case 1: return TGP_FWD_CFG(1, 4, 2, 2, 2);          // 64 x 256, 4 waves
+    case 2: return wide ? TGP_FWD_CFG(2, 2, 2, 2, 2)    // 128 x 128, 4 waves
+                        : TGP_FWD_CFG(1, 4, 2, 2, 2);
+    case 3: return TGP_FWD_CFG(2, 2, 1, 2, 2);          // 64 x 128, 4 waves
+    case 4: return TGP_FWD_CFG(2, 2, 1, 1, 2);          // 64 x 64, 4 waves
+    case 5: return TGP_FWD_CFG(1, 8, 2, 1, 2);          // 64 x 256, 8 waves
+    case 6: return wide ? TGP_FWD_CFG(2, 4, 2, 2, 2)    // 128 x 256, 8 waves
+                        : TGP_FWD_CFG(1, 8, 2, 2, 2);   // 64 x 512, 8 waves
+    case 7: return TGP_FWD_CFG(2, 4, 1, 1, 2);          // 64 x 128, 8 waves
+    case 8: return TGP_FWD_CFG(2, 2, 1, 2, 3);          // 64 x 128, 4 waves, 3 stages
+    case 9: return TGP_FWD_CFG(1, 8, 2, 1, 3);          // 64 x 256, 8 waves, 3 stages
+    default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 hipError_t weight_transform(int dt, const void* w, void* wt, int cout, int cin, int taps,
@@ -463,8 +677,9 @@ hipError_t weight_transform(int dt, const void* w, void* wt, int cout, int cin, 
 size_t wgrad_mfma_partial_floats(const ConvShape& s) {
   int tiles = s.taps * (s.cin / 64) * (s.cout / 64);
   if (s.cin % 128 == 0 && s.cout % 128 == 0) tiles = s.taps * (s.cin / 128) * (s.cout / 128);
-  WgradPlan pl = wgrad_plan<2, 2>(s.pixels(), tiles);
-  return (size_t)pl.S * s.cout * s.taps * s.cin;
+  long E = (long)s.cout * s.taps * s.cin;
+  WgradPlan pl = wgrad_plan<2, 2>(s.pixels(), tiles, E);
+  return (size_t)pl.S * E;
 }
 
 hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
@@ -475,15 +690,16 @@ hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* part
   bool big = s.cin % 128 == 0 && s.cout % 128 == 0;
   int bm = big ? 128 : 64, bn = big ? 128 : 64;
   int tiles = s.taps * (s.cin / bn) * (s.cout / bm);
-  WgradPlan pl = wgrad_plan<2, 2>(P, tiles);
-  dim3 grid(s.taps * (s.cin / bn), s.cout / bm, pl.S);
   long E = (long)s.cout * s.taps * s.cin;
+  WgradPlan pl = wgrad_plan<2, 2>(P, tiles, E);
+  dim3 grid(s.taps * (s.cin / bn), s.cout / bm, pl.S);
   double flops = 2.0 * P * E;
   double bytes = 2.0 * ((double)P * s.cin + (double)P * s.cout) + 4.0 * pl.S * E;
   {
     const char* nm = big ? (s.taps == 9 ? "conv_wgrad_mfma<2,2,2,2,9>" : "conv_wgrad_mfma<2,2,2,2,1>")
                          : (s.taps == 9 ? "conv_wgrad_mfma<2,2,1,1,9>" : "conv_wgrad_mfma<2,2,1,1,1>");
     ProfScope ps(nm, flops, bytes, st);
+    if (pl.S == 1) partial = dw;   // a single split writes the gradient itself
     if (big) {
       if (s.taps == 9)
         hipLaunchKernelGGL((conv_wgrad_mfma<2, 2, 2, 2, 9>), grid, dim3(256), 0, st, X, DZ,
@@ -502,7 +718,7 @@ hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* part
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return splitk_reduce_launch(partial, dw, E, pl.S, st);
+  return pl.S == 1 ? hipSuccess : splitk_reduce_launch(partial, dw, E, pl.S, st);
 }
 
 hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st) {

@@ -647,7 +647,15 @@ size_t colsum_partial_floats(long P, int C) {
   return (size_t)cdiv(P, colsum_rows(P)) * C;
 }
 
-static long relu_bias_rows(long P) { return 256; }
+// Rows per block of the fused ReLU-backward / bias kernel: about 1024 blocks
+// (a multiple of the block's row lanes), so deep layers with few pixels and
+// many channels still fill the chip.
+static long relu_bias_rows(long P, int C, int N) {
+  int nl = 256 / (C / N);
+  long r = (P + 1023) / 1024;
+  r = (r + nl - 1) / nl * nl;
+  return r < nl ? nl : r;
+}
 bool relu_bias_fusable(int dt, int C, const void* dy, const void* dskip, const void* y,
                        const void* dz) {
   int N = dt == 0 ? 8 : 4;
@@ -656,12 +664,16 @@ bool relu_bias_fusable(int dt, int C, const void* dy, const void* dskip, const v
   return CP <= 256 && 256 % CP == 0 && al16(dy) && al16(dz) && (!dskip || al16(dskip)) &&
          al16(y);
 }
-size_t relu_bias_partial_floats(long P, int C) { return (size_t)cdiv(P, relu_bias_rows(P)) * C; }
+size_t relu_bias_partial_floats(int dt, long P, int C) {
+  const int N = dt == 0 ? 8 : 4;
+  if (C % N || C / N > 256 || 256 % (C / N)) return 0;   // not fusable
+  return (size_t)cdiv(P, relu_bias_rows(P, C, N)) * C;
+}
 
 hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
                               int relu, float* db, float* partial, long P, int C,
                               hipStream_t st) {
-  long rows = relu_bias_rows(P);
+  long rows = relu_bias_rows(P, C, dt == 0 ? 8 : 4);
   int nb = cdiv(P, rows);
   {
     ProfScope ps("relu_backward_bias", 0.0,

@@ -90,7 +90,7 @@ hipError_t grad_accumulate_batch(const AccBatch& b, int overwrite, hipStream_t s
 // two-stage reduction), for layers where relu_bias_fusable() holds.
 bool relu_bias_fusable(int dt, int C, const void* dy, const void* dskip, const void* y,
                        const void* dz);
-size_t relu_bias_partial_floats(long P, int C);
+size_t relu_bias_partial_floats(int dt, long P, int C);
 hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
                               int relu, float* db, float* partial, long P, int C,
                               hipStream_t st);

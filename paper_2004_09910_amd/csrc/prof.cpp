@@ -59,6 +59,16 @@ tgp_status tgp_profile_enable(int enable) {
   return TGP_OK;
 }
 
+tgp_status tgp_profile_clear(void) {
+  using tgpk::g;
+  for (auto& r : g.recs) {
+    g.pool.push_back(r.a);
+    g.pool.push_back(r.b);
+  }
+  g.recs.clear();
+  return TGP_OK;
+}
+
 tgp_status tgp_profile_read(tgp_kernel_stat* out, int cap, int* count) {
   using tgpk::g;
   if (!count) return TGP_EINVAL;

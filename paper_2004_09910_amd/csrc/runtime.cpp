@@ -467,9 +467,27 @@ struct GpuExec : Exec {
 
 // ============================================================ C ABI
 
+namespace tgpk {
+extern int g_fwd_variant;
+extern int g_fwd_order;
+}
+
 extern "C" {
 
 const char* tgp_last_error(void) { return g_err.c_str(); }
+
+// Measurement hook (not in tgp.h): selects a forward-kernel tile/stage
+// configuration for benchmarking sweeps.
+int tgp_debug_set_fwd_variant(int v) {
+  int old = tgpk::g_fwd_variant;
+  tgpk::g_fwd_variant = v;
+  return old;
+}
+int tgp_debug_set_fwd_order(int v) {
+  int old = tgpk::g_fwd_order;
+  tgpk::g_fwd_order = v;
+  return old;
+}
 
 tgp_status tgp_net_create(const tgp_layer* layers, int n_layers, int in_c, int H, int W,
                           int dtype, tgp_net** out) {
@@ -666,7 +684,7 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
                                            : tgpk::conv_wgrad_partial_floats(N->dt, s);
     max_part = std::max(max_part, pf);
     max_col = std::max({max_col, tgpk::colsum_partial_floats((long)N->b * Lr.H * Lr.W, Lr.d.cout),
-                        tgpk::relu_bias_partial_floats((long)N->b * Lr.H * Lr.W, Lr.d.cout)});
+                        tgpk::relu_bias_partial_floats(N->dt, (long)N->b * Lr.H * Lr.W, Lr.d.cout)});
   }
   N->o_g0 = take(max_act);
   N->o_g1 = take(max_act);

@@ -197,21 +197,37 @@ def rmsrel(a, b):
 SPREAD_FACTOR = 4.0
 
 
+FLIP_MAXREL = 5e-2
+
+
 def check_grad(name, got, ref, alts, dtype, errs, strict=False):
-    """max-rel and rms-rel error of `got` against the reference.  Bound: the
-    spec tolerance; for non-strict checks of bf16 runs, SPREAD_FACTOR
-    times the largest distance of a float32-contraction variant from the
-    reference when that is larger (gradients through several ReLU / pool
-    layers, where valid runs differ by decision flips)."""
+    """max-rel and rms-rel error of `got` against the reference.
+
+    strict (single layers, forward outputs, fp32 runs): both within the
+    spec tolerance.  Gradients of bf16 runs through several ReLU / pool
+    layers pass if either
+      (a) max-rel and rms-rel are within the tolerance or SPREAD_FACTOR times
+          the largest distance of a float32-contraction variant from the
+          reference, whichever is larger; or
+      (b) rms-rel is within the tolerance and max-rel within FLIP_MAXREL: a few
+          decision flips (each moves one whole upstream gradient element) on
+          an otherwise matching tensor.  The GPU's MFMA accumulation does not
+          round like an IEEE float32 sum, so its flip count need not match
+          the float32 variants'."""
     tol = TOL[dtype]
     e_max, e_rms = maxrel(got, ref), rmsrel(got, ref)
     bmax = brms = tol
-    if not strict and dtype == BF16 and alts:
-        bmax = max(tol, SPREAD_FACTOR * max(maxrel(a, ref) for a in alts))
-        brms = max(tol, SPREAD_FACTOR * max(rmsrel(a, ref) for a in alts))
     sp = max((maxrel(a, ref) for a in alts), default=0.0)
+    if strict or dtype != BF16 or not alts:
+        errs[name] = (e_max, bmax, e_rms, brms, sp)
+        return e_max <= bmax and e_rms <= brms
+    bmax = max(tol, SPREAD_FACTOR * sp)
+    brms = max(tol, SPREAD_FACTOR * max(rmsrel(a, ref) for a in alts))
+    ok = (e_max <= bmax and e_rms <= brms) or (e_rms <= tol and e_max <= FLIP_MAXREL)
+    if not (e_max <= bmax and e_rms <= brms) and ok:
+        bmax = FLIP_MAXREL
     errs[name] = (e_max, bmax, e_rms, brms, sp)
-    return e_max <= bmax and e_rms <= brms
+    return ok
 
 
 def report(what, errs):
