@@ -322,24 +322,31 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_dma(
     if (ks + NS - 1 < nk) issue(ks + NS - 1, (ks + NS - 1) % NS);
     const u32x4* As = smem[ks % NS];
     const u32x4* Bs = smem[ks % NS] + BN * 8;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
+    // the fragments of K sub-step kk + 1 are read while the MFMAs of kk run
+    bf16x8_t a[2][TM], b[2][TN];
+    auto load = [&](int kk, int buf) __attribute__((always_inline)) {
       const int qq = 2 * kk + (lane >> 5);
-      bf16x8_t a[TM], b[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = wco * TM * 32 + i * 32 + (lane & 31);
-        a[i] = as_bf16x8(As[row * 8 + swz(row, qq)]);
+        a[buf][i] = as_bf16x8(As[row * 8 + swz(row, qq)]);
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int row = wp * TN * 32 + j * 32 + (lane & 31);
-        b[j] = as_bf16x8(Bs[row * 8 + swz(row, qq)]);
+        b[buf][j] = as_bf16x8(Bs[row * 8 + swz(row, qq)]);
       }
+    };
+    load(0, 0);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      if (kk + 1 < 4) load(kk + 1, (kk + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(a[kk & 1][i], b[kk & 1][j], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
@@ -367,6 +374,229 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_dma(
       }
     }
   }
+}
+
+// ---------------------------------------------------------------- forward, row-stage 3x3
+
+// 3x3 implicit GEMM whose K loop runs over stages (64-channel chunk c, filter
+// row r).  A stage holds, for a block of BM consecutive output pixels
+// [p0, p0 + BM), the BM + 2 input pixel rows q = p0 + (r-1) W - 1 + j
+// (j = 0 .. BM+1) and the weights of the three taps (r, 0..2); the three
+// column taps then read the pixel rows at offsets 0, 1, 2 from LDS, so each
+// input row is fetched once per filter row instead of once per tap.  A B
+// fragment whose source pixel (h + r - 1, w + s - 1) lies outside the image
+// is zeroed after the LDS read (that covers the left / right padding and the
+// rows that belong to the neighbouring sample).  K order (chunk, r, s,
+// channel) is fixed by the shape, so recomputation is bit-identical.
+//
+// SPLIT: the stages are divided over gridDim.x / tiles splits; each split
+// writes fp32 partials part[split][p][co] and conv_rows_epilogue sums them
+// in split order and applies bias, ReLU and the bf16 rounding.
+template <int WCO, int WP, int TM, int TN, int NS, bool SPLIT>
+__global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_rows(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
+    const float* __restrict__ bias, bf16_t* __restrict__ Y, float* __restrict__ part, int P,
+    int H, int W, int Cin, int Cout, int relu, int co_major, int tiles, int st_per_split) {
+  constexpr int NW = WCO * WP;
+  constexpr int BN = WCO * TM * 32;
+  constexpr int BM = WP * TN * 32;
+  constexpr int RA = 3 * BN;                               // weight rows per stage
+  constexpr int ROWS = (RA + BM + 2 + 8 * NW - 1) / (8 * NW) * (8 * NW);
+  constexpr int LPS = ROWS / (8 * NW);                     // DMA instructions per wave per stage
+  static_assert(BN % 64 == 0, "weight rows must keep the swizzle phase");
+  __shared__ u32x4 smem[NS][ROWS * 8];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wco = wave / WP, wp = wave % WP;
+  const int nct = Cout / BN;
+  const int npt = tiles / nct;
+  int lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = lb / tiles;
+  lb -= split * tiles;
+  const int p0 = (co_major ? lb % npt : lb / nct) * BM;
+  const int co0 = (co_major ? lb / npt : lb % nct) * BN;
+  const int nst = 3 * (Cin / 64);
+  const int s_begin = SPLIT ? split * st_per_split : 0;
+  const int s_end = SPLIT ? min(nst, s_begin + st_per_split) : nst;
+  const int HW = H * W;
+
+  // DMA sources: row rr of the stage (A: weight row of tap (r, rr / BN),
+  // B: input pixel row rr - RA); logical chunk from the swizzle.
+  const bf16_t* abase[LPS];
+  int brow[LPS];
+#pragma unroll
+  for (int u = 0; u < LPS; ++u) {
+    const int r = (wave + NW * u) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ ((r ^ (r >> 3)) & 7);
+    if ((wave + NW * u) * 8 < RA) {
+      const int t3 = r / BN, co = co0 + r % BN;
+      abase[u] = Wt + ((long)co * 9 + t3) * Cin + c * 8;   // + 3 * rfilt * Cin + c0
+      brow[u] = 0;
+    } else {
+      abase[u] = X + c * 8;
+      brow[u] = r - RA;                                   // j
+    }
+  }
+  const bf16_t* zero = (const bf16_t*)g_zero16;
+
+  // Validity of the B fragment of tile j for filter row rf, column tap t3.
+  unsigned vmask[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j) {
+    const int p = p0 + wp * TN * 32 + j * 32 + (lane & 31);
+    unsigned m = 0;
+    if (p < P) {
+      const int rem = p % HW, h = rem / W, w = rem - (rem / W) * W;
+#pragma unroll
+      for (int rf = 0; rf < 3; ++rf)
+#pragma unroll
+        for (int t3 = 0; t3 < 3; ++t3)
+          if ((unsigned)(h + rf - 1) < (unsigned)H && (unsigned)(w + t3 - 1) < (unsigned)W)
+            m |= 1u << (rf * 3 + t3);
+    }
+    vmask[j] = m;
+  }
+
+  auto issue = [&](int st, int slot) __attribute__((always_inline)) {
+    const int chunk = st / 3, rf = st - chunk * 3;
+    const int c0 = chunk * 64;
+    const long qbase = (long)p0 + (long)(rf - 1) * W - 1;
+#pragma unroll
+    for (int u = 0; u < LPS; ++u) {
+      const bf16_t* g;
+      if ((wave + NW * u) * 8 < RA) {
+        g = abase[u] + (long)rf * 3 * Cin + c0;
+      } else {
+        const long q = qbase + brow[u];
+        const bool ok = brow[u] < BM + 2 && q >= 0 && q < P;
+        g = ok ? abase[u] + q * Cin + c0 : zero;
+      }
+      __builtin_amdgcn_global_load_lds((const void*)g,
+                                       TGP_LDS(&smem[slot][(wave + NW * u) * 64]), 16, 0, 0);
+    }
+  };
+
+  f32x16_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
+
+  const int n = s_end - s_begin;
+#pragma unroll
+  for (int k = 0; k < NS - 1; ++k)
+    if (k < n) issue(s_begin + k, k);
+  for (int k = 0; k < n; ++k) {
+    const int ahead = min(NS - 2, n - 1 - k);
+    wait_stages<NS, LPS>(ahead);
+    __builtin_amdgcn_s_barrier();
+    if (k + NS - 1 < n) issue(s_begin + k + NS - 1, (k + NS - 1) % NS);
+    const int st = s_begin + k;
+    const int rf = st % 3;
+    const u32x4* As = smem[k % NS];
+    const u32x4* Bs = smem[k % NS] + RA * 8;
+    // 12 steps (3 column taps x 4 K sub-steps); the fragments of step t + 1
+    // are read from LDS while the MFMAs of step t run.
+    bf16x8_t fa[2][TM];
+    u32x4 fb[2][TN];
+    auto load = [&](int t, int buf) __attribute__((always_inline)) {
+      const int t3 = t >> 2, kk = t & 3;
+      const int qq = 2 * kk + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int row = t3 * BN + wco * TM * 32 + i * 32 + (lane & 31);
+        fa[buf][i] = as_bf16x8(As[row * 8 + swz(row, qq)]);
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int row = wp * TN * 32 + j * 32 + (lane & 31) + t3;
+        fb[buf][j] = Bs[row * 8 + swz(row, qq)];
+      }
+    };
+    load(0, 0);
+#pragma unroll
+    for (int t = 0; t < 12; ++t) {
+      const int cur = t & 1;
+      // the B rows of a column tap that falls outside the image are zeroed
+      // here, at use, so that the wait for the LDS read sits after the
+      // previous step's MFMAs
+      bf16x8_t bm[TN];
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const bool ok = (vmask[j] >> (rf * 3 + (t >> 2))) & 1u;
+        bm[j] = as_bf16x8(ok ? fb[cur][j] : u32x4{0, 0, 0, 0});
+      }
+      if (t + 1 < 12) load(t + 1, cur ^ 1);
+      // fence: the reads above are issued before the MFMAs below, which
+      // then cover their latency
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fa[cur][i], bm[j], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int p = p0 + wp * TN * 32 + j * 32 + (lane & 31);
+      if (p >= P) continue;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int co = co0 + wco * TM * 32 + i * 32 + 8 * g + 4 * (lane >> 5);
+        if constexpr (SPLIT) {
+          float4 o = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2],
+                                 acc[i][j][4 * g + 3]);
+          *(float4*)(part + ((long)split * P + p) * Cout + co) = o;
+        } else {
+          float v[4];
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            v[t] = acc[i][j][4 * g + t];
+            if (bias) v[t] += bias[co + t];
+            if (relu) v[t] = fmaxf(v[t], 0.0f);
+          }
+          uint2 o;
+          o.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
+          o.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+          *(uint2*)(Y + (long)p * Cout + co) = o;
+        }
+      }
+    }
+  }
+}
+
+// y[p][co] = bf16(act(sum_{s < S} part[s][p][co] + b[co])), s ascending.
+__global__ __launch_bounds__(256) void conv_rows_epilogue(const float* __restrict__ part,
+                                                          const float* __restrict__ bias,
+                                                          bf16_t* __restrict__ Y, long P,
+                                                          int Cout, int S, int relu) {
+  const long e = ((long)blockIdx.x * 256 + threadIdx.x) * 8;
+  const long n = P * Cout;
+  if (e >= n) return;
+  float v[8];
+  const float4 a0 = *(const float4*)(part + e), a1 = *(const float4*)(part + e + 4);
+  v[0] = a0.x; v[1] = a0.y; v[2] = a0.z; v[3] = a0.w;
+  v[4] = a1.x; v[5] = a1.y; v[6] = a1.z; v[7] = a1.w;
+  for (int s = 1; s < S; ++s) {
+    const float4 b0 = *(const float4*)(part + (long)s * n + e);
+    const float4 b1 = *(const float4*)(part + (long)s * n + e + 4);
+    v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+    v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+  }
+  const int co = e % Cout;
+  u32x4 o;
+#pragma unroll
+  for (int t = 0; t < 8; t += 2) {
+    float x0 = v[t], x1 = v[t + 1];
+    if (bias) { x0 += bias[co + t]; x1 += bias[co + t + 1]; }
+    if (relu) { x0 = fmaxf(x0, 0.f); x1 = fmaxf(x1, 0.f); }
+    o[t / 2] = f2bf(x0) | (f2bf(x1) << 16);
+  }
+  *(u32x4*)(Y + e) = o;
 }
 
 // ---------------------------------------------------------------- wgrad
@@ -471,24 +701,31 @@ __global__ __launch_bounds__(256) void conv_wgrad_mfma(
     if (ks + 1 < nk) gload(ks + 1);
     const u32x4* As = smem[buf];
     const u32x4* Bs = smem[buf] + BMc * 8;
-#pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
+    // the fragments of K sub-step kk + 1 are read while the MFMAs of kk run
+    bf16x8_t a[2][TM], b[2][TN];
+    auto load = [&](int kk, int fb) __attribute__((always_inline)) {
       const int qq = 2 * kk + (lane >> 5);
-      bf16x8_t a[TM], b[TN];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
-        int row = wm * TM * 32 + i * 32 + (lane & 31);
-        a[i] = as_bf16x8(As[row * 8 + swz(row, qq)]);
+        const int row = wm * TM * 32 + i * 32 + (lane & 31);
+        a[fb][i] = as_bf16x8(As[row * 8 + swz(row, qq)]);
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
-        int row = wn * TN * 32 + j * 32 + (lane & 31);
-        b[j] = as_bf16x8(Bs[row * 8 + swz(row, qq)]);
+        const int row = wn * TN * 32 + j * 32 + (lane & 31);
+        b[fb][j] = as_bf16x8(Bs[row * 8 + swz(row, qq)]);
       }
+    };
+    load(0, 0);
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      if (kk + 1 < BK / 16) load(kk + 1, (kk + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(a[i], b[j], acc[i][j]);
+        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(a[kk & 1][i], b[kk & 1][j], acc[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
     }
     if (ks + 1 < nk) lstore(buf ^ 1);
     __syncthreads();
@@ -628,36 +865,115 @@ hipError_t launch_fwd_dma(const char* name, const bf16_t* X, const bf16_t* Wt, c
 #define TGP_FWD_CFG(WCO, WP, TM, TN, NS) \
   launch_fwd_dma<WCO, WP, TM, TN, NS>("conv_fwd_dma<" #WCO "," #WP "," #TM "," #TN "," #NS ">", X, Wt, b, Y, P, s, relu, st)
 
-// Measured on MI355X at the benchmark's micro-batch shapes: 64 x 64 tiles
-// (4 waves) win for deep, pixel-poor layers; 64 x 128 tiles with 8 waves for
-// pixel-rich layers with few output channels per pixel row.
-int fwd_config(const ConvShape& s) {
-  if (g_fwd_variant > 0) return g_fwd_variant;
+// Row-stage forward launches.  S > 1 splits the stages over S blocks per
+// tile; the partials live in `part` (capacity part_cap floats; S is reduced
+// to fit, which only happens under measurement overrides).
+template <int WCO, int WP, int TM, int TN, int NS>
+hipError_t launch_fwd_rows(const char* name, const bf16_t* X, const bf16_t* Wt, const float* b,
+                           bf16_t* Y, float* part, size_t part_cap, long P, const ConvShape& s,
+                           int relu, int S, hipStream_t st) {
+  constexpr int BN = WCO * TM * 32, BM = WP * TN * 32;
+  if (s.cout % BN || s.cin % 64 || s.taps != 9) return hipErrorInvalidValue;
+  const int tiles = cdiv(P, BM) * (s.cout / BN);
+  const int nst = 3 * (s.cin / 64);
+  if (S > nst) S = nst;
+  while (S > 1 && (size_t)S * P * s.cout > part_cap) --S;
+  const int sps = cdiv(nst, S > 1 ? S : 1);
+  S = cdiv(nst, sps);
+  const double flops = 2.0 * P * s.cout * 9 * s.cin;
+  const double xbytes = 2.0 * P * s.cin, wbytes = 2.0 * s.cout * 9 * s.cin;
+  const int co_major = g_fwd_order >= 0 ? g_fwd_order : (wbytes > xbytes ? 1 : 0);
+  dim3 grid(tiles * S), block(WCO * WP * 64);
+  if (S == 1) {
+    ProfScope ps(name, flops, xbytes + wbytes + 2.0 * P * s.cout, st);
+    hipLaunchKernelGGL((conv_fwd_rows<WCO, WP, TM, TN, NS, false>), grid, block, 0, st, X, Wt, b,
+                       Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, tiles, sps);
+    return hipGetLastError();
+  }
+  {
+    ProfScope ps(name, flops, xbytes + wbytes + 4.0 * S * P * s.cout, st);
+    hipLaunchKernelGGL((conv_fwd_rows<WCO, WP, TM, TN, NS, true>), grid, block, 0, st, X, Wt, b,
+                       Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, tiles, sps);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  ProfScope ps2("conv_rows_epilogue", 0.0, 4.0 * S * P * s.cout + 2.0 * P * s.cout, st);
+  hipLaunchKernelGGL(conv_rows_epilogue, dim3(cdiv(P * s.cout, 2048)), dim3(256), 0, st, part, b,
+                     Y, P, s.cout, S, relu);
+  return hipGetLastError();
+}
+
+#define TGP_ROWS_CFG(WCO, WP, TM, TN, NS, S)                                               \
+  launch_fwd_rows<WCO, WP, TM, TN, NS>("conv_fwd_rows<" #WCO "," #WP "," #TM "," #TN "," #NS ">", \
+                                       X, Wt, b, Y, part, part_cap, P, s, relu, S, st)
+
+int g_fwd_split = 0;   // > 0 forces the split count (measurement only)
+
+struct FwdPlan {
+  int cfg;   // 1..: row-stage configurations; 100+: per-tap configurations
+  int S;
+};
+
+// Pure function of the shape (plus the measurement overrides).
+FwdPlan fwd_plan(const ConvShape& s) {
   const long P = s.pixels();
-  if (P >= 32768 && s.cout <= 128) return 7;
-  return 4;
+  FwdPlan pl{0, 1};
+  // Row-stage tiles pay off only on the deep, small-image layers (few pixel
+  // tiles, long K); elsewhere the per-tap kernel keeps more blocks per CU.
+  if (s.taps == 9 && s.cin % 64 == 0 && s.cin >= 256 && P <= 4096) {
+    pl.cfg = 3;    // 64 x 256, 8 waves
+  } else {
+    pl.cfg = 100;
+  }
+  if (g_fwd_variant > 0) pl.cfg = g_fwd_variant;
+  if ((pl.cfg == 2 || pl.cfg == 5) && s.cout % 128) pl.cfg = pl.cfg == 2 ? 1 : 3;  // 128-wide tiles need cout % 128 == 0
+  if (pl.cfg < 100) {
+    const int BN = (pl.cfg == 2 || pl.cfg == 5) ? 128 : 64;
+    const int BM = (pl.cfg == 2 || pl.cfg == 5 || pl.cfg == 6 || pl.cfg == 7) ? 128 : 256;
+    const long tiles = cdiv(P, BM) * (s.cout / BN);
+    const int nst = 3 * (s.cin / 64);
+    int S = tiles > 0 ? (int)cdiv(512, tiles) : 1;
+    if (S > nst / 3) S = nst / 3 > 0 ? nst / 3 : 1;   // at least one channel chunk per split
+    if (S < 1) S = 1;
+    pl.S = g_fwd_split > 0 ? g_fwd_split : S;
+  }
+  return pl;
+}
+
+size_t conv_forward_partial_floats(int dt, const ConvShape& s) {
+  if (!mfma_conv_ok(dt, s.cin, s.cout)) return 0;
+  FwdPlan pl = fwd_plan(s);
+  return pl.cfg < 100 && pl.S > 1 ? (size_t)pl.S * s.pixels() * s.cout : 0;
 }
 
 hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void* y,
-                             const ConvShape& s, int relu, hipStream_t st) {
+                             const ConvShape& s, int relu, float* part, size_t part_cap,
+                             hipStream_t st) {
   long P = s.pixels();
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* Wt = (const bf16_t*)w;
   bf16_t* Y = (bf16_t*)y;
+  const FwdPlan pl = fwd_plan(s);
   const bool wide = s.cout % 128 == 0;
-  switch (fwd_config(s)) {
-    case 1: return TGP_FWD_CFG(1, 4, 2, 2, 2);          // 64 x 256, 4 waves
-    case 2: return wide ? TGP_FWD_CFG(2, 2, 2, 2, 2)    // 128 x 128, 4 waves
-                        : TGP_FWD_CFG(1, 4, 2, 2, 2);
-    case 3: return TGP_FWD_CFG(2, 2, 1, 2, 2);          // 64 x 128, 4 waves
-    case 4: return TGP_FWD_CFG(2, 2, 1, 1, 2);          // 64 x 64, 4 waves
-    case 5: return TGP_FWD_CFG(1, 8, 2, 1, 2);          // 64 x 256, 8 waves
-    case 6: return wide ? TGP_FWD_CFG(2, 4, 2, 2, 2)    // 128 x 256, 8 waves
-                        : TGP_FWD_CFG(1, 8, 2, 2, 2);   // 64 x 512, 8 waves
-    case 7: return TGP_FWD_CFG(2, 4, 1, 1, 2);          // 64 x 128, 8 waves
-    case 8: return TGP_FWD_CFG(2, 2, 1, 2, 3);          // 64 x 128, 4 waves, 3 stages
-    case 9: return TGP_FWD_CFG(1, 8, 2, 1, 3);          // 64 x 256, 8 waves, 3 stages
-    default: return hipErrorInvalidValue;
+  switch (pl.cfg) {
+    case 1: return TGP_ROWS_CFG(1, 4, 2, 2, 2, pl.S);                 // 64 x 256, 4 waves
+    case 2: return wide ? TGP_ROWS_CFG(2, 2, 2, 2, 2, pl.S)           // 128 x 128, 4 waves
+                        : TGP_ROWS_CFG(1, 4, 2, 2, 2, pl.S);
+    case 3: return TGP_ROWS_CFG(1, 8, 2, 1, 2, pl.S);                 // 64 x 256, 8 waves
+    case 4: return TGP_ROWS_CFG(2, 4, 1, 2, 2, pl.S);                 // 64 x 256, 8 waves
+    case 5: return wide ? TGP_ROWS_CFG(2, 4, 2, 1, 2, pl.S)           // 128 x 128, 8 waves
+                        : TGP_ROWS_CFG(1, 8, 2, 1, 2, pl.S);
+    case 6: return TGP_ROWS_CFG(1, 4, 2, 1, 2, pl.S);                 // 64 x 128, 4 waves
+    case 7: return TGP_ROWS_CFG(1, 4, 2, 1, 3, pl.S);                 // 64 x 128, 4 waves, 3 stages
+    default: break;
+  }
+  // per-tap kernel (1x1 convolutions, and reference configurations)
+  const int v = pl.cfg >= 100 ? pl.cfg - 100 : 0;
+  switch (v) {
+    case 1: return TGP_FWD_CFG(2, 2, 1, 1, 2);          // 64 x 64, 4 waves
+    case 2: return TGP_FWD_CFG(2, 4, 1, 1, 2);          // 64 x 128, 8 waves
+    default: return P >= 32768 && s.cout <= 128 ? TGP_FWD_CFG(2, 4, 1, 1, 2)
+                                                 : TGP_FWD_CFG(2, 2, 1, 1, 2);
   }
 }
 

@@ -11,7 +11,8 @@ namespace tgpk {
 
 bool mfma_conv_ok(int dt, int cin, int cout);
 hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void* y,
-                             const ConvShape& s, int relu, hipStream_t st);
+                             const ConvShape& s, int relu, float* part, size_t part_cap,
+                             hipStream_t st);
 size_t wgrad_mfma_partial_floats(const ConvShape& s);
 hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
                            const ConvShape& s, hipStream_t st);
@@ -507,8 +508,10 @@ inline bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 // ---------------------------------------------------------------- dispatch
 
 hipError_t conv_forward(int dt, const void* x, const void* w, const float* b, void* y,
-                        const ConvShape& s, int relu, hipStream_t st) {
-  if (mfma_conv_ok(dt, s.cin, s.cout)) return conv_forward_mfma(x, w, b, y, s, relu, st);
+                        const ConvShape& s, int relu, float* part, size_t part_cap,
+                        hipStream_t st) {
+  if (mfma_conv_ok(dt, s.cin, s.cout))
+    return conv_forward_mfma(x, w, b, y, s, relu, part, part_cap, st);
   long P = s.pixels();
   dim3 g(cdiv(P * s.cout, 256));
   int esz = dt == 0 ? 2 : 4;
@@ -526,10 +529,10 @@ hipError_t conv_forward(int dt, const void* x, const void* w, const float* b, vo
 bool conv_dgrad_uses_wt(int dt, const ConvShape& s) { return mfma_conv_ok(dt, s.cout, s.cin); }
 
 hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, void* dx,
-                      const ConvShape& s, hipStream_t st) {
+                      const ConvShape& s, float* part, size_t part_cap, hipStream_t st) {
   if (conv_dgrad_uses_wt(dt, s)) {
     ConvShape t{s.nb, s.H, s.W, s.cout, s.cin, s.taps};
-    return conv_forward_mfma(dz, wt, nullptr, dx, t, 0, st);
+    return conv_forward_mfma(dz, wt, nullptr, dx, t, 0, part, part_cap, st);
   }
   long P = s.pixels();
   dim3 g(cdiv(P * s.cin, 256));

@@ -14,9 +14,13 @@ struct ConvShape {
   long pixels() const { return (long)nb * H * W; }
 };
 
-// y = act(conv(x, w) + b); w is KRSC [cout][taps][cin].
+// y = act(conv(x, w) + b); w is KRSC [cout][taps][cin].  Deep shapes split
+// the K loop; their fp32 partials go to `part` (conv_forward_partial_floats
+// floats; part_cap is the space available).
+size_t conv_forward_partial_floats(int dt, const ConvShape& s);
 hipError_t conv_forward(int dt, const void* x, const void* w, const float* b, void* y,
-                        const ConvShape& s, int relu, hipStream_t st);
+                        const ConvShape& s, int relu, float* part, size_t part_cap,
+                        hipStream_t st);
 // Whether the data-gradient kernel for this shape reads the transformed
 // weight wt = [cin][taps][cout] (taps rotated by 180 degrees).
 bool conv_dgrad_uses_wt(int dt, const ConvShape& s);
@@ -24,7 +28,7 @@ hipError_t weight_transform(int dt, const void* w, void* wt, int cout, int cin, 
                             hipStream_t st);
 // dx[p][ci] = sum_{co,tap} dz[p - off(tap)][co] w[co][tap][ci]
 hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, void* dx,
-                      const ConvShape& s, hipStream_t st);
+                      const ConvShape& s, float* part, size_t part_cap, hipStream_t st);
 // Weight gradient of one micro-batch into dw (float32, KRSC), via split-K
 // partials in `partial` (conv_wgrad_partial_floats floats) reduced in fixed
 // split order.

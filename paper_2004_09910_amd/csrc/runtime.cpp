@@ -72,7 +72,7 @@ struct tgp_net {
   std::map<int, size_t> o_stash, o_stash_grad;  // offsets for micro-batch 1
   size_t stash_stride = 0;                      // bytes per micro-batch of stash area
   size_t o_g0 = 0, o_g1 = 0, o_dinp = 0, o_dz = 0, o_part = 0, o_colpart = 0, o_msepart = 0,
-         o_loss = 0;
+         o_loss = 0, o_fpart = 0, fpart_floats = 0;
   std::vector<size_t> o_bnd, o_gbnd;  // per (i, j) pipeline boundaries, [i*n + j]
   size_t o_out = 0, o_dy = 0, out_bytes_mb = 0;
   // state per (i, j): index (i-1)*n + (j-1)
@@ -211,7 +211,7 @@ tgp_status run_forward(tgp_net* N, int j, int i, int phase, const void* x_in, vo
     } else {
       tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
       HIPCHK(tgpk::conv_forward(N->dt, cin_ptr, Lr.w, d.bias ? Lr.b : nullptr, out, s, d.relu,
-                                st),
+                                (float*)W_(N, N->o_fpart), N->fpart_floats, st),
              "conv_forward");
     }
     src = out;
@@ -305,7 +305,7 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
     } else {
       tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
       HIPCHK(tgpk::conv_dgrad(N->dt, dz, Lr.w, Lr.has_wt ? W_(N, Lr.o_wt) : nullptr, dgrad_out,
-                              s, st),
+                              s, (float*)W_(N, N->o_fpart), N->fpart_floats, st),
              "conv_dgrad");
     }
     if (d.prologue == TGP_PRO_MAXPOOL2) {
@@ -470,6 +470,7 @@ struct GpuExec : Exec {
 namespace tgpk {
 extern int g_fwd_variant;
 extern int g_fwd_order;
+extern int g_fwd_split;
 }
 
 extern "C" {
@@ -481,6 +482,11 @@ const char* tgp_last_error(void) { return g_err.c_str(); }
 int tgp_debug_set_fwd_variant(int v) {
   int old = tgpk::g_fwd_variant;
   tgpk::g_fwd_variant = v;
+  return old;
+}
+int tgp_debug_set_fwd_split(int v) {
+  int old = tgpk::g_fwd_split;
+  tgpk::g_fwd_split = v;
   return old;
 }
 int tgp_debug_set_fwd_order(int v) {
@@ -691,6 +697,16 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
   N->o_dz = take(max_act);
   N->o_dinp = take(std::max<size_t>(max_pro, 16));
   N->o_part = take(max_part * 4);
+  size_t max_fpart = 0;   // split-K partials of forward / data-gradient convolutions
+  for (auto& Lr : N->L) {
+    if (Lr.d.kind == TGP_DWCONV3X3) continue;
+    tgpk::ConvShape f{N->b, Lr.H, Lr.W, Lr.d.cin, Lr.d.cout, Lr.taps};
+    tgpk::ConvShape d{N->b, Lr.H, Lr.W, Lr.d.cout, Lr.d.cin, Lr.taps};
+    max_fpart = std::max({max_fpart, tgpk::conv_forward_partial_floats(N->dt, f),
+                          tgpk::conv_forward_partial_floats(N->dt, d)});
+  }
+  N->fpart_floats = max_fpart;
+  N->o_fpart = take(std::max<size_t>(max_fpart, 4) * 4);
   N->o_colpart = take(max_col * 4);
   const LayerRt& last = N->L.back();
   long out_mb = (long)N->b * last.H * last.W * last.d.cout;
