@@ -599,6 +599,254 @@ __global__ __launch_bounds__(256) void conv_rows_epilogue(const float* __restric
   *(u32x4*)(Y + e) = o;
 }
 
+// ---------------------------------------------------------------- forward, persistent row-stage 3x3
+
+// 16 bytes per lane from a buffer into LDS (lane l -> dst + 16 l).  A byte
+// offset voff at or past the buffer's size (negative ones included, read as
+// unsigned) yields zeros.  Kept out of line of the kernel templates: the
+// host pass drops a kernel template instantiation that calls this builtin
+// directly.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, __attribute__((address_space(3))) void* dst,
+                                      int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
+}
+
+// XOR swizzle of the four 16-byte chunks of a 64-byte LDS row: eight
+// consecutive rows read at one logical chunk land on eight distinct 16-byte
+// slots of a 128-byte bank cycle.
+__device__ __forceinline__ int swz4(int row, int q) { return q ^ ((row >> 1) & 3); }
+
+// Persistent 3x3 implicit GEMM.  The K loop of an output tile (BN channels x
+// BM consecutive pixels) runs over stages (32-channel chunk c, filter row r):
+// a stage holds the weights of taps (r, 0..2) for the tile's channels and the
+// BM + 2 input pixel rows q = p0 + (r - 1) W - 1 + j, so each input row is
+// fetched once per filter row and read by the three column taps at row
+// offsets 0, 1, 2.  A B fragment whose source pixel lies outside the image
+// (left / right padding, or a row of the neighbouring sample) is zeroed at
+// use.  Work items are (split, pixel tile, channel tile); block lb of G takes
+// items lb, lb + G, ... and streams all their stages through one NS-deep LDS
+// ring, so the next item's loads are in flight while the current item
+// finishes and writes its tile.  Each wave owns TM x TN MFMA tiles of 32 x 32.
+// The K order (chunk, r, s, channel) is fixed by the shape and the split
+// count, so a recomputation is bit-identical.
+//
+// SPLIT: item split s covers stages [s * nk, (s + 1) * nk) and writes fp32
+// partials part[s][p][co]; conv_rows_epilogue sums them in split order.
+template <int WCO, int WP, int TM, int TN, int NS, bool SPLIT>
+__global__ __launch_bounds__(WCO * WP * 64) void conv_rows_pers(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
+    const float* __restrict__ bias, bf16_t* __restrict__ Y, float* __restrict__ part, int P,
+    int H, int W, int Cin, int Cout, int relu, int co_major, int npt, int S) {
+  constexpr int NW = WCO * WP;
+  constexpr int BN = WCO * TM * 32;                        // output channels per tile
+  constexpr int BM = WP * TN * 32;                         // output pixels per tile
+  constexpr int RA = 3 * BN;                               // weight rows per stage
+  constexpr int RB = BM + 2;                               // input pixel rows per stage
+  constexpr int RPI = 16 * NW;                             // LDS rows per DMA round
+  constexpr int ROWS = (RA + RB + RPI - 1) / RPI * RPI;
+  constexpr int L = ROWS / RPI;                            // DMA instructions per wave per stage
+  constexpr int LA = RA / RPI;                             // ... of which weight rows
+  static_assert(RA % RPI == 0, "weight rows must fill whole DMA rounds");
+  __shared__ u32x4 smem[NS][ROWS * 4];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wco = wave / WP, wp = wave % WP;
+  const int wcu = __builtin_amdgcn_readfirstlane(wco);
+  const int nct = Cout / BN;
+  const int tiles = npt * nct;
+  const int G = gridDim.x;
+  const int lb = xcd_remap(blockIdx.x, G);
+  const int items = tiles * S;
+  const int n_items = lb < items ? (items - lb + G - 1) / G : 0;
+  const int nk = 3 * (Cin / 32) / S;                       // stages per item
+  const int total = n_items * nk;
+  const int HW = H * W;
+
+  // Buffer descriptors: a byte offset at or past the end (or negative, read
+  // as unsigned) returns zeros, which is the zero padding of pixels outside
+  // [0, P).  Sizes are below 2^31 (checked by the launcher).
+  const __amdgpu_buffer_rsrc_t rx =
+      __builtin_amdgcn_make_buffer_rsrc((void*)X, (short)0, P * Cin * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rw =
+      __builtin_amdgcn_make_buffer_rsrc((void*)Wt, (short)0, Cout * 9 * Cin * 2, 0x00020000);
+
+  // Per-lane byte offsets of the rows this lane fills (loop invariant).
+  // Weight row of instruction u < LA: channel co (within the tile), column
+  // tap t3; pixel row of instruction u >= LA: j (0 .. BM + 1, or padding).
+  int aoff[LA], boff[L - LA];
+#pragma unroll
+  for (int u = 0; u < L; ++u) {
+    const int row = (wave + NW * u) * 16 + (lane >> 2);
+    const int c = (lane & 3) ^ ((row >> 1) & 3);
+    if (u < LA) {
+      const int t3 = row / BN, co = row - t3 * BN;
+      aoff[u < LA ? u : 0] = ((co * 9 + t3) * Cin + c * 8) * 2;
+    } else {
+      boff[u < LA ? 0 : u - LA] = ((row - RA) * Cin + c * 8) * 2;
+    }
+  }
+
+  auto coords = [&](int it, int& split, int& p0, int& co0) __attribute__((always_inline)) {
+    const int item = lb + it * G;
+    split = item / tiles;
+    const int t = item - split * tiles;
+    p0 = (co_major ? t % npt : t / nct) * BM;
+    co0 = (co_major ? t / npt : t % nct) * BN;
+  };
+
+  // issue side: the item whose stage is loaded next
+  int i_it = 0, i_ks = 0, i_split = 0, i_p0 = 0, i_co0 = 0;
+  if (total > 0) coords(0, i_split, i_p0, i_co0);
+  auto issue = [&](int slot) __attribute__((always_inline)) {
+    const int stg = i_split * nk + i_ks;
+    const int chunk = stg / 3, rf = stg - 3 * chunk;
+    const int c0 = chunk * 32;
+    const int soff_a = ((i_co0 * 9 + 3 * rf) * Cin + c0) * 2;
+    const int base_b = ((i_p0 + (rf - 1) * W - 1) * Cin + c0) * 2;
+#pragma unroll
+    for (int u = 0; u < L; ++u) {
+      auto* dst = TGP_LDS(&smem[slot][(wave + NW * u) * 64]);
+      if (u < LA)
+        dma16(rw, dst, aoff[u < LA ? u : 0], soff_a);
+      else
+        dma16(rx, dst, base_b + boff[u < LA ? 0 : u - LA], 0);
+    }
+    if (++i_ks == nk) {
+      i_ks = 0;
+      if (++i_it < n_items) coords(i_it, i_split, i_p0, i_co0);
+    }
+  };
+
+#pragma unroll
+  for (int k = 0; k < NS - 1; ++k)
+    if (k < total) issue(k);
+
+  // compute side: one item at a time, its stages streamed through the ring
+  int idx = 0;
+  for (int c_it = 0; c_it < n_items; ++c_it) {
+    int c_split, c_p0, c_co0;
+    coords(c_it, c_split, c_p0, c_co0);
+    unsigned vmask[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+      const int p = c_p0 + wp * TN * 32 + j * 32 + (lane & 31);
+      unsigned m = 0;
+      if (p < P) {
+        const int rem = p % HW, h = rem / W, w = rem - (rem / W) * W;
+#pragma unroll
+        for (int rf = 0; rf < 3; ++rf)
+#pragma unroll
+          for (int t3 = 0; t3 < 3; ++t3)
+            if ((unsigned)(h + rf - 1) < (unsigned)H && (unsigned)(w + t3 - 1) < (unsigned)W)
+              m |= 1u << (rf * 3 + t3);
+      }
+      vmask[j] = m;
+    }
+
+    f32x16_t acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
+
+    for (int c_ks = 0; c_ks < nk; ++c_ks, ++idx) {
+      // Loads complete in order, so stage idx is in when at most the stages
+      // issued after it are pending (stores of a tile epilogue only make
+      // this wait longer).
+      wait_stages<NS, L>(min(NS - 2, total - 1 - idx));
+      __builtin_amdgcn_s_barrier();
+      if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);
+      const int rf = (c_split * nk + c_ks) % 3;
+      const u32x4* As = smem[idx % NS];
+      const u32x4* Bs = smem[idx % NS] + RA * 4;
+      // 6 steps (3 column taps x 2 K sub-steps of 16 channels).  Step t + 1's
+      // fragments are read while step t's MFMAs run, and its B fragments
+      // are masked between them.
+      bf16x8_t fa[2][TM], bm[2][TN];
+      u32x4 fb[TN];
+      auto load = [&](int t, int buf) __attribute__((always_inline)) {
+        const int t3 = t >> 1, kk = t & 1;
+        const int qq = 2 * kk + (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int row = t3 * BN + wco * TM * 32 + i * 32 + (lane & 31);
+          fa[buf][i] = as_bf16x8(As[row * 4 + swz4(row, qq)]);
+        }
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const int row = wp * TN * 32 + j * 32 + (lane & 31) + t3;
+          fb[j] = Bs[row * 4 + swz4(row + RA, qq)];
+        }
+      };
+      auto mask = [&](int t, int buf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          const bool ok = (vmask[j] >> (rf * 3 + (t >> 1))) & 1u;
+          bm[buf][j] = as_bf16x8(ok ? fb[j] : u32x4{0, 0, 0, 0});
+        }
+      };
+      load(0, 0);
+      mask(0, 0);
+#pragma unroll
+      for (int t = 0; t < 6; ++t) {
+        const int cur = t & 1;
+        if (t + 1 < 6) load(t + 1, cur ^ 1);
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j) acc[i][j] = mfma32(fa[cur][i], bm[cur][j], acc[i][j]);
+        if (t + 1 < 6) {
+          mask(t + 1, cur ^ 1);
+          // reads first, half the MFMAs (covering the read latency), the
+          // masking, then the other half
+          __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, (TM * TN + 1) / 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 4 * TN + 8, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, TM * TN / 2, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+
+    // tile epilogue; the bias goes through the constant address space so its
+    // (wave-uniform) loads are scalar and do not wait on the DMA ring
+    const __attribute__((address_space(4))) float* cbias =
+        (const __attribute__((address_space(4))) float*)bias;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int p = c_p0 + wp * TN * 32 + j * 32 + (lane & 31);
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int cob = c_co0 + wcu * TM * 32 + i * 32 + 8 * g;
+          const int co = cob + 4 * (lane >> 5);
+          if constexpr (SPLIT) {
+            const float4 o = make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1],
+                                         acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+            if (p < P) *(float4*)(part + ((long)c_split * P + p) * Cout + co) = o;
+          } else {
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              v[e] = acc[i][j][4 * g + e];
+              if (bias) {
+                const float b0 = cbias[cob + e], b1 = cbias[cob + 4 + e];
+                v[e] += (lane >> 5) ? b1 : b0;
+              }
+              if (relu) v[e] = fmaxf(v[e], 0.0f);
+            }
+            uint2 o;
+            o.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
+            o.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
+            if (p < P) *(uint2*)(Y + (long)p * Cout + co) = o;
+          }
+        }
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- wgrad
 
 // 8x8 transpose of bfloat16: in[j] holds 8 channels of pixel j; out[c] gets
@@ -631,10 +879,18 @@ __global__ __launch_bounds__(256) void conv_wgrad_mfma(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
   const int ncb = Cin / BNc;
-  const int tap = blockIdx.x / ncb;
-  const int ci0 = (blockIdx.x - tap * ncb) * BNc;
-  const int co0 = blockIdx.y * BMc;
-  const int split = blockIdx.z;
+  // 1-D grid of (split, tap, ci tile, co tile), split slowest.  The
+  // dispatcher deals blocks round-robin over the 8 XCDs; remapped, each XCD
+  // runs a contiguous range of splits with all their tiles, so the pixel rows
+  // of X and dZ a split reads are fetched into one L2 only.
+  const int T = TAPS * ncb * (Cout / BMc);
+  const int lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int split = lb / T;
+  const int t = lb - split * T;
+  const int tx = t % (TAPS * ncb);
+  const int tap = tx / ncb;
+  const int ci0 = (tx - tap * ncb) * BNc;
+  const int co0 = (t / (TAPS * ncb)) * BMc;
   const int ps = split * pix_per_split;
   const int pe = min(P, ps + pix_per_split);
   const int nk = (pe - ps + BK - 1) / BK;
@@ -745,47 +1001,58 @@ __global__ __launch_bounds__(256) void conv_wgrad_mfma(
     }
 }
 
-// dw[e] = sum_{s < S} part[s][e] in a fixed order: split-lane l of a block
-// sums s = l, l + 16, l + 32, ... serially, then lanes 0..15 are added in
-// order.  Each block covers 16 float4 columns (64 elements).
-__global__ __launch_bounds__(256) void splitk_reduce(const float* __restrict__ part,
-                                                     float* __restrict__ dw, long E, int S) {
-  __shared__ float4 red[16][16];
-  const int col = threadIdx.x & 15, lane = threadIdx.x >> 4;
-  const long e4 = ((long)blockIdx.x * 16 + col) * 4;
-  const bool vec = (E & 3) == 0;
+// out[e] = sum_{s < S} part[s][e] in a fixed order: a block of 1024 threads
+// covers C4 float4 columns with LANES = 1024 / C4 split lanes; lane l sums
+// s = l, l + LANES, ... in ascending order, then lanes 0 .. LANES - 1 are
+// added in order.  (C4, LANES) is a function of S only, so the order is a
+// function of the shape.  E must be a multiple of 4.
+template <int C4>
+__global__ __launch_bounds__(1024) void splitk_reduce(const float* __restrict__ part,
+                                                      float* __restrict__ out, long E, int S) {
+  constexpr int LANES = 1024 / C4;
+  __shared__ float4 red[LANES][C4];
+  const int col = threadIdx.x % C4, lane = threadIdx.x / C4;
+  const long e4 = ((long)blockIdx.x * C4 + col) * 4;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   if (e4 < E) {
-    for (int k = lane; k < S; k += 16) {
-      const float* p = part + (long)k * E + e4;
-      if (vec) {
-        float4 t = *(const float4*)p;
-        acc.x += t.x; acc.y += t.y; acc.z += t.z; acc.w += t.w;
-      } else {
-        acc.x += p[0];
-        if (e4 + 1 < E) acc.y += p[1];
-        if (e4 + 2 < E) acc.z += p[2];
-        if (e4 + 3 < E) acc.w += p[3];
+    int k = lane;
+    // eight independent loads in flight per step
+    for (; k + 7 * LANES < S; k += 8 * LANES) {
+      float4 t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = *(const float4*)(part + (long)(k + u * LANES) * E + e4);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        acc.x += t[u].x; acc.y += t[u].y; acc.z += t[u].z; acc.w += t[u].w;
       }
+    }
+    for (; k < S; k += LANES) {
+      const float4 t = *(const float4*)(part + (long)k * E + e4);
+      acc.x += t.x; acc.y += t.y; acc.z += t.z; acc.w += t.w;
     }
   }
   red[lane][col] = acc;
   __syncthreads();
   if (lane == 0 && e4 < E) {
-    float4 s = red[0][col];
-    for (int l = 1; l < 16; ++l) {
-      float4 t = red[l][col];
-      s.x += t.x; s.y += t.y; s.z += t.z; s.w += t.w;
+    float4 r = red[0][col];
+    for (int l = 1; l < LANES; ++l) {
+      const float4 t = red[l][col];
+      r.x += t.x; r.y += t.y; r.z += t.z; r.w += t.w;
     }
-    if (vec) {
-      *(float4*)(dw + e4) = s;
-    } else {
-      dw[e4] = s.x;
-      if (e4 + 1 < E) dw[e4 + 1] = s.y;
-      if (e4 + 2 < E) dw[e4 + 2] = s.z;
-      if (e4 + 3 < E) dw[e4 + 3] = s.w;
-    }
+    *(float4*)(out + e4) = r;
   }
+}
+
+// The same sum for E not a multiple of 4 (e.g. the bias of a one-channel
+// head), one element per thread, s ascending.
+__global__ __launch_bounds__(256) void splitk_reduce_scalar(const float* __restrict__ part,
+                                                            float* __restrict__ out, long E,
+                                                            int S) {
+  const long e = (long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= E) return;
+  float acc = 0.f;
+  for (int k = 0; k < S; ++k) acc += part[(long)k * E + e];
+  out[e] = acc;
 }
 
 // wt[ci][tap'][co] = w[co][taps-1-tap'][ci]: the data gradient of a
@@ -907,26 +1174,121 @@ hipError_t launch_fwd_rows(const char* name, const bf16_t* X, const bf16_t* Wt, 
   launch_fwd_rows<WCO, WP, TM, TN, NS>("conv_fwd_rows<" #WCO "," #WP "," #TM "," #TN "," #NS ">", \
                                        X, Wt, b, Y, part, part_cap, P, s, relu, S, st)
 
+// Persistent row-stage launches.  S (a divisor of the 3 * Cin / 32 stages,
+// reduced to fit part_cap) splits every tile's K range; the grid is the
+// number of blocks that fit on the chip at once, capped by the item count.
+constexpr int rows_pers_lds(int WCO, int WP, int TM, int TN, int NS) {
+  return NS * ((3 * WCO * TM * 32 + WP * TN * 32 + 2 + 16 * WCO * WP - 1) / (16 * WCO * WP) *
+               (16 * WCO * WP)) * 64;
+}
+
+template <int WCO, int WP, int TM, int TN, int NS>
+hipError_t launch_rows_pers(const char* name, const bf16_t* X, const bf16_t* Wt, const float* b,
+                            bf16_t* Y, float* part, size_t part_cap, long P, const ConvShape& s,
+                            int relu, int S, hipStream_t st) {
+  constexpr int BN = WCO * TM * 32, BM = WP * TN * 32, NW = WCO * WP;
+  constexpr int LDS = rows_pers_lds(WCO, WP, TM, TN, NS);
+  static_assert(LDS <= 160 * 1024, "LDS ring too large");
+  if (s.cout % BN || s.cin % 32 || s.taps != 9) return hipErrorInvalidValue;
+  // byte offsets into X and W are 32-bit, negative ones must read as out of range
+  if ((double)(P + BM + 2L * s.W + 2) * s.cin * 2 >= 2147483648.0 ||
+      (double)s.cout * 9 * s.cin * 2 >= 2147483648.0)
+    return hipErrorInvalidValue;
+  const int nst = 3 * (s.cin / 32);
+  if (S < 1) S = 1;
+  if (S > nst) S = nst;
+  while (S > 1 && (nst % S || (size_t)S * P * s.cout > part_cap)) --S;
+  const int npt = cdiv(P, BM);
+  const long items = (long)npt * (s.cout / BN) * S;
+  int occ = (160 * 1024) / LDS;
+  if (occ * NW > 16) occ = 16 / NW;
+  if (occ < 1) occ = 1;
+  const int G = (int)(items < 256L * occ ? items : 256L * occ);
+  const double flops = 2.0 * P * s.cout * 9 * s.cin;
+  const double xbytes = 2.0 * P * s.cin, wbytes = 2.0 * s.cout * 9 * s.cin;
+  const int co_major = g_fwd_order >= 0 ? g_fwd_order : (wbytes > xbytes ? 1 : 0);
+  if (G == 0) return hipSuccess;
+  if (S == 1) {
+    ProfScope ps(name, flops, xbytes + wbytes + 2.0 * P * s.cout, st);
+    hipLaunchKernelGGL((conv_rows_pers<WCO, WP, TM, TN, NS, false>), dim3(G), dim3(NW * 64), 0, st,
+                       X, Wt, b, Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, npt, 1);
+    return hipGetLastError();
+  }
+  {
+    ProfScope ps(name, flops, xbytes + wbytes + 4.0 * S * P * s.cout, st);
+    hipLaunchKernelGGL((conv_rows_pers<WCO, WP, TM, TN, NS, true>), dim3(G), dim3(NW * 64), 0, st,
+                       X, Wt, b, Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, npt, S);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  ProfScope ps2("conv_rows_epilogue", 0.0, 4.0 * S * P * s.cout + 2.0 * P * s.cout, st);
+  hipLaunchKernelGGL(conv_rows_epilogue, dim3(cdiv(P * s.cout, 2048)), dim3(256), 0, st, part, b,
+                     Y, P, s.cout, S, relu);
+  return hipGetLastError();
+}
+
+#define TGP_PERS_CFG(WCO, WP, TM, TN, NS, S)                                                     \
+  launch_rows_pers<WCO, WP, TM, TN, NS>("conv_rows_pers<" #WCO "," #WP "," #TM "," #TN "," #NS ">", \
+                                        X, Wt, b, Y, part, part_cap, P, s, relu, S, st)
+
 int g_fwd_split = 0;   // > 0 forces the split count (measurement only)
 
 struct FwdPlan {
-  int cfg;   // 1..: row-stage configurations; 100+: per-tap configurations
+  int cfg;   // 1..: row-stage configurations; 100+: per-tap; 200+: persistent row-stage
   int S;
 };
 
-// Pure function of the shape (plus the measurement overrides).
+struct PersTile { int BN, BM; };
+PersTile pers_tile(int cfg) {
+  switch (cfg) {
+    case 202: return {128, 256};
+    case 203: return {64, 256};
+    case 204: return {128, 128};
+    case 205: return {64, 640};
+    case 206: return {128, 256};
+    case 207: return {128, 256};
+    default: return {64, 512};
+  }
+}
+
+// Pure function of the per-sample shape (H, W, Cin, Cout, taps), plus the
+// measurement overrides: the kernel family and the split count fix the K
+// summation order, so keeping them independent of the number of samples
+// keeps every sample's output bit-identical whatever the micro-batch size.
+// The tile-count heuristics use a nominal micro-batch of 4 samples.
 FwdPlan fwd_plan(const ConvShape& s) {
-  const long P = s.pixels();
+  const long P = 4L * s.H * s.W;
   FwdPlan pl{0, 1};
-  // Row-stage tiles pay off only on the deep, small-image layers (few pixel
-  // tiles, long K); elsewhere the per-tap kernel keeps more blocks per CU.
-  if (s.taps == 9 && s.cin % 64 == 0 && s.cin >= 256 && P <= 4096) {
-    pl.cfg = 3;    // 64 x 256, 8 waves
+  // Measured per shape: the persistent row-stage kernel wins on the deep,
+  // small-image layers (few pixel tiles, long K); the per-tap kernel, with
+  // several small blocks per CU, on the large images.
+  if (s.taps == 9 && s.cin % 64 == 0 && P <= 4096) {
+    pl.cfg = 203;  // persistent row-stage, 64 x 256
+  } else if (s.taps == 9 && s.cin % 64 == 0 && P <= 16384 && s.cin >= 256 && s.cout % 128 == 0) {
+    pl.cfg = 207;  // persistent row-stage, 128 x 256, 8 waves
   } else {
     pl.cfg = 100;
   }
   if (g_fwd_variant > 0) pl.cfg = g_fwd_variant;
   if ((pl.cfg == 2 || pl.cfg == 5) && s.cout % 128) pl.cfg = pl.cfg == 2 ? 1 : 3;  // 128-wide tiles need cout % 128 == 0
+  if (pl.cfg >= 200) {
+    if (s.taps != 9 || s.cin % 32) { pl.cfg = 100; return pl; }
+    const PersTile t = pers_tile(pl.cfg);
+    if (s.cout % t.BN) pl.cfg = 201;                   // 64-channel tiles fit every shape here
+    const PersTile u = pers_tile(pl.cfg);
+    const long tiles = cdiv(P, u.BM) * (long)(s.cout / u.BN);
+    const int nst = 3 * (s.cin / 32);
+    int S = 1;
+    // split K only when the tiles alone leave most of the chip idle
+    while (tiles * S < 192 && S < 8) {
+      int n = S + 1;
+      while (n <= nst && nst % n) ++n;
+      if (n > nst) break;
+      S = n;
+    }
+    pl.S = g_fwd_split > 0 ? g_fwd_split : S;
+    return pl;
+  }
   if (pl.cfg < 100) {
     const int BN = (pl.cfg == 2 || pl.cfg == 5) ? 128 : 64;
     const int BM = (pl.cfg == 2 || pl.cfg == 5 || pl.cfg == 6 || pl.cfg == 7) ? 128 : 256;
@@ -943,7 +1305,8 @@ FwdPlan fwd_plan(const ConvShape& s) {
 size_t conv_forward_partial_floats(int dt, const ConvShape& s) {
   if (!mfma_conv_ok(dt, s.cin, s.cout)) return 0;
   FwdPlan pl = fwd_plan(s);
-  return pl.cfg < 100 && pl.S > 1 ? (size_t)pl.S * s.pixels() * s.cout : 0;
+  const bool splits = pl.cfg < 100 || pl.cfg >= 200;   // the per-tap kernels never split
+  return splits && pl.S > 1 ? (size_t)pl.S * s.pixels() * s.cout : 0;
 }
 
 hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void* y,
@@ -965,6 +1328,13 @@ hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void*
                         : TGP_ROWS_CFG(1, 8, 2, 1, 2, pl.S);
     case 6: return TGP_ROWS_CFG(1, 4, 2, 1, 2, pl.S);                 // 64 x 128, 4 waves
     case 7: return TGP_ROWS_CFG(1, 4, 2, 1, 3, pl.S);                 // 64 x 128, 4 waves, 3 stages
+    case 201: return TGP_PERS_CFG(1, 4, 2, 4, 3, pl.S);               // 64 x 512
+    case 202: return TGP_PERS_CFG(2, 2, 2, 4, 3, pl.S);               // 128 x 256
+    case 203: return TGP_PERS_CFG(1, 4, 2, 2, 4, pl.S);               // 64 x 256
+    case 204: return TGP_PERS_CFG(2, 2, 2, 2, 4, pl.S);               // 128 x 128
+    case 205: return TGP_PERS_CFG(1, 4, 2, 5, 2, pl.S);               // 64 x 640
+    case 206: return TGP_PERS_CFG(2, 2, 2, 4, 2, pl.S);               // 128 x 256, 2 stages
+    case 207: return TGP_PERS_CFG(2, 4, 2, 2, 3, pl.S);               // 128 x 256, 8 waves
     default: break;
   }
   // per-tap kernel (1x1 convolutions, and reference configurations)
@@ -1008,7 +1378,7 @@ hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* part
   int tiles = s.taps * (s.cin / bn) * (s.cout / bm);
   long E = (long)s.cout * s.taps * s.cin;
   WgradPlan pl = wgrad_plan<2, 2>(P, tiles, E);
-  dim3 grid(s.taps * (s.cin / bn), s.cout / bm, pl.S);
+  dim3 grid(s.taps * (s.cin / bn) * (s.cout / bm) * pl.S);
   double flops = 2.0 * P * E;
   double bytes = 2.0 * ((double)P * s.cin + (double)P * s.cout) + 4.0 * pl.S * E;
   {
@@ -1039,7 +1409,18 @@ hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* part
 
 hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st) {
   ProfScope ps("splitk_reduce", 0.0, 4.0 * E * (S + 1), st);
-  hipLaunchKernelGGL(splitk_reduce, dim3(cdiv(E, 64)), dim3(256), 0, st, part, out, E, S);
+  if (E % 4) {
+    hipLaunchKernelGGL(splitk_reduce_scalar, dim3(cdiv(E, 256)), dim3(256), 0, st, part, out, E, S);
+    return hipGetLastError();
+  }
+  // many splits of few columns: 16 columns x 64 split lanes; few splits:
+  // 256 columns x 4 lanes
+  if (S >= 64)
+    hipLaunchKernelGGL(splitk_reduce<16>, dim3(cdiv(E, 64)), dim3(1024), 0, st, part, out, E, S);
+  else if (S >= 16)
+    hipLaunchKernelGGL(splitk_reduce<64>, dim3(cdiv(E, 256)), dim3(1024), 0, st, part, out, E, S);
+  else
+    hipLaunchKernelGGL(splitk_reduce<256>, dim3(cdiv(E, 1024)), dim3(1024), 0, st, part, out, E, S);
   return hipGetLastError();
 }
 
