@@ -29,6 +29,148 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+# ---------------------------------------------------------------- profiles
+# rocprofv3 summaries live in profiles/ as text.  The HBM traffic of the
+# dominant kernel comes from two counter runs (FETCH_SIZE, WRITE_SIZE, KiB
+# per dispatch), each scaled by what the same counter reads for a device
+# copy of known size.  A summary records a hash of the kernel sources; the
+# bench reports its traffic only while the sources are unchanged.
+PROFILES = os.path.join(HERE, "profiles")
+KERNEL_SOURCES = ["paper_2004_09910_amd/csrc/conv_mfma.hip",
+                  "paper_2004_09910_amd/csrc/elementwise.hip",
+                  "paper_2004_09910_amd/csrc/common.h"]
+PROFILE_COMMANDS = {
+    "trace": "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_kt -o kt "
+             "-- python3 bench.py --steps 10 --warmup 2 --no-cpu-baseline",
+    "fetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/prof_fetch -o f "
+             "-- python3 bench.py --eager --steps 1 --warmup 1 --no-cpu-baseline",
+    "write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/prof_write -o w "
+             "-- python3 bench.py --eager --steps 1 --warmup 1 --no-cpu-baseline",
+    "copy_fetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/prof_cfetch -o cf "
+                  "-- python3 bench.py --copy-calibration",
+    "copy_write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/prof_cwrite -o cw "
+                  "-- python3 bench.py --copy-calibration",
+}
+
+
+def kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(HERE, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def short_kernel_name(full):
+    """'void ns::(anonymous namespace)::k<2, 4>(int, ...)' -> 'k<2,4>'."""
+    n = full.replace("(anonymous namespace)::", "")
+    if n.startswith("void "):
+        n = n[5:]
+    depth, cut = 0, len(n)
+    for i, ch in enumerate(n):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            cut = i
+            break
+    n = n[:cut]
+    head, sep, tail = n.partition("<")
+    head = head.split("::")[-1]
+    return (head + sep + tail).replace(" ", "")
+
+
+def _counter_means(path):
+    import csv
+    import glob
+    sums, counts = {}, {}
+    for f in glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            k = short_kernel_name(r["Kernel_Name"])
+            sums[k] = sums.get(k, 0.0) + float(r["Counter_Value"])
+            counts[k] = counts.get(k, 0) + 1
+    return {k: sums[k] / counts[k] for k in sums}, counts
+
+
+def summarize_profiles(out_dir, workload):
+    """Writes profiles/kernel_trace_<workload>.md and
+    profiles/traffic_<kernel>_<workload>.md from the rocprofv3 runs listed in
+    PROFILE_COMMANDS (their output under out_dir)."""
+    import csv
+    import glob
+    import json as _json
+    os.makedirs(PROFILES, exist_ok=True)
+    stats_csv = glob.glob(os.path.join(out_dir, "prof_kt", "**", "*kernel_stats.csv"), recursive=True)[0]
+    rows = list(csv.DictReader(open(stats_csv)))
+    lines = [f"# Kernel trace: {workload}", "",
+             "Command (from the repository root on the GPU host):", "",
+             "    " + PROFILE_COMMANDS["trace"], "",
+             "rocprofv3 `--stats` summary (all dispatches of the run: warmup, HIP-graph replays and "
+             "the eager per-kernel timing pass).", "",
+             "| kernel | calls | avg us | total ms | % |", "|---|---:|---:|---:|---:|"]
+    for r in rows:
+        lines.append(f"| `{short_kernel_name(r['Name'])}` | {r['Calls']} | "
+                     f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['TotalDurationNs']) / 1e6:.3f} | "
+                     f"{float(r['Percentage']):.2f} |")
+    with open(os.path.join(PROFILES, f"kernel_trace_{workload}.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    top = short_kernel_name(rows[0]["Name"])
+    fetch, nf = _counter_means(os.path.join(out_dir, "prof_fetch"))
+    write, nw = _counter_means(os.path.join(out_dir, "prof_write"))
+    cf, _ = _counter_means(os.path.join(out_dir, "prof_cfetch"))
+    cw, _ = _counter_means(os.path.join(out_dir, "prof_cwrite"))
+    copy_k = [k for k in cf if "copyBuffer" in k or "copy" in k.lower()]
+    gib_kib = float(1 << 20)                       # 1 GiB copied, in KiB
+    f_fetch = gib_kib / cf[copy_k[0]]
+    f_write = gib_kib / cw[copy_k[0]]
+    fb = fetch[top] * 1024 * f_fetch
+    wb = write[top] * 1024 * f_write
+    info = {"kernel": top, "workload": workload, "fetch_bytes": fb, "write_bytes": wb,
+            "bytes_per_launch": fb + wb, "dispatches": nf.get(top, 0),
+            "fetch_scale": f_fetch, "write_scale": f_write, "source_hash": kernel_source_hash()}
+    tl = [f"# HBM traffic of `{top}`: {workload}", "",
+          "Commands (from the repository root on the GPU host):", ""]
+    for k in ("fetch", "write", "copy_fetch", "copy_write"):
+        tl.append("    " + PROFILE_COMMANDS[k])
+    tl += ["",
+           f"- FETCH_SIZE, mean per dispatch: {fetch[top]:.1f} KiB over {nf.get(top, 0)} dispatches; "
+           f"a 1 GiB device copy reads {cf[copy_k[0]]:.1f} KiB, so the scale is {f_fetch:.4f}.",
+           f"- WRITE_SIZE, mean per dispatch: {write[top]:.1f} KiB over {nw.get(top, 0)} dispatches; "
+           f"the copy writes {cw[copy_k[0]]:.1f} KiB, scale {f_write:.4f}.",
+           f"- HBM bytes per launch: {fb / 1e6:.2f} MB read + {wb / 1e6:.2f} MB written = "
+           f"{(fb + wb) / 1e6:.2f} MB.", "",
+           "Other kernels of the same runs (mean KiB per dispatch, unscaled):", "",
+           "| kernel | FETCH_SIZE | WRITE_SIZE |", "|---|---:|---:|"]
+    for k in sorted(fetch, key=lambda k: -fetch[k] * nf[k])[:12]:
+        tl.append(f"| `{k}` | {fetch[k]:.1f} | {write.get(k, float('nan')):.1f} |")
+    tl += ["", "traffic_json: " + _json.dumps(info)]
+    safe = top.replace("<", "_").replace(">", "").replace(",", "_")
+    with open(os.path.join(PROFILES, f"traffic_{safe}_{workload}.md"), "w") as f:
+        f.write("\n".join(tl) + "\n")
+    print(_json.dumps(info))
+
+
+def recorded_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from a profiles/ summary taken with
+    the current kernel sources, else None."""
+    import glob
+    import json as _json
+    try:
+        cur = kernel_source_hash()
+    except OSError:
+        return None
+    for path in glob.glob(os.path.join(PROFILES, "traffic_*.md")):
+        for line in open(path):
+            if line.startswith("traffic_json: "):
+                info = _json.loads(line[len("traffic_json: "):])
+                if info.get("kernel") == kernel and info.get("workload") == workload and \
+                        info.get("source_hash") == cur:
+                    return info["bytes_per_launch"]
+    return None
+
+
 def cpu_baseline(wl, lo, hi, samples, dtype):
     """The oracle (float64 CPU, bf16 storage points) on a bounded sample of the
     same workload: `samples` single-sample forward + backward passes of the
@@ -75,7 +217,13 @@ def main():
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three device-to-device copies of 1 GiB (the reference "
                          "kernel that scales the HBM byte counters)")
+    ap.add_argument("--summarize-profiles", metavar="DIR",
+                    help="write the profiles/ summaries from rocprofv3 output under DIR")
     args = ap.parse_args()
+    if args.summarize_profiles:
+        from workloads import specs
+        summarize_profiles(args.summarize_profiles, specs.unet_stage().name)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); this build has no "
               f"multi-GPU path", file=sys.stderr)
@@ -196,6 +344,8 @@ def main():
         achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                 "frac": achieved / (HBM_PEAK / 1e9), "traffic": None}
+    roof["traffic"] = recorded_traffic(dom["name"], wl.name)
+    roof["algorithmic_bytes_per_launch"] = dom["bytes"] / dom["launches"]
     roof["kernel"] = dom["name"]
     roof["launches_per_step"] = dom["launches"] / per_step_div
     roof["avg_launch_us"] = 1e3 * per_launch_ms

@@ -1110,8 +1110,10 @@ int g_fwd_variant = 0;
 int g_fwd_order = -1;   // -1: by operand size; 0/1 forced (measurement only)
 
 template <int WCO, int WP, int TM, int TN, int NS>
-hipError_t launch_fwd_dma(const char* name, const bf16_t* X, const bf16_t* Wt, const float* b,
-                          bf16_t* Y, long P, const ConvShape& s, int relu, hipStream_t st) {
+hipError_t launch_fwd_dma(const char* name9, const char* name1, const bf16_t* X, const bf16_t* Wt,
+                          const float* b, bf16_t* Y, long P, const ConvShape& s, int relu,
+                          hipStream_t st) {
+  const char* name = s.taps == 9 ? name9 : name1;
   constexpr int BN = WCO * TM * 32, BM = WP * TN * 32;
   if (s.cout % BN) return hipErrorInvalidValue;
   dim3 grid(cdiv(P, BM) * (s.cout / BN));
@@ -1121,22 +1123,25 @@ hipError_t launch_fwd_dma(const char* name, const bf16_t* X, const bf16_t* Wt, c
   const double xbytes = 2.0 * P * s.cin, wbytes = 2.0 * s.cout * s.taps * s.cin;
   const int co_major = g_fwd_order >= 0 ? g_fwd_order : (wbytes > xbytes ? 1 : 0);
   if (s.taps == 9)
-    hipLaunchKernelGGL((conv_fwd_dma<WCO, WP, TM, TN, 9, NS>), grid, dim3(WCO * WP * 64), 0, st, X,
+    TGP_LAUNCH(ps, (conv_fwd_dma<WCO, WP, TM, TN, 9, NS>), grid, dim3(WCO * WP * 64), 0, st, X,
                        Wt, b, Y, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major);
   else
-    hipLaunchKernelGGL((conv_fwd_dma<WCO, WP, TM, TN, 1, NS>), grid, dim3(WCO * WP * 64), 0, st, X,
+    TGP_LAUNCH(ps, (conv_fwd_dma<WCO, WP, TM, TN, 1, NS>), grid, dim3(WCO * WP * 64), 0, st, X,
                        Wt, b, Y, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major);
   return hipGetLastError();
 }
 
-#define TGP_FWD_CFG(WCO, WP, TM, TN, NS) \
-  launch_fwd_dma<WCO, WP, TM, TN, NS>("conv_fwd_dma<" #WCO "," #WP "," #TM "," #TN "," #NS ">", X, Wt, b, Y, P, s, relu, st)
+#define TGP_FWD_CFG(WCO, WP, TM, TN, NS)                                                        \
+  launch_fwd_dma<WCO, WP, TM, TN, NS>("conv_fwd_dma<" #WCO "," #WP "," #TM "," #TN ",9," #NS ">", \
+                                      "conv_fwd_dma<" #WCO "," #WP "," #TM "," #TN ",1," #NS ">", \
+                                      X, Wt, b, Y, P, s, relu, st)
 
 // Row-stage forward launches.  S > 1 splits the stages over S blocks per
 // tile; the partials live in `part` (capacity part_cap floats; S is reduced
 // to fit, which only happens under measurement overrides).
 template <int WCO, int WP, int TM, int TN, int NS>
-hipError_t launch_fwd_rows(const char* name, const bf16_t* X, const bf16_t* Wt, const float* b,
+hipError_t launch_fwd_rows(const char* name_f, const char* name_t, const bf16_t* X,
+                           const bf16_t* Wt, const float* b,
                            bf16_t* Y, float* part, size_t part_cap, long P, const ConvShape& s,
                            int relu, int S, hipStream_t st) {
   constexpr int BN = WCO * TM * 32, BM = WP * TN * 32;
@@ -1152,27 +1157,29 @@ hipError_t launch_fwd_rows(const char* name, const bf16_t* X, const bf16_t* Wt, 
   const int co_major = g_fwd_order >= 0 ? g_fwd_order : (wbytes > xbytes ? 1 : 0);
   dim3 grid(tiles * S), block(WCO * WP * 64);
   if (S == 1) {
-    ProfScope ps(name, flops, xbytes + wbytes + 2.0 * P * s.cout, st);
-    hipLaunchKernelGGL((conv_fwd_rows<WCO, WP, TM, TN, NS, false>), grid, block, 0, st, X, Wt, b,
+    ProfScope ps(name_f, flops, xbytes + wbytes + 2.0 * P * s.cout, st);
+    TGP_LAUNCH(ps, (conv_fwd_rows<WCO, WP, TM, TN, NS, false>), grid, block, 0, st, X, Wt, b,
                        Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, tiles, sps);
     return hipGetLastError();
   }
   {
-    ProfScope ps(name, flops, xbytes + wbytes + 4.0 * S * P * s.cout, st);
-    hipLaunchKernelGGL((conv_fwd_rows<WCO, WP, TM, TN, NS, true>), grid, block, 0, st, X, Wt, b,
+    ProfScope ps(name_t, flops, xbytes + wbytes + 4.0 * S * P * s.cout, st);
+    TGP_LAUNCH(ps, (conv_fwd_rows<WCO, WP, TM, TN, NS, true>), grid, block, 0, st, X, Wt, b,
                        Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, tiles, sps);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   ProfScope ps2("conv_rows_epilogue", 0.0, 4.0 * S * P * s.cout + 2.0 * P * s.cout, st);
-  hipLaunchKernelGGL(conv_rows_epilogue, dim3(cdiv(P * s.cout, 2048)), dim3(256), 0, st, part, b,
+  TGP_LAUNCH(ps2, conv_rows_epilogue, dim3(cdiv(P * s.cout, 2048)), dim3(256), 0, st, part, b,
                      Y, P, s.cout, S, relu);
   return hipGetLastError();
 }
 
-#define TGP_ROWS_CFG(WCO, WP, TM, TN, NS, S)                                               \
-  launch_fwd_rows<WCO, WP, TM, TN, NS>("conv_fwd_rows<" #WCO "," #WP "," #TM "," #TN "," #NS ">", \
-                                       X, Wt, b, Y, part, part_cap, P, s, relu, S, st)
+#define TGP_ROWS_CFG(WCO, WP, TM, TN, NS, S)                                                   \
+  launch_fwd_rows<WCO, WP, TM, TN, NS>(                                                        \
+      "conv_fwd_rows<" #WCO "," #WP "," #TM "," #TN "," #NS ",false>",                          \
+      "conv_fwd_rows<" #WCO "," #WP "," #TM "," #TN "," #NS ",true>", X, Wt, b, Y, part, part_cap, \
+      P, s, relu, S, st)
 
 // Persistent row-stage launches.  S (a divisor of the 3 * Cin / 32 stages,
 // reduced to fit part_cap) splits every tile's K range; the grid is the
@@ -1183,7 +1190,8 @@ constexpr int rows_pers_lds(int WCO, int WP, int TM, int TN, int NS) {
 }
 
 template <int WCO, int WP, int TM, int TN, int NS>
-hipError_t launch_rows_pers(const char* name, const bf16_t* X, const bf16_t* Wt, const float* b,
+hipError_t launch_rows_pers(const char* name_f, const char* name_t, const bf16_t* X,
+                            const bf16_t* Wt, const float* b,
                             bf16_t* Y, float* part, size_t part_cap, long P, const ConvShape& s,
                             int relu, int S, hipStream_t st) {
   constexpr int BN = WCO * TM * 32, BM = WP * TN * 32, NW = WCO * WP;
@@ -1209,27 +1217,29 @@ hipError_t launch_rows_pers(const char* name, const bf16_t* X, const bf16_t* Wt,
   const int co_major = g_fwd_order >= 0 ? g_fwd_order : (wbytes > xbytes ? 1 : 0);
   if (G == 0) return hipSuccess;
   if (S == 1) {
-    ProfScope ps(name, flops, xbytes + wbytes + 2.0 * P * s.cout, st);
-    hipLaunchKernelGGL((conv_rows_pers<WCO, WP, TM, TN, NS, false>), dim3(G), dim3(NW * 64), 0, st,
+    ProfScope ps(name_f, flops, xbytes + wbytes + 2.0 * P * s.cout, st);
+    TGP_LAUNCH(ps, (conv_rows_pers<WCO, WP, TM, TN, NS, false>), dim3(G), dim3(NW * 64), 0, st,
                        X, Wt, b, Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, npt, 1);
     return hipGetLastError();
   }
   {
-    ProfScope ps(name, flops, xbytes + wbytes + 4.0 * S * P * s.cout, st);
-    hipLaunchKernelGGL((conv_rows_pers<WCO, WP, TM, TN, NS, true>), dim3(G), dim3(NW * 64), 0, st,
+    ProfScope ps(name_t, flops, xbytes + wbytes + 4.0 * S * P * s.cout, st);
+    TGP_LAUNCH(ps, (conv_rows_pers<WCO, WP, TM, TN, NS, true>), dim3(G), dim3(NW * 64), 0, st,
                        X, Wt, b, Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, npt, S);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   ProfScope ps2("conv_rows_epilogue", 0.0, 4.0 * S * P * s.cout + 2.0 * P * s.cout, st);
-  hipLaunchKernelGGL(conv_rows_epilogue, dim3(cdiv(P * s.cout, 2048)), dim3(256), 0, st, part, b,
+  TGP_LAUNCH(ps2, conv_rows_epilogue, dim3(cdiv(P * s.cout, 2048)), dim3(256), 0, st, part, b,
                      Y, P, s.cout, S, relu);
   return hipGetLastError();
 }
 
-#define TGP_PERS_CFG(WCO, WP, TM, TN, NS, S)                                                     \
-  launch_rows_pers<WCO, WP, TM, TN, NS>("conv_rows_pers<" #WCO "," #WP "," #TM "," #TN "," #NS ">", \
-                                        X, Wt, b, Y, part, part_cap, P, s, relu, S, st)
+#define TGP_PERS_CFG(WCO, WP, TM, TN, NS, S)                                                    \
+  launch_rows_pers<WCO, WP, TM, TN, NS>(                                                        \
+      "conv_rows_pers<" #WCO "," #WP "," #TM "," #TN "," #NS ",false>",                          \
+      "conv_rows_pers<" #WCO "," #WP "," #TM "," #TN "," #NS ",true>", X, Wt, b, Y, part, part_cap, \
+      P, s, relu, S, st)
 
 int g_fwd_split = 0;   // > 0 forces the split count (measurement only)
 
@@ -1352,10 +1362,10 @@ hipError_t weight_transform(int dt, const void* w, void* wt, int cout, int cin, 
   long n = (long)cout * cin * taps;
   ProfScope ps("wtransform", 0.0, 2.0 * n * (dt == 0 ? 2 : 4), st);
   if (dt == 0)
-    hipLaunchKernelGGL(wtransform_kernel<bf16_t>, dim3(cdiv(n, 256)), dim3(256), 0, st,
+    TGP_LAUNCH(ps, wtransform_kernel<bf16_t>, dim3(cdiv(n, 256)), dim3(256), 0, st,
                        (const bf16_t*)w, (bf16_t*)wt, cout, cin, taps);
   else
-    hipLaunchKernelGGL(wtransform_kernel<float>, dim3(cdiv(n, 256)), dim3(256), 0, st,
+    TGP_LAUNCH(ps, wtransform_kernel<float>, dim3(cdiv(n, 256)), dim3(256), 0, st,
                        (const float*)w, (float*)wt, cout, cin, taps);
   return hipGetLastError();
 }
@@ -1388,17 +1398,17 @@ hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* part
     if (pl.S == 1) partial = dw;   // a single split writes the gradient itself
     if (big) {
       if (s.taps == 9)
-        hipLaunchKernelGGL((conv_wgrad_mfma<2, 2, 2, 2, 9>), grid, dim3(256), 0, st, X, DZ,
+        TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 2, 2, 9>), grid, dim3(256), 0, st, X, DZ,
                            partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
       else
-        hipLaunchKernelGGL((conv_wgrad_mfma<2, 2, 2, 2, 1>), grid, dim3(256), 0, st, X, DZ,
+        TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 2, 2, 1>), grid, dim3(256), 0, st, X, DZ,
                            partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
     } else {
       if (s.taps == 9)
-        hipLaunchKernelGGL((conv_wgrad_mfma<2, 2, 1, 1, 9>), grid, dim3(256), 0, st, X, DZ,
+        TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 9>), grid, dim3(256), 0, st, X, DZ,
                            partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
       else
-        hipLaunchKernelGGL((conv_wgrad_mfma<2, 2, 1, 1, 1>), grid, dim3(256), 0, st, X, DZ,
+        TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 1>), grid, dim3(256), 0, st, X, DZ,
                            partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
     }
   }
@@ -1410,17 +1420,17 @@ hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* part
 hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st) {
   ProfScope ps("splitk_reduce", 0.0, 4.0 * E * (S + 1), st);
   if (E % 4) {
-    hipLaunchKernelGGL(splitk_reduce_scalar, dim3(cdiv(E, 256)), dim3(256), 0, st, part, out, E, S);
+    TGP_LAUNCH(ps, splitk_reduce_scalar, dim3(cdiv(E, 256)), dim3(256), 0, st, part, out, E, S);
     return hipGetLastError();
   }
   // many splits of few columns: 16 columns x 64 split lanes; few splits:
   // 256 columns x 4 lanes
   if (S >= 64)
-    hipLaunchKernelGGL(splitk_reduce<16>, dim3(cdiv(E, 64)), dim3(1024), 0, st, part, out, E, S);
+    TGP_LAUNCH(ps, splitk_reduce<16>, dim3(cdiv(E, 64)), dim3(1024), 0, st, part, out, E, S);
   else if (S >= 16)
-    hipLaunchKernelGGL(splitk_reduce<64>, dim3(cdiv(E, 256)), dim3(1024), 0, st, part, out, E, S);
+    TGP_LAUNCH(ps, splitk_reduce<64>, dim3(cdiv(E, 256)), dim3(1024), 0, st, part, out, E, S);
   else
-    hipLaunchKernelGGL(splitk_reduce<256>, dim3(cdiv(E, 1024)), dim3(1024), 0, st, part, out, E, S);
+    TGP_LAUNCH(ps, splitk_reduce<256>, dim3(cdiv(E, 1024)), dim3(1024), 0, st, part, out, E, S);
   return hipGetLastError();
 }
 

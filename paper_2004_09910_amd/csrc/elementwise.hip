@@ -518,10 +518,10 @@ hipError_t conv_forward(int dt, const void* x, const void* w, const float* b, vo
   ProfScope ps("conv_fwd_direct", 2.0 * P * s.cout * s.taps * s.cin,
                (double)esz * (P * s.cin + (double)s.cout * s.taps * s.cin + P * s.cout), st);
   if (dt == 0)
-    hipLaunchKernelGGL(conv_fwd_direct<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
+    TGP_LAUNCH(ps, conv_fwd_direct<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
                        (const bf16_t*)w, b, (bf16_t*)y, P, s.H, s.W, s.cin, s.cout, s.taps, relu);
   else
-    hipLaunchKernelGGL(conv_fwd_direct<float>, g, dim3(256), 0, st, (const float*)x,
+    TGP_LAUNCH(ps, conv_fwd_direct<float>, g, dim3(256), 0, st, (const float*)x,
                        (const float*)w, b, (float*)y, P, s.H, s.W, s.cin, s.cout, s.taps, relu);
   return hipGetLastError();
 }
@@ -540,10 +540,10 @@ hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, voi
   ProfScope ps("conv_dgrad_direct", 2.0 * P * s.cout * s.taps * s.cin,
                (double)esz * (P * s.cin + (double)s.cout * s.taps * s.cin + P * s.cout), st);
   if (dt == 0)
-    hipLaunchKernelGGL(conv_dgrad_direct<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dz,
+    TGP_LAUNCH(ps, conv_dgrad_direct<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dz,
                        (const bf16_t*)w, (bf16_t*)dx, P, s.H, s.W, s.cin, s.cout, s.taps);
   else
-    hipLaunchKernelGGL(conv_dgrad_direct<float>, g, dim3(256), 0, st, (const float*)dz,
+    TGP_LAUNCH(ps, conv_dgrad_direct<float>, g, dim3(256), 0, st, (const float*)dz,
                        (const float*)w, (float*)dx, P, s.H, s.W, s.cin, s.cout, s.taps);
   return hipGetLastError();
 }
@@ -565,10 +565,10 @@ hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* p
   int esz = dt == 0 ? 2 : 4;
   ProfScope ps("conv_wgrad_direct", 2.0 * P * E, (double)esz * P * (s.cin + s.cout) + 4.0 * S * E, st);
   if (dt == 0)
-    hipLaunchKernelGGL(conv_wgrad_direct<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
+    TGP_LAUNCH(ps, conv_wgrad_direct<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
                        (const bf16_t*)dz, partial, P, s.H, s.W, s.cin, s.cout, s.taps, pps);
   else
-    hipLaunchKernelGGL(conv_wgrad_direct<float>, g, dim3(256), 0, st, (const float*)x,
+    TGP_LAUNCH(ps, conv_wgrad_direct<float>, g, dim3(256), 0, st, (const float*)x,
                        (const float*)dz, partial, P, s.H, s.W, s.cin, s.cout, s.taps, pps);
   }
   hipError_t e = hipGetLastError();
@@ -582,10 +582,10 @@ hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void
   dim3 g(cdiv(P * C, 256));
   ProfScope ps("dw_forward", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
   if (dt == 0)
-    hipLaunchKernelGGL(dw_fwd<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, (const bf16_t*)w,
+    TGP_LAUNCH(ps, dw_fwd<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, (const bf16_t*)w,
                        b, (bf16_t*)y, P, H, W, C, relu);
   else
-    hipLaunchKernelGGL(dw_fwd<float>, g, dim3(256), 0, st, (const float*)x, (const float*)w, b,
+    TGP_LAUNCH(ps, dw_fwd<float>, g, dim3(256), 0, st, (const float*)x, (const float*)w, b,
                        (float*)y, P, H, W, C, relu);
   return hipGetLastError();
 }
@@ -596,10 +596,10 @@ hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int
   dim3 g(cdiv(P * C, 256));
   ProfScope ps("dw_dgrad", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
   if (dt == 0)
-    hipLaunchKernelGGL(dw_dgrad_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dz,
+    TGP_LAUNCH(ps, dw_dgrad_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dz,
                        (const bf16_t*)w, (bf16_t*)dx, P, H, W, C);
   else
-    hipLaunchKernelGGL(dw_dgrad_k<float>, g, dim3(256), 0, st, (const float*)dz,
+    TGP_LAUNCH(ps, dw_dgrad_k<float>, g, dim3(256), 0, st, (const float*)dz,
                        (const float*)w, (float*)dx, P, H, W, C);
   return hipGetLastError();
 }
@@ -619,10 +619,10 @@ hipError_t dw_wgrad(int dt, const void* x, const void* dz, float* dw, float* par
   {
   ProfScope ps("dw_wgrad", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C + 4.0 * S * E, st);
   if (dt == 0)
-    hipLaunchKernelGGL(dw_wgrad_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
+    TGP_LAUNCH(ps, dw_wgrad_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
                        (const bf16_t*)dz, partial, P, H, W, C, pps);
   else
-    hipLaunchKernelGGL(dw_wgrad_k<float>, g, dim3(256), 0, st, (const float*)x,
+    TGP_LAUNCH(ps, dw_wgrad_k<float>, g, dim3(256), 0, st, (const float*)x,
                        (const float*)dz, partial, P, H, W, C, pps);
   }
   hipError_t e = hipGetLastError();
@@ -637,10 +637,10 @@ hipError_t relu_backward(int dt, const void* dy, const void* dskip, const void* 
   dim3 g(cdiv(n, 256L * N));
   ProfScope ps("relu_backward", 0.0, (dt == 0 ? 2.0 : 4.0) * n * (3 + (dskip ? 1 : 0) - (relu ? 0 : 1)), st);
   if (dt == 0)
-    hipLaunchKernelGGL(relu_bwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dy,
+    TGP_LAUNCH(ps, relu_bwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dy,
                        (const bf16_t*)dskip, (const bf16_t*)y, (bf16_t*)dz, relu, n, vec);
   else
-    hipLaunchKernelGGL(relu_bwd_k<float>, g, dim3(256), 0, st, (const float*)dy,
+    TGP_LAUNCH(ps, relu_bwd_k<float>, g, dim3(256), 0, st, (const float*)dy,
                        (const float*)dskip, (const float*)y, (float*)dz, relu, n, vec);
   return hipGetLastError();
 }
@@ -682,11 +682,11 @@ hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const v
     ProfScope ps("relu_backward_bias", 0.0,
                  (dt == 0 ? 2.0 : 4.0) * P * C * (3 + (dskip ? 1 : 0) - (relu ? 0 : 1)) + 4.0 * nb * C, st);
     if (dt == 0)
-      hipLaunchKernelGGL(relu_bwd_bias_k<bf16_t>, dim3(nb), dim3(256), 0, st, (const bf16_t*)dy,
+      TGP_LAUNCH(ps, relu_bwd_bias_k<bf16_t>, dim3(nb), dim3(256), 0, st, (const bf16_t*)dy,
                          (const bf16_t*)dskip, (const bf16_t*)y, (bf16_t*)dz, partial, relu, P, C,
                          rows);
     else
-      hipLaunchKernelGGL(relu_bwd_bias_k<float>, dim3(nb), dim3(256), 0, st, (const float*)dy,
+      TGP_LAUNCH(ps, relu_bwd_bias_k<float>, dim3(nb), dim3(256), 0, st, (const float*)dy,
                          (const float*)dskip, (const float*)y, (float*)dz, partial, relu, P, C,
                          rows);
   }
@@ -703,9 +703,9 @@ hipError_t bias_grad(int dt, const void* dz, float* db, float* partial, long P, 
   {
   ProfScope ps("bias_colsum", 0.0, (dt == 0 ? 2.0 : 4.0) * P * C + 4.0 * nb * C, st);
   if (dt == 0)
-    hipLaunchKernelGGL(colsum_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dz, partial, P, C, rows);
+    TGP_LAUNCH(ps, colsum_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)dz, partial, P, C, rows);
   else
-    hipLaunchKernelGGL(colsum_k<float>, g, dim3(256), 0, st, (const float*)dz, partial, P, C, rows);
+    TGP_LAUNCH(ps, colsum_k<float>, g, dim3(256), 0, st, (const float*)dz, partial, P, C, rows);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -719,9 +719,9 @@ hipError_t maxpool_forward(int dt, const void* x, void* y, int nb, int H, int W,
   dim3 g(cdiv(total, 256));
   ProfScope ps("maxpool_forward", 0.0, (dt == 0 ? 2.0 : 4.0) * nb * H * W * C * 1.25, st);
   if (dt == 0)
-    hipLaunchKernelGGL(maxpool_fwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)y, nb, H, W, C);
+    TGP_LAUNCH(ps, maxpool_fwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)y, nb, H, W, C);
   else
-    hipLaunchKernelGGL(maxpool_fwd_k<float>, g, dim3(256), 0, st, (const float*)x, (float*)y, nb, H, W, C);
+    TGP_LAUNCH(ps, maxpool_fwd_k<float>, g, dim3(256), 0, st, (const float*)x, (float*)y, nb, H, W, C);
   return hipGetLastError();
 }
 
@@ -732,10 +732,10 @@ hipError_t maxpool_backward(int dt, const void* x, const void* dy, void* dx, int
   dim3 g(cdiv(total, 256));
   ProfScope ps("maxpool_backward", 0.0, (dt == 0 ? 2.0 : 4.0) * nb * H * W * C * 2.25, st);
   if (dt == 0)
-    hipLaunchKernelGGL(maxpool_bwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
+    TGP_LAUNCH(ps, maxpool_bwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x,
                        (const bf16_t*)dy, (bf16_t*)dx, nb, H, W, C);
   else
-    hipLaunchKernelGGL(maxpool_bwd_k<float>, g, dim3(256), 0, st, (const float*)x,
+    TGP_LAUNCH(ps, maxpool_bwd_k<float>, g, dim3(256), 0, st, (const float*)x,
                        (const float*)dy, (float*)dx, nb, H, W, C);
   return hipGetLastError();
 }
@@ -747,10 +747,10 @@ hipError_t upcat_forward(int dt, const void* prev, const void* skip, void* out, 
   dim3 g(cdiv(total, 256));
   ProfScope ps("upcat_forward", 0.0, (dt == 0 ? 2.0 : 4.0) * nb * H * W * (0.25 * C1 + C2 + C1 + C2), st);
   if (dt == 0)
-    hipLaunchKernelGGL(upcat_fwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)prev,
+    TGP_LAUNCH(ps, upcat_fwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)prev,
                        (const bf16_t*)skip, (bf16_t*)out, nb, H, W, C1, C2);
   else
-    hipLaunchKernelGGL(upcat_fwd_k<float>, g, dim3(256), 0, st, (const float*)prev,
+    TGP_LAUNCH(ps, upcat_fwd_k<float>, g, dim3(256), 0, st, (const float*)prev,
                        (const float*)skip, (float*)out, nb, H, W, C1, C2);
   return hipGetLastError();
 }
@@ -762,14 +762,14 @@ hipError_t upcat_backward(int dt, const void* dcat, void* dprev, void* dskip, in
   long P = (long)nb * H * W;
   ProfScope ps("upcat_backward", 0.0, (dt == 0 ? 2.0 : 4.0) * P * (C1 + 0.25 * C1 + 2.0 * C2), st);
   if (dt == 0) {
-    hipLaunchKernelGGL(upcat_bwd_prev_k<bf16_t>, dim3(cdiv(t1, 256)), dim3(256), 0, st,
+    TGP_LAUNCH(ps, upcat_bwd_prev_k<bf16_t>, dim3(cdiv(t1, 256)), dim3(256), 0, st,
                        (const bf16_t*)dcat, (bf16_t*)dprev, nb, H, W, C1, C2);
-    hipLaunchKernelGGL(upcat_bwd_skip_k<bf16_t>, dim3(cdiv(P * (C2 / N), 256)), dim3(256), 0, st,
+    TGP_LAUNCH(ps, upcat_bwd_skip_k<bf16_t>, dim3(cdiv(P * (C2 / N), 256)), dim3(256), 0, st,
                        (const bf16_t*)dcat, (bf16_t*)dskip, P, C1, C2);
   } else {
-    hipLaunchKernelGGL(upcat_bwd_prev_k<float>, dim3(cdiv(t1, 256)), dim3(256), 0, st,
+    TGP_LAUNCH(ps, upcat_bwd_prev_k<float>, dim3(cdiv(t1, 256)), dim3(256), 0, st,
                        (const float*)dcat, (float*)dprev, nb, H, W, C1, C2);
-    hipLaunchKernelGGL(upcat_bwd_skip_k<float>, dim3(cdiv(P * (C2 / N), 256)), dim3(256), 0, st,
+    TGP_LAUNCH(ps, upcat_bwd_skip_k<float>, dim3(cdiv(P * (C2 / N), 256)), dim3(256), 0, st,
                        (const float*)dcat, (float*)dskip, P, C1, C2);
   }
   return hipGetLastError();
@@ -786,10 +786,10 @@ hipError_t mse_forward_backward(int dt, const void* y, const void* t, void* dy,
   {
   ProfScope ps("mse", 3.0 * n, (dt == 0 ? 6.0 : 12.0) * n, st);
   if (dt == 0)
-    hipLaunchKernelGGL(mse_k<bf16_t>, dim3(nb), dim3(256), 0, st, (const bf16_t*)y,
+    TGP_LAUNCH(ps, mse_k<bf16_t>, dim3(nb), dim3(256), 0, st, (const bf16_t*)y,
                        (const bf16_t*)t, (bf16_t*)dy, partial, n, inv_numel, pb);
   else
-    hipLaunchKernelGGL(mse_k<float>, dim3(nb), dim3(256), 0, st, (const float*)y,
+    TGP_LAUNCH(ps, mse_k<float>, dim3(nb), dim3(256), 0, st, (const float*)y,
                        (const float*)t, (float*)dy, partial, n, inv_numel, pb);
   }
   hipError_t e = hipGetLastError();
@@ -814,13 +814,13 @@ hipError_t grad_accumulate_batch(const AccBatch& b, int overwrite, hipStream_t s
   }
   if (maxn == 0) return hipSuccess;
   ProfScope ps("grad_accumulate", 0.0, bytes, st);
-  hipLaunchKernelGGL(accumulate_multi_k, dim3(cdiv(maxn, 1024)), dim3(256), 0, st, b, overwrite);
+  TGP_LAUNCH(ps, accumulate_multi_k, dim3(cdiv(maxn, 1024)), dim3(256), 0, st, b, overwrite);
   return hipGetLastError();
 }
 
 hipError_t grad_accumulate(float* acc, const float* g, long n, int overwrite, hipStream_t st) {
   ProfScope ps("grad_accumulate", (double)n, (overwrite ? 8.0 : 12.0) * n, st);
-  hipLaunchKernelGGL(accumulate_k, dim3(cdiv(n, 1024)), dim3(256), 0, st, acc, g, n, overwrite);
+  TGP_LAUNCH(ps, accumulate_k, dim3(cdiv(n, 1024)), dim3(256), 0, st, acc, g, n, overwrite);
   return hipGetLastError();
 }
 

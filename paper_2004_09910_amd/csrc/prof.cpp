@@ -13,6 +13,7 @@ struct Rec {
   std::string name;
   double flops, bytes;
   hipEvent_t a, b;
+  bool launched;
 };
 
 struct State {
@@ -37,17 +38,18 @@ thread_local State g;
 
 bool prof_enabled() { return g.on; }
 
-ProfScope::ProfScope(const char* name, double flops, double bytes, hipStream_t st) : st_(st) {
+ProfScope::ProfScope(const char* name, double flops, double bytes, hipStream_t) {
   if (!g.on) return;
   hipEvent_t a = g.get(), b = g.get();
   if (!a || !b) return;
-  hipEventRecord(a, st);
-  g.recs.push_back({name, flops, bytes, a, b});
+  g.recs.push_back({name, flops, bytes, a, b, false});
   rec_ = (int)g.recs.size() - 1;
 }
 
-ProfScope::~ProfScope() {
-  if (rec_ >= 0) hipEventRecord(g.recs[rec_].b, st_);
+hipEvent_t ProfScope::start_event() const { return rec_ >= 0 ? g.recs[rec_].a : nullptr; }
+hipEvent_t ProfScope::stop_event() const { return rec_ >= 0 ? g.recs[rec_].b : nullptr; }
+void ProfScope::mark_launched() {
+  if (rec_ >= 0) g.recs[rec_].launched = true;
 }
 
 }  // namespace tgpk
@@ -74,6 +76,11 @@ tgp_status tgp_profile_read(tgp_kernel_stat* out, int cap, int* count) {
   if (!count) return TGP_EINVAL;
   std::vector<tgp_kernel_stat> agg;
   for (auto& r : g.recs) {
+    if (!r.launched) {   // a scope that launched nothing (early return)
+      g.pool.push_back(r.a);
+      g.pool.push_back(r.b);
+      continue;
+    }
     if (hipEventSynchronize(r.b) != hipSuccess) return TGP_EHIP;
     float ms = 0.f;
     if (hipEventElapsedTime(&ms, r.a, r.b) != hipSuccess) return TGP_EHIP;
