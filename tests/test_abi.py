@@ -9,6 +9,8 @@ import re
 
 import pytest
 
+import golden_data
+
 import paper_2004_09910_amd as tgp
 from oracle import pipeline as opipe
 from paper_2004_09910_amd.harness import layer_tuple
@@ -54,12 +56,14 @@ def test_schedule_trace_follows_clock_cycle(m, n, mode):
 
 
 def test_schedule_trace_m4_n3_written_out():
+    """The library's clock order for m=4, n=3 (except-last) against the
+    hand-written fixture tests/golden/clock_cycle_m4_n3.txt (Algorithm 1)."""
+    g = golden_data.clock_cycle()
     ops = tgp.schedule_trace(4, 3, 1)   # except-last
-    want_f = [(1, 1), (2, 1), (1, 2), (3, 1), (2, 2), (1, 3), (4, 1), (3, 2), (2, 3), (4, 2),
-              (3, 3), (4, 3)]
-    assert [(i, j) for op, i, j in ops if op == tgp.OP_FORWARD] == want_f
+    assert [(i, j) for op, i, j in ops if op == tgp.OP_FORWARD] == \
+        [t for c in g["FORWARD"] for t in c]
     assert [(i, j) for op, i, j in ops if op == tgp.OP_RECOMPUTE] == \
-        [(3, 3), (2, 3), (3, 2), (1, 3), (2, 2), (3, 1), (1, 2), (2, 1), (1, 1)]
+        [t for c in g["RECOMPUTE_EXCEPT_LAST"] for t in c]
 
 
 def _brute_balance(cost, n):

@@ -4,6 +4,8 @@ micro-batch gradient-sum and recompute invariants of Sec. 2 / Sec. 2.1, and
 the clock-cycle order of Algorithm 1."""
 import numpy as np
 import pytest
+
+import golden_data
 import torch
 import torch.nn.functional as F
 
@@ -242,17 +244,10 @@ def test_pipeline_trace_policies():
 
 def test_forward_clocks_match_algorithm1_m4_n3():
     """Clock k runs every F_{i,j} with i + j - 1 = k (Algorithm 1; m=4, n=3 as
-    in Fig. 1), written out by hand."""
-    want = [[(1, 1)],
-            [(2, 1), (1, 2)],
-            [(3, 1), (2, 2), (1, 3)],
-            [(4, 1), (3, 2), (2, 3)],
-            [(4, 2), (3, 3)],
-            [(4, 3)]]
-    assert pipeline.forward_clocks(4, 3) == want
-    bw = [t for c in pipeline.backward_clocks(4, 3) for t in c]
-    assert bw == [(4, 3), (3, 3), (4, 2), (2, 3), (3, 2), (4, 1), (1, 3), (2, 2), (3, 1),
-                  (1, 2), (2, 1), (1, 1)]
+    in Fig. 1): the hand-written fixture tests/golden/clock_cycle_m4_n3.txt."""
+    g = golden_data.clock_cycle()
+    assert pipeline.forward_clocks(4, 3) == g["FORWARD"]
+    assert pipeline.backward_clocks(4, 3) == g["BACKWARD"]
 
 
 @pytest.mark.parametrize("m", range(1, 9))
