@@ -34,7 +34,7 @@ def round_bf16(a: np.ndarray) -> np.ndarray:
 # bit flip, and each flip moves a whole upstream gradient element).
 
 _CONTRACT = ["f64"]
-CONTRACTIONS = ("f64", "f32", "f32rev", "f32split")
+CONTRACTIONS = ("f64", "f32", "f32rev", "f32split", "f32c32")
 
 
 class contraction:
@@ -42,8 +42,11 @@ class contraction:
     'f64'      float64 (every parity reference);
     'f32'      float32 operands and accumulation;
     'f32rev'   float32 with the contracted channel order reversed;
-    'f32split' float32 in two halves of the channels, added at the end.
-    The three float32 variants are equally valid ways to evaluate the same
+    'f32split' float32 in two halves of the channels, added at the end;
+    'f32c32'   float32 in blocks of 32 channels, the block sums added one by
+               one in channel order (the blocking of a K loop that contracts
+               32 channels per step).
+    The float32 variants are equally valid ways to evaluate the same
     bf16-storage network; the spread among them and the float64 reference
     measures how many ReLU / pool decisions are within rounding distance of
     flipping."""
@@ -70,6 +73,15 @@ def _td(a, b, axes):
     if mode == "f32rev":
         a = np.flip(a, axis=k)
         b = np.flip(b, axis=ax_b[0])
+    if mode == "f32c32" and a.shape[k] > 32:
+        out = None
+        for c0 in range(0, a.shape[k], 32):
+            sa = [slice(None)] * a.ndim
+            sb = [slice(None)] * b.ndim
+            sa[k], sb[ax_b[0]] = slice(c0, c0 + 32), slice(c0, c0 + 32)
+            t = np.tensordot(a[tuple(sa)], b[tuple(sb)], axes=axes)
+            out = t if out is None else out + t
+        return out
     if mode == "f32split" and a.shape[k] > 1:
         h = a.shape[k] // 2
         sa = [slice(None)] * a.ndim

@@ -17,27 +17,16 @@
 // kernel sums the splits in fixed order (deterministic, no atomics).
 #include "common.h"
 #include "kernels.h"
+#include "mfma_util.h"
 #include "prof.h"
 
 namespace tgpk {
 namespace {
 
-typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef float f32x16_t __attribute__((ext_vector_type(16)));
-// 16-byte chunk as a native vector (HIP's u32x4 wraps a union that keeps
-// arrays of it out of registers)
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
 // XOR swizzle of the eight 16-byte chunks of a 128-byte LDS row, so that
 // eight consecutive rows read at the same logical chunk, and rows eight apart
 // written at the same chunk, hit distinct banks.
 __device__ __forceinline__ int swz(int row, int q) { return q ^ ((row ^ (row >> 3)) & 7); }
-
-__device__ __forceinline__ bf16x8_t as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8_t, v); }
-
-__device__ __forceinline__ f32x16_t mfma32(bf16x8_t a, bf16x8_t b, f32x16_t c) {
-  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-}
 
 // Global -> register prefetch of one 64-wide K step of the forward GEMM:
 // A = weight rows (16-byte chunk q of each of A_CH rows), B = im2col rows
@@ -196,40 +185,12 @@ __global__ __launch_bounds__(256) void conv_fwd_mfma(
 // direct global -> LDS copies.
 __device__ __attribute__((aligned(16))) unsigned int g_zero16[4];
 
-#define TGP_LDS(p) ((__attribute__((address_space(3))) void*)(p))
-
-// s_waitcnt with only the vector-memory counter limited to N (gfx9 encoding:
-// vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt left at their maxima).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x70 | 0xF00);
-}
-
-// Waits until at most `ahead` stages of LPS loads each are still in flight.
-template <int NS, int LPS>
-__device__ __forceinline__ void wait_stages(int ahead) {
-  if constexpr (NS >= 4) {
-    if (ahead >= 2) { wait_vmcnt<2 * LPS>(); return; }
-  }
-  if constexpr (NS >= 3) {
-    if (ahead >= 1) { wait_vmcnt<LPS>(); return; }
-  }
-  wait_vmcnt<0>();
-}
-
 // Implicit-GEMM forward with an NS-stage ring of LDS tiles filled by
 // global_load_lds_dwordx4: each wave instruction copies 8 rows of 128 bytes;
 // lane l fills physical chunk l & 7 of row l >> 3 with the logical chunk that
 // the XOR swizzle puts there.  Loads run NS - 1 K steps ahead of the MFMAs.
-// Block index remapped so that consecutive pixel tiles (which share halo
-// rows and read the same weights) run on the same XCD: the dispatcher deals
-// blocks round-robin over the 8 XCDs, each with its own L2.
-__device__ __forceinline__ int xcd_remap(int bid, int nb) {
-  const int per = nb / 8, rem = nb % 8;
-  const int x = bid % 8, i = bid / 8;
-  return x < rem ? x * (per + 1) + i : rem * (per + 1) + (x - rem) * per + i;
-}
+// Block index remapped (xcd_remap) so that consecutive pixel tiles, which
+// share halo rows and read the same weights, run on the same XCD.
 
 template <int WCO, int WP, int TM, int TN, int TAPS, int NS>
 __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_dma(
@@ -601,16 +562,6 @@ __global__ __launch_bounds__(256) void conv_rows_epilogue(const float* __restric
 
 // ---------------------------------------------------------------- forward, persistent row-stage 3x3
 
-// 16 bytes per lane from a buffer into LDS (lane l -> dst + 16 l).  A byte
-// offset voff at or past the buffer's size (negative ones included, read as
-// unsigned) yields zeros.  Kept out of line of the kernel templates: the
-// host pass drops a kernel template instantiation that calls this builtin
-// directly.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, __attribute__((address_space(3))) void* dst,
-                                      int voff, int soff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
-}
-
 // XOR swizzle of the four 16-byte chunks of a 64-byte LDS row: eight
 // consecutive rows read at one logical chunk land on eight distinct 16-byte
 // slots of a 128-byte bank cycle.
@@ -665,10 +616,8 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_rows_pers(
   // Buffer descriptors: a byte offset at or past the end (or negative, read
   // as unsigned) returns zeros, which is the zero padding of pixels outside
   // [0, P).  Sizes are below 2^31 (checked by the launcher).
-  const __amdgpu_buffer_rsrc_t rx =
-      __builtin_amdgcn_make_buffer_rsrc((void*)X, (short)0, P * Cin * 2, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rw =
-      __builtin_amdgcn_make_buffer_rsrc((void*)Wt, (short)0, Cout * 9 * Cin * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X, P * Cin * 2);
+  const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wt, Cout * 9 * Cin * 2);
 
   // Per-lane byte offsets of the rows this lane fills (loop invariant).
   // Weight row of instruction u < LA: channel co (within the tile), column
@@ -1242,6 +1191,10 @@ hipError_t launch_rows_pers(const char* name_f, const char* name_t, const bf16_t
       P, s, relu, S, st)
 
 int g_fwd_split = 0;   // > 0 forces the split count (measurement only)
+// Measurement only: bit 0 allows the row-tiled kernel for forward calls, bit
+// 1 for data-gradient calls.
+int g_rowtile_mask = 3;
+thread_local int t_in_dgrad = 0;
 
 struct FwdPlan {
   int cfg;   // 1..: row-stage configurations; 100+: per-tap; 200+: persistent row-stage
@@ -1269,17 +1222,26 @@ PersTile pers_tile(int cfg) {
 FwdPlan fwd_plan(const ConvShape& s) {
   const long P = 4L * s.H * s.W;
   FwdPlan pl{0, 1};
-  // Measured per shape: the persistent row-stage kernel wins on the deep,
-  // small-image layers (few pixel tiles, long K); the per-tap kernel, with
-  // several small blocks per CU, on the large images.
-  if (s.taps == 9 && s.cin % 64 == 0 && P <= 4096) {
+  // Measured per shape (3x3, b = 4, kernel time in a stage step): the
+  // row-tiled kernel is fastest on images of 96 x 96 and up; the persistent
+  // row-stage kernel with split K on the small, deep layers (few pixel tiles,
+  // long K); the per-tap kernel in between.
+  const bool k3 = s.taps == 9 && s.cin % 64 == 0;
+  if (k3 && (long)s.H * s.W >= 96 * 96 && conv_rowtile_ok(s) &&
+      (g_rowtile_mask >> (t_in_dgrad ? 1 : 0) & 1)) {
+    pl.cfg = 300;  // row-tiled 16x16x32
+  } else if (k3 && P <= 4096) {
     pl.cfg = 203;  // persistent row-stage, 64 x 256
-  } else if (s.taps == 9 && s.cin % 64 == 0 && P <= 16384 && s.cin >= 256 && s.cout % 128 == 0) {
+  } else if (k3 && P <= 16384 && s.cin >= 256 && s.cout % 128 == 0) {
     pl.cfg = 207;  // persistent row-stage, 128 x 256, 8 waves
   } else {
     pl.cfg = 100;
   }
   if (g_fwd_variant > 0) pl.cfg = g_fwd_variant;
+  if (pl.cfg >= 300) {
+    if (!conv_rowtile_ok(s)) pl.cfg = 100;
+    return pl;
+  }
   if ((pl.cfg == 2 || pl.cfg == 5) && s.cout % 128) pl.cfg = pl.cfg == 2 ? 1 : 3;  // 128-wide tiles need cout % 128 == 0
   if (pl.cfg >= 200) {
     if (s.taps != 9 || s.cin % 32) { pl.cfg = 100; return pl; }
@@ -1315,7 +1277,7 @@ FwdPlan fwd_plan(const ConvShape& s) {
 size_t conv_forward_partial_floats(int dt, const ConvShape& s) {
   if (!mfma_conv_ok(dt, s.cin, s.cout)) return 0;
   FwdPlan pl = fwd_plan(s);
-  const bool splits = pl.cfg < 100 || pl.cfg >= 200;   // the per-tap kernels never split
+  const bool splits = pl.cfg < 100 || (pl.cfg >= 200 && pl.cfg < 300);   // per-tap and row-tiled never split
   return splits && pl.S > 1 ? (size_t)pl.S * s.pixels() * s.cout : 0;
 }
 
@@ -1328,6 +1290,12 @@ hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void*
   bf16_t* Y = (bf16_t*)y;
   const FwdPlan pl = fwd_plan(s);
   const bool wide = s.cout % 128 == 0;
+  if (pl.cfg >= 300) {
+    g_rowtile_cfg = pl.cfg >= 301 ? pl.cfg - 301 : -1;
+    const hipError_t e = conv_forward_rowtile(x, w, b, y, s, relu, st);
+    g_rowtile_cfg = -1;
+    return e;
+  }
   switch (pl.cfg) {
     case 1: return TGP_ROWS_CFG(1, 4, 2, 2, 2, pl.S);                 // 64 x 256, 4 waves
     case 2: return wide ? TGP_ROWS_CFG(2, 2, 2, 2, 2, pl.S)           // 128 x 128, 4 waves

@@ -532,7 +532,10 @@ hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, voi
                       const ConvShape& s, float* part, size_t part_cap, hipStream_t st) {
   if (conv_dgrad_uses_wt(dt, s)) {
     ConvShape t{s.nb, s.H, s.W, s.cout, s.cin, s.taps};
-    return conv_forward_mfma(dz, wt, nullptr, dx, t, 0, part, part_cap, st);
+    t_in_dgrad = 1;
+    const hipError_t e = conv_forward_mfma(dz, wt, nullptr, dx, t, 0, part, part_cap, st);
+    t_in_dgrad = 0;
+    return e;
   }
   long P = s.pixels();
   dim3 g(cdiv(P * s.cin, 256));

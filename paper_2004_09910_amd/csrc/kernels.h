@@ -21,6 +21,17 @@ size_t conv_forward_partial_floats(int dt, const ConvShape& s);
 hipError_t conv_forward(int dt, const void* x, const void* w, const float* b, void* y,
                         const ConvShape& s, int relu, float* part, size_t part_cap,
                         hipStream_t st);
+// 16x16x32-MFMA 3x3 convolution on row-aligned tiles (bf16; Cin % 32 == 0,
+// Cout % 64 == 0, Cout <= 1024): whether it supports a shape, and the launch
+// (y = act(conv(x, w) + b), or the data gradient when given the transformed
+// weight and no bias).
+bool conv_rowtile_ok(const ConvShape& s);
+hipError_t conv_forward_rowtile(const void* x, const void* w, const float* b, void* y,
+                                const ConvShape& s, int relu, hipStream_t st);
+extern int g_rowtile_cfg;
+extern int g_rowtile_mask;
+extern thread_local int t_in_dgrad;
+
 // Whether the data-gradient kernel for this shape reads the transformed
 // weight wt = [cin][taps][cout] (taps rotated by 180 degrees).
 bool conv_dgrad_uses_wt(int dt, const ConvShape& s);

@@ -471,6 +471,7 @@ namespace tgpk {
 extern int g_fwd_variant;
 extern int g_fwd_order;
 extern int g_fwd_split;
+extern int g_rowtile_mask;
 }
 
 extern "C" {
@@ -487,6 +488,11 @@ int tgp_debug_set_fwd_variant(int v) {
 int tgp_debug_set_fwd_split(int v) {
   int old = tgpk::g_fwd_split;
   tgpk::g_fwd_split = v;
+  return old;
+}
+int tgp_debug_set_rowtile_mask(int v) {
+  int old = tgpk::g_rowtile_mask;
+  tgpk::g_rowtile_mask = v;
   return old;
 }
 int tgp_debug_set_fwd_order(int v) {

@@ -110,7 +110,7 @@ def oracle_stage(net, dtype, lo, hi, xv, G, samples=None, stash_in=None):
                        stash_in=st)
 
 
-ALTS = ("f32", "f32rev", "f32split")
+ALTS = ("f32", "f32rev", "f32split", "f32c32")
 
 
 def oracle_stage_variants(net, dtype, lo, hi, xv, G, samples=None, stash_in=None):
