@@ -37,7 +37,10 @@ def log(*a):
 # bench reports its traffic only while the sources are unchanged.
 PROFILES = os.path.join(HERE, "profiles")
 KERNEL_SOURCES = ["paper_2004_09910_amd/csrc/conv_mfma.hip",
+                  "paper_2004_09910_amd/csrc/conv_rowtile.hip",
+                  "paper_2004_09910_amd/csrc/wgrad_rows.hip",
                   "paper_2004_09910_amd/csrc/elementwise.hip",
+                  "paper_2004_09910_amd/csrc/mfma_util.h",
                   "paper_2004_09910_amd/csrc/common.h"]
 PROFILE_COMMANDS = {
     "trace": "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_kt -o kt "

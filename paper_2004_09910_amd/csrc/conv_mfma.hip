@@ -1193,7 +1193,7 @@ hipError_t launch_rows_pers(const char* name_f, const char* name_t, const bf16_t
 int g_fwd_split = 0;   // > 0 forces the split count (measurement only)
 // Measurement only: bit 0 allows the row-tiled kernel for forward calls, bit
 // 1 for data-gradient calls.
-int g_rowtile_mask = 3;
+int g_rowtile_mask = 7;
 thread_local int t_in_dgrad = 0;
 
 struct FwdPlan {
@@ -1338,7 +1338,13 @@ hipError_t weight_transform(int dt, const void* w, void* wt, int cout, int cin, 
   return hipGetLastError();
 }
 
+// Bit 2 of g_rowtile_mask selects the row-blocked weight-gradient kernel.
+static bool use_wgrad_rows(const ConvShape& s) {
+  return (g_rowtile_mask >> 2 & 1) && wgrad_rows_ok(s);
+}
+
 size_t wgrad_mfma_partial_floats(const ConvShape& s) {
+  if (use_wgrad_rows(s)) return wgrad_rows_partial_floats(s);
   int tiles = s.taps * (s.cin / 64) * (s.cout / 64);
   if (s.cin % 128 == 0 && s.cout % 128 == 0) tiles = s.taps * (s.cin / 128) * (s.cout / 128);
   long E = (long)s.cout * s.taps * s.cin;
@@ -1348,6 +1354,7 @@ size_t wgrad_mfma_partial_floats(const ConvShape& s) {
 
 hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
                            const ConvShape& s, hipStream_t st) {
+  if (use_wgrad_rows(s)) return conv_wgrad_rows_launch(x, dz, dw, partial, s, st);
   long P = s.pixels();
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* DZ = (const bf16_t*)dz;

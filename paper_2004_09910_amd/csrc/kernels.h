@@ -31,6 +31,16 @@ hipError_t conv_forward_rowtile(const void* x, const void* w, const float* b, vo
 extern int g_rowtile_cfg;
 extern int g_rowtile_mask;
 extern thread_local int t_in_dgrad;
+// Row-blocked 3x3 weight gradient on 32x32x16 MFMA with transpose LDS reads
+// (bf16; W in {48, 96, 192}, Cin and Cout multiples of 64): whether it
+// supports a shape, the fp32 partial-slice scratch it needs, and the launch
+// (dw = sum over pixels, summed over its K ranges in a fixed order).
+// out[e] = sum_{k < S} part[k E + e] in the order k = 0, 1, ..
+hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st);
+bool wgrad_rows_ok(const ConvShape& s);
+size_t wgrad_rows_partial_floats(const ConvShape& s);
+hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
+                                  const ConvShape& s, hipStream_t st);
 
 // Whether the data-gradient kernel for this shape reads the transformed
 // weight wt = [cin][taps][cout] (taps rotated by 180 degrees).

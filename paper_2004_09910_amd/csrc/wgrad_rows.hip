@@ -1,0 +1,281 @@
+// bf16 3x3 weight gradient on 32 x 32 x 16 MFMA, operands read from LDS
+// with the gfx950 transpose loads.
+//
+// dW[co][r][s][ci] = sum_p dZ[p][co] X[p + (r - 1) W + (s - 1)][ci]: a GEMM
+// with M = co, N = ci, K = pixels, one per tap.  Both operands live in
+// NHWC, where a pixel's channels are contiguous but an MFMA fragment needs
+// 8 consecutive pixels of one channel; ds_read_b64_tr_b16 gathers exactly
+// that from pixel-major LDS rows, so the tiles go global -> LDS by buffer
+// DMA and are never transposed in registers.
+//
+// A work item is (K range, filter row r, 64 output channels, 64 input
+// channels): it accumulates the three column taps s = 0..2 of filter row r
+// over the K range, a block of whole image rows of one sample.  A stage
+// holds RPS image rows h.. of dZ (RPS W pixels) and the RPS input rows
+// h + r - 1.. each padded with a zero pixel on either side (in a block of
+// W + 4 LDS rows, so every block starts at a multiple of 4 rows), so tap s
+// of pixel (h, w) reads padded row w + s; the padding pixels and rows outside the image are
+// buffer reads at out-of-range offsets and hold zeros.  Rows are 64 channels
+// (128 bytes) with their 16-byte chunks XOR-swizzled by 2 (row & 3), which
+// keeps the transpose reads of four consecutive rows on distinct banks.
+//
+// Each wave owns a 32 x 32 (co x ci) quarter of the item for all three
+// taps.  Blocks are persistent over items, their stages streamed through
+// one NS-deep LDS ring.  Each item writes its fp32 partial dW slice for its
+// K range; the slices are summed in K-range order by splitk_reduce (or, with
+// one K range, the item writes dW directly).  The summation order is fixed
+// by the shape.
+#include "common.h"
+#include "kernels.h"
+#include "mfma_util.h"
+#include "prof.h"
+
+namespace tgpk {
+namespace {
+
+constexpr int WG_OOB = (int)0x80000000;
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// Transpose read: within each group of 16 lanes, lane i receives element
+// i % 4 of the 8-byte blocks addressed by lanes 4 e + i / 4, e = 0..3.
+__device__ __forceinline__ s16x4 tr16(const unsigned char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)TGP_LDS(p));
+}
+
+__device__ __forceinline__ bf16x8_t frag2(s16x4 lo, s16x4 hi) {
+  const u32x4 v = {__builtin_bit_cast(unsigned, (short __attribute__((ext_vector_type(2)))){lo[0], lo[1]}),
+                   __builtin_bit_cast(unsigned, (short __attribute__((ext_vector_type(2)))){lo[2], lo[3]}),
+                   __builtin_bit_cast(unsigned, (short __attribute__((ext_vector_type(2)))){hi[0], hi[1]}),
+                   __builtin_bit_cast(unsigned, (short __attribute__((ext_vector_type(2)))){hi[2], hi[3]})};
+  return as_bf16x8(v);
+}
+
+constexpr int round32(int v) { return (v + 31) / 32 * 32; }
+
+template <int W, int RPS, int NS>
+__global__ __launch_bounds__(256) void conv_wgrad_rows(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ dZ, float* __restrict__ out,
+    int nb, int H, int Cin, int Cout, int R) {
+  constexpr int AR = round32(RPS * W);          // dZ rows per stage
+  constexpr int BW = W + 4;                     // LDS rows per padded input row
+  constexpr int BR = round32(RPS * BW);         // padded X rows per stage
+  constexpr int SB = (AR + BR) * 128;           // stage bytes
+  constexpr int LA = AR / 32, LB = BR / 32;     // DMA instructions per wave
+  constexpr int KS = W / 16;                    // k steps per image row
+  static_assert(W % 16 == 0, "k steps within an image row");
+  __shared__ __attribute__((aligned(16))) unsigned char smem[NS * SB];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int cw = wave >> 1, nw = wave & 1;      // this wave's co / ci halves
+  const int nct = Cout / 64, ncit = Cin / 64;
+  const int nrb = (H + R - 1) / R;
+  const int per_k = 3 * nct * ncit;             // items per K range
+  const int items = nb * nrb * per_k;
+  const int G = gridDim.x;
+  const int lb = xcd_remap(blockIdx.x, G);
+  const int n_items = lb < items ? (items - lb + G - 1) / G : 0;
+  const long E = (long)Cout * 9 * Cin;
+  const int spr = (R + RPS - 1) / RPS;          // stages per full row block
+
+  const __amdgpu_buffer_rsrc_t rz = make_rsrc(dZ, nb * H * W * Cout * 2);
+  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X, nb * H * W * Cin * 2);
+
+  // DMA lane constants: instruction u of this wave fills rows (4 u + wave) * 8
+  // + lane / 8 of the A (u < LA) or B region, physical chunk lane % 8, which
+  // holds logical chunk (lane % 8) ^ (2 (row & 3)).
+  int aoff[LA], arow[LA], boff[LB], brow[LB];
+#pragma unroll
+  for (int u = 0; u < LA + LB; ++u) {
+    const int row = (u < LA ? u : u - LA) * 32 + wave * 8 + (lane >> 3);
+    const int lc = (lane & 7) ^ (2 * (row & 3));
+    if (u < LA) {
+      const int rr = row / W, w = row - rr * W;
+      const bool ok = row < RPS * W;
+      aoff[u < LA ? u : 0] = ok ? ((rr * W + w) * Cout + 8 * lc) * 2 : WG_OOB;
+      arow[u < LA ? u : 0] = ok ? rr : -1;
+    } else {
+      const int rr = row / BW, q = row - rr * BW;
+      const bool ok = rr < RPS && q >= 1 && q <= W;
+      boff[u < LA ? 0 : u - LA] = ok ? ((rr * W + q - 1) * Cin + 8 * lc) * 2 : WG_OOB;
+      brow[u < LA ? 0 : u - LA] = ok ? rr : -1;
+    }
+  }
+
+  // Fragment lane constants (byte offsets in a stage).  Lane group g = lane /
+  // 16 holds MFMA rows / columns 16 (g % 2) .. + 15 and k 8 (g / 2) .. + 7;
+  // lane j = lane % 16 addresses pixel k + j / 4, channels + 4 (j % 4).
+  const int g = lane >> 4, j = lane & 15;
+  const int kb = 8 * (g >> 1) + (j >> 2);
+  const int cha = (cw * 32 + 16 * (g & 1) + 4 * (j & 3)) * 2;   // byte within a row
+  const int chb = (nw * 32 + 16 * (g & 1) + 4 * (j & 3)) * 2;
+  const int fa = kb * 128 + (((cha >> 4) ^ (2 * (kb & 3))) << 4) + (cha & 15);
+  int fb[3];
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+    fb[s] = AR * 128 + (kb + s) * 128 + (((chb >> 4) ^ (2 * ((kb + s) & 3))) << 4) + (chb & 15);
+
+  auto coords = [&](int it, int& kr, int& r, int& co0, int& ci0) __attribute__((always_inline)) {
+    const int item = lb + it * G;
+    kr = item / per_k;
+    int t = item - kr * per_k;
+    r = t / (nct * ncit);
+    t -= r * nct * ncit;
+    co0 = (t / ncit) * 64;
+    ci0 = (t % ncit) * 64;
+  };
+  auto stages_of = [&](int kr) __attribute__((always_inline)) {
+    const int rb = kr % nrb;
+    const int rows = min(R, H - rb * R);
+    return (rows + RPS - 1) / RPS;
+  };
+
+  // issue side
+  int i_it = 0, i_st = 0, i_kr = 0, i_r = 0, i_co0 = 0, i_ci0 = 0, i_ns = 0;
+  if (n_items > 0) {
+    coords(0, i_kr, i_r, i_co0, i_ci0);
+    i_ns = stages_of(i_kr);
+  }
+  auto issue = [&](int slot) __attribute__((always_inline)) {
+    const int n = i_kr / nrb, rb = i_kr - n * nrb;
+    const int h = rb * R + i_st * RPS;                       // first image row of the stage
+    const int zsoff = (((n * H + h) * W) * Cout + i_co0) * 2;
+    const int hb = h + i_r - 1;                              // input row of stage row 0
+    const int xsoff = (((n * H + hb) * W) * Cin + i_ci0) * 2;
+#pragma unroll
+    for (int u = 0; u < LA + LB; ++u) {
+      auto* dst = TGP_LDS(smem + slot * SB + (u < LA ? u * 32 : AR + (u - LA) * 32) * 128 + wave * 1024);
+      if (u < LA) {
+        const int k = u < LA ? u : 0;
+        const bool ok = arow[k] >= 0 && h + arow[k] < H;
+        dma16(rz, dst, ok ? aoff[k] + zsoff : WG_OOB, 0);
+      } else {
+        const int k = u < LA ? 0 : u - LA;
+        const bool ok = brow[k] >= 0 && (unsigned)(hb + brow[k]) < (unsigned)H && h + brow[k] < H;
+        // the row offset can be negative for filter row 0 (rows above are
+        // out of range there), so it goes into the per-lane offset
+        dma16(rx, dst, ok ? boff[k] + xsoff : WG_OOB, 0);
+      }
+    }
+    if (++i_st == i_ns) {
+      i_st = 0;
+      if (++i_it < n_items) {
+        coords(i_it, i_kr, i_r, i_co0, i_ci0);
+        i_ns = stages_of(i_kr);
+      }
+    }
+  };
+
+  // total stages of this block
+  int total = 0;
+  for (int it = 0; it < n_items; ++it) {
+    int kr, r, co0, ci0;
+    coords(it, kr, r, co0, ci0);
+    total += stages_of(kr);
+  }
+
+#pragma unroll
+  for (int k = 0; k < NS - 1; ++k)
+    if (k < total) issue(k);
+
+  int idx = 0;
+  for (int c_it = 0; c_it < n_items; ++c_it) {
+    int kr, r, co0, ci0;
+    coords(c_it, kr, r, co0, ci0);
+    const int ns = stages_of(kr);
+    f32x16_t acc[3] = {f32x16_t{}, f32x16_t{}, f32x16_t{}};
+    for (int st = 0; st < ns; ++st, ++idx) {
+      // loads complete in order: stage idx is in once at most the stages
+      // issued after it are pending (epilogue stores only lengthen this wait)
+      wait_stages<NS, LA + LB>(min(NS - 2, total - 1 - idx));
+      __builtin_amdgcn_s_barrier();
+      if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);
+      const unsigned char* sp = smem + (idx % NS) * SB;
+#pragma unroll
+      for (int rr = 0; rr < RPS; ++rr) {
+#pragma unroll
+        for (int t = 0; t < KS; ++t) {
+          // k step: pixels 16 t .. 16 t + 15 of stage row rr
+          const int ka = (rr * W + 16 * t) * 128;
+          const int kx = (rr * BW + 16 * t) * 128;
+          const bf16x8_t a = frag2(tr16(sp + fa + ka), tr16(sp + fa + ka + 4 * 128));
+          bf16x8_t b[3];
+#pragma unroll
+          for (int s = 0; s < 3; ++s)
+            b[s] = frag2(tr16(sp + fb[s] + kx), tr16(sp + fb[s] + kx + 4 * 128));
+#pragma unroll
+          for (int s = 0; s < 3; ++s) acc[s] = mfma32(a, b[s], acc[s]);
+        }
+      }
+    }
+    // epilogue: element v of lane l is co 8 (v / 4) + 4 (l / 32) + v % 4, ci
+    // l % 32 of this wave's quarter
+    float* o = out + (long)kr * E;
+    const int ci = ci0 + nw * 32 + (lane & 31);
+#pragma unroll
+    for (int s = 0; s < 3; ++s)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int co = co0 + cw * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        o[((long)co * 9 + 3 * r + s) * Cin + ci] = acc[s][v];
+      }
+  }
+}
+
+struct WgPlan { int R, nK; };
+
+}  // namespace
+
+// Rows per K range: the fewest (a multiple of the rows per stage) that keep
+// the item count within one wave of 256 blocks.
+static WgPlan wgrad_rows_plan(const ConvShape& s) {
+  const long per_k = 3L * (s.cout / 64) * (s.cin / 64);
+  const int rps = s.W >= 192 ? 1 : (s.W >= 96 ? 2 : 4);
+  int R = rps;
+  while (R < s.H && (long)s.nb * ((s.H + R - 1) / R) * per_k > 256) R += rps;
+  if (R > s.H) R = s.H;
+  return {R, s.nb * ((s.H + R - 1) / R)};
+}
+
+bool wgrad_rows_ok(const ConvShape& s) {
+  return s.taps == 9 && (s.W == 192 || s.W == 96 || s.W == 48) && s.cin % 64 == 0 &&
+         s.cout % 64 == 0 && (double)s.pixels() * (s.cin > s.cout ? s.cin : s.cout) * 2 < 2147483648.0;
+}
+
+size_t wgrad_rows_partial_floats(const ConvShape& s) {
+  const WgPlan p = wgrad_rows_plan(s);
+  return p.nK > 1 ? (size_t)p.nK * s.cout * 9 * s.cin : 0;
+}
+
+template <int W, int RPS>
+static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* DZ, float* out,
+                                    const ConvShape& s, const WgPlan& p, hipStream_t st) {
+  const long items = (long)p.nK * 3 * (s.cout / 64) * (s.cin / 64);
+  const int G = (int)(items < 256 ? items : 256);
+  const double flops = 2.0 * s.pixels() * s.cout * 9 * s.cin;
+  const double bytes = 2.0 * s.pixels() * (s.cin + s.cout) + 4.0 * p.nK * s.cout * 9 * s.cin;
+  static const char* names[] = {"conv_wgrad_rows<192,1,3>", "conv_wgrad_rows<96,2,3>",
+                                "conv_wgrad_rows<48,4,3>"};
+  ProfScope ps(names[W == 192 ? 0 : (W == 96 ? 1 : 2)], flops, bytes, st);
+  TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, 3>), dim3(G), dim3(256), 0, st, X, DZ, out, s.nb, s.H,
+             s.cin, s.cout, p.R);
+  return hipGetLastError();
+}
+
+hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
+                                  const ConvShape& s, hipStream_t st) {
+  if (!wgrad_rows_ok(s)) return hipErrorInvalidValue;
+  const WgPlan p = wgrad_rows_plan(s);
+  float* out = p.nK > 1 ? partial : dw;
+  const bf16_t* X = (const bf16_t*)x;
+  const bf16_t* DZ = (const bf16_t*)dz;
+  hipError_t e;
+  if (s.W == 192) e = launch_wgrad_rows<192, 1>(X, DZ, out, s, p, st);
+  else if (s.W == 96) e = launch_wgrad_rows<96, 2>(X, DZ, out, s, p, st);
+  else e = launch_wgrad_rows<48, 4>(X, DZ, out, s, p, st);
+  if (e != hipSuccess || p.nK == 1) return e;
+  return splitk_reduce_launch(partial, dw, (long)s.cout * 9 * s.cin, p.nK, st);
+}
+
+}  // namespace tgpk
