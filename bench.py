@@ -38,6 +38,7 @@ def log(*a):
 PROFILES = os.path.join(HERE, "profiles")
 KERNEL_SOURCES = ["paper_2004_09910_amd/csrc/conv_mfma.hip",
                   "paper_2004_09910_amd/csrc/conv_rowtile.hip",
+                  "paper_2004_09910_amd/csrc/conv_rows32.hip",
                   "paper_2004_09910_amd/csrc/wgrad_rows.hip",
                   "paper_2004_09910_amd/csrc/elementwise.hip",
                   "paper_2004_09910_amd/csrc/mfma_util.h",
@@ -216,6 +217,8 @@ def main():
     ap.add_argument("--cpu-samples", type=int, default=40)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mode", default="always", choices=["always", "except_last", "never"])
+    ap.add_argument("--lanes", type=int, default=2,
+                    help="concurrency lanes: micro-batch i runs on stream (i - 1) %% lanes")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of a HIP graph")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three device-to-device copies of 1 GiB (the reference "
@@ -253,7 +256,7 @@ def main():
     log("setting up", wl.name)
     sess = Session(net, BF16, n=wl.n, bind_layers=None)
     lo, hi = sess.bounds[0]
-    sess.plan(wl.batch, wl.m, mode)
+    sess.plan(wl.batch, wl.m, mode, args.lanes)
     B, m = wl.batch, wl.m
     _, xraw = synth.input_x(net, B, BF16)
     x = nchw_to_device_nhwc(xraw, BF16)
@@ -362,7 +365,8 @@ def main():
         "config": {"workload": wl.name, "network": net.name, "partition": f"1 of {wl.n}",
                    "layers": hi - lo, "global_batch": B, "micro_batches": m,
                    "checkpoint": args.mode, "input": f"{B}x{net.in_channels}x{net.height}x{net.width}",
-                   "dx_in": True, "launch": "hip_graph" if graph is not None else "eager"},
+                   "dx_in": True, "launch": "hip_graph" if graph is not None else "eager",
+                   "lanes": args.lanes},
         "mfma_util_pct": 100.0 * step_flops / (ms_step * 1e-3) / BF16_PEAK,
         "step_tflop": step_flops / 1e12,
         "kernel_busy_ms_per_step": kernel_ms,

@@ -123,6 +123,24 @@ tgp_status tgp_balance_minmax(const int64_t* cost, int L, int n, int* balance);
 tgp_status tgp_bind_params(tgp_net* net, int layer, const void* w, const float* b,
                            float* dw_acc, float* db_acc);
 
+/* Concurrency lanes (1..TGP_MAX_LANES, default 1; invalidates the plan, so
+ * call before tgp_plan).  The workspace holds one copy per lane of every
+ * buffer a task uses only while it runs (activations of checkpointed
+ * passes, transformed weights, temporaries); micro-batch i uses lane
+ * (i - 1) % lanes.  With more than one lane, each micro-batch also gets its
+ * own slot for g_i^j.  Tasks of different lanes may then run concurrently
+ * on different streams (micro-batches have no dependency on each other,
+ * which is what lets Sec. 3.2.3 give each micro-batch its own stream),
+ * provided the caller keeps each lane's tasks in order on one stream (or
+ * orders them with events), runs tgp_grad_accumulate(j, i) after B_{i,j}
+ * and after tgp_grad_accumulate(j, i + 1) (one accumulation stream that
+ * waits for each B_{i,j} does both, and keeps the sum over i in its order,
+ * so results stay bit-identical), and makes B_{i,j} wait for whatever
+ * produced its dy_out.  With one stream every lane count gives the same
+ * results as lanes = 1. */
+#define TGP_MAX_LANES 16
+tgp_status tgp_set_lanes(tgp_net* net, int lanes);
+
 /* Fixes the mini-batch size B, the micro-batch count m (B % m == 0) and the
  * checkpoint policy for the following calls, and returns the workspace size
  * in bytes.  Resets the per-task state.  Requires a partition. */
@@ -202,6 +220,26 @@ tgp_status tgp_profile_enable(int enable);
 tgp_status tgp_profile_read(tgp_kernel_stat* out, int cap, int* count);
 /* Drops the recorded events without reading them. */
 tgp_status tgp_profile_clear(void);
+
+/* Kernel-selection overrides, for testing and tuning only (process-wide,
+ * not synchronised: set them while no other thread launches work).  Each
+ * returns the previous value.
+ *
+ * tgp_debug_set_fwd_variant(v) forces the kernel family and tile
+ * configuration of every bf16 convolution launch that goes through the
+ * forward-convolution path (forward, recompute and data gradient): 0 is the
+ * automatic per-shape plan; 1..7 row-stage tiles; 100..102 per-tap tiles;
+ * 201..207 persistent row-stage tiles; 300 the 16x16x32 row-tiled kernel
+ * (301 + i its configuration i); 400 the nine-tap whole-row kernel (401 + i
+ * its configuration i).  A forced choice that does not fit a shape falls
+ * back to the per-tap kernel.
+ *
+ * tgp_debug_set_rowtile_mask(m) enables kernel families in the automatic
+ * plan: bit 0 the row-tiled kernel for forward calls, bit 1 for data-gradient
+ * calls, bit 2 the row-blocked weight gradient, bit 3 the nine-tap whole-row
+ * kernel (default: all set). */
+int tgp_debug_set_fwd_variant(int v);
+int tgp_debug_set_rowtile_mask(int m);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char* tgp_last_error(void);

@@ -84,6 +84,12 @@ _lib.tgp_profile_read.argtypes = [ctypes.POINTER(KernelStat), _I, ctypes.POINTER
 _lib.tgp_profile_read.restype = ctypes.c_int
 _lib.tgp_profile_clear.argtypes = []
 _lib.tgp_profile_clear.restype = ctypes.c_int
+_lib.tgp_set_lanes.argtypes = [_P, _I]
+_lib.tgp_set_lanes.restype = ctypes.c_int
+_lib.tgp_debug_set_fwd_variant.argtypes = [_I]
+_lib.tgp_debug_set_fwd_variant.restype = _I
+_lib.tgp_debug_set_rowtile_mask.argtypes = [_I]
+_lib.tgp_debug_set_rowtile_mask.restype = _I
 _lib.tgp_net_destroy.argtypes = [_P]
 _lib.tgp_net_destroy.restype = None
 _lib.tgp_last_error.argtypes = []
@@ -152,6 +158,10 @@ def bind_params(net: int, layer: int, w: int, b: Optional[int], dw_acc: int,
            "tgp_bind_params")
 
 
+def set_lanes(net: int, lanes: int) -> None:
+    _check(_lib.tgp_set_lanes(net, int(lanes)), "tgp_set_lanes")
+
+
 def plan(net: int, B: int, m: int, ckpt_mode: int) -> int:
     v = ctypes.c_size_t()
     _check(_lib.tgp_plan(net, B, m, ckpt_mode, ctypes.byref(v)), "tgp_plan")
@@ -216,3 +226,15 @@ def profile_read() -> List[dict]:
 
 def profile_clear() -> None:
     _check(_lib.tgp_profile_clear(), "tgp_profile_clear")
+
+
+def debug_set_fwd_variant(v: int) -> int:
+    """Forces the convolution kernel configuration (0 = automatic plan);
+    returns the previous value.  Testing and tuning only."""
+    return _lib.tgp_debug_set_fwd_variant(int(v))
+
+
+def debug_set_rowtile_mask(m: int) -> int:
+    """Enables kernel families in the automatic plan (bit mask); returns the
+    previous mask.  Testing and tuning only."""
+    return _lib.tgp_debug_set_rowtile_mask(int(m))

@@ -14,7 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libtgp.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-SOURCES = ["runtime.cpp", "prof.cpp", "conv_mfma.hip", "conv_rowtile.hip", "wgrad_rows.hip", "elementwise.hip"]
+SOURCES = ["runtime.cpp", "prof.cpp", "conv_mfma.hip", "conv_rowtile.hip", "conv_rows32.hip", "wgrad_rows.hip", "elementwise.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
          "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
          # packed fp32 VALU forms are disabled for every HIP translation unit

@@ -279,7 +279,7 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_dma(
   for (int ks = 0; ks < nk; ++ks) {
     const int ahead = min(NS - 2, nk - 1 - ks);
     wait_stages<NS, LPS>(ahead);
-    __builtin_amdgcn_s_barrier();
+    ring_barrier();
     if (ks + NS - 1 < nk) issue(ks + NS - 1, (ks + NS - 1) % NS);
     const u32x4* As = smem[ks % NS];
     const u32x4* Bs = smem[ks % NS] + BN * 8;
@@ -450,7 +450,7 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_rows(
   for (int k = 0; k < n; ++k) {
     const int ahead = min(NS - 2, n - 1 - k);
     wait_stages<NS, LPS>(ahead);
-    __builtin_amdgcn_s_barrier();
+    ring_barrier();
     if (k + NS - 1 < n) issue(s_begin + k + NS - 1, (k + NS - 1) % NS);
     const int st = s_begin + k;
     const int rf = st % 3;
@@ -616,8 +616,8 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_rows_pers(
   // Buffer descriptors: a byte offset at or past the end (or negative, read
   // as unsigned) returns zeros, which is the zero padding of pixels outside
   // [0, P).  Sizes are below 2^31 (checked by the launcher).
-  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X, P * Cin * 2);
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wt, Cout * 9 * Cin * 2);
+  const u32x4 rx = make_rsrc(X, P * Cin * 2);
+  const u32x4 rw = make_rsrc(Wt, Cout * 9 * Cin * 2);
 
   // Per-lane byte offsets of the rows this lane fills (loop invariant).
   // Weight row of instruction u < LA: channel co (within the tile), column
@@ -703,7 +703,7 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_rows_pers(
       // issued after it are pending (stores of a tile epilogue only make
       // this wait longer).
       wait_stages<NS, L>(min(NS - 2, total - 1 - idx));
-      __builtin_amdgcn_s_barrier();
+      ring_barrier();
       if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);
       const int rf = (c_split * nk + c_ks) % 3;
       const u32x4* As = smem[idx % NS];
@@ -1192,8 +1192,9 @@ hipError_t launch_rows_pers(const char* name_f, const char* name_t, const bf16_t
 
 int g_fwd_split = 0;   // > 0 forces the split count (measurement only)
 // Measurement only: bit 0 allows the row-tiled kernel for forward calls, bit
-// 1 for data-gradient calls.
-int g_rowtile_mask = 7;
+// 1 for data-gradient calls, bit 2 the row-blocked weight gradient, bit 3
+// the nine-tap row kernel.
+int g_rowtile_mask = 15;
 thread_local int t_in_dgrad = 0;
 
 struct FwdPlan {
@@ -1227,7 +1228,9 @@ FwdPlan fwd_plan(const ConvShape& s) {
   // row-stage kernel with split K on the small, deep layers (few pixel tiles,
   // long K); the per-tap kernel in between.
   const bool k3 = s.taps == 9 && s.cin % 64 == 0;
-  if (k3 && (long)s.H * s.W >= 96 * 96 && conv_rowtile_ok(s) &&
+  if (k3 && (long)s.H * s.W >= 96 * 96 && (g_rowtile_mask >> 3 & 1) && conv_rows32_ok(s)) {
+    pl.cfg = 400;  // whole-row tiles, nine taps per stage, 32x32x16
+  } else if (k3 && (long)s.H * s.W >= 96 * 96 && conv_rowtile_ok(s) &&
       (g_rowtile_mask >> (t_in_dgrad ? 1 : 0) & 1)) {
     pl.cfg = 300;  // row-tiled 16x16x32
   } else if (k3 && P <= 4096) {
@@ -1238,6 +1241,12 @@ FwdPlan fwd_plan(const ConvShape& s) {
     pl.cfg = 100;
   }
   if (g_fwd_variant > 0) pl.cfg = g_fwd_variant;
+  if (pl.cfg >= 400) {
+    g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
+    if (!conv_rows32_ok(s)) pl.cfg = 100;
+    g_rows32_cfg = -1;
+    return pl;
+  }
   if (pl.cfg >= 300) {
     if (!conv_rowtile_ok(s)) pl.cfg = 100;
     return pl;
@@ -1290,6 +1299,12 @@ hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void*
   bf16_t* Y = (bf16_t*)y;
   const FwdPlan pl = fwd_plan(s);
   const bool wide = s.cout % 128 == 0;
+  if (pl.cfg >= 400) {
+    g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
+    const hipError_t e = conv_forward_rows32(x, w, b, y, s, relu, st);
+    g_rows32_cfg = -1;
+    return e;
+  }
   if (pl.cfg >= 300) {
     g_rowtile_cfg = pl.cfg >= 301 ? pl.cfg - 301 : -1;
     const hipError_t e = conv_forward_rowtile(x, w, b, y, s, relu, st);

@@ -1,0 +1,324 @@
+// bf16 3x3 convolution (forward, and data gradient on the rotated,
+// transposed weights) on 32 x 32 x 16 MFMA with whole-row pixel tiles and
+// all nine taps per stage.
+//
+// An output tile is 64 output channels x R whole image rows of one sample
+// (R W pixels, a multiple of 32).  Its K loop runs over 16-channel chunks
+// of the input; a stage holds in LDS, for one chunk:
+//   - the weights of all nine taps for the 64 channels: 576 rows, tap-major;
+//   - the R + 2 input rows h0 - 1 .. h0 + R, each as a block of BWP LDS rows
+//     (BWP = W + 2 rounded up to a multiple of 16): row 0 and row W + 1 of a
+//     block are the zero padding of the convolution, the rest are pixels.
+// Every LDS row is 16 channels (32 bytes), its two 16-byte halves swapped
+// when bit 3 of the row index is set.  With that swizzle a fragment read of
+// 32 consecutive rows at one half is free of bank conflicts from any start
+// row, and since BWP is a multiple of 16 a filter-row shift of the input is
+// an immediate offset: output pixel (rho, w) at tap (r, s) reads block row
+// rho + r, LDS row w + s.  So the input rows are loaded once per chunk for
+// all three filter rows, and no fragment is masked: the zero padding and the
+// rows outside the image are buffer reads at out-of-range offsets.
+//
+// The tile's R W / 32 pixel fragments are dealt to the 4 waves, FW each (the
+// last waves may hold fewer real ones and compute on a clamped copy); each
+// wave covers all 64 channels (2 x FW MFMA tiles).  Blocks are persistent
+// over tiles, their stages streamed through one NS-deep LDS ring.  Bias and
+// ReLU are applied in the epilogue (the bias through scalar loads).  The K
+// order (chunk, tap, channel) is fixed by the per-sample shape, so a
+// recomputation is bit-identical.
+#include "common.h"
+#include "kernels.h"
+#include "mfma_util.h"
+#include "prof.h"
+
+namespace tgpk {
+namespace {
+
+constexpr int R32_OOB = (int)0x80000000;   // byte offset that reads as out of range
+constexpr int R32_AROWS = 9 * 64;          // weight rows per stage
+
+typedef __bf16 bf16x2_r32 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ unsigned pack2_bf16(float a, float b) {
+  const bf16x2_r32 h = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(unsigned, h);
+}
+
+template <int W, int R>
+struct Rows32Geom {
+  static constexpr int BWP = (W + 2 + 15) / 16 * 16;           // LDS rows per input row
+  static constexpr int BROWS = (R + 2) * BWP;
+  static constexpr int SB = ((R32_AROWS + BROWS) * 32 + 4095) / 4096 * 4096;  // stage bytes
+  static constexpr int L = SB / 4096;                           // DMA instructions per wave
+  static constexpr int F = R * W / 32;                          // pixel fragments per tile
+  static_assert(R * W % 32 == 0, "whole fragments per tile");
+  static_assert(R32_AROWS * 32 % 1024 == 0, "weight region ends on a DMA chunk");
+};
+
+template <int W, int R, int FW, int NS>
+__global__ __launch_bounds__(256) void conv3x3_rows32(
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
+    const float* __restrict__ bias, bf16_t* __restrict__ Y, int nb, int H, int Cin,
+    int Cout, int relu) {
+  typedef Rows32Geom<W, R> G_;
+  constexpr int BWP = G_::BWP, SB = G_::SB, L = G_::L, F = G_::F;
+  constexpr int ACH = R32_AROWS * 32 / 1024;                    // DMA chunks of weights
+  static_assert(F <= 4 * FW, "fragments per wave");
+  static_assert(NS * SB <= 160 * 1024, "LDS ring");
+  __shared__ __attribute__((aligned(16))) unsigned char smem[NS * SB];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nrb = (H + R - 1) / R;                              // row blocks per sample
+  const int nct = Cout / 64;
+  const int items = nb * nrb * nct;
+  const int G = gridDim.x;
+  const int lb = xcd_remap(blockIdx.x, G);
+  const int n_items = lb < items ? (items - lb + G - 1) / G : 0;
+  const int nk = Cin / 16;                                      // stages per tile
+  const int total = n_items * nk;
+
+  const u32x4 rx = make_rsrc(X, nb * H * W * Cin * 2);
+  const u32x4 rw = make_rsrc(Wt, Cout * 9 * Cin * 2);
+
+  // DMA: instruction u of this wave fills stage chunk k = 4 u + wave (1 KiB);
+  // lane l the 16 bytes at + 16 l: row k * 32 + l / 2, physical half l % 2,
+  // which holds logical half (l % 2) ^ bit 3 of the row.  Chunks below ACH
+  // are weight rows (tap, channel), the rest input rows (block row, pixel).
+  int doff[L], drow[L];
+#pragma unroll
+  for (int u = 0; u < L; ++u) {
+    const int k = 4 * u + wave;
+    const int row = k * 32 + (lane >> 1);
+    const int lh = (lane & 1) ^ ((row >> 3) & 1);
+    if (k < ACH) {
+      const int tap = row >> 6, co = row & 63;
+      doff[u] = ((co * 9 + tap) * Cin + 8 * lh) * 2;
+      drow[u] = 0;
+    } else {
+      const int q = row - R32_AROWS;
+      const int rr = q / BWP, wp = q - rr * BWP;
+      const bool ok = rr < R + 2 && wp >= 1 && wp <= W;
+      doff[u] = ok ? ((rr * W + wp - 1) * Cin + 8 * lh) * 2 : 0;
+      drow[u] = ok ? rr : -1;
+    }
+  }
+
+  // Fragment addresses (bytes within a stage).  A: weight row tap * 64 +
+  // 32 i + l % 32 at logical half l / 32, tap and i as immediates.  B: for
+  // each fragment j and column tap s, LDS row rho BWP + w + s of the input
+  // region (filter row r adds r BWP rows as an immediate).
+  const int abase = (lane & 31) * 32 + (((lane >> 5) ^ ((lane >> 3) & 1)) << 4);
+  int bq[FW][3];
+  int opix[FW];
+#pragma unroll
+  for (int j = 0; j < FW; ++j) {
+    const int f = wave * FW + j;
+    int tp = f * 32 + (lane & 31);
+    opix[j] = f < F ? tp : -1;
+    if (tp >= R * W) tp = R * W - 1;                            // clamped copy for padding fragments
+    const int rho = tp / W, w = tp - rho * W;
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      const int q = rho * BWP + w + s;
+      bq[j][s] = R32_AROWS * 32 + q * 32 + (((lane >> 5) ^ ((q >> 3) & 1)) << 4);
+    }
+  }
+
+  auto coords = [&](int it, int& n, int& h0, int& co0) __attribute__((always_inline)) {
+    const int item = lb + it * G;
+    const int ct = item % nct, rest = item / nct;
+    const int rb = rest % nrb;
+    n = rest / nrb;
+    h0 = rb * R;
+    co0 = ct * 64;
+  };
+
+  // issue side
+  int i_it = 0, i_ks = 0, i_n = 0, i_h0 = 0, i_co0 = 0;
+  if (total > 0) coords(0, i_n, i_h0, i_co0);
+  auto issue = [&](int slot) __attribute__((always_inline)) {
+    const int c0 = i_ks * 16;
+    const int soff_a = (i_co0 * 9 * Cin + c0) * 2;
+    const int hb = i_h0 - 1;                                    // input row of block row 0
+    const int base_b = ((i_n * H + hb) * W * Cin + c0) * 2;    // negative for hb = -1
+    const bool interior = hb >= 0 && hb + R + 2 <= H;
+#pragma unroll
+    for (int u = 0; u < L; ++u) {
+      const int k = 4 * u + wave;
+      auto* dst = TGP_LDS(smem + slot * SB + k * 1024);
+      if (k < ACH) {
+        dma16(rw, dst, doff[u], soff_a);
+      } else {
+        const bool ok = drow[u] >= 0 && (interior || (unsigned)(hb + drow[u]) < (unsigned)H);
+        dma16(rx, dst, ok ? base_b + doff[u] : R32_OOB, 0);
+      }
+    }
+    if (++i_ks == nk) {
+      i_ks = 0;
+      if (++i_it < n_items) coords(i_it, i_n, i_h0, i_co0);
+    }
+  };
+
+#pragma unroll
+  for (int k = 0; k < NS - 1; ++k)
+    if (k < total) issue(k);
+
+  const __attribute__((address_space(4))) float* cbias =
+      (const __attribute__((address_space(4))) float*)bias;
+
+  int idx = 0;
+  for (int c_it = 0; c_it < n_items; ++c_it) {
+    int n, h0, co0;
+    coords(c_it, n, h0, co0);
+    f32x16_t acc[2][FW];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < FW; ++j) acc[i][j] = f32x16_t{};
+
+    for (int ks = 0; ks < nk; ++ks, ++idx) {
+      // loads complete in order: stage idx is in once at most the stages
+      // issued after it are pending (epilogue stores only lengthen the wait)
+      wait_stages<NS, L>(min(NS - 2, total - 1 - idx));
+      ring_barrier();
+      if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);
+      const unsigned char* st = smem + (idx % NS) * SB;
+      // nine taps; tap t + 1's fragments are read while tap t's MFMAs run
+      bf16x8_t fa[2][2], fb[2][FW];
+      auto load = [&](int t, int buf) __attribute__((always_inline)) {
+        const int r = t / 3, s = t - 3 * (t / 3);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+          fa[buf][i] = as_bf16x8(*(const u32x4*)(st + abase + (t * 64 + 32 * i) * 32));
+#pragma unroll
+        for (int j = 0; j < FW; ++j)
+          fb[buf][j] = as_bf16x8(*(const u32x4*)(st + bq[j][s] + r * BWP * 32));
+      };
+      load(0, 0);
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        if (t + 1 < 9) load(t + 1, (t + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int j = 0; j < FW; ++j) acc[i][j] = mfma32(fa[t & 1][i], fb[t & 1][j], acc[i][j]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+
+    // epilogue: element v of lane l is output channel co0 + 32 i + 8 (v / 4)
+    // + 4 (l / 32) + v % 4 of tile pixel opix[j]
+    const long pix0 = (long)(n * H + h0) * W;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int cob = co0 + 32 * i + 8 * g;
+        const int co = cob + 4 * (lane >> 5);
+        float b4[4] = {0.f, 0.f, 0.f, 0.f};
+        if (bias) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float b0 = cbias[cob + e], b1 = cbias[cob + 4 + e];
+            b4[e] = (lane >> 5) ? b1 : b0;
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < FW; ++j) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            v[e] = acc[i][j][4 * g + e] + b4[e];
+            if (relu) v[e] = fmaxf(v[e], 0.0f);
+          }
+          const int tp = opix[j];
+          if (tp >= 0 && h0 + tp / W < H) {
+            uint2 o;
+            o.x = pack2_bf16(v[0], v[1]);
+            o.y = pack2_bf16(v[2], v[3]);
+            *(uint2*)(Y + (pix0 + tp) * Cout + co) = o;
+          }
+        }
+      }
+    }
+  }
+}
+
+struct R32Cfg { int W, R, FW, NS; };
+constexpr R32Cfg kR32Cfgs[] = {
+    {192, 3, 5, 3}, {192, 1, 2, 4},
+    {96, 6, 5, 3},  {96, 3, 3, 4},  {96, 2, 2, 4},
+    {48, 12, 5, 3}, {48, 6, 3, 4},  {48, 4, 2, 4},
+    {24, 24, 5, 3}, {24, 12, 3, 4}, {24, 8, 2, 4},
+};
+constexpr int kR32N = sizeof(kR32Cfgs) / sizeof(kR32Cfgs[0]);
+
+}  // namespace
+
+// Configuration for a per-sample shape: among those for its width, the one
+// with the fewest rounds of 256 tiles (for a nominal 4-sample micro-batch)
+// times fragments per wave.  Returns an index into kR32Cfgs, or -1.
+int g_rows32_cfg = -1;   // >= 0 forces a configuration (measurement only)
+
+static int rows32_pick(const ConvShape& s) {
+  if (s.taps != 9 || s.cin % 16 || s.cout % 64) return -1;
+  int best = -1;
+  long best_cost = 0;
+  for (int c = 0; c < kR32N; ++c) {
+    const R32Cfg k = kR32Cfgs[c];
+    if (k.W != s.W || k.R > s.H) continue;
+    const long items = 4L * ((s.H + k.R - 1) / k.R) * (s.cout / 64);
+    const long cost = (items + 255) / 256 * k.FW;
+    if (g_rows32_cfg == c || (g_rows32_cfg < 0 && (best < 0 || cost < best_cost))) {
+      best = c;
+      best_cost = cost;
+    }
+  }
+  return best;
+}
+
+bool conv_rows32_ok(const ConvShape& s) {
+  return rows32_pick(s) >= 0 && (double)s.pixels() * s.cin * 2 < 2147483648.0 &&
+         (double)s.cout * 9 * s.cin * 2 < 2147483648.0;
+}
+
+template <int W, int R, int FW, int NS>
+static hipError_t launch_rows32(const bf16_t* X, const bf16_t* Wt, const float* b, bf16_t* Y,
+                                const ConvShape& s, int relu, hipStream_t st) {
+  static const char* name = nullptr;
+  static char buf[64];
+  if (!name) {
+    snprintf(buf, sizeof buf, "conv3x3_rows32<%d,%d,%d,%d>", W, R, FW, NS);
+    name = buf;
+  }
+  const long items = (long)s.nb * ((s.H + R - 1) / R) * (s.cout / 64);
+  const int G = (int)(items < 256 ? items : 256);
+  if (G == 0) return hipSuccess;
+  const long P = s.pixels();
+  ProfScope ps(name, 2.0 * P * s.cout * 9 * s.cin,
+               2.0 * ((double)P * s.cin + 9.0 * s.cin * s.cout + (double)P * s.cout), st);
+  TGP_LAUNCH(ps, (conv3x3_rows32<W, R, FW, NS>), dim3(G), dim3(256), 0, st, X, Wt, b, Y, s.nb,
+             s.H, s.cin, s.cout, relu);
+  return hipGetLastError();
+}
+
+hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, void* y,
+                               const ConvShape& s, int relu, hipStream_t st) {
+  const int c = rows32_pick(s);
+  if (c < 0 || !conv_rows32_ok(s)) return hipErrorInvalidValue;
+  const bf16_t* X = (const bf16_t*)x;
+  const bf16_t* Wt = (const bf16_t*)w;
+  bf16_t* Y = (bf16_t*)y;
+  switch (c) {
+#define R32_CASE(i)                                                                      \
+  case i:                                                                                \
+    return launch_rows32<kR32Cfgs[i].W, kR32Cfgs[i].R, kR32Cfgs[i].FW, kR32Cfgs[i].NS>( \
+        X, Wt, b, Y, s, relu, st);
+    R32_CASE(0) R32_CASE(1) R32_CASE(2) R32_CASE(3) R32_CASE(4) R32_CASE(5)
+    R32_CASE(6) R32_CASE(7) R32_CASE(8) R32_CASE(9) R32_CASE(10)
+#undef R32_CASE
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace tgpk

@@ -72,8 +72,8 @@ __global__ __launch_bounds__(256) void conv3x3_rowtile(
     for (int c = tid; c < Cout; c += 256) sbias[c] = bias[c];
   __syncthreads();   // the stage loop's barriers do not wait for LDS writes
 
-  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X, nb * H * W * Cin * 2);
-  const __amdgpu_buffer_rsrc_t rw = make_rsrc(Wt, Cout * 9 * Cin * 2);
+  const u32x4 rx = make_rsrc(X, nb * H * W * Cin * 2);
+  const u32x4 rw = make_rsrc(Wt, Cout * 9 * Cin * 2);
 
   // DMA: instruction u of this wave fills stage bytes [(4 u + wave) KiB, + 1
   // KiB); lane l the 16 bytes at + 16 l, i.e. row off / 80, chunk
@@ -166,7 +166,7 @@ __global__ __launch_bounds__(256) void conv3x3_rowtile(
       // issued after it are pending (stores of an epilogue only make this
       // wait longer)
       wait_stages<NS, L>(min(NS - 2, total - 1 - idx));
-      __builtin_amdgcn_s_barrier();
+      ring_barrier();
       if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);
       const unsigned char* st = smem + (idx % NS) * SB;
       // 3 column taps; tap s + 1's fragments are read while tap s's MFMAs run

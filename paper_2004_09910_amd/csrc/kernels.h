@@ -29,6 +29,14 @@ bool conv_rowtile_ok(const ConvShape& s);
 hipError_t conv_forward_rowtile(const void* x, const void* w, const float* b, void* y,
                                 const ConvShape& s, int relu, hipStream_t st);
 extern int g_rowtile_cfg;
+// 32x32x16-MFMA 3x3 convolution on whole-row tiles with all nine taps per
+// 16-channel stage (bf16; W in {24, 48, 96, 192}, Cin % 16 == 0, Cout % 64
+// == 0): whether it supports a shape, and the launch (same contract as
+// conv_forward_rowtile).
+bool conv_rows32_ok(const ConvShape& s);
+hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, void* y,
+                               const ConvShape& s, int relu, hipStream_t st);
+extern int g_rows32_cfg;
 extern int g_rowtile_mask;
 extern thread_local int t_in_dgrad;
 // Row-blocked 3x3 weight gradient on 32x32x16 MFMA with transpose LDS reads

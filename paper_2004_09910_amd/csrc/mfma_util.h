@@ -61,19 +61,40 @@ __device__ __forceinline__ int xcd_remap(int bid, int nb) {
   return x < rem ? x * (per + 1) + i : rem * (per + 1) + (x - rem) * per + i;
 }
 
-// 16 bytes per lane from a buffer into LDS (lane l -> dst + 16 l).  A byte
-// offset voff at or past the buffer's size (negative ones included, read as
-// unsigned) yields zeros.  Kept out of line of the kernel templates: the
-// host pass drops a kernel template instantiation that calls this builtin
-// directly.
-__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r,
-                                      __attribute__((address_space(3))) void* dst, int voff,
-                                      int soff) {
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, dst, 16, voff, soff, 0, 0);
+// Buffer resource descriptor for raw (unswizzled, stride 0) loads of `bytes`
+// bytes at p: base address, record count, and the data-format word.
+__device__ __forceinline__ u32x4 make_rsrc(const void* p, int bytes) {
+  const unsigned long a = (unsigned long)p;
+  return u32x4{(unsigned)a, (unsigned)(a >> 32) & 0xffffu, (unsigned)bytes, 0x00020000u};
 }
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc((void*)p, (short)0, bytes, 0x00020000);
+// 16 bytes per lane from a buffer into LDS (lane l -> dst + 16 l).  A byte
+// offset voff + soff at or past the buffer's size (negative voff included,
+// read as unsigned) yields zeros; soff must be wave-uniform.  Issued from inline assembly so that the
+// compiler does not see an LDS write: it cannot tell the ring slots apart
+// and would otherwise wait for every load in flight before the next LDS
+// read, which serialises the ring.  The kernels order their rings
+// themselves (wait_vmcnt / wait_stages, then ring_barrier).  M0 holds the
+// LDS destination only while the load issues and is restored after it.
+__device__ __forceinline__ void dma16(u32x4 rsrc, __attribute__((address_space(3))) void* dst,
+                                      int voff, int soff) {
+  const unsigned m = __builtin_amdgcn_readfirstlane((unsigned)(unsigned long)dst);
+  unsigned saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %1\n\t"
+      "buffer_load_dwordx4 %2, %3, %4 offen lds\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "s"(m), "v"(voff), "s"(rsrc), "s"(__builtin_amdgcn_readfirstlane(soff))
+      : "memory");
+}
+
+// Workgroup barrier of a DMA ring: s_barrier, plus a compiler fence so that
+// no LDS read of the stage just waited for is moved above it.
+__device__ __forceinline__ void ring_barrier() {
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
 }
 
 }  // namespace

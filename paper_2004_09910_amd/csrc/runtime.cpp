@@ -75,6 +75,17 @@ struct tgp_net {
          o_loss = 0, o_fpart = 0, fpart_floats = 0;
   std::vector<size_t> o_bnd, o_gbnd;  // per (i, j) pipeline boundaries, [i*n + j]
   size_t o_out = 0, o_dy = 0, out_bytes_mb = 0;
+  // Transient buffers (activations of checkpointed passes, per-micro-batch
+  // gradients, transformed weights, temporaries) exist once per lane;
+  // micro-batch i uses lane (i - 1) % lanes.  Their offsets above are
+  // relative to the lane's base o_lane + lane * lane_stride.
+  int lanes = 1;
+  size_t o_lane = 0, lane_stride = 0;
+  // Per-micro-batch gradients g_i^j (o_gw / o_gb of each layer, relative to
+  // a slot): one slot with one lane, one per micro-batch with several, so
+  // that no lane waits for the accumulation of its previous micro-batch.
+  int gslots = 1;
+  size_t o_gslot = 0, gslot_stride = 0;
   // state per (i, j): index (i-1)*n + (j-1)
   std::vector<uint8_t> st;
   std::vector<const void*> saved_x;
@@ -160,6 +171,14 @@ hipStream_t S(void* s) { return (hipStream_t)s; }
   } while (0)
 
 char* W_(tgp_net* N, size_t off) { return N->ws + off; }
+// Gradient slot buffer at slot-relative offset off, for micro-batch i.
+char* G_(tgp_net* N, int i, size_t off) {
+  return N->ws + N->o_gslot + (size_t)((i - 1) % N->gslots) * N->gslot_stride + off;
+}
+// Transient buffer at lane-relative offset off, for micro-batch i.
+char* T_(tgp_net* N, int i, size_t off) {
+  return N->ws + N->o_lane + (size_t)((i - 1) % N->lanes) * N->lane_stride + off;
+}
 
 // ------------------------------------------------------------ per-layer device work
 
@@ -185,14 +204,14 @@ tgp_status run_forward(tgp_net* N, int j, int i, int phase, const void* x_in, vo
     LayerRt& Lr = N->L[l];
     const tgp_layer& d = Lr.d;
     void* out;
-    if (phase == 2) out = W_(N, Lr.o_scr_out);
+    if (phase == 2) out = T_(N, i, Lr.o_scr_out);
     else if (l == hi - 1) out = y_out;
     else if (d.stash_id >= 0) out = W_(N, stash_off(N, i, d.stash_id, false));
     else if (phase == 1) out = W_(N, Lr.o_sto_out[set]);
-    else out = W_(N, Lr.o_scr_out);
+    else out = T_(N, i, Lr.o_scr_out);
     const void* cin_ptr = src;
     if (d.prologue != TGP_PRO_NONE) {
-      void* pro = (phase == 1) ? W_(N, Lr.o_sto_pro[set]) : W_(N, Lr.o_scr_pro);
+      void* pro = (phase == 1) ? W_(N, Lr.o_sto_pro[set]) : T_(N, i, Lr.o_scr_pro);
       if (d.prologue == TGP_PRO_MAXPOOL2) {
         HIPCHK(tgpk::maxpool_forward(N->dt, src, pro, N->b, Lr.inH, Lr.inW, Lr.inC, st),
                "maxpool_forward");
@@ -211,7 +230,7 @@ tgp_status run_forward(tgp_net* N, int j, int i, int phase, const void* x_in, vo
     } else {
       tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
       HIPCHK(tgpk::conv_forward(N->dt, cin_ptr, Lr.w, d.bias ? Lr.b : nullptr, out, s, d.relu,
-                                (float*)W_(N, N->o_fpart), N->fpart_floats, st),
+                                (float*)T_(N, i, N->o_fpart), N->fpart_floats, st),
              "conv_forward");
     }
     src = out;
@@ -230,8 +249,8 @@ void activation_view(tgp_net* N, int j, int i, bool ckpt, ActView& v) {
   for (int l = lo; l < hi; ++l) {
     LayerRt& Lr = N->L[l];
     if (ckpt) {
-      v.out[l - lo] = W_(N, Lr.o_scr_out);
-      if (Lr.d.prologue != TGP_PRO_NONE) v.pro[l - lo] = W_(N, Lr.o_scr_pro);
+      v.out[l - lo] = T_(N, i, Lr.o_scr_out);
+      if (Lr.d.prologue != TGP_PRO_NONE) v.pro[l - lo] = T_(N, i, Lr.o_scr_pro);
     } else {
       if (l == hi - 1) v.out[l - lo] = N->saved_y[c];
       else if (Lr.d.stash_id >= 0) v.out[l - lo] = W_(N, stash_off(N, i, Lr.d.stash_id, false));
@@ -249,25 +268,25 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
     tgp_status r = run_forward(N, j, i, 2, N->saved_x[cell(N, i, j)], nullptr, st);
     if (r != TGP_OK) return r;
   }
-  if (i == N->m) {
-    // first backward of partition j in this step: refresh the transformed
-    // weights used by the data-gradient kernels
+  if (i > N->m - N->lanes) {
+    // first backward of partition j on this lane in this step: refresh the
+    // lane's transformed weights used by the data-gradient kernels
     for (int l = lo; l < hi; ++l) {
       LayerRt& Lr = N->L[l];
       if (Lr.has_wt)
-        HIPCHK(tgpk::weight_transform(N->dt, Lr.w, W_(N, Lr.o_wt), Lr.d.cout, Lr.d.cin, Lr.taps,
+        HIPCHK(tgpk::weight_transform(N->dt, Lr.w, T_(N, i, Lr.o_wt), Lr.d.cout, Lr.d.cin, Lr.taps,
                                       st),
                "weight_transform");
     }
   }
   ActView v;
   activation_view(N, j, i, ckpt, v);
-  void* gcur = W_(N, N->o_g0);
-  void* gnext = W_(N, N->o_g1);
-  void* dz = W_(N, N->o_dz);
-  void* dinp = W_(N, N->o_dinp);
-  float* part = (float*)W_(N, N->o_part);
-  float* colpart = (float*)W_(N, N->o_colpart);
+  void* gcur = T_(N, i, N->o_g0);
+  void* gnext = T_(N, i, N->o_g1);
+  void* dz = T_(N, i, N->o_dz);
+  void* dinp = T_(N, i, N->o_dinp);
+  float* part = (float*)T_(N, i, N->o_part);
+  float* colpart = (float*)T_(N, i, N->o_colpart);
   const void* dy = dy_out;
   for (int l = hi - 1; l >= lo; --l) {
     LayerRt& Lr = N->L[l];
@@ -279,16 +298,16 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
     long nout = out_elems_mb(N, Lr);
     long P = (long)N->b * Lr.H * Lr.W;
     if (d.bias && tgpk::relu_bias_fusable(N->dt, d.cout, dy, dskip, y, dz)) {
-      HIPCHK(tgpk::relu_backward_bias(N->dt, dy, dskip, y, dz, d.relu, (float*)W_(N, Lr.o_gb),
+      HIPCHK(tgpk::relu_backward_bias(N->dt, dy, dskip, y, dz, d.relu, (float*)G_(N, i, Lr.o_gb),
                                       colpart, P, d.cout, st),
              "relu_backward_bias");
     } else {
       HIPCHK(tgpk::relu_backward(N->dt, dy, dskip, y, dz, d.relu, nout, st), "relu_backward");
       if (d.bias)
-        HIPCHK(tgpk::bias_grad(N->dt, dz, (float*)W_(N, Lr.o_gb), colpart, P, d.cout, st),
+        HIPCHK(tgpk::bias_grad(N->dt, dz, (float*)G_(N, i, Lr.o_gb), colpart, P, d.cout, st),
                "bias_grad");
     }
-    float* gw = (float*)W_(N, Lr.o_gw);
+    float* gw = (float*)G_(N, i, Lr.o_gw);
     if (d.kind == TGP_DWCONV3X3) {
       HIPCHK(tgpk::dw_wgrad(N->dt, cin_ptr, dz, gw, part, N->b, Lr.H, Lr.W, d.cout, st),
              "dw_wgrad");
@@ -304,8 +323,8 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
              "dw_dgrad");
     } else {
       tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
-      HIPCHK(tgpk::conv_dgrad(N->dt, dz, Lr.w, Lr.has_wt ? W_(N, Lr.o_wt) : nullptr, dgrad_out,
-                              s, (float*)W_(N, N->o_fpart), N->fpart_floats, st),
+      HIPCHK(tgpk::conv_dgrad(N->dt, dz, Lr.w, Lr.has_wt ? T_(N, i, Lr.o_wt) : nullptr, dgrad_out,
+                              s, (float*)T_(N, i, N->o_fpart), N->fpart_floats, st),
              "conv_dgrad");
     }
     if (d.prologue == TGP_PRO_MAXPOOL2) {
@@ -325,7 +344,7 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
   return TGP_OK;
 }
 
-tgp_status run_accumulate(tgp_net* N, int j, int overwrite, hipStream_t st) {
+tgp_status run_accumulate(tgp_net* N, int j, int i, int overwrite, hipStream_t st) {
   tgpk::AccBatch batch;
   batch.count = 0;
   auto flush = [&]() -> tgp_status {
@@ -347,8 +366,8 @@ tgp_status run_accumulate(tgp_net* N, int j, int overwrite, hipStream_t st) {
   };
   for (int l = N->lo[j - 1]; l < N->hi[j - 1]; ++l) {
     LayerRt& Lr = N->L[l];
-    tgp_status r = add(Lr.dw_acc, (const float*)W_(N, Lr.o_gw), Lr.w_elems);
-    if (r == TGP_OK && Lr.d.bias) r = add(Lr.db_acc, (const float*)W_(N, Lr.o_gb), Lr.d.cout);
+    tgp_status r = add(Lr.dw_acc, (const float*)G_(N, i, Lr.o_gw), Lr.w_elems);
+    if (r == TGP_OK && Lr.d.bias) r = add(Lr.db_acc, (const float*)G_(N, i, Lr.o_gb), Lr.d.cout);
     if (r != TGP_OK) return r;
   }
   return flush();
@@ -449,7 +468,7 @@ struct GpuExec : Exec {
     HIPCHK(tgpk::mse_forward_backward(N->dt, bnd(i, N->n),
                                       target + (size_t)(i - 1) * out_mb_bytes, gbnd(i, N->n),
                                       (float*)W_(N, N->o_loss) + (i - 1),
-                                      (float*)W_(N, N->o_msepart), n_mb, 1.0f / (float)numel,
+                                      (float*)T_(N, i, N->o_msepart), n_mb, 1.0f / (float)numel,
                                       st),
            "mse_forward_backward");
     return TGP_OK;
@@ -478,8 +497,8 @@ extern "C" {
 
 const char* tgp_last_error(void) { return g_err.c_str(); }
 
-// Measurement hook (not in tgp.h): selects a forward-kernel tile/stage
-// configuration for benchmarking sweeps.
+// Kernel-selection overrides for tests and measurement sweeps (the first
+// two are declared in tgp.h; split and order are sweep-only).
 int tgp_debug_set_fwd_variant(int v) {
   int old = tgpk::g_fwd_variant;
   tgpk::g_fwd_variant = v;
@@ -639,6 +658,15 @@ tgp_status tgp_bind_params(tgp_net* N, int layer, const void* w, const float* b,
   return TGP_OK;
 }
 
+tgp_status tgp_set_lanes(tgp_net* N, int lanes) {
+  if (!N) return fail(TGP_EINVAL, "net is NULL");
+  if (lanes < 1 || lanes > TGP_MAX_LANES) return fail(TGP_EINVAL, "lanes=%d out of 1..%d", lanes, TGP_MAX_LANES);
+  N->lanes = lanes;
+  N->planned = false;
+  N->ws = nullptr;
+  return TGP_OK;
+}
+
 tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
   if (!N || !bytes) return fail(TGP_EINVAL, "NULL argument");
   if (m < 1 || B < 1) return fail(TGP_EINVAL, "B and m must be positive");
@@ -649,8 +677,11 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
   for (auto& l : N->L)
     if ((long)N->b * l.H * l.W >= (1L << 31) / 4 || (long)N->b * l.inH * l.inW >= (1L << 31) / 4)
       return fail(TGP_EINVAL, "micro-batch too large for 32-bit pixel indices");
-  size_t off = 0;
+  size_t off = 0, loff = 0;
   auto take = [&](size_t bytes_) { size_t o = off; off += al256(bytes_); return o; };
+  auto takeL = [&](size_t bytes_) { size_t o = loff; loff += al256(bytes_); return o; };
+  size_t goff = 0;
+  auto takeG = [&](size_t bytes_) { size_t o = goff; goff += al256(bytes_); return o; };
   // skips and their gradients, one slot per micro-batch
   N->o_stash.clear(); N->o_stash_grad.clear();
   size_t stride = 0;
@@ -669,8 +700,8 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
     size_t in_bytes = (size_t)N->b * Lr.inH * Lr.inW * Lr.inC * N->esz;
     max_act = std::max({max_act, Lr.out_bytes, in_bytes});
     max_pro = std::max(max_pro, Lr.pro_bytes);
-    Lr.o_scr_out = take(Lr.out_bytes);
-    Lr.o_scr_pro = Lr.pro_bytes ? take(Lr.pro_bytes) : 0;
+    Lr.o_scr_out = takeL(Lr.out_bytes);
+    Lr.o_scr_pro = Lr.pro_bytes ? takeL(Lr.pro_bytes) : 0;
   }
   // stored activations of non-checkpointed micro-batches
   N->nsets = mode == TGP_CKPT_NEVER ? m : (mode == TGP_CKPT_EXCEPT_LAST ? 1 : 0);
@@ -687,22 +718,22 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
   // per-micro-batch gradients g_i and transformed weights
   size_t max_part = 0, max_col = 0;
   for (auto& Lr : N->L) {
-    Lr.o_gw = take(Lr.w_elems * 4);
-    Lr.o_gb = Lr.d.bias ? take(Lr.d.cout * 4) : 0;
+    Lr.o_gw = takeG(Lr.w_elems * 4);
+    Lr.o_gb = Lr.d.bias ? takeG(Lr.d.cout * 4) : 0;
     tgpk::ConvShape s{N->b, Lr.H, Lr.W, Lr.d.cin, Lr.d.cout, Lr.taps};
     Lr.has_wt = Lr.d.kind != TGP_DWCONV3X3 && tgpk::conv_dgrad_uses_wt(N->dt, s);
-    Lr.o_wt = Lr.has_wt ? take(Lr.w_elems * N->esz) : 0;
+    Lr.o_wt = Lr.has_wt ? takeL(Lr.w_elems * N->esz) : 0;
     size_t pf = Lr.d.kind == TGP_DWCONV3X3 ? tgpk::dw_wgrad_partial_floats(N->b, Lr.H, Lr.W, Lr.d.cout)
                                            : tgpk::conv_wgrad_partial_floats(N->dt, s);
     max_part = std::max(max_part, pf);
     max_col = std::max({max_col, tgpk::colsum_partial_floats((long)N->b * Lr.H * Lr.W, Lr.d.cout),
                         tgpk::relu_bias_partial_floats(N->dt, (long)N->b * Lr.H * Lr.W, Lr.d.cout)});
   }
-  N->o_g0 = take(max_act);
-  N->o_g1 = take(max_act);
-  N->o_dz = take(max_act);
-  N->o_dinp = take(std::max<size_t>(max_pro, 16));
-  N->o_part = take(max_part * 4);
+  N->o_g0 = takeL(max_act);
+  N->o_g1 = takeL(max_act);
+  N->o_dz = takeL(max_act);
+  N->o_dinp = takeL(std::max<size_t>(max_pro, 16));
+  N->o_part = takeL(max_part * 4);
   size_t max_fpart = 0;   // split-K partials of forward / data-gradient convolutions
   for (auto& Lr : N->L) {
     if (Lr.d.kind == TGP_DWCONV3X3) continue;
@@ -712,12 +743,12 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
                           tgpk::conv_forward_partial_floats(N->dt, d)});
   }
   N->fpart_floats = max_fpart;
-  N->o_fpart = take(std::max<size_t>(max_fpart, 4) * 4);
-  N->o_colpart = take(max_col * 4);
+  N->o_fpart = takeL(std::max<size_t>(max_fpart, 4) * 4);
+  N->o_colpart = takeL(max_col * 4);
   const LayerRt& last = N->L.back();
   long out_mb = (long)N->b * last.H * last.W * last.d.cout;
   N->out_bytes_mb = out_mb * N->esz;
-  N->o_msepart = take(tgpk::mse_partial_floats(out_mb) * 4);
+  N->o_msepart = takeL(tgpk::mse_partial_floats(out_mb) * 4);
   N->o_loss = take(m * 4);
   // pipeline boundaries
   N->o_bnd.assign((size_t)m * n + n, 0);
@@ -729,6 +760,11 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
     }
   N->o_out = take(al256(N->out_bytes_mb) * m);
   N->o_dy = take(al256(N->out_bytes_mb) * m);
+  N->lane_stride = al256(loff);
+  N->o_lane = take(N->lane_stride * N->lanes);
+  N->gslots = N->lanes > 1 ? m : 1;
+  N->gslot_stride = al256(goff);
+  N->o_gslot = take(N->gslot_stride * N->gslots);
   N->ws_need = off;
   N->planned = true;
   N->ws = nullptr;
@@ -809,7 +845,7 @@ tgp_status tgp_grad_accumulate(tgp_net* N, int j, int i, int overwrite, void* st
     return fail(TGP_EINVAL, "overwrite must be 1 exactly for i = m");
   int c = cell(N, i, j);
   if (N->st[c] != BWD) return fail(TGP_ESTATE, "accumulate (%d,%d) needs B_{%d,%d} first", i, j, i, j);
-  r = run_accumulate(N, j, overwrite, S(stream));
+  r = run_accumulate(N, j, i, overwrite, S(stream));
   if (r != TGP_OK) return r;
   N->st[c] = ACC;
   return TGP_OK;

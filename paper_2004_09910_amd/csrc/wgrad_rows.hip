@@ -79,8 +79,8 @@ __global__ __launch_bounds__(256) void conv_wgrad_rows(
   const long E = (long)Cout * 9 * Cin;
   const int spr = (R + RPS - 1) / RPS;          // stages per full row block
 
-  const __amdgpu_buffer_rsrc_t rz = make_rsrc(dZ, nb * H * W * Cout * 2);
-  const __amdgpu_buffer_rsrc_t rx = make_rsrc(X, nb * H * W * Cin * 2);
+  const u32x4 rz = make_rsrc(dZ, nb * H * W * Cout * 2);
+  const u32x4 rx = make_rsrc(X, nb * H * W * Cin * 2);
 
   // DMA lane constants: instruction u of this wave fills rows (4 u + wave) * 8
   // + lane / 8 of the A (u < LA) or B region, physical chunk lane % 8, which
@@ -189,7 +189,7 @@ __global__ __launch_bounds__(256) void conv_wgrad_rows(
       // loads complete in order: stage idx is in once at most the stages
       // issued after it are pending (epilogue stores only lengthen this wait)
       wait_stages<NS, LA + LB>(min(NS - 2, total - 1 - idx));
-      __builtin_amdgcn_s_barrier();
+      ring_barrier();
       if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);
       const unsigned char* sp = smem + (idx % NS) * SB;
 #pragma unroll

@@ -77,6 +77,8 @@ class Session:
             self._bind_layer(idx, seed_offset)
         self.ws = None
         self.B = self.m = self.b = self.mode = None
+        self.lanes = 1
+        self._lane_streams = None
 
     def _bind_layer(self, idx: int, seed_offset: int):
         L = self.net.layers[idx]
@@ -95,7 +97,10 @@ class Session:
         self.params[idx] = {"w": wk, "b": bt, "dw": dw, "db": db, "w64": w64,
                             "b64": None if b is None else b[0]}
 
-    def plan(self, B: int, m: int, mode: int) -> int:
+    def plan(self, B: int, m: int, mode: int, lanes: int = 1) -> int:
+        tgp.set_lanes(self.h, lanes)
+        self.lanes = lanes
+        self._lane_streams = None
         nbytes = tgp.plan(self.h, B, m, mode)
         self.ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
         tgp.bind_workspace(self.h, self.ws.data_ptr(), self.ws.numel())
@@ -159,12 +164,44 @@ class Session:
         NHWC; micro-batch slices are pointer offsets."""
         def sl(t, i):
             return t.data_ptr() + (i - 1) * (t.numel() // self.m) * t.element_size()
+        if self.lanes > 1:
+            return self._stage_step_lanes(j, x, y, dy, dx, sl)
         for i in range(1, self.m + 1):
             tgp.stage_forward(self.h, j, i, self.checkpointed(i), sl(x, i), sl(y, i), stream)
         for i in range(self.m, 0, -1):
             tgp.stage_backward_recompute(self.h, j, i, sl(dy, i),
                                          None if dx is None else sl(dx, i), stream)
             tgp.grad_accumulate(self.h, j, i, i == self.m, stream)
+
+    def _stage_step_lanes(self, j, x, y, dy, dx, sl):
+        """stage_step with micro-batch i on lane stream (i - 1) % lanes and the
+        accumulations, in the order m..1, on one more stream that waits for
+        each backward; all forked from and joined back into the current
+        stream.  Every cross-stream dependency points from a lane to the
+        accumulation stream, never back."""
+        cur = torch.cuda.current_stream()
+        K = min(self.lanes, self.m)
+        if self._lane_streams is None:
+            self._lane_streams = [torch.cuda.Stream() for _ in range(K + 1)]
+        lanes, acc = self._lane_streams[:K], self._lane_streams[K]
+        for s in self._lane_streams:
+            s.wait_stream(cur)
+        for i in range(1, self.m + 1):
+            s = lanes[(i - 1) % K]
+            tgp.stage_forward(self.h, j, i, self.checkpointed(i), sl(x, i), sl(y, i), s.cuda_stream)
+        # the events stay referenced until the next step
+        self._events = []
+        for i in range(self.m, 0, -1):
+            s = lanes[(i - 1) % K]
+            tgp.stage_backward_recompute(self.h, j, i, sl(dy, i), None if dx is None else sl(dx, i),
+                                         s.cuda_stream)
+            ev = torch.cuda.Event()
+            ev.record(s)
+            self._events.append(ev)
+            acc.wait_event(ev)
+            tgp.grad_accumulate(self.h, j, i, i == self.m, acc.cuda_stream)
+        for s in self._lane_streams:
+            cur.wait_stream(s)
 
     def pipeline_step(self, x: torch.Tensor, target: torch.Tensor, loss: torch.Tensor,
                       y: Optional[torch.Tensor] = None, stream: int = 0):

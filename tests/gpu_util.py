@@ -66,13 +66,13 @@ def stage_inputs(sess, j, B, dtype):
 
 
 def gpu_stage(net, dtype, B, m, mode, balance, j, want_dx=True, G_override=None, sess=None,
-              neutral=True, neutral_samples=None, stash_in=None):
+              neutral=True, neutral_samples=None, stash_in=None, lanes=1):
     n = len(balance)
     lo = sum(balance[:j - 1])
     hi = lo + balance[j - 1]
     if sess is None:
         sess = Session(net, dtype, n=n, balance=balance, bind_layers=range(lo, hi))
-        sess.plan(B, m, mode)
+        sess.plan(B, m, mode, lanes)
     xv, xraw, G = stage_inputs(sess, j, B, dtype)
     if G_override is not None:
         G = G_override
@@ -90,7 +90,7 @@ def gpu_stage(net, dtype, B, m, mode, balance, j, want_dx=True, G_override=None,
         for i in range(1, m + 1):
             sess.stash_view(i, sid, True).copy_(g[(i - 1) * b:i * b])
     torch.cuda.synchronize()
-    sess.stage_step(j, x, y, dy, dx)
+    sess.stage_step(j, x, y, dy, dx, torch.cuda.current_stream().cuda_stream)
     torch.cuda.synchronize()
     stash = {sid: torch.cat([sess.stash_view(i, sid, False) for i in range(1, m + 1)])
              for sid in ex}

@@ -164,6 +164,30 @@ def test_plan_and_workspace_validation():
     tgp.net_destroy(h)
 
 
+def test_lanes_replicate_only_the_transient_buffers():
+    """tgp_set_lanes: 1..TGP_MAX_LANES, invalidates the plan, and each extra
+    lane adds the same per-lane block (stash slots, stored activations and
+    pipeline boundaries are not replicated); several lanes add one gradient
+    slot per micro-batch."""
+    h, one = _bound_net(mode=0, B=8, m=4, n=2)
+    assert tgp.call_status("tgp_set_lanes", h, 0) == tgp.EINVAL
+    assert tgp.call_status("tgp_set_lanes", h, 17) == tgp.EINVAL
+    sizes = []
+    for k in (1, 2, 3, 4):
+        tgp.set_lanes(h, k)
+        # the plan is gone until tgp_plan runs again
+        assert tgp.call_status("tgp_bind_workspace", h, FAKE, 1 << 40) == tgp.ESTATE
+        sizes.append(tgp.plan(h, 8, 4, 0))
+    assert sizes[0] == one
+    # from two lanes on, each lane adds the same block (the per-micro-batch
+    # gradient slots appear once, at two lanes)
+    step = sizes[2] - sizes[1]
+    assert step > 0 and sizes[3] - sizes[2] == step
+    assert sizes[1] - sizes[0] > step
+    assert step < sizes[0]
+    tgp.net_destroy(h)
+
+
 def test_stage_state_machine_rejects_out_of_order_calls():
     h, nbytes = _bound_net(mode=1, B=4, m=2, n=2)
     tgp.bind_workspace(h, FAKE, nbytes)

@@ -55,6 +55,26 @@ def test_conv3x3(cin, cout, h, w, B, m):
     run_and_check(net, (1,), 1, BF16, B, m, f"conv3x3 {cin}->{cout} @{h}x{w} B={B} m={m}")
 
 
+# Configurations of the nine-tap whole-row kernel: (index, W, rows per tile).
+ROWS32 = [(0, 192, 3), (1, 192, 1), (2, 96, 6), (3, 96, 3), (4, 96, 2), (5, 48, 12),
+          (6, 48, 6), (7, 48, 4), (8, 24, 24), (9, 24, 12), (10, 24, 8)]
+
+
+@pytest.mark.parametrize("cfg,w,r", ROWS32)
+def test_rows32_configurations(cfg, w, r):
+    """Each configuration of the nine-tap whole-row kernel, forced, on a layer
+    whose last row block is ragged (H = R + 1), with four 16-channel stages
+    and two output-channel tiles; the data gradient (64 output channels from
+    128) runs the same configuration on the transposed weights."""
+    import paper_2004_09910_amd as tgp
+    old = tgp.debug_set_fwd_variant(401 + cfg)
+    try:
+        net = one_layer(Layer(CONV3X3, 64, 128), r + 1, w)
+        run_and_check(net, (1,), 1, BF16, 2, 1, f"rows32 cfg {cfg} 64->128 @{r + 1}x{w}")
+    finally:
+        tgp.debug_set_fwd_variant(old)
+
+
 def test_conv1x1_and_depthwise():
     net = one_layer(Layer(CONV1X1, 256, 256), 14, 14)
     run_and_check(net, (1,), 1, BF16, 4, 2, "conv1x1 256->256 @14x14")

@@ -63,6 +63,26 @@ def same_bits(a, b):
             np.testing.assert_array_equal(a["grads"][idx][1], b["grads"][idx][1])
 
 
+@pytest.mark.parametrize("mode", MODES)
+def test_lanes_are_bit_identical(mode):
+    """Micro-batches on 2 and 3 concurrent lane streams (each lane with its
+    own transient buffers, accumulations chained in the order m..1) give the
+    same bits as one stream: outputs, input gradients, exported-skip values
+    and every weight and bias gradient."""
+    net = specs.unet(5, 64, 64, 48, "unet5-c64-48")
+    bal = (7, 5, 3, 4)
+    runs = []
+    for k in (1, 2, 3):
+        say(f"lanes={k} mode={mode}")
+        runs.append(gpu_stage(net, BF16, 8, 4, mode, bal, 1, neutral=False, lanes=k))
+    for r in runs[1:]:
+        same_bits(runs[0], r)
+        assert torch.equal(r["y"], runs[0]["y"])
+        assert torch.equal(r["dx"], runs[0]["dx"])
+        for sid in runs[0]["stash"]:
+            assert torch.equal(r["stash"][sid], runs[0]["stash"][sid])
+
+
 def test_tiny_fp32_pipeline_all_modes():
     """4-layer conv3x3+bias+ReLU stack, C=16, 8x16x32x32 fp32, m=4, n=2."""
     wl = specs.tiny()
