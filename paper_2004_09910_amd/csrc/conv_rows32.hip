@@ -22,7 +22,8 @@
 // last waves may hold fewer real ones and compute on a clamped copy); each
 // wave covers all 64 channels (2 x FW MFMA tiles).  Blocks are persistent
 // over tiles, their stages streamed through one NS-deep LDS ring.  Bias and
-// ReLU are applied in the epilogue (the bias through scalar loads).  The K
+// ReLU are applied in the epilogue, which transposes each fragment through
+// LDS into whole pixel rows.  The K
 // order (chunk, tap, channel) is fixed by the per-sample shape, so a
 // recomputation is bit-identical.
 #include "common.h"
@@ -108,12 +109,10 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
   // region (filter row r adds r BWP rows as an immediate).
   const int abase = (lane & 31) * 32 + (((lane >> 5) ^ ((lane >> 3) & 1)) << 4);
   int bq[FW][3];
-  int opix[FW];
 #pragma unroll
   for (int j = 0; j < FW; ++j) {
     const int f = wave * FW + j;
     int tp = f * 32 + (lane & 31);
-    opix[j] = f < F ? tp : -1;
     if (tp >= R * W) tp = R * W - 1;                            // clamped copy for padding fragments
     const int rho = tp / W, w = tp - rho * W;
 #pragma unroll
@@ -132,10 +131,13 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
     co0 = ct * 64;
   };
 
-  // issue side
+  // issue side: a stage's DMA is issued in parts (u in [u0, u1)) so that
+  // inside the stage loop it is spread over the nine taps; the instruction
+  // issue stalls while the memory pipeline is full, and spread out those
+  // stalls overlap the MFMAs already queued
   int i_it = 0, i_ks = 0, i_n = 0, i_h0 = 0, i_co0 = 0;
   if (total > 0) coords(0, i_n, i_h0, i_co0);
-  auto issue = [&](int slot) __attribute__((always_inline)) {
+  auto issue_part = [&](int slot, int u0, int u1) __attribute__((always_inline)) {
     const int c0 = i_ks * 16;
     const int soff_a = (i_co0 * 9 * Cin + c0) * 2;
     const int hb = i_h0 - 1;                                    // input row of block row 0
@@ -143,6 +145,7 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
     const bool interior = hb >= 0 && hb + R + 2 <= H;
 #pragma unroll
     for (int u = 0; u < L; ++u) {
+      if (u < u0 || u >= u1) continue;
       const int k = 4 * u + wave;
       auto* dst = TGP_LDS(smem + slot * SB + k * 1024);
       if (k < ACH) {
@@ -152,6 +155,8 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
         dma16(rx, dst, ok ? base_b + doff[u] : R32_OOB, 0);
       }
     }
+  };
+  auto issue_done = [&]() __attribute__((always_inline)) {
     if (++i_ks == nk) {
       i_ks = 0;
       if (++i_it < n_items) coords(i_it, i_n, i_h0, i_co0);
@@ -160,15 +165,24 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
 
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k)
-    if (k < total) issue(k);
-
-  const __attribute__((address_space(4))) float* cbias =
-      (const __attribute__((address_space(4))) float*)bias;
+    if (k < total) {
+      issue_part(k, 0, L);
+      issue_done();
+    }
 
   int idx = 0;
   for (int c_it = 0; c_it < n_items; ++c_it) {
     int n, h0, co0;
     coords(c_it, n, h0, co0);
+    // this lane's bias values for the epilogue, loaded up front: channel
+    // co0 + 32 i + 8 g + 4 (l / 32) + e is bv[i][g][e]
+    f32x4_t bv[2][4];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        bv[i][g] = bias ? *(const f32x4_t*)(bias + co0 + 32 * i + 8 * g + 4 * (lane >> 5))
+                        : f32x4_t{};
     f32x16_t acc[2][FW];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
@@ -180,7 +194,8 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
       // issued after it are pending (epilogue stores only lengthen the wait)
       wait_stages<NS, L>(min(NS - 2, total - 1 - idx));
       ring_barrier();
-      if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);
+      const bool fill = idx + NS - 1 < total;                   // refill the slot freed last stage
+      const int fslot = (idx + NS - 1) % NS;
       const unsigned char* st = smem + (idx % NS) * SB;
       // nine taps; tap t + 1's fragments are read while tap t's MFMAs run
       bf16x8_t fa[2][2], fb[2][FW];
@@ -196,49 +211,61 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
       load(0, 0);
 #pragma unroll
       for (int t = 0; t < 9; ++t) {
+        // reads for tap t + 1, half of tap t's MFMAs, this tap's share of the
+        // next stage's DMA, the other half of the MFMAs
         if (t + 1 < 9) load(t + 1, (t + 1) & 1);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int q = 0; q < 2 * FW; ++q)
+          if (q < FW) acc[q & 1][q >> 1] = mfma32(fa[t & 1][q & 1], fb[t & 1][q >> 1], acc[q & 1][q >> 1]);
+        __builtin_amdgcn_sched_barrier(0);
+        if (fill) issue_part(fslot, t * L / 9, (t + 1) * L / 9);
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-          for (int j = 0; j < FW; ++j) acc[i][j] = mfma32(fa[t & 1][i], fb[t & 1][j], acc[i][j]);
+        for (int q = 0; q < 2 * FW; ++q)
+          if (q >= FW) acc[q & 1][q >> 1] = mfma32(fa[t & 1][q & 1], fb[t & 1][q >> 1], acc[q & 1][q >> 1]);
         __builtin_amdgcn_sched_barrier(0);
       }
+      if (fill) issue_done();
     }
 
-    // epilogue: element v of lane l is output channel co0 + 32 i + 8 (v / 4)
-    // + 4 (l / 32) + v % 4 of tile pixel opix[j]
+    // Epilogue, staged through LDS so that every store writes a whole
+    // 128-byte run of one pixel's channels (scattered 8-byte stores cost a
+    // memory-pipeline cycle per lane).  The slot of the stage just consumed
+    // is free once every wave is past its last MFMAs; its DMA refill is issued
+    // only after the next stage's barrier.  Per fragment j each wave uses its
+    // own 4 KiB: 32 pixel rows of 64 channels, 16-byte chunk c of row p at
+    // position c ^ (p % 8).  Element v of lane l of acc[i][j] is channel
+    // 32 i + 8 (v / 4) + 4 (l / 32) + v % 4 of pixel l % 32.
+    ring_barrier();
+    unsigned char* ep = smem + ((idx - 1) % NS) * SB + wave * 4096;
     const long pix0 = (long)(n * H + h0) * W;
+    const int pw = lane & 31, hw = lane >> 5;
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int j = 0; j < FW; ++j) {
 #pragma unroll
-      for (int g = 0; g < 4; ++g) {
-        const int cob = co0 + 32 * i + 8 * g;
-        const int co = cob + 4 * (lane >> 5);
-        float b4[4] = {0.f, 0.f, 0.f, 0.f};
-        if (bias) {
+      for (int i = 0; i < 2; ++i) {
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float b0 = cbias[cob + e], b1 = cbias[cob + 4 + e];
-            b4[e] = (lane >> 5) ? b1 : b0;
-          }
-        }
-#pragma unroll
-        for (int j = 0; j < FW; ++j) {
+        for (int g = 0; g < 4; ++g) {
           float v[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            v[e] = acc[i][j][4 * g + e] + b4[e];
+            v[e] = acc[i][j][4 * g + e] + bv[i][g][e];
             if (relu) v[e] = fmaxf(v[e], 0.0f);
           }
-          const int tp = opix[j];
-          if (tp >= 0 && h0 + tp / W < H) {
-            uint2 o;
-            o.x = pack2_bf16(v[0], v[1]);
-            o.y = pack2_bf16(v[2], v[3]);
-            *(uint2*)(Y + (pix0 + tp) * Cout + co) = o;
-          }
+          uint2 o;
+          o.x = pack2_bf16(v[0], v[1]);
+          o.y = pack2_bf16(v[2], v[3]);
+          *(uint2*)(ep + pw * 128 + (((4 * i + g) ^ (pw & 7)) << 4) + 8 * hw) = o;
         }
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int p = (lane >> 3) + 8 * q, c = lane & 7;
+        const u32x4 val = *(const u32x4*)(ep + p * 128 + ((c ^ (p & 7)) << 4));
+        const int tp = (wave * FW + j) * 32 + p;
+        if (wave * FW + j < F && h0 + tp / W < H)
+          *(u32x4*)(Y + (pix0 + tp) * Cout + co0 + 8 * c) = val;
       }
     }
   }
