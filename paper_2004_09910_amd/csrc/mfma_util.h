@@ -43,6 +43,19 @@ __device__ __forceinline__ void wait_vmcnt() {
 // Waits until at most `ahead` stages of LPS loads each are still in flight.
 template <int NS, int LPS>
 __device__ __forceinline__ void wait_stages(int ahead) {
+  static_assert(NS >= 2 && NS <= 8 && (NS - 2) * LPS < 64, "vmcnt range");
+  if constexpr (NS >= 8) {
+    if (ahead >= 6) { wait_vmcnt<6 * LPS>(); return; }
+  }
+  if constexpr (NS >= 7) {
+    if (ahead >= 5) { wait_vmcnt<5 * LPS>(); return; }
+  }
+  if constexpr (NS >= 6) {
+    if (ahead >= 4) { wait_vmcnt<4 * LPS>(); return; }
+  }
+  if constexpr (NS >= 5) {
+    if (ahead >= 3) { wait_vmcnt<3 * LPS>(); return; }
+  }
   if constexpr (NS >= 4) {
     if (ahead >= 2) { wait_vmcnt<2 * LPS>(); return; }
   }

@@ -63,8 +63,8 @@ __global__ __launch_bounds__(256) void conv_wgrad_rows(
   constexpr int BR = round32(RPS * BW);         // padded X rows per stage
   constexpr int SB = (AR + BR) * 128;           // stage bytes
   constexpr int LA = AR / 32, LB = BR / 32;     // DMA instructions per wave
-  constexpr int KS = W / 16;                    // k steps per image row
-  static_assert(W % 16 == 0, "k steps within an image row");
+  constexpr int KT = RPS * W / 16;               // k steps per stage
+  static_assert(RPS * W % 16 == 0 && W % 8 == 0, "k steps of 16 pixels, halves within a row");
   __shared__ __attribute__((aligned(16))) unsigned char smem[NS * SB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -115,6 +115,15 @@ __global__ __launch_bounds__(256) void conv_wgrad_rows(
 #pragma unroll
   for (int s = 0; s < 3; ++s)
     fb[s] = AR * 128 + (kb + s) * 128 + (((chb >> 4) ^ (2 * ((kb + s) & 3))) << 4) + (chb & 15);
+  // k step t covers stage pixels 16 t .. + 15; this lane group's 8 of them,
+  // 16 t + 8 (g / 2) .., lie in stage row rr = (16 t + 8 (g / 2)) / W, whose
+  // padded X block starts 4 rr rows after its pixels' own index (the B row
+  // of pixel q at column tap s is q + 4 rr + s).  With W a multiple of 16 the
+  // row is the same for the whole step and the offset is an immediate.
+  auto xoff = [&](int t) __attribute__((always_inline)) {
+    if constexpr (W % 16 == 0) return (16 * t + 4 * ((16 * t) / W)) * 128;
+    else return (16 * t + 4 * ((16 * t + 8 * (g >> 1)) / W)) * 128;
+  };
 
   auto coords = [&](int it, int& kr, int& r, int& co0, int& ci0) __attribute__((always_inline)) {
     const int item = lb + it * G;
@@ -193,20 +202,17 @@ __global__ __launch_bounds__(256) void conv_wgrad_rows(
       if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);
       const unsigned char* sp = smem + (idx % NS) * SB;
 #pragma unroll
-      for (int rr = 0; rr < RPS; ++rr) {
+      for (int t = 0; t < KT; ++t) {
+        // k step: stage pixels 16 t .. 16 t + 15 (dZ rows are the pixel index)
+        const int ka = 16 * t * 128;
+        const int kx = xoff(t);
+        const bf16x8_t a = frag2(tr16(sp + fa + ka), tr16(sp + fa + ka + 4 * 128));
+        bf16x8_t b[3];
 #pragma unroll
-        for (int t = 0; t < KS; ++t) {
-          // k step: pixels 16 t .. 16 t + 15 of stage row rr
-          const int ka = (rr * W + 16 * t) * 128;
-          const int kx = (rr * BW + 16 * t) * 128;
-          const bf16x8_t a = frag2(tr16(sp + fa + ka), tr16(sp + fa + ka + 4 * 128));
-          bf16x8_t b[3];
+        for (int s = 0; s < 3; ++s)
+          b[s] = frag2(tr16(sp + fb[s] + kx), tr16(sp + fb[s] + kx + 4 * 128));
 #pragma unroll
-          for (int s = 0; s < 3; ++s)
-            b[s] = frag2(tr16(sp + fb[s] + kx), tr16(sp + fb[s] + kx + 4 * 128));
-#pragma unroll
-          for (int s = 0; s < 3; ++s) acc[s] = mfma32(a, b[s], acc[s]);
-        }
+        for (int s = 0; s < 3; ++s) acc[s] = mfma32(a, b[s], acc[s]);
       }
     }
     // epilogue: element v of lane l is co 8 (v / 4) + 4 (l / 32) + v % 4, ci
@@ -239,7 +245,7 @@ static WgPlan wgrad_rows_plan(const ConvShape& s) {
 }
 
 bool wgrad_rows_ok(const ConvShape& s) {
-  return s.taps == 9 && (s.W == 192 || s.W == 96 || s.W == 48) && s.cin % 64 == 0 &&
+  return s.taps == 9 && (s.W == 192 || s.W == 96 || s.W == 48 || s.W == 24) && s.cin % 64 == 0 &&
          s.cout % 64 == 0 && (double)s.pixels() * (s.cin > s.cout ? s.cin : s.cout) * 2 < 2147483648.0;
 }
 
@@ -248,7 +254,7 @@ size_t wgrad_rows_partial_floats(const ConvShape& s) {
   return p.nK > 1 ? (size_t)p.nK * s.cout * 9 * s.cin : 0;
 }
 
-template <int W, int RPS>
+template <int W, int RPS, int NS>
 static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* DZ, float* out,
                                     const ConvShape& s, const WgPlan& p, hipStream_t st) {
   const long items = (long)p.nK * 3 * (s.cout / 64) * (s.cin / 64);
@@ -256,10 +262,10 @@ static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* DZ, float* ou
   const double flops = 2.0 * s.pixels() * s.cout * 9 * s.cin;
   const double bytes = 2.0 * s.pixels() * (s.cin + s.cout) + 4.0 * p.nK * s.cout * 9 * s.cin;
   static const char* names[] = {"conv_wgrad_rows<192,1,3>", "conv_wgrad_rows<96,2,3>",
-                                "conv_wgrad_rows<48,4,3>"};
-  ProfScope ps(names[W == 192 ? 0 : (W == 96 ? 1 : 2)], flops, bytes, st);
-  TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, 3>), dim3(G), dim3(256), 0, st, X, DZ, out, s.nb, s.H,
-             s.cin, s.cout, p.R);
+                                "conv_wgrad_rows<48,4,3>", "conv_wgrad_rows<24,4,5>"};
+  ProfScope ps(names[W == 192 ? 0 : (W == 96 ? 1 : (W == 48 ? 2 : 3))], flops, bytes, st);
+  TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, NS>), dim3(G), dim3(256), 0, st, X, DZ, out, s.nb,
+             s.H, s.cin, s.cout, p.R);
   return hipGetLastError();
 }
 
@@ -271,9 +277,10 @@ hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, floa
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* DZ = (const bf16_t*)dz;
   hipError_t e;
-  if (s.W == 192) e = launch_wgrad_rows<192, 1>(X, DZ, out, s, p, st);
-  else if (s.W == 96) e = launch_wgrad_rows<96, 2>(X, DZ, out, s, p, st);
-  else e = launch_wgrad_rows<48, 4>(X, DZ, out, s, p, st);
+  if (s.W == 192) e = launch_wgrad_rows<192, 1, 3>(X, DZ, out, s, p, st);
+  else if (s.W == 96) e = launch_wgrad_rows<96, 2, 3>(X, DZ, out, s, p, st);
+  else if (s.W == 48) e = launch_wgrad_rows<48, 4, 3>(X, DZ, out, s, p, st);
+  else e = launch_wgrad_rows<24, 4, 5>(X, DZ, out, s, p, st);
   if (e != hipSuccess || p.nK == 1) return e;
   return splitk_reduce_launch(partial, dw, (long)s.cout * 9 * s.cin, p.nK, st);
 }
