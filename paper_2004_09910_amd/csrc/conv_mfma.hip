@@ -955,13 +955,23 @@ __global__ __launch_bounds__(256) void conv_wgrad_mfma(
 // s = l, l + LANES, ... in ascending order, then lanes 0 .. LANES - 1 are
 // added in order.  (C4, LANES) is a function of S only, so the order is a
 // function of the shape.  E must be a multiple of 4.
+// Blocks from nblk1 on run a second, independent sum (part2, out2, E2, S2)
+// in the same launch.
 template <int C4>
 __global__ __launch_bounds__(1024) void splitk_reduce(const float* __restrict__ part,
-                                                      float* __restrict__ out, long E, int S) {
+                                                      float* __restrict__ out, long E, int S,
+                                                      const float* __restrict__ part2,
+                                                      float* __restrict__ out2, long E2, int S2,
+                                                      int nblk1) {
   constexpr int LANES = 1024 / C4;
   __shared__ float4 red[LANES][C4];
+  int bx = blockIdx.x;
+  if (bx >= nblk1) {   // block-uniform
+    bx -= nblk1;
+    part = part2; out = out2; E = E2; S = S2;
+  }
   const int col = threadIdx.x % C4, lane = threadIdx.x / C4;
-  const long e4 = ((long)blockIdx.x * C4 + col) * 4;
+  const long e4 = ((long)bx * C4 + col) * 4;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   if (e4 < E) {
     int k = lane;
@@ -1045,8 +1055,6 @@ WgradPlan wgrad_plan(long P, int tiles, long E) {
 }  // namespace
 
 // ---------------------------------------------------------------- dispatch
-
-hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st);
 
 bool mfma_conv_ok(int dt, int cin, int cout) {
   return dt == 0 && cin % 64 == 0 && cout % 64 == 0;
@@ -1368,8 +1376,8 @@ size_t wgrad_mfma_partial_floats(const ConvShape& s) {
 }
 
 hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
-                           const ConvShape& s, hipStream_t st) {
-  if (use_wgrad_rows(s)) return conv_wgrad_rows_launch(x, dz, dw, partial, s, st);
+                           const ConvShape& s, hipStream_t st, const ReduceJob* extra) {
+  if (use_wgrad_rows(s)) return conv_wgrad_rows_launch(x, dz, dw, partial, s, st, extra);
   long P = s.pixels();
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* DZ = (const bf16_t*)dz;
@@ -1404,23 +1412,43 @@ hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* part
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return pl.S == 1 ? hipSuccess : splitk_reduce_launch(partial, dw, E, pl.S, st);
+  if (pl.S == 1)
+    return extra ? splitk_reduce_launch(extra->part, extra->out, extra->E, extra->S, st) : hipSuccess;
+  return splitk_reduce_launch(partial, dw, E, pl.S, st, extra);
 }
 
-hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st) {
-  ProfScope ps("splitk_reduce", 0.0, 4.0 * E * (S + 1), st);
+hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st,
+                               const ReduceJob* extra) {
+  if (extra && (E % 4 || extra->E % 4)) {   // scalar sums run on their own
+    const hipError_t e = splitk_reduce_launch(extra->part, extra->out, extra->E, extra->S, st);
+    if (e != hipSuccess) return e;
+    extra = nullptr;
+  }
+  ProfScope ps("splitk_reduce", 0.0,
+               4.0 * E * (S + 1) + (extra ? 4.0 * extra->E * (extra->S + 1) : 0.0), st);
   if (E % 4) {
     TGP_LAUNCH(ps, splitk_reduce_scalar, dim3(cdiv(E, 256)), dim3(256), 0, st, part, out, E, S);
     return hipGetLastError();
   }
   // many splits of few columns: 16 columns x 64 split lanes; few splits:
-  // 256 columns x 4 lanes
-  if (S >= 64)
-    TGP_LAUNCH(ps, splitk_reduce<16>, dim3(cdiv(E, 64)), dim3(1024), 0, st, part, out, E, S);
-  else if (S >= 16)
-    TGP_LAUNCH(ps, splitk_reduce<64>, dim3(cdiv(E, 256)), dim3(1024), 0, st, part, out, E, S);
+  // 256 columns x 4 lanes (chosen by the first sum's S; the second, if any,
+  // uses the same layout)
+  const int C4 = S >= 64 ? 16 : (S >= 16 ? 64 : 256);
+  const int nb1 = (int)cdiv(E, 4L * C4);
+  const int nb2 = extra ? (int)cdiv(extra->E, 4L * C4) : 0;
+  const float* p2 = extra ? extra->part : nullptr;
+  float* o2 = extra ? extra->out : nullptr;
+  const long E2 = extra ? extra->E : 0;
+  const int S2 = extra ? extra->S : 0;
+  if (C4 == 16)
+    TGP_LAUNCH(ps, splitk_reduce<16>, dim3(nb1 + nb2), dim3(1024), 0, st, part, out, E, S, p2, o2,
+               E2, S2, nb1);
+  else if (C4 == 64)
+    TGP_LAUNCH(ps, splitk_reduce<64>, dim3(nb1 + nb2), dim3(1024), 0, st, part, out, E, S, p2, o2,
+               E2, S2, nb1);
   else
-    TGP_LAUNCH(ps, splitk_reduce<256>, dim3(cdiv(E, 1024)), dim3(1024), 0, st, part, out, E, S);
+    TGP_LAUNCH(ps, splitk_reduce<256>, dim3(nb1 + nb2), dim3(1024), 0, st, part, out, E, S, p2,
+               o2, E2, S2, nb1);
   return hipGetLastError();
 }
 

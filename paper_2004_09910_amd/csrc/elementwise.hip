@@ -15,8 +15,7 @@ hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void*
                              hipStream_t st);
 size_t wgrad_mfma_partial_floats(const ConvShape& s);
 hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
-                           const ConvShape& s, hipStream_t st);
-hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st);
+                           const ConvShape& s, hipStream_t st, const ReduceJob* extra);
 
 namespace {
 
@@ -557,8 +556,8 @@ size_t conv_wgrad_partial_floats(int dt, const ConvShape& s) {
 }
 
 hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial,
-                      const ConvShape& s, hipStream_t st) {
-  if (mfma_conv_ok(dt, s.cin, s.cout)) return conv_wgrad_mfma(x, dz, dw, partial, s, st);
+                      const ConvShape& s, hipStream_t st, const ReduceJob* extra) {
+  if (mfma_conv_ok(dt, s.cin, s.cout)) return conv_wgrad_mfma(x, dz, dw, partial, s, st, extra);
   long P = s.pixels();
   long E = (long)s.cout * s.taps * s.cin;
   long pps = direct_wgrad_pps(P);
@@ -576,7 +575,7 @@ hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* p
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return splitk_reduce_launch(partial, dw, E, S, st);
+  return splitk_reduce_launch(partial, dw, E, S, st, extra);
 }
 
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
@@ -678,7 +677,7 @@ size_t relu_bias_partial_floats(int dt, long P, int C) {
 
 hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
                               int relu, float* db, float* partial, long P, int C,
-                              hipStream_t st) {
+                              hipStream_t st, ReduceJob* defer) {
   long rows = relu_bias_rows(P, C, dt == 0 ? 8 : 4);
   int nb = cdiv(P, rows);
   {
@@ -695,6 +694,10 @@ hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const v
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (defer) {
+    *defer = ReduceJob{partial, db, (long)C, nb};
+    return hipSuccess;
+  }
   return splitk_reduce_launch(partial, db, C, nb, st);
 }
 

@@ -43,12 +43,22 @@ extern thread_local int t_in_dgrad;
 // (bf16; W in {48, 96, 192}, Cin and Cout multiples of 64): whether it
 // supports a shape, the fp32 partial-slice scratch it needs, and the launch
 // (dw = sum over pixels, summed over its K ranges in a fixed order).
-// out[e] = sum_{k < S} part[k E + e] in the order k = 0, 1, ..
-hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st);
+// out[e] = sum_{k < S} part[k E + e] in a fixed order that depends only on
+// (E, S); `extra`, if given, is a second independent sum of the same kind run
+// in the same launch (its order then also depends on the first sum's S).
+struct ReduceJob {
+  const float* part;
+  float* out;
+  long E;
+  int S;
+};
+hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hipStream_t st,
+                               const ReduceJob* extra = nullptr);
 bool wgrad_rows_ok(const ConvShape& s);
 size_t wgrad_rows_partial_floats(const ConvShape& s);
 hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
-                                  const ConvShape& s, hipStream_t st);
+                                  const ConvShape& s, hipStream_t st,
+                                  const ReduceJob* extra = nullptr);
 
 // Whether the data-gradient kernel for this shape reads the transformed
 // weight wt = [cin][taps][cout] (taps rotated by 180 degrees).
@@ -60,10 +70,11 @@ hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, voi
                       const ConvShape& s, float* part, size_t part_cap, hipStream_t st);
 // Weight gradient of one micro-batch into dw (float32, KRSC), via split-K
 // partials in `partial` (conv_wgrad_partial_floats floats) reduced in fixed
-// split order.
+// split order.  `extra`, if given, is a pending sum (the bias gradient's)
+// that runs in the same reduction launch.
 size_t conv_wgrad_partial_floats(int dt, const ConvShape& s);
 hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial,
-                      const ConvShape& s, hipStream_t st);
+                      const ConvShape& s, hipStream_t st, const ReduceJob* extra = nullptr);
 
 // Depthwise 3x3 (pad 1), w = [c][9].
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
@@ -124,8 +135,10 @@ hipError_t grad_accumulate_batch(const AccBatch& b, int overwrite, hipStream_t s
 bool relu_bias_fusable(int dt, int C, const void* dy, const void* dskip, const void* y,
                        const void* dz);
 size_t relu_bias_partial_floats(int dt, long P, int C);
+// With `defer`, the bias gradient's column sums are left in `partial` and
+// *defer describes the sum still to run (the caller passes it to conv_wgrad).
 hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
                               int relu, float* db, float* partial, long P, int C,
-                              hipStream_t st);
+                              hipStream_t st, ReduceJob* defer = nullptr);
 
 }  // namespace tgpk

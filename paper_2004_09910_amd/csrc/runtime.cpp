@@ -297,9 +297,14 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
     const void* dskip = d.stash_id >= 0 ? W_(N, stash_off(N, i, d.stash_id, true)) : nullptr;
     long nout = out_elems_mb(N, Lr);
     long P = (long)N->b * Lr.H * Lr.W;
+    // the bias gradient's column sums are reduced in the weight gradient's
+    // reduction launch (conv layers; a depthwise layer reduces them here)
+    tgpk::ReduceJob bias_sum{};
+    bool bias_pending = false;
     if (d.bias && tgpk::relu_bias_fusable(N->dt, d.cout, dy, dskip, y, dz)) {
+      bias_pending = d.kind != TGP_DWCONV3X3;
       HIPCHK(tgpk::relu_backward_bias(N->dt, dy, dskip, y, dz, d.relu, (float*)G_(N, i, Lr.o_gb),
-                                      colpart, P, d.cout, st),
+                                      colpart, P, d.cout, st, bias_pending ? &bias_sum : nullptr),
              "relu_backward_bias");
     } else {
       HIPCHK(tgpk::relu_backward(N->dt, dy, dskip, y, dz, d.relu, nout, st), "relu_backward");
@@ -313,7 +318,9 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
              "dw_wgrad");
     } else {
       tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
-      HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr, dz, gw, part, s, st), "conv_wgrad");
+      HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr, dz, gw, part, s, st,
+                              bias_pending ? &bias_sum : nullptr),
+             "conv_wgrad");
     }
     if (l == lo && dx_in == nullptr) break;
     void* dest_prev = (l == lo) ? dx_in : gnext;  // gradient of the pre-prologue input

@@ -270,7 +270,7 @@ static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* DZ, float* ou
 }
 
 hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
-                                  const ConvShape& s, hipStream_t st) {
+                                  const ConvShape& s, hipStream_t st, const ReduceJob* extra) {
   if (!wgrad_rows_ok(s)) return hipErrorInvalidValue;
   const WgPlan p = wgrad_rows_plan(s);
   float* out = p.nK > 1 ? partial : dw;
@@ -281,8 +281,10 @@ hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, floa
   else if (s.W == 96) e = launch_wgrad_rows<96, 2, 3>(X, DZ, out, s, p, st);
   else if (s.W == 48) e = launch_wgrad_rows<48, 4, 3>(X, DZ, out, s, p, st);
   else e = launch_wgrad_rows<24, 4, 5>(X, DZ, out, s, p, st);
-  if (e != hipSuccess || p.nK == 1) return e;
-  return splitk_reduce_launch(partial, dw, (long)s.cout * 9 * s.cin, p.nK, st);
+  if (e != hipSuccess) return e;
+  if (p.nK == 1)
+    return extra ? splitk_reduce_launch(extra->part, extra->out, extra->E, extra->S, st) : e;
+  return splitk_reduce_launch(partial, dw, (long)s.cout * 9 * s.cin, p.nK, st, extra);
 }
 
 }  // namespace tgpk
