@@ -158,13 +158,16 @@ class Session:
         return self.mode == specs.CKPT_ALWAYS or (self.mode == specs.CKPT_EXCEPT_LAST and i < self.m)
 
     def stage_step(self, j: int, x: torch.Tensor, y: torch.Tensor, dy: torch.Tensor,
-                   dx: Optional[torch.Tensor], stream: int = 0):
+                   dx: Optional[torch.Tensor], stream: int = 0, serial: bool = False):
         """All m forwards of partition j, then backward + accumulate for
         i = m..1 (one stage's work per mini-batch).  Tensors are full-batch
-        NHWC; micro-batch slices are pointer offsets."""
+        NHWC; micro-batch slices are pointer offsets.  With several lanes the
+        micro-batches run on lane streams forked from torch's current stream
+        (`stream` is then unused) unless `serial`, which issues everything on
+        `stream` in order."""
         def sl(t, i):
             return t.data_ptr() + (i - 1) * (t.numel() // self.m) * t.element_size()
-        if self.lanes > 1:
+        if self.lanes > 1 and not serial:
             return self._stage_step_lanes(j, x, y, dy, dx, sl)
         for i in range(1, self.m + 1):
             tgp.stage_forward(self.h, j, i, self.checkpointed(i), sl(x, i), sl(y, i), stream)
