@@ -18,9 +18,10 @@
 // all three filter rows, and no fragment is masked: the zero padding and the
 // rows outside the image are buffer reads at out-of-range offsets.
 //
-// The tile's R W / 32 pixel fragments are dealt to the 4 waves, FW each (the
-// last waves may hold fewer real ones and compute on a clamped copy); each
-// wave covers all 64 channels (2 x FW MFMA tiles).  Blocks are persistent
+// The tile's R W / 32 pixel fragments are dealt to 4 pixel groups, FW each
+// (the last groups may hold fewer real ones and compute on a clamped copy);
+// with 4 waves each wave is a pixel group over all 64 channels (2 x FW MFMA
+// tiles), with 8 waves two waves share a group, one per 32-channel half.  Blocks are persistent
 // over tiles, their stages streamed through one NS-deep LDS ring.  Bias and
 // ReLU are applied in the epilogue, which transposes each fragment through
 // LDS into whole pixel rows.  The K
@@ -55,19 +56,29 @@ struct Rows32Geom {
   static_assert(R32_AROWS * 32 % 1024 == 0, "weight region ends on a DMA chunk");
 };
 
-template <int W, int R, int FW, int NS>
-__global__ __launch_bounds__(256) void conv3x3_rows32(
+// CH is the number of 32-channel halves a wave covers: CH = 2 runs 4 waves
+// (one per SIMD), each over all 64 channels; CH = 1 runs 8 waves (two per
+// SIMD), the two waves of a SIMD on the two channel halves of the same
+// pixels, so that one wave's MFMAs run while the other waits on its DMA
+// issue or its LDS reads.
+template <int W, int R, int FW, int NS, int CH>
+__global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
     const float* __restrict__ bias, bf16_t* __restrict__ Y, int nb, int H, int Cin,
     int Cout, int relu) {
   typedef Rows32Geom<W, R> G_;
-  constexpr int BWP = G_::BWP, SB = G_::SB, L = G_::L, F = G_::F;
+  constexpr int BWP = G_::BWP, SB = G_::SB, F = G_::F;
+  constexpr int NW = CH == 2 ? 4 : 8;                           // waves
+  constexpr int NCH = SB / 1024;                                // DMA chunks per stage
+  constexpr int LW = (NCH + NW - 1) / NW;                       // ... per wave, at most
   constexpr int ACH = R32_AROWS * 32 / 1024;                    // DMA chunks of weights
-  static_assert(F <= 4 * FW, "fragments per wave");
+  static_assert(F <= 4 * FW, "fragments per pixel group");
   static_assert(NS * SB <= 160 * 1024, "LDS ring");
   __shared__ __attribute__((aligned(16))) unsigned char smem[NS * SB];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int pg = wave & 3;                                      // pixel group (the SIMD)
+  const int chf = CH == 2 ? 0 : wave >> 2;                      // channel half (CH = 1)
   const int nrb = (H + R - 1) / R;                              // row blocks per sample
   const int nct = Cout / 64;
   const int items = nb * nrb * nct;
@@ -76,18 +87,29 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
   const int n_items = lb < items ? (items - lb + G - 1) / G : 0;
   const int nk = Cin / 16;                                      // stages per tile
   const int total = n_items * nk;
+  // DMA instructions of this wave per stage (waits count them)
+  const bool full = NCH % NW == 0 || wave < NCH % NW;
+  auto wait_ring = [&](int ahead) __attribute__((always_inline)) {
+    if constexpr (NCH % NW == 0) {
+      wait_stages<NS, LW>(ahead);
+    } else {
+      if (full) wait_stages<NS, LW>(ahead);
+      else wait_stages<NS, LW - 1>(ahead);
+    }
+  };
 
   const u32x4 rx = make_rsrc(X, nb * H * W * Cin * 2);
   const u32x4 rw = make_rsrc(Wt, Cout * 9 * Cin * 2);
 
-  // DMA: instruction u of this wave fills stage chunk k = 4 u + wave (1 KiB);
-  // lane l the 16 bytes at + 16 l: row k * 32 + l / 2, physical half l % 2,
-  // which holds logical half (l % 2) ^ bit 3 of the row.  Chunks below ACH
-  // are weight rows (tap, channel), the rest input rows (block row, pixel).
-  int doff[L], drow[L];
+  // DMA: instruction u of this wave fills stage chunk k = NW u + wave
+  // (1 KiB); lane l the 16 bytes at + 16 l: row k * 32 + l / 2, physical half
+  // l % 2, which holds logical half (l % 2) ^ bit 3 of the row.  Chunks below
+  // ACH are weight rows (tap, channel), the rest input rows (block row,
+  // pixel).
+  int doff[LW], drow[LW];
 #pragma unroll
-  for (int u = 0; u < L; ++u) {
-    const int k = 4 * u + wave;
+  for (int u = 0; u < LW; ++u) {
+    const int k = NW * u + wave;
     const int row = k * 32 + (lane >> 1);
     const int lh = (lane & 1) ^ ((row >> 3) & 1);
     if (k < ACH) {
@@ -104,14 +126,15 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
   }
 
   // Fragment addresses (bytes within a stage).  A: weight row tap * 64 +
-  // 32 i + l % 32 at logical half l / 32, tap and i as immediates.  B: for
-  // each fragment j and column tap s, LDS row rho BWP + w + s of the input
-  // region (filter row r adds r BWP rows as an immediate).
-  const int abase = (lane & 31) * 32 + (((lane >> 5) ^ ((lane >> 3) & 1)) << 4);
+  // 32 (channel half) + l % 32 at logical half l / 32, tap as an immediate.
+  // B: for each fragment j of the pixel group and column tap s, LDS row
+  // rho BWP + w + s of the input region (filter row r adds r BWP rows as an
+  // immediate).
+  const int abase = (lane & 31) * 32 + (((lane >> 5) ^ ((lane >> 3) & 1)) << 4) + chf * 32 * 32;
   int bq[FW][3];
 #pragma unroll
   for (int j = 0; j < FW; ++j) {
-    const int f = wave * FW + j;
+    const int f = pg * FW + j;
     int tp = f * 32 + (lane & 31);
     if (tp >= R * W) tp = R * W - 1;                            // clamped copy for padding fragments
     const int rho = tp / W, w = tp - rho * W;
@@ -144,9 +167,10 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
     const int base_b = ((i_n * H + hb) * W * Cin + c0) * 2;    // negative for hb = -1
     const bool interior = hb >= 0 && hb + R + 2 <= H;
 #pragma unroll
-    for (int u = 0; u < L; ++u) {
+    for (int u = 0; u < LW; ++u) {
       if (u < u0 || u >= u1) continue;
-      const int k = 4 * u + wave;
+      const int k = NW * u + wave;
+      if (NCH % NW != 0 && k >= NCH) continue;                  // wave-uniform
       auto* dst = TGP_LDS(smem + slot * SB + k * 1024);
       if (k < ACH) {
         dma16(rw, dst, doff[u], soff_a);
@@ -166,7 +190,7 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k)
     if (k < total) {
-      issue_part(k, 0, L);
+      issue_part(k, 0, LW);
       issue_done();
     }
 
@@ -175,40 +199,42 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
     int n, h0, co0;
     coords(c_it, n, h0, co0);
     // this lane's bias values for the epilogue, loaded up front: channel
-    // co0 + 32 i + 8 g + 4 (l / 32) + e is bv[i][g][e]
-    f32x4_t bv[2][4];
+    // co0 + 32 (half) + 8 g + 4 (l / 32) + e is bv[i][g][e], half = i (CH = 2)
+    // or chf (CH = 1)
+    f32x4_t bv[CH][4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < CH; ++i)
 #pragma unroll
       for (int g = 0; g < 4; ++g)
-        bv[i][g] = bias ? *(const f32x4_t*)(bias + co0 + 32 * i + 8 * g + 4 * (lane >> 5))
+        bv[i][g] = bias ? *(const f32x4_t*)(bias + co0 + 32 * (i + chf) + 8 * g + 4 * (lane >> 5))
                         : f32x4_t{};
-    f32x16_t acc[2][FW];
+    f32x16_t acc[CH][FW];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < CH; ++i)
 #pragma unroll
       for (int j = 0; j < FW; ++j) acc[i][j] = f32x16_t{};
 
     for (int ks = 0; ks < nk; ++ks, ++idx) {
       // loads complete in order: stage idx is in once at most the stages
       // issued after it are pending (epilogue stores only lengthen the wait)
-      wait_stages<NS, L>(min(NS - 2, total - 1 - idx));
+      wait_ring(min(NS - 2, total - 1 - idx));
       ring_barrier();
       const bool fill = idx + NS - 1 < total;                   // refill the slot freed last stage
       const int fslot = (idx + NS - 1) % NS;
       const unsigned char* st = smem + (idx % NS) * SB;
       // nine taps; tap t + 1's fragments are read while tap t's MFMAs run
-      bf16x8_t fa[2][2], fb[2][FW];
+      bf16x8_t fa[2][CH], fb[2][FW];
       auto load = [&](int t, int buf) __attribute__((always_inline)) {
         const int r = t / 3, s = t - 3 * (t / 3);
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < CH; ++i)
           fa[buf][i] = as_bf16x8(*(const u32x4*)(st + abase + (t * 64 + 32 * i) * 32));
 #pragma unroll
         for (int j = 0; j < FW; ++j)
           fb[buf][j] = as_bf16x8(*(const u32x4*)(st + bq[j][s] + r * BWP * 32));
       };
       load(0, 0);
+      constexpr int NQ = CH * FW;                               // MFMAs per tap
 #pragma unroll
       for (int t = 0; t < 9; ++t) {
         // reads for tap t + 1, half of tap t's MFMAs, this tap's share of the
@@ -216,35 +242,40 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
         if (t + 1 < 9) load(t + 1, (t + 1) & 1);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int q = 0; q < 2 * FW; ++q)
-          if (q < FW) acc[q & 1][q >> 1] = mfma32(fa[t & 1][q & 1], fb[t & 1][q >> 1], acc[q & 1][q >> 1]);
+        for (int q = 0; q < NQ; ++q)
+          if (q < NQ / 2)
+            acc[q % CH][q / CH] = mfma32(fa[t & 1][q % CH], fb[t & 1][q / CH], acc[q % CH][q / CH]);
         __builtin_amdgcn_sched_barrier(0);
-        if (fill) issue_part(fslot, t * L / 9, (t + 1) * L / 9);
+        if (fill) issue_part(fslot, t * LW / 9, (t + 1) * LW / 9);
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int q = 0; q < 2 * FW; ++q)
-          if (q >= FW) acc[q & 1][q >> 1] = mfma32(fa[t & 1][q & 1], fb[t & 1][q >> 1], acc[q & 1][q >> 1]);
+        for (int q = 0; q < NQ; ++q)
+          if (q >= NQ / 2)
+            acc[q % CH][q / CH] = mfma32(fa[t & 1][q % CH], fb[t & 1][q / CH], acc[q % CH][q / CH]);
         __builtin_amdgcn_sched_barrier(0);
       }
       if (fill) issue_done();
     }
 
-    // Epilogue, staged through LDS so that every store writes a whole
-    // 128-byte run of one pixel's channels (scattered 8-byte stores cost a
-    // memory-pipeline cycle per lane).  The slot of the stage just consumed
-    // is free once every wave is past its last MFMAs; its DMA refill is issued
-    // only after the next stage's barrier.  Per fragment j each wave uses its
-    // own 4 KiB: 32 pixel rows of 64 channels, 16-byte chunk c of row p at
-    // position c ^ (p % 8).  Element v of lane l of acc[i][j] is channel
-    // 32 i + 8 (v / 4) + 4 (l / 32) + v % 4 of pixel l % 32.
+    // Epilogue, staged through LDS so that every store writes whole runs of
+    // one pixel's channels (scattered 8-byte stores cost a memory-pipeline
+    // cycle per lane).  The slot of the stage just consumed is free once
+    // every wave is past its last MFMAs; its DMA refill is issued only after
+    // the next stage's barrier.  Per fragment j each wave uses its own 4 KiB
+    // (CH = 2: 32 pixel rows of 64 channels, 16-byte chunk c of row p at
+    // position c ^ (p % 8)) or 2 KiB (CH = 1: rows of 32 channels, chunk c at
+    // c ^ (p % 4)).  Element v of lane l of acc[i][j] is channel 32 (half) +
+    // 8 (v / 4) + 4 (l / 32) + v % 4 of pixel l % 32.
     ring_barrier();
-    unsigned char* ep = smem + ((idx - 1) % NS) * SB + wave * 4096;
+    constexpr int ROWB = 64 * CH;                               // staged bytes per pixel
+    constexpr int NCK = 4 * CH;                                 // 16-byte chunks per pixel
+    unsigned char* ep = smem + ((idx - 1) % NS) * SB + wave * 32 * ROWB;
     const long pix0 = (long)(n * H + h0) * W;
     const int pw = lane & 31, hw = lane >> 5;
 #pragma unroll
     for (int j = 0; j < FW; ++j) {
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
+      for (int i = 0; i < CH; ++i) {
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
           float v[4];
@@ -256,36 +287,41 @@ __global__ __launch_bounds__(256) void conv3x3_rows32(
           uint2 o;
           o.x = pack2_bf16(v[0], v[1]);
           o.y = pack2_bf16(v[2], v[3]);
-          *(uint2*)(ep + pw * 128 + (((4 * i + g) ^ (pw & 7)) << 4) + 8 * hw) = o;
+          *(uint2*)(ep + pw * ROWB + (((4 * i + g) ^ (pw & (NCK - 1))) << 4) + 8 * hw) = o;
         }
       }
+      constexpr int PPI = 64 / NCK;                             // pixels per read
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int p = (lane >> 3) + 8 * q, c = lane & 7;
-        const u32x4 val = *(const u32x4*)(ep + p * 128 + ((c ^ (p & 7)) << 4));
-        const int tp = (wave * FW + j) * 32 + p;
-        if (wave * FW + j < F && h0 + tp / W < H)
-          *(u32x4*)(Y + (pix0 + tp) * Cout + co0 + 8 * c) = val;
+      for (int q = 0; q < 32 / PPI; ++q) {
+        const int p = lane / NCK + PPI * q, c = lane % NCK;
+        const u32x4 val = *(const u32x4*)(ep + p * ROWB + ((c ^ (p & (NCK - 1))) << 4));
+        const int tp = (pg * FW + j) * 32 + p;
+        if (pg * FW + j < F && h0 + tp / W < H)
+          *(u32x4*)(Y + (pix0 + tp) * Cout + co0 + 32 * chf + 8 * c) = val;
       }
     }
   }
 }
 
-struct R32Cfg { int W, R, FW, NS; };
+struct R32Cfg { int W, R, FW, NS, CH; };
 constexpr R32Cfg kR32Cfgs[] = {
-    {192, 3, 5, 3}, {192, 1, 2, 4},
-    {96, 6, 5, 3},  {96, 3, 3, 4},  {96, 2, 2, 4},
-    {48, 12, 5, 3}, {48, 6, 3, 4},  {48, 4, 2, 4},
-    {24, 24, 5, 3}, {24, 12, 3, 4}, {24, 8, 2, 4},
+    {192, 3, 5, 3, 2}, {192, 1, 2, 4, 2},
+    {96, 6, 5, 3, 2},  {96, 3, 3, 4, 2},  {96, 2, 2, 4, 2},
+    {48, 12, 5, 3, 2}, {48, 6, 3, 4, 2},  {48, 4, 2, 4, 2},
+    {24, 24, 5, 3, 2}, {24, 12, 3, 4, 2}, {24, 8, 2, 4, 2},
+    // eight waves, two per SIMD
+    {192, 3, 5, 3, 1}, {96, 3, 3, 4, 1}, {96, 2, 2, 4, 1}, {48, 4, 2, 4, 1}, {24, 8, 2, 4, 1},
 };
 constexpr int kR32N = sizeof(kR32Cfgs) / sizeof(kR32Cfgs[0]);
 
 }  // namespace
 
-// Configuration for a per-sample shape: among those for its width, the one
-// with the fewest rounds of 256 tiles (for a nominal 4-sample micro-batch)
-// times fragments per wave.  Returns an index into kR32Cfgs, or -1.
+// Configuration for a per-sample shape: among those for its width and the
+// chosen wave layout (eight waves unless measuring), the one with the fewest
+// rounds of 256 tiles (for a nominal 4-sample micro-batch) times fragments
+// per wave.  Returns an index into kR32Cfgs, or -1.
 int g_rows32_cfg = -1;   // >= 0 forces a configuration (measurement only)
+int g_rows32_ch = 1;     // channel halves per wave the automatic choice uses
 
 static int rows32_pick(const ConvShape& s) {
   if (s.taps != 9 || s.cin % 16 || s.cout % 64) return -1;
@@ -294,6 +330,7 @@ static int rows32_pick(const ConvShape& s) {
   for (int c = 0; c < kR32N; ++c) {
     const R32Cfg k = kR32Cfgs[c];
     if (k.W != s.W || k.R > s.H) continue;
+    if (g_rows32_cfg < 0 && k.CH != g_rows32_ch) continue;
     const long items = 4L * ((s.H + k.R - 1) / k.R) * (s.cout / 64);
     const long cost = (items + 255) / 256 * k.FW;
     if (g_rows32_cfg == c || (g_rows32_cfg < 0 && (best < 0 || cost < best_cost))) {
@@ -309,13 +346,14 @@ bool conv_rows32_ok(const ConvShape& s) {
          (double)s.cout * 9 * s.cin * 2 < 2147483648.0;
 }
 
-template <int W, int R, int FW, int NS>
+template <int W, int R, int FW, int NS, int CH>
 static hipError_t launch_rows32(const bf16_t* X, const bf16_t* Wt, const float* b, bf16_t* Y,
                                 const ConvShape& s, int relu, hipStream_t st) {
   static const char* name = nullptr;
   static char buf[64];
   if (!name) {
-    snprintf(buf, sizeof buf, "conv3x3_rows32<%d,%d,%d,%d>", W, R, FW, NS);
+    if (CH == 2) snprintf(buf, sizeof buf, "conv3x3_rows32<%d,%d,%d,%d>", W, R, FW, NS);
+    else snprintf(buf, sizeof buf, "conv3x3_rows32<%d,%d,%d,%d,8w>", W, R, FW, NS);
     name = buf;
   }
   const long items = (long)s.nb * ((s.H + R - 1) / R) * (s.cout / 64);
@@ -324,8 +362,8 @@ static hipError_t launch_rows32(const bf16_t* X, const bf16_t* Wt, const float* 
   const long P = s.pixels();
   ProfScope ps(name, 2.0 * P * s.cout * 9 * s.cin,
                2.0 * ((double)P * s.cin + 9.0 * s.cin * s.cout + (double)P * s.cout), st);
-  TGP_LAUNCH(ps, (conv3x3_rows32<W, R, FW, NS>), dim3(G), dim3(256), 0, st, X, Wt, b, Y, s.nb,
-             s.H, s.cin, s.cout, relu);
+  TGP_LAUNCH(ps, (conv3x3_rows32<W, R, FW, NS, CH>), dim3(G), dim3(CH == 2 ? 256 : 512), 0, st, X,
+             Wt, b, Y, s.nb, s.H, s.cin, s.cout, relu);
   return hipGetLastError();
 }
 
@@ -339,10 +377,11 @@ hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, voi
   switch (c) {
 #define R32_CASE(i)                                                                      \
   case i:                                                                                \
-    return launch_rows32<kR32Cfgs[i].W, kR32Cfgs[i].R, kR32Cfgs[i].FW, kR32Cfgs[i].NS>( \
-        X, Wt, b, Y, s, relu, st);
+    return launch_rows32<kR32Cfgs[i].W, kR32Cfgs[i].R, kR32Cfgs[i].FW, kR32Cfgs[i].NS,   \
+                         kR32Cfgs[i].CH>(X, Wt, b, Y, s, relu, st);
     R32_CASE(0) R32_CASE(1) R32_CASE(2) R32_CASE(3) R32_CASE(4) R32_CASE(5)
-    R32_CASE(6) R32_CASE(7) R32_CASE(8) R32_CASE(9) R32_CASE(10)
+    R32_CASE(6) R32_CASE(7) R32_CASE(8) R32_CASE(9) R32_CASE(10) R32_CASE(11)
+    R32_CASE(12) R32_CASE(13) R32_CASE(14) R32_CASE(15)
 #undef R32_CASE
     default: return hipErrorInvalidValue;
   }

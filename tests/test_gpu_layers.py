@@ -58,7 +58,9 @@ def test_conv3x3(cin, cout, h, w, B, m):
 
 # Configurations of the nine-tap whole-row kernel: (index, W, rows per tile).
 ROWS32 = [(0, 192, 3), (1, 192, 1), (2, 96, 6), (3, 96, 3), (4, 96, 2), (5, 48, 12),
-          (6, 48, 6), (7, 48, 4), (8, 24, 24), (9, 24, 12), (10, 24, 8)]
+          (6, 48, 6), (7, 48, 4), (8, 24, 24), (9, 24, 12), (10, 24, 8),
+          # eight-wave layouts
+          (11, 192, 3), (12, 96, 3), (13, 96, 2), (14, 48, 4), (15, 24, 8)]
 
 
 @pytest.mark.parametrize("cfg,w,r", ROWS32)
