@@ -95,7 +95,15 @@ def short_kernel_name(full):
     n = n[:cut]
     head, sep, tail = n.partition("<")
     head = head.split("::")[-1]
-    return (head + sep + tail).replace(" ", "")
+    n = (head + sep + tail).replace(" ", "")
+    # the wave-layout template argument is named the way the launchers name
+    # their profiling scopes: ",8w" for the eight-wave layouts, else nothing
+    args = tail.rstrip(">").replace(" ", "").split(",") if sep else []
+    if head == "conv3x3_rows32" and len(args) == 5:
+        n = f"{head}<{','.join(args[:4])}{',8w' if args[4] == '1' else ''}>"
+    elif head == "conv_wgrad_rows" and len(args) == 4:
+        n = f"{head}<{','.join(args[:3])}{',8w' if args[3] == '2' else ''}>"
+    return n
 
 
 def _counter_means(path):

@@ -238,7 +238,8 @@ tgp_status tgp_profile_clear(void);
  * plan: bit 0 the row-tiled kernel for forward calls, bit 1 for data-gradient
  * calls, bit 2 the row-blocked weight gradient, bit 3 the nine-tap whole-row
  * kernel (default: bits 0-3 set); bit 4 makes the nine-tap kernel use its
- * four-wave layouts instead of the eight-wave ones. */
+ * four-wave layouts instead of the eight-wave ones, bit 5 makes the
+ * row-blocked weight gradient use its four-wave layout at every width. */
 int tgp_debug_set_fwd_variant(int v);
 int tgp_debug_set_rowtile_mask(int m);
 

@@ -38,6 +38,7 @@ hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, voi
                                const ConvShape& s, int relu, hipStream_t st);
 extern int g_rows32_cfg;
 extern int g_rows32_ch;
+extern int g_wgrad_ks;
 extern int g_rowtile_mask;
 extern thread_local int t_in_dgrad;
 // Row-blocked 3x3 weight gradient on 32x32x16 MFMA with transpose LDS reads

@@ -499,6 +499,7 @@ extern int g_fwd_order;
 extern int g_fwd_split;
 extern int g_rowtile_mask;
 extern int g_rows32_ch;
+extern int g_wgrad_ks;
 }
 
 extern "C" {
@@ -521,6 +522,7 @@ int tgp_debug_set_rowtile_mask(int v) {
   int old = tgpk::g_rowtile_mask;
   tgpk::g_rowtile_mask = v;
   tgpk::g_rows32_ch = (v >> 4 & 1) ? 2 : 1;
+  tgpk::g_wgrad_ks = (v >> 5 & 1) ? 1 : 0;
   return old;
 }
 int tgp_debug_set_fwd_order(int v) {

@@ -54,21 +54,41 @@ __device__ __forceinline__ bf16x8_t frag2(s16x4 lo, s16x4 hi) {
 
 constexpr int round32(int v) { return (v + 31) / 32 * 32; }
 
-template <int W, int RPS, int NS>
-__global__ __launch_bounds__(256) void conv_wgrad_rows(
+// Barrier after LDS writes (or before LDS writes over data) that other waves
+// of the block read (or wrote) on the other side: this wave's LDS accesses
+// have completed when it arrives, and the compiler moves none across it.
+__device__ __forceinline__ void lds_handoff_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// KS is the number of waves per SIMD: with KS = 2 the two waves of a SIMD
+// own the same 32 x 32 quarter and take alternate k steps, and the second's
+// sums are added to the first's through LDS before the store, so one wave's
+// MFMAs run while the other waits on its DMA issue or LDS reads.
+template <int W, int RPS, int NS, int KS>
+__global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ dZ, float* __restrict__ out,
     int nb, int H, int Cin, int Cout, int R) {
   constexpr int AR = round32(RPS * W);          // dZ rows per stage
   constexpr int BW = W + 4;                     // LDS rows per padded input row
   constexpr int BR = round32(RPS * BW);         // padded X rows per stage
   constexpr int SB = (AR + BR) * 128;           // stage bytes
-  constexpr int LA = AR / 32, LB = BR / 32;     // DMA instructions per wave
+  constexpr int NW = 4 * KS;                    // waves
+  constexpr int AC = AR / 8, BC = BR / 8;       // DMA chunks (8 rows, 1 KiB) per region
+  constexpr int LA = (AC + NW - 1) / NW, LB = (BC + NW - 1) / NW;   // per wave, at most
   constexpr int KT = RPS * W / 16;               // k steps per stage
   static_assert(RPS * W % 16 == 0 && W % 8 == 0, "k steps of 16 pixels, halves within a row");
+  static_assert(KT % KS == 0, "k steps shared evenly");
+  static_assert(NW * 2048 <= SB, "exchange of the sums fits a slot");
   __shared__ __attribute__((aligned(16))) unsigned char smem[NS * SB];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int cw = wave >> 1, nw = wave & 1;      // this wave's co / ci halves
+  // the wave index is uniform: readfirstlane lets the compiler branch on it
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qw = wave & 3, kh = wave >> 2;      // quarter of the item, k-step phase
+  const int cw = qw >> 1, nw = qw & 1;          // this wave's co / ci halves
   const int nct = Cout / 64, ncit = Cin / 64;
   const int nrb = (H + R - 1) / R;
   const int per_k = 3 * nct * ncit;             // items per K range
@@ -77,31 +97,45 @@ __global__ __launch_bounds__(256) void conv_wgrad_rows(
   const int lb = xcd_remap(blockIdx.x, G);
   const int n_items = lb < items ? (items - lb + G - 1) / G : 0;
   const long E = (long)Cout * 9 * Cin;
-  const int spr = (R + RPS - 1) / RPS;          // stages per full row block
 
   const u32x4 rz = make_rsrc(dZ, nb * H * W * Cout * 2);
   const u32x4 rx = make_rsrc(X, nb * H * W * Cin * 2);
 
-  // DMA lane constants: instruction u of this wave fills rows (4 u + wave) * 8
-  // + lane / 8 of the A (u < LA) or B region, physical chunk lane % 8, which
-  // holds logical chunk (lane % 8) ^ (2 (row & 3)).
+  // DMA lane constants: instruction u of this wave fills chunk c = NW u +
+  // wave of the A (dZ) or B (padded X) region, rows 8 c + lane / 8, physical
+  // chunk lane % 8, which holds logical chunk (lane % 8) ^ (2 (row & 3)).
+  // Chunks past a region's end are not issued (wave-uniform).
   int aoff[LA], arow[LA], boff[LB], brow[LB];
 #pragma unroll
-  for (int u = 0; u < LA + LB; ++u) {
-    const int row = (u < LA ? u : u - LA) * 32 + wave * 8 + (lane >> 3);
+  for (int u = 0; u < LA; ++u) {
+    const int row = (NW * u + wave) * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ (2 * (row & 3));
-    if (u < LA) {
-      const int rr = row / W, w = row - rr * W;
-      const bool ok = row < RPS * W;
-      aoff[u < LA ? u : 0] = ok ? ((rr * W + w) * Cout + 8 * lc) * 2 : WG_OOB;
-      arow[u < LA ? u : 0] = ok ? rr : -1;
-    } else {
-      const int rr = row / BW, q = row - rr * BW;
-      const bool ok = rr < RPS && q >= 1 && q <= W;
-      boff[u < LA ? 0 : u - LA] = ok ? ((rr * W + q - 1) * Cin + 8 * lc) * 2 : WG_OOB;
-      brow[u < LA ? 0 : u - LA] = ok ? rr : -1;
-    }
+    const int rr = row / W, w = row - rr * W;
+    const bool ok = row < RPS * W;
+    aoff[u] = ok ? ((rr * W + w) * Cout + 8 * lc) * 2 : WG_OOB;
+    arow[u] = ok ? rr : -1;
   }
+#pragma unroll
+  for (int u = 0; u < LB; ++u) {
+    const int row = (NW * u + wave) * 8 + (lane >> 3);
+    const int lc = (lane & 7) ^ (2 * (row & 3));
+    const int rr = row / BW, q = row - rr * BW;
+    const bool ok = rr < RPS && q >= 1 && q <= W;
+    boff[u] = ok ? ((rr * W + q - 1) * Cin + 8 * lc) * 2 : WG_OOB;
+    brow[u] = ok ? rr : -1;
+  }
+  // DMA instructions this wave issues per stage (the waits count them)
+  const int na = (AC - wave + NW - 1) / NW, nbq = (BC - wave + NW - 1) / NW;
+  const int mine = na + nbq;
+  auto wait_ring = [&](int ahead) __attribute__((always_inline)) {
+    if constexpr (AC % NW == 0 && BC % NW == 0) {
+      wait_stages<NS, LA + LB>(ahead);
+    } else {
+      if (mine == LA + LB) wait_stages<NS, LA + LB>(ahead);
+      else if (mine == LA + LB - 1) wait_stages<NS, LA + LB - 1>(ahead);
+      else wait_stages<NS, LA + LB - 2>(ahead);
+    }
+  };
 
   // Fragment lane constants (byte offsets in a stage).  Lane group g = lane /
   // 16 holds MFMA rows / columns 16 (g % 2) .. + 15 and k 8 (g / 2) .. + 7;
@@ -153,19 +187,22 @@ __global__ __launch_bounds__(256) void conv_wgrad_rows(
     const int hb = h + i_r - 1;                              // input row of stage row 0
     const int xsoff = (((n * H + hb) * W) * Cin + i_ci0) * 2;
 #pragma unroll
-    for (int u = 0; u < LA + LB; ++u) {
-      auto* dst = TGP_LDS(smem + slot * SB + (u < LA ? u * 32 : AR + (u - LA) * 32) * 128 + wave * 1024);
-      if (u < LA) {
-        const int k = u < LA ? u : 0;
-        const bool ok = arow[k] >= 0 && h + arow[k] < H;
-        dma16(rz, dst, ok ? aoff[k] + zsoff : WG_OOB, 0);
-      } else {
-        const int k = u < LA ? 0 : u - LA;
-        const bool ok = brow[k] >= 0 && (unsigned)(hb + brow[k]) < (unsigned)H && h + brow[k] < H;
-        // the row offset can be negative for filter row 0 (rows above are
-        // out of range there), so it goes into the per-lane offset
-        dma16(rx, dst, ok ? boff[k] + xsoff : WG_OOB, 0);
-      }
+    for (int u = 0; u < LA; ++u) {
+      const int c = NW * u + wave;
+      if (AC % NW != 0 && c >= AC) continue;                 // wave-uniform
+      auto* dst = TGP_LDS(smem + slot * SB + c * 1024);
+      const bool ok = arow[u] >= 0 && h + arow[u] < H;
+      dma16(rz, dst, ok ? aoff[u] + zsoff : WG_OOB, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < LB; ++u) {
+      const int c = NW * u + wave;
+      if (BC % NW != 0 && c >= BC) continue;                 // wave-uniform
+      auto* dst = TGP_LDS(smem + slot * SB + AR * 128 + c * 1024);
+      const bool ok = brow[u] >= 0 && (unsigned)(hb + brow[u]) < (unsigned)H && h + brow[u] < H;
+      // the row offset can be negative for filter row 0 (rows above are out
+      // of range there), so it goes into the per-lane offset
+      dma16(rx, dst, ok ? boff[u] + xsoff : WG_OOB, 0);
     }
     if (++i_st == i_ns) {
       i_st = 0;
@@ -197,15 +234,19 @@ __global__ __launch_bounds__(256) void conv_wgrad_rows(
     for (int st = 0; st < ns; ++st, ++idx) {
       // loads complete in order: stage idx is in once at most the stages
       // issued after it are pending (epilogue stores only lengthen this wait)
-      wait_stages<NS, LA + LB>(min(NS - 2, total - 1 - idx));
+      wait_ring(min(NS - 2, total - 1 - idx));
       ring_barrier();
       if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);
       const unsigned char* sp = smem + (idx % NS) * SB;
 #pragma unroll
-      for (int t = 0; t < KT; ++t) {
-        // k step: stage pixels 16 t .. 16 t + 15 (dZ rows are the pixel index)
+      for (int tt = 0; tt < KT / KS; ++tt) {
+        // k step t: stage pixels 16 t .. 16 t + 15 (dZ rows are the pixel
+        // index); with KS = 2 this wave takes every other step
+        const int t = KS * tt + (KS == 1 ? 0 : kh);
         const int ka = 16 * t * 128;
-        const int kx = xoff(t);
+        int kx;
+        if constexpr (KS == 1) kx = xoff(t);
+        else kx = kh ? xoff(KS * tt + 1) : xoff(KS * tt);
         const bf16x8_t a = frag2(tr16(sp + fa + ka), tr16(sp + fa + ka + 4 * 128));
         bf16x8_t b[3];
 #pragma unroll
@@ -215,17 +256,61 @@ __global__ __launch_bounds__(256) void conv_wgrad_rows(
         for (int s = 0; s < 3; ++s) acc[s] = mfma32(a, b[s], acc[s]);
       }
     }
+    if constexpr (KS == 2) {
+      // the two waves of a SIMD swap halves of their sums through the slot
+      // just consumed (free once every wave is past its last MFMAs; its
+      // refill is issued only after the next stage's barrier): wave kh keeps
+      // elements 8 kh .. 8 kh + 7 of each tap and adds the partner's.  The
+      // sum is the same from either side, so the order is fixed.  2 KiB per
+      // wave per tap, 16-byte chunk c of lane l at c * 64 + l.
+      f32x4_t* xo = (f32x4_t*)(smem + ((idx - 1) % NS) * SB) + wave * 128 + lane;
+      const f32x4_t* xi = (const f32x4_t*)(smem + ((idx - 1) % NS) * SB) + (wave ^ 4) * 128 + lane;
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        lds_handoff_barrier();
+        if (kh) {
+          xo[0] = f32x4_t{acc[s][0], acc[s][1], acc[s][2], acc[s][3]};
+          xo[64] = f32x4_t{acc[s][4], acc[s][5], acc[s][6], acc[s][7]};
+        } else {
+          xo[0] = f32x4_t{acc[s][8], acc[s][9], acc[s][10], acc[s][11]};
+          xo[64] = f32x4_t{acc[s][12], acc[s][13], acc[s][14], acc[s][15]};
+        }
+        lds_handoff_barrier();
+        const f32x4_t v0 = xi[0], v1 = xi[64];
+        if (kh) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[s][8 + e] += v0[e];
+            acc[s][12 + e] += v1[e];
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            acc[s][e] += v0[e];
+            acc[s][4 + e] += v1[e];
+          }
+        }
+      }
+      // the exchange reads are done before the slot's refill is issued
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
     // epilogue: element v of lane l is co 8 (v / 4) + 4 (l / 32) + v % 4, ci
-    // l % 32 of this wave's quarter
+    // l % 32 of this wave's quarter; with KS = 2 wave kh stores v = 8 kh ..
+    // 8 kh + 7
     float* o = out + (long)kr * E;
     const int ci = ci0 + nw * 32 + (lane & 31);
+    auto store = [&](int v0, int v1) __attribute__((always_inline)) {
 #pragma unroll
-    for (int s = 0; s < 3; ++s)
+      for (int s = 0; s < 3; ++s)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int co = co0 + cw * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        o[((long)co * 9 + 3 * r + s) * Cin + ci] = acc[s][v];
-      }
+        for (int v = v0; v < v1; ++v) {
+          const int co = co0 + cw * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+          o[((long)co * 9 + 3 * r + s) * Cin + ci] = acc[s][v];
+        }
+    };
+    if (KS == 1) store(0, 16);
+    else if (kh) store(8, 16);
+    else store(0, 8);
   }
 }
 
@@ -244,6 +329,9 @@ static WgPlan wgrad_rows_plan(const ConvShape& s) {
   return {R, s.nb * ((s.H + R - 1) / R)};
 }
 
+// waves per SIMD of the row-blocked weight gradient (0: chosen by width)
+int g_wgrad_ks = 0;
+
 bool wgrad_rows_ok(const ConvShape& s) {
   return s.taps == 9 && (s.W == 192 || s.W == 96 || s.W == 48 || s.W == 24) && s.cin % 64 == 0 &&
          s.cout % 64 == 0 && (double)s.pixels() * (s.cin > s.cout ? s.cin : s.cout) * 2 < 2147483648.0;
@@ -254,19 +342,32 @@ size_t wgrad_rows_partial_floats(const ConvShape& s) {
   return p.nK > 1 ? (size_t)p.nK * s.cout * 9 * s.cin : 0;
 }
 
-template <int W, int RPS, int NS>
+template <int W, int RPS, int NS, int KS>
 static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* DZ, float* out,
                                     const ConvShape& s, const WgPlan& p, hipStream_t st) {
   const long items = (long)p.nK * 3 * (s.cout / 64) * (s.cin / 64);
   const int G = (int)(items < 256 ? items : 256);
   const double flops = 2.0 * s.pixels() * s.cout * 9 * s.cin;
   const double bytes = 2.0 * s.pixels() * (s.cin + s.cout) + 4.0 * p.nK * s.cout * 9 * s.cin;
-  static const char* names[] = {"conv_wgrad_rows<192,1,3>", "conv_wgrad_rows<96,2,3>",
-                                "conv_wgrad_rows<48,4,3>", "conv_wgrad_rows<24,4,5>"};
-  ProfScope ps(names[W == 192 ? 0 : (W == 96 ? 1 : (W == 48 ? 2 : 3))], flops, bytes, st);
-  TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, NS>), dim3(G), dim3(256), 0, st, X, DZ, out, s.nb,
-             s.H, s.cin, s.cout, p.R);
+  static const char* names[2][4] = {
+      {"conv_wgrad_rows<192,1,3>", "conv_wgrad_rows<96,2,3>", "conv_wgrad_rows<48,4,3>",
+       "conv_wgrad_rows<24,4,5>"},
+      {"conv_wgrad_rows<192,1,3,8w>", "conv_wgrad_rows<96,2,3,8w>", "conv_wgrad_rows<48,4,3,8w>",
+       "conv_wgrad_rows<24,4,5,8w>"}};
+  ProfScope ps(names[KS - 1][W == 192 ? 0 : (W == 96 ? 1 : (W == 48 ? 2 : 3))], flops, bytes, st);
+  TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, NS, KS>), dim3(G), dim3(256 * KS), 0, st, X, DZ, out,
+             s.nb, s.H, s.cin, s.cout, p.R);
   return hipGetLastError();
+}
+
+template <int W, int RPS, int NS>
+static hipError_t launch_wgrad_rows_ks(const bf16_t* X, const bf16_t* DZ, float* out,
+                                       const ConvShape& s, const WgPlan& p, hipStream_t st) {
+  // two waves per SIMD pay off where a stage has many k steps (widths 192
+  // and 48 measured 1-3 % faster; 96 about even, 24 slower)
+  const int ks = g_wgrad_ks ? g_wgrad_ks : ((W == 192 || W == 48) ? 2 : 1);
+  return ks == 2 ? launch_wgrad_rows<W, RPS, NS, 2>(X, DZ, out, s, p, st)
+                 : launch_wgrad_rows<W, RPS, NS, 1>(X, DZ, out, s, p, st);
 }
 
 hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
@@ -277,10 +378,10 @@ hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, floa
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* DZ = (const bf16_t*)dz;
   hipError_t e;
-  if (s.W == 192) e = launch_wgrad_rows<192, 1, 3>(X, DZ, out, s, p, st);
-  else if (s.W == 96) e = launch_wgrad_rows<96, 2, 3>(X, DZ, out, s, p, st);
-  else if (s.W == 48) e = launch_wgrad_rows<48, 4, 3>(X, DZ, out, s, p, st);
-  else e = launch_wgrad_rows<24, 4, 5>(X, DZ, out, s, p, st);
+  if (s.W == 192) e = launch_wgrad_rows_ks<192, 1, 3>(X, DZ, out, s, p, st);
+  else if (s.W == 96) e = launch_wgrad_rows_ks<96, 2, 3>(X, DZ, out, s, p, st);
+  else if (s.W == 48) e = launch_wgrad_rows_ks<48, 4, 3>(X, DZ, out, s, p, st);
+  else e = launch_wgrad_rows_ks<24, 4, 5>(X, DZ, out, s, p, st);
   if (e != hipSuccess) return e;
   if (p.nK == 1)
     return extra ? splitk_reduce_launch(extra->part, extra->out, extra->E, extra->S, st) : e;

@@ -78,6 +78,21 @@ def test_rows32_configurations(cfg, w, r):
         tgp.debug_set_fwd_variant(old)
 
 
+@pytest.mark.parametrize("cin,cout,h,w", [(64, 128, 7, 48), (128, 64, 5, 96), (64, 64, 3, 192),
+                                          (128, 128, 5, 24)])
+def test_wgrad_rows_four_wave_layout(cin, cout, h, w):
+    """The row-blocked weight gradient's four-wave layout forced at every
+    width (the automatic choice takes the eight-wave one at widths 192 and
+    48), on the same shapes as the conv3x3 cases above."""
+    import paper_2004_09910_amd as tgp
+    old = tgp.debug_set_rowtile_mask(15 | 32)
+    try:
+        net = one_layer(Layer(CONV3X3, cin, cout), h, w)
+        run_and_check(net, (1,), 1, BF16, 2, 1, f"wgrad four-wave {cin}->{cout} @{h}x{w}")
+    finally:
+        tgp.debug_set_rowtile_mask(old)
+
+
 def test_conv1x1_and_depthwise():
     net = one_layer(Layer(CONV1X1, 256, 256), 14, 14)
     run_and_check(net, (1,), 1, BF16, 4, 2, "conv1x1 256->256 @14x14")
