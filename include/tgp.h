@@ -176,13 +176,14 @@ tgp_status tgp_stage_forward(tgp_net* net, int j, int i, int checkpoint, const v
  * (then the first layer's data gradient is skipped).  Gradients of skips
  * popped here go to their gradient slots; skips stashed here add the
  * gradient found in theirs.  The weight gradient g_i^j is left for
- * tgp_grad_accumulate.  Order (Sec. 2.1): for a given j, i = m, m-1, .., 1,
+ * tgp_grad_accumulate, as partial sums over pixel ranges in the workspace.  Order (Sec. 2.1): for a given j, i = m, m-1, .., 1,
  * each after F_{i,j} and after tgp_grad_accumulate(j, i+1); ESTATE otherwise. */
 tgp_status tgp_stage_backward_recompute(tgp_net* net, int j, int i, const void* dy_out,
                                         void* dx_in, void* stream);
 
 /* g^j (+)= g_i^j into the bound float32 accumulators of partition j's layers
- * (Sec. 2: the gradient is the sum of g_i^j over i).  overwrite must be 1
+ * (Sec. 2: the gradient is the sum of g_i^j over i); the partial sums B_{i,j}
+ * left are added up here, in an order fixed by the shapes.  overwrite must be 1
  * exactly for i = m (the first backward of a step), else 0.  Requires
  * B_{i,j}; ESTATE otherwise. */
 tgp_status tgp_grad_accumulate(tgp_net* net, int j, int i, int overwrite, void* stream);

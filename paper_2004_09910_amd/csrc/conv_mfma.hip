@@ -1376,8 +1376,9 @@ size_t wgrad_mfma_partial_floats(const ConvShape& s) {
 }
 
 hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
-                           const ConvShape& s, hipStream_t st, const ReduceJob* extra) {
-  if (use_wgrad_rows(s)) return conv_wgrad_rows_launch(x, dz, dw, partial, s, st, extra);
+                           const ConvShape& s, hipStream_t st, const ReduceJob* extra,
+                           ReduceJob* defer) {
+  if (use_wgrad_rows(s)) return conv_wgrad_rows_launch(x, dz, dw, partial, s, st, extra, defer);
   long P = s.pixels();
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* DZ = (const bf16_t*)dz;
@@ -1412,6 +1413,10 @@ hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* part
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (defer) {
+    *defer = ReduceJob{partial, dw, E, pl.S};   // partial == dw when S == 1
+    return extra ? hipErrorInvalidValue : hipSuccess;
+  }
   if (pl.S == 1)
     return extra ? splitk_reduce_launch(extra->part, extra->out, extra->E, extra->S, st) : hipSuccess;
   return splitk_reduce_launch(partial, dw, E, pl.S, st, extra);

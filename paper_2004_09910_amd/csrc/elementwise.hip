@@ -15,7 +15,8 @@ hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void*
                              hipStream_t st);
 size_t wgrad_mfma_partial_floats(const ConvShape& s);
 hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
-                           const ConvShape& s, hipStream_t st, const ReduceJob* extra);
+                           const ConvShape& s, hipStream_t st, const ReduceJob* extra,
+                           ReduceJob* defer);
 
 namespace {
 
@@ -478,25 +479,80 @@ __global__ __launch_bounds__(256) void accumulate_k(float* __restrict__ acc, con
   }
 }
 
-// acc_k (+)= g_k for up to kMaxAcc (acc, g, n) entries in one launch; block
-// b covers float4 column range [b*1024, (b+1)*1024) of every entry.
-__global__ __launch_bounds__(256) void accumulate_multi_k(AccBatch batch, int overwrite) {
-  for (int k = 0; k < batch.count; ++k) {
-    const long n = batch.n[k];
-    const long e0 = ((long)blockIdx.x * 256 + threadIdx.x) * 4;
-    if (e0 >= n) continue;
-    float* acc = batch.acc[k];
-    const float* g = batch.g[k];
-    if (e0 + 4 <= n) {
-      float4 v = *(const float4*)(g + e0);
-      if (!overwrite) {
-        float4 a = *(const float4*)(acc + e0);
-        v.x = a.x + v.x; v.y = a.y + v.y; v.z = a.z + v.z; v.w = a.w + v.w;
-      }
-      *(float4*)(acc + e0) = v;
-    } else {
-      for (long e = e0; e < n; ++e) acc[e] = overwrite ? g[e] : acc[e] + g[e];
+// acc_k = r_k or acc_k + r_k with r_k = sum_{s < S_k} g_k[s n_k + e], every
+// entry in one launch.  Blocks blk0[k] .. blk0[k + 1] - 1 serve entry k.  A
+// block of 1024 threads covers C4 float4 columns with LANES = 1024 / C4
+// split lanes; lane l sums s = l, l + LANES, .. in ascending order, then the
+// lanes are added in order 0 .. LANES - 1, with (C4, LANES) a function of S
+// only (the layout splitk_reduce uses for the same S, plus a single lane
+// when S = 1), so the sum is fixed by the shape.  An entry with n not a
+// multiple of 4 takes one element per thread, s ascending.
+__device__ __forceinline__ int acc_c4(int S) {
+  return S >= 64 ? 16 : (S >= 16 ? 64 : (S >= 2 ? 256 : 1024));
+}
+
+__global__ __launch_bounds__(1024) void reduce_accumulate_k(AccBatch b, int overwrite) {
+  __shared__ float4 red[1024];
+  int k = 0;   // entry of this block (block-uniform)
+  while (k + 1 < b.count && (int)blockIdx.x >= b.blk0[k + 1]) ++k;
+  const long bx = (long)blockIdx.x - b.blk0[k];
+  const long E = b.n[k];
+  const int S = b.S[k];
+  const float* __restrict__ part = b.g[k];
+  float* __restrict__ acc = b.acc[k];
+  if (E % 4) {
+    const long e = bx * 1024 + threadIdx.x;
+    if (e < E) {
+      float r = 0.f;
+      for (int s = 0; s < S; ++s) r += part[(long)s * E + e];
+      acc[e] = overwrite ? r : acc[e] + r;
     }
+    return;
+  }
+  const int C4 = acc_c4(S), LANES = 1024 / C4;
+  const int col = threadIdx.x % C4, lane = threadIdx.x / C4;
+  const long e4 = (bx * C4 + col) * 4;
+  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (e4 < E) {
+    int s = lane;
+    // eight independent loads in flight per step
+    for (; s + 7 * LANES < S; s += 8 * LANES) {
+      float4 t[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t[u] = *(const float4*)(part + (long)(s + u * LANES) * E + e4);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        a.x += t[u].x; a.y += t[u].y; a.z += t[u].z; a.w += t[u].w;
+      }
+    }
+    for (; s < S; s += LANES) {
+      const float4 t = *(const float4*)(part + (long)s * E + e4);
+      a.x += t.x; a.y += t.y; a.z += t.z; a.w += t.w;
+    }
+  }
+  if (LANES == 1) {   // block-uniform
+    if (e4 < E) {
+      if (!overwrite) {
+        const float4 o = *(const float4*)(acc + e4);
+        a.x = o.x + a.x; a.y = o.y + a.y; a.z = o.z + a.z; a.w = o.w + a.w;
+      }
+      *(float4*)(acc + e4) = a;
+    }
+    return;
+  }
+  red[lane * C4 + col] = a;
+  __syncthreads();
+  if (lane == 0 && e4 < E) {
+    float4 r = red[col];
+    for (int l = 1; l < LANES; ++l) {
+      const float4 t = red[l * C4 + col];
+      r.x += t.x; r.y += t.y; r.z += t.z; r.w += t.w;
+    }
+    if (!overwrite) {
+      const float4 o = *(const float4*)(acc + e4);
+      r.x = o.x + r.x; r.y = o.y + r.y; r.z = o.z + r.z; r.w = o.w + r.w;
+    }
+    *(float4*)(acc + e4) = r;
   }
 }
 
@@ -556,8 +612,11 @@ size_t conv_wgrad_partial_floats(int dt, const ConvShape& s) {
 }
 
 hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial,
-                      const ConvShape& s, hipStream_t st, const ReduceJob* extra) {
-  if (mfma_conv_ok(dt, s.cin, s.cout)) return conv_wgrad_mfma(x, dz, dw, partial, s, st, extra);
+                      const ConvShape& s, hipStream_t st, const ReduceJob* extra,
+                      ReduceJob* defer) {
+  if (defer && extra) return hipErrorInvalidValue;
+  if (mfma_conv_ok(dt, s.cin, s.cout))
+    return conv_wgrad_mfma(x, dz, dw, partial, s, st, extra, defer);
   long P = s.pixels();
   long E = (long)s.cout * s.taps * s.cin;
   long pps = direct_wgrad_pps(P);
@@ -575,6 +634,10 @@ hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* p
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  if (defer) {
+    *defer = ReduceJob{partial, dw, E, S};
+    return hipSuccess;
+  }
   return splitk_reduce_launch(partial, dw, E, S, st, extra);
 }
 
@@ -811,16 +874,25 @@ hipError_t loss_finalize(const float* parts, int m, float inv_numel, float* loss
   return hipGetLastError();
 }
 
-hipError_t grad_accumulate_batch(const AccBatch& b, int overwrite, hipStream_t st) {
-  long maxn = 0;
+hipError_t grad_accumulate_batch(AccBatch b, int overwrite, hipStream_t st) {
+  if (b.count < 0 || b.count > kMaxAcc) return hipErrorInvalidValue;
+  long blocks = 0;
   double bytes = 0;
+  int used = 0;
   for (int k = 0; k < b.count; ++k) {
-    maxn = b.n[k] > maxn ? b.n[k] : maxn;
-    bytes += (overwrite ? 8.0 : 12.0) * b.n[k];
+    if (b.n[k] <= 0 || b.S[k] < 1) continue;
+    b.acc[used] = b.acc[k]; b.g[used] = b.g[k]; b.n[used] = b.n[k]; b.S[used] = b.S[k];
+    b.blk0[used] = (int)blocks;
+    const int C4 = b.S[k] >= 64 ? 16 : (b.S[k] >= 16 ? 64 : (b.S[k] >= 2 ? 256 : 1024));
+    blocks += b.n[k] % 4 ? cdiv(b.n[k], 1024L) : cdiv(b.n[k], 4L * C4);
+    bytes += 4.0 * b.n[k] * (b.S[k] + (overwrite ? 1 : 2));
+    ++used;
   }
-  if (maxn == 0) return hipSuccess;
-  ProfScope ps("grad_accumulate", 0.0, bytes, st);
-  TGP_LAUNCH(ps, accumulate_multi_k, dim3(cdiv(maxn, 1024)), dim3(256), 0, st, b, overwrite);
+  b.count = used;
+  if (used == 0) return hipSuccess;
+  if (blocks >= (1L << 31)) return hipErrorInvalidValue;
+  ProfScope ps("reduce_accumulate", 0.0, bytes, st);
+  TGP_LAUNCH(ps, reduce_accumulate_k, dim3((unsigned)blocks), dim3(1024), 0, st, b, overwrite);
   return hipGetLastError();
 }
 

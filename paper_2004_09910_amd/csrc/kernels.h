@@ -60,7 +60,7 @@ bool wgrad_rows_ok(const ConvShape& s);
 size_t wgrad_rows_partial_floats(const ConvShape& s);
 hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
                                   const ConvShape& s, hipStream_t st,
-                                  const ReduceJob* extra = nullptr);
+                                  const ReduceJob* extra = nullptr, ReduceJob* defer = nullptr);
 
 // Whether the data-gradient kernel for this shape reads the transformed
 // weight wt = [cin][taps][cout] (taps rotated by 180 degrees).
@@ -73,10 +73,13 @@ hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, voi
 // Weight gradient of one micro-batch into dw (float32, KRSC), via split-K
 // partials in `partial` (conv_wgrad_partial_floats floats) reduced in fixed
 // split order.  `extra`, if given, is a pending sum (the bias gradient's)
-// that runs in the same reduction launch.
+// that runs in the same reduction launch.  With `defer` (and no `extra`)
+// only the partials are written and *defer describes the sum still to run
+// (S = 1 with part = dw when the kernel wrote the gradient itself).
 size_t conv_wgrad_partial_floats(int dt, const ConvShape& s);
 hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial,
-                      const ConvShape& s, hipStream_t st, const ReduceJob* extra = nullptr);
+                      const ConvShape& s, hipStream_t st, const ReduceJob* extra = nullptr,
+                      ReduceJob* defer = nullptr);
 
 // Depthwise 3x3 (pad 1), w = [c][9].
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
@@ -122,15 +125,20 @@ hipError_t loss_finalize(const float* parts, int m, float inv_numel, float* loss
 // acc = g (overwrite) or acc + g, float32.
 hipError_t grad_accumulate(float* acc, const float* g, long n, int overwrite, hipStream_t st);
 
-// The same for up to kMaxAcc tensors in one launch (passed by value).
-constexpr int kMaxAcc = 64;
+// acc_k = r_k (overwrite) or acc_k + r_k, r_k = sum_{s < S_k} g_k[s n_k ..]
+// (the pending split-K sums of one micro-batch's gradients), for up to
+// kMaxAcc tensors in one launch (passed by value).  Each r_k is summed in
+// the order splitk_reduce_launch uses for (n_k, S_k).
+constexpr int kMaxAcc = 48;
 struct AccBatch {
   int count;
   float* acc[kMaxAcc];
   const float* g[kMaxAcc];
   long n[kMaxAcc];
+  int S[kMaxAcc];
+  int blk0[kMaxAcc];   // first block of each entry (filled by the launcher)
 };
-hipError_t grad_accumulate_batch(const AccBatch& b, int overwrite, hipStream_t st);
+hipError_t grad_accumulate_batch(AccBatch b, int overwrite, hipStream_t st);
 
 // relu_backward fused with the bias gradient's column sums (fixed-order
 // two-stage reduction), for layers where relu_bias_fusable() holds.

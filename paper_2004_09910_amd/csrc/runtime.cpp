@@ -6,6 +6,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <array>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -50,6 +51,9 @@ struct LayerRt {
   size_t out_bytes = 0, pro_bytes = 0;
   // workspace offsets
   size_t o_scr_out = 0, o_scr_pro = 0, o_gw = 0, o_gb = 0, o_wt = 0;
+  // gradient-slot offsets of the weight gradient's split-K partial slices
+  // and the bias gradient's column-sum partials (0 bytes when unused)
+  size_t o_gpart = 0, o_gcol = 0, o_gcol_floats = 0;
   std::vector<size_t> o_sto_out, o_sto_pro;  // per stored set
   bool has_wt = false;
 };
@@ -81,11 +85,15 @@ struct tgp_net {
   // relative to the lane's base o_lane + lane * lane_stride.
   int lanes = 1;
   size_t o_lane = 0, lane_stride = 0;
-  // Per-micro-batch gradients g_i^j (o_gw / o_gb of each layer, relative to
-  // a slot): one slot with one lane, one per micro-batch with several, so
-  // that no lane waits for the accumulation of its previous micro-batch.
+  // Per-micro-batch gradients g_i^j (o_gw / o_gb / o_gpart / o_gcol of each
+  // layer, relative to a slot): one slot with one lane, one per micro-batch
+  // with several, so that no lane waits for the accumulation of its previous
+  // micro-batch.  B_{i,j} leaves each gradient as partial sums in the slot
+  // (pend[(i-1) L + l][0 weight, 1 bias] describes them) and
+  // tgp_grad_accumulate reduces them straight into the accumulators.
   int gslots = 1;
   size_t o_gslot = 0, gslot_stride = 0;
+  std::vector<std::array<tgpk::ReduceJob, 2>> pend;
   // state per (i, j): index (i-1)*n + (j-1)
   std::vector<uint8_t> st;
   std::vector<const void*> saved_x;
@@ -285,8 +293,8 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
   void* gnext = T_(N, i, N->o_g1);
   void* dz = T_(N, i, N->o_dz);
   void* dinp = T_(N, i, N->o_dinp);
-  float* part = (float*)T_(N, i, N->o_part);
-  float* colpart = (float*)T_(N, i, N->o_colpart);
+  float* part = (float*)T_(N, i, N->o_part);          // depthwise weight gradient
+  float* colpart = (float*)T_(N, i, N->o_colpart);    // bias_grad
   const void* dy = dy_out;
   for (int l = hi - 1; l >= lo; --l) {
     LayerRt& Lr = N->L[l];
@@ -297,29 +305,31 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
     const void* dskip = d.stash_id >= 0 ? W_(N, stash_off(N, i, d.stash_id, true)) : nullptr;
     long nout = out_elems_mb(N, Lr);
     long P = (long)N->b * Lr.H * Lr.W;
-    // the bias gradient's column sums are reduced in the weight gradient's
-    // reduction launch (conv layers; a depthwise layer reduces them here)
-    tgpk::ReduceJob bias_sum{};
-    bool bias_pending = false;
-    if (d.bias && tgpk::relu_bias_fusable(N->dt, d.cout, dy, dskip, y, dz)) {
-      bias_pending = d.kind != TGP_DWCONV3X3;
-      HIPCHK(tgpk::relu_backward_bias(N->dt, dy, dskip, y, dz, d.relu, (float*)G_(N, i, Lr.o_gb),
-                                      colpart, P, d.cout, st, bias_pending ? &bias_sum : nullptr),
+    // both gradients stay partial sums in the slot, reduced by the
+    // accumulation (the bias's column sums only where relu_backward_bias
+    // computes them; bias_grad reduces its own)
+    std::array<tgpk::ReduceJob, 2>& pj = N->pend[(size_t)(i - 1) * N->L.size() + l];
+    float* gb = d.bias ? (float*)G_(N, i, Lr.o_gb) : nullptr;
+    pj[1] = tgpk::ReduceJob{gb, gb, d.bias ? (long)d.cout : 0, 1};
+    if (d.bias && Lr.o_gcol_floats &&
+        tgpk::relu_bias_fusable(N->dt, d.cout, dy, dskip, y, dz)) {
+      HIPCHK(tgpk::relu_backward_bias(N->dt, dy, dskip, y, dz, d.relu, gb,
+                                      (float*)G_(N, i, Lr.o_gcol), P, d.cout, st, &pj[1]),
              "relu_backward_bias");
     } else {
       HIPCHK(tgpk::relu_backward(N->dt, dy, dskip, y, dz, d.relu, nout, st), "relu_backward");
       if (d.bias)
-        HIPCHK(tgpk::bias_grad(N->dt, dz, (float*)G_(N, i, Lr.o_gb), colpart, P, d.cout, st),
-               "bias_grad");
+        HIPCHK(tgpk::bias_grad(N->dt, dz, gb, colpart, P, d.cout, st), "bias_grad");
     }
     float* gw = (float*)G_(N, i, Lr.o_gw);
+    pj[0] = tgpk::ReduceJob{gw, gw, Lr.w_elems, 1};
     if (d.kind == TGP_DWCONV3X3) {
       HIPCHK(tgpk::dw_wgrad(N->dt, cin_ptr, dz, gw, part, N->b, Lr.H, Lr.W, d.cout, st),
              "dw_wgrad");
     } else {
       tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
-      HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr, dz, gw, part, s, st,
-                              bias_pending ? &bias_sum : nullptr),
+      HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr, dz, gw, (float*)G_(N, i, Lr.o_gpart), s, st,
+                              nullptr, &pj[0]),
              "conv_wgrad");
     }
     if (l == lo && dx_in == nullptr) break;
@@ -360,21 +370,23 @@ tgp_status run_accumulate(tgp_net* N, int j, int i, int overwrite, hipStream_t s
     batch.count = 0;
     return TGP_OK;
   };
-  auto add = [&](float* acc, const float* g, long n) -> tgp_status {
+  auto add = [&](float* acc, const tgpk::ReduceJob& job) -> tgp_status {
     if (batch.count == tgpk::kMaxAcc) {
       tgp_status r = flush();
       if (r != TGP_OK) return r;
     }
     batch.acc[batch.count] = acc;
-    batch.g[batch.count] = g;
-    batch.n[batch.count] = n;
+    batch.g[batch.count] = job.part;
+    batch.n[batch.count] = job.E;
+    batch.S[batch.count] = job.S;
     ++batch.count;
     return TGP_OK;
   };
   for (int l = N->lo[j - 1]; l < N->hi[j - 1]; ++l) {
     LayerRt& Lr = N->L[l];
-    tgp_status r = add(Lr.dw_acc, (const float*)G_(N, i, Lr.o_gw), Lr.w_elems);
-    if (r == TGP_OK && Lr.d.bias) r = add(Lr.db_acc, (const float*)G_(N, i, Lr.o_gb), Lr.d.cout);
+    const std::array<tgpk::ReduceJob, 2>& pj = N->pend[(size_t)(i - 1) * N->L.size() + l];
+    tgp_status r = add(Lr.dw_acc, pj[0]);
+    if (r == TGP_OK && Lr.d.bias) r = add(Lr.db_acc, pj[1]);
     if (r != TGP_OK) return r;
   }
   return flush();
@@ -734,17 +746,23 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
     tgpk::ConvShape s{N->b, Lr.H, Lr.W, Lr.d.cin, Lr.d.cout, Lr.taps};
     Lr.has_wt = Lr.d.kind != TGP_DWCONV3X3 && tgpk::conv_dgrad_uses_wt(N->dt, s);
     Lr.o_wt = Lr.has_wt ? takeL(Lr.w_elems * N->esz) : 0;
-    size_t pf = Lr.d.kind == TGP_DWCONV3X3 ? tgpk::dw_wgrad_partial_floats(N->b, Lr.H, Lr.W, Lr.d.cout)
-                                           : tgpk::conv_wgrad_partial_floats(N->dt, s);
-    max_part = std::max(max_part, pf);
-    max_col = std::max({max_col, tgpk::colsum_partial_floats((long)N->b * Lr.H * Lr.W, Lr.d.cout),
-                        tgpk::relu_bias_partial_floats(N->dt, (long)N->b * Lr.H * Lr.W, Lr.d.cout)});
+    const long P = (long)N->b * Lr.H * Lr.W;
+    if (Lr.d.kind == TGP_DWCONV3X3) {
+      max_part = std::max(max_part, tgpk::dw_wgrad_partial_floats(N->b, Lr.H, Lr.W, Lr.d.cout));
+      Lr.o_gpart = 0;
+    } else {
+      const size_t pf = tgpk::conv_wgrad_partial_floats(N->dt, s);
+      Lr.o_gpart = takeG(std::max<size_t>(pf, 1) * 4);
+    }
+    Lr.o_gcol_floats = Lr.d.bias ? tgpk::relu_bias_partial_floats(N->dt, P, Lr.d.cout) : 0;
+    Lr.o_gcol = Lr.o_gcol_floats ? takeG(Lr.o_gcol_floats * 4) : 0;
+    max_col = std::max(max_col, tgpk::colsum_partial_floats(P, Lr.d.cout));
   }
   N->o_g0 = takeL(max_act);
   N->o_g1 = takeL(max_act);
   N->o_dz = takeL(max_act);
   N->o_dinp = takeL(std::max<size_t>(max_pro, 16));
-  N->o_part = takeL(max_part * 4);
+  N->o_part = takeL(std::max<size_t>(max_part, 1) * 4);
   size_t max_fpart = 0;   // split-K partials of forward / data-gradient convolutions
   for (auto& Lr : N->L) {
     if (Lr.d.kind == TGP_DWCONV3X3) continue;
@@ -784,6 +802,7 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
   N->saved_x.assign((size_t)m * n, nullptr);
   N->saved_y.assign((size_t)m * n, nullptr);
   N->saved_ckpt.assign((size_t)m * n, 0);
+  N->pend.assign((size_t)m * N->L.size(), std::array<tgpk::ReduceJob, 2>{});
   *bytes = off;
   return TGP_OK;
 }

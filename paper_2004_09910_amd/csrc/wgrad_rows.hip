@@ -371,7 +371,8 @@ static hipError_t launch_wgrad_rows_ks(const bf16_t* X, const bf16_t* DZ, float*
 }
 
 hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
-                                  const ConvShape& s, hipStream_t st, const ReduceJob* extra) {
+                                  const ConvShape& s, hipStream_t st, const ReduceJob* extra,
+                                  ReduceJob* defer) {
   if (!wgrad_rows_ok(s)) return hipErrorInvalidValue;
   const WgPlan p = wgrad_rows_plan(s);
   float* out = p.nK > 1 ? partial : dw;
@@ -383,6 +384,10 @@ hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, floa
   else if (s.W == 48) e = launch_wgrad_rows_ks<48, 4, 3>(X, DZ, out, s, p, st);
   else e = launch_wgrad_rows_ks<24, 4, 5>(X, DZ, out, s, p, st);
   if (e != hipSuccess) return e;
+  if (defer) {
+    *defer = ReduceJob{out, dw, (long)s.cout * 9 * s.cin, p.nK};
+    return extra ? hipErrorInvalidValue : hipSuccess;
+  }
   if (p.nK == 1)
     return extra ? splitk_reduce_launch(extra->part, extra->out, extra->E, extra->S, st) : e;
   return splitk_reduce_launch(partial, dw, (long)s.cout * 9 * s.cin, p.nK, st, extra);
