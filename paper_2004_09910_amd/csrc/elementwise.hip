@@ -261,6 +261,84 @@ __global__ __launch_bounds__(256) void relu_bwd_bias_k(const T* __restrict__ dy,
   }
 }
 
+// relu_bwd_bias_k for a layer whose output feeds a 2x2/2 max pool: dy is
+// the pool gradient dp routed to the first maximal element of each window
+// of y.  Block b covers pooled pixels [b*rows, (b+1)*rows); thread t handles
+// channel pack t % CP of windows t / CP, t / CP + 256 / CP, ... (the four
+// pixels of a window in row-major order), then row lanes are added in order
+// in LDS and part[b][c] is written.
+template <typename T>
+__global__ __launch_bounds__(256) void pool_relu_bwd_bias_k(const T* __restrict__ dp,
+                                                            const T* __restrict__ ds,
+                                                            const T* __restrict__ y,
+                                                            T* __restrict__ dz,
+                                                            float* __restrict__ part, int relu,
+                                                            int nb, int H, int W, int C,
+                                                            long rows) {
+  constexpr int N = Pk<T>::N;
+  __shared__ float red[256 * N];
+  const int CP = C / N;
+  const int cp = threadIdx.x % CP, rl = threadIdx.x / CP, nl = 256 / CP;
+  const int H2 = H / 2, W2 = W / 2;
+  const long P2 = (long)nb * H2 * W2;
+  const long q0 = (long)blockIdx.x * rows, q1 = q0 + rows < P2 ? q0 + rows : P2;
+  float sum[N];
+#pragma unroll
+  for (int i = 0; i < N; ++i) sum[i] = 0.f;
+  for (long q = q0 + rl; q < q1; q += nl) {
+    const int w2 = q % W2;
+    const long r = q / W2;
+    const int h2 = r % H2, n = r / H2;
+    const long o = (((long)n * H + 2 * h2) * W + 2 * w2) * C + cp * N;
+    const long off[4] = {0, C, (long)W * C, (long)W * C + C};
+    float v[4][N], g[N], a[4][N];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) Pk<T>::un(ld16(y + o + off[k]), v[k]);
+    Pk<T>::un(ld16(dp + q * C + cp * N), g);
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+      int arg = 0;
+      float best = v[0][i];
+#pragma unroll
+      for (int k = 1; k < 4; ++k)
+        if (v[k][i] > best) { best = v[k][i]; arg = k; }
+#pragma unroll
+      for (int k = 0; k < 4; ++k) a[k][i] = k == arg ? g[i] : 0.f;
+    }
+    if (ds) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        float s2[N];
+        Pk<T>::un(ld16(ds + o + off[k]), s2);
+#pragma unroll
+        for (int i = 0; i < N; ++i) a[k][i] += s2[i];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (relu) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) a[k][i] = v[k][i] > 0.f ? a[k][i] : 0.f;
+      }
+      const uint4 o16 = Pk<T>::pk(a[k]);
+      st16(dz + o + off[k], o16);
+      Pk<T>::un(o16, a[k]);   // the bias gradient sums the stored (rounded) dz
+#pragma unroll
+      for (int i = 0; i < N; ++i) sum[i] += a[k][i];
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < N; ++i) red[threadIdx.x * N + i] = sum[i];
+  __syncthreads();
+  if (rl == 0) {
+    for (int l = 1; l < nl; ++l)
+#pragma unroll
+      for (int i = 0; i < N; ++i) sum[i] += red[(l * CP + cp) * N + i];
+#pragma unroll
+    for (int i = 0; i < N; ++i) part[(long)blockIdx.x * C + cp * N + i] = sum[i];
+  }
+}
+
 // Column sums of a P x C matrix: block (cg, pb) sums rows [pb*rows, ...) for
 // channels cg*64 .. +63; 4 row lanes, combined in fixed order.
 template <typename T>
@@ -735,7 +813,14 @@ bool relu_bias_fusable(int dt, int C, const void* dy, const void* dskip, const v
 size_t relu_bias_partial_floats(int dt, long P, int C) {
   const int N = dt == 0 ? 8 : 4;
   if (C % N || C / N > 256 || 256 % (C / N)) return 0;   // not fusable
-  return (size_t)cdiv(P, relu_bias_rows(P, C, N)) * C;
+  // blocks over P pixels, or over the P / 4 windows of the pooled variant
+  const long b1 = cdiv(P, relu_bias_rows(P, C, N));
+  const long b2 = cdiv(P / 4, relu_bias_rows(P / 4, C, N));
+  return (size_t)(b1 > b2 ? b1 : b2) * C;
+}
+bool pool_relu_bias_fusable(int dt, int C, int H, int W, const void* dp, const void* dskip,
+                            const void* y, const void* dz) {
+  return H % 2 == 0 && W % 2 == 0 && H >= 2 && W >= 2 && relu_bias_fusable(dt, C, dp, dskip, y, dz);
 }
 
 hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
@@ -762,6 +847,35 @@ hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const v
     return hipSuccess;
   }
   return splitk_reduce_launch(partial, db, C, nb, st);
+}
+
+hipError_t pool_relu_backward_bias(int dt, const void* dp, const void* dskip, const void* y,
+                                   void* dz, int relu, float* db, float* partial, int nb, int H,
+                                   int W, int C, hipStream_t st, ReduceJob* defer) {
+  if (!pool_relu_bias_fusable(dt, C, H, W, dp, dskip, y, dz)) return hipErrorInvalidValue;
+  const long P2 = (long)nb * (H / 2) * (W / 2);
+  const long rows = relu_bias_rows(P2, C, dt == 0 ? 8 : 4);
+  const int nbk = cdiv(P2, rows);
+  {
+    const double esz = dt == 0 ? 2.0 : 4.0;
+    ProfScope ps("pool_relu_backward_bias", 0.0,
+                 esz * 4.0 * P2 * C * (2 + (dskip ? 1 : 0)) + esz * P2 * C + 4.0 * nbk * C, st);
+    if (dt == 0)
+      TGP_LAUNCH(ps, pool_relu_bwd_bias_k<bf16_t>, dim3(nbk), dim3(256), 0, st,
+                 (const bf16_t*)dp, (const bf16_t*)dskip, (const bf16_t*)y, (bf16_t*)dz, partial,
+                 relu, nb, H, W, C, rows);
+    else
+      TGP_LAUNCH(ps, pool_relu_bwd_bias_k<float>, dim3(nbk), dim3(256), 0, st,
+                 (const float*)dp, (const float*)dskip, (const float*)y, (float*)dz, partial,
+                 relu, nb, H, W, C, rows);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (defer) {
+    *defer = ReduceJob{partial, db, (long)C, nbk};
+    return hipSuccess;
+  }
+  return splitk_reduce_launch(partial, db, C, nbk, st);
 }
 
 hipError_t bias_grad(int dt, const void* dz, float* db, float* partial, long P, int C,

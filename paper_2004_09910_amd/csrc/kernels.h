@@ -150,5 +150,15 @@ size_t relu_bias_partial_floats(int dt, long P, int C);
 hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
                               int relu, float* db, float* partial, long P, int C,
                               hipStream_t st, ReduceJob* defer = nullptr);
+// The same for a layer whose output y (nb x H x W x C, H and W even) feeds a
+// 2x2/2 max pool, taking the pool's gradient dp (nb x H/2 x W/2 x C): dy is
+// dp routed to the first maximal element of each window of y (the pool's
+// backward, maxpool_backward), formed on the fly.  Same dz and partial-sum
+// contract (its partials fit relu_bias_partial_floats(dt, nb H W, C)).
+bool pool_relu_bias_fusable(int dt, int C, int H, int W, const void* dp, const void* dskip,
+                            const void* y, const void* dz);
+hipError_t pool_relu_backward_bias(int dt, const void* dp, const void* dskip, const void* y,
+                                   void* dz, int relu, float* db, float* partial, int nb, int H,
+                                   int W, int C, hipStream_t st, ReduceJob* defer = nullptr);
 
 }  // namespace tgpk

@@ -296,6 +296,10 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
   float* part = (float*)T_(N, i, N->o_part);          // depthwise weight gradient
   float* colpart = (float*)T_(N, i, N->o_colpart);    // bias_grad
   const void* dy = dy_out;
+  // the pool gradient of layer l + 1's max-pool prologue, when its backward
+  // is left to layer l's ReLU backward (dy then names the buffer it would
+  // have filled)
+  const void* dy_pool = nullptr;
   for (int l = hi - 1; l >= lo; --l) {
     LayerRt& Lr = N->L[l];
     const tgp_layer& d = Lr.d;
@@ -310,16 +314,29 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
     // computes them; bias_grad reduces its own)
     std::array<tgpk::ReduceJob, 2>& pj = N->pend[(size_t)(i - 1) * N->L.size() + l];
     float* gb = d.bias ? (float*)G_(N, i, Lr.o_gb) : nullptr;
-    pj[1] = tgpk::ReduceJob{gb, gb, d.bias ? (long)d.cout : 0, 1};
-    if (d.bias && Lr.o_gcol_floats &&
+    pj[1] = tgpk::ReduceJob{gb, gb, d.bias ? (long)d.cout : 0, 0};   // S = 0: not yet run
+    if (dy_pool && d.bias && Lr.o_gcol_floats &&
+        tgpk::pool_relu_bias_fusable(N->dt, d.cout, Lr.H, Lr.W, dy_pool, dskip, y, dz)) {
+      HIPCHK(tgpk::pool_relu_backward_bias(N->dt, dy_pool, dskip, y, dz, d.relu, gb,
+                                           (float*)G_(N, i, Lr.o_gcol), N->b, Lr.H, Lr.W,
+                                           d.cout, st, &pj[1]),
+             "pool_relu_backward_bias");
+      dy_pool = nullptr;
+    } else if (dy_pool) {
+      HIPCHK(tgpk::maxpool_backward(N->dt, y, dy_pool, (void*)dy, N->b, Lr.H, Lr.W, d.cout, st),
+             "maxpool_backward");
+      dy_pool = nullptr;
+    }
+    if (pj[1].S == 0 && d.bias && Lr.o_gcol_floats &&
         tgpk::relu_bias_fusable(N->dt, d.cout, dy, dskip, y, dz)) {
       HIPCHK(tgpk::relu_backward_bias(N->dt, dy, dskip, y, dz, d.relu, gb,
                                       (float*)G_(N, i, Lr.o_gcol), P, d.cout, st, &pj[1]),
              "relu_backward_bias");
-    } else {
+    } else if (pj[1].S == 0) {
       HIPCHK(tgpk::relu_backward(N->dt, dy, dskip, y, dz, d.relu, nout, st), "relu_backward");
       if (d.bias)
         HIPCHK(tgpk::bias_grad(N->dt, dz, gb, colpart, P, d.cout, st), "bias_grad");
+      pj[1].S = 1;
     }
     float* gw = (float*)G_(N, i, Lr.o_gw);
     pj[0] = tgpk::ReduceJob{gw, gw, Lr.w_elems, 1};
@@ -344,7 +361,9 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
                               s, (float*)T_(N, i, N->o_fpart), N->fpart_floats, st),
              "conv_dgrad");
     }
-    if (d.prologue == TGP_PRO_MAXPOOL2) {
+    if (d.prologue == TGP_PRO_MAXPOOL2 && l > lo) {
+      dy_pool = dinp;   // routed by layer l - 1's ReLU backward
+    } else if (d.prologue == TGP_PRO_MAXPOOL2) {
       HIPCHK(tgpk::maxpool_backward(N->dt, src, dinp, dest_prev, N->b, Lr.inH, Lr.inW, Lr.inC,
                                     st),
              "maxpool_backward");

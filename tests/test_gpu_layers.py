@@ -119,6 +119,20 @@ def test_upcat_prologue():
                   popped=True)
 
 
+@pytest.mark.parametrize("dtype,c,bias", [(BF16, 64, True), (BF16, 64, False), (FP32, 16, True)])
+def test_pool_backward_inside_a_partition(dtype, c, bias):
+    """A max-pool prologue that is not its partition's first layer: its
+    backward is formed inside the previous layer's fused ReLU-backward / bias
+    kernel (without a bias there, by the plain pool backward).  The pooled
+    layer's output is also stashed and popped by an upsample-concat in the
+    same partition, so a skip gradient joins the routed one."""
+    net = Net("poolin", (Layer(CONV3X3, c, c, bias=bias, stash_id=0),
+                         Layer(CONV3X3, c, 2 * c, prologue=PRO_MAXPOOL2),
+                         Layer(CONV3X3, 3 * c, c, prologue=PRO_UPCAT2, pop_id=0)), c, 16, 24)
+    run_and_check(net, (3,), 1, dtype, 4, 2,
+                  f"pool inside a partition, {'bf16' if dtype == BF16 else 'fp32'} c={c} bias={bias}")
+
+
 def test_fp32_direct_conv():
     net = one_layer(Layer(CONV3X3, 16, 16), 32, 32)
     run_and_check(net, (1,), 1, FP32, 8, 4, "fp32 conv3x3 16->16")
