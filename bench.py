@@ -246,6 +246,58 @@ def cpu_baseline(wl, lo, hi, samples, dtype):
                       f"{dt:.1f} s"}
 
 
+def balance_report(mode_name, iters=5):
+    """Per-layer times (tgp_layer_times: F, F' and B plus the accumulation of
+    one micro-batch, eager launches) of the whole 5-level U-Net at the bench's
+    micro-batch of 4, and the 4-way partitions the min-max rule picks on them
+    and on forward FLOPs."""
+    import math
+    import paper_2004_09910_amd as tgp
+    from paper_2004_09910_amd.harness import Session
+    from workloads import specs
+    from workloads.specs import BF16, CKPT_NAMES
+
+    wl = specs.unet_network()
+    net = wl.net
+    b = wl.batch // wl.m
+    log("setting up", wl.name)
+    sess = Session(net, BF16, n=wl.n)
+    flop_bal = list(sess.balance)
+    us = sess.layer_times(b, CKPT_NAMES[mode_name], iters=iters)
+    ns = [int(math.floor(float(u) * 1000.0 + 0.5)) for u in us]
+    time_bal = tgp.balance_minmax(ns, wl.n)
+    flops = [tgp.layer_flops(sess.h, k) for k in range(len(net.layers))]
+    sess.close()
+
+    def parts(bal):
+        out, lo = [], 0
+        for c in bal:
+            out.append(sum(us[lo:lo + c]))
+            lo += c
+        return out
+
+    ft, tt = parts(flop_bal), parts(time_bal)
+    lines = [f"# Per-layer times and time-based balance: {wl.name}", "",
+             "Command (from the repository root on the GPU host):", "",
+             f"    python3 bench.py --balance-by-time --mode {mode_name}", "",
+             f"Micro-batch of {b} samples at {net.height}x{net.width}, checkpoint mode {mode_name}; "
+             f"each time is the mean of {iters} eager runs of F (and F' when checkpointed), B and "
+             "the accumulation of a one-layer partition (`tgp_layer_times`), launch gaps included.",
+             "", "| layer | GFLOP/sample (fwd) | us | us per GFLOP |", "|---|---:|---:|---:|"]
+    for L, f, u in zip(net.layers, flops, us):
+        lines.append(f"| {L.name} | {f / 1e9:.3f} | {u:.1f} | {u / (f / 1e9 * b):.2f} |")
+    lines += ["", "| partition rule | balance | per-partition us | slowest us |", "|---|---|---|---:|",
+              f"| forward FLOPs | {flop_bal} | {[round(v, 1) for v in ft]} | {max(ft):.1f} |",
+              f"| measured time | {time_bal} | {[round(v, 1) for v in tt]} | {max(tt):.1f} |"]
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"layer_times_{wl.name}.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps({"network": wl.name, "micro_batch": b, "mode": mode_name,
+                      "layer_us": [round(u, 2) for u in us], "flop_balance": flop_bal,
+                      "time_balance": time_bal, "flop_balance_slowest_us": round(max(ft), 2),
+                      "time_balance_slowest_us": round(max(tt), 2)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -262,6 +314,10 @@ def main():
                          "kernel that scales the HBM byte counters)")
     ap.add_argument("--summarize-profiles", metavar="DIR",
                     help="write the profiles/ summaries from rocprofv3 output under DIR")
+    ap.add_argument("--balance-by-time", action="store_true",
+                    help="only measure per-layer times of the whole 5-level U-Net at the "
+                         "bench's micro-batch, compare the time-based and FLOP-based 4-way "
+                         "partitions and write profiles/layer_times_<network>.md")
     args = ap.parse_args()
     if args.summarize_profiles:
         from workloads import specs
@@ -281,6 +337,9 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": src.numel() * 2, "copy_bytes_written": dst.numel() * 2,
                           "launches": 3}), flush=True)
+        return
+    if args.balance_by_time:
+        balance_report(args.mode)
         return
     import paper_2004_09910_amd as tgp
     from paper_2004_09910_amd.harness import Session, nchw_to_device_nhwc

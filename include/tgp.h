@@ -116,6 +116,37 @@ tgp_status tgp_get_partition(const tgp_net* net, int* n, int* balance /* >= n en
  * parts; writes balance[n].  Host only. */
 tgp_status tgp_balance_minmax(const int64_t* cost, int L, int n, int* balance);
 
+/* Time-based balance (Sec. 3: partitions balanced on per-layer costs that
+ * are measured by running the layers, rather than on an estimate).
+ *
+ * tgp_layer_times_plan plans the network as n_layers one-layer partitions
+ * for one micro-batch of b samples (m = 1) under checkpoint mode `mode`,
+ * keeping the current partition aside, and writes the workspace size the
+ * timing needs to *bytes (the plan's workspace plus four activation buffers:
+ * a layer's input, output, output gradient and input gradient).
+ *
+ * tgp_layer_times binds ws (device, 256-byte aligned, at least *bytes,
+ * caller-owned; zeroed here, so timings see zero data), then for each layer
+ * l runs F (and F' when `mode` checkpoints), B and the accumulation of
+ * partition l + 1 once to warm up and `iters` times timed with HIP events on
+ * `stream`, and writes the mean microseconds of those three calls to
+ * us[n_layers].  Layer 0 skips its input gradient, as in tgp_pipeline_step.
+ * Every layer's parameters must be bound; the accumulators are overwritten.
+ * It synchronizes `stream`, then restores the partition kept aside and
+ * leaves no plan (call tgp_plan again).  ESTATE without a timing plan;
+ * ENOSPACE / EINVAL from the workspace binding keep the timing plan.
+ *
+ * tgp_balance_by_time runs tgp_layer_times and then sets the partition that
+ * tgp_balance_minmax picks for the measured times (in whole nanoseconds)
+ * into n parts; writes it to balance[n], and the times to us (if not NULL).
+ * A later tgp_plan is required. */
+tgp_status tgp_layer_times_plan(tgp_net* net, int b, int mode, size_t* bytes);
+tgp_status tgp_layer_times(tgp_net* net, void* ws, size_t bytes, int iters, float* us,
+                           void* stream);
+tgp_status tgp_balance_by_time(tgp_net* net, void* ws, size_t bytes, int iters, int n,
+                               int* balance, float* us /* NULL or n_layers entries */,
+                               void* stream);
+
 /* Binds layer parameters (device pointers, caller-owned):
  * w: weights (net dtype, KRSC); b: float32 bias (NULL iff the layer has no
  * bias); dw_acc, db_acc: float32 gradient accumulators g^j, same layouts

@@ -66,6 +66,10 @@ _SIG = {
     "tgp_grad_accumulate": [_P, _I, _I, _I, _P],
     "tgp_pipeline_step": [_P, _P, _P, _I, _I, _I, _I, _P, _P, _P],
     "tgp_schedule_trace": [_I, _I, _I, ctypes.POINTER(ctypes.c_int32), _I, ctypes.POINTER(_I)],
+    "tgp_layer_times_plan": [_P, _I, _I, ctypes.POINTER(ctypes.c_size_t)],
+    "tgp_layer_times": [_P, _P, ctypes.c_size_t, _I, ctypes.POINTER(ctypes.c_float), _P],
+    "tgp_balance_by_time": [_P, _P, ctypes.c_size_t, _I, _I, ctypes.POINTER(_I),
+                            ctypes.POINTER(ctypes.c_float), _P],
 }
 for _name, _args in _SIG.items():
     _f = getattr(_lib, _name)
@@ -150,6 +154,31 @@ def balance_minmax(cost: Sequence[int], n: int) -> List[int]:
     out = (_I * n)()
     _check(_lib.tgp_balance_minmax(c, len(cost), n, out), "tgp_balance_minmax")
     return list(out)
+
+
+def layer_times_plan(net: int, b: int, ckpt_mode: int) -> int:
+    v = ctypes.c_size_t()
+    _check(_lib.tgp_layer_times_plan(net, b, ckpt_mode, ctypes.byref(v)), "tgp_layer_times_plan")
+    return v.value
+
+
+def _n_layers(net: int) -> int:
+    return sum(get_partition(net))
+
+
+def layer_times(net: int, ws: int, nbytes: int, iters: int, stream: int = 0) -> List[float]:
+    us = (ctypes.c_float * _n_layers(net))()
+    _check(_lib.tgp_layer_times(net, _vp(ws), nbytes, iters, us, _vp(stream)), "tgp_layer_times")
+    return list(us)
+
+
+def balance_by_time(net: int, ws: int, nbytes: int, iters: int, n: int,
+                    stream: int = 0) -> Tuple[List[int], List[float]]:
+    us = (ctypes.c_float * _n_layers(net))()
+    out = (_I * n)()
+    _check(_lib.tgp_balance_by_time(net, _vp(ws), nbytes, iters, n, out, us, _vp(stream)),
+           "tgp_balance_by_time")
+    return list(out), list(us)
 
 
 def bind_params(net: int, layer: int, w: int, b: Optional[int], dw_acc: int,

@@ -7,6 +7,7 @@
 
 #include <algorithm>
 #include <array>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -94,6 +95,13 @@ struct tgp_net {
   int gslots = 1;
   size_t o_gslot = 0, gslot_stride = 0;
   std::vector<std::array<tgpk::ReduceJob, 2>> pend;
+  // Per-layer timing plan (tgp_layer_times_plan): one-layer partitions,
+  // m = 1, plus four activation buffers from o_lt on; the caller's
+  // partition is kept aside until tgp_layer_times restores it.
+  bool lt_planned = false;
+  size_t o_lt = 0, lt_act = 0;
+  int lt_saved_n = 0;
+  std::vector<int> lt_saved_lo, lt_saved_hi;
   // state per (i, j): index (i-1)*n + (j-1)
   std::vector<uint8_t> st;
   std::vector<const void*> saved_x;
@@ -241,6 +249,13 @@ tgp_status run_forward(tgp_net* N, int j, int i, int phase, const void* x_in, vo
                                 (float*)T_(N, i, N->o_fpart), N->fpart_floats, st),
              "conv_forward");
     }
+    // a stashed layer that ends the partition wrote the partition output;
+    // its consumer reads the stash slot (a recompute leaves the slot as the
+    // forward wrote it, bit for bit)
+    if (phase != 2 && l == hi - 1 && d.stash_id >= 0)
+      HIPCHK(hipMemcpyAsync(W_(N, stash_off(N, i, d.stash_id, false)), out, Lr.out_bytes,
+                            hipMemcpyDeviceToDevice, st),
+             "stash copy");
     src = out;
   }
   return TGP_OK;
@@ -649,6 +664,7 @@ tgp_status tgp_balance_minmax(const int64_t* cost, int L, int n, int* balance) {
 
 tgp_status tgp_set_partition(tgp_net* N, int n, const int* balance) {
   if (!N) return fail(TGP_EINVAL, "net is NULL");
+  N->lt_planned = false;
   int L = (int)N->L.size();
   if (n < 1 || n > L) return fail(TGP_EINVAL, "n=%d must be in 1..%d", n, L);
   std::vector<int> bal;
@@ -711,6 +727,7 @@ tgp_status tgp_set_lanes(tgp_net* N, int lanes) {
 
 tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
   if (!N || !bytes) return fail(TGP_EINVAL, "NULL argument");
+  N->lt_planned = false;
   if (m < 1 || B < 1) return fail(TGP_EINVAL, "B and m must be positive");
   if (B % m) return fail(TGP_EINVAL, "B=%d is not divisible by m=%d", B, m);
   if (mode < 0 || mode > 2) return fail(TGP_EINVAL, "bad checkpoint mode %d", mode);
@@ -844,6 +861,119 @@ tgp_status tgp_stash_ptr(tgp_net* N, int i, int stash_id, int grad, void** p) {
   if (i < 1 || i > N->m) return fail(TGP_EINVAL, "micro-batch %d out of 1..%d", i, N->m);
   if (!N->stash_layer.count(stash_id)) return fail(TGP_EINVAL, "no skip %d", stash_id);
   *p = W_(N, stash_off(N, i, stash_id, grad != 0));
+  return TGP_OK;
+}
+
+// ------------------------------------------------------------ time-based balance
+
+tgp_status tgp_layer_times_plan(tgp_net* N, int b, int mode, size_t* bytes) {
+  if (!N || !bytes) return fail(TGP_EINVAL, "NULL argument");
+  if (b < 1) return fail(TGP_EINVAL, "b must be positive");
+  const int L = (int)N->L.size();
+  if (!N->lt_planned) {   // keep the caller's partition (not an earlier timing plan's)
+    N->lt_saved_n = N->n;
+    N->lt_saved_lo = N->lo;
+    N->lt_saved_hi = N->hi;
+  }
+  const int saved_n = N->lt_saved_n;
+  const std::vector<int> saved_lo = N->lt_saved_lo, saved_hi = N->lt_saved_hi;
+  std::vector<int> ones(L, 1);
+  tgp_status r = tgp_set_partition(N, L, ones.data());
+  size_t off = 0;
+  if (r == TGP_OK) r = tgp_plan(N, b, 1, mode, &off);
+  N->lt_saved_n = saved_n;
+  N->lt_saved_lo = saved_lo;
+  N->lt_saved_hi = saved_hi;
+  if (r != TGP_OK) return r;
+  size_t act = 16;
+  for (const auto& l : N->L)
+    act = std::max({act, l.out_bytes, (size_t)b * l.inH * l.inW * l.inC * N->esz});
+  N->o_lt = al256(off);
+  N->lt_act = al256(act);
+  N->ws_need = N->o_lt + 4 * N->lt_act;
+  N->lt_planned = true;
+  *bytes = N->ws_need;
+  return TGP_OK;
+}
+
+// The caller's partition back, no plan.
+static void lt_restore(tgp_net* N) {
+  const int L = (int)N->L.size();
+  N->n = N->lt_saved_n;
+  N->lo = N->lt_saved_lo;
+  N->hi = N->lt_saved_hi;
+  for (int k = 0; k < N->n; ++k)
+    for (int l = N->lo[k]; l < N->hi[k] && l < L; ++l) N->L[l].part = k;
+  N->lt_planned = false;
+  N->planned = false;
+  N->ws = nullptr;
+}
+
+static tgp_status lt_run(tgp_net* N, int iters, float* us, hipStream_t st, hipEvent_t e0, hipEvent_t e1) {
+  const int L = (int)N->L.size();
+  HIPCHK(hipMemsetAsync(N->ws, 0, N->ws_need, st), "hipMemsetAsync");
+  char* X = N->ws + N->o_lt;
+  char* Y = X + N->lt_act;
+  char* DY = Y + N->lt_act;
+  char* DX = DY + N->lt_act;
+  const int ckpt = ckpt_of(N->mode, 1, 1) ? 1 : 0;
+  for (int l = 0; l < L; ++l) {
+    const int j = l + 1;
+    double total_ms = 0;
+    for (int it = 0; it <= iters; ++it) {   // it = 0 warms up
+      HIPCHK(hipEventRecord(e0, st), "hipEventRecord");
+      tgp_status r = tgp_stage_forward(N, j, 1, ckpt, X, Y, st);
+      if (r == TGP_OK) r = tgp_stage_backward_recompute(N, j, 1, DY, l == 0 ? nullptr : DX, st);
+      if (r == TGP_OK) r = tgp_grad_accumulate(N, j, 1, 1, st);
+      if (r != TGP_OK) return r;
+      HIPCHK(hipEventRecord(e1, st), "hipEventRecord");
+      HIPCHK(hipEventSynchronize(e1), "hipEventSynchronize");
+      float ms = 0;
+      HIPCHK(hipEventElapsedTime(&ms, e0, e1), "hipEventElapsedTime");
+      if (it > 0) total_ms += ms;
+    }
+    us[l] = (float)(total_ms / iters * 1000.0);
+  }
+  return TGP_OK;
+}
+
+tgp_status tgp_layer_times(tgp_net* N, void* ws, size_t bytes, int iters, float* us,
+                           void* stream) {
+  if (!N || !us) return fail(TGP_EINVAL, "NULL argument");
+  if (!N->lt_planned) return fail(TGP_ESTATE, "tgp_layer_times_plan has not been called");
+  if (iters < 1) return fail(TGP_EINVAL, "iters must be positive");
+  tgp_status r = tgp_bind_workspace(N, ws, bytes);
+  if (r == TGP_OK) r = check_ready(N);
+  if (r != TGP_OK) return r;   // plan and partition kept: the caller may bind and retry
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+    if (e0) (void)hipEventDestroy(e0);
+    lt_restore(N);
+    return fail(TGP_EHIP, "hipEventCreate failed");
+  }
+  r = lt_run(N, iters, us, S(stream), e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  lt_restore(N);
+  return r;
+}
+
+tgp_status tgp_balance_by_time(tgp_net* N, void* ws, size_t bytes, int iters, int n,
+                               int* balance, float* us, void* stream) {
+  if (!N || !balance) return fail(TGP_EINVAL, "NULL argument");
+  const int L = (int)N->L.size();
+  if (n < 1 || n > L) return fail(TGP_EINVAL, "n=%d must be in 1..%d", n, L);
+  std::vector<float> t(L, 0.f);
+  tgp_status r = tgp_layer_times(N, ws, bytes, iters, t.data(), stream);
+  if (r != TGP_OK) return r;
+  std::vector<int64_t> cost(L);
+  for (int l = 0; l < L; ++l) cost[l] = (int64_t)std::llround((double)t[l] * 1000.0);   // ns
+  std::vector<int> bal;
+  if (!balance_dp(cost, n, bal)) return fail(TGP_EINVAL, "no split");
+  r = tgp_set_partition(N, n, bal.data());
+  if (r != TGP_OK) return r;
+  std::copy(bal.begin(), bal.end(), balance);
+  if (us) std::copy(t.begin(), t.end(), us);
   return TGP_OK;
 }
 

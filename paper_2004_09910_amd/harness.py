@@ -97,6 +97,38 @@ class Session:
         self.params[idx] = {"w": wk, "b": bt, "dw": dw, "db": db, "w64": w64,
                             "b64": None if b is None else b[0]}
 
+    def _set_bounds(self):
+        self.balance = tgp.get_partition(self.h)
+        self.n = len(self.balance)
+        self.bounds = []
+        lo = 0
+        for c in self.balance:
+            self.bounds.append((lo, lo + c))
+            lo += c
+
+    def layer_times(self, b: int, mode: int, iters: int = 3) -> List[float]:
+        """Mean microseconds of F (+ F'), B and the accumulation of each layer
+        for one micro-batch of b samples (tgp_layer_times).  Drops the plan."""
+        nbytes = tgp.layer_times_plan(self.h, b, mode)
+        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        us = tgp.layer_times(self.h, ws.data_ptr(), ws.numel(), iters,
+                             torch.cuda.current_stream().cuda_stream)
+        self.ws = None
+        return us
+
+    def balance_by_time(self, b: int, n: int, mode: int, iters: int = 3):
+        """Re-partitions into n parts on measured per-layer times
+        (tgp_balance_by_time); returns (balance, per-layer microseconds).
+        Drops the plan."""
+        nbytes = tgp.layer_times_plan(self.h, b, mode)
+        ws = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=self.device)
+        bal, us = tgp.balance_by_time(self.h, ws.data_ptr(), ws.numel(), iters, n,
+                                      torch.cuda.current_stream().cuda_stream)
+        self.ws = None
+        self._set_bounds()
+        assert self.balance == bal
+        return bal, us
+
     def plan(self, B: int, m: int, mode: int, lanes: int = 1) -> int:
         tgp.set_lanes(self.h, lanes)
         self.lanes = lanes

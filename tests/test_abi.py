@@ -164,6 +164,39 @@ def test_plan_and_workspace_validation():
     tgp.net_destroy(h)
 
 
+def test_layer_times_plan_and_error_paths():
+    """tgp_layer_times_plan: one-layer partitions for one micro-batch, a
+    workspace at least the plan's plus four activation buffers; the caller's
+    partition comes back only through tgp_layer_times, and the checks that
+    run before any GPU work."""
+    h, plan_bytes = _bound_net(mode=0, B=4, m=2, n=2)
+    try:
+        assert tgp.get_partition(h) == [2, 2]
+        us = (tgp.ctypes.c_float * 4)()
+        bal = (tgp.ctypes.c_int * 2)()
+        # no timing plan yet
+        assert tgp.call_status("tgp_layer_times", h, FAKE, 1 << 30, 1, us, None) == tgp.ESTATE
+        nbytes = tgp.layer_times_plan(h, 2, 0)
+        assert tgp.get_partition(h) == [1, 1, 1, 1]
+        act = 2 * 8 * 8 * 8 * 4          # the largest activation of one 2-sample micro-batch
+        assert nbytes >= 4 * act
+        # a second timing plan keeps the original partition aside, not the singletons
+        assert tgp.layer_times_plan(h, 2, 0) == nbytes
+        assert tgp.call_status("tgp_layer_times", h, FAKE, nbytes, 0, us, None) == tgp.EINVAL
+        assert tgp.call_status("tgp_layer_times", h, FAKE, nbytes - 1, 1, us, None) == tgp.ENOSPACE
+        assert tgp.call_status("tgp_balance_by_time", h, FAKE, nbytes, 1, 0, bal, us, None) == \
+            tgp.EINVAL
+        assert tgp.call_status("tgp_balance_by_time", h, FAKE, nbytes, 1, 5, bal, us, None) == \
+            tgp.EINVAL
+        # the failed binding kept the timing plan; a new partition drops it
+        tgp.set_partition(h, 2)
+        assert tgp.call_status("tgp_layer_times", h, FAKE, nbytes, 1, us, None) == tgp.ESTATE
+        assert tgp.call_status("tgp_layer_times_plan", h, 0, 0, tgp.ctypes.byref(
+            tgp.ctypes.c_size_t())) == tgp.EINVAL
+    finally:
+        tgp.net_destroy(h)
+
+
 def test_lanes_replicate_only_the_transient_buffers():
     """tgp_set_lanes: 1..TGP_MAX_LANES, invalidates the plan, and each extra
     lane adds the same per-lane block (stash slots, stored activations and

@@ -117,6 +117,24 @@ def test_small_unet_bf16_pipeline(m, n):
         same_bits(runs[0], r)
 
 
+@pytest.mark.parametrize("bal", [(4, 3, 4), (2, 4, 5), (4, 7)])
+def test_partition_ending_at_a_stashed_layer(bal):
+    """Partitions whose last layer is also stashed (enc1b with skip 1, enc0b
+    with skip 0): the layer's output is the partition output and must reach
+    its stash slot too, where a later partition's upsample-concat pops it."""
+    net = specs.unet(3, 64, 64, 24, "unet3-c64")
+    B = 4
+    pair = oracle_network_variants(net, BF16, B)
+    runs = []
+    for mode in MODES:
+        say(f"unet3 balance {bal} mode={mode}")
+        got = gpu_network(net, BF16, B, 2, len(bal), mode, balance=list(bal))
+        check_network(got, pair, BF16, f"unet3 balance {bal} mode={mode}")
+        runs.append(got)
+    for r in runs[1:]:
+        same_bits(runs[0], r)
+
+
 def test_microbatch_count_changes_only_accumulation_order():
     """Per-sample activations do not depend on m (no intra-batch computation,
     Sec. 2), so outputs are bit-identical across m and gradients differ only by
