@@ -132,6 +132,90 @@ __global__ __launch_bounds__(256) void conv_wgrad_direct(const T* __restrict__ x
   part[(long)blockIdx.y * E + e] = acc;
 }
 
+// 1x1 convolution with at most kSmallCo output channels (the network head):
+// one thread per pixel reads its channels in 16-byte packs.
+constexpr int kSmallCo = 4;
+
+template <typename T>
+__global__ __launch_bounds__(256) void conv1x1_small_fwd_k(const T* __restrict__ x,
+                                                           const T* __restrict__ w,
+                                                           const float* __restrict__ b,
+                                                           T* __restrict__ y, long P, int Cin,
+                                                           int Cout, int relu) {
+  constexpr int N = Pk<T>::N;
+  const long p = (long)blockIdx.x * 256 + threadIdx.x;
+  if (p >= P) return;
+  float acc[kSmallCo];
+#pragma unroll
+  for (int co = 0; co < kSmallCo; ++co) acc[co] = (co < Cout && b) ? b[co] : 0.f;
+  for (int c0 = 0; c0 < Cin; c0 += N) {
+    float xv[N];
+    Pk<T>::un(ld16(x + p * Cin + c0), xv);
+#pragma unroll
+    for (int co = 0; co < kSmallCo; ++co) {
+      if (co >= Cout) break;
+#pragma unroll
+      for (int i = 0; i < N; ++i) acc[co] += xv[i] * Elt<T>::ld(w + (long)co * Cin + c0 + i);
+    }
+  }
+#pragma unroll
+  for (int co = 0; co < kSmallCo; ++co) {
+    if (co >= Cout) break;
+    Elt<T>::st(y + p * Cout + co, relu ? fmaxf(acc[co], 0.f) : acc[co]);
+  }
+}
+
+// Its weight gradient dW[co][ci] = sum_p dz[p][co] x[p][ci]: block b covers
+// pixels [b*rows, (b+1)*rows); thread t takes channel pack t % CP of pixels
+// t / CP, t / CP + 256 / CP, ... in order; row lanes are then added in order
+// in LDS and part[b][co][ci] is written.  Needs 256 % CP == 0 (CP = Cin / pack).
+template <typename T>
+__global__ __launch_bounds__(256) void wgrad1x1_small_k(const T* __restrict__ x,
+                                                        const T* __restrict__ dz,
+                                                        float* __restrict__ part, long P,
+                                                        int Cin, int Cout, long rows) {
+  constexpr int N = Pk<T>::N;
+  __shared__ float red[256 * N];
+  const int CP = Cin / N;
+  const int cp = threadIdx.x % CP, rl = threadIdx.x / CP, nl = 256 / CP;
+  const long p0 = (long)blockIdx.x * rows, p1 = p0 + rows < P ? p0 + rows : P;
+  float acc[kSmallCo][N];
+#pragma unroll
+  for (int co = 0; co < kSmallCo; ++co)
+#pragma unroll
+    for (int i = 0; i < N; ++i) acc[co][i] = 0.f;
+  for (long p = p0 + rl; p < p1; p += nl) {
+    float xv[N];
+    Pk<T>::un(ld16(x + p * Cin + cp * N), xv);
+#pragma unroll
+    for (int co = 0; co < kSmallCo; ++co) {
+      if (co >= Cout) break;
+      const float g = Elt<T>::ld(dz + p * Cout + co);
+#pragma unroll
+      for (int i = 0; i < N; ++i) acc[co][i] += g * xv[i];
+    }
+  }
+  const long E = (long)Cout * Cin;
+#pragma unroll
+  for (int co = 0; co < kSmallCo; ++co) {   // one output channel at a time through LDS
+    if (co >= Cout) break;                  // block-uniform
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < N; ++i) red[threadIdx.x * N + i] = acc[co][i];
+    __syncthreads();
+    if (rl == 0) {
+      float sum[N];
+#pragma unroll
+      for (int i = 0; i < N; ++i) sum[i] = red[cp * N + i];
+      for (int l = 1; l < nl; ++l)
+#pragma unroll
+        for (int i = 0; i < N; ++i) sum[i] += red[(l * CP + cp) * N + i];
+#pragma unroll
+      for (int i = 0; i < N; ++i) part[(long)blockIdx.x * E + (long)co * Cin + cp * N + i] = sum[i];
+    }
+  }
+}
+
 long direct_wgrad_pps(long P) { return P < 256 ? 256 : (P + 63) / 64; }
 int direct_wgrad_splits(long P) { return (int)((P + direct_wgrad_pps(P) - 1) / direct_wgrad_pps(P)); }
 
@@ -640,11 +724,33 @@ inline bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 // ---------------------------------------------------------------- dispatch
 
+static long relu_bias_rows(long P, int C, int N);
+
+// The 1x1 path for few output channels (the network head).
+static bool small1x1_ok(int dt, const ConvShape& s, const void* x) {
+  const int N = dt == 0 ? 8 : 4;
+  if (s.taps != 1 || s.cout > kSmallCo || s.cin % N || !al16(x)) return false;
+  const int CP = s.cin / N;
+  return CP <= 256 && 256 % CP == 0;
+}
+
 hipError_t conv_forward(int dt, const void* x, const void* w, const float* b, void* y,
                         const ConvShape& s, int relu, float* part, size_t part_cap,
                         hipStream_t st) {
   if (mfma_conv_ok(dt, s.cin, s.cout))
     return conv_forward_mfma(x, w, b, y, s, relu, part, part_cap, st);
+  if (small1x1_ok(dt, s, x)) {
+    const long P = s.pixels();
+    ProfScope ps("conv1x1_small_fwd", 2.0 * P * s.cout * s.cin,
+                 (dt == 0 ? 2.0 : 4.0) * P * (s.cin + s.cout), st);
+    if (dt == 0)
+      TGP_LAUNCH(ps, conv1x1_small_fwd_k<bf16_t>, dim3(cdiv(P, 256)), dim3(256), 0, st,
+                 (const bf16_t*)x, (const bf16_t*)w, b, (bf16_t*)y, P, s.cin, s.cout, relu);
+    else
+      TGP_LAUNCH(ps, conv1x1_small_fwd_k<float>, dim3(cdiv(P, 256)), dim3(256), 0, st,
+                 (const float*)x, (const float*)w, b, (float*)y, P, s.cin, s.cout, relu);
+    return hipGetLastError();
+  }
   long P = s.pixels();
   dim3 g(cdiv(P * s.cout, 256));
   int esz = dt == 0 ? 2 : 4;
@@ -686,6 +792,12 @@ hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, voi
 
 size_t conv_wgrad_partial_floats(int dt, const ConvShape& s) {
   if (mfma_conv_ok(dt, s.cin, s.cout)) return wgrad_mfma_partial_floats(s);
+  const int N = dt == 0 ? 8 : 4;
+  if (small1x1_ok(dt, s, (const void*)16)) {   // (alignment is checked per call)
+    const size_t direct = (size_t)direct_wgrad_splits(s.pixels()) * s.cout * s.taps * s.cin;
+    const size_t small = (size_t)cdiv(s.pixels(), relu_bias_rows(s.pixels(), s.cin, N)) * s.cout * s.cin;
+    return direct > small ? direct : small;
+  }
   return (size_t)direct_wgrad_splits(s.pixels()) * s.cout * s.taps * s.cin;
 }
 
@@ -695,6 +807,28 @@ hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* p
   if (defer && extra) return hipErrorInvalidValue;
   if (mfma_conv_ok(dt, s.cin, s.cout))
     return conv_wgrad_mfma(x, dz, dw, partial, s, st, extra, defer);
+  if (small1x1_ok(dt, s, x)) {
+    const long P = s.pixels(), E = (long)s.cout * s.cin;
+    const long rows = relu_bias_rows(P, s.cin, dt == 0 ? 8 : 4);
+    const int nbk = cdiv(P, rows);
+    {
+      ProfScope ps("wgrad1x1_small", 2.0 * P * E,
+                   (dt == 0 ? 2.0 : 4.0) * P * (s.cin + s.cout) + 4.0 * nbk * E, st);
+      if (dt == 0)
+        TGP_LAUNCH(ps, wgrad1x1_small_k<bf16_t>, dim3(nbk), dim3(256), 0, st, (const bf16_t*)x,
+                   (const bf16_t*)dz, partial, P, s.cin, s.cout, rows);
+      else
+        TGP_LAUNCH(ps, wgrad1x1_small_k<float>, dim3(nbk), dim3(256), 0, st, (const float*)x,
+                   (const float*)dz, partial, P, s.cin, s.cout, rows);
+    }
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    if (defer) {
+      *defer = ReduceJob{partial, dw, E, nbk};
+      return hipSuccess;
+    }
+    return splitk_reduce_launch(partial, dw, E, nbk, st, extra);
+  }
   long P = s.pixels();
   long E = (long)s.cout * s.taps * s.cin;
   long pps = direct_wgrad_pps(P);

@@ -105,6 +105,15 @@ def test_head_without_relu():
     run_and_check(net, (1,), 1, BF16, 4, 2, "head 1x1 64->1")
 
 
+@pytest.mark.parametrize("dtype,cin,cout,relu", [(BF16, 64, 3, True), (BF16, 128, 4, False),
+                                                 (FP32, 16, 2, True)])
+def test_small_output_1x1(dtype, cin, cout, relu):
+    """1x1 convolutions with at most four output channels (the head's path:
+    one thread per pixel forward, block-reduced weight gradient)."""
+    net = one_layer(Layer(CONV1X1, cin, cout, relu=relu), 20, 12)
+    run_and_check(net, (1,), 1, dtype, 4, 2, f"1x1 {cin}->{cout} relu={relu}")
+
+
 def test_maxpool_prologue():
     net = Net("pool", (Layer(CONV3X3, 64, 64), Layer(CONV3X3, 64, 128, prologue=PRO_MAXPOOL2)),
               64, 24, 20)
