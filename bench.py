@@ -246,6 +246,141 @@ def cpu_baseline(wl, lo, hi, samples, dtype):
                       f"{dt:.1f} s"}
 
 
+def memory_account(net, B, m, mode):
+    """Bytes one training step of `net` needs on the device, all of it caller
+    memory (the library allocates nothing): bf16 weights, fp32 biases, fp32
+    gradient accumulators, the tgp_plan workspace, and the bf16 input, target
+    and output plus the loss.  Returns (parameters, parameter bytes,
+    workspace bytes, total bytes), or None if the plan is refused."""
+    import paper_2004_09910_amd as tgp
+    from paper_2004_09910_amd.harness import layer_tuple
+    from workloads.specs import BF16
+    h = tgp.net_create([layer_tuple(L) for L in net.layers], net.in_channels, net.height,
+                       net.width, BF16)
+    try:
+        tgp.set_partition(h, 1)
+        ws = tgp.plan(h, B, m, mode)
+    except tgp.TgpError:
+        return None
+    finally:
+        tgp.net_destroy(h)
+    w = sum(L.cout * L.taps * L.cin for L in net.layers)
+    nb = sum(L.cout for L in net.layers if L.bias)
+    pbytes = 2 * w + 4 * nb + 4 * (w + nb)
+    oh, ow = net.out_hw()
+    io = 2 * B * (net.in_channels * net.height * net.width + 2 * net.out_channels() * oh * ow) + 4
+    return w + nb, pbytes, ws, pbytes + ws + io
+
+
+def memory_report():
+    """U-Net memory benchmark analog (Sec. 4.2.2 and its table): the largest
+    U-Net (B conv blocks per level, C channels at the first level; six levels,
+    so five down-samplings; 3x192x192 input, 1x192x192 output, batch 32) whose
+    planned memory fits one MI355X, without checkpointing or micro-batches and
+    with checkpointing at m = 8 and m = 32."""
+    from workloads import specs
+    from workloads.specs import CKPT_ALWAYS, CKPT_NEVER
+    HBM = 288e9
+    B, hw, in_ch, levels = 32, 192, 3, 6
+    settings = [("no checkpointing, m = 1", 1, CKPT_NEVER),
+                ("checkpointing (always), m = 8", 8, CKPT_ALWAYS),
+                ("checkpointing (always), m = 32", 32, CKPT_ALWAYS)]
+    channels = [32, 48, 64, 72, 96, 128, 160, 192, 224, 256, 320, 384]
+    rows = []
+    for label, m, mode in settings:
+        best = None
+        for C in channels:
+            def fits(blocks):
+                net = specs.unet(levels, C, in_ch, hw, f"unet6-B{blocks}-C{C}", blocks=blocks)
+                a = memory_account(net, B, m, mode)
+                return a if a is not None and a[3] <= HBM else None
+            if not fits(1):
+                continue
+            lo, hi = 1, 2
+            while fits(hi) and hi < 512:
+                lo, hi = hi, hi * 2
+            while hi - lo > 1:          # largest blocks count that fits
+                mid = (lo + hi) // 2
+                if fits(mid):
+                    lo = mid
+                else:
+                    hi = mid
+            a = fits(lo)
+            if best is None or a[0] > best[2][0]:
+                best = (lo, C, a)
+        blocks, C, (params, pbytes, ws, total) = best
+        log(f"{label}: (B, C) = ({blocks}, {C}), {params / 1e9:.2f}B parameters, {total / 1e9:.1f} GB")
+        rows.append({"setting": label, "m": m, "blocks": blocks, "channels": C, "params": params,
+                     "param_gb": pbytes / 1e9, "workspace_gb": ws / 1e9, "total_gb": total / 1e9})
+    lines = ["# U-Net memory benchmark analog: largest model on one MI355X", "",
+             "Command (from the repository root; the search runs on the host planner, the check "
+             "below on the GPU):", "", "    python3 bench.py --memory", "",
+             f"Six-level U-Net (five down-samplings), B conv blocks per level, C channels at the "
+             f"first level, input 3x192x192, output 1x192x192, batch {B}, bf16.  Memory is what "
+             "the caller allocates: bf16 weights, fp32 biases and accumulators (6 bytes per "
+             "weight), the `tgp_plan` workspace and the input, target and output.  Budget "
+             f"{HBM / 1e9:.0f} GB.  Among C in {channels} and any B, the configuration with the "
+             "most parameters that fits:", "",
+             "| setting | (B, C) | parameters | parameter memory | workspace | total |",
+             "|---|---|---:|---:|---:|---:|"]
+    for r in rows:
+        lines.append(f"| {r['setting']} | ({r['blocks']}, {r['channels']}) | {r['params'] / 1e9:.2f}B | "
+                     f"{r['param_gb']:.1f} GB | {r['workspace_gb']:.1f} GB | {r['total_gb']:.1f} GB |")
+    check = memory_check()
+    if check:
+        lines += ["", "Planned against allocated memory on the GPU for the 5-level, 64-channel network "
+                  "(64x192x192 input, batch 32), one `tgp_pipeline_step` each; allocated is "
+                  "torch's peak over the step, including the caller's tensors:", "",
+                  "| setting | planned | allocated peak | workspace |", "|---|---:|---:|---:|"]
+        for c in check:
+            lines.append(f"| {c['setting']} | {c['planned_gb']:.3f} GB | {c['allocated_gb']:.3f} GB | "
+                         f"{c['workspace_gb']:.3f} GB |")
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, "memory_unet.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps({"largest": rows, "check": check}), flush=True)
+
+
+def memory_check():
+    """On a GPU: plan, allocate and run one pipeline step of the 5-level,
+    64-channel U-Net at batch 32 without and with checkpointing; the planned
+    bytes against torch's allocated peak."""
+    import torch
+    if not torch.cuda.is_available():
+        return None
+    from paper_2004_09910_amd.harness import Session, nchw_to_device_nhwc
+    from workloads import specs, synth
+    from workloads.specs import BF16, CKPT_ALWAYS, CKPT_NEVER
+    wl = specs.unet_network()
+    net = wl.net
+    out = []
+    for label, m, mode in [("no checkpointing, m = 1", 1, CKPT_NEVER),
+                           ("checkpointing (always), m = 8", 8, CKPT_ALWAYS)]:
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        sess = Session(net, BF16, n=1)
+        ws = sess.plan(wl.batch, m, mode)
+        _, xraw = synth.input_x(net, wl.batch, BF16)
+        h, w = net.out_hw()
+        _, traw = synth.target_like((wl.batch, net.out_channels(), h, w), BF16)
+        x = nchw_to_device_nhwc(xraw, BF16)
+        t = nchw_to_device_nhwc(traw, BF16)
+        loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+        y = torch.empty((wl.batch, h, w, net.out_channels()), dtype=x.dtype, device="cuda")
+        log(f"memory check: {label}")
+        sess.pipeline_step(x, t, loss, y)
+        torch.cuda.synchronize()
+        peak = torch.cuda.max_memory_allocated() - base
+        planned = memory_account(net, wl.batch, m, mode)[3]
+        out.append({"setting": label, "planned_gb": planned / 1e9, "allocated_gb": peak / 1e9,
+                    "workspace_gb": ws / 1e9})
+        sess.close()
+        del sess, x, t, y, loss
+    return out
+
+
 def balance_report(mode_name, iters=5):
     """Per-layer times (tgp_layer_times: F, F' and B plus the accumulation of
     one micro-batch, eager launches) of the whole 5-level U-Net at the bench's
@@ -314,6 +449,12 @@ def main():
                          "kernel that scales the HBM byte counters)")
     ap.add_argument("--summarize-profiles", metavar="DIR",
                     help="write the profiles/ summaries from rocprofv3 output under DIR")
+    ap.add_argument("--memory", action="store_true",
+                    help="only run the U-Net memory benchmark analog: the largest (blocks, "
+                         "channels) U-Net whose planned memory fits one MI355X, with and "
+                         "without checkpointing, and (on a GPU) the planned against the "
+                         "allocated memory of the 5-level network; writes "
+                         "profiles/memory_unet.md")
     ap.add_argument("--balance-by-time", action="store_true",
                     help="only measure per-layer times of the whole 5-level U-Net at the "
                          "bench's micro-batch, compare the time-based and FLOP-based 4-way "
@@ -340,6 +481,9 @@ def main():
         return
     if args.balance_by_time:
         balance_report(args.mode)
+        return
+    if args.memory:
+        memory_report()
         return
     import paper_2004_09910_amd as tgp
     from paper_2004_09910_amd.harness import Session, nchw_to_device_nhwc

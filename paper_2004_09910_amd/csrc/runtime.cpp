@@ -55,6 +55,7 @@ struct LayerRt {
   // gradient-slot offsets of the weight gradient's split-K partial slices
   // and the bias gradient's column-sum partials (0 bytes when unused)
   size_t o_gpart = 0, o_gcol = 0, o_gcol_floats = 0;
+  bool defer_w = false, defer_b = false;   // partials kept for the accumulation
   std::vector<size_t> o_sto_out, o_sto_pro;  // per stored set
   bool has_wt = false;
 };
@@ -308,8 +309,8 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
   void* gnext = T_(N, i, N->o_g1);
   void* dz = T_(N, i, N->o_dz);
   void* dinp = T_(N, i, N->o_dinp);
-  float* part = (float*)T_(N, i, N->o_part);          // depthwise weight gradient
-  float* colpart = (float*)T_(N, i, N->o_colpart);    // bias_grad
+  float* part = (float*)T_(N, i, N->o_part);          // weight partials reduced at once
+  float* colpart = (float*)T_(N, i, N->o_colpart);    // bias partials reduced at once
   const void* dy = dy_out;
   // the pool gradient of layer l + 1's max-pool prologue, when its backward
   // is left to layer l's ReLU backward (dy then names the buffer it would
@@ -330,12 +331,15 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
     std::array<tgpk::ReduceJob, 2>& pj = N->pend[(size_t)(i - 1) * N->L.size() + l];
     float* gb = d.bias ? (float*)G_(N, i, Lr.o_gb) : nullptr;
     pj[1] = tgpk::ReduceJob{gb, gb, d.bias ? (long)d.cout : 0, 0};   // S = 0: not yet run
+    // column partials: kept in the slot, or (too large to keep) reduced at once
+    float* bpart = Lr.defer_b ? (float*)G_(N, i, Lr.o_gcol) : colpart;
+    tgpk::ReduceJob* bdefer = Lr.defer_b ? &pj[1] : nullptr;
     if (dy_pool && d.bias && Lr.o_gcol_floats &&
         tgpk::pool_relu_bias_fusable(N->dt, d.cout, Lr.H, Lr.W, dy_pool, dskip, y, dz)) {
-      HIPCHK(tgpk::pool_relu_backward_bias(N->dt, dy_pool, dskip, y, dz, d.relu, gb,
-                                           (float*)G_(N, i, Lr.o_gcol), N->b, Lr.H, Lr.W,
-                                           d.cout, st, &pj[1]),
+      HIPCHK(tgpk::pool_relu_backward_bias(N->dt, dy_pool, dskip, y, dz, d.relu, gb, bpart,
+                                           N->b, Lr.H, Lr.W, d.cout, st, bdefer),
              "pool_relu_backward_bias");
+      if (!bdefer) pj[1].S = 1;
       dy_pool = nullptr;
     } else if (dy_pool) {
       HIPCHK(tgpk::maxpool_backward(N->dt, y, dy_pool, (void*)dy, N->b, Lr.H, Lr.W, d.cout, st),
@@ -344,9 +348,10 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
     }
     if (pj[1].S == 0 && d.bias && Lr.o_gcol_floats &&
         tgpk::relu_bias_fusable(N->dt, d.cout, dy, dskip, y, dz)) {
-      HIPCHK(tgpk::relu_backward_bias(N->dt, dy, dskip, y, dz, d.relu, gb,
-                                      (float*)G_(N, i, Lr.o_gcol), P, d.cout, st, &pj[1]),
+      HIPCHK(tgpk::relu_backward_bias(N->dt, dy, dskip, y, dz, d.relu, gb, bpart, P, d.cout, st,
+                                      bdefer),
              "relu_backward_bias");
+      if (!bdefer) pj[1].S = 1;
     } else if (pj[1].S == 0) {
       HIPCHK(tgpk::relu_backward(N->dt, dy, dskip, y, dz, d.relu, nout, st), "relu_backward");
       if (d.bias)
@@ -360,8 +365,9 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
              "dw_wgrad");
     } else {
       tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
-      HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr, dz, gw, (float*)G_(N, i, Lr.o_gpart), s, st,
-                              nullptr, &pj[0]),
+      HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr, dz, gw,
+                              Lr.defer_w ? (float*)G_(N, i, Lr.o_gpart) : part, s, st, nullptr,
+                              Lr.defer_w ? &pj[0] : nullptr),
              "conv_wgrad");
     }
     if (l == lo && dx_in == nullptr) break;
@@ -782,16 +788,26 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
     tgpk::ConvShape s{N->b, Lr.H, Lr.W, Lr.d.cin, Lr.d.cout, Lr.taps};
     Lr.has_wt = Lr.d.kind != TGP_DWCONV3X3 && tgpk::conv_dgrad_uses_wt(N->dt, s);
     Lr.o_wt = Lr.has_wt ? takeL(Lr.w_elems * N->esz) : 0;
+    // Split-K partials stay in the slot for the accumulation to sum when a
+    // layer's are at most kDeferBytes per micro-batch; larger ones (deep,
+    // wide layers) are reduced at once through a lane buffer, so the slots
+    // do not grow with the sum of every layer's partials.
+    constexpr size_t kDeferBytes = 32u << 20;
     const long P = (long)N->b * Lr.H * Lr.W;
+    Lr.defer_w = false;
+    Lr.o_gpart = 0;
     if (Lr.d.kind == TGP_DWCONV3X3) {
       max_part = std::max(max_part, tgpk::dw_wgrad_partial_floats(N->b, Lr.H, Lr.W, Lr.d.cout));
-      Lr.o_gpart = 0;
     } else {
       const size_t pf = tgpk::conv_wgrad_partial_floats(N->dt, s);
-      Lr.o_gpart = takeG(std::max<size_t>(pf, 1) * 4);
+      Lr.defer_w = pf * 4 <= kDeferBytes;
+      if (Lr.defer_w) Lr.o_gpart = takeG(std::max<size_t>(pf, 1) * 4);
+      else max_part = std::max(max_part, pf);
     }
     Lr.o_gcol_floats = Lr.d.bias ? tgpk::relu_bias_partial_floats(N->dt, P, Lr.d.cout) : 0;
-    Lr.o_gcol = Lr.o_gcol_floats ? takeG(Lr.o_gcol_floats * 4) : 0;
+    Lr.defer_b = Lr.o_gcol_floats && Lr.o_gcol_floats * 4 <= kDeferBytes;
+    Lr.o_gcol = Lr.defer_b ? takeG(Lr.o_gcol_floats * 4) : 0;
+    if (Lr.o_gcol_floats && !Lr.defer_b) max_col = std::max(max_col, Lr.o_gcol_floats);
     max_col = std::max(max_col, tgpk::colsum_partial_floats(P, Lr.d.cout));
   }
   N->o_g0 = takeL(max_act);

@@ -50,6 +50,7 @@ def run_and_check(net, bal, j, dtype, B, m, what, popped=False):
     (128, 64, 5, 96, 2, 1),      # 2 rows a stage, two input-channel tiles
     (64, 64, 3, 192, 2, 2),      # 1 row a stage, K ranges of one row
     (128, 128, 5, 24, 4, 2),     # 4 rows a stage, 16-pixel k steps across rows
+    (512, 512, 24, 24, 8, 2),    # weight-gradient partials too large to keep: reduced at once
 ])
 def test_conv3x3(cin, cout, h, w, B, m):
     net = one_layer(Layer(CONV3X3, cin, cout), h, w)

@@ -136,24 +136,35 @@ def plain_stack(n_layers: int, c: int, h: int, w: int, name="stack") -> Net:
     return Net(name, layers, c, h, w)
 
 
-def unet(levels: int, base: int, in_ch: int, hw: int, name="unet", head=True) -> Net:
-    """Symmetric U-Net: per level two conv3x3+bias+ReLU; max-pool between
-    encoder levels; decoder level l = nearest 2x upsample of level l+1, concat
-    with the stashed encoder output of level l, then two conv3x3+ReLU; a 1x1
-    head to one channel without ReLU."""
+def unet(levels: int, base: int, in_ch: int, hw: int, name="unet", head=True,
+         blocks: int = 2) -> Net:
+    """Symmetric U-Net: per level `blocks` conv3x3+bias+ReLU (two in every
+    benchmark network); max-pool between encoder levels; decoder level l =
+    nearest 2x upsample of level l+1, concat with the stashed encoder output
+    of level l, then `blocks` conv3x3+ReLU; a 1x1 head to one channel without
+    ReLU.  Channels double at each down-sampling (base at level 0)."""
+    assert blocks >= 1
     C = [base * (2 ** l) for l in range(levels)]
+
+    def nm(prefix, k):
+        return f"{prefix}{chr(ord('a') + k)}" if k < 26 else f"{prefix}_{k}"
+
     layers = []
     prev = in_ch
     for l in range(levels):
-        pro = PRO_NONE if l == 0 else PRO_MAXPOOL2
-        layers.append(Layer(CONV3X3, prev, C[l], prologue=pro, name=f"enc{l}a"))
-        stash = l if l < levels - 1 else -1
-        layers.append(Layer(CONV3X3, C[l], C[l], stash_id=stash, name=f"enc{l}b"))
+        for k in range(blocks):
+            pro = PRO_MAXPOOL2 if (l > 0 and k == 0) else PRO_NONE
+            stash = l if (k == blocks - 1 and l < levels - 1) else -1
+            layers.append(Layer(CONV3X3, prev if k == 0 else C[l], C[l], prologue=pro,
+                                stash_id=stash, name=nm(f"enc{l}", k)))
         prev = C[l]
     for l in range(levels - 2, -1, -1):
-        layers.append(Layer(CONV3X3, prev + C[l], C[l], prologue=PRO_UPCAT2, pop_id=l,
-                            name=f"dec{l}a"))
-        layers.append(Layer(CONV3X3, C[l], C[l], name=f"dec{l}b"))
+        for k in range(blocks):
+            if k == 0:
+                layers.append(Layer(CONV3X3, prev + C[l], C[l], prologue=PRO_UPCAT2, pop_id=l,
+                                    name=nm(f"dec{l}", 0)))
+            else:
+                layers.append(Layer(CONV3X3, C[l], C[l], name=nm(f"dec{l}", k)))
         prev = C[l]
     if head:
         layers.append(Layer(CONV1X1, prev, 1, relu=False, name="head"))
