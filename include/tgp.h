@@ -207,8 +207,9 @@ tgp_status tgp_stage_forward(tgp_net* net, int j, int i, int checkpoint, const v
  * (then the first layer's data gradient is skipped).  Gradients of skips
  * popped here go to their gradient slots; skips stashed here add the
  * gradient found in theirs.  The weight gradient g_i^j is left for
- * tgp_grad_accumulate, as partial sums over pixel ranges in the workspace.  Order (Sec. 2.1): for a given j, i = m, m-1, .., 1,
- * each after F_{i,j} and after tgp_grad_accumulate(j, i+1); ESTATE otherwise. */
+ * tgp_grad_accumulate, as partial sums over pixel ranges in the workspace.
+ * Order (Sec. 2.1): for a given j, i = m, m-1, .., 1, each after F_{i,j}
+ * and after tgp_grad_accumulate(j, i+1); ESTATE otherwise. */
 tgp_status tgp_stage_backward_recompute(tgp_net* net, int j, int i, const void* dy_out,
                                         void* dx_in, void* stream);
 
@@ -226,7 +227,15 @@ tgp_status tgp_grad_accumulate(tgp_net* net, int j, int i, int overwrite, void* 
  * 1/2 factor; backward clocks k = m+n-1..1 with j descending, each task
  * F'_{i,j} (if checkpointed) + B_{i,j} + grad accumulate.  Writes the loss
  * (float32) to *loss_dev and the network output to y_out (may be NULL).
- * B, m, n and ckpt_mode must match tgp_plan and tgp_set_partition. */
+ * B, m, n and ckpt_mode must match tgp_plan and tgp_set_partition.
+ * With more than one lane (tgp_set_lanes) the step forks from `stream`
+ * onto library-owned streams (default priority), micro-batch i's tasks on
+ * lane (i - 1) % lanes and the accumulations, in schedule order, on one
+ * more stream that waits for each B_{i,j}, and joins back into `stream`
+ * before the loss; the results are bit-identical to one lane.  The streams
+ * are created on first use (on the current device) and destroyed with the
+ * net; the fork and join are events, so the step can be captured into a
+ * HIP graph from `stream`. */
 tgp_status tgp_pipeline_step(tgp_net* net, const void* x, const void* target, int B, int m,
                              int n, int ckpt_mode, float* loss_dev, void* y_out, void* stream);
 

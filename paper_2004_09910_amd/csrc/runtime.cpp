@@ -96,6 +96,16 @@ struct tgp_net {
   int gslots = 1;
   size_t o_gslot = 0, gslot_stride = 0;
   std::vector<std::array<tgpk::ReduceJob, 2>> pend;
+  // Streams and events tgp_pipeline_step forks onto with several lanes (one
+  // per lane plus one for the accumulations), created on first use on the
+  // device current then; default priority.
+  std::vector<hipStream_t> lane_streams;
+  std::vector<hipEvent_t> lane_events;
+  int lane_device = -1;
+  ~tgp_net() {
+    for (auto e : lane_events) (void)hipEventDestroy(e);
+    for (auto st : lane_streams) (void)hipStreamDestroy(st);
+  }
   // Per-layer timing plan (tgp_layer_times_plan): one-layer partitions,
   // m = 1, plus four activation buffers from o_lt on; the caller's
   // partition is kept aside until tgp_layer_times restores it.
@@ -507,6 +517,15 @@ struct GpuExec : Exec {
   char* y_out;
   hipStream_t st;
   size_t in_mb_bytes, out_mb_bytes;
+  // With K > 1 lanes, micro-batch i's tasks run on lane[(i - 1) % K] and the
+  // accumulations, in schedule order, on acc, which waits for each B_{i,j}
+  // through its lane's event (every cross-stream edge points from a lane to
+  // acc, never back).  K = 1: everything on st.
+  int K = 1;
+  hipStream_t lane[TGP_MAX_LANES] = {};
+  hipEvent_t lane_ev[TGP_MAX_LANES] = {};
+  hipStream_t acc = nullptr;
+  hipStream_t on(int i) const { return K > 1 ? lane[(i - 1) % K] : st; }
   const void* bnd(int i, int j) {  // output of partition j for micro-batch i (j = 0: input)
     if (j == 0) return x + (size_t)(i - 1) * in_mb_bytes;
     if (j == N->n) return y_out ? (const void*)(y_out + (size_t)(i - 1) * out_mb_bytes)
@@ -518,7 +537,7 @@ struct GpuExec : Exec {
     return W_(N, N->o_gbnd[(i - 1) * N->n + j]);
   }
   tgp_status forward(int i, int j, bool ckpt) override {
-    return tgp_stage_forward(N, j, i, ckpt ? 1 : 0, bnd(i, j - 1), (void*)bnd(i, j), st);
+    return tgp_stage_forward(N, j, i, ckpt ? 1 : 0, bnd(i, j - 1), (void*)bnd(i, j), on(i));
   }
   tgp_status loss(int i) override {
     const LayerRt& last = N->L.back();
@@ -528,16 +547,21 @@ struct GpuExec : Exec {
                                       target + (size_t)(i - 1) * out_mb_bytes, gbnd(i, N->n),
                                       (float*)W_(N, N->o_loss) + (i - 1),
                                       (float*)T_(N, i, N->o_msepart), n_mb, 1.0f / (float)numel,
-                                      st),
+                                      on(i)),
            "mse_forward_backward");
     return TGP_OK;
   }
   tgp_status backward(int i, int j, bool) override {
-    return tgp_stage_backward_recompute(N, j, i, gbnd(i, j), j > 1 ? gbnd(i, j - 1) : nullptr,
-                                        st);
+    tgp_status r = tgp_stage_backward_recompute(N, j, i, gbnd(i, j),
+                                                j > 1 ? gbnd(i, j - 1) : nullptr, on(i));
+    if (r != TGP_OK || K == 1) return r;
+    const int k = (i - 1) % K;
+    HIPCHK(hipEventRecord(lane_ev[k], lane[k]), "hipEventRecord");
+    HIPCHK(hipStreamWaitEvent(acc, lane_ev[k], 0), "hipStreamWaitEvent");
+    return TGP_OK;
   }
   tgp_status accumulate(int i, int j, bool ow) override {
-    return tgp_grad_accumulate(N, j, i, ow ? 1 : 0, st);
+    return tgp_grad_accumulate(N, j, i, ow ? 1 : 0, K > 1 ? acc : st);
   }
 };
 
@@ -1046,6 +1070,31 @@ tgp_status tgp_grad_accumulate(tgp_net* N, int j, int i, int overwrite, void* st
   return TGP_OK;
 }
 
+// Streams (count) and events (2 count) for tgp_pipeline_step's lanes, on the
+// current device; recreated if the device changed.
+static tgp_status lane_streams_ready(tgp_net* N, int count) {
+  int dev = 0;
+  HIPCHK(hipGetDevice(&dev), "hipGetDevice");
+  if (N->lane_device != dev) {
+    for (auto e : N->lane_events) (void)hipEventDestroy(e);
+    for (auto st : N->lane_streams) (void)hipStreamDestroy(st);
+    N->lane_events.clear();
+    N->lane_streams.clear();
+    N->lane_device = dev;
+  }
+  while ((int)N->lane_streams.size() < count) {
+    hipStream_t st = nullptr;
+    HIPCHK(hipStreamCreateWithFlags(&st, hipStreamNonBlocking), "hipStreamCreateWithFlags");
+    N->lane_streams.push_back(st);
+  }
+  while ((int)N->lane_events.size() < 2 * count) {
+    hipEvent_t e = nullptr;
+    HIPCHK(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreateWithFlags");
+    N->lane_events.push_back(e);
+  }
+  return TGP_OK;
+}
+
 tgp_status tgp_pipeline_step(tgp_net* N, const void* x, const void* target, int B, int m, int n,
                              int mode, float* loss_dev, void* y_out, void* stream) {
   tgp_status r = check_ready(N);
@@ -1066,7 +1115,30 @@ tgp_status tgp_pipeline_step(tgp_net* N, const void* x, const void* target, int 
   ex.st = S(stream);
   ex.in_mb_bytes = (size_t)N->b * N->H * N->W * N->in_c * N->esz;
   ex.out_mb_bytes = N->out_bytes_mb;
+  ex.K = std::min(N->lanes, m);
+  if (ex.K > 1) {
+    // fork: lanes + the accumulation stream wait for the caller's stream
+    r = lane_streams_ready(N, ex.K + 1);
+    if (r != TGP_OK) return r;
+    for (int k = 0; k < ex.K; ++k) {
+      ex.lane[k] = N->lane_streams[k];
+      ex.lane_ev[k] = N->lane_events[k];
+    }
+    ex.acc = N->lane_streams[ex.K];
+    hipEvent_t fork = N->lane_events[ex.K];
+    HIPCHK(hipEventRecord(fork, ex.st), "hipEventRecord");
+    for (int k = 0; k <= ex.K; ++k)
+      HIPCHK(hipStreamWaitEvent(N->lane_streams[k], fork, 0), "hipStreamWaitEvent");
+  }
   r = run_schedule(m, n, mode, ex);
+  if (ex.K > 1) {
+    // join (also after an error, so that no fork is left open in a capture)
+    for (int k = 0; k <= ex.K; ++k) {
+      hipEvent_t e = N->lane_events[ex.K + 1 + k];
+      HIPCHK(hipEventRecord(e, N->lane_streams[k]), "hipEventRecord");
+      HIPCHK(hipStreamWaitEvent(ex.st, e, 0), "hipStreamWaitEvent");
+    }
+  }
   if (r != TGP_OK) return r;
   const LayerRt& last = N->L.back();
   long numel = (long)N->B * last.H * last.W * last.d.cout;

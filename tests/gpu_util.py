@@ -30,9 +30,9 @@ def storage(dtype):
     return "bf16" if dtype == BF16 else "f64"
 
 
-def gpu_network(net, dtype, B, m, n, mode, balance=None):
+def gpu_network(net, dtype, B, m, n, mode, balance=None, lanes=1):
     sess = Session(net, dtype, n=n, balance=balance)
-    sess.plan(B, m, mode)
+    sess.plan(B, m, mode, lanes)
     _, xraw = synth.input_x(net, B, dtype)
     h, w = net.out_hw()
     _, traw = synth.target_like((B, net.out_channels(), h, w), dtype)

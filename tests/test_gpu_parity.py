@@ -117,6 +117,48 @@ def test_small_unet_bf16_pipeline(m, n):
         same_bits(runs[0], r)
 
 
+@pytest.mark.parametrize("mode", MODES)
+def test_pipeline_lanes_are_bit_identical(mode):
+    """tgp_pipeline_step with 2 and 3 lanes, forked onto the library's own
+    streams, against one lane: loss, output and every weight and bias
+    gradient, bit for bit (3-level U-Net, 3 partitions, m = 4)."""
+    net = specs.unet(3, 64, 64, 24, "unet3-c64")
+    runs = []
+    for k in (1, 2, 3):
+        say(f"pipeline lanes={k} mode={mode}")
+        runs.append(gpu_network(net, BF16, 8, 4, 3, mode, lanes=k))
+    for r in runs[1:]:
+        same_bits(runs[0], r)
+        assert r["loss"] == runs[0]["loss"]
+        assert torch.equal(r["y_t"], runs[0]["y_t"])
+
+
+def test_pipeline_step_graph_capture():
+    """A two-lane pipeline step captured into a HIP graph from one stream
+    (the fork onto the lane streams and the join are events) and replayed
+    three times, with eager work and synchronisation between replays: every
+    replay matches the eager step bit for bit."""
+    net = specs.unet(3, 64, 64, 24, "unet3-c64")
+    say("pipeline graph capture, 2 lanes")
+    eager = gpu_network(net, BF16, 8, 4, 3, CKPT_ALWAYS, lanes=2)
+    sess, x, t, loss, y = eager["sess"], eager["x"], eager["t"], eager["loss_t"], eager["y_t"]
+    ref_y = y.clone()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        sess.pipeline_step(x, t, loss, y, stream=torch.cuda.current_stream().cuda_stream)
+    for rep in range(3):
+        loss.zero_()
+        y.zero_()
+        for p in sess.params.values():
+            p["dw"].fill_(7.0)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert float(loss.item()) == eager["loss"], rep
+        assert torch.equal(y, ref_y), rep
+        same_bits(eager, {"grads": sess.grads64()})
+        torch.randn(4096, device="cuda").sum().item()   # eager work between replays
+
+
 @pytest.mark.parametrize("bal", [(4, 3, 4), (2, 4, 5), (4, 7)])
 def test_partition_ending_at_a_stashed_layer(bal):
     """Partitions whose last layer is also stashed (enc1b with skip 1, enc0b
