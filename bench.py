@@ -381,6 +381,88 @@ def memory_check():
     return out
 
 
+def sweep_report(steps, warmup):
+    """The whole 5-level U-Net (4 partitions, batch 32) trained by
+    tgp_pipeline_step, one step captured as a HIP graph (two lanes when
+    m > 1), for m in 1, 4, 16, 32 under each checkpoint mode: samples/s,
+    the recompute overhead against never, the planned memory and whether
+    every gradient is bit-identical to the never run at the same m (the
+    checkpoint modes change only when values are computed, Sec. 2.1)."""
+    import numpy as np
+    import torch
+    from paper_2004_09910_amd.harness import Session, nchw_to_device_nhwc
+    from workloads import specs, synth
+    from workloads.specs import BF16, CKPT_NAMES
+
+    wl = specs.unet_network()
+    net, B = wl.net, wl.batch
+    _, xraw = synth.input_x(net, B, BF16)
+    oh, ow = net.out_hw()
+    _, traw = synth.target_like((B, net.out_channels(), oh, ow), BF16)
+    x = nchw_to_device_nhwc(xraw, BF16)
+    t = nchw_to_device_nhwc(traw, BF16)
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    y = torch.empty((B, oh, ow, net.out_channels()), dtype=x.dtype, device="cuda")
+    rows = []
+    for m in (1, 4, 16, 32):
+        grads = {}
+        for mode_name in ("never", "except_last", "always"):
+            mode = CKPT_NAMES[mode_name]
+            lanes = 2 if m > 1 else 1
+            log(f"sweep: m={m} {mode_name}")
+            sess = Session(net, BF16, n=wl.n)
+            sess.plan(B, m, mode, lanes)
+            for _ in range(warmup):
+                sess.pipeline_step(x, t, loss, y, stream=torch.cuda.current_stream().cuda_stream)
+            torch.cuda.synchronize()
+            grads[mode_name] = sess.grads64()
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                sess.pipeline_step(x, t, loss, y, stream=torch.cuda.current_stream().cuda_stream)
+            graph.replay()
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                graph.replay()
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) * 1e3 / steps
+            total = memory_account(net, B, m, mode)[3]
+            rows.append({"m": m, "mode": mode_name, "ms_per_step": ms, "samples_per_s": B * 1e3 / ms,
+                         "memory_gb": total / 1e9, "loss": float(loss.item())})
+            del graph
+            sess.close()
+        for mode_name in ("except_last", "always"):
+            same = all(np.array_equal(grads[mode_name][k][0], grads["never"][k][0]) and
+                       (grads["never"][k][1] is None or
+                        np.array_equal(grads[mode_name][k][1], grads["never"][k][1]))
+                       for k in grads["never"])
+            for r in rows:
+                if r["m"] == m and r["mode"] == mode_name:
+                    r["bit_identical_to_never"] = same
+    for r in rows:
+        base = next(q for q in rows if q["m"] == r["m"] and q["mode"] == "never")
+        r["recompute_overhead"] = r["ms_per_step"] / base["ms_per_step"] - 1.0
+    lines = [f"# Checkpoint / micro-batch sweep: {wl.name}", "",
+             "Command (from the repository root on the GPU host):", "",
+             f"    python3 bench.py --sweep --steps {steps} --warmup {warmup}", "",
+             f"The 5-level, 64-channel U-Net in {wl.n} partitions (FLOP balance), batch {B}, "
+             "trained by `tgp_pipeline_step` (MSE loss), one step captured as a HIP graph "
+             "and replayed; two concurrency lanes when m > 1.  Memory is the planned total "
+             "(parameters, accumulators, workspace, input, target, output).  The overhead is the "
+             "step time against never at the same m; the paper's bound for recomputing every "
+             "forward is one extra forward, a third of forward plus backward.", "",
+             "| m | mode | ms/step | samples/s | overhead vs never | memory | gradients = never |",
+             "|---:|---|---:|---:|---:|---:|---|"]
+    for r in rows:
+        ident = "" if r["mode"] == "never" else ("bit-identical" if r["bit_identical_to_never"] else "DIFFER")
+        lines.append(f"| {r['m']} | {r['mode']} | {r['ms_per_step']:.2f} | {r['samples_per_s']:.0f} | "
+                     f"{100 * r['recompute_overhead']:+.1f}% | {r['memory_gb']:.2f} GB | {ident} |")
+    os.makedirs(PROFILES, exist_ok=True)
+    with open(os.path.join(PROFILES, f"sweep_{wl.name}.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print(json.dumps({"network": wl.name, "rows": rows}), flush=True)
+
+
 def balance_report(mode_name, iters=5):
     """Per-layer times (tgp_layer_times: F, F' and B plus the accumulation of
     one micro-batch, eager launches) of the whole 5-level U-Net at the bench's
@@ -455,6 +537,11 @@ def main():
                          "without checkpointing, and (on a GPU) the planned against the "
                          "allocated memory of the 5-level network; writes "
                          "profiles/memory_unet.md")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only run the checkpoint / micro-batch sweep of the whole 5-level "
+                         "U-Net pipeline (m in 1, 4, 16, 32 under each checkpoint mode): "
+                         "samples/s, recompute overhead, planned memory and bit-identity of "
+                         "gradients across modes; writes profiles/sweep_unet5-network.md")
     ap.add_argument("--balance-by-time", action="store_true",
                     help="only measure per-layer times of the whole 5-level U-Net at the "
                          "bench's micro-batch, compare the time-based and FLOP-based 4-way "
@@ -484,6 +571,9 @@ def main():
         return
     if args.memory:
         memory_report()
+        return
+    if args.sweep:
+        sweep_report(args.steps, args.warmup)
         return
     import paper_2004_09910_amd as tgp
     from paper_2004_09910_amd.harness import Session, nchw_to_device_nhwc
