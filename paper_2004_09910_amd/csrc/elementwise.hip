@@ -642,79 +642,85 @@ __global__ __launch_bounds__(256) void accumulate_k(float* __restrict__ acc, con
 }
 
 // acc_k = r_k or acc_k + r_k with r_k = sum_{s < S_k} g_k[s n_k + e], every
-// entry in one launch.  Blocks blk0[k] .. blk0[k + 1] - 1 serve entry k.  A
-// block of 1024 threads covers C4 float4 columns with LANES = 1024 / C4
+// entry in one launch.  Tiles blk0[k] .. blk0[k + 1] - 1 serve entry k.  A
+// tile of 1024 threads covers C4 float4 columns with LANES = 1024 / C4
 // split lanes; lane l sums s = l, l + LANES, .. in ascending order, then the
 // lanes are added in order 0 .. LANES - 1, with (C4, LANES) a function of S
-// only (the layout splitk_reduce uses for the same S, plus a single lane
-// when S = 1), so the sum is fixed by the shape.  An entry with n not a
-// multiple of 4 takes one element per thread, s ascending.
-__device__ __forceinline__ int acc_c4(int S) {
-  return S >= 64 ? 16 : (S >= 16 ? 64 : (S >= 2 ? 256 : 1024));
+// only, so the sum is fixed by the shape.  An entry with n not a multiple of
+// 4 takes one element per thread, s ascending.
+__host__ __device__ __forceinline__ int acc_c4(int S) {
+  // about four slices per split lane: C4 = 4096 / S rounded down to a power
+  // of two, within 16 .. 1024
+  int c = 1024;
+  while (c > 16 && (long)c * S > 4096) c >>= 1;
+  return c;
 }
 
-__global__ __launch_bounds__(1024) void reduce_accumulate_k(AccBatch b, int overwrite) {
+__global__ __launch_bounds__(1024) void reduce_accumulate_k(AccBatch b, int overwrite,
+                                                            int ntiles) {
+  // blocks are persistent over tiles (tile = the block of the layout above),
+  // so the entry lookup and the block start are paid once per block
   __shared__ float4 red[1024];
-  int k = 0;   // entry of this block (block-uniform)
-  while (k + 1 < b.count && (int)blockIdx.x >= b.blk0[k + 1]) ++k;
-  const long bx = (long)blockIdx.x - b.blk0[k];
-  const long E = b.n[k];
-  const int S = b.S[k];
-  const float* __restrict__ part = b.g[k];
-  float* __restrict__ acc = b.acc[k];
-  if (E % 4) {
-    const long e = bx * 1024 + threadIdx.x;
-    if (e < E) {
-      float r = 0.f;
-      for (int s = 0; s < S; ++s) r += part[(long)s * E + e];
-      acc[e] = overwrite ? r : acc[e] + r;
+  int k = 0;   // entry of the current tile (tiles only increase)
+  for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    while (k + 1 < b.count && tile >= b.blk0[k + 1]) ++k;
+    const long bx = (long)tile - b.blk0[k];
+    const long E = b.n[k];
+    const int S = b.S[k];
+    const float* __restrict__ part = b.g[k];
+    float* __restrict__ acc = b.acc[k];
+    if (E % 4) {   // tile-uniform
+      const long e = bx * 1024 + threadIdx.x;
+      if (e < E) {
+        float r = 0.f;
+        for (int s = 0; s < S; ++s) r += part[(long)s * E + e];
+        acc[e] = overwrite ? r : acc[e] + r;
+      }
+      continue;
     }
-    return;
-  }
-  const int C4 = acc_c4(S), LANES = 1024 / C4;
-  const int col = threadIdx.x % C4, lane = threadIdx.x / C4;
-  const long e4 = (bx * C4 + col) * 4;
-  float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-  if (e4 < E) {
-    int s = lane;
-    // eight independent loads in flight per step
-    for (; s + 7 * LANES < S; s += 8 * LANES) {
-      float4 t[8];
+    const int C4 = acc_c4(S), LANES = 1024 / C4;
+    const int col = threadIdx.x % C4, lane = threadIdx.x / C4;
+    const long e4 = (bx * C4 + col) * 4;
+    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (e4 < E) {
+      // up to eight loads in flight per step; slices past S add zeros
+      for (int s = lane; s < S; s += 8 * LANES) {
+        float4 t[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) t[u] = *(const float4*)(part + (long)(s + u * LANES) * E + e4);
+        for (int u = 0; u < 8; ++u)
+          t[u] = s + u * LANES < S ? *(const float4*)(part + (long)(s + u * LANES) * E + e4)
+                                   : make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        a.x += t[u].x; a.y += t[u].y; a.z += t[u].z; a.w += t[u].w;
+        for (int u = 0; u < 8; ++u) {
+          a.x += t[u].x; a.y += t[u].y; a.z += t[u].z; a.w += t[u].w;
+        }
       }
     }
-    for (; s < S; s += LANES) {
-      const float4 t = *(const float4*)(part + (long)s * E + e4);
-      a.x += t.x; a.y += t.y; a.z += t.z; a.w += t.w;
+    if (LANES == 1) {   // tile-uniform
+      if (e4 < E) {
+        if (!overwrite) {
+          const float4 o = *(const float4*)(acc + e4);
+          a.x = o.x + a.x; a.y = o.y + a.y; a.z = o.z + a.z; a.w = o.w + a.w;
+        }
+        *(float4*)(acc + e4) = a;
+      }
+      continue;
     }
-  }
-  if (LANES == 1) {   // block-uniform
-    if (e4 < E) {
+    red[lane * C4 + col] = a;
+    __syncthreads();
+    if (lane == 0 && e4 < E) {
+      float4 r = red[col];
+      for (int l = 1; l < LANES; ++l) {
+        const float4 t = red[l * C4 + col];
+        r.x += t.x; r.y += t.y; r.z += t.z; r.w += t.w;
+      }
       if (!overwrite) {
         const float4 o = *(const float4*)(acc + e4);
-        a.x = o.x + a.x; a.y = o.y + a.y; a.z = o.z + a.z; a.w = o.w + a.w;
+        r.x = o.x + r.x; r.y = o.y + r.y; r.z = o.z + r.z; r.w = o.w + r.w;
       }
-      *(float4*)(acc + e4) = a;
+      *(float4*)(acc + e4) = r;
     }
-    return;
-  }
-  red[lane * C4 + col] = a;
-  __syncthreads();
-  if (lane == 0 && e4 < E) {
-    float4 r = red[col];
-    for (int l = 1; l < LANES; ++l) {
-      const float4 t = red[l * C4 + col];
-      r.x += t.x; r.y += t.y; r.z += t.z; r.w += t.w;
-    }
-    if (!overwrite) {
-      const float4 o = *(const float4*)(acc + e4);
-      r.x = o.x + r.x; r.y = o.y + r.y; r.z = o.z + r.z; r.w = o.w + r.w;
-    }
-    *(float4*)(acc + e4) = r;
+    __syncthreads();   // red is rewritten by the next tile
   }
 }
 
@@ -1131,7 +1137,7 @@ hipError_t grad_accumulate_batch(AccBatch b, int overwrite, hipStream_t st) {
     if (b.n[k] <= 0 || b.S[k] < 1) continue;
     b.acc[used] = b.acc[k]; b.g[used] = b.g[k]; b.n[used] = b.n[k]; b.S[used] = b.S[k];
     b.blk0[used] = (int)blocks;
-    const int C4 = b.S[k] >= 64 ? 16 : (b.S[k] >= 16 ? 64 : (b.S[k] >= 2 ? 256 : 1024));
+    const int C4 = acc_c4(b.S[k]);
     blocks += b.n[k] % 4 ? cdiv(b.n[k], 1024L) : cdiv(b.n[k], 4L * C4);
     bytes += 4.0 * b.n[k] * (b.S[k] + (overwrite ? 1 : 2));
     ++used;
@@ -1140,7 +1146,8 @@ hipError_t grad_accumulate_batch(AccBatch b, int overwrite, hipStream_t st) {
   if (used == 0) return hipSuccess;
   if (blocks >= (1L << 31)) return hipErrorInvalidValue;
   ProfScope ps("reduce_accumulate", 0.0, bytes, st);
-  TGP_LAUNCH(ps, reduce_accumulate_k, dim3((unsigned)blocks), dim3(1024), 0, st, b, overwrite);
+  const unsigned grid = (unsigned)(blocks < 512 ? blocks : 512);   // two blocks per CU
+  TGP_LAUNCH(ps, reduce_accumulate_k, dim3(grid), dim3(1024), 0, st, b, overwrite, (int)blocks);
   return hipGetLastError();
 }
 
