@@ -525,6 +525,8 @@ def main():
     ap.add_argument("--mode", default="always", choices=["always", "except_last", "never"])
     ap.add_argument("--lanes", type=int, default=2,
                     help="concurrency lanes: micro-batch i runs on stream (i - 1) %% lanes")
+    ap.add_argument("--pairs", action="store_true",
+                    help="two micro-batches per launch (needs even lanes and m)")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of a HIP graph")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three device-to-device copies of 1 GiB (the reference "
@@ -587,6 +589,7 @@ def main():
     sess = Session(net, BF16, n=wl.n, bind_layers=None)
     lo, hi = sess.bounds[0]
     sess.plan(wl.batch, wl.m, mode, args.lanes)
+    sess.pairs = args.pairs
     B, m = wl.batch, wl.m
     _, xraw = synth.input_x(net, B, BF16)
     x = nchw_to_device_nhwc(xraw, BF16)
@@ -688,6 +691,8 @@ def main():
     roof["avg_launch_us"] = 1e3 * per_launch_ms
     roof["timed"] = "eager pass of the step on one stream, each launch timed alone" \
         if graph is not None else "the timed eager steps"
+    if args.pairs:
+        roof["timed"] += "; two micro-batches per launch"
     kernel_ms = sum(r["ms"] for r in stats) / per_step_div
 
     out = {
@@ -699,7 +704,7 @@ def main():
                    "layers": hi - lo, "global_batch": B, "micro_batches": m,
                    "checkpoint": args.mode, "input": f"{B}x{net.in_channels}x{net.height}x{net.width}",
                    "dx_in": True, "launch": "hip_graph" if graph is not None else "eager",
-                   "lanes": args.lanes},
+                   "lanes": args.lanes, "pairs": args.pairs},
         "mfma_util_pct": 100.0 * step_flops / (ms_step * 1e-3) / BF16_PEAK,
         "step_tflop": step_flops / 1e12,
         "kernel_busy_ms_per_step": kernel_ms,

@@ -213,11 +213,28 @@ tgp_status tgp_stage_forward(tgp_net* net, int j, int i, int checkpoint, const v
 tgp_status tgp_stage_backward_recompute(tgp_net* net, int j, int i, const void* dy_out,
                                         void* dx_in, void* stream);
 
-/* g^j (+)= g_i^j into the bound float32 accumulators of partition j's layers
+/* Two tasks at once (Sec. 3.2.3: micro-batches are independent).
+ * tgp_stage_forward2 runs F_{i0,j} and F_{i1,j}, and
+ * tgp_stage_backward_recompute2 runs F'_{i0,j} + B_{i0,j} and F'_{i1,j} +
+ * B_{i1,j} with i1 = i0 - 1, layer by layer, each convolution and weight
+ * gradient as one launch over both micro-batches where its kernel takes two
+ * tensors.  Each micro-batch's arguments, checks and results are those of
+ * the single-task call (bit-identical values); the two must be on different
+ * lanes, and the backward pair needs two or more lanes (per-micro-batch
+ * gradient slots), so B_{i1,j} may run before the accumulation of i0;
+ * tgp_grad_accumulate still runs in the order i = m..1.  dx0 and dx1 are
+ * both NULL or both set. */
+tgp_status tgp_stage_forward2(tgp_net* net, int j, int i0, int i1, int checkpoint0,
+                              int checkpoint1, const void* x0, const void* x1, void* y0,
+                              void* y1, void* stream);
+tgp_status tgp_stage_backward_recompute2(tgp_net* net, int j, int i0, int i1, const void* dy0,
+                                         const void* dy1, void* dx0, void* dx1, void* stream);
+
+/* g^j (+)= g_i^j into the bound float32 accumulators of partition j's layers/* g^j (+)= g_i^j into the bound float32 accumulators of partition j's layers
  * (Sec. 2: the gradient is the sum of g_i^j over i); the partial sums B_{i,j}
  * left are added up here, in an order fixed by the shapes.  overwrite must be 1
  * exactly for i = m (the first backward of a step), else 0.  Requires
- * B_{i,j}; ESTATE otherwise. */
+ * B_{i,j} and, for i < m, the accumulation of i + 1; ESTATE otherwise. */
 tgp_status tgp_grad_accumulate(tgp_net* net, int j, int i, int overwrite, void* stream);
 
 /* One training step over the whole network: scatter x (B samples) into m

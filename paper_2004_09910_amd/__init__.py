@@ -66,6 +66,8 @@ _SIG = {
     "tgp_grad_accumulate": [_P, _I, _I, _I, _P],
     "tgp_pipeline_step": [_P, _P, _P, _I, _I, _I, _I, _P, _P, _P],
     "tgp_schedule_trace": [_I, _I, _I, ctypes.POINTER(ctypes.c_int32), _I, ctypes.POINTER(_I)],
+    "tgp_stage_forward2": [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P],
+    "tgp_stage_backward_recompute2": [_P, _I, _I, _I, _P, _P, _P, _P, _P],
     "tgp_layer_times_plan": [_P, _I, _I, ctypes.POINTER(ctypes.c_size_t)],
     "tgp_layer_times": [_P, _P, ctypes.c_size_t, _I, ctypes.POINTER(ctypes.c_float), _P],
     "tgp_balance_by_time": [_P, _P, ctypes.c_size_t, _I, _I, ctypes.POINTER(_I),
@@ -217,6 +219,20 @@ def stage_backward_recompute(net: int, j: int, i: int, dy_out: int, dx_in: Optio
                              stream: int = 0) -> None:
     _check(_lib.tgp_stage_backward_recompute(net, j, i, _vp(dy_out), _vp(dx_in), _vp(stream)),
            "tgp_stage_backward_recompute")
+
+
+def stage_forward2(net: int, j: int, i0: int, i1: int, checkpoint0: bool, checkpoint1: bool,
+                   x0: int, x1: int, y0: int, y1: int, stream: int = 0) -> None:
+    _check(_lib.tgp_stage_forward2(net, j, i0, i1, int(checkpoint0), int(checkpoint1),
+                                   _vp(x0), _vp(x1), _vp(y0), _vp(y1), _vp(stream)),
+           "tgp_stage_forward2")
+
+
+def stage_backward_recompute2(net: int, j: int, i0: int, i1: int, dy0: int, dy1: int,
+                              dx0: Optional[int], dx1: Optional[int], stream: int = 0) -> None:
+    _check(_lib.tgp_stage_backward_recompute2(net, j, i0, i1, _vp(dy0), _vp(dy1), _vp(dx0),
+                                              _vp(dx1), _vp(stream)),
+           "tgp_stage_backward_recompute2")
 
 
 def grad_accumulate(net: int, j: int, i: int, overwrite: bool, stream: int = 0) -> None:

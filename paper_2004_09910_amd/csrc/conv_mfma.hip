@@ -1457,4 +1457,36 @@ hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hi
   return hipGetLastError();
 }
 
+// Two micro-batches of one layer: one launch where the planned kernel takes
+// two tensors (the nine-tap kernel), else one launch each; the same values
+// as two conv_forward_mfma calls either way.
+hipError_t conv_forward_mfma2(const void* x0, const void* x1, const void* w, const float* b,
+                              void* y0, void* y1, const ConvShape& s, int relu, float* part0,
+                              float* part1, size_t part_cap, hipStream_t st) {
+  const FwdPlan pl = fwd_plan(s);
+  if (pl.cfg >= 400) {
+    g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
+    const hipError_t e = conv_forward_rows32(x0, w, b, y0, s, relu, st, x1, y1);
+    g_rows32_cfg = -1;
+    return e;
+  }
+  hipError_t e = conv_forward_mfma(x0, w, b, y0, s, relu, part0, part_cap, st);
+  if (e != hipSuccess) return e;
+  return conv_forward_mfma(x1, w, b, y1, s, relu, part1, part_cap, st);
+}
+
+// The weight gradients of two micro-batches, both sums left pending: one
+// launch of the row-blocked kernel where it applies, else one each.
+hipError_t conv_wgrad_mfma2(const void* x0, const void* x1, const void* dz0, const void* dz1,
+                            float* dw0, float* dw1, float* part0, float* part1,
+                            const ConvShape& s, hipStream_t st, ReduceJob* defer0,
+                            ReduceJob* defer1) {
+  if (use_wgrad_rows(s))
+    return conv_wgrad_rows_launch2(x0, x1, dz0, dz1, dw0, dw1, part0, part1, s, st, defer0,
+                                   defer1);
+  hipError_t e = conv_wgrad_mfma(x0, dz0, dw0, part0, s, st, nullptr, defer0);
+  if (e != hipSuccess) return e;
+  return conv_wgrad_mfma(x1, dz1, dw1, part1, s, st, nullptr, defer1);
+}
+
 }  // namespace tgpk

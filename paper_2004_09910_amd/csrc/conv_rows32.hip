@@ -61,11 +61,16 @@ struct Rows32Geom {
 // SIMD), the two waves of a SIMD on the two channel halves of the same
 // pixels, so that one wave's MFMAs run while the other waits on its DMA
 // issue or its LDS reads.
+//
+// X2 / Y2 (both null or both set) are a second micro-batch of nb samples
+// with the same weights: its tiles follow the first's (sample index nb ..
+// 2 nb - 1), so one launch covers both and each block streams a tile of
+// each through its ring.
 template <int W, int R, int FW, int NS, int CH>
 __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
-    const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
-    const float* __restrict__ bias, bf16_t* __restrict__ Y, int nb, int H, int Cin,
-    int Cout, int relu) {
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ X2, const bf16_t* __restrict__ Wt,
+    const float* __restrict__ bias, bf16_t* __restrict__ Y, bf16_t* __restrict__ Y2, int nb,
+    int H, int Cin, int Cout, int relu) {
   typedef Rows32Geom<W, R> G_;
   constexpr int BWP = G_::BWP, SB = G_::SB, F = G_::F;
   constexpr int NW = CH == 2 ? 4 : 8;                           // waves
@@ -81,7 +86,8 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
   const int chf = CH == 2 ? 0 : wave >> 2;                      // channel half (CH = 1)
   const int nrb = (H + R - 1) / R;                              // row blocks per sample
   const int nct = Cout / 64;
-  const int items = nb * nrb * nct;
+  const int ng = X2 ? 2 : 1;                                     // micro-batches
+  const int items = ng * nb * nrb * nct;
   const int G = gridDim.x;
   const int lb = xcd_remap(blockIdx.x, G);
   const int n_items = lb < items ? (items - lb + G - 1) / G : 0;
@@ -99,6 +105,7 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
   };
 
   const u32x4 rx = make_rsrc(X, nb * H * W * Cin * 2);
+  const u32x4 rx2 = make_rsrc(X2 ? X2 : X, nb * H * W * Cin * 2);
   const u32x4 rw = make_rsrc(Wt, Cout * 9 * Cin * 2);
 
   // DMA: instruction u of this wave fills stage chunk k = NW u + wave
@@ -164,7 +171,10 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
     const int c0 = i_ks * 16;
     const int soff_a = (i_co0 * 9 * Cin + c0) * 2;
     const int hb = i_h0 - 1;                                    // input row of block row 0
-    const int base_b = ((i_n * H + hb) * W * Cin + c0) * 2;    // negative for hb = -1
+    const bool g1 = i_n >= nb;                                  // second micro-batch (uniform)
+    const int nn = g1 ? i_n - nb : i_n;
+    const u32x4 rxg = g1 ? rx2 : rx;
+    const int base_b = ((nn * H + hb) * W * Cin + c0) * 2;     // negative for hb = -1
     const bool interior = hb >= 0 && hb + R + 2 <= H;
 #pragma unroll
     for (int u = 0; u < LW; ++u) {
@@ -176,7 +186,7 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
         dma16(rw, dst, doff[u], soff_a);
       } else {
         const bool ok = drow[u] >= 0 && (interior || (unsigned)(hb + drow[u]) < (unsigned)H);
-        dma16(rx, dst, ok ? base_b + doff[u] : R32_OOB, 0);
+        dma16(rxg, dst, ok ? base_b + doff[u] : R32_OOB, 0);
       }
     }
   };
@@ -270,7 +280,9 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
     constexpr int ROWB = 64 * CH;                               // staged bytes per pixel
     constexpr int NCK = 4 * CH;                                 // 16-byte chunks per pixel
     unsigned char* ep = smem + ((idx - 1) % NS) * SB + wave * 32 * ROWB;
-    const long pix0 = (long)(n * H + h0) * W;
+    const bool g1 = n >= nb;
+    bf16_t* const Yg = g1 ? Y2 : Y;
+    const long pix0 = (long)((g1 ? n - nb : n) * H + h0) * W;
     const int pw = lane & 31, hw = lane >> 5;
 #pragma unroll
     for (int j = 0; j < FW; ++j) {
@@ -297,7 +309,7 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
         const u32x4 val = *(const u32x4*)(ep + p * ROWB + ((c ^ (p & (NCK - 1))) << 4));
         const int tp = (pg * FW + j) * 32 + p;
         if (pg * FW + j < F && h0 + tp / W < H)
-          *(u32x4*)(Y + (pix0 + tp) * Cout + co0 + 32 * chf + 8 * c) = val;
+          *(u32x4*)(Yg + (pix0 + tp) * Cout + co0 + 32 * chf + 8 * c) = val;
       }
     }
   }
@@ -347,8 +359,9 @@ bool conv_rows32_ok(const ConvShape& s) {
 }
 
 template <int W, int R, int FW, int NS, int CH>
-static hipError_t launch_rows32(const bf16_t* X, const bf16_t* Wt, const float* b, bf16_t* Y,
-                                const ConvShape& s, int relu, hipStream_t st) {
+static hipError_t launch_rows32(const bf16_t* X, const bf16_t* X2, const bf16_t* Wt,
+                                const float* b, bf16_t* Y, bf16_t* Y2, const ConvShape& s,
+                                int relu, hipStream_t st) {
   static const char* name = nullptr;
   static char buf[64];
   if (!name) {
@@ -356,29 +369,34 @@ static hipError_t launch_rows32(const bf16_t* X, const bf16_t* Wt, const float* 
     else snprintf(buf, sizeof buf, "conv3x3_rows32<%d,%d,%d,%d,8w>", W, R, FW, NS);
     name = buf;
   }
-  const long items = (long)s.nb * ((s.H + R - 1) / R) * (s.cout / 64);
+  const int ng = X2 ? 2 : 1;
+  const long items = (long)ng * s.nb * ((s.H + R - 1) / R) * (s.cout / 64);
   const int G = (int)(items < 256 ? items : 256);
   if (G == 0) return hipSuccess;
-  const long P = s.pixels();
+  const long P = (long)ng * s.pixels();
   ProfScope ps(name, 2.0 * P * s.cout * 9 * s.cin,
                2.0 * ((double)P * s.cin + 9.0 * s.cin * s.cout + (double)P * s.cout), st);
   TGP_LAUNCH(ps, (conv3x3_rows32<W, R, FW, NS, CH>), dim3(G), dim3(CH == 2 ? 256 : 512), 0, st, X,
-             Wt, b, Y, s.nb, s.H, s.cin, s.cout, relu);
+             X2, Wt, b, Y, Y2, s.nb, s.H, s.cin, s.cout, relu);
   return hipGetLastError();
 }
 
 hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, void* y,
-                               const ConvShape& s, int relu, hipStream_t st) {
+                               const ConvShape& s, int relu, hipStream_t st, const void* x2,
+                               void* y2) {
   const int c = rows32_pick(s);
-  if (c < 0 || !conv_rows32_ok(s)) return hipErrorInvalidValue;
+  if (c < 0 || !conv_rows32_ok(s) || (x2 == nullptr) != (y2 == nullptr))
+    return hipErrorInvalidValue;
   const bf16_t* X = (const bf16_t*)x;
+  const bf16_t* X2 = (const bf16_t*)x2;
   const bf16_t* Wt = (const bf16_t*)w;
   bf16_t* Y = (bf16_t*)y;
+  bf16_t* Y2 = (bf16_t*)y2;
   switch (c) {
 #define R32_CASE(i)                                                                      \
   case i:                                                                                \
     return launch_rows32<kR32Cfgs[i].W, kR32Cfgs[i].R, kR32Cfgs[i].FW, kR32Cfgs[i].NS,   \
-                         kR32Cfgs[i].CH>(X, Wt, b, Y, s, relu, st);
+                         kR32Cfgs[i].CH>(X, X2, Wt, b, Y, Y2, s, relu, st);
     R32_CASE(0) R32_CASE(1) R32_CASE(2) R32_CASE(3) R32_CASE(4) R32_CASE(5)
     R32_CASE(6) R32_CASE(7) R32_CASE(8) R32_CASE(9) R32_CASE(10) R32_CASE(11)
     R32_CASE(12) R32_CASE(13) R32_CASE(14) R32_CASE(15)

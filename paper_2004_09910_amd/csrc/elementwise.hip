@@ -17,6 +17,13 @@ size_t wgrad_mfma_partial_floats(const ConvShape& s);
 hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
                            const ConvShape& s, hipStream_t st, const ReduceJob* extra,
                            ReduceJob* defer);
+hipError_t conv_forward_mfma2(const void* x0, const void* x1, const void* w, const float* b,
+                              void* y0, void* y1, const ConvShape& s, int relu, float* part0,
+                              float* part1, size_t part_cap, hipStream_t st);
+hipError_t conv_wgrad_mfma2(const void* x0, const void* x1, const void* dz0, const void* dz1,
+                            float* dw0, float* dw1, float* part0, float* part1,
+                            const ConvShape& s, hipStream_t st, ReduceJob* defer0,
+                            ReduceJob* defer1);
 
 namespace {
 
@@ -857,6 +864,43 @@ hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* p
     return hipSuccess;
   }
   return splitk_reduce_launch(partial, dw, E, S, st, extra);
+}
+
+hipError_t conv_forward2(int dt, const void* x0, const void* x1, const void* w, const float* b,
+                         void* y0, void* y1, const ConvShape& s, int relu, float* part0,
+                         float* part1, size_t part_cap, hipStream_t st) {
+  if (mfma_conv_ok(dt, s.cin, s.cout))
+    return conv_forward_mfma2(x0, x1, w, b, y0, y1, s, relu, part0, part1, part_cap, st);
+  hipError_t e = conv_forward(dt, x0, w, b, y0, s, relu, part0, part_cap, st);
+  if (e != hipSuccess) return e;
+  return conv_forward(dt, x1, w, b, y1, s, relu, part1, part_cap, st);
+}
+
+hipError_t conv_dgrad2(int dt, const void* dz0, const void* dz1, const void* w, const void* wt,
+                       void* dx0, void* dx1, const ConvShape& s, float* part0, float* part1,
+                       size_t part_cap, hipStream_t st) {
+  if (conv_dgrad_uses_wt(dt, s)) {
+    ConvShape t{s.nb, s.H, s.W, s.cout, s.cin, s.taps};
+    t_in_dgrad = 1;
+    const hipError_t e = conv_forward_mfma2(dz0, dz1, wt, nullptr, dx0, dx1, t, 0, part0, part1,
+                                            part_cap, st);
+    t_in_dgrad = 0;
+    return e;
+  }
+  hipError_t e = conv_dgrad(dt, dz0, w, wt, dx0, s, part0, part_cap, st);
+  if (e != hipSuccess) return e;
+  return conv_dgrad(dt, dz1, w, wt, dx1, s, part1, part_cap, st);
+}
+
+hipError_t conv_wgrad2(int dt, const void* x0, const void* x1, const void* dz0, const void* dz1,
+                       float* dw0, float* dw1, float* part0, float* part1, const ConvShape& s,
+                       hipStream_t st, ReduceJob* defer0, ReduceJob* defer1) {
+  if (!defer0 || !defer1) return hipErrorInvalidValue;
+  if (mfma_conv_ok(dt, s.cin, s.cout))
+    return conv_wgrad_mfma2(x0, x1, dz0, dz1, dw0, dw1, part0, part1, s, st, defer0, defer1);
+  hipError_t e = conv_wgrad(dt, x0, dz0, dw0, part0, s, st, nullptr, defer0);
+  if (e != hipSuccess) return e;
+  return conv_wgrad(dt, x1, dz1, dw1, part1, s, st, nullptr, defer1);
 }
 
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,

@@ -35,7 +35,8 @@ extern int g_rowtile_cfg;
 // conv_forward_rowtile).
 bool conv_rows32_ok(const ConvShape& s);
 hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, void* y,
-                               const ConvShape& s, int relu, hipStream_t st);
+                               const ConvShape& s, int relu, hipStream_t st,
+                               const void* x2 = nullptr, void* y2 = nullptr);
 extern int g_rows32_cfg;
 extern int g_rows32_ch;
 extern int g_wgrad_ks;
@@ -61,6 +62,10 @@ size_t wgrad_rows_partial_floats(const ConvShape& s);
 hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
                                   const ConvShape& s, hipStream_t st,
                                   const ReduceJob* extra = nullptr, ReduceJob* defer = nullptr);
+hipError_t conv_wgrad_rows_launch2(const void* x0, const void* x1, const void* dz0,
+                                   const void* dz1, float* dw0, float* dw1, float* partial0,
+                                   float* partial1, const ConvShape& s, hipStream_t st,
+                                   ReduceJob* defer0, ReduceJob* defer1);
 
 // Whether the data-gradient kernel for this shape reads the transformed
 // weight wt = [cin][taps][cout] (taps rotated by 180 degrees).
@@ -80,6 +85,20 @@ size_t conv_wgrad_partial_floats(int dt, const ConvShape& s);
 hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial,
                       const ConvShape& s, hipStream_t st, const ReduceJob* extra = nullptr,
                       ReduceJob* defer = nullptr);
+
+// The same three operations for two micro-batches of one layer (the same
+// weights, separate tensors): one launch where the chosen kernel takes two
+// tensors, else one launch each, with the same values as two single calls.
+// conv_wgrad2 always leaves both sums pending.
+hipError_t conv_forward2(int dt, const void* x0, const void* x1, const void* w, const float* b,
+                         void* y0, void* y1, const ConvShape& s, int relu, float* part0,
+                         float* part1, size_t part_cap, hipStream_t st);
+hipError_t conv_dgrad2(int dt, const void* dz0, const void* dz1, const void* w, const void* wt,
+                       void* dx0, void* dx1, const ConvShape& s, float* part0, float* part1,
+                       size_t part_cap, hipStream_t st);
+hipError_t conv_wgrad2(int dt, const void* x0, const void* x1, const void* dz0, const void* dz1,
+                       float* dw0, float* dw1, float* part0, float* part1, const ConvShape& s,
+                       hipStream_t st, ReduceJob* defer0, ReduceJob* defer1);
 
 // Depthwise 3x3 (pad 1), w = [c][9].
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,

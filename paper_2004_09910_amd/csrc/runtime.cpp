@@ -220,56 +220,80 @@ size_t stash_off(const tgp_net* N, int i, int sid, bool grad) {
   return m.at(sid) + (size_t)(i - 1) * N->stash_stride;
 }
 
-// Forward over partition j for micro-batch i.  phase: 0 = checkpointed
-// forward, 1 = storing forward, 2 = recompute.
-tgp_status run_forward(tgp_net* N, int j, int i, int phase, const void* x_in, void* y_out,
-                       hipStream_t st) {
+// Forward over partition j for a group of cnt (1 or 2) micro-batches
+// iv[k], layer by layer; phase[k]: 0 = checkpointed forward, 1 = storing
+// forward, 2 = recompute.  A group of two runs each convolution as one
+// launch where the kernel takes two tensors (same values as one at a time).
+tgp_status run_forward_g(tgp_net* N, int j, int cnt, const int* iv, const int* phase,
+                         const void* const* x_in, void* const* y_out, hipStream_t st) {
   const int lo = N->lo[j - 1], hi = N->hi[j - 1];
-  int set = (phase == 1) ? (N->mode == TGP_CKPT_NEVER ? i - 1 : 0) : -1;
-  const void* src = x_in;
+  int set[2];
+  const void* src[2];
+  for (int k = 0; k < cnt; ++k) {
+    set[k] = (phase[k] == 1) ? (N->mode == TGP_CKPT_NEVER ? iv[k] - 1 : 0) : -1;
+    src[k] = x_in[k];
+  }
   for (int l = lo; l < hi; ++l) {
     LayerRt& Lr = N->L[l];
     const tgp_layer& d = Lr.d;
-    void* out;
-    if (phase == 2) out = T_(N, i, Lr.o_scr_out);
-    else if (l == hi - 1) out = y_out;
-    else if (d.stash_id >= 0) out = W_(N, stash_off(N, i, d.stash_id, false));
-    else if (phase == 1) out = W_(N, Lr.o_sto_out[set]);
-    else out = T_(N, i, Lr.o_scr_out);
-    const void* cin_ptr = src;
-    if (d.prologue != TGP_PRO_NONE) {
-      void* pro = (phase == 1) ? W_(N, Lr.o_sto_pro[set]) : T_(N, i, Lr.o_scr_pro);
-      if (d.prologue == TGP_PRO_MAXPOOL2) {
-        HIPCHK(tgpk::maxpool_forward(N->dt, src, pro, N->b, Lr.inH, Lr.inW, Lr.inC, st),
-               "maxpool_forward");
-      } else {
-        const LayerRt& sl = N->L[N->stash_layer.at(d.pop_id)];
-        HIPCHK(tgpk::upcat_forward(N->dt, src, W_(N, stash_off(N, i, d.pop_id, false)), pro,
-                                   N->b, Lr.H, Lr.W, Lr.inC, sl.d.cout, st),
-               "upcat_forward");
+    void* out[2];
+    const void* cin_ptr[2];
+    for (int k = 0; k < cnt; ++k) {
+      const int i = iv[k];
+      if (phase[k] == 2) out[k] = T_(N, i, Lr.o_scr_out);
+      else if (l == hi - 1) out[k] = y_out[k];
+      else if (d.stash_id >= 0) out[k] = W_(N, stash_off(N, i, d.stash_id, false));
+      else if (phase[k] == 1) out[k] = W_(N, Lr.o_sto_out[set[k]]);
+      else out[k] = T_(N, i, Lr.o_scr_out);
+      cin_ptr[k] = src[k];
+      if (d.prologue != TGP_PRO_NONE) {
+        void* pro = (phase[k] == 1) ? W_(N, Lr.o_sto_pro[set[k]]) : T_(N, i, Lr.o_scr_pro);
+        if (d.prologue == TGP_PRO_MAXPOOL2) {
+          HIPCHK(tgpk::maxpool_forward(N->dt, src[k], pro, N->b, Lr.inH, Lr.inW, Lr.inC, st),
+                 "maxpool_forward");
+        } else {
+          const LayerRt& sl = N->L[N->stash_layer.at(d.pop_id)];
+          HIPCHK(tgpk::upcat_forward(N->dt, src[k], W_(N, stash_off(N, i, d.pop_id, false)), pro,
+                                     N->b, Lr.H, Lr.W, Lr.inC, sl.d.cout, st),
+                 "upcat_forward");
+        }
+        cin_ptr[k] = pro;
       }
-      cin_ptr = pro;
     }
     if (d.kind == TGP_DWCONV3X3) {
-      HIPCHK(tgpk::dw_forward(N->dt, cin_ptr, Lr.w, d.bias ? Lr.b : nullptr, out, N->b, Lr.H,
-                              Lr.W, d.cout, d.relu, st),
-             "dw_forward");
+      for (int k = 0; k < cnt; ++k)
+        HIPCHK(tgpk::dw_forward(N->dt, cin_ptr[k], Lr.w, d.bias ? Lr.b : nullptr, out[k], N->b,
+                                Lr.H, Lr.W, d.cout, d.relu, st),
+               "dw_forward");
     } else {
       tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
-      HIPCHK(tgpk::conv_forward(N->dt, cin_ptr, Lr.w, d.bias ? Lr.b : nullptr, out, s, d.relu,
-                                (float*)T_(N, i, N->o_fpart), N->fpart_floats, st),
-             "conv_forward");
+      if (cnt == 2)
+        HIPCHK(tgpk::conv_forward2(N->dt, cin_ptr[0], cin_ptr[1], Lr.w, d.bias ? Lr.b : nullptr,
+                                   out[0], out[1], s, d.relu, (float*)T_(N, iv[0], N->o_fpart),
+                                   (float*)T_(N, iv[1], N->o_fpart), N->fpart_floats, st),
+               "conv_forward2");
+      else
+        HIPCHK(tgpk::conv_forward(N->dt, cin_ptr[0], Lr.w, d.bias ? Lr.b : nullptr, out[0], s,
+                                  d.relu, (float*)T_(N, iv[0], N->o_fpart), N->fpart_floats, st),
+               "conv_forward");
     }
-    // a stashed layer that ends the partition wrote the partition output;
-    // its consumer reads the stash slot (a recompute leaves the slot as the
-    // forward wrote it, bit for bit)
-    if (phase != 2 && l == hi - 1 && d.stash_id >= 0)
-      HIPCHK(hipMemcpyAsync(W_(N, stash_off(N, i, d.stash_id, false)), out, Lr.out_bytes,
-                            hipMemcpyDeviceToDevice, st),
-             "stash copy");
-    src = out;
+    for (int k = 0; k < cnt; ++k) {
+      // a stashed layer that ends the partition wrote the partition output;
+      // its consumer reads the stash slot (a recompute leaves the slot as
+      // the forward wrote it, bit for bit)
+      if (phase[k] != 2 && l == hi - 1 && d.stash_id >= 0)
+        HIPCHK(hipMemcpyAsync(W_(N, stash_off(N, iv[k], d.stash_id, false)), out[k], Lr.out_bytes,
+                              hipMemcpyDeviceToDevice, st),
+               "stash copy");
+      src[k] = out[k];
+    }
   }
   return TGP_OK;
+}
+
+tgp_status run_forward(tgp_net* N, int j, int i, int phase, const void* x_in, void* y_out,
+                       hipStream_t st) {
+  return run_forward_g(N, j, 1, &i, &phase, &x_in, &y_out, st);
 }
 
 // Pointers the backward of (i, j) reads: layer outputs and prologue outputs.
@@ -294,121 +318,195 @@ void activation_view(tgp_net* N, int j, int i, bool ckpt, ActView& v) {
   }
 }
 
-tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_in,
-                        hipStream_t st) {
-  const int lo = N->lo[j - 1], hi = N->hi[j - 1];
-  bool ckpt = N->saved_ckpt[cell(N, i, j)];
-  if (ckpt) {
-    tgp_status r = run_forward(N, j, i, 2, N->saved_x[cell(N, i, j)], nullptr, st);
-    if (r != TGP_OK) return r;
-  }
-  if (i > N->m - N->lanes) {
-    // first backward of partition j on this lane in this step: refresh the
-    // lane's transformed weights used by the data-gradient kernels
-    for (int l = lo; l < hi; ++l) {
-      LayerRt& Lr = N->L[l];
-      if (Lr.has_wt)
-        HIPCHK(tgpk::weight_transform(N->dt, Lr.w, T_(N, i, Lr.o_wt), Lr.d.cout, Lr.d.cin, Lr.taps,
-                                      st),
-               "weight_transform");
-    }
-  }
+// Per-micro-batch state of a backward pass.
+struct BwdMb {
+  int i = 0;
   ActView v;
-  activation_view(N, j, i, ckpt, v);
-  void* gcur = T_(N, i, N->o_g0);
-  void* gnext = T_(N, i, N->o_g1);
-  void* dz = T_(N, i, N->o_dz);
-  void* dinp = T_(N, i, N->o_dinp);
-  float* part = (float*)T_(N, i, N->o_part);          // weight partials reduced at once
-  float* colpart = (float*)T_(N, i, N->o_colpart);    // bias partials reduced at once
-  const void* dy = dy_out;
+  void *gcur = nullptr, *gnext = nullptr, *dz = nullptr, *dinp = nullptr;
+  float *part = nullptr, *colpart = nullptr;
+  const void* dy = nullptr;
   // the pool gradient of layer l + 1's max-pool prologue, when its backward
   // is left to layer l's ReLU backward (dy then names the buffer it would
   // have filled)
   const void* dy_pool = nullptr;
+};
+
+// F' (where checkpointed) and B for a group of cnt (1 or 2) micro-batches
+// iv[k] of partition j, layer by layer; a group of two runs the weight and
+// data gradients of each convolution as one launch where the kernel takes
+// two tensors (same values as one at a time).  dx_in[k] are all null or all
+// set.
+tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
+                          const void* const* dy_out, void* const* dx_in, hipStream_t st) {
+  const int lo = N->lo[j - 1], hi = N->hi[j - 1];
+  {
+    int rc[2], ph[2] = {2, 2}, rcn = 0;
+    const void* rx[2];
+    void* ry[2] = {nullptr, nullptr};
+    for (int k = 0; k < cnt; ++k)
+      if (N->saved_ckpt[cell(N, iv[k], j)]) {
+        rc[rcn] = iv[k];
+        rx[rcn] = N->saved_x[cell(N, iv[k], j)];
+        ++rcn;
+      }
+    if (rcn) {
+      tgp_status r = run_forward_g(N, j, rcn, rc, ph, rx, ry, st);
+      if (r != TGP_OK) return r;
+    }
+  }
+  BwdMb M[2];
+  for (int k = 0; k < cnt; ++k) {
+    const int i = iv[k];
+    if (i > N->m - N->lanes) {
+      // first backward of partition j on this lane in this step: refresh the
+      // lane's transformed weights used by the data-gradient kernels
+      for (int l = lo; l < hi; ++l) {
+        LayerRt& Lr = N->L[l];
+        if (Lr.has_wt)
+          HIPCHK(tgpk::weight_transform(N->dt, Lr.w, T_(N, i, Lr.o_wt), Lr.d.cout, Lr.d.cin,
+                                        Lr.taps, st),
+                 "weight_transform");
+      }
+    }
+    BwdMb& B = M[k];
+    B.i = i;
+    activation_view(N, j, i, N->saved_ckpt[cell(N, i, j)], B.v);
+    B.gcur = T_(N, i, N->o_g0);
+    B.gnext = T_(N, i, N->o_g1);
+    B.dz = T_(N, i, N->o_dz);
+    B.dinp = T_(N, i, N->o_dinp);
+    B.part = (float*)T_(N, i, N->o_part);          // weight partials reduced at once
+    B.colpart = (float*)T_(N, i, N->o_colpart);    // bias partials reduced at once
+    B.dy = dy_out[k];
+  }
   for (int l = hi - 1; l >= lo; --l) {
     LayerRt& Lr = N->L[l];
     const tgp_layer& d = Lr.d;
-    const void* y = v.out[l - lo];
-    const void* src = (l == lo) ? v.in0 : v.out[l - 1 - lo];  // pre-prologue input
-    const void* cin_ptr = d.prologue != TGP_PRO_NONE ? v.pro[l - lo] : src;
-    const void* dskip = d.stash_id >= 0 ? W_(N, stash_off(N, i, d.stash_id, true)) : nullptr;
-    long nout = out_elems_mb(N, Lr);
-    long P = (long)N->b * Lr.H * Lr.W;
-    // both gradients stay partial sums in the slot, reduced by the
-    // accumulation (the bias's column sums only where relu_backward_bias
-    // computes them; bias_grad reduces its own)
-    std::array<tgpk::ReduceJob, 2>& pj = N->pend[(size_t)(i - 1) * N->L.size() + l];
-    float* gb = d.bias ? (float*)G_(N, i, Lr.o_gb) : nullptr;
-    pj[1] = tgpk::ReduceJob{gb, gb, d.bias ? (long)d.cout : 0, 0};   // S = 0: not yet run
-    // column partials: kept in the slot, or (too large to keep) reduced at once
-    float* bpart = Lr.defer_b ? (float*)G_(N, i, Lr.o_gcol) : colpart;
-    tgpk::ReduceJob* bdefer = Lr.defer_b ? &pj[1] : nullptr;
-    if (dy_pool && d.bias && Lr.o_gcol_floats &&
-        tgpk::pool_relu_bias_fusable(N->dt, d.cout, Lr.H, Lr.W, dy_pool, dskip, y, dz)) {
-      HIPCHK(tgpk::pool_relu_backward_bias(N->dt, dy_pool, dskip, y, dz, d.relu, gb, bpart,
-                                           N->b, Lr.H, Lr.W, d.cout, st, bdefer),
-             "pool_relu_backward_bias");
-      if (!bdefer) pj[1].S = 1;
-      dy_pool = nullptr;
-    } else if (dy_pool) {
-      HIPCHK(tgpk::maxpool_backward(N->dt, y, dy_pool, (void*)dy, N->b, Lr.H, Lr.W, d.cout, st),
-             "maxpool_backward");
-      dy_pool = nullptr;
+    const void* src[2];
+    const void* cin_ptr[2];
+    std::array<tgpk::ReduceJob, 2>* pjs[2];
+    for (int k = 0; k < cnt; ++k) {
+      BwdMb& B = M[k];
+      const int i = B.i;
+      const void* y = B.v.out[l - lo];
+      src[k] = (l == lo) ? B.v.in0 : B.v.out[l - 1 - lo];  // pre-prologue input
+      cin_ptr[k] = d.prologue != TGP_PRO_NONE ? B.v.pro[l - lo] : src[k];
+      const void* dskip = d.stash_id >= 0 ? W_(N, stash_off(N, i, d.stash_id, true)) : nullptr;
+      long nout = out_elems_mb(N, Lr);
+      long P = (long)N->b * Lr.H * Lr.W;
+      // both gradients stay partial sums in the slot, reduced by the
+      // accumulation (the bias's column sums only where relu_backward_bias
+      // computes them; bias_grad reduces its own)
+      std::array<tgpk::ReduceJob, 2>& pj = N->pend[(size_t)(i - 1) * N->L.size() + l];
+      pjs[k] = &pj;
+      float* gb = d.bias ? (float*)G_(N, i, Lr.o_gb) : nullptr;
+      pj[1] = tgpk::ReduceJob{gb, gb, d.bias ? (long)d.cout : 0, 0};   // S = 0: not yet run
+      // column partials: kept in the slot, or (too large to keep) reduced at once
+      float* bpart = Lr.defer_b ? (float*)G_(N, i, Lr.o_gcol) : B.colpart;
+      tgpk::ReduceJob* bdefer = Lr.defer_b ? &pj[1] : nullptr;
+      if (B.dy_pool && d.bias && Lr.o_gcol_floats &&
+          tgpk::pool_relu_bias_fusable(N->dt, d.cout, Lr.H, Lr.W, B.dy_pool, dskip, y, B.dz)) {
+        HIPCHK(tgpk::pool_relu_backward_bias(N->dt, B.dy_pool, dskip, y, B.dz, d.relu, gb, bpart,
+                                             N->b, Lr.H, Lr.W, d.cout, st, bdefer),
+               "pool_relu_backward_bias");
+        if (!bdefer) pj[1].S = 1;
+        B.dy_pool = nullptr;
+      } else if (B.dy_pool) {
+        HIPCHK(tgpk::maxpool_backward(N->dt, y, B.dy_pool, (void*)B.dy, N->b, Lr.H, Lr.W, d.cout,
+                                      st),
+               "maxpool_backward");
+        B.dy_pool = nullptr;
+      }
+      if (pj[1].S == 0 && d.bias && Lr.o_gcol_floats &&
+          tgpk::relu_bias_fusable(N->dt, d.cout, B.dy, dskip, y, B.dz)) {
+        HIPCHK(tgpk::relu_backward_bias(N->dt, B.dy, dskip, y, B.dz, d.relu, gb, bpart, P, d.cout,
+                                        st, bdefer),
+               "relu_backward_bias");
+        if (!bdefer) pj[1].S = 1;
+      } else if (pj[1].S == 0) {
+        HIPCHK(tgpk::relu_backward(N->dt, B.dy, dskip, y, B.dz, d.relu, nout, st),
+               "relu_backward");
+        if (d.bias)
+          HIPCHK(tgpk::bias_grad(N->dt, B.dz, gb, B.colpart, P, d.cout, st), "bias_grad");
+        pj[1].S = 1;
+      }
+      float* gw = (float*)G_(N, i, Lr.o_gw);
+      pj[0] = tgpk::ReduceJob{gw, gw, Lr.w_elems, 1};
     }
-    if (pj[1].S == 0 && d.bias && Lr.o_gcol_floats &&
-        tgpk::relu_bias_fusable(N->dt, d.cout, dy, dskip, y, dz)) {
-      HIPCHK(tgpk::relu_backward_bias(N->dt, dy, dskip, y, dz, d.relu, gb, bpart, P, d.cout, st,
-                                      bdefer),
-             "relu_backward_bias");
-      if (!bdefer) pj[1].S = 1;
-    } else if (pj[1].S == 0) {
-      HIPCHK(tgpk::relu_backward(N->dt, dy, dskip, y, dz, d.relu, nout, st), "relu_backward");
-      if (d.bias)
-        HIPCHK(tgpk::bias_grad(N->dt, dz, gb, colpart, P, d.cout, st), "bias_grad");
-      pj[1].S = 1;
-    }
-    float* gw = (float*)G_(N, i, Lr.o_gw);
-    pj[0] = tgpk::ReduceJob{gw, gw, Lr.w_elems, 1};
-    if (d.kind == TGP_DWCONV3X3) {
-      HIPCHK(tgpk::dw_wgrad(N->dt, cin_ptr, dz, gw, part, N->b, Lr.H, Lr.W, d.cout, st),
-             "dw_wgrad");
+    // weight gradient
+    tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
+    if (d.kind != TGP_DWCONV3X3 && cnt == 2 && Lr.defer_w) {
+      HIPCHK(tgpk::conv_wgrad2(N->dt, cin_ptr[0], cin_ptr[1], M[0].dz, M[1].dz,
+                               (float*)G_(N, M[0].i, Lr.o_gw), (float*)G_(N, M[1].i, Lr.o_gw),
+                               (float*)G_(N, M[0].i, Lr.o_gpart),
+                               (float*)G_(N, M[1].i, Lr.o_gpart), s, st, &(*pjs[0])[0],
+                               &(*pjs[1])[0]),
+             "conv_wgrad2");
     } else {
-      tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
-      HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr, dz, gw,
-                              Lr.defer_w ? (float*)G_(N, i, Lr.o_gpart) : part, s, st, nullptr,
-                              Lr.defer_w ? &pj[0] : nullptr),
-             "conv_wgrad");
+      for (int k = 0; k < cnt; ++k) {
+        BwdMb& B = M[k];
+        float* gw = (float*)G_(N, B.i, Lr.o_gw);
+        if (d.kind == TGP_DWCONV3X3) {
+          HIPCHK(tgpk::dw_wgrad(N->dt, cin_ptr[k], B.dz, gw, B.part, N->b, Lr.H, Lr.W, d.cout, st),
+                 "dw_wgrad");
+        } else {
+          HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr[k], B.dz, gw,
+                                  Lr.defer_w ? (float*)G_(N, B.i, Lr.o_gpart) : B.part, s, st,
+                                  nullptr, Lr.defer_w ? &(*pjs[k])[0] : nullptr),
+                 "conv_wgrad");
+        }
+      }
     }
-    if (l == lo && dx_in == nullptr) break;
-    void* dest_prev = (l == lo) ? dx_in : gnext;  // gradient of the pre-prologue input
-    void* dgrad_out = d.prologue == TGP_PRO_NONE ? dest_prev : dinp;
+    if (l == lo && dx_in[0] == nullptr) break;
+    // data gradient, into the gradient of the pre-prologue input
+    void* dest_prev[2];
+    void* dgrad_out[2];
+    for (int k = 0; k < cnt; ++k) {
+      dest_prev[k] = (l == lo) ? dx_in[k] : M[k].gnext;
+      dgrad_out[k] = d.prologue == TGP_PRO_NONE ? dest_prev[k] : M[k].dinp;
+    }
     if (d.kind == TGP_DWCONV3X3) {
-      HIPCHK(tgpk::dw_dgrad(N->dt, dz, Lr.w, dgrad_out, N->b, Lr.H, Lr.W, d.cout, st),
-             "dw_dgrad");
+      for (int k = 0; k < cnt; ++k)
+        HIPCHK(tgpk::dw_dgrad(N->dt, M[k].dz, Lr.w, dgrad_out[k], N->b, Lr.H, Lr.W, d.cout, st),
+               "dw_dgrad");
+    } else if (cnt == 2) {
+      // the lanes' transformed weights are equal copies; the first's serves both
+      HIPCHK(tgpk::conv_dgrad2(N->dt, M[0].dz, M[1].dz, Lr.w,
+                               Lr.has_wt ? T_(N, M[0].i, Lr.o_wt) : nullptr, dgrad_out[0],
+                               dgrad_out[1], s, (float*)T_(N, M[0].i, N->o_fpart),
+                               (float*)T_(N, M[1].i, N->o_fpart), N->fpart_floats, st),
+             "conv_dgrad2");
     } else {
-      tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
-      HIPCHK(tgpk::conv_dgrad(N->dt, dz, Lr.w, Lr.has_wt ? T_(N, i, Lr.o_wt) : nullptr, dgrad_out,
-                              s, (float*)T_(N, i, N->o_fpart), N->fpart_floats, st),
+      HIPCHK(tgpk::conv_dgrad(N->dt, M[0].dz, Lr.w, Lr.has_wt ? T_(N, M[0].i, Lr.o_wt) : nullptr,
+                              dgrad_out[0], s, (float*)T_(N, M[0].i, N->o_fpart),
+                              N->fpart_floats, st),
              "conv_dgrad");
     }
-    if (d.prologue == TGP_PRO_MAXPOOL2 && l > lo) {
-      dy_pool = dinp;   // routed by layer l - 1's ReLU backward
-    } else if (d.prologue == TGP_PRO_MAXPOOL2) {
-      HIPCHK(tgpk::maxpool_backward(N->dt, src, dinp, dest_prev, N->b, Lr.inH, Lr.inW, Lr.inC,
-                                    st),
-             "maxpool_backward");
-    } else if (d.prologue == TGP_PRO_UPCAT2) {
-      const LayerRt& sl = N->L[N->stash_layer.at(d.pop_id)];
-      HIPCHK(tgpk::upcat_backward(N->dt, dinp, dest_prev,
-                                  W_(N, stash_off(N, i, d.pop_id, true)), N->b, Lr.H, Lr.W,
-                                  Lr.inC, sl.d.cout, st),
-             "upcat_backward");
+    for (int k = 0; k < cnt; ++k) {
+      BwdMb& B = M[k];
+      if (d.prologue == TGP_PRO_MAXPOOL2 && l > lo) {
+        B.dy_pool = B.dinp;   // routed by layer l - 1's ReLU backward
+      } else if (d.prologue == TGP_PRO_MAXPOOL2) {
+        HIPCHK(tgpk::maxpool_backward(N->dt, src[k], B.dinp, dest_prev[k], N->b, Lr.inH, Lr.inW,
+                                      Lr.inC, st),
+               "maxpool_backward");
+      } else if (d.prologue == TGP_PRO_UPCAT2) {
+        const LayerRt& sl = N->L[N->stash_layer.at(d.pop_id)];
+        HIPCHK(tgpk::upcat_backward(N->dt, B.dinp, dest_prev[k],
+                                    W_(N, stash_off(N, B.i, d.pop_id, true)), N->b, Lr.H, Lr.W,
+                                    Lr.inC, sl.d.cout, st),
+               "upcat_backward");
+      }
+      B.dy = B.gnext;
+      std::swap(B.gcur, B.gnext);
     }
-    dy = gnext;
-    std::swap(gcur, gnext);
   }
   return TGP_OK;
+}
+
+tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_in,
+                        hipStream_t st) {
+  return run_backward_g(N, j, 1, &i, &dy_out, &dx_in, st);
 }
 
 tgp_status run_accumulate(tgp_net* N, int j, int i, int overwrite, hipStream_t st) {
@@ -1055,6 +1153,65 @@ tgp_status tgp_stage_backward_recompute(tgp_net* N, int j, int i, const void* dy
   return TGP_OK;
 }
 
+tgp_status tgp_stage_forward2(tgp_net* N, int j, int i0, int i1, int checkpoint0,
+                              int checkpoint1, const void* x0, const void* x1, void* y0,
+                              void* y1, void* stream) {
+  tgp_status r = check_ready(N, j);
+  if (r != TGP_OK) return r;
+  if (j < 1 || j > N->n) return fail(TGP_EINVAL, "partition %d out of 1..%d", j, N->n);
+  const int iv[2] = {i0, i1};
+  const int ck[2] = {checkpoint0, checkpoint1};
+  for (int k = 0; k < 2; ++k) {
+    if (iv[k] < 1 || iv[k] > N->m) return fail(TGP_EINVAL, "micro-batch %d out of 1..%d", iv[k], N->m);
+    if ((ck[k] != 0) != ckpt_of(N->mode, iv[k], N->m))
+      return fail(TGP_EINVAL, "checkpoint=%d disagrees with the planned policy for i=%d", ck[k], iv[k]);
+    const int c = cell(N, iv[k], j);
+    if (N->st[c] == FWD || N->st[c] == BWD)
+      return fail(TGP_ESTATE, "F_{%d,%d} already ran in this step", iv[k], j);
+  }
+  if (i0 == i1 || (i0 - 1) % N->lanes == (i1 - 1) % N->lanes)
+    return fail(TGP_EINVAL, "micro-batches %d and %d share a lane (lanes = %d)", i0, i1, N->lanes);
+  if (!x0 || !x1 || !y0 || !y1) return fail(TGP_EINVAL, "NULL x_in or y_out");
+  const int ph[2] = {checkpoint0 ? 0 : 1, checkpoint1 ? 0 : 1};
+  const void* xs[2] = {x0, x1};
+  void* ys[2] = {y0, y1};
+  r = run_forward_g(N, j, 2, iv, ph, xs, ys, S(stream));
+  if (r != TGP_OK) return r;
+  for (int k = 0; k < 2; ++k) {
+    const int c = cell(N, iv[k], j);
+    N->st[c] = FWD;
+    N->saved_x[c] = xs[k];
+    N->saved_y[c] = ys[k];
+    N->saved_ckpt[c] = ck[k] ? 1 : 0;
+  }
+  return TGP_OK;
+}
+
+tgp_status tgp_stage_backward_recompute2(tgp_net* N, int j, int i0, int i1, const void* dy0,
+                                         const void* dy1, void* dx0, void* dx1, void* stream) {
+  tgp_status r = check_ready(N, j);
+  if (r != TGP_OK) return r;
+  if (j < 1 || j > N->n) return fail(TGP_EINVAL, "partition %d out of 1..%d", j, N->n);
+  if (i0 < 2 || i0 > N->m || i1 != i0 - 1)
+    return fail(TGP_EINVAL, "need i1 = i0 - 1 within 1..%d (got %d, %d)", N->m, i0, i1);
+  if (N->gslots < N->m || (i0 - 1) % N->lanes == (i1 - 1) % N->lanes)
+    return fail(TGP_EINVAL, "two backwards at once need two or more lanes");
+  if (!dy0 || !dy1) return fail(TGP_EINVAL, "NULL dy_out");
+  if ((dx0 == nullptr) != (dx1 == nullptr)) return fail(TGP_EINVAL, "dx_in: both or neither");
+  for (int i : {i0, i1})
+    if (N->st[cell(N, i, j)] != FWD) return fail(TGP_ESTATE, "B_{%d,%d} needs F_{%d,%d} first", i, j, i, j);
+  if (i0 < N->m && N->st[cell(N, i0 + 1, j)] != ACC)
+    return fail(TGP_ESTATE, "B_{%d,%d} must follow B_{%d,%d} and its accumulation", i0, j, i0 + 1, j);
+  const int iv[2] = {i0, i1};
+  const void* dys[2] = {dy0, dy1};
+  void* dxs[2] = {dx0, dx1};
+  r = run_backward_g(N, j, 2, iv, dys, dxs, S(stream));
+  if (r != TGP_OK) return r;
+  N->st[cell(N, i0, j)] = BWD;
+  N->st[cell(N, i1, j)] = BWD;
+  return TGP_OK;
+}
+
 tgp_status tgp_grad_accumulate(tgp_net* N, int j, int i, int overwrite, void* stream) {
   tgp_status r = check_ready(N, j);
   if (r != TGP_OK) return r;
@@ -1064,6 +1221,8 @@ tgp_status tgp_grad_accumulate(tgp_net* N, int j, int i, int overwrite, void* st
     return fail(TGP_EINVAL, "overwrite must be 1 exactly for i = m");
   int c = cell(N, i, j);
   if (N->st[c] != BWD) return fail(TGP_ESTATE, "accumulate (%d,%d) needs B_{%d,%d} first", i, j, i, j);
+  if (i < N->m && N->st[cell(N, i + 1, j)] != ACC)
+    return fail(TGP_ESTATE, "accumulate (%d,%d) must follow accumulate (%d,%d)", i, j, i + 1, j);
   r = run_accumulate(N, j, i, overwrite, S(stream));
   if (r != TGP_OK) return r;
   N->st[c] = ACC;

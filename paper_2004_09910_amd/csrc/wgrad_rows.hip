@@ -63,14 +63,19 @@ __device__ __forceinline__ void lds_handoff_barrier() {
   asm volatile("" ::: "memory");
 }
 
+// X2 / dZ2 / out2 (all null or all set) are a second micro-batch: its K
+// ranges follow the first's (sample index nb .. 2 nb - 1) and its slices go
+// to out2, so one launch covers both.
+//
 // KS is the number of waves per SIMD: with KS = 2 the two waves of a SIMD
 // own the same 32 x 32 quarter and take alternate k steps, and the second's
 // sums are added to the first's through LDS before the store, so one wave's
 // MFMAs run while the other waits on its DMA issue or LDS reads.
 template <int W, int RPS, int NS, int KS>
 __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
-    const bf16_t* __restrict__ X, const bf16_t* __restrict__ dZ, float* __restrict__ out,
-    int nb, int H, int Cin, int Cout, int R) {
+    const bf16_t* __restrict__ X, const bf16_t* __restrict__ X2, const bf16_t* __restrict__ dZ,
+    const bf16_t* __restrict__ dZ2, float* __restrict__ out, float* __restrict__ out2, int nb,
+    int H, int Cin, int Cout, int R) {
   constexpr int AR = round32(RPS * W);          // dZ rows per stage
   constexpr int BW = W + 4;                     // LDS rows per padded input row
   constexpr int BR = round32(RPS * BW);         // padded X rows per stage
@@ -92,7 +97,8 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
   const int nct = Cout / 64, ncit = Cin / 64;
   const int nrb = (H + R - 1) / R;
   const int per_k = 3 * nct * ncit;             // items per K range
-  const int items = nb * nrb * per_k;
+  const int ng = X2 ? 2 : 1;                    // micro-batches
+  const int items = ng * nb * nrb * per_k;
   const int G = gridDim.x;
   const int lb = xcd_remap(blockIdx.x, G);
   const int n_items = lb < items ? (items - lb + G - 1) / G : 0;
@@ -100,6 +106,8 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
 
   const u32x4 rz = make_rsrc(dZ, nb * H * W * Cout * 2);
   const u32x4 rx = make_rsrc(X, nb * H * W * Cin * 2);
+  const u32x4 rz2 = make_rsrc(X2 ? dZ2 : dZ, nb * H * W * Cout * 2);
+  const u32x4 rx2 = make_rsrc(X2 ? X2 : X, nb * H * W * Cin * 2);
 
   // DMA lane constants: instruction u of this wave fills chunk c = NW u +
   // wave of the A (dZ) or B (padded X) region, rows 8 c + lane / 8, physical
@@ -181,7 +189,10 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
     i_ns = stages_of(i_kr);
   }
   auto issue = [&](int slot) __attribute__((always_inline)) {
-    const int n = i_kr / nrb, rb = i_kr - n * nrb;
+    const int ns_ = i_kr / nrb, rb = i_kr - ns_ * nrb;
+    const bool g1 = ns_ >= nb;                               // second micro-batch (uniform)
+    const int n = g1 ? ns_ - nb : ns_;
+    const u32x4 rzg = g1 ? rz2 : rz, rxg = g1 ? rx2 : rx;
     const int h = rb * R + i_st * RPS;                       // first image row of the stage
     const int zsoff = (((n * H + h) * W) * Cout + i_co0) * 2;
     const int hb = h + i_r - 1;                              // input row of stage row 0
@@ -192,7 +203,7 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
       if (AC % NW != 0 && c >= AC) continue;                 // wave-uniform
       auto* dst = TGP_LDS(smem + slot * SB + c * 1024);
       const bool ok = arow[u] >= 0 && h + arow[u] < H;
-      dma16(rz, dst, ok ? aoff[u] + zsoff : WG_OOB, 0);
+      dma16(rzg, dst, ok ? aoff[u] + zsoff : WG_OOB, 0);
     }
 #pragma unroll
     for (int u = 0; u < LB; ++u) {
@@ -202,7 +213,7 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
       const bool ok = brow[u] >= 0 && (unsigned)(hb + brow[u]) < (unsigned)H && h + brow[u] < H;
       // the row offset can be negative for filter row 0 (rows above are out
       // of range there), so it goes into the per-lane offset
-      dma16(rx, dst, ok ? boff[u] + xsoff : WG_OOB, 0);
+      dma16(rxg, dst, ok ? boff[u] + xsoff : WG_OOB, 0);
     }
     if (++i_st == i_ns) {
       i_st = 0;
@@ -297,7 +308,8 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
     // epilogue: element v of lane l is co 8 (v / 4) + 4 (l / 32) + v % 4, ci
     // l % 32 of this wave's quarter; with KS = 2 wave kh stores v = 8 kh ..
     // 8 kh + 7
-    float* o = out + (long)kr * E;
+    const bool g1 = kr >= nb * nrb;
+    float* o = (g1 ? out2 : out) + (long)(g1 ? kr - nb * nrb : kr) * E;
     const int ci = ci0 + nw * 32 + (lane & 31);
     auto store = [&](int v0, int v1) __attribute__((always_inline)) {
 #pragma unroll
@@ -343,31 +355,34 @@ size_t wgrad_rows_partial_floats(const ConvShape& s) {
 }
 
 template <int W, int RPS, int NS, int KS>
-static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* DZ, float* out,
+static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* X2, const bf16_t* DZ,
+                                    const bf16_t* DZ2, float* out, float* out2,
                                     const ConvShape& s, const WgPlan& p, hipStream_t st) {
-  const long items = (long)p.nK * 3 * (s.cout / 64) * (s.cin / 64);
+  const int ng = X2 ? 2 : 1;
+  const long items = (long)ng * p.nK * 3 * (s.cout / 64) * (s.cin / 64);
   const int G = (int)(items < 256 ? items : 256);
-  const double flops = 2.0 * s.pixels() * s.cout * 9 * s.cin;
-  const double bytes = 2.0 * s.pixels() * (s.cin + s.cout) + 4.0 * p.nK * s.cout * 9 * s.cin;
+  const double flops = 2.0 * ng * s.pixels() * s.cout * 9 * s.cin;
+  const double bytes = ng * (2.0 * s.pixels() * (s.cin + s.cout) + 4.0 * p.nK * s.cout * 9 * s.cin);
   static const char* names[2][4] = {
       {"conv_wgrad_rows<192,1,3>", "conv_wgrad_rows<96,2,3>", "conv_wgrad_rows<48,4,3>",
        "conv_wgrad_rows<24,4,5>"},
       {"conv_wgrad_rows<192,1,3,8w>", "conv_wgrad_rows<96,2,3,8w>", "conv_wgrad_rows<48,4,3,8w>",
        "conv_wgrad_rows<24,4,5,8w>"}};
   ProfScope ps(names[KS - 1][W == 192 ? 0 : (W == 96 ? 1 : (W == 48 ? 2 : 3))], flops, bytes, st);
-  TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, NS, KS>), dim3(G), dim3(256 * KS), 0, st, X, DZ, out,
-             s.nb, s.H, s.cin, s.cout, p.R);
+  TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, NS, KS>), dim3(G), dim3(256 * KS), 0, st, X, X2, DZ,
+             DZ2, out, out2, s.nb, s.H, s.cin, s.cout, p.R);
   return hipGetLastError();
 }
 
 template <int W, int RPS, int NS>
-static hipError_t launch_wgrad_rows_ks(const bf16_t* X, const bf16_t* DZ, float* out,
+static hipError_t launch_wgrad_rows_ks(const bf16_t* X, const bf16_t* X2, const bf16_t* DZ,
+                                       const bf16_t* DZ2, float* out, float* out2,
                                        const ConvShape& s, const WgPlan& p, hipStream_t st) {
   // two waves per SIMD pay off where a stage has many k steps (widths 192
   // and 48 measured 1-3 % faster; 96 about even, 24 slower)
   const int ks = g_wgrad_ks ? g_wgrad_ks : ((W == 192 || W == 48) ? 2 : 1);
-  return ks == 2 ? launch_wgrad_rows<W, RPS, NS, 2>(X, DZ, out, s, p, st)
-                 : launch_wgrad_rows<W, RPS, NS, 1>(X, DZ, out, s, p, st);
+  return ks == 2 ? launch_wgrad_rows<W, RPS, NS, 2>(X, X2, DZ, DZ2, out, out2, s, p, st)
+                 : launch_wgrad_rows<W, RPS, NS, 1>(X, X2, DZ, DZ2, out, out2, s, p, st);
 }
 
 hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
@@ -379,10 +394,10 @@ hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, floa
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* DZ = (const bf16_t*)dz;
   hipError_t e;
-  if (s.W == 192) e = launch_wgrad_rows_ks<192, 1, 3>(X, DZ, out, s, p, st);
-  else if (s.W == 96) e = launch_wgrad_rows_ks<96, 2, 3>(X, DZ, out, s, p, st);
-  else if (s.W == 48) e = launch_wgrad_rows_ks<48, 4, 3>(X, DZ, out, s, p, st);
-  else e = launch_wgrad_rows_ks<24, 4, 5>(X, DZ, out, s, p, st);
+  if (s.W == 192) e = launch_wgrad_rows_ks<192, 1, 3>(X, nullptr, DZ, nullptr, out, nullptr, s, p, st);
+  else if (s.W == 96) e = launch_wgrad_rows_ks<96, 2, 3>(X, nullptr, DZ, nullptr, out, nullptr, s, p, st);
+  else if (s.W == 48) e = launch_wgrad_rows_ks<48, 4, 3>(X, nullptr, DZ, nullptr, out, nullptr, s, p, st);
+  else e = launch_wgrad_rows_ks<24, 4, 5>(X, nullptr, DZ, nullptr, out, nullptr, s, p, st);
   if (e != hipSuccess) return e;
   if (defer) {
     *defer = ReduceJob{out, dw, (long)s.cout * 9 * s.cin, p.nK};
@@ -391,6 +406,30 @@ hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, floa
   if (p.nK == 1)
     return extra ? splitk_reduce_launch(extra->part, extra->out, extra->E, extra->S, st) : e;
   return splitk_reduce_launch(partial, dw, (long)s.cout * 9 * s.cin, p.nK, st, extra);
+}
+
+// Two micro-batches in one launch, each sum left pending (*defer0, *defer1):
+// the same slices as two conv_wgrad_rows_launch calls with `defer`.
+hipError_t conv_wgrad_rows_launch2(const void* x0, const void* x1, const void* dz0,
+                                   const void* dz1, float* dw0, float* dw1, float* partial0,
+                                   float* partial1, const ConvShape& s, hipStream_t st,
+                                   ReduceJob* defer0, ReduceJob* defer1) {
+  if (!wgrad_rows_ok(s) || !defer0 || !defer1) return hipErrorInvalidValue;
+  const WgPlan p = wgrad_rows_plan(s);
+  float* o0 = p.nK > 1 ? partial0 : dw0;
+  float* o1 = p.nK > 1 ? partial1 : dw1;
+  const bf16_t *X0 = (const bf16_t*)x0, *X1 = (const bf16_t*)x1;
+  const bf16_t *D0 = (const bf16_t*)dz0, *D1 = (const bf16_t*)dz1;
+  hipError_t e;
+  if (s.W == 192) e = launch_wgrad_rows_ks<192, 1, 3>(X0, X1, D0, D1, o0, o1, s, p, st);
+  else if (s.W == 96) e = launch_wgrad_rows_ks<96, 2, 3>(X0, X1, D0, D1, o0, o1, s, p, st);
+  else if (s.W == 48) e = launch_wgrad_rows_ks<48, 4, 3>(X0, X1, D0, D1, o0, o1, s, p, st);
+  else e = launch_wgrad_rows_ks<24, 4, 5>(X0, X1, D0, D1, o0, o1, s, p, st);
+  if (e != hipSuccess) return e;
+  const long E = (long)s.cout * 9 * s.cin;
+  *defer0 = ReduceJob{o0, dw0, E, p.nK};
+  *defer1 = ReduceJob{o1, dw1, E, p.nK};
+  return hipSuccess;
 }
 
 }  // namespace tgpk

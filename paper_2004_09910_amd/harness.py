@@ -78,6 +78,7 @@ class Session:
         self.ws = None
         self.B = self.m = self.b = self.mode = None
         self.lanes = 1
+        self.pairs = False
         self._lane_streams = None
 
     def _bind_layer(self, idx: int, seed_offset: int):
@@ -196,9 +197,11 @@ class Session:
         NHWC; micro-batch slices are pointer offsets.  With several lanes the
         micro-batches run on lane streams forked from torch's current stream
         (`stream` is then unused) unless `serial`, which issues everything on
-        `stream` in order."""
+        `stream` in order (two micro-batches per call with `pairs`)."""
         def sl(t, i):
             return t.data_ptr() + (i - 1) * (t.numel() // self.m) * t.element_size()
+        if self.pairs:
+            return self._stage_step_pairs(j, x, y, dy, dx, sl, stream if serial else None)
         if self.lanes > 1 and not serial:
             return self._stage_step_lanes(j, x, y, dy, dx, sl)
         for i in range(1, self.m + 1):
@@ -235,6 +238,56 @@ class Session:
             self._events.append(ev)
             acc.wait_event(ev)
             tgp.grad_accumulate(self.h, j, i, i == self.m, acc.cuda_stream)
+        for s in self._lane_streams:
+            cur.wait_stream(s)
+
+    def _stage_step_pairs(self, j, x, y, dy, dx, sl, serial_stream=None):
+        """stage_step with two micro-batches per launch: forwards (1, 2),
+        (3, 4), ..., backwards (m, m - 1), (m - 2, m - 3), ..., each pair on
+        one stream per lane pair, and the accumulations, in the order m..1,
+        on one more stream that waits for each pair's backward (all on
+        `serial_stream`, in that order, when given).  Needs an even number of
+        lanes and an even m."""
+        K = min(self.lanes, self.m)
+        if K % 2 or self.m % 2:
+            raise ValueError(f"pairs need even lanes and m (lanes={self.lanes}, m={self.m})")
+        if serial_stream is not None:
+            for i in range(1, self.m + 1, 2):
+                tgp.stage_forward2(self.h, j, i, i + 1, self.checkpointed(i),
+                                   self.checkpointed(i + 1), sl(x, i), sl(x, i + 1), sl(y, i),
+                                   sl(y, i + 1), serial_stream)
+            for i in range(self.m, 0, -2):
+                tgp.stage_backward_recompute2(self.h, j, i, i - 1, sl(dy, i), sl(dy, i - 1),
+                                              None if dx is None else sl(dx, i),
+                                              None if dx is None else sl(dx, i - 1), serial_stream)
+                tgp.grad_accumulate(self.h, j, i, i == self.m, serial_stream)
+                tgp.grad_accumulate(self.h, j, i - 1, False, serial_stream)
+            return
+        cur = torch.cuda.current_stream()
+        if self._lane_streams is None:
+            self._lane_streams = [torch.cuda.Stream() for _ in range(K // 2 + 1)]
+        streams, acc = self._lane_streams[:K // 2], self._lane_streams[K // 2]
+        for s in self._lane_streams:
+            s.wait_stream(cur)
+
+        def pair_stream(i0, i1):
+            return streams[min((i0 - 1) % K, (i1 - 1) % K) // 2]
+        for i in range(1, self.m + 1, 2):
+            s = pair_stream(i, i + 1)
+            tgp.stage_forward2(self.h, j, i, i + 1, self.checkpointed(i), self.checkpointed(i + 1),
+                               sl(x, i), sl(x, i + 1), sl(y, i), sl(y, i + 1), s.cuda_stream)
+        self._events = []
+        for i in range(self.m, 0, -2):
+            s = pair_stream(i, i - 1)
+            tgp.stage_backward_recompute2(self.h, j, i, i - 1, sl(dy, i), sl(dy, i - 1),
+                                          None if dx is None else sl(dx, i),
+                                          None if dx is None else sl(dx, i - 1), s.cuda_stream)
+            ev = torch.cuda.Event()
+            ev.record(s)
+            self._events.append(ev)
+            acc.wait_event(ev)
+            tgp.grad_accumulate(self.h, j, i, i == self.m, acc.cuda_stream)
+            tgp.grad_accumulate(self.h, j, i - 1, False, acc.cuda_stream)
         for s in self._lane_streams:
             cur.wait_stream(s)
 

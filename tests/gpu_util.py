@@ -66,13 +66,14 @@ def stage_inputs(sess, j, B, dtype):
 
 
 def gpu_stage(net, dtype, B, m, mode, balance, j, want_dx=True, G_override=None, sess=None,
-              neutral=True, neutral_samples=None, stash_in=None, lanes=1):
+              neutral=True, neutral_samples=None, stash_in=None, lanes=1, pairs=False):
     n = len(balance)
     lo = sum(balance[:j - 1])
     hi = lo + balance[j - 1]
     if sess is None:
         sess = Session(net, dtype, n=n, balance=balance, bind_layers=range(lo, hi))
         sess.plan(B, m, mode, lanes)
+        sess.pairs = pairs
     xv, xraw, G = stage_inputs(sess, j, B, dtype)
     if G_override is not None:
         G = G_override

@@ -244,6 +244,36 @@ def test_stage_state_machine_rejects_out_of_order_calls():
     tgp.net_destroy(h)
 
 
+def test_paired_stage_calls_check_lanes_and_order():
+    """tgp_stage_forward2 / tgp_stage_backward_recompute2: the two
+    micro-batches must sit on different lanes, the backward pair must be
+    (i0, i0 - 1) with per-micro-batch gradient slots, and each micro-batch
+    passes the single call's checks (checkpoint policy, NULLs, state)."""
+    h, _ = _bound_net(mode=1, B=8, m=4, n=2)
+    tgp.set_lanes(h, 2)
+    tgp.bind_workspace(h, FAKE, tgp.plan(h, 8, 4, 1))
+    st = lambda name, *a: tgp.call_status(name, h, *a)
+    F = FAKE
+    assert st("tgp_stage_forward2", 1, 1, 1, 1, 1, F, F, F, F, None) == tgp.EINVAL   # same i
+    assert st("tgp_stage_forward2", 1, 1, 3, 1, 1, F, F, F, F, None) == tgp.EINVAL   # same lane
+    assert st("tgp_stage_forward2", 1, 3, 4, 1, 1, F, F, F, F, None) == tgp.EINVAL   # i=4 is not checkpointed
+    assert st("tgp_stage_forward2", 1, 1, 5, 1, 1, F, F, F, F, None) == tgp.EINVAL   # bad i
+    assert st("tgp_stage_forward2", 1, 1, 2, 1, 1, F, None, F, F, None) == tgp.EINVAL
+    assert st("tgp_stage_backward_recompute2", 1, 4, 3, F, F, None, None, None) == tgp.ESTATE
+    assert st("tgp_stage_backward_recompute2", 1, 4, 2, F, F, None, None, None) == tgp.EINVAL
+    assert st("tgp_stage_backward_recompute2", 1, 1, 0, F, F, None, None, None) == tgp.EINVAL
+    assert st("tgp_stage_backward_recompute2", 1, 4, 3, F, None, None, None, None) == tgp.EINVAL
+    assert st("tgp_stage_backward_recompute2", 1, 4, 3, F, F, F, None, None) == tgp.EINVAL
+    assert "both" in tgp.last_error()
+    # one lane: a single gradient slot, so no backward pair
+    tgp.set_lanes(h, 1)
+    tgp.bind_workspace(h, FAKE, tgp.plan(h, 8, 4, 1))
+    assert st("tgp_stage_forward2", 1, 1, 2, 1, 1, F, F, F, F, None) == tgp.EINVAL
+    assert st("tgp_stage_backward_recompute2", 1, 4, 3, F, F, None, None, None) == tgp.EINVAL
+    assert "lanes" in tgp.last_error()
+    tgp.net_destroy(h)
+
+
 def test_unbound_layers_are_rejected():
     net = specs.plain_stack(2, 8, 8, 8)
     h = _net(net, dtype=1)

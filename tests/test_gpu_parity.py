@@ -83,6 +83,41 @@ def test_lanes_are_bit_identical(mode):
             assert torch.equal(r["stash"][sid], runs[0]["stash"][sid])
 
 
+@pytest.mark.parametrize("mode", MODES)
+def test_micro_batch_pairs_are_bit_identical(mode):
+    """Two micro-batches per launch (tgp_stage_forward2 /
+    tgp_stage_backward_recompute2 on two lanes) give the same bits as one
+    micro-batch per launch on one stream, on a stage that holds both
+    nine-tap kernel widths, pooling, an exported skip and a ragged mix of
+    layer shapes."""
+    net = specs.unet(5, 64, 64, 48, "unet5-c64-48")
+    bal = (7, 5, 3, 4)
+    runs = []
+    for k, pairs in ((1, False), (2, True)):
+        say(f"pairs={pairs} mode={mode}")
+        runs.append(gpu_stage(net, BF16, 8, 4, mode, bal, 1, neutral=False, lanes=k, pairs=pairs))
+    same_bits(runs[0], runs[1])
+    assert torch.equal(runs[1]["y"], runs[0]["y"])
+    assert torch.equal(runs[1]["dx"], runs[0]["dx"])
+    for sid in runs[0]["stash"]:
+        assert torch.equal(runs[1]["stash"][sid], runs[0]["stash"][sid])
+
+
+def test_micro_batch_pairs_bench_stage():
+    """The pair path on the benchmark's own stage (U-Net level-0 layers at
+    192 x 192, micro-batch 4), m = 2, against one micro-batch per launch."""
+    net = specs.unet(5, 64, 64, 192, "unet5-c64")
+    bal = (7, 5, 3, 4)
+    runs = []
+    for k, pairs in ((1, False), (2, True)):
+        say(f"bench stage pairs={pairs}")
+        runs.append(gpu_stage(net, BF16, 8, 2, CKPT_EXCEPT_LAST, bal, 1, neutral=False, lanes=k,
+                              pairs=pairs))
+    same_bits(runs[0], runs[1])
+    assert torch.equal(runs[1]["y"], runs[0]["y"])
+    assert torch.equal(runs[1]["dx"], runs[0]["dx"])
+
+
 def test_tiny_fp32_pipeline_all_modes():
     """4-layer conv3x3+bias+ReLU stack, C=16, 8x16x32x32 fp32, m=4, n=2."""
     wl = specs.tiny()
