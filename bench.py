@@ -168,7 +168,11 @@ def summarize_profiles(out_dir, workload):
     f_write = gib_kib / cw[copy_k[0]]
     fb = fetch[top] * 1024 * f_fetch
     wb = write[top] * 1024 * f_write
-    info = {"kernel": top, "workload": workload, "fetch_bytes": fb, "write_bytes": wb,
+    pairs = False
+    for line in open(os.path.join(out_dir, "prof_fetch.log")):
+        if line.startswith("{"):
+            pairs = bool(_json.loads(line)["config"].get("pairs", False))
+    info = {"kernel": top, "workload": workload, "pairs": pairs, "fetch_bytes": fb, "write_bytes": wb,
             "bytes_per_launch": fb + wb, "dispatches": nf.get(top, 0),
             "fetch_scale": f_fetch, "write_scale": f_write, "source_hash": kernel_source_hash(top)}
     tl = [f"# HBM traffic of `{top}`: {workload}", "",
@@ -180,6 +184,7 @@ def summarize_profiles(out_dir, workload):
            f"a 1 GiB device copy reads {cf[copy_k[0]]:.1f} KiB, so the scale is {f_fetch:.4f}.",
            f"- WRITE_SIZE, mean per dispatch: {write[top]:.1f} KiB over {nw.get(top, 0)} dispatches; "
            f"the copy writes {cw[copy_k[0]]:.1f} KiB, scale {f_write:.4f}.",
+           f"- Launches: {'two micro-batches' if pairs else 'one micro-batch'} per launch.",
            f"- HBM bytes per launch: {fb / 1e6:.2f} MB read + {wb / 1e6:.2f} MB written = "
            f"{(fb + wb) / 1e6:.2f} MB.", "",
            "Other kernels of the same runs (mean KiB per dispatch, unscaled):", "",
@@ -193,9 +198,10 @@ def summarize_profiles(out_dir, workload):
     print(_json.dumps(info))
 
 
-def recorded_traffic(kernel, workload):
+def recorded_traffic(kernel, workload, pairs):
     """HBM bytes per launch of `kernel` from a profiles/ summary taken with
-    the current kernel sources, else None."""
+    the current kernel sources and the same micro-batches per launch, else
+    None."""
     import glob
     import json as _json
     try:
@@ -207,7 +213,7 @@ def recorded_traffic(kernel, workload):
             if line.startswith("traffic_json: "):
                 info = _json.loads(line[len("traffic_json: "):])
                 if info.get("kernel") == kernel and info.get("workload") == workload and \
-                        info.get("source_hash") == cur:
+                        info.get("source_hash") == cur and info.get("pairs", False) == pairs:
                     return info["bytes_per_launch"]
     return None
 
@@ -525,8 +531,9 @@ def main():
     ap.add_argument("--mode", default="always", choices=["always", "except_last", "never"])
     ap.add_argument("--lanes", type=int, default=2,
                     help="concurrency lanes: micro-batch i runs on stream (i - 1) %% lanes")
-    ap.add_argument("--pairs", action="store_true",
-                    help="two micro-batches per launch (needs even lanes and m)")
+    ap.add_argument("--no-pairs", dest="pairs", action="store_false",
+                    help="one micro-batch per launch (default: two per launch when lanes and m "
+                         "are even)")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of a HIP graph")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three device-to-device copies of 1 GiB (the reference "
@@ -589,6 +596,7 @@ def main():
     sess = Session(net, BF16, n=wl.n, bind_layers=None)
     lo, hi = sess.bounds[0]
     sess.plan(wl.batch, wl.m, mode, args.lanes)
+    args.pairs = args.pairs and min(args.lanes, wl.m) % 2 == 0 and wl.m % 2 == 0
     sess.pairs = args.pairs
     B, m = wl.batch, wl.m
     _, xraw = synth.input_x(net, B, BF16)
@@ -684,7 +692,7 @@ def main():
         achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
         roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
                 "frac": achieved / (HBM_PEAK / 1e9), "traffic": None}
-    roof["traffic"] = recorded_traffic(dom["name"], wl.name)
+    roof["traffic"] = recorded_traffic(dom["name"], wl.name, args.pairs)
     roof["algorithmic_bytes_per_launch"] = dom["bytes"] / dom["launches"]
     roof["kernel"] = dom["name"]
     roof["launches_per_step"] = dom["launches"] / per_step_div
