@@ -534,6 +534,12 @@ def main():
     ap.add_argument("--no-pairs", dest="pairs", action="store_false",
                     help="one micro-batch per launch (default: two per launch when lanes and m "
                          "are even)")
+    ap.add_argument("--one-stream", dest="one_stream", action="store_true", default=None,
+                    help="issue the whole step on one stream, accumulations included (the "
+                         "default with two micro-batches per launch)")
+    ap.add_argument("--lane-streams", dest="one_stream", action="store_false",
+                    help="issue micro-batches on lane streams and the accumulations on one more "
+                         "stream (the default with one micro-batch per launch)")
     ap.add_argument("--eager", action="store_true", help="time eager launches instead of a HIP graph")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run three device-to-device copies of 1 GiB (the reference "
@@ -598,6 +604,11 @@ def main():
     sess.plan(wl.batch, wl.m, mode, args.lanes)
     args.pairs = args.pairs and min(args.lanes, wl.m) % 2 == 0 and wl.m % 2 == 0
     sess.pairs = args.pairs
+    if args.one_stream is None:
+        # measured: with two micro-batches per launch the accumulations on a
+        # stream of their own slow the persistent convolutions they overlap
+        # more than they gain; with one per launch, two lane streams win
+        args.one_stream = args.pairs
     B, m = wl.batch, wl.m
     _, xraw = synth.input_x(net, B, BF16)
     x = nchw_to_device_nhwc(xraw, BF16)
@@ -618,7 +629,7 @@ def main():
 
     log("warmup", args.warmup)
     for _ in range(args.warmup):
-        sess.stage_step(1, x, y, dy, dx, stream)
+        sess.stage_step(1, x, y, dy, dx, stream, serial=args.one_stream)
     torch.cuda.synchronize()
 
     # One step captured as a HIP graph: the ~600 launches of a step replay
@@ -630,7 +641,8 @@ def main():
         try:
             graph = torch.cuda.CUDAGraph()
             with torch.cuda.graph(graph):
-                sess.stage_step(1, x, y, dy, dx, torch.cuda.current_stream().cuda_stream)
+                sess.stage_step(1, x, y, dy, dx, torch.cuda.current_stream().cuda_stream,
+                                serial=args.one_stream)
             graph.replay()
             torch.cuda.synchronize()
         except Exception as exc:
@@ -647,7 +659,7 @@ def main():
         tgp.profile_enable(True)
         tgp.profile_read()
         for s_ in range(args.steps):
-            sess.stage_step(1, x, y, dy, dx, stream)
+            sess.stage_step(1, x, y, dy, dx, stream, serial=args.one_stream)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     if graph is not None and profiled_graph:
@@ -712,7 +724,7 @@ def main():
                    "layers": hi - lo, "global_batch": B, "micro_batches": m,
                    "checkpoint": args.mode, "input": f"{B}x{net.in_channels}x{net.height}x{net.width}",
                    "dx_in": True, "launch": "hip_graph" if graph is not None else "eager",
-                   "lanes": args.lanes, "pairs": args.pairs},
+                   "lanes": args.lanes, "pairs": args.pairs, "one_stream": args.one_stream},
         "mfma_util_pct": 100.0 * step_flops / (ms_step * 1e-3) / BF16_PEAK,
         "step_tflop": step_flops / 1e12,
         "kernel_busy_ms_per_step": kernel_ms,

@@ -47,8 +47,9 @@ def gpu_network(net, dtype, B, m, n, mode, balance=None, lanes=1):
     return out
 
 
-def oracle_network(net, dtype, B):
-    P = oracle.net_params(net, dtype)
+def oracle_network(net, dtype, B, P=None):
+    if P is None:
+        P = oracle.net_params(net, dtype)
     xv, _ = synth.input_x(net, B, dtype)
     h, w = net.out_hw()
     tv, _ = synth.target_like((B, net.out_channels(), h, w), dtype)

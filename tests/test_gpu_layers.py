@@ -6,7 +6,7 @@ dW, db) is held to the benchmark spec's tolerance directly: 2e-2 max-rel for bf16,
 level-0 and deepest layer shapes at its micro-batch size."""
 import pytest
 
-from gpu_util import (TOL, check_grad, gpu_stage, gpu_stage_with_popped, maxrel,
+from gpu_util import (TOL, check_grad, gpu_stage, gpu_stage_with_popped, maxrel, oracle_stage,
                       oracle_stage_variants, report, say)
 from paper_2004_09910_amd.harness import nhwc_to_nchw64
 from workloads import specs
@@ -20,14 +20,21 @@ def one_layer(L, h, w, name="one"):
     return Net(name, (L,), L.cin, h, w)
 
 
-def run_and_check(net, bal, j, dtype, B, m, what, popped=False):
+def run_and_check(net, bal, j, dtype, B, m, what, popped=False, variants=True):
+    """variants=False skips the float32-contraction oracle runs, which only
+    report a spread here (every check below is strict)."""
     say(what)
     if popped:
         got = gpu_stage_with_popped(net, bal, j, dtype=dtype, B=B, m=m)
     else:
         got = gpu_stage(net, dtype, B, m, 0, bal, j)
-    ref, alts = oracle_stage_variants(net, dtype, got["lo"], got["hi"], got["xv"], got["G"],
-                                 stash_in=got.get("stash_in"))
+    if variants:
+        ref, alts = oracle_stage_variants(net, dtype, got["lo"], got["hi"], got["xv"], got["G"],
+                                          stash_in=got.get("stash_in"))
+    else:
+        ref = oracle_stage(net, dtype, got["lo"], got["hi"], got["xv"], got["G"],
+                           stash_in=got.get("stash_in"))
+        alts = []
     errs = {}
     ok = check_grad("y", nhwc_to_nchw64(got["y"]), ref["y"], [a["y"] for a in alts], dtype, errs, strict=True)
     ok &= check_grad("dx", nhwc_to_nchw64(got["dx"]), ref["dx"], [a["dx"] for a in alts], dtype, errs, strict=True)
@@ -159,3 +166,18 @@ def test_benchmark_layer_shapes(cin, cout, h):
     deepest layer (2304 x 512 x 2304) at the benchmark's micro-batch size 4."""
     net = one_layer(Layer(CONV3X3, cin, cout), h, h)
     run_and_check(net, (1,), 1, BF16, 4, 1, f"bench layer {cin}->{cout} @{h}x{h} b=4")
+
+
+@pytest.mark.parametrize("cin,cout,h,B", [
+    (4096, 4096, 8, 2),     # 6-level U-Net enc5b: 128 x 4096 x 36864 at micro-batch 2
+    (6144, 2048, 16, 2),    # 6-level U-Net dec4a (upsample-concat input): K = 55296
+    (1536, 512, 24, 4),     # 5-level U-Net dec3a: 9216 x 512 x 13824 at micro-batch 4
+    (128, 128, 256, 2),     # 6-level U-Net level 0: 131072 x 128 x 1152 at micro-batch 2
+])
+def test_largest_layers_at_full_shape(cin, cout, h, B):
+    """The layers with the longest K (and the 6-level network's widest image)
+    at their real per-micro-batch shape: forward, data gradient, weight and
+    bias gradient against the float64 oracle."""
+    net = one_layer(Layer(CONV3X3, cin, cout), h, h)
+    run_and_check(net, (1,), 1, BF16, B, 1, f"full-shape layer {cin}->{cout} @{h}x{h} b={B}",
+                  variants=False)

@@ -15,7 +15,9 @@ import pytest
 import torch
 
 from gpu_util import (TOL, check_grad, gpu_network, gpu_stage, gpu_stage_with_popped, maxrel,
-                      oracle_network_variants, oracle_stage_variants, report, say)
+                      oracle_network, oracle_network_variants, oracle_stage_variants, report, say)
+import oracle
+from oracle import ops
 from paper_2004_09910_amd.harness import nhwc_to_nchw64
 from workloads import specs
 from workloads.specs import BF16, CKPT_ALWAYS, CKPT_EXCEPT_LAST, CKPT_NEVER, FP32
@@ -269,6 +271,43 @@ def test_amoeba_cells_stage_except_last():
             check_stage(got, pair, BF16, f"cells m={m} mode={mode}")
         for r in runs[1:]:
             same_bits(runs[0], r)
+
+
+def test_amoeba_cells_pairs_are_bit_identical():
+    """Two micro-batches per launch on the depthwise / pointwise cells (the
+    depthwise kernels run once per micro-batch inside the pair) against one
+    per launch, except-last."""
+    net = specs.amoeba_cells(4, 256, 14, "cells4-c256")
+    runs = []
+    for k, pairs in ((1, False), (2, True)):
+        say(f"cells pairs={pairs}")
+        runs.append(gpu_stage(net, BF16, 8, 4, CKPT_EXCEPT_LAST, (8,), 1, neutral=False, lanes=k,
+                              pairs=pairs))
+    same_bits(runs[0], runs[1])
+    assert torch.equal(runs[1]["y"], runs[0]["y"])
+    assert torch.equal(runs[1]["dx"], runs[0]["dx"])
+
+
+def test_six_level_unet_network():
+    """The 6-level, 128-channel U-Net (128 -> 4096 channels, 503 M
+    parameters) in 8 partitions, B = 2, m = 2, at 32 x 32, so that its
+    deepest level is a 1 x 1 image (a 3 x 3 convolution there sees only its
+    centre tap).  One float32-contraction variant bounds the decision spread
+    (each oracle run of this network takes tens of seconds)."""
+    net = specs.unet(6, 128, 128, 32, "unet6-c128-32")
+    say("unet6 oracle")
+    P = oracle.net_params(net, BF16)
+    ref = oracle_network(net, BF16, 2, P)
+    with ops.contraction("f32"):
+        alt = oracle_network(net, BF16, 2, P)
+    runs = []
+    for mode in (CKPT_ALWAYS, CKPT_NEVER):
+        say(f"unet6 gpu mode={mode}")
+        got = gpu_network(net, BF16, 2, 2, 8, mode)
+        check_network(got, (ref, [alt]), BF16, f"unet6 mode {mode}")
+        got.pop("sess").close()
+        runs.append(got)
+    same_bits(runs[0], runs[1])
 
 
 def test_micro_batch_of_one_sample():
