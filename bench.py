@@ -218,6 +218,126 @@ def recorded_traffic(kernel, workload, pairs):
     return None
 
 
+def roofline_of(dom, per_step_div):
+    """Roofline entry of the dominant kernel from its profiled launches:
+    algorithmic FLOPs (or bytes) per launch over the mean launch time.  A
+    contraction is priced against the bf16 MFMA peak unless its arithmetic
+    intensity is below half the ridge point (2.5 PFLOP/s / 8 TB/s), where it
+    is plainly HBM-bound and priced against HBM; both fractions are listed."""
+    sec = dom["ms"] * 1e-3
+    tflops = dom["flops"] / sec / 1e12
+    gbps = dom["bytes"] / sec / 1e9
+    ridge = BF16_PEAK / HBM_PEAK
+    if dom["flops"] > 0 and dom["flops"] / dom["bytes"] >= 0.5 * ridge:
+        roof = {"bound": "mfma", "achieved": tflops, "peak": BF16_PEAK / 1e12, "unit": "TFLOP/s",
+                "frac": tflops / (BF16_PEAK / 1e12), "traffic": None}
+    else:
+        roof = {"bound": "hbm", "achieved": gbps, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
+                "frac": gbps / (HBM_PEAK / 1e9), "traffic": None}
+    roof["mfma_frac"] = tflops / (BF16_PEAK / 1e12)
+    roof["hbm_frac"] = gbps / (HBM_PEAK / 1e9)
+    roof["algorithmic_bytes_per_launch"] = dom["bytes"] / dom["launches"]
+    roof["algorithmic_flops_per_launch"] = dom["flops"] / dom["launches"]
+    roof["kernel"] = dom["name"]
+    roof["launches_per_step"] = dom["launches"] / per_step_div
+    roof["avg_launch_us"] = 1e3 * dom["ms"] / dom["launches"]
+    return roof
+
+
+def network_bench(args, wl, mode):
+    """A whole network trained by tgp_pipeline_step (MSE loss, Algorithm 1
+    clock order over all partitions), one step captured as a HIP graph and
+    replayed; per-kernel durations from an eager one-lane pass afterwards;
+    per-partition times from the per-layer measurement (tgp_layer_times)."""
+    import torch
+    import paper_2004_09910_amd as tgp
+    from paper_2004_09910_amd.harness import Session, nchw_to_device_nhwc
+    from workloads import specs, synth
+    from workloads.specs import BF16
+    net, B, m = wl.net, wl.batch, wl.m
+    lanes = args.lanes if m > 1 else 1
+    log("setting up", wl.name)
+    sess = Session(net, BF16, n=wl.n)
+    sess.plan(B, m, mode, lanes)
+    _, xraw = synth.input_x(net, B, BF16)
+    oh, ow = net.out_hw()
+    _, traw = synth.target_like((B, net.out_channels(), oh, ow), BF16)
+    x = nchw_to_device_nhwc(xraw, BF16)
+    t = nchw_to_device_nhwc(traw, BF16)
+    del xraw, traw
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    y = torch.empty((B, oh, ow, net.out_channels()), dtype=x.dtype, device="cuda")
+    cur = lambda: torch.cuda.current_stream().cuda_stream
+    log("warmup", args.warmup)
+    for _ in range(max(args.warmup, 1)):
+        sess.pipeline_step(x, t, loss, y, stream=cur())
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        sess.pipeline_step(x, t, loss, y, stream=cur())
+    graph.replay()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        graph.replay()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    del graph
+    log(f"timed {args.steps} steps (graph): {ms_step:.2f} ms/step")
+    # per-kernel durations: one eager step with a single lane
+    sess.plan(B, m, mode, 1)
+    tgp.profile_enable(True)
+    tgp.profile_read()
+    sess.pipeline_step(x, t, loss, y, stream=cur())
+    torch.cuda.synchronize()
+    stats = tgp.profile_read()
+    tgp.profile_enable(False)
+    stats.sort(key=lambda r: -r["ms"])
+    for r in stats[:12]:
+        log(f"  {r['name']:32s} n={r['launches']:6d} {r['ms']:9.3f} ms "
+            f"{(r['flops'] / (r['ms'] * 1e-3) / 1e12) if r['ms'] > 0 else 0:8.1f} TF/s")
+    roof = roofline_of(stats[0], 1)
+    roof["traffic"] = recorded_traffic(stats[0]["name"], wl.name, False)
+    roof["timed"] = "one eager step with one lane, each launch timed"
+    fwd = net.flops_per_sample()
+    r_fac = {specs.CKPT_ALWAYS: 1.0, specs.CKPT_EXCEPT_LAST: (m - 1) / m,
+             specs.CKPT_NEVER: 0.0}[mode]
+    # forward, recompute and weight gradient of every layer; no data
+    # gradient for the first layer (the network input needs none)
+    step_flops = B * (sum(fwd) * (2.0 + r_fac) + sum(fwd[1:]))
+    planned = memory_account(net, B, m, mode)
+    b = B // m
+    log("per-layer times")
+    us = sess.layer_times(b, mode, iters=2)
+    parts = []
+    for lo, hi in sess.bounds:
+        parts.append(m * sum(us[lo:hi]) / 1e3)
+    sess.close()
+    out = {
+        "metric": "pipeline step samples/sec at 1 MI355X (whole network, all partitions in "
+                  "clock order); MFMA util % of bf16 peak",
+        "value": B * 1e3 / ms_step, "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "network": net.name, "partitions": wl.n,
+                   "balance": list(sess.balance), "global_batch": B, "micro_batches": m,
+                   "checkpoint": args.mode,
+                   "input": f"{B}x{net.in_channels}x{net.height}x{net.width}",
+                   "launch": "hip_graph", "lanes": lanes},
+        "mfma_util_pct": 100.0 * step_flops / (ms_step * 1e-3) / BF16_PEAK,
+        "step_tflop": step_flops / 1e12,
+        "planned_memory_gb": planned[3] / 1e9 if planned else None,
+        "partition_ms_per_step": [round(p, 2) for p in parts],
+        "partition_note": "m x the per-layer times of one micro-batch (F, F' and B plus the "
+                          "accumulation, eager launches), summed per partition",
+        "roofline": roof,
+        "cpu_baseline": None,
+        "cpu_baseline_note": "not run: one single-sample float64 oracle pass of this network "
+                             "takes minutes on the host",
+    }
+    print(json.dumps(out), flush=True)
+
+
 def cpu_baseline(wl, lo, hi, samples, dtype):
     """The oracle (float64 CPU, bf16 storage points) on a bounded sample of the
     same workload: `samples` single-sample forward + backward passes of the
@@ -526,9 +646,16 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--cpu-samples", type=int, default=40)
+    ap.add_argument("--cpu-samples", type=int, default=None,
+                    help="single-sample oracle passes for cpu_baseline (default: about 20 s "
+                         "of CPU work for the workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--mode", default="always", choices=["always", "except_last", "never"])
+    ap.add_argument("--workload", default="unet5-stage1of4",
+                    choices=["unet5-stage1of4", "amoeba18-c256-stage", "unet6-c128-network"],
+                    help="unet5-stage1of4 is the headline; the depthwise/pointwise cell stage "
+                         "and the 6-level U-Net network print a line of their own")
+    ap.add_argument("--mode", default=None, choices=["always", "except_last", "never"],
+                    help="checkpoint mode (default: the workload's own)")
     ap.add_argument("--lanes", type=int, default=2,
                     help="concurrency lanes: micro-batch i runs on stream (i - 1) %% lanes")
     ap.add_argument("--no-pairs", dest="pairs", action="store_false",
@@ -595,9 +722,14 @@ def main():
     from workloads import specs, synth
     from workloads.specs import BF16, CKPT_NAMES
 
-    wl = specs.unet_stage()
-    net = wl.net
+    wl = specs.ALL[args.workload]
+    if args.mode is None:
+        args.mode = {v: k for k, v in CKPT_NAMES.items()}[wl.mode]
     mode = CKPT_NAMES[args.mode]
+    if wl.kind != "stage":
+        network_bench(args, wl, mode)
+        return
+    net = wl.net
     log("setting up", wl.name)
     sess = Session(net, BF16, n=wl.n, bind_layers=None)
     lo, hi = sess.bounds[0]
@@ -695,20 +827,8 @@ def main():
             f"{(r['flops'] / (r['ms'] * 1e-3) / 1e12) if r['ms'] > 0 else 0:8.1f} TF/s "
             f"{(r['bytes'] / (r['ms'] * 1e-3) / 1e9) if r['ms'] > 0 else 0:8.1f} GB/s")
     dom = stats[0]
-    per_launch_ms = dom["ms"] / dom["launches"]
-    if dom["flops"] > 0:
-        achieved = dom["flops"] / (dom["ms"] * 1e-3) / 1e12
-        roof = {"bound": "mfma", "achieved": achieved, "peak": BF16_PEAK / 1e12,
-                "unit": "TFLOP/s", "frac": achieved / (BF16_PEAK / 1e12), "traffic": None}
-    else:
-        achieved = dom["bytes"] / (dom["ms"] * 1e-3) / 1e9
-        roof = {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK / 1e9, "unit": "GB/s",
-                "frac": achieved / (HBM_PEAK / 1e9), "traffic": None}
+    roof = roofline_of(dom, per_step_div)
     roof["traffic"] = recorded_traffic(dom["name"], wl.name, args.pairs)
-    roof["algorithmic_bytes_per_launch"] = dom["bytes"] / dom["launches"]
-    roof["kernel"] = dom["name"]
-    roof["launches_per_step"] = dom["launches"] / per_step_div
-    roof["avg_launch_us"] = 1e3 * per_launch_ms
     roof["timed"] = "eager pass of the step on one stream, each launch timed alone" \
         if graph is not None else "the timed eager steps"
     if args.pairs:
@@ -720,7 +840,7 @@ def main():
         "value": samples_s, "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": wl.name, "network": net.name, "partition": f"1 of {wl.n}",
+        "config": {"workload": wl.name, "network": net.name, "partition": f"{wl.stage_j} of {wl.n}",
                    "layers": hi - lo, "global_batch": B, "micro_batches": m,
                    "checkpoint": args.mode, "input": f"{B}x{net.in_channels}x{net.height}x{net.width}",
                    "dx_in": True, "launch": "hip_graph" if graph is not None else "eager",
@@ -732,7 +852,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("cpu baseline")
-        out["cpu_baseline"] = cpu_baseline(wl, lo, hi, args.cpu_samples, BF16)
+        samples = args.cpu_samples or {"unet5-stage1of4": 40}.get(wl.name, 12)
+        out["cpu_baseline"] = cpu_baseline(wl, lo, hi, samples, BF16)
     print(json.dumps(out), flush=True)
 
 

@@ -268,6 +268,176 @@ __global__ __launch_bounds__(256) void dw_dgrad_k(const T* __restrict__ dz, cons
   Elt<T>::st(dx + e, acc);
 }
 
+// Depthwise 3x3 over bf16 NHWC with C % 8 == 0 and C / 8 dividing 256.
+// Thread q of block (chunk, strip) owns column wc = q / CP and channel pack
+// cp = q % CP (CP = C / 8, eight channels per 16-byte pack) and produces the
+// output rows [h0, h0 + RS) of that column: the 3 x 3 window of input packs
+// slides down the rows, three new packs per output row, so each input pack
+// is fetched about (RS + 2) / RS times per column and its horizontal
+// neighbours come from the same block's loads.  The nine filter taps of the
+// thread's eight channels are one contiguous 144-byte run (w is [C][9]).
+// FLIP applies the filter rotated by 180 degrees, which is the data
+// gradient (dx = dz correlated with the flipped filter); the sum runs over
+// the window in row-major order.
+template <int RS, bool FLIP>
+__global__ __launch_bounds__(256) void dw3_rows_k(const bf16_t* __restrict__ x,
+                                                  const bf16_t* __restrict__ w,
+                                                  const float* __restrict__ b,
+                                                  bf16_t* __restrict__ y, int H, int W, int C,
+                                                  int relu) {
+  const int CP = C >> 3;
+  const int q = blockIdx.x * 256 + threadIdx.x;
+  const int wc = q / CP, cp = q - (q / CP) * CP;
+  if (wc >= W) return;
+  const int strips = (H + RS - 1) / RS;
+  const int n = blockIdx.y / strips, h0 = (blockIdx.y - n * strips) * RS;
+  float wt[9][8];
+  {
+    const uint4* wp = (const uint4*)(w + (long)cp * 72);
+#pragma unroll
+    for (int u = 0; u < 9; ++u) {
+      float f[8];
+      Pk<bf16_t>::un(wp[u], f);
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        const int e = u * 8 + v, c = e / 9, t = e - (e / 9) * 9;
+        wt[FLIP ? 8 - t : t][c] = f[v];
+      }
+    }
+  }
+  float bias[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) bias[i] = b ? b[cp * 8 + i] : 0.f;
+  const bf16_t* xn = x + (long)n * H * W * C + cp * 8;
+  auto ld = [&](int hh, int ww) __attribute__((always_inline)) {
+    return ((unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W)
+               ? ld16(xn + ((long)hh * W + ww) * C)
+               : make_uint4(0u, 0u, 0u, 0u);
+  };
+  uint4 win[3][3];
+#pragma unroll
+  for (int s = 0; s < 3; ++s) {
+    win[0][s] = ld(h0 - 1, wc + s - 1);
+    win[1][s] = ld(h0, wc + s - 1);
+  }
+  for (int h = h0; h < h0 + RS && h < H; ++h) {
+#pragma unroll
+    for (int s = 0; s < 3; ++s) win[2][s] = ld(h + 1, wc + s - 1);
+    float acc[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[i] = 0.f;
+#pragma unroll
+    for (int r = 0; r < 3; ++r)
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        float f[8];
+        Pk<bf16_t>::un(win[r][s], f);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc[i] = fmaf(wt[r * 3 + s][i], f[i], acc[i]);
+      }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      acc[i] += bias[i];
+      if (relu) acc[i] = fmaxf(acc[i], 0.f);
+    }
+    st16(y + (long)n * H * W * C + ((long)h * W + wc) * C + cp * 8, Pk<bf16_t>::pk(acc));
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      win[0][s] = win[1][s];
+      win[1][s] = win[2][s];
+    }
+  }
+}
+
+// Depthwise 3x3 weight-gradient partials over bf16 NHWC (same shape rules
+// as dw3_rows_k).  Thread (column, pack) of block (chunk, strip) sums
+// dz[p] * x[p + tap] over the rows [h0, h0 + RS) of its column for its
+// eight channels and nine taps (x through the sliding window); the block
+// then adds its 256 / CP column groups in order in LDS and writes
+// part[blk][c * 9 + t], blk = strip block * chunks + chunk.  The partials
+// are summed in block order afterwards, so the result is deterministic.
+template <int RS>
+__global__ __launch_bounds__(256) void dw3_wgrad_rows_k(const bf16_t* __restrict__ x,
+                                                        const bf16_t* __restrict__ dz,
+                                                        float* __restrict__ part, int H, int W,
+                                                        int C) {
+  __shared__ float red[72][256];
+  const int CP = C >> 3;
+  const int q = blockIdx.x * 256 + threadIdx.x;
+  const int wc = q / CP, cp = q - (q / CP) * CP;
+  const int strips = (H + RS - 1) / RS;
+  const int n = blockIdx.y / strips, h0 = (blockIdx.y - n * strips) * RS;
+  float acc[9][8];
+#pragma unroll
+  for (int t = 0; t < 9; ++t)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[t][i] = 0.f;
+  if (wc < W) {
+    const long base = (long)n * H * W * C + cp * 8;
+    const bf16_t* xn = x + base;
+    auto ld = [&](int hh, int ww) __attribute__((always_inline)) {
+      return ((unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W)
+                 ? ld16(xn + ((long)hh * W + ww) * C)
+                 : make_uint4(0u, 0u, 0u, 0u);
+    };
+    uint4 win[3][3];
+#pragma unroll
+    for (int s = 0; s < 3; ++s) {
+      win[0][s] = ld(h0 - 1, wc + s - 1);
+      win[1][s] = ld(h0, wc + s - 1);
+    }
+    for (int h = h0; h < h0 + RS && h < H; ++h) {
+#pragma unroll
+      for (int s = 0; s < 3; ++s) win[2][s] = ld(h + 1, wc + s - 1);
+      float d[8];
+      Pk<bf16_t>::un(ld16(dz + base + ((long)h * W + wc) * C), d);
+#pragma unroll
+      for (int r = 0; r < 3; ++r)
+#pragma unroll
+        for (int s = 0; s < 3; ++s) {
+          float f[8];
+          Pk<bf16_t>::un(win[r][s], f);
+#pragma unroll
+          for (int i = 0; i < 8; ++i) acc[r * 3 + s][i] = fmaf(d[i], f[i], acc[r * 3 + s][i]);
+        }
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        win[0][s] = win[1][s];
+        win[1][s] = win[2][s];
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < 9; ++t)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) red[t * 8 + i][threadIdx.x] = acc[t][i];
+  __syncthreads();
+  const int E = C * 9, NG = 256 / CP;
+  float* out = part + ((long)blockIdx.y * gridDim.x + blockIdx.x) * E;
+  for (int e = threadIdx.x; e < E; e += 256) {
+    const int c = e / 9, t = e - (e / 9) * 9, pk = c >> 3, i = c & 7;
+    float s = 0.f;
+    for (int g = 0; g < NG; ++g) s += red[t * 8 + i][g * CP + pk];
+    out[e] = s;
+  }
+}
+
+constexpr int kDwRows = 4;       // output rows per thread, forward and data gradient
+constexpr int kDwWgradRows = 8;  // rows per thread of the weight gradient
+
+// The row-window depthwise kernels apply: bf16, whole 16-byte packs, a pack
+// count dividing the block, and 16-byte aligned tensors and weights.
+static bool dw3_rows_ok(int dt, int nb, int H, int C, const void* a, const void* b2,
+                        const void* c2) {
+  auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  return dt == 0 && C > 0 && C % 8 == 0 && 256 % (C / 8) == 0 && al(a) && al(b2) && al(c2) &&
+         (long)nb * cdiv(H, kDwRows) <= 65535;
+}
+
+static int dw3_wgrad_blocks(int nb, int H, int W, int C) {
+  return (int)cdiv((long)W * (C / 8), 256) * nb * (int)cdiv(H, kDwWgradRows);
+}
+
 // ---------------------------------------------------------------- elementwise
 
 template <typename T>
@@ -906,6 +1076,14 @@ hipError_t conv_wgrad2(int dt, const void* x0, const void* x1, const void* dz0, 
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
                       int H, int W, int C, int relu, hipStream_t st) {
   long P = (long)nb * H * W;
+  if (dw3_rows_ok(dt, nb, H, C, x, w, y)) {
+    if (P == 0) return hipSuccess;
+    const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwRows)));
+    ProfScope ps("dw3_rows_fwd", 18.0 * P * C, 4.0 * P * C, st);
+    TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, false>), g, dim3(256), 0, st, (const bf16_t*)x,
+               (const bf16_t*)w, b, (bf16_t*)y, H, W, C, relu);
+    return hipGetLastError();
+  }
   dim3 g(cdiv(P * C, 256));
   ProfScope ps("dw_forward", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
   if (dt == 0)
@@ -920,6 +1098,14 @@ hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void
 hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int H, int W,
                     int C, hipStream_t st) {
   long P = (long)nb * H * W;
+  if (dw3_rows_ok(dt, nb, H, C, dz, w, dx)) {
+    if (P == 0) return hipSuccess;
+    const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwRows)));
+    ProfScope ps("dw3_rows_dgrad", 18.0 * P * C, 4.0 * P * C, st);
+    TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, true>), g, dim3(256), 0, st, (const bf16_t*)dz,
+               (const bf16_t*)w, (const float*)nullptr, (bf16_t*)dx, H, W, C, 0);
+    return hipGetLastError();
+  }
   dim3 g(cdiv(P * C, 256));
   ProfScope ps("dw_dgrad", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
   if (dt == 0)
@@ -933,13 +1119,29 @@ hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int
 
 size_t dw_wgrad_partial_floats(int nb, int H, int W, int C) {
   long P = (long)nb * H * W;
-  return (size_t)direct_wgrad_splits(P) * C * 9;
+  const size_t direct = (size_t)direct_wgrad_splits(P) * C * 9;
+  const size_t rows = (C % 8 == 0 && C > 0 && 256 % (C / 8) == 0)
+                          ? (size_t)dw3_wgrad_blocks(nb, H, W, C) * C * 9
+                          : 0;
+  return direct > rows ? direct : rows;
 }
 
 hipError_t dw_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial, int nb,
                     int H, int W, int C, hipStream_t st) {
   long P = (long)nb * H * W;
   long E = (long)C * 9;
+  if (dw3_rows_ok(dt, nb, H, C, x, dz, partial) && P > 0) {
+    const int S = dw3_wgrad_blocks(nb, H, W, C);
+    const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwWgradRows)));
+    {
+      ProfScope ps("dw3_wgrad_rows", 18.0 * P * C, 4.0 * P * C + 4.0 * S * E, st);
+      TGP_LAUNCH(ps, (dw3_wgrad_rows_k<kDwWgradRows>), g, dim3(256), 0, st, (const bf16_t*)x,
+                 (const bf16_t*)dz, partial, H, W, C);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return splitk_reduce_launch(partial, dw, E, S, st);
+  }
   long pps = direct_wgrad_pps(P);
   int S = direct_wgrad_splits(P);
   dim3 g(cdiv(E, 256), S);

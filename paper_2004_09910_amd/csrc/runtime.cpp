@@ -384,9 +384,11 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     const tgp_layer& d = Lr.d;
     const void* src[2];
     const void* cin_ptr[2];
+    const void* dzk[2];   // the layer's dz: B.dz, or the incoming dy itself
     std::array<tgpk::ReduceJob, 2>* pjs[2];
     for (int k = 0; k < cnt; ++k) {
       BwdMb& B = M[k];
+      dzk[k] = B.dz;
       const int i = B.i;
       const void* y = B.v.out[l - lo];
       src[k] = (l == lo) ? B.v.in0 : B.v.out[l - 1 - lo];  // pre-prologue input
@@ -423,6 +425,11 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
                                         st, bdefer),
                "relu_backward_bias");
         if (!bdefer) pj[1].S = 1;
+      } else if (pj[1].S == 0 && !d.relu && !d.bias && !dskip) {
+        // no ReLU, bias or skip: dz is dy itself, read in place (the
+        // buffer holding dy is not written again before the next layer)
+        dzk[k] = B.dy;
+        pj[1].S = 1;
       } else if (pj[1].S == 0) {
         HIPCHK(tgpk::relu_backward(N->dt, B.dy, dskip, y, B.dz, d.relu, nout, st),
                "relu_backward");
@@ -436,7 +443,7 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     // weight gradient
     tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
     if (d.kind != TGP_DWCONV3X3 && cnt == 2 && Lr.defer_w) {
-      HIPCHK(tgpk::conv_wgrad2(N->dt, cin_ptr[0], cin_ptr[1], M[0].dz, M[1].dz,
+      HIPCHK(tgpk::conv_wgrad2(N->dt, cin_ptr[0], cin_ptr[1], dzk[0], dzk[1],
                                (float*)G_(N, M[0].i, Lr.o_gw), (float*)G_(N, M[1].i, Lr.o_gw),
                                (float*)G_(N, M[0].i, Lr.o_gpart),
                                (float*)G_(N, M[1].i, Lr.o_gpart), s, st, &(*pjs[0])[0],
@@ -447,10 +454,11 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
         BwdMb& B = M[k];
         float* gw = (float*)G_(N, B.i, Lr.o_gw);
         if (d.kind == TGP_DWCONV3X3) {
-          HIPCHK(tgpk::dw_wgrad(N->dt, cin_ptr[k], B.dz, gw, B.part, N->b, Lr.H, Lr.W, d.cout, st),
+          HIPCHK(tgpk::dw_wgrad(N->dt, cin_ptr[k], dzk[k], gw, B.part, N->b, Lr.H, Lr.W, d.cout,
+                                st),
                  "dw_wgrad");
         } else {
-          HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr[k], B.dz, gw,
+          HIPCHK(tgpk::conv_wgrad(N->dt, cin_ptr[k], dzk[k], gw,
                                   Lr.defer_w ? (float*)G_(N, B.i, Lr.o_gpart) : B.part, s, st,
                                   nullptr, Lr.defer_w ? &(*pjs[k])[0] : nullptr),
                  "conv_wgrad");
@@ -467,17 +475,17 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     }
     if (d.kind == TGP_DWCONV3X3) {
       for (int k = 0; k < cnt; ++k)
-        HIPCHK(tgpk::dw_dgrad(N->dt, M[k].dz, Lr.w, dgrad_out[k], N->b, Lr.H, Lr.W, d.cout, st),
+        HIPCHK(tgpk::dw_dgrad(N->dt, dzk[k], Lr.w, dgrad_out[k], N->b, Lr.H, Lr.W, d.cout, st),
                "dw_dgrad");
     } else if (cnt == 2) {
       // the lanes' transformed weights are equal copies; the first's serves both
-      HIPCHK(tgpk::conv_dgrad2(N->dt, M[0].dz, M[1].dz, Lr.w,
+      HIPCHK(tgpk::conv_dgrad2(N->dt, dzk[0], dzk[1], Lr.w,
                                Lr.has_wt ? T_(N, M[0].i, Lr.o_wt) : nullptr, dgrad_out[0],
                                dgrad_out[1], s, (float*)T_(N, M[0].i, N->o_fpart),
                                (float*)T_(N, M[1].i, N->o_fpart), N->fpart_floats, st),
              "conv_dgrad2");
     } else {
-      HIPCHK(tgpk::conv_dgrad(N->dt, M[0].dz, Lr.w, Lr.has_wt ? T_(N, M[0].i, Lr.o_wt) : nullptr,
+      HIPCHK(tgpk::conv_dgrad(N->dt, dzk[0], Lr.w, Lr.has_wt ? T_(N, M[0].i, Lr.o_wt) : nullptr,
                               dgrad_out[0], s, (float*)T_(N, M[0].i, N->o_fpart),
                               N->fpart_floats, st),
              "conv_dgrad");

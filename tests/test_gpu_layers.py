@@ -108,6 +108,16 @@ def test_conv1x1_and_depthwise():
     run_and_check(net, (1,), 1, BF16, 4, 2, "dwconv3x3 256 @14x14")
 
 
+@pytest.mark.parametrize("c,h,w,relu", [(64, 15, 9, True), (16, 7, 33, False), (2048, 5, 5, True),
+                                         (24, 6, 6, True)])
+def test_depthwise_shapes(c, h, w, relu):
+    """Depthwise 3x3 with one to 256 channel packs per pixel, ragged row
+    strips and column chunks; 24 channels (three packs, not a divisor of the
+    block) takes the per-element kernels."""
+    net = one_layer(Layer(DWCONV3X3, c, c, relu=relu, bias=relu), h, w)
+    run_and_check(net, (1,), 1, BF16, 4, 2, f"dwconv3x3 {c} @{h}x{w} relu={relu}")
+
+
 def test_head_without_relu():
     net = one_layer(Layer(CONV1X1, 64, 1, relu=False), 16, 16)
     run_and_check(net, (1,), 1, BF16, 4, 2, "head 1x1 64->1")
