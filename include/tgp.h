@@ -295,9 +295,10 @@ tgp_status tgp_profile_clear(void);
  * tgp_debug_set_rowtile_mask(m) enables kernel families in the automatic
  * plan: bit 0 the row-tiled kernel for forward calls, bit 1 for data-gradient
  * calls, bit 2 the row-blocked weight gradient, bit 3 the nine-tap whole-row
- * kernel (default: bits 0-3 set); bit 4 makes the nine-tap kernel use its
- * four-wave layouts instead of the eight-wave ones, bit 5 makes the
- * row-blocked weight gradient use its four-wave layout at every width. */
+ * kernel (default: bits 0-3 set); bit 4 restricts the nine-tap kernel to
+ * its four-wave layouts (by default it picks among four- and eight-wave
+ * ones), bit 5 makes the row-blocked weight gradient use its four-wave
+ * layout at every width. */
 int tgp_debug_set_fwd_variant(int v);
 int tgp_debug_set_rowtile_mask(int m);
 

@@ -328,23 +328,26 @@ constexpr int kR32N = sizeof(kR32Cfgs) / sizeof(kR32Cfgs[0]);
 
 }  // namespace
 
-// Configuration for a per-sample shape: among those for its width and the
-// chosen wave layout (eight waves unless measuring), the one with the fewest
-// rounds of 256 tiles (for a nominal 4-sample micro-batch) times fragments
-// per wave.  Returns an index into kR32Cfgs, or -1.
+// Configuration for a per-sample shape and ng micro-batches per launch:
+// among those for its width, the one with the fewest rounds of 256 tiles
+// (for a nominal 4 ng samples) times fragments per wave, a four-wave
+// configuration's fragments weighted 1.1 (measured: at equal rounds and
+// fragments it runs about 10% slower than the eight-wave layout).  The
+// summation order of every output is the same in all configurations, so
+// the choice does not change values.  Returns an index into kR32Cfgs, or -1.
 int g_rows32_cfg = -1;   // >= 0 forces a configuration (measurement only)
-int g_rows32_ch = 1;     // channel halves per wave the automatic choice uses
+int g_rows32_ch = 0;     // 1 or 2: only that wave layout (measurement); 0: both
 
-static int rows32_pick(const ConvShape& s) {
+static int rows32_pick(const ConvShape& s, int ng = 1) {
   if (s.taps != 9 || s.cin % 16 || s.cout % 64) return -1;
   int best = -1;
   long best_cost = 0;
   for (int c = 0; c < kR32N; ++c) {
     const R32Cfg k = kR32Cfgs[c];
     if (k.W != s.W || k.R > s.H) continue;
-    if (g_rows32_cfg < 0 && k.CH != g_rows32_ch) continue;
-    const long items = 4L * ((s.H + k.R - 1) / k.R) * (s.cout / 64);
-    const long cost = (items + 255) / 256 * k.FW;
+    if (g_rows32_cfg < 0 && g_rows32_ch && k.CH != g_rows32_ch) continue;
+    const long items = 4L * ng * ((s.H + k.R - 1) / k.R) * (s.cout / 64);
+    const long cost = (items + 255) / 256 * k.FW * (k.CH == 2 ? 11 : 10);
     if (g_rows32_cfg == c || (g_rows32_cfg < 0 && (best < 0 || cost < best_cost))) {
       best = c;
       best_cost = cost;
@@ -384,7 +387,7 @@ static hipError_t launch_rows32(const bf16_t* X, const bf16_t* X2, const bf16_t*
 hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, void* y,
                                const ConvShape& s, int relu, hipStream_t st, const void* x2,
                                void* y2) {
-  const int c = rows32_pick(s);
+  const int c = rows32_pick(s, x2 ? 2 : 1);
   if (c < 0 || !conv_rows32_ok(s) || (x2 == nullptr) != (y2 == nullptr))
     return hipErrorInvalidValue;
   const bf16_t* X = (const bf16_t*)x;

@@ -703,7 +703,7 @@ int tgp_debug_set_fwd_split(int v) {
 int tgp_debug_set_rowtile_mask(int v) {
   int old = tgpk::g_rowtile_mask;
   tgpk::g_rowtile_mask = v;
-  tgpk::g_rows32_ch = (v >> 4 & 1) ? 2 : 1;
+  tgpk::g_rows32_ch = (v >> 4 & 1) ? 2 : 0;
   tgpk::g_wgrad_ks = (v >> 5 & 1) ? 1 : 0;
   return old;
 }
