@@ -330,11 +330,24 @@ struct WgPlan { int R, nK; };
 
 }  // namespace
 
+// Image rows per stage and ring depth per width: stages of 128 to 256
+// pixels, ring within the 160 KiB of LDS.
+struct WgCfg { int W, RPS, NS; };
+constexpr WgCfg kWgCfgs[] = {{256, 1, 2}, {192, 1, 3}, {128, 1, 4}, {96, 2, 3}, {64, 3, 3},
+                             {48, 4, 3},  {32, 6, 3},  {24, 4, 5},  {16, 8, 4}, {8, 8, 4}};
+static_assert(sizeof(kWgCfgs) / sizeof(kWgCfgs[0]) == 10, "one launch case per width");
+
+static int wgrad_rows_rps(int W) {
+  for (const WgCfg& c : kWgCfgs)
+    if (c.W == W) return c.RPS;
+  return 0;
+}
+
 // Rows per K range: the fewest (a multiple of the rows per stage) that keep
 // the item count within one wave of 256 blocks.
 static WgPlan wgrad_rows_plan(const ConvShape& s) {
   const long per_k = 3L * (s.cout / 64) * (s.cin / 64);
-  const int rps = s.W >= 192 ? 1 : (s.W >= 96 ? 2 : 4);
+  const int rps = wgrad_rows_rps(s.W);
   int R = rps;
   while (R < s.H && (long)s.nb * ((s.H + R - 1) / R) * per_k > 256) R += rps;
   if (R > s.H) R = s.H;
@@ -345,7 +358,7 @@ static WgPlan wgrad_rows_plan(const ConvShape& s) {
 int g_wgrad_ks = 0;
 
 bool wgrad_rows_ok(const ConvShape& s) {
-  return s.taps == 9 && (s.W == 192 || s.W == 96 || s.W == 48 || s.W == 24) && s.cin % 64 == 0 &&
+  return s.taps == 9 && wgrad_rows_rps(s.W) > 0 && s.cin % 64 == 0 &&
          s.cout % 64 == 0 && (double)s.pixels() * (s.cin > s.cout ? s.cin : s.cout) * 2 < 2147483648.0;
 }
 
@@ -363,12 +376,10 @@ static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* X2, const bf1
   const int G = (int)(items < 256 ? items : 256);
   const double flops = 2.0 * ng * s.pixels() * s.cout * 9 * s.cin;
   const double bytes = ng * (2.0 * s.pixels() * (s.cin + s.cout) + 4.0 * p.nK * s.cout * 9 * s.cin);
-  static const char* names[2][4] = {
-      {"conv_wgrad_rows<192,1,3>", "conv_wgrad_rows<96,2,3>", "conv_wgrad_rows<48,4,3>",
-       "conv_wgrad_rows<24,4,5>"},
-      {"conv_wgrad_rows<192,1,3,8w>", "conv_wgrad_rows<96,2,3,8w>", "conv_wgrad_rows<48,4,3,8w>",
-       "conv_wgrad_rows<24,4,5,8w>"}};
-  ProfScope ps(names[KS - 1][W == 192 ? 0 : (W == 96 ? 1 : (W == 48 ? 2 : 3))], flops, bytes, st);
+  static char name[48];
+  if (!name[0])
+    snprintf(name, sizeof name, "conv_wgrad_rows<%d,%d,%d%s>", W, RPS, NS, KS == 2 ? ",8w" : "");
+  ProfScope ps(name, flops, bytes, st);
   TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, NS, KS>), dim3(G), dim3(256 * KS), 0, st, X, X2, DZ,
              DZ2, out, out2, s.nb, s.H, s.cin, s.cout, p.R);
   return hipGetLastError();
@@ -385,6 +396,21 @@ static hipError_t launch_wgrad_rows_ks(const bf16_t* X, const bf16_t* X2, const 
                  : launch_wgrad_rows<W, RPS, NS, 1>(X, X2, DZ, DZ2, out, out2, s, p, st);
 }
 
+static hipError_t launch_wgrad_rows_w(const bf16_t* X, const bf16_t* X2, const bf16_t* DZ,
+                                      const bf16_t* DZ2, float* out, float* out2,
+                                      const ConvShape& s, const WgPlan& p, hipStream_t st) {
+  switch (s.W) {
+#define WG_CASE(i)                                                                           \
+  case kWgCfgs[i].W:                                                                         \
+    return launch_wgrad_rows_ks<kWgCfgs[i].W, kWgCfgs[i].RPS, kWgCfgs[i].NS>(X, X2, DZ, DZ2,  \
+                                                                             out, out2, s, p, st);
+    WG_CASE(0) WG_CASE(1) WG_CASE(2) WG_CASE(3) WG_CASE(4)
+    WG_CASE(5) WG_CASE(6) WG_CASE(7) WG_CASE(8) WG_CASE(9)
+#undef WG_CASE
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
                                   const ConvShape& s, hipStream_t st, const ReduceJob* extra,
                                   ReduceJob* defer) {
@@ -393,11 +419,7 @@ hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, floa
   float* out = p.nK > 1 ? partial : dw;
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* DZ = (const bf16_t*)dz;
-  hipError_t e;
-  if (s.W == 192) e = launch_wgrad_rows_ks<192, 1, 3>(X, nullptr, DZ, nullptr, out, nullptr, s, p, st);
-  else if (s.W == 96) e = launch_wgrad_rows_ks<96, 2, 3>(X, nullptr, DZ, nullptr, out, nullptr, s, p, st);
-  else if (s.W == 48) e = launch_wgrad_rows_ks<48, 4, 3>(X, nullptr, DZ, nullptr, out, nullptr, s, p, st);
-  else e = launch_wgrad_rows_ks<24, 4, 5>(X, nullptr, DZ, nullptr, out, nullptr, s, p, st);
+  hipError_t e = launch_wgrad_rows_w(X, nullptr, DZ, nullptr, out, nullptr, s, p, st);
   if (e != hipSuccess) return e;
   if (defer) {
     *defer = ReduceJob{out, dw, (long)s.cout * 9 * s.cin, p.nK};
@@ -420,11 +442,7 @@ hipError_t conv_wgrad_rows_launch2(const void* x0, const void* x1, const void* d
   float* o1 = p.nK > 1 ? partial1 : dw1;
   const bf16_t *X0 = (const bf16_t*)x0, *X1 = (const bf16_t*)x1;
   const bf16_t *D0 = (const bf16_t*)dz0, *D1 = (const bf16_t*)dz1;
-  hipError_t e;
-  if (s.W == 192) e = launch_wgrad_rows_ks<192, 1, 3>(X0, X1, D0, D1, o0, o1, s, p, st);
-  else if (s.W == 96) e = launch_wgrad_rows_ks<96, 2, 3>(X0, X1, D0, D1, o0, o1, s, p, st);
-  else if (s.W == 48) e = launch_wgrad_rows_ks<48, 4, 3>(X0, X1, D0, D1, o0, o1, s, p, st);
-  else e = launch_wgrad_rows_ks<24, 4, 5>(X0, X1, D0, D1, o0, o1, s, p, st);
+  hipError_t e = launch_wgrad_rows_w(X0, X1, D0, D1, o0, o1, s, p, st);
   if (e != hipSuccess) return e;
   const long E = (long)s.cout * 9 * s.cin;
   *defer0 = ReduceJob{o0, dw0, E, p.nK};

@@ -64,6 +64,15 @@ def test_conv3x3(cin, cout, h, w, B, m):
     run_and_check(net, (1,), 1, BF16, B, m, f"conv3x3 {cin}->{cout} @{h}x{w} B={B} m={m}")
 
 
+@pytest.mark.parametrize("cin,cout,h,w", [(64, 64, 3, 256), (64, 128, 5, 128), (64, 64, 7, 64),
+                                          (128, 64, 9, 32), (64, 64, 11, 16), (128, 128, 9, 8)])
+def test_wgrad_rows_other_widths(cin, cout, h, w):
+    """The row-blocked weight gradient at the 6-level U-Net's widths 256 ...
+    8 (stages of one to eight image rows), with a ragged last row block."""
+    net = one_layer(Layer(CONV3X3, cin, cout), h, w)
+    run_and_check(net, (1,), 1, BF16, 2, 1, f"wgrad rows {cin}->{cout} @{h}x{w}")
+
+
 # Configurations of the nine-tap whole-row kernel: (index, W, rows per tile).
 ROWS32 = [(0, 192, 3), (1, 192, 1), (2, 96, 6), (3, 96, 3), (4, 96, 2), (5, 48, 12),
           (6, 48, 6), (7, 48, 4), (8, 24, 24), (9, 24, 12), (10, 24, 8),
