@@ -475,13 +475,27 @@ __global__ __launch_bounds__(256) void relu_bwd_k(const T* __restrict__ dy, cons
 // fused in: block b covers rows [b*rows, (b+1)*rows); thread t handles the
 // 16-byte channel pack t % CP for rows t / CP, t / CP + 256 / CP, ...
 // (serial, fixed order); row lanes are then added in order in LDS and
-// part[b][c] is written.  Needs 256 % CP == 0 (CP = C / pack).
+// part[b][c] is written.  Needs 256 % CP == 0 (CP = C / pack).  A launch
+// covers gridDim.y (1 or 2) micro-batches of the same shape; blockIdx.y
+// selects the pointer set.
 template <typename T>
-__global__ __launch_bounds__(256) void relu_bwd_bias_k(const T* __restrict__ dy,
-                                                       const T* __restrict__ ds,
-                                                       const T* __restrict__ y,
-                                                       T* __restrict__ dz, float* __restrict__ part,
-                                                       int relu, long P, int C, long rows) {
+struct RbPtrs {
+  const T* dy;   // the incoming gradient (the pool gradient for the pooled kernel)
+  const T* ds;
+  const T* y;
+  T* dz;
+  float* part;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void relu_bwd_bias_k(RbPtrs<T> g0, RbPtrs<T> g1, int relu,
+                                                       long P, int C, long rows) {
+  const RbPtrs<T> g = blockIdx.y ? g1 : g0;
+  const T* __restrict__ dy = g.dy;
+  const T* __restrict__ ds = g.ds;
+  const T* __restrict__ y = g.y;
+  T* __restrict__ dz = g.dz;
+  float* __restrict__ part = g.part;
   constexpr int N = Pk<T>::N;
   __shared__ float red[256 * N];
   const int CP = C / N;
@@ -529,13 +543,15 @@ __global__ __launch_bounds__(256) void relu_bwd_bias_k(const T* __restrict__ dy,
 // pixels of a window in row-major order), then row lanes are added in order
 // in LDS and part[b][c] is written.
 template <typename T>
-__global__ __launch_bounds__(256) void pool_relu_bwd_bias_k(const T* __restrict__ dp,
-                                                            const T* __restrict__ ds,
-                                                            const T* __restrict__ y,
-                                                            T* __restrict__ dz,
-                                                            float* __restrict__ part, int relu,
+__global__ __launch_bounds__(256) void pool_relu_bwd_bias_k(RbPtrs<T> g0, RbPtrs<T> g1, int relu,
                                                             int nb, int H, int W, int C,
                                                             long rows) {
+  const RbPtrs<T> gp = blockIdx.y ? g1 : g0;
+  const T* __restrict__ dp = gp.dy;
+  const T* __restrict__ ds = gp.ds;
+  const T* __restrict__ y = gp.y;
+  T* __restrict__ dz = gp.dz;
+  float* __restrict__ part = gp.part;
   constexpr int N = Pk<T>::N;
   __shared__ float red[256 * N];
   const int CP = C / N;
@@ -644,9 +660,14 @@ __global__ __launch_bounds__(256) void dw_wgrad_k(const T* __restrict__ x, const
 
 // ---------------------------------------------------------------- pool
 
+// 2x2/2 max pool of gridDim.y (1 or 2) micro-batches (blockIdx.y selects
+// x0 / y0 or x1 / y1).
 template <typename T>
-__global__ __launch_bounds__(256) void maxpool_fwd_k(const T* __restrict__ x, T* __restrict__ y,
+__global__ __launch_bounds__(256) void maxpool_fwd_k(const T* __restrict__ x0, T* __restrict__ y0,
+                                                     const T* __restrict__ x1, T* __restrict__ y1,
                                                      int nb, int H, int W, int C) {
+  const T* __restrict__ x = blockIdx.y ? x1 : x0;
+  T* __restrict__ y = blockIdx.y ? y1 : y0;
   constexpr int N = Pk<T>::N;
   int CP = C / N, H2 = H / 2, W2 = W / 2;
   long e = (long)blockIdx.x * 256 + threadIdx.x;
@@ -1209,59 +1230,89 @@ bool pool_relu_bias_fusable(int dt, int C, int H, int W, const void* dp, const v
   return H % 2 == 0 && W % 2 == 0 && H >= 2 && W >= 2 && relu_bias_fusable(dt, C, dp, dskip, y, dz);
 }
 
-hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
-                              int relu, float* db, float* partial, long P, int C,
-                              hipStream_t st, ReduceJob* defer) {
+template <typename T>
+static RbPtrs<T> rb_ptrs(const RbArgs& a) {
+  return RbPtrs<T>{(const T*)a.dy, (const T*)a.dskip, (const T*)a.y, (T*)a.dz, a.partial};
+}
+
+// The bias sums of n launched micro-batches: left pending (defer) or reduced.
+static hipError_t rb_finish(int n, const RbArgs* a, long C, int nblk, hipStream_t st) {
+  for (int k = 0; k < n; ++k) {
+    if (a[k].defer) {
+      *a[k].defer = ReduceJob{a[k].partial, a[k].db, C, nblk};
+    } else {
+      const hipError_t e = splitk_reduce_launch(a[k].partial, a[k].db, C, nblk, st);
+      if (e != hipSuccess) return e;
+    }
+  }
+  return hipSuccess;
+}
+
+hipError_t relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, long P, int C,
+                                hipStream_t st) {
+  if (n < 1 || n > 2 || (n == 2 && ((a[0].dskip == nullptr) != (a[1].dskip == nullptr))))
+    return hipErrorInvalidValue;
   long rows = relu_bias_rows(P, C, dt == 0 ? 8 : 4);
   int nb = cdiv(P, rows);
+  const RbArgs& b = a[n - 1];
   {
     ProfScope ps("relu_backward_bias", 0.0,
-                 (dt == 0 ? 2.0 : 4.0) * P * C * (3 + (dskip ? 1 : 0) - (relu ? 0 : 1)) + 4.0 * nb * C, st);
+                 n * ((dt == 0 ? 2.0 : 4.0) * P * C * (3 + (a[0].dskip ? 1 : 0) - (relu ? 0 : 1)) +
+                      4.0 * nb * C),
+                 st);
     if (dt == 0)
-      TGP_LAUNCH(ps, relu_bwd_bias_k<bf16_t>, dim3(nb), dim3(256), 0, st, (const bf16_t*)dy,
-                         (const bf16_t*)dskip, (const bf16_t*)y, (bf16_t*)dz, partial, relu, P, C,
-                         rows);
+      TGP_LAUNCH(ps, relu_bwd_bias_k<bf16_t>, dim3(nb, n), dim3(256), 0, st,
+                 rb_ptrs<bf16_t>(a[0]), rb_ptrs<bf16_t>(b), relu, P, C, rows);
     else
-      TGP_LAUNCH(ps, relu_bwd_bias_k<float>, dim3(nb), dim3(256), 0, st, (const float*)dy,
-                         (const float*)dskip, (const float*)y, (float*)dz, partial, relu, P, C,
-                         rows);
+      TGP_LAUNCH(ps, relu_bwd_bias_k<float>, dim3(nb, n), dim3(256), 0, st,
+                 rb_ptrs<float>(a[0]), rb_ptrs<float>(b), relu, P, C, rows);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (defer) {
-    *defer = ReduceJob{partial, db, (long)C, nb};
-    return hipSuccess;
+  return rb_finish(n, a, C, nb, st);
+}
+
+hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
+                              int relu, float* db, float* partial, long P, int C,
+                              hipStream_t st, ReduceJob* defer) {
+  const RbArgs a{dy, dskip, y, dz, db, partial, defer};
+  return relu_backward_bias_n(dt, 1, &a, relu, P, C, st);
+}
+
+hipError_t pool_relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, int nb, int H,
+                                     int W, int C, hipStream_t st) {
+  if (n < 1 || n > 2 || (n == 2 && ((a[0].dskip == nullptr) != (a[1].dskip == nullptr))))
+    return hipErrorInvalidValue;
+  for (int k = 0; k < n; ++k)
+    if (!pool_relu_bias_fusable(dt, C, H, W, a[k].dy, a[k].dskip, a[k].y, a[k].dz))
+      return hipErrorInvalidValue;
+  const long P2 = (long)nb * (H / 2) * (W / 2);
+  const long rows = relu_bias_rows(P2, C, dt == 0 ? 8 : 4);
+  const int nbk = cdiv(P2, rows);
+  const RbArgs& b = a[n - 1];
+  {
+    const double esz = dt == 0 ? 2.0 : 4.0;
+    ProfScope ps("pool_relu_backward_bias", 0.0,
+                 n * (esz * 4.0 * P2 * C * (2 + (a[0].dskip ? 1 : 0)) + esz * P2 * C +
+                      4.0 * nbk * C),
+                 st);
+    if (dt == 0)
+      TGP_LAUNCH(ps, pool_relu_bwd_bias_k<bf16_t>, dim3(nbk, n), dim3(256), 0, st,
+                 rb_ptrs<bf16_t>(a[0]), rb_ptrs<bf16_t>(b), relu, nb, H, W, C, rows);
+    else
+      TGP_LAUNCH(ps, pool_relu_bwd_bias_k<float>, dim3(nbk, n), dim3(256), 0, st,
+                 rb_ptrs<float>(a[0]), rb_ptrs<float>(b), relu, nb, H, W, C, rows);
   }
-  return splitk_reduce_launch(partial, db, C, nb, st);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return rb_finish(n, a, C, nbk, st);
 }
 
 hipError_t pool_relu_backward_bias(int dt, const void* dp, const void* dskip, const void* y,
                                    void* dz, int relu, float* db, float* partial, int nb, int H,
                                    int W, int C, hipStream_t st, ReduceJob* defer) {
-  if (!pool_relu_bias_fusable(dt, C, H, W, dp, dskip, y, dz)) return hipErrorInvalidValue;
-  const long P2 = (long)nb * (H / 2) * (W / 2);
-  const long rows = relu_bias_rows(P2, C, dt == 0 ? 8 : 4);
-  const int nbk = cdiv(P2, rows);
-  {
-    const double esz = dt == 0 ? 2.0 : 4.0;
-    ProfScope ps("pool_relu_backward_bias", 0.0,
-                 esz * 4.0 * P2 * C * (2 + (dskip ? 1 : 0)) + esz * P2 * C + 4.0 * nbk * C, st);
-    if (dt == 0)
-      TGP_LAUNCH(ps, pool_relu_bwd_bias_k<bf16_t>, dim3(nbk), dim3(256), 0, st,
-                 (const bf16_t*)dp, (const bf16_t*)dskip, (const bf16_t*)y, (bf16_t*)dz, partial,
-                 relu, nb, H, W, C, rows);
-    else
-      TGP_LAUNCH(ps, pool_relu_bwd_bias_k<float>, dim3(nbk), dim3(256), 0, st,
-                 (const float*)dp, (const float*)dskip, (const float*)y, (float*)dz, partial,
-                 relu, nb, H, W, C, rows);
-  }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  if (defer) {
-    *defer = ReduceJob{partial, db, (long)C, nbk};
-    return hipSuccess;
-  }
-  return splitk_reduce_launch(partial, db, C, nbk, st);
+  const RbArgs a{dp, dskip, y, dz, db, partial, defer};
+  return pool_relu_backward_bias_n(dt, 1, &a, relu, nb, H, W, C, st);
 }
 
 hipError_t bias_grad(int dt, const void* dz, float* db, float* partial, long P, int C,
@@ -1281,17 +1332,26 @@ hipError_t bias_grad(int dt, const void* dz, float* db, float* partial, long P, 
   return splitk_reduce_launch(partial, db, C, nb, st);
 }
 
-hipError_t maxpool_forward(int dt, const void* x, void* y, int nb, int H, int W, int C,
-                           hipStream_t st) {
+hipError_t maxpool_forward2(int dt, const void* x0, void* y0, const void* x1, void* y1, int nb,
+                            int H, int W, int C, hipStream_t st) {
+  const int n = x1 ? 2 : 1;
+  if ((x1 == nullptr) != (y1 == nullptr)) return hipErrorInvalidValue;
   int N = dt == 0 ? 8 : 4;
   long total = (long)nb * (H / 2) * (W / 2) * (C / N);
-  dim3 g(cdiv(total, 256));
-  ProfScope ps("maxpool_forward", 0.0, (dt == 0 ? 2.0 : 4.0) * nb * H * W * C * 1.25, st);
+  dim3 g(cdiv(total, 256), n);
+  ProfScope ps("maxpool_forward", 0.0, n * (dt == 0 ? 2.0 : 4.0) * nb * H * W * C * 1.25, st);
   if (dt == 0)
-    TGP_LAUNCH(ps, maxpool_fwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x, (bf16_t*)y, nb, H, W, C);
+    TGP_LAUNCH(ps, maxpool_fwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x0, (bf16_t*)y0,
+               (const bf16_t*)(n == 2 ? x1 : x0), (bf16_t*)(n == 2 ? y1 : y0), nb, H, W, C);
   else
-    TGP_LAUNCH(ps, maxpool_fwd_k<float>, g, dim3(256), 0, st, (const float*)x, (float*)y, nb, H, W, C);
+    TGP_LAUNCH(ps, maxpool_fwd_k<float>, g, dim3(256), 0, st, (const float*)x0, (float*)y0,
+               (const float*)(n == 2 ? x1 : x0), (float*)(n == 2 ? y1 : y0), nb, H, W, C);
   return hipGetLastError();
+}
+
+hipError_t maxpool_forward(int dt, const void* x, void* y, int nb, int H, int W, int C,
+                           hipStream_t st) {
+  return maxpool_forward2(dt, x, y, nullptr, nullptr, nb, H, W, C, st);
 }
 
 hipError_t maxpool_backward(int dt, const void* x, const void* dy, void* dx, int nb, int H,

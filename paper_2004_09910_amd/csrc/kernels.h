@@ -119,6 +119,9 @@ hipError_t bias_grad(int dt, const void* dz, float* db, float* partial, long P, 
 
 // 2x2/2 max-pool of x (nb x H x W x C) into y; backward routes dy to the first
 // maximal element of each window (row-major).
+// Two micro-batches in one launch (x1 / y1 null: one).
+hipError_t maxpool_forward2(int dt, const void* x0, void* y0, const void* x1, void* y1, int nb,
+                            int H, int W, int C, hipStream_t st);
 hipError_t maxpool_forward(int dt, const void* x, void* y, int nb, int H, int W, int C,
                            hipStream_t st);
 hipError_t maxpool_backward(int dt, const void* x, const void* dy, void* dx, int nb, int H,
@@ -166,6 +169,23 @@ bool relu_bias_fusable(int dt, int C, const void* dy, const void* dskip, const v
 size_t relu_bias_partial_floats(int dt, long P, int C);
 // With `defer`, the bias gradient's column sums are left in `partial` and
 // *defer describes the sum still to run (the caller passes it to conv_wgrad).
+// One micro-batch's tensors for the fused ReLU-backward / bias-sum kernels
+// (dy is the pool gradient for the pooled variant).
+struct RbArgs {
+  const void* dy;
+  const void* dskip;
+  const void* y;
+  void* dz;
+  float* db;
+  float* partial;
+  ReduceJob* defer;
+};
+// n (1 or 2) micro-batches of the same shape in one launch; both with or
+// both without a skip gradient.
+hipError_t relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, long P, int C,
+                                hipStream_t st);
+hipError_t pool_relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, int nb, int H,
+                                     int W, int C, hipStream_t st);
 hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const void* y, void* dz,
                               int relu, float* db, float* partial, long P, int C,
                               hipStream_t st, ReduceJob* defer = nullptr);

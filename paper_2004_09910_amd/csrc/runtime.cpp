@@ -248,10 +248,7 @@ tgp_status run_forward_g(tgp_net* N, int j, int cnt, const int* iv, const int* p
       cin_ptr[k] = src[k];
       if (d.prologue != TGP_PRO_NONE) {
         void* pro = (phase[k] == 1) ? W_(N, Lr.o_sto_pro[set[k]]) : T_(N, i, Lr.o_scr_pro);
-        if (d.prologue == TGP_PRO_MAXPOOL2) {
-          HIPCHK(tgpk::maxpool_forward(N->dt, src[k], pro, N->b, Lr.inH, Lr.inW, Lr.inC, st),
-                 "maxpool_forward");
-        } else {
+        if (d.prologue == TGP_PRO_UPCAT2) {
           const LayerRt& sl = N->L[N->stash_layer.at(d.pop_id)];
           HIPCHK(tgpk::upcat_forward(N->dt, src[k], W_(N, stash_off(N, i, d.pop_id, false)), pro,
                                      N->b, Lr.H, Lr.W, Lr.inC, sl.d.cout, st),
@@ -260,6 +257,11 @@ tgp_status run_forward_g(tgp_net* N, int j, int cnt, const int* iv, const int* p
         cin_ptr[k] = pro;
       }
     }
+    if (d.prologue == TGP_PRO_MAXPOOL2)   // both micro-batches' pools in one launch
+      HIPCHK(tgpk::maxpool_forward2(N->dt, src[0], (void*)cin_ptr[0], cnt == 2 ? src[1] : nullptr,
+                                    cnt == 2 ? (void*)cin_ptr[1] : nullptr, N->b, Lr.inH, Lr.inW,
+                                    Lr.inC, st),
+             "maxpool_forward");
     if (d.kind == TGP_DWCONV3X3) {
       for (int k = 0; k < cnt; ++k)
         HIPCHK(tgpk::dw_forward(N->dt, cin_ptr[k], Lr.w, d.bias ? Lr.b : nullptr, out[k], N->b,
@@ -386,58 +388,109 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     const void* cin_ptr[2];
     const void* dzk[2];   // the layer's dz: B.dz, or the incoming dy itself
     std::array<tgpk::ReduceJob, 2>* pjs[2];
+    const void* yk[2];
+    const void* dskipk[2];
+    float* gbk[2];
+    float* bpartk[2];
+    tgpk::ReduceJob* bdeferk[2];
+    const long nout = out_elems_mb(N, Lr);
+    const long P = (long)N->b * Lr.H * Lr.W;
     for (int k = 0; k < cnt; ++k) {
       BwdMb& B = M[k];
       dzk[k] = B.dz;
       const int i = B.i;
-      const void* y = B.v.out[l - lo];
+      yk[k] = B.v.out[l - lo];
       src[k] = (l == lo) ? B.v.in0 : B.v.out[l - 1 - lo];  // pre-prologue input
       cin_ptr[k] = d.prologue != TGP_PRO_NONE ? B.v.pro[l - lo] : src[k];
-      const void* dskip = d.stash_id >= 0 ? W_(N, stash_off(N, i, d.stash_id, true)) : nullptr;
-      long nout = out_elems_mb(N, Lr);
-      long P = (long)N->b * Lr.H * Lr.W;
+      dskipk[k] = d.stash_id >= 0 ? W_(N, stash_off(N, i, d.stash_id, true)) : nullptr;
       // both gradients stay partial sums in the slot, reduced by the
       // accumulation (the bias's column sums only where relu_backward_bias
       // computes them; bias_grad reduces its own)
       std::array<tgpk::ReduceJob, 2>& pj = N->pend[(size_t)(i - 1) * N->L.size() + l];
       pjs[k] = &pj;
-      float* gb = d.bias ? (float*)G_(N, i, Lr.o_gb) : nullptr;
-      pj[1] = tgpk::ReduceJob{gb, gb, d.bias ? (long)d.cout : 0, 0};   // S = 0: not yet run
+      gbk[k] = d.bias ? (float*)G_(N, i, Lr.o_gb) : nullptr;
+      pj[1] = tgpk::ReduceJob{gbk[k], gbk[k], d.bias ? (long)d.cout : 0, 0};   // S = 0: not yet run
       // column partials: kept in the slot, or (too large to keep) reduced at once
-      float* bpart = Lr.defer_b ? (float*)G_(N, i, Lr.o_gcol) : B.colpart;
-      tgpk::ReduceJob* bdefer = Lr.defer_b ? &pj[1] : nullptr;
+      bpartk[k] = Lr.defer_b ? (float*)G_(N, i, Lr.o_gcol) : B.colpart;
+      bdeferk[k] = Lr.defer_b ? &pj[1] : nullptr;
+    }
+    // The fused kernels take both micro-batches of a pair in one launch when
+    // both qualify (they always do together: same shape and flags, buffers
+    // of the same alignment).
+    tgpk::RbArgs ra[2];
+    auto fill_ra = [&](const void* const* dyv) {
+      for (int k = 0; k < cnt; ++k)
+        ra[k] = tgpk::RbArgs{dyv[k], dskipk[k], yk[k], M[k].dz, gbk[k], bpartk[k], bdeferk[k]};
+    };
+    auto ran = [&](int k) {
+      if (!bdeferk[k]) (*pjs[k])[1].S = 1;
+    };
+    bool all_pool = cnt > 0;
+    for (int k = 0; k < cnt; ++k)
+      all_pool = all_pool && M[k].dy_pool && d.bias && Lr.o_gcol_floats &&
+                 tgpk::pool_relu_bias_fusable(N->dt, d.cout, Lr.H, Lr.W, M[k].dy_pool, dskipk[k],
+                                              yk[k], M[k].dz);
+    if (all_pool) {
+      const void* dps[2] = {M[0].dy_pool, cnt == 2 ? M[1].dy_pool : nullptr};
+      fill_ra(dps);
+      HIPCHK(tgpk::pool_relu_backward_bias_n(N->dt, cnt, ra, d.relu, N->b, Lr.H, Lr.W, d.cout, st),
+             "pool_relu_backward_bias");
+      for (int k = 0; k < cnt; ++k) {
+        ran(k);
+        M[k].dy_pool = nullptr;
+      }
+    }
+    for (int k = 0; k < cnt; ++k) {
+      BwdMb& B = M[k];
       if (B.dy_pool && d.bias && Lr.o_gcol_floats &&
-          tgpk::pool_relu_bias_fusable(N->dt, d.cout, Lr.H, Lr.W, B.dy_pool, dskip, y, B.dz)) {
-        HIPCHK(tgpk::pool_relu_backward_bias(N->dt, B.dy_pool, dskip, y, B.dz, d.relu, gb, bpart,
-                                             N->b, Lr.H, Lr.W, d.cout, st, bdefer),
+          tgpk::pool_relu_bias_fusable(N->dt, d.cout, Lr.H, Lr.W, B.dy_pool, dskipk[k], yk[k],
+                                       B.dz)) {
+        HIPCHK(tgpk::pool_relu_backward_bias(N->dt, B.dy_pool, dskipk[k], yk[k], B.dz, d.relu,
+                                             gbk[k], bpartk[k], N->b, Lr.H, Lr.W, d.cout, st,
+                                             bdeferk[k]),
                "pool_relu_backward_bias");
-        if (!bdefer) pj[1].S = 1;
+        ran(k);
         B.dy_pool = nullptr;
       } else if (B.dy_pool) {
-        HIPCHK(tgpk::maxpool_backward(N->dt, y, B.dy_pool, (void*)B.dy, N->b, Lr.H, Lr.W, d.cout,
-                                      st),
+        HIPCHK(tgpk::maxpool_backward(N->dt, yk[k], B.dy_pool, (void*)B.dy, N->b, Lr.H, Lr.W,
+                                      d.cout, st),
                "maxpool_backward");
         B.dy_pool = nullptr;
       }
+    }
+    bool all_rb = cnt > 0;
+    for (int k = 0; k < cnt; ++k)
+      all_rb = all_rb && (*pjs[k])[1].S == 0 && d.bias && Lr.o_gcol_floats &&
+               tgpk::relu_bias_fusable(N->dt, d.cout, M[k].dy, dskipk[k], yk[k], M[k].dz);
+    if (all_rb) {
+      const void* dys[2] = {M[0].dy, cnt == 2 ? M[1].dy : nullptr};
+      fill_ra(dys);
+      HIPCHK(tgpk::relu_backward_bias_n(N->dt, cnt, ra, d.relu, P, d.cout, st),
+             "relu_backward_bias");
+      for (int k = 0; k < cnt; ++k) ran(k);
+    }
+    for (int k = 0; k < cnt; ++k) {
+      BwdMb& B = M[k];
+      std::array<tgpk::ReduceJob, 2>& pj = *pjs[k];
       if (pj[1].S == 0 && d.bias && Lr.o_gcol_floats &&
-          tgpk::relu_bias_fusable(N->dt, d.cout, B.dy, dskip, y, B.dz)) {
-        HIPCHK(tgpk::relu_backward_bias(N->dt, B.dy, dskip, y, B.dz, d.relu, gb, bpart, P, d.cout,
-                                        st, bdefer),
+          tgpk::relu_bias_fusable(N->dt, d.cout, B.dy, dskipk[k], yk[k], B.dz)) {
+        HIPCHK(tgpk::relu_backward_bias(N->dt, B.dy, dskipk[k], yk[k], B.dz, d.relu, gbk[k],
+                                        bpartk[k], P, d.cout, st, bdeferk[k]),
                "relu_backward_bias");
-        if (!bdefer) pj[1].S = 1;
-      } else if (pj[1].S == 0 && !d.relu && !d.bias && !dskip) {
+        ran(k);
+      } else if (pj[1].S == 0 && !d.relu && !d.bias && !dskipk[k]) {
         // no ReLU, bias or skip: dz is dy itself, read in place (the
         // buffer holding dy is not written again before the next layer)
         dzk[k] = B.dy;
         pj[1].S = 1;
       } else if (pj[1].S == 0) {
-        HIPCHK(tgpk::relu_backward(N->dt, B.dy, dskip, y, B.dz, d.relu, nout, st),
+        HIPCHK(tgpk::relu_backward(N->dt, B.dy, dskipk[k], yk[k], B.dz, d.relu, nout, st),
                "relu_backward");
         if (d.bias)
-          HIPCHK(tgpk::bias_grad(N->dt, B.dz, gb, B.colpart, P, d.cout, st), "bias_grad");
+          HIPCHK(tgpk::bias_grad(N->dt, B.dz, gbk[k], B.colpart, P, d.cout, st), "bias_grad");
         pj[1].S = 1;
       }
-      float* gw = (float*)G_(N, i, Lr.o_gw);
+      float* gw = (float*)G_(N, B.i, Lr.o_gw);
       pj[0] = tgpk::ReduceJob{gw, gw, Lr.w_elems, 1};
     }
     // weight gradient
