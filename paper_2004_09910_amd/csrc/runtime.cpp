@@ -96,6 +96,10 @@ struct tgp_net {
   int gslots = 1;
   size_t o_gslot = 0, gslot_stride = 0;
   std::vector<std::array<tgpk::ReduceJob, 2>> pend;
+  // [lane * n + j - 1]: the lane's transformed weights of partition j were
+  // not refreshed at its first backward of this step (a paired backward
+  // reads only its first micro-batch's lane); refreshed before a later use
+  std::vector<char> wt_stale;
   // Streams and events tgp_pipeline_step forks onto with several lanes (one
   // per lane plus one for the accumulations), created on first use on the
   // device current then; default priority.
@@ -357,19 +361,41 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     }
   }
   BwdMb M[2];
+  auto stale = [&](int i) -> char& {
+    return N->wt_stale[(size_t)((i - 1) % N->lanes) * N->n + (j - 1)];
+  };
+  auto refresh_wt = [&](int i) -> tgp_status {
+    for (int l = lo; l < hi; ++l) {
+      LayerRt& Lr = N->L[l];
+      if (Lr.has_wt)
+        HIPCHK(tgpk::weight_transform(N->dt, Lr.w, T_(N, i, Lr.o_wt), Lr.d.cout, Lr.d.cin,
+                                      Lr.taps, st),
+               "weight_transform");
+    }
+    stale(i) = 0;
+    return TGP_OK;
+  };
   for (int k = 0; k < cnt; ++k) {
     const int i = iv[k];
     if (i > N->m - N->lanes) {
       // first backward of partition j on this lane in this step: refresh the
-      // lane's transformed weights used by the data-gradient kernels
-      for (int l = lo; l < hi; ++l) {
-        LayerRt& Lr = N->L[l];
-        if (Lr.has_wt)
-          HIPCHK(tgpk::weight_transform(N->dt, Lr.w, T_(N, i, Lr.o_wt), Lr.d.cout, Lr.d.cin,
-                                        Lr.taps, st),
-                 "weight_transform");
+      // lane's transformed weights used by the data-gradient kernels (the
+      // second of a pair reads the first's, so its lane is refreshed when
+      // a later backward of this step reads it)
+      if (cnt == 2 && k == 1) {
+        stale(i) = 1;
+      } else {
+        tgp_status r = refresh_wt(i);
+        if (r != TGP_OK) return r;
       }
     }
+  }
+  if (stale(iv[0])) {
+    tgp_status r = refresh_wt(iv[0]);
+    if (r != TGP_OK) return r;
+  }
+  for (int k = 0; k < cnt; ++k) {
+    const int i = iv[k];
     BwdMb& B = M[k];
     B.i = i;
     activation_view(N, j, i, N->saved_ckpt[cell(N, i, j)], B.v);
@@ -1038,6 +1064,7 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
   N->saved_y.assign((size_t)m * n, nullptr);
   N->saved_ckpt.assign((size_t)m * n, 0);
   N->pend.assign((size_t)m * N->L.size(), std::array<tgpk::ReduceJob, 2>{});
+  N->wt_stale.assign((size_t)N->lanes * N->n, 0);
   *bytes = off;
   return TGP_OK;
 }

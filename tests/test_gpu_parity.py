@@ -105,6 +105,43 @@ def test_micro_batch_pairs_are_bit_identical(mode):
         assert torch.equal(runs[1]["stash"][sid], runs[0]["stash"][sid])
 
 
+def test_pair_then_single_calls_in_one_step():
+    """Forwards in pairs, then a paired backward (4, 3) followed by single
+    backwards of 2 and 1 on one stream: the single backward on the second
+    lane must see that lane's transformed weights refreshed (the pair read
+    only the first lane's).  Bits equal one micro-batch per launch."""
+    import paper_2004_09910_amd as tgp
+    from paper_2004_09910_amd.harness import Session
+
+    class Mixed(Session):
+        def stage_step(self, j, x, y, dy, dx, stream=0, serial=False):
+            def sl(t, i):
+                return t.data_ptr() + (i - 1) * (t.numel() // self.m) * t.element_size()
+            for i in (1, 3):
+                tgp.stage_forward2(self.h, j, i, i + 1, self.checkpointed(i),
+                                   self.checkpointed(i + 1), sl(x, i), sl(x, i + 1), sl(y, i),
+                                   sl(y, i + 1), stream)
+            tgp.stage_backward_recompute2(self.h, j, 4, 3, sl(dy, 4), sl(dy, 3), sl(dx, 4),
+                                          sl(dx, 3), stream)
+            tgp.grad_accumulate(self.h, j, 4, True, stream)
+            tgp.grad_accumulate(self.h, j, 3, False, stream)
+            for i in (2, 1):
+                tgp.stage_backward_recompute(self.h, j, i, sl(dy, i), sl(dx, i), stream)
+                tgp.grad_accumulate(self.h, j, i, False, stream)
+
+    net = specs.unet(5, 64, 64, 48, "unet5-c64-48")
+    bal = (7, 5, 3, 4)
+    say("mixed: reference, one per launch")
+    ref = gpu_stage(net, BF16, 8, 4, CKPT_ALWAYS, bal, 1, neutral=False)
+    say("mixed: pair then singles")
+    sess = Mixed(net, BF16, n=len(bal), balance=bal, bind_layers=range(0, 7))
+    sess.plan(8, 4, CKPT_ALWAYS, 2)
+    got = gpu_stage(net, BF16, 8, 4, CKPT_ALWAYS, bal, 1, neutral=False, sess=sess)
+    same_bits(ref, got)
+    assert torch.equal(got["y"], ref["y"])
+    assert torch.equal(got["dx"], ref["dx"])
+
+
 def test_micro_batch_pairs_bench_stage():
     """The pair path on the benchmark's own stage (U-Net level-0 layers at
     192 x 192, micro-batch 4), m = 2, against one micro-batch per launch."""
