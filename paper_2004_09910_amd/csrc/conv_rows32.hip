@@ -45,11 +45,16 @@ __device__ __forceinline__ unsigned pack2_bf16(float a, float b) {
   return __builtin_bit_cast(unsigned, h);
 }
 
-template <int W, int R>
+// RK > 0: the weights of all RK stages (Cin = 16 RK, one 64-channel output
+// tile) stay resident in LDS ahead of the ring, loaded once per block, and
+// a ring slot holds only the input rows.
+template <int W, int R, int RK = 0>
 struct Rows32Geom {
   static constexpr int BWP = (W + 2 + 15) / 16 * 16;           // LDS rows per input row
   static constexpr int BROWS = (R + 2) * BWP;
-  static constexpr int SB = ((R32_AROWS + BROWS) * 32 + 4095) / 4096 * 4096;  // stage bytes
+  static constexpr int AR = RK ? 0 : R32_AROWS;                 // weight rows per slot
+  static constexpr int SB = ((AR + BROWS) * 32 + 4095) / 4096 * 4096;  // stage (slot) bytes
+  static constexpr int RB = RK * R32_AROWS * 32;                // resident weight bytes
   static constexpr int L = SB / 4096;                           // DMA instructions per wave
   static constexpr int F = R * W / 32;                          // pixel fragments per tile
   static_assert(R * W % 32 == 0, "whole fragments per tile");
@@ -66,20 +71,22 @@ struct Rows32Geom {
 // with the same weights: its tiles follow the first's (sample index nb ..
 // 2 nb - 1), so one launch covers both and each block streams a tile of
 // each through its ring.
-template <int W, int R, int FW, int NS, int CH>
+template <int W, int R, int FW, int NS, int CH, int RK>
 __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
     const bf16_t* __restrict__ X, const bf16_t* __restrict__ X2, const bf16_t* __restrict__ Wt,
     const float* __restrict__ bias, bf16_t* __restrict__ Y, bf16_t* __restrict__ Y2, int nb,
     int H, int Cin, int Cout, int relu) {
-  typedef Rows32Geom<W, R> G_;
-  constexpr int BWP = G_::BWP, SB = G_::SB, F = G_::F;
+  typedef Rows32Geom<W, R, RK> G_;
+  constexpr int BWP = G_::BWP, SB = G_::SB, F = G_::F, AR = G_::AR, RB = G_::RB;
   constexpr int NW = CH == 2 ? 4 : 8;                           // waves
   constexpr int NCH = SB / 1024;                                // DMA chunks per stage
   constexpr int LW = (NCH + NW - 1) / NW;                       // ... per wave, at most
-  constexpr int ACH = R32_AROWS * 32 / 1024;                    // DMA chunks of weights
+  constexpr int ACH = AR * 32 / 1024;                           // DMA chunks of weights per stage
+  constexpr int WCH = R32_AROWS * 32 / 1024;                    // ... of one stage's weights
   static_assert(F <= 4 * FW, "fragments per pixel group");
-  static_assert(NS * SB <= 160 * 1024, "LDS ring");
-  __shared__ __attribute__((aligned(16))) unsigned char smem[NS * SB];
+  static_assert(RB + NS * SB <= 160 * 1024, "LDS ring");
+  __shared__ __attribute__((aligned(16))) unsigned char smem[RB + NS * SB];
+  unsigned char* const ring = smem + RB;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int pg = wave & 3;                                      // pixel group (the SIMD)
@@ -124,7 +131,7 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
       doff[u] = ((co * 9 + tap) * Cin + 8 * lh) * 2;
       drow[u] = 0;
     } else {
-      const int q = row - R32_AROWS;
+      const int q = row - AR;
       const int rr = q / BWP, wp = q - rr * BWP;
       const bool ok = rr < R + 2 && wp >= 1 && wp <= W;
       doff[u] = ok ? ((rr * W + wp - 1) * Cin + 8 * lh) * 2 : 0;
@@ -148,7 +155,7 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
       const int q = rho * BWP + w + s;
-      bq[j][s] = R32_AROWS * 32 + q * 32 + (((lane >> 5) ^ ((q >> 3) & 1)) << 4);
+      bq[j][s] = AR * 32 + q * 32 + (((lane >> 5) ^ ((q >> 3) & 1)) << 4);
     }
   }
 
@@ -181,7 +188,7 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
       if (u < u0 || u >= u1) continue;
       const int k = NW * u + wave;
       if (NCH % NW != 0 && k >= NCH) continue;                  // wave-uniform
-      auto* dst = TGP_LDS(smem + slot * SB + k * 1024);
+      auto* dst = TGP_LDS(ring + slot * SB + k * 1024);
       if (k < ACH) {
         dma16(rw, dst, doff[u], soff_a);
       } else {
@@ -197,6 +204,23 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
     }
   };
 
+  if constexpr (RK > 0) {
+    // every stage's weights of the block's single output-channel tile, once,
+    // in the slot layout (chunk c: stage c / WCH, weight chunk c % WCH); the
+    // ring's waits cover them since loads complete in order
+    if (total > 0) {
+#pragma unroll
+      for (int u = 0; u < (RK * WCH + NW - 1) / NW; ++u) {
+        const int c = NW * u + wave;
+        if (c >= RK * WCH) continue;                             // wave-uniform
+        const int row = (c % WCH) * 32 + (lane >> 1);
+        const int lh = (lane & 1) ^ ((row >> 3) & 1);
+        const int tap = row >> 6, co = row & 63;
+        dma16(rw, TGP_LDS(smem + c * 1024), ((co * 9 + tap) * Cin + 8 * lh) * 2,
+              (c / WCH) * 16 * 2);
+      }
+    }
+  }
 #pragma unroll
   for (int k = 0; k < NS - 1; ++k)
     if (k < total) {
@@ -231,14 +255,15 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
       ring_barrier();
       const bool fill = idx + NS - 1 < total;                   // refill the slot freed last stage
       const int fslot = (idx + NS - 1) % NS;
-      const unsigned char* st = smem + (idx % NS) * SB;
+      const unsigned char* st = ring + (idx % NS) * SB;
+      const unsigned char* sa = RK ? smem + ks * R32_AROWS * 32 : st;   // weights of this stage
       // nine taps; tap t + 1's fragments are read while tap t's MFMAs run
       bf16x8_t fa[2][CH], fb[2][FW];
       auto load = [&](int t, int buf) __attribute__((always_inline)) {
         const int r = t / 3, s = t - 3 * (t / 3);
 #pragma unroll
         for (int i = 0; i < CH; ++i)
-          fa[buf][i] = as_bf16x8(*(const u32x4*)(st + abase + (t * 64 + 32 * i) * 32));
+          fa[buf][i] = as_bf16x8(*(const u32x4*)(sa + abase + (t * 64 + 32 * i) * 32));
 #pragma unroll
         for (int j = 0; j < FW; ++j)
           fb[buf][j] = as_bf16x8(*(const u32x4*)(st + bq[j][s] + r * BWP * 32));
@@ -279,7 +304,8 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
     ring_barrier();
     constexpr int ROWB = 64 * CH;                               // staged bytes per pixel
     constexpr int NCK = 4 * CH;                                 // 16-byte chunks per pixel
-    unsigned char* ep = smem + ((idx - 1) % NS) * SB + wave * 32 * ROWB;
+    unsigned char* ep = ring + ((idx - 1) % NS) * SB + wave * 32 * ROWB;
+    static_assert(NW * 32 * ROWB <= SB, "epilogue staging fits a slot");
     const bool g1 = n >= nb;
     bf16_t* const Yg = g1 ? Y2 : Y;
     const long pix0 = (long)((g1 ? n - nb : n) * H + h0) * W;
@@ -315,14 +341,17 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
   }
 }
 
-struct R32Cfg { int W, R, FW, NS, CH; };
+struct R32Cfg { int W, R, FW, NS, CH, RK; };
 constexpr R32Cfg kR32Cfgs[] = {
-    {192, 3, 5, 3, 2}, {192, 1, 2, 4, 2},
-    {96, 6, 5, 3, 2},  {96, 3, 3, 4, 2},  {96, 2, 2, 4, 2},
-    {48, 12, 5, 3, 2}, {48, 6, 3, 4, 2},  {48, 4, 2, 4, 2},
-    {24, 24, 5, 3, 2}, {24, 12, 3, 4, 2}, {24, 8, 2, 4, 2},
+    {192, 3, 5, 3, 2, 0}, {192, 1, 2, 4, 2, 0},
+    {96, 6, 5, 3, 2, 0},  {96, 3, 3, 4, 2, 0},  {96, 2, 2, 4, 2, 0},
+    {48, 12, 5, 3, 2, 0}, {48, 6, 3, 4, 2, 0},  {48, 4, 2, 4, 2, 0},
+    {24, 24, 5, 3, 2, 0}, {24, 12, 3, 4, 2, 0}, {24, 8, 2, 4, 2, 0},
     // eight waves, two per SIMD
-    {192, 3, 5, 3, 1}, {96, 3, 3, 4, 1}, {96, 2, 2, 4, 1}, {48, 4, 2, 4, 1}, {24, 8, 2, 4, 1},
+    {192, 3, 5, 3, 1, 0}, {96, 3, 3, 4, 1, 0}, {96, 2, 2, 4, 1, 0}, {48, 4, 2, 4, 1, 0},
+    {24, 8, 2, 4, 1, 0},
+    // eight waves, weights of 64 input channels resident (Cin = 64, Cout = 64)
+    {192, 2, 3, 3, 1, 4}, {192, 3, 5, 2, 1, 4},
 };
 constexpr int kR32N = sizeof(kR32Cfgs) / sizeof(kR32Cfgs[0]);
 
@@ -345,9 +374,10 @@ static int rows32_pick(const ConvShape& s, int ng = 1) {
   for (int c = 0; c < kR32N; ++c) {
     const R32Cfg k = kR32Cfgs[c];
     if (k.W != s.W || k.R > s.H) continue;
+    if (k.RK && (s.cin != 16 * k.RK || s.cout != 64)) continue;
     if (g_rows32_cfg < 0 && g_rows32_ch && k.CH != g_rows32_ch) continue;
     const long items = 4L * ng * ((s.H + k.R - 1) / k.R) * (s.cout / 64);
-    const long cost = (items + 255) / 256 * k.FW * (k.CH == 2 ? 11 : 10);
+    const long cost = (items + 255) / 256 * k.FW * (k.RK ? 8 : (k.CH == 2 ? 11 : 10));
     if (g_rows32_cfg == c || (g_rows32_cfg < 0 && (best < 0 || cost < best_cost))) {
       best = c;
       best_cost = cost;
@@ -361,17 +391,18 @@ bool conv_rows32_ok(const ConvShape& s) {
          (double)s.cout * 9 * s.cin * 2 < 2147483648.0;
 }
 
-template <int W, int R, int FW, int NS, int CH>
+template <int W, int R, int FW, int NS, int CH, int RK>
 static hipError_t launch_rows32(const bf16_t* X, const bf16_t* X2, const bf16_t* Wt,
                                 const float* b, bf16_t* Y, bf16_t* Y2, const ConvShape& s,
                                 int relu, hipStream_t st) {
   static const char* name = nullptr;
   static char buf[64];
   if (!name) {
-    if (CH == 2) snprintf(buf, sizeof buf, "conv3x3_rows32<%d,%d,%d,%d>", W, R, FW, NS);
-    else snprintf(buf, sizeof buf, "conv3x3_rows32<%d,%d,%d,%d,8w>", W, R, FW, NS);
+    snprintf(buf, sizeof buf, "conv3x3_rows32<%d,%d,%d,%d%s%s>", W, R, FW, NS,
+             CH == 2 ? "" : ",8w", RK ? ",rk" : "");
     name = buf;
   }
+  if (RK && (s.cin != 16 * RK || s.cout != 64)) return hipErrorInvalidValue;
   const int ng = X2 ? 2 : 1;
   const long items = (long)ng * s.nb * ((s.H + R - 1) / R) * (s.cout / 64);
   const int G = (int)(items < 256 ? items : 256);
@@ -379,7 +410,7 @@ static hipError_t launch_rows32(const bf16_t* X, const bf16_t* X2, const bf16_t*
   const long P = (long)ng * s.pixels();
   ProfScope ps(name, 2.0 * P * s.cout * 9 * s.cin,
                2.0 * ((double)P * s.cin + 9.0 * s.cin * s.cout + (double)P * s.cout), st);
-  TGP_LAUNCH(ps, (conv3x3_rows32<W, R, FW, NS, CH>), dim3(G), dim3(CH == 2 ? 256 : 512), 0, st, X,
+  TGP_LAUNCH(ps, (conv3x3_rows32<W, R, FW, NS, CH, RK>), dim3(G), dim3(CH == 2 ? 256 : 512), 0, st, X,
              X2, Wt, b, Y, Y2, s.nb, s.H, s.cin, s.cout, relu);
   return hipGetLastError();
 }
@@ -399,10 +430,10 @@ hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, voi
 #define R32_CASE(i)                                                                      \
   case i:                                                                                \
     return launch_rows32<kR32Cfgs[i].W, kR32Cfgs[i].R, kR32Cfgs[i].FW, kR32Cfgs[i].NS,   \
-                         kR32Cfgs[i].CH>(X, X2, Wt, b, Y, Y2, s, relu, st);
+                         kR32Cfgs[i].CH, kR32Cfgs[i].RK>(X, X2, Wt, b, Y, Y2, s, relu, st);
     R32_CASE(0) R32_CASE(1) R32_CASE(2) R32_CASE(3) R32_CASE(4) R32_CASE(5)
     R32_CASE(6) R32_CASE(7) R32_CASE(8) R32_CASE(9) R32_CASE(10) R32_CASE(11)
-    R32_CASE(12) R32_CASE(13) R32_CASE(14) R32_CASE(15)
+    R32_CASE(12) R32_CASE(13) R32_CASE(14) R32_CASE(15) R32_CASE(16) R32_CASE(17)
 #undef R32_CASE
     default: return hipErrorInvalidValue;
   }

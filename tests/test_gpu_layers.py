@@ -95,6 +95,20 @@ def test_rows32_configurations(cfg, w, r):
         tgp.debug_set_fwd_variant(old)
 
 
+@pytest.mark.parametrize("cfg,r", [(16, 2), (17, 3)])
+def test_rows32_resident_weights(cfg, r):
+    """The nine-tap kernel's configurations that keep the weights of all 64
+    input channels in LDS (64 -> 64 channels only), forced, with a ragged
+    last row block; the data gradient takes the same configuration."""
+    import paper_2004_09910_amd as tgp
+    old = tgp.debug_set_fwd_variant(401 + cfg)
+    try:
+        net = one_layer(Layer(CONV3X3, 64, 64), r + 1, 192)
+        run_and_check(net, (1,), 1, BF16, 2, 1, f"rows32 resident cfg {cfg} @{r + 1}x192")
+    finally:
+        tgp.debug_set_fwd_variant(old)
+
+
 @pytest.mark.parametrize("cin,cout,h,w", [(64, 128, 7, 48), (128, 64, 5, 96), (64, 64, 3, 192),
                                           (128, 128, 5, 24)])
 def test_wgrad_rows_four_wave_layout(cin, cout, h, w):
