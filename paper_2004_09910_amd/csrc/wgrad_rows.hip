@@ -344,15 +344,20 @@ static int wgrad_rows_rps(int W) {
 }
 
 // Rows per K range: the fewest (a multiple of the rows per stage) that keep
-// one micro-batch's item count within 128, so that a launch over two
-// micro-batches fills one round of 256 blocks.  (Measured on the U-Net
-// stage: a bound of 256 writes twice the partial slices and was 2.5% slower
-// per step, 192 leaves 1.5 rounds.)
+// one micro-batch's item count within 128 for micro-batches of four or more
+// samples, so that a launch over two micro-batches fills one round of 256
+// blocks, and within 256 for smaller ones, which the pipelined schedule
+// launches one at a time.  (Measured: on the U-Net stage at four samples a
+// bound of 256 writes twice the partial slices and was 2.5% slower per
+// step, 192 leaves 1.5 rounds; on the 6-level network at two samples, one
+// micro-batch per launch, 128 halved the weight gradient's rate at widths
+// 256 and 128.)
 static WgPlan wgrad_rows_plan(const ConvShape& s) {
   const long per_k = 3L * (s.cout / 64) * (s.cin / 64);
   const int rps = wgrad_rows_rps(s.W);
   int R = rps;
-  while (R < s.H && (long)s.nb * ((s.H + R - 1) / R) * per_k > 128) R += rps;
+  const long cap = s.nb >= 4 ? 128 : 256;
+  while (R < s.H && (long)s.nb * ((s.H + R - 1) / R) * per_k > cap) R += rps;
   if (R > s.H) R = s.H;
   return {R, s.nb * ((s.H + R - 1) / R)};
 }

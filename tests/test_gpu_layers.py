@@ -77,7 +77,9 @@ def test_wgrad_rows_other_widths(cin, cout, h, w):
 ROWS32 = [(0, 192, 3), (1, 192, 1), (2, 96, 6), (3, 96, 3), (4, 96, 2), (5, 48, 12),
           (6, 48, 6), (7, 48, 4), (8, 24, 24), (9, 24, 12), (10, 24, 8),
           # eight-wave layouts
-          (11, 192, 3), (12, 96, 3), (13, 96, 2), (14, 48, 4), (15, 24, 8)]
+          (11, 192, 3), (12, 96, 3), (13, 96, 2), (14, 48, 4), (15, 24, 8),
+          # widths 64 and 32
+          (18, 64, 4), (19, 64, 6), (20, 32, 8), (21, 32, 12)]
 
 
 @pytest.mark.parametrize("cfg,w,r", ROWS32)
