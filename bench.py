@@ -710,7 +710,7 @@ def main():
                           "launches": 3}), flush=True)
         return
     if args.balance_by_time:
-        balance_report(args.mode)
+        balance_report(args.mode or "always")
         return
     if args.memory:
         memory_report()

@@ -1231,14 +1231,17 @@ PersTile pers_tile(int cfg) {
 FwdPlan fwd_plan(const ConvShape& s) {
   const long P = 4L * s.H * s.W;
   FwdPlan pl{0, 1};
-  // Measured per shape (3x3, b = 4, kernel time in a stage step that runs
-  // two micro-batches per launch): the nine-tap whole-row kernel is fastest
-  // on images of 24 x 24 and up (at 24 x 24 a paired launch of it takes 27
-  // us where the split-K row-stage kernel and its epilogue take 40); the
-  // persistent row-stage kernel with split K on smaller, deep layers (few
-  // pixel tiles, long K); the per-tap kernel for the rest.
+  // Measured per shape (3x3, kernel time in a step): the nine-tap
+  // whole-row kernel is fastest on images of 48 x 48 and up, and from 24 x 24
+  // where one micro-batch gives it at least 48 tiles (at 24 x 24 a paired
+  // launch of it takes 27 us where the split-K row-stage kernel and its
+  // epilogue take 40; with fewer tiles, as at one or two samples, most CUs
+  // idle); the persistent row-stage kernel with split K on the other small,
+  // deep layers (few pixel tiles, long K); the per-tap kernel for the rest.
   const bool k3 = s.taps == 9 && s.cin % 64 == 0;
-  if (k3 && (long)s.H * s.W >= 24 * 24 && (g_rowtile_mask >> 3 & 1) && conv_rows32_ok(s)) {
+  const long hw = (long)s.H * s.W;
+  if (k3 && (hw >= 48 * 48 || (hw >= 24 * 24 && conv_rows32_tiles(s) >= 48)) &&
+      (g_rowtile_mask >> 3 & 1) && conv_rows32_ok(s)) {
     pl.cfg = 400;  // whole-row tiles, nine taps per stage, 32x32x16
   } else if (k3 && (long)s.H * s.W >= 96 * 96 && conv_rowtile_ok(s) &&
       (g_rowtile_mask >> (t_in_dgrad ? 1 : 0) & 1)) {

@@ -388,6 +388,13 @@ static int rows32_pick(const ConvShape& s, int ng = 1) {
   return best;
 }
 
+// Tiles of one micro-batch in the configuration a single launch takes.
+int conv_rows32_tiles(const ConvShape& s) {
+  const int c = rows32_pick(s);
+  if (c < 0) return 0;
+  return s.nb * ((s.H + kR32Cfgs[c].R - 1) / kR32Cfgs[c].R) * (s.cout / 64);
+}
+
 bool conv_rows32_ok(const ConvShape& s) {
   return rows32_pick(s) >= 0 && (double)s.pixels() * s.cin * 2 < 2147483648.0 &&
          (double)s.cout * 9 * s.cin * 2 < 2147483648.0;

@@ -33,6 +33,7 @@ extern int g_rowtile_cfg;
 // 16-channel stage (bf16; W in {24, 48, 96, 192}, Cin % 16 == 0, Cout % 64
 // == 0): whether it supports a shape, and the launch (same contract as
 // conv_forward_rowtile).
+int conv_rows32_tiles(const ConvShape& s);
 bool conv_rows32_ok(const ConvShape& s);
 hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, void* y,
                                const ConvShape& s, int relu, hipStream_t st,
