@@ -251,16 +251,21 @@ def test_partition_ending_at_a_stashed_layer(bal):
         same_bits(runs[0], r)
 
 
-def test_microbatch_count_changes_only_accumulation_order():
+def test_microbatch_count_changes_values_only_within_tolerance():
     """Per-sample activations do not depend on m (no intra-batch computation,
-    Sec. 2), so outputs are bit-identical across m and gradients differ only by
-    the fp32 order of the sum over micro-batches."""
+    Sec. 2), but a kernel's configuration may depend on the micro-batch size
+    b = B / m (for example the 24 x 24 path and the weight gradient's K
+    ranges), so across m outputs and gradients agree to the bf16 tolerance,
+    not bit for bit (the sum over micro-batches also changes order).  At a
+    fixed m the checkpoint modes stay bit-identical (other tests)."""
     net = specs.unet(3, 64, 64, 24, "unet3-c64")
     a = gpu_network(net, BF16, 8, 1, 2, CKPT_ALWAYS)
     b = gpu_network(net, BF16, 8, 8, 2, CKPT_ALWAYS)
-    np.testing.assert_array_equal(a["y"], b["y"])
+    assert maxrel(b["y"], a["y"]) < TOL[BF16]
     for idx in a["grads"]:
-        assert maxrel(b["grads"][idx][0], a["grads"][idx][0]) < 1e-5
+        assert maxrel(b["grads"][idx][0], a["grads"][idx][0]) < TOL[BF16]
+        if a["grads"][idx][1] is not None:
+            assert maxrel(b["grads"][idx][1], a["grads"][idx][1]) < TOL[BF16]
 
 
 def test_unet_stage_reduced_size():
