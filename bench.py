@@ -44,15 +44,15 @@ KERNEL_SOURCES = ["paper_2004_09910_amd/csrc/conv_mfma.hip",
                   "paper_2004_09910_amd/csrc/mfma_util.h",
                   "paper_2004_09910_amd/csrc/common.h"]
 PROFILE_COMMANDS = {
-    "trace": "rocprofv3 --kernel-trace --stats --output-format csv -d gpurun_out/prof_kt -o kt "
+    "trace": "rocprofv3 --kernel-trace --stats --output-format csv -d rocprof_out/prof_kt -o kt "
              "-- python3 bench.py --steps 10 --warmup 2 --no-cpu-baseline",
-    "fetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/prof_fetch -o f "
+    "fetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d rocprof_out/prof_fetch -o f "
              "-- python3 bench.py --eager --steps 1 --warmup 1 --no-cpu-baseline",
-    "write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/prof_write -o w "
+    "write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d rocprof_out/prof_write -o w "
              "-- python3 bench.py --eager --steps 1 --warmup 1 --no-cpu-baseline",
-    "copy_fetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/prof_cfetch -o cf "
+    "copy_fetch": "rocprofv3 --pmc FETCH_SIZE --output-format csv -d rocprof_out/prof_cfetch -o cf "
                   "-- python3 bench.py --copy-calibration",
-    "copy_write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/prof_cwrite -o cw "
+    "copy_write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d rocprof_out/prof_cwrite -o cw "
                   "-- python3 bench.py --copy-calibration",
 }
 

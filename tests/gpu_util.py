@@ -206,7 +206,7 @@ def check_grad(name, got, ref, alts, dtype, errs, strict=False):
     """max-rel and rms-rel error of `got` against the reference.
 
     strict (single layers, forward outputs, fp32 runs): both within the
-    spec tolerance.  Gradients of bf16 runs through several ReLU / pool
+    parity tolerance.  Gradients of bf16 runs through several ReLU / pool
     layers pass if either
       (a) max-rel and rms-rel are within the tolerance or SPREAD_FACTOR times
           the largest distance of a float32-contraction variant from the

@@ -1,7 +1,7 @@
 """Single-layer parity: each kernel family through the C ABI, as a one-layer
 stage with an injected upstream gradient.  Both sides start from identical
 bf16 inputs, so no ReLU or pool decision can differ and every output (y, dx,
-dW, db) is held to the benchmark spec's tolerance directly: 2e-2 max-rel for bf16,
+dW, db) is held to the parity tolerance directly: 2e-2 max-rel for bf16,
 1e-4 for fp32.  Shapes include ragged pixel tiles and the benchmark's own
 level-0 and deepest layer shapes at its micro-batch size."""
 import pytest

@@ -1,7 +1,7 @@
 """GPU parity for whole networks and multi-layer stages: the HIP path through
 the C ABI against the oracle on the same seeded inputs, element by element.
 
-Forward outputs and the loss are held to the benchmark spec's tolerance (2e-2
+Forward outputs and the loss are held to the parity tolerance (2e-2
 max-rel bf16, 1e-4 fp32).  Gradients of bf16 runs through several ReLU and
 max-pool layers are held to that tolerance or, where larger, to 4x the
 spread between the reference and the same oracle with float32 contraction;
