@@ -192,11 +192,13 @@ __device__ __attribute__((aligned(16))) unsigned int g_zero16[4];
 // Block index remapped (xcd_remap) so that consecutive pixel tiles, which
 // share halo rows and read the same weights, run on the same XCD.
 
+// X2 / Y2 (both null or both set): a second micro-batch of P pixels; the
+// grid then holds both micro-batches' tiles, the second half for it.
 template <int WCO, int WP, int TM, int TN, int TAPS, int NS>
 __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_dma(
-    const bf16_t* __restrict__ X, const bf16_t* __restrict__ Wt,
-    const float* __restrict__ bias, bf16_t* __restrict__ Y, int P, int H, int W, int Cin,
-    int Cout, int relu, int co_major) {
+    const bf16_t* __restrict__ X0, const bf16_t* __restrict__ X2, const bf16_t* __restrict__ Wt,
+    const float* __restrict__ bias, bf16_t* __restrict__ Y0, bf16_t* __restrict__ Y2, int P,
+    int H, int W, int Cin, int Cout, int relu, int co_major) {
   constexpr int NW = WCO * WP;       // waves per block
   constexpr int BN = WCO * TM * 32;  // output channels per block
   constexpr int BM = WP * TN * 32;   // pixels per block
@@ -213,8 +215,13 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_dma(
   // in its L2), channel-tile-major when the weights are (a slice of the
   // weights plus the whole activation tile set).
   const int nct = Cout / BN;
-  const int npt = gridDim.x / nct;
-  const int lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int per = X2 ? gridDim.x / 2 : gridDim.x;              // blocks per micro-batch
+  const int npt = per / nct;
+  const int lb0 = xcd_remap(blockIdx.x, gridDim.x);
+  const bool g1 = lb0 >= per;                                   // second micro-batch (uniform)
+  const int lb = g1 ? lb0 - per : lb0;
+  const bf16_t* __restrict__ X = g1 ? X2 : X0;
+  bf16_t* __restrict__ Y = g1 ? Y2 : Y0;
   const int p0 = (co_major ? lb % npt : lb / nct) * BM;
   const int co0 = (co_major ? lb / npt : lb % nct) * BN;
   const int K = TAPS * Cin;
@@ -1069,29 +1076,31 @@ int g_fwd_order = -1;   // -1: by operand size; 0/1 forced (measurement only)
 template <int WCO, int WP, int TM, int TN, int NS>
 hipError_t launch_fwd_dma(const char* name9, const char* name1, const bf16_t* X, const bf16_t* Wt,
                           const float* b, bf16_t* Y, long P, const ConvShape& s, int relu,
-                          hipStream_t st) {
+                          hipStream_t st, const bf16_t* X2 = nullptr, bf16_t* Y2 = nullptr) {
   const char* name = s.taps == 9 ? name9 : name1;
   constexpr int BN = WCO * TM * 32, BM = WP * TN * 32;
-  if (s.cout % BN) return hipErrorInvalidValue;
-  dim3 grid(cdiv(P, BM) * (s.cout / BN));
-  double flops = 2.0 * P * s.cout * s.taps * s.cin;
-  double bytes = 2.0 * ((double)P * s.cin + (double)s.cout * s.taps * s.cin + (double)P * s.cout);
+  if (s.cout % BN || (X2 == nullptr) != (Y2 == nullptr)) return hipErrorInvalidValue;
+  const int ng = X2 ? 2 : 1;
+  dim3 grid(ng * cdiv(P, BM) * (s.cout / BN));
+  double flops = 2.0 * ng * P * s.cout * s.taps * s.cin;
+  double bytes = 2.0 * ((double)ng * P * s.cin + (double)s.cout * s.taps * s.cin +
+                        (double)ng * P * s.cout);
   ProfScope ps(name, flops, bytes, st);
   const double xbytes = 2.0 * P * s.cin, wbytes = 2.0 * s.cout * s.taps * s.cin;
   const int co_major = g_fwd_order >= 0 ? g_fwd_order : (wbytes > xbytes ? 1 : 0);
   if (s.taps == 9)
     TGP_LAUNCH(ps, (conv_fwd_dma<WCO, WP, TM, TN, 9, NS>), grid, dim3(WCO * WP * 64), 0, st, X,
-                       Wt, b, Y, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major);
+                       X2, Wt, b, Y, Y2, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major);
   else
     TGP_LAUNCH(ps, (conv_fwd_dma<WCO, WP, TM, TN, 1, NS>), grid, dim3(WCO * WP * 64), 0, st, X,
-                       Wt, b, Y, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major);
+                       X2, Wt, b, Y, Y2, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major);
   return hipGetLastError();
 }
 
 #define TGP_FWD_CFG(WCO, WP, TM, TN, NS)                                                        \
   launch_fwd_dma<WCO, WP, TM, TN, NS>("conv_fwd_dma<" #WCO "," #WP "," #TM "," #TN ",9," #NS ">", \
                                       "conv_fwd_dma<" #WCO "," #WP "," #TM "," #TN ",1," #NS ">", \
-                                      X, Wt, b, Y, P, s, relu, st)
+                                      X, Wt, b, Y, P, s, relu, st, X2, Y2)
 
 // Row-stage forward launches.  S > 1 splits the stages over S blocks per
 // tile; the partials live in `part` (capacity part_cap floats; S is reduced
@@ -1310,6 +1319,8 @@ hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void*
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* Wt = (const bf16_t*)w;
   bf16_t* Y = (bf16_t*)y;
+  const bf16_t* X2 = nullptr;   // per-tap configurations: one micro-batch
+  bf16_t* Y2 = nullptr;
   const FwdPlan pl = fwd_plan(s);
   const bool wide = s.cout % 128 == 0;
   if (pl.cfg >= 400) {
@@ -1474,6 +1485,21 @@ hipError_t conv_forward_mfma2(const void* x0, const void* x1, const void* w, con
     const hipError_t e = conv_forward_rows32(x0, w, b, y0, s, relu, st, x1, y1);
     g_rows32_cfg = -1;
     return e;
+  }
+  if (pl.cfg >= 100 && pl.cfg < 200) {
+    // the per-tap kernel: both micro-batches' tiles in one grid
+    const long P = s.pixels();
+    const bf16_t* X = (const bf16_t*)x0;
+    const bf16_t* X2 = (const bf16_t*)x1;
+    const bf16_t* Wt = (const bf16_t*)w;
+    bf16_t* Y = (bf16_t*)y0;
+    bf16_t* Y2 = (bf16_t*)y1;
+    switch (pl.cfg - 100) {
+      case 1: return TGP_FWD_CFG(2, 2, 1, 1, 2);
+      case 2: return TGP_FWD_CFG(2, 4, 1, 1, 2);
+      default: return P >= 32768 && s.cout <= 128 ? TGP_FWD_CFG(2, 4, 1, 1, 2)
+                                                   : TGP_FWD_CFG(2, 2, 1, 1, 2);
+    }
   }
   hipError_t e = conv_forward_mfma(x0, w, b, y0, s, relu, part0, part_cap, st);
   if (e != hipSuccess) return e;

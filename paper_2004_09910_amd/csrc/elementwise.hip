@@ -279,12 +279,16 @@ __global__ __launch_bounds__(256) void dw_dgrad_k(const T* __restrict__ dz, cons
 // FLIP applies the filter rotated by 180 degrees, which is the data
 // gradient (dx = dz correlated with the flipped filter); the sum runs over
 // the window in row-major order.
+// gridDim.z (1 or 2) micro-batches: blockIdx.z selects x0 / y0 or x1 / y1.
 template <int RS, bool FLIP>
-__global__ __launch_bounds__(256) void dw3_rows_k(const bf16_t* __restrict__ x,
+__global__ __launch_bounds__(256) void dw3_rows_k(const bf16_t* __restrict__ x0,
+                                                  const bf16_t* __restrict__ x1,
                                                   const bf16_t* __restrict__ w,
                                                   const float* __restrict__ b,
-                                                  bf16_t* __restrict__ y, int H, int W, int C,
-                                                  int relu) {
+                                                  bf16_t* __restrict__ y0, bf16_t* __restrict__ y1,
+                                                  int H, int W, int C, int relu) {
+  const bf16_t* __restrict__ x = blockIdx.z ? x1 : x0;
+  bf16_t* __restrict__ y = blockIdx.z ? y1 : y0;
   const int CP = C >> 3;
   const int q = blockIdx.x * 256 + threadIdx.x;
   const int wc = q / CP, cp = q - (q / CP) * CP;
@@ -356,11 +360,19 @@ __global__ __launch_bounds__(256) void dw3_rows_k(const bf16_t* __restrict__ x,
 // then adds its 256 / CP column groups in order in LDS and writes
 // part[blk][c * 9 + t], blk = strip block * chunks + chunk.  The partials
 // are summed in block order afterwards, so the result is deterministic.
+// gridDim.z (1 or 2) micro-batches: blockIdx.z selects (x0, dz0, part0) or
+// (x1, dz1, part1).
 template <int RS>
-__global__ __launch_bounds__(256) void dw3_wgrad_rows_k(const bf16_t* __restrict__ x,
-                                                        const bf16_t* __restrict__ dz,
-                                                        float* __restrict__ part, int H, int W,
+__global__ __launch_bounds__(256) void dw3_wgrad_rows_k(const bf16_t* __restrict__ x0,
+                                                        const bf16_t* __restrict__ x1,
+                                                        const bf16_t* __restrict__ dz0,
+                                                        const bf16_t* __restrict__ dz1,
+                                                        float* __restrict__ part0,
+                                                        float* __restrict__ part1, int H, int W,
                                                         int C) {
+  const bf16_t* __restrict__ x = blockIdx.z ? x1 : x0;
+  const bf16_t* __restrict__ dz = blockIdx.z ? dz1 : dz0;
+  float* __restrict__ part = blockIdx.z ? part1 : part0;
   __shared__ float red[72][256];
   const int CP = C >> 3;
   const int q = blockIdx.x * 256 + threadIdx.x;
@@ -1094,17 +1106,66 @@ hipError_t conv_wgrad2(int dt, const void* x0, const void* x1, const void* dz0, 
   return conv_wgrad(dt, x1, dz1, dw1, part1, s, st, nullptr, defer1);
 }
 
+// The row-window depthwise kernels over one or two micro-batches (x1 null:
+// one); false where they do not apply.
+bool dw_pair_ok(int dt, int nb, int H, int C, const void* a0, const void* a1, const void* b0,
+                const void* b1, const void* c) {
+  return dw3_rows_ok(dt, nb, H, C, a0, b0, c) && dw3_rows_ok(dt, nb, H, C, a1, b1, c);
+}
+
+hipError_t dw_forward2(const void* x0, const void* x1, const void* w, const float* b, void* y0,
+                       void* y1, int nb, int H, int W, int C, int relu, hipStream_t st) {
+  const long P = (long)nb * H * W;
+  const int n = x1 ? 2 : 1;
+  if (P == 0) return hipSuccess;
+  const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwRows)), n);
+  ProfScope ps("dw3_rows_fwd", n * 18.0 * P * C, n * 4.0 * P * C, st);
+  TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, false>), g, dim3(256), 0, st, (const bf16_t*)x0,
+             (const bf16_t*)(x1 ? x1 : x0), (const bf16_t*)w, b, (bf16_t*)y0,
+             (bf16_t*)(x1 ? y1 : y0), H, W, C, relu);
+  return hipGetLastError();
+}
+
+hipError_t dw_dgrad2(const void* dz0, const void* dz1, const void* w, void* dx0, void* dx1,
+                     int nb, int H, int W, int C, hipStream_t st) {
+  const long P = (long)nb * H * W;
+  const int n = dz1 ? 2 : 1;
+  if (P == 0) return hipSuccess;
+  const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwRows)), n);
+  ProfScope ps("dw3_rows_dgrad", n * 18.0 * P * C, n * 4.0 * P * C, st);
+  TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, true>), g, dim3(256), 0, st, (const bf16_t*)dz0,
+             (const bf16_t*)(dz1 ? dz1 : dz0), (const bf16_t*)w, (const float*)nullptr,
+             (bf16_t*)dx0, (bf16_t*)(dz1 ? dx1 : dx0), H, W, C, 0);
+  return hipGetLastError();
+}
+
+hipError_t dw_wgrad2(const void* x0, const void* x1, const void* dz0, const void* dz1,
+                     float* dw0, float* dw1, float* part0, float* part1, int nb, int H, int W,
+                     int C, hipStream_t st) {
+  const long P = (long)nb * H * W;
+  const long E = (long)C * 9;
+  const int n = x1 ? 2 : 1;
+  if (P == 0) return hipSuccess;
+  const int S = dw3_wgrad_blocks(nb, H, W, C);
+  const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwWgradRows)), n);
+  {
+    ProfScope ps("dw3_wgrad_rows", n * 18.0 * P * C, n * (4.0 * P * C + 4.0 * S * E), st);
+    TGP_LAUNCH(ps, (dw3_wgrad_rows_k<kDwWgradRows>), g, dim3(256), 0, st, (const bf16_t*)x0,
+               (const bf16_t*)(x1 ? x1 : x0), (const bf16_t*)dz0,
+               (const bf16_t*)(x1 ? dz1 : dz0), part0, x1 ? part1 : part0, H, W, C);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = splitk_reduce_launch(part0, dw0, E, S, st);
+  if (e != hipSuccess || n == 1) return e;
+  return splitk_reduce_launch(part1, dw1, E, S, st);
+}
+
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
                       int H, int W, int C, int relu, hipStream_t st) {
   long P = (long)nb * H * W;
-  if (dw3_rows_ok(dt, nb, H, C, x, w, y)) {
-    if (P == 0) return hipSuccess;
-    const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwRows)));
-    ProfScope ps("dw3_rows_fwd", 18.0 * P * C, 4.0 * P * C, st);
-    TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, false>), g, dim3(256), 0, st, (const bf16_t*)x,
-               (const bf16_t*)w, b, (bf16_t*)y, H, W, C, relu);
-    return hipGetLastError();
-  }
+  if (dw3_rows_ok(dt, nb, H, C, x, w, y))
+    return dw_forward2(x, nullptr, w, b, y, nullptr, nb, H, W, C, relu, st);
   dim3 g(cdiv(P * C, 256));
   ProfScope ps("dw_forward", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
   if (dt == 0)
@@ -1119,14 +1180,8 @@ hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void
 hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int H, int W,
                     int C, hipStream_t st) {
   long P = (long)nb * H * W;
-  if (dw3_rows_ok(dt, nb, H, C, dz, w, dx)) {
-    if (P == 0) return hipSuccess;
-    const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwRows)));
-    ProfScope ps("dw3_rows_dgrad", 18.0 * P * C, 4.0 * P * C, st);
-    TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, true>), g, dim3(256), 0, st, (const bf16_t*)dz,
-               (const bf16_t*)w, (const float*)nullptr, (bf16_t*)dx, H, W, C, 0);
-    return hipGetLastError();
-  }
+  if (dw3_rows_ok(dt, nb, H, C, dz, w, dx))
+    return dw_dgrad2(dz, nullptr, w, dx, nullptr, nb, H, W, C, st);
   dim3 g(cdiv(P * C, 256));
   ProfScope ps("dw_dgrad", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
   if (dt == 0)
@@ -1151,18 +1206,8 @@ hipError_t dw_wgrad(int dt, const void* x, const void* dz, float* dw, float* par
                     int H, int W, int C, hipStream_t st) {
   long P = (long)nb * H * W;
   long E = (long)C * 9;
-  if (dw3_rows_ok(dt, nb, H, C, x, dz, partial) && P > 0) {
-    const int S = dw3_wgrad_blocks(nb, H, W, C);
-    const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwWgradRows)));
-    {
-      ProfScope ps("dw3_wgrad_rows", 18.0 * P * C, 4.0 * P * C + 4.0 * S * E, st);
-      TGP_LAUNCH(ps, (dw3_wgrad_rows_k<kDwWgradRows>), g, dim3(256), 0, st, (const bf16_t*)x,
-                 (const bf16_t*)dz, partial, H, W, C);
-    }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    return splitk_reduce_launch(partial, dw, E, S, st);
-  }
+  if (dw3_rows_ok(dt, nb, H, C, x, dz, partial) && P > 0)
+    return dw_wgrad2(x, nullptr, dz, nullptr, dw, nullptr, partial, nullptr, nb, H, W, C, st);
   long pps = direct_wgrad_pps(P);
   int S = direct_wgrad_splits(P);
   dim3 g(cdiv(E, 256), S);
