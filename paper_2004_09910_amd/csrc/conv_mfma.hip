@@ -821,10 +821,13 @@ __device__ __forceinline__ void transpose8x8(const u32x4 (&in)[8], u32x4 (&out)[
   }
 }
 
+// X2 / dZ2 / part2 (all null or all set): a second micro-batch, whose blocks
+// form the second half of the grid.
 template <int WM, int WN, int TM, int TN, int TAPS>
 __global__ __launch_bounds__(256) void conv_wgrad_mfma(
-    const bf16_t* __restrict__ X, const bf16_t* __restrict__ dZ, float* __restrict__ part,
-    int P, int H, int W, int Cin, int Cout, int pix_per_split) {
+    const bf16_t* __restrict__ X0, const bf16_t* __restrict__ X2, const bf16_t* __restrict__ dZ0,
+    const bf16_t* __restrict__ dZ2, float* __restrict__ part0, float* __restrict__ part2, int P,
+    int H, int W, int Cin, int Cout, int pix_per_split) {
   static_assert(WM * WN == 4, "4 waves");
   constexpr int BMc = WM * TM * 32;  // output channels (co) per block
   constexpr int BNc = WN * TN * 32;  // input channels (ci) per block
@@ -840,7 +843,13 @@ __global__ __launch_bounds__(256) void conv_wgrad_mfma(
   // runs a contiguous range of splits with all their tiles, so the pixel rows
   // of X and dZ a split reads are fetched into one L2 only.
   const int T = TAPS * ncb * (Cout / BMc);
-  const int lb = xcd_remap(blockIdx.x, gridDim.x);
+  const int per = X2 ? gridDim.x / 2 : gridDim.x;               // blocks per micro-batch
+  const int lb0 = xcd_remap(blockIdx.x, gridDim.x);
+  const bool g1 = lb0 >= per;                                   // second micro-batch (uniform)
+  const int lb = g1 ? lb0 - per : lb0;
+  const bf16_t* __restrict__ X = g1 ? X2 : X0;
+  const bf16_t* __restrict__ dZ = g1 ? dZ2 : dZ0;
+  float* __restrict__ part = g1 ? part2 : part0;
   const int split = lb / T;
   const int t = lb - split * T;
   const int tx = t % (TAPS * ncb);
@@ -1391,43 +1400,61 @@ size_t wgrad_mfma_partial_floats(const ConvShape& s) {
   return (size_t)pl.S * E;
 }
 
-hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
-                           const ConvShape& s, hipStream_t st, const ReduceJob* extra,
-                           ReduceJob* defer) {
-  if (use_wgrad_rows(s)) return conv_wgrad_rows_launch(x, dz, dw, partial, s, st, extra, defer);
+// The per-tap weight gradient of one micro-batch, or of two in one grid
+// (x1 / dz1 / partial1 set; dw1 their sum's target); the split plan is the
+// single micro-batch's either way.
+static hipError_t launch_wgrad_mfma(const void* x, const void* x1, const void* dz,
+                                    const void* dz1, float* dw, float* dw1, float*& partial,
+                                    float*& partial1, const ConvShape& s, WgradPlan& pl,
+                                    hipStream_t st) {
   long P = s.pixels();
   const bf16_t* X = (const bf16_t*)x;
   const bf16_t* DZ = (const bf16_t*)dz;
+  const bf16_t* X2 = (const bf16_t*)x1;
+  const bf16_t* DZ2 = (const bf16_t*)dz1;
+  const int ng = x1 ? 2 : 1;
   bool big = s.cin % 128 == 0 && s.cout % 128 == 0;
   int bm = big ? 128 : 64, bn = big ? 128 : 64;
   int tiles = s.taps * (s.cin / bn) * (s.cout / bm);
   long E = (long)s.cout * s.taps * s.cin;
-  WgradPlan pl = wgrad_plan<2, 2>(P, tiles, E);
-  dim3 grid(s.taps * (s.cin / bn) * (s.cout / bm) * pl.S);
-  double flops = 2.0 * P * E;
-  double bytes = 2.0 * ((double)P * s.cin + (double)P * s.cout) + 4.0 * pl.S * E;
-  {
-    const char* nm = big ? (s.taps == 9 ? "conv_wgrad_mfma<2,2,2,2,9>" : "conv_wgrad_mfma<2,2,2,2,1>")
-                         : (s.taps == 9 ? "conv_wgrad_mfma<2,2,1,1,9>" : "conv_wgrad_mfma<2,2,1,1,1>");
-    ProfScope ps(nm, flops, bytes, st);
-    if (pl.S == 1) partial = dw;   // a single split writes the gradient itself
-    if (big) {
-      if (s.taps == 9)
-        TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 2, 2, 9>), grid, dim3(256), 0, st, X, DZ,
-                           partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
-      else
-        TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 2, 2, 1>), grid, dim3(256), 0, st, X, DZ,
-                           partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
-    } else {
-      if (s.taps == 9)
-        TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 9>), grid, dim3(256), 0, st, X, DZ,
-                           partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
-      else
-        TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 1>), grid, dim3(256), 0, st, X, DZ,
-                           partial, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
-    }
+  pl = wgrad_plan<2, 2>(P, tiles, E);
+  dim3 grid(ng * s.taps * (s.cin / bn) * (s.cout / bm) * pl.S);
+  double flops = 2.0 * ng * P * E;
+  double bytes = ng * (2.0 * ((double)P * s.cin + (double)P * s.cout) + 4.0 * pl.S * E);
+  const char* nm = big ? (s.taps == 9 ? "conv_wgrad_mfma<2,2,2,2,9>" : "conv_wgrad_mfma<2,2,2,2,1>")
+                       : (s.taps == 9 ? "conv_wgrad_mfma<2,2,1,1,9>" : "conv_wgrad_mfma<2,2,1,1,1>");
+  ProfScope ps(nm, flops, bytes, st);
+  if (pl.S == 1) {   // a single split writes the gradient itself
+    partial = dw;
+    partial1 = dw1;
   }
-  hipError_t e = hipGetLastError();
+  float* P2 = x1 ? partial1 : nullptr;
+  if (big) {
+    if (s.taps == 9)
+      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 2, 2, 9>), grid, dim3(256), 0, st, X, X2, DZ, DZ2,
+                 partial, P2, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+    else
+      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 2, 2, 1>), grid, dim3(256), 0, st, X, X2, DZ, DZ2,
+                 partial, P2, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+  } else {
+    if (s.taps == 9)
+      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 9>), grid, dim3(256), 0, st, X, X2, DZ, DZ2,
+                 partial, P2, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+    else
+      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 1>), grid, dim3(256), 0, st, X, X2, DZ, DZ2,
+                 partial, P2, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+  }
+  return hipGetLastError();
+}
+
+hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
+                           const ConvShape& s, hipStream_t st, const ReduceJob* extra,
+                           ReduceJob* defer) {
+  if (use_wgrad_rows(s)) return conv_wgrad_rows_launch(x, dz, dw, partial, s, st, extra, defer);
+  long E = (long)s.cout * s.taps * s.cin;
+  WgradPlan pl;
+  float* unused = nullptr;
+  hipError_t e = launch_wgrad_mfma(x, nullptr, dz, nullptr, dw, nullptr, partial, unused, s, pl, st);
   if (e != hipSuccess) return e;
   if (defer) {
     *defer = ReduceJob{partial, dw, E, pl.S};   // partial == dw when S == 1
@@ -1515,9 +1542,13 @@ hipError_t conv_wgrad_mfma2(const void* x0, const void* x1, const void* dz0, con
   if (use_wgrad_rows(s))
     return conv_wgrad_rows_launch2(x0, x1, dz0, dz1, dw0, dw1, part0, part1, s, st, defer0,
                                    defer1);
-  hipError_t e = conv_wgrad_mfma(x0, dz0, dw0, part0, s, st, nullptr, defer0);
+  WgradPlan pl;
+  hipError_t e = launch_wgrad_mfma(x0, x1, dz0, dz1, dw0, dw1, part0, part1, s, pl, st);
   if (e != hipSuccess) return e;
-  return conv_wgrad_mfma(x1, dz1, dw1, part1, s, st, nullptr, defer1);
+  const long E = (long)s.cout * s.taps * s.cin;
+  *defer0 = ReduceJob{part0, dw0, E, pl.S};   // partial == dw when S == 1
+  *defer1 = ReduceJob{part1, dw1, E, pl.S};
+  return hipSuccess;
 }
 
 }  // namespace tgpk
