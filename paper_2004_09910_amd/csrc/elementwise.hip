@@ -1156,9 +1156,9 @@ hipError_t dw_wgrad2(const void* x0, const void* x1, const void* dz0, const void
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = splitk_reduce_launch(part0, dw0, E, S, st);
-  if (e != hipSuccess || n == 1) return e;
-  return splitk_reduce_launch(part1, dw1, E, S, st);
+  if (n == 1) return splitk_reduce_launch(part0, dw0, E, S, st);
+  const ReduceJob second{part1, dw1, E, S};   // both sums in one launch
+  return splitk_reduce_launch(part0, dw0, E, S, st, &second);
 }
 
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
