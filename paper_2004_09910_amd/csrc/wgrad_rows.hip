@@ -95,10 +95,15 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
   const int qw = wave & 3, kh = wave >> 2;      // quarter of the item, k-step phase
   const int cw = qw >> 1, nw = qw & 1;          // this wave's co / ci halves
   const int nct = Cout / 64, ncit = Cin / 64;
-  const int nrb = (H + R - 1) / R;
+  // R = 0: one K range per micro-batch spanning all nb samples' whole
+  // images (sample-major stages, each stage within one sample)
+  const bool merged = R == 0;
+  const int nrb = merged ? 1 : (H + R - 1) / R;
+  const int kpg = merged ? 1 : nb * nrb;          // K ranges per micro-batch
+  const int sps = (H + RPS - 1) / RPS;            // stages per sample image (merged)
   const int per_k = 3 * nct * ncit;             // items per K range
   const int ng = X2 ? 2 : 1;                    // micro-batches
-  const int items = ng * nb * nrb * per_k;
+  const int items = ng * kpg * per_k;
   const int G = gridDim.x;
   const int lb = xcd_remap(blockIdx.x, G);
   const int n_items = lb < items ? (items - lb + G - 1) / G : 0;
@@ -177,6 +182,7 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
     ci0 = (t % ncit) * 64;
   };
   auto stages_of = [&](int kr) __attribute__((always_inline)) {
+    if (merged) return nb * sps;
     const int rb = kr % nrb;
     const int rows = min(R, H - rb * R);
     return (rows + RPS - 1) / RPS;
@@ -189,11 +195,12 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
     i_ns = stages_of(i_kr);
   }
   auto issue = [&](int slot) __attribute__((always_inline)) {
-    const int ns_ = i_kr / nrb, rb = i_kr - ns_ * nrb;
-    const bool g1 = ns_ >= nb;                               // second micro-batch (uniform)
-    const int n = g1 ? ns_ - nb : ns_;
+    const bool g1 = i_kr >= kpg;                             // second micro-batch (uniform)
+    const int krl = g1 ? i_kr - kpg : i_kr;
+    const int n = merged ? i_st / sps : krl / nrb;
+    const int h = merged ? (i_st - (i_st / sps) * sps) * RPS
+                         : (krl - (krl / nrb) * nrb) * R + i_st * RPS;   // first image row
     const u32x4 rzg = g1 ? rz2 : rz, rxg = g1 ? rx2 : rx;
-    const int h = rb * R + i_st * RPS;                       // first image row of the stage
     const int zsoff = (((n * H + h) * W) * Cout + i_co0) * 2;
     const int hb = h + i_r - 1;                              // input row of stage row 0
     const int xsoff = (((n * H + hb) * W) * Cin + i_ci0) * 2;
@@ -308,8 +315,8 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
     // epilogue: element v of lane l is co 8 (v / 4) + 4 (l / 32) + v % 4, ci
     // l % 32 of this wave's quarter; with KS = 2 wave kh stores v = 8 kh ..
     // 8 kh + 7
-    const bool g1 = kr >= nb * nrb;
-    float* o = (g1 ? out2 : out) + (long)(g1 ? kr - nb * nrb : kr) * E;
+    const bool g1 = kr >= kpg;
+    float* o = (g1 ? out2 : out) + (long)(g1 ? kr - kpg : kr) * E;
     const int ci = ci0 + nw * 32 + (lane & 31);
     auto store = [&](int v0, int v1) __attribute__((always_inline)) {
 #pragma unroll
@@ -326,7 +333,7 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
   }
 }
 
-struct WgPlan { int R, nK; };
+struct WgPlan { int R, nK; };   // image rows per K range (0: whole micro-batch), K ranges
 
 }  // namespace
 
@@ -359,6 +366,10 @@ static WgPlan wgrad_rows_plan(const ConvShape& s) {
   const long cap = s.nb >= 4 ? 128 : 256;
   while (R < s.H && (long)s.nb * ((s.H + R - 1) / R) * per_k > cap) R += rps;
   if (R > s.H) R = s.H;
+  // Deep layers whose items fill the chip even with one K range per
+  // micro-batch: let it span all samples (R = 0), so the kernel writes the
+  // gradient itself and no partial slices are written or summed.
+  if (R == s.H && s.nb > 1 && per_k >= 128) return {0, 1};
   return {R, s.nb * ((s.H + R - 1) / R)};
 }
 

@@ -65,10 +65,13 @@ def test_conv3x3(cin, cout, h, w, B, m):
 
 
 @pytest.mark.parametrize("cin,cout,h,w", [(64, 64, 3, 256), (64, 128, 5, 128), (64, 64, 7, 64),
-                                          (128, 64, 9, 32), (64, 64, 11, 16), (128, 128, 9, 8)])
+                                          (128, 64, 9, 32), (64, 64, 11, 16), (128, 128, 9, 8),
+                                          (512, 512, 5, 8), (512, 512, 7, 32)])
 def test_wgrad_rows_other_widths(cin, cout, h, w):
     """The row-blocked weight gradient at the 6-level U-Net's widths 256 ...
-    8 (stages of one to eight image rows), with a ragged last row block."""
+    8 (stages of one to eight image rows), with a ragged last row block; the
+    two 512-channel cases take one K range over both samples of the
+    micro-batch (no partial slices)."""
     net = one_layer(Layer(CONV3X3, cin, cout), h, w)
     run_and_check(net, (1,), 1, BF16, 2, 1, f"wgrad rows {cin}->{cout} @{h}x{w}")
 
