@@ -354,6 +354,8 @@ constexpr R32Cfg kR32Cfgs[] = {
     {192, 2, 3, 3, 1, 4}, {192, 3, 5, 2, 1, 4},
     // widths 64 and 32 (the 6-level U-Net's deeper levels)
     {64, 4, 2, 4, 1, 0}, {64, 6, 3, 3, 2, 0}, {32, 8, 2, 4, 1, 0}, {32, 12, 3, 3, 2, 0},
+    // eight waves, twelve whole fragments per tile
+    {48, 8, 3, 3, 1, 0}, {96, 4, 3, 3, 1, 0},
 };
 constexpr int kR32N = sizeof(kR32Cfgs) / sizeof(kR32Cfgs[0]);
 
@@ -443,7 +445,7 @@ hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, voi
     R32_CASE(0) R32_CASE(1) R32_CASE(2) R32_CASE(3) R32_CASE(4) R32_CASE(5)
     R32_CASE(6) R32_CASE(7) R32_CASE(8) R32_CASE(9) R32_CASE(10) R32_CASE(11)
     R32_CASE(12) R32_CASE(13) R32_CASE(14) R32_CASE(15) R32_CASE(16) R32_CASE(17)
-    R32_CASE(18) R32_CASE(19) R32_CASE(20) R32_CASE(21)
+    R32_CASE(18) R32_CASE(19) R32_CASE(20) R32_CASE(21) R32_CASE(22) R32_CASE(23)
 #undef R32_CASE
     default: return hipErrorInvalidValue;
   }

@@ -82,7 +82,9 @@ ROWS32 = [(0, 192, 3), (1, 192, 1), (2, 96, 6), (3, 96, 3), (4, 96, 2), (5, 48, 
           # eight-wave layouts
           (11, 192, 3), (12, 96, 3), (13, 96, 2), (14, 48, 4), (15, 24, 8),
           # widths 64 and 32
-          (18, 64, 4), (19, 64, 6), (20, 32, 8), (21, 32, 12)]
+          (18, 64, 4), (19, 64, 6), (20, 32, 8), (21, 32, 12),
+          # eight waves, twelve fragments
+          (22, 48, 8), (23, 96, 4)]
 
 
 @pytest.mark.parametrize("cfg,w,r", ROWS32)
