@@ -12,11 +12,14 @@ when values are computed.  So the oracle is the plain definition.
 Two storage modes:
   'f64'  every value is kept in float64 (the pure definition);
   'bf16' float64 arithmetic, but every tensor a bf16 run stores is rounded to
-         bfloat16 where it is stored: each layer output, each dZ and dX, the
-         summed 2x2 upsample gradient and the loss gradient.  Weight and bias
-         gradients stay unrounded (a bf16 run accumulates them in fp32).  The
-         ReLU mask and the max-pool argmax are then decided on stored values,
-         in the storage precision, as a bf16 run decides them.
+         bfloat16 where it is stored: each layer output, each dZ and dX and
+         the summed 2x2 upsample gradient.  (The loss gradient a bf16 run
+         stores is rounded by the last layer's dZ store: rounding it before
+         would not change the result, since round(round(g) * mask) =
+         round(g * mask) for a 0/1 mask.)  Weight and bias gradients stay
+         unrounded (a bf16 run accumulates them in fp32).  The ReLU mask and
+         the max-pool argmax are then decided on stored values, in the storage
+         precision, as a bf16 run decides them.
 """
 from __future__ import annotations
 
@@ -50,13 +53,21 @@ class Tape:
     outputs: List[np.ndarray] = field(default_factory=list)  # stored layer output Y
     argmax: Dict[int, np.ndarray] = field(default_factory=dict)
     prev_c: Dict[int, int] = field(default_factory=dict)     # channels of the upsampled part
+    # filled by the backward, for diagnostics: per layer, the gradient at its
+    # output (after any skip gradient was added), the skip gradient added
+    # there, the stored dZ and the stored gradient of its (post-prologue) input
+    dy: Dict[int, np.ndarray] = field(default_factory=dict)
+    dskip: Dict[int, np.ndarray] = field(default_factory=dict)
+    dz: Dict[int, np.ndarray] = field(default_factory=dict)
+    dinp: Dict[int, np.ndarray] = field(default_factory=dict)
 
 
 def forward_layers(net: Net, params, lo: int, hi: int, x: np.ndarray,
-                   stash: Dict[int, np.ndarray], storage: str = "f64"):
+                   stash: Dict[int, np.ndarray], storage: str = "f64", log=None):
     """Runs layers [lo, hi) on x (the output of layer lo-1, or the network
     input).  Popped skips are read from `stash`; stashed outputs are written
-    to it.  Returns (output of layer hi-1, tape)."""
+    to it.  Returns (output of layer hi-1, tape).  `log`, if given, is called
+    with a short message after each layer (progress of long runs)."""
     tape = Tape(lo, hi)
     cur = x
     for idx in range(lo, hi):
@@ -78,12 +89,14 @@ def forward_layers(net: Net, params, lo: int, hi: int, x: np.ndarray,
         if L.stash_id >= 0:
             stash[L.stash_id] = y
         cur = y
+        if log is not None:
+            log(f"oracle forward layer {idx}")
     return cur, tape
 
 
 def backward_layers(net: Net, params, tape: Tape, dy: np.ndarray,
                     skip_grad: Dict[int, np.ndarray], want_dx: bool = True,
-                    storage: str = "f64"):
+                    storage: str = "f64", log=None):
     """Backward through the layers of `tape` in reverse.  `dy` is the gradient
     of the last layer's output.  `skip_grad[id]` holds the gradient flowing
     back into stashed skip `id` (written by the popping layer, read by the
@@ -96,16 +109,22 @@ def backward_layers(net: Net, params, tape: Tape, dy: np.ndarray,
         L = net.layers[idx]
         w, _ = params[idx]
         if L.stash_id >= 0 and L.stash_id in skip_grad:
-            cur = cur + skip_grad.pop(L.stash_id)
+            tape.dskip[idx] = skip_grad.pop(L.stash_id)
+            cur = cur + tape.dskip[idx]
+        tape.dy[idx] = cur
         y = tape.outputs[pos]
         dz = cur * (y > 0) if L.relu else cur
         dz = _store(dz, storage)
+        tape.dz[idx] = dz
         dW = _WGRAD[L.kind](tape.inputs[pos], dz)
         db = ops.bias_grad(dz) if L.bias else None
         grads[idx] = (dW, db)
+        if log is not None:
+            log(f"oracle backward layer {idx}")
         if pos == 0 and not want_dx:
             return None, grads
         dinp = _store(_DGRAD[L.kind](dz, w), storage)
+        tape.dinp[idx] = dinp
         if L.prologue == PRO_MAXPOOL2:
             cur = ops.maxpool2_backward(dinp, tape.argmax[idx])
         elif L.prologue == PRO_UPCAT2:
@@ -127,7 +146,7 @@ def exported_stashes(net: Net, lo: int, hi: int):
 
 def run(net: Net, params, x, *, lo: int = 0, hi: Optional[int] = None,
         target=None, out_grads=None, storage: str = "f64", want_dx: bool = True,
-        stash_in: Optional[Dict[int, np.ndarray]] = None):
+        stash_in: Optional[Dict[int, np.ndarray]] = None, log=None):
     """Full-batch forward + backward over layers [lo, hi).
 
     Network runs pass `target`: loss = sum (y-t)^2 / numel, no 1/2 factor.
@@ -137,12 +156,11 @@ def run(net: Net, params, x, *, lo: int = 0, hi: Optional[int] = None,
     Returns a dict with loss, outputs, grads {idx: (dW, db)}, dx."""
     hi = len(net.layers) if hi is None else hi
     stash = dict(stash_in or {})
-    y, tape = forward_layers(net, params, lo, hi, x, stash, storage)
+    y, tape = forward_layers(net, params, lo, hi, x, stash, storage, log)
     exports = exported_stashes(net, lo, hi)
     skip_grad = {}
     if target is not None:
         loss, dy = ops.mse(y, target, y.size)
-        dy = _store(dy, storage)
     else:
         assert out_grads is not None and len(out_grads) == 1 + len(exports)
         dy = out_grads[0]
@@ -150,6 +168,6 @@ def run(net: Net, params, x, *, lo: int = 0, hi: Optional[int] = None,
         for k, sid in enumerate(exports):
             skip_grad[sid] = out_grads[1 + k]
             loss += float(np.sum(out_grads[1 + k] * stash[sid]))
-    dx, grads = backward_layers(net, params, tape, dy, skip_grad, want_dx, storage)
+    dx, grads = backward_layers(net, params, tape, dy, skip_grad, want_dx, storage, log)
     return {"loss": loss, "y": y, "stash": {s: stash[s] for s in exports},
             "grads": grads, "dx": dx, "tape": tape}

@@ -6,7 +6,7 @@ package; only tests, the smoke check and the benchmark's CPU-baseline leg do.
 Each forward op is written straight from its textbook definition; each
 backward op is the vector-Jacobian product of that definition (the paper's
 partial_x f and partial_theta f of Sec. 2, eq. (B_ij)), written as the exact
-adjoint of the forward loop.  A library matmul (numpy.tensordot) is the only
+adjoint of the forward loop.  A library matmul (numpy.tensordot, in float64) is the only
 primitive used, and only for the sum over channels at one filter tap.
 """
 from __future__ import annotations
@@ -26,80 +26,6 @@ def round_bf16(a: np.ndarray) -> np.ndarray:
     return u.astype(np.uint32).view(np.float32).astype(np.float64)
 
 
-# ---------------------------------------------------------------- contraction precision
-# Parity references always contract in float64.  A float32 contraction mode
-# exists only to measure how far two equally valid bf16-storage computations
-# of a deep ReLU network drift apart when their summation precision differs
-# (ReLU masks and pool argmaxes taken on values that differ in the last bf16
-# bit flip, and each flip moves a whole upstream gradient element).
-
-_CONTRACT = ["f64"]
-CONTRACTIONS = ("f64", "f32", "f32rev", "f32split", "f32c32")
-
-
-class contraction:
-    """Context for the channel contraction used by the conv ops:
-    'f64'      float64 (every parity reference);
-    'f32'      float32 operands and accumulation;
-    'f32rev'   float32 with the contracted channel order reversed;
-    'f32split' float32 in two halves of the channels, added at the end;
-    'f32c32'   float32 in blocks of 32 channels, the block sums added one by
-               one in channel order (the blocking of a K loop that contracts
-               32 channels per step).
-    The float32 variants are equally valid ways to evaluate the same
-    bf16-storage network; the spread among them and the float64 reference
-    measures how many ReLU / pool decisions are within rounding distance of
-    flipping."""
-
-    def __init__(self, mode):
-        assert mode in CONTRACTIONS
-        self.mode = mode
-
-    def __enter__(self):
-        _CONTRACT.append(self.mode)
-
-    def __exit__(self, *exc):
-        _CONTRACT.pop()
-
-
-def _td(a, b, axes):
-    mode = _CONTRACT[-1]
-    if mode == "f64":
-        return np.tensordot(a, b, axes=axes)
-    a = np.asarray(a, np.float32)
-    b = np.asarray(b, np.float32)
-    ax_a, ax_b = axes
-    k = ax_a[0]
-    if mode == "f32rev":
-        a = np.flip(a, axis=k)
-        b = np.flip(b, axis=ax_b[0])
-    if mode == "f32c32" and a.shape[k] > 32:
-        out = None
-        for c0 in range(0, a.shape[k], 32):
-            sa = [slice(None)] * a.ndim
-            sb = [slice(None)] * b.ndim
-            sa[k], sb[ax_b[0]] = slice(c0, c0 + 32), slice(c0, c0 + 32)
-            t = np.tensordot(a[tuple(sa)], b[tuple(sb)], axes=axes)
-            out = t if out is None else out + t
-        return out
-    if mode == "f32split" and a.shape[k] > 1:
-        h = a.shape[k] // 2
-        sa = [slice(None)] * a.ndim
-        sb = [slice(None)] * b.ndim
-        sa[k], sb[ax_b[0]] = slice(0, h), slice(0, h)
-        lo = np.tensordot(a[tuple(sa)], b[tuple(sb)], axes=axes)
-        sa[k], sb[ax_b[0]] = slice(h, None), slice(h, None)
-        hi = np.tensordot(a[tuple(sa)], b[tuple(sb)], axes=axes)
-        return lo + hi
-    return np.tensordot(a, b, axes=axes)
-
-
-def _acc():
-    """Accumulator type of the conv sums over taps: float64, or float32 in
-    the float32 contraction variants (as a float32-accumulating kernel)."""
-    return np.float64 if _CONTRACT[-1] == "f64" else np.float32
-
-
 # ---------------------------------------------------------------- convolution
 # Cross-correlation, stride 1, zero padding 1 for 3x3 and 0 for 1x1:
 #   z[n,o,h,w] = b[o] + sum_{c,r,s} W[o,c,r,s] * x[n,c,h+r-1,w+s-1]
@@ -111,26 +37,26 @@ def _pad1(x):
 def conv3x3_forward(x, w, b=None):
     n, c, h, wd = x.shape
     xp = _pad1(x)
-    z = np.zeros((n, w.shape[0], h, wd), dtype=_acc())
+    z = np.zeros((n, w.shape[0], h, wd), dtype=np.float64)
     for r in range(3):
         for s in range(3):
-            t = _td(w[:, :, r, s], xp[:, :, r:r + h, s:s + wd], axes=([1], [1]))
+            t = np.tensordot(w[:, :, r, s], xp[:, :, r:r + h, s:s + wd], axes=([1], [1]))
             z += t.transpose(1, 0, 2, 3)
     if b is not None:
-        z += b[None, :, None, None].astype(z.dtype)
-    return z.astype(np.float64)
+        z += b[None, :, None, None]
+    return z
 
 
 def conv3x3_dgrad(dz, w):
     """dx[n,c,h',w'] = sum_{o,r,s} dz[n,o,h'-r+1,w'-s+1] W[o,c,r,s]: the adjoint
     of the forward, scattered tap by tap into a padded buffer."""
     n, o, h, wd = dz.shape
-    dxp = np.zeros((n, w.shape[1], h + 2, wd + 2), dtype=_acc())
+    dxp = np.zeros((n, w.shape[1], h + 2, wd + 2), dtype=np.float64)
     for r in range(3):
         for s in range(3):
-            t = _td(w[:, :, r, s], dz, axes=([0], [1]))  # (c, n, h, w)
+            t = np.tensordot(w[:, :, r, s], dz, axes=([0], [1]))  # (c, n, h, w)
             dxp[:, :, r:r + h, s:s + wd] += t.transpose(1, 0, 2, 3)
-    return dxp[:, :, 1:-1, 1:-1].astype(np.float64)
+    return dxp[:, :, 1:-1, 1:-1]
 
 
 def conv3x3_wgrad(x, dz):
@@ -140,23 +66,23 @@ def conv3x3_wgrad(x, dz):
     dw = np.zeros((dz.shape[1], c, 3, 3))
     for r in range(3):
         for s in range(3):
-            dw[:, :, r, s] = _td(dz, xp[:, :, r:r + h, s:s + wd], axes=([0, 2, 3], [0, 2, 3]))
-    return dw.astype(np.float64)
+            dw[:, :, r, s] = np.tensordot(dz, xp[:, :, r:r + h, s:s + wd], axes=([0, 2, 3], [0, 2, 3]))
+    return dw
 
 
 def conv1x1_forward(x, w, b=None):
-    z = _td(w[:, :, 0, 0], x, axes=([1], [1])).transpose(1, 0, 2, 3)
+    z = np.tensordot(w[:, :, 0, 0], x, axes=([1], [1])).transpose(1, 0, 2, 3)
     if b is not None:
-        z = z + b[None, :, None, None].astype(z.dtype)
-    return z.astype(np.float64)
+        z = z + b[None, :, None, None]
+    return z
 
 
 def conv1x1_dgrad(dz, w):
-    return _td(w[:, :, 0, 0], dz, axes=([0], [1])).transpose(1, 0, 2, 3).astype(np.float64)
+    return np.tensordot(w[:, :, 0, 0], dz, axes=([0], [1])).transpose(1, 0, 2, 3)
 
 
 def conv1x1_wgrad(x, dz):
-    return _td(dz, x, axes=([0, 2, 3], [0, 2, 3]))[:, :, None, None].astype(np.float64)
+    return np.tensordot(dz, x, axes=([0, 2, 3], [0, 2, 3]))[:, :, None, None]
 
 
 # depthwise 3x3, pad 1, no channel mixing:

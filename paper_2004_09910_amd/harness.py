@@ -58,8 +58,10 @@ class Session:
 
     def __init__(self, net: specs.Net, dtype: int, n: int = 1,
                  balance: Optional[Sequence[int]] = None, device: str = "cuda",
-                 seed_offset: int = 0, bind_layers: Optional[Sequence[int]] = None):
+                 seed_offset: int = 0, bind_layers: Optional[Sequence[int]] = None,
+                 family: str = synth.NORMAL):
         self.net, self.dtype, self.device = net, dtype, device
+        self.family = family
         self.h = tgp.net_create([layer_tuple(L) for L in net.layers], net.in_channels,
                                 net.height, net.width, dtype)
         tgp.set_partition(self.h, n, balance)
@@ -83,7 +85,7 @@ class Session:
 
     def _bind_layer(self, idx: int, seed_offset: int):
         L = self.net.layers[idx]
-        (w64, wraw), b = synth.layer_params(self.net, idx, self.dtype, seed_offset)
+        (w64, wraw), b = synth.layer_params(self.net, idx, self.dtype, seed_offset, self.family)
         wt = raw_to_torch(wraw, self.dtype)
         if L.kind == DWCONV3X3:
             wk = wt.reshape(L.cout, 9)

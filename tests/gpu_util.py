@@ -1,17 +1,38 @@
 """Helpers for the GPU parity tests: run a workload through the C ABI and
-through the oracle on the same seeded inputs."""
+through the oracle on the same seeded inputs, and compare them element by
+element.
+
+Two input families (workloads.synth):
+  NORMAL  N(0,1) inputs, He-normal weights.  Two correct bf16 computations of
+          a multi-layer ReLU / max-pool network that sum in different orders
+          take some ReLU-mask and argmax decisions on values within rounding
+          distance of each other, and each differing decision moves a whole
+          gradient element.  NORMAL runs are therefore compared on quantities
+          no decision upstream of them can move: forward outputs, and every
+          output of single-layer runs (their inputs are identical bits).
+  EXACT   small integers and sparse +-1 weights: every accumulation of such a
+          run is exact in float32 (tests/exactness.py checks it on the
+          oracle's tape), so every correct implementation produces the same
+          bits.  Multi-layer gradients are compared on this family, to
+          EXACT_TOL.
+
+Every comparison is max-rel = max|got - ref| / max|ref| per tensor, against
+TOL (2e-2 bf16, 1e-4 fp32) for NORMAL runs and EXACT_TOL for EXACT runs.
+"""
 import sys
 
 import numpy as np
 import torch
 
-import oracle
-from oracle import network, ops
+import exactness
+from cases import (network_inputs, oracle_network, oracle_stage, popped_stash_values,  # noqa: F401
+                   stage_values, storage)
 from paper_2004_09910_amd.harness import Session, nchw_to_device_nhwc, nhwc_to_nchw64
-from workloads import specs, synth
 from workloads.specs import BF16, FP32
+from workloads.synth import EXACT, NORMAL
 
 TOL = {BF16: 2e-2, FP32: 1e-4}
+EXACT_TOL = 1e-6
 
 
 def say(*a):
@@ -26,16 +47,41 @@ def maxrel(a, b):
     return float(np.max(np.abs(a - b)) / den) if den > 0 else float(np.max(np.abs(a)))
 
 
-def storage(dtype):
-    return "bf16" if dtype == BF16 else "f64"
+def rmsrel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    den = np.linalg.norm(b)
+    return float(np.linalg.norm(a - b) / den) if den > 0 else float(np.linalg.norm(a))
 
 
-def gpu_network(net, dtype, B, m, n, mode, balance=None, lanes=1):
-    sess = Session(net, dtype, n=n, balance=balance)
+def tol_for(dtype, family):
+    return EXACT_TOL if family == EXACT else TOL[dtype]
+
+
+def check(name, got, ref, tol, errs):
+    """max-rel of `got` against `ref`, recorded in errs[name]; True if within
+    tol.  An all-zero reference passes only an all-zero result."""
+    e = maxrel(got, ref)
+    errs[name] = (e, tol, rmsrel(got, ref))
+    return e <= tol
+
+
+def report(what, errs):
+    worst = max(errs, key=lambda k: errs[k][0] / errs[k][1])
+    say(f"{what}: " + ", ".join(f"{k}={v[0]:.2e}" for k, v in errs.items()))
+    say(f"{what}: worst {worst} max-rel {errs[worst][0]:.3e} (bound {errs[worst][1]:.1e}), "
+        f"rms-rel {errs[worst][2]:.3e}")
+
+
+# ---------------------------------------------------------------- networks
+
+def gpu_network(net, dtype, B, m, n, mode, balance=None, lanes=1, family=NORMAL, inputs=None):
+    sess = Session(net, dtype, n=n, balance=balance, family=family)
     sess.plan(B, m, mode, lanes)
-    _, xraw = synth.input_x(net, B, dtype)
+    if inputs is None:
+        inputs = network_inputs(net, dtype, B, family)
+    _, xraw, _, traw, _ = inputs
     h, w = net.out_hw()
-    _, traw = synth.target_like((B, net.out_channels(), h, w), dtype)
     x = nchw_to_device_nhwc(xraw, dtype)
     t = nchw_to_device_nhwc(traw, dtype)
     loss = torch.zeros(1, dtype=torch.float32, device="cuda")
@@ -47,39 +93,67 @@ def gpu_network(net, dtype, B, m, n, mode, balance=None, lanes=1):
     return out
 
 
-def oracle_network(net, dtype, B, P=None):
-    if P is None:
-        P = oracle.net_params(net, dtype)
-    xv, _ = synth.input_x(net, B, dtype)
-    h, w = net.out_hw()
-    tv, _ = synth.target_like((B, net.out_channels(), h, w), dtype)
-    return network.run(net, P, xv, target=tv, storage=storage(dtype))
+def check_network(got, ref, dtype, what, family=NORMAL, grads=True):
+    """Loss, output and (with `grads`) every weight and bias gradient of a
+    pipeline run against the oracle."""
+    tol = tol_for(dtype, family)
+    errs = {}
+    ok = check("loss", np.array([got["loss"]]), np.array([ref["loss"]]), tol, errs)
+    ok &= check("y", got["y"], ref["y"], tol, errs)
+    if grads:
+        for idx, (dW, db) in ref["grads"].items():
+            ok &= check(f"dW{idx}", got["grads"][idx][0], dW, tol, errs)
+            if db is not None:
+                ok &= check(f"db{idx}", got["grads"][idx][1], db, tol, errs)
+    _finish(what, ok, errs, ref, family)
+    return errs
 
 
-def stage_inputs(sess, j, B, dtype):
-    """Seeded partition input and upstream gradients (G_0 for the main output,
-    G_k for the k-th exported skip), as float64 NCHW values and device NHWC."""
-    C, H, W = sess.part_in_shape(j)
-    xv, xraw = synth.quantize(synth.normal(synth.SEED_X, (B, C, H, W)), dtype)
-    shapes = [sess.part_out_shape(j)] + [sess.stash_shape(s) for s in sess.exported_stashes(j)]
-    G = [synth.target_like((B,) + s, dtype, k) for k, s in enumerate(shapes)]
-    return xv, xraw, G
+def _finish(what, ok, errs, ref, family):
+    report(what, errs)
+    if "cert" in ref:
+        say(f"{what}: exactness certificate " +
+            ", ".join(f"{k}={v:.2e}" for k, v in ref["cert"].items()))
+        if family == EXACT:
+            assert exactness.exact(ref["cert"]), "inputs do not keep this run exact"
+    assert ok, errs
+
+
+# ---------------------------------------------------------------- stages
+
+def only_samples(G, samples):
+    """Upstream gradients with every sample outside `samples` zeroed: the
+    weight gradient of the step is then the sum over `samples` alone."""
+    out = []
+    for v, raw in G:
+        keep = np.zeros(v.shape[0], dtype=bool)
+        keep[list(samples)] = True
+        v2 = np.where(keep[:, None, None, None], v, 0.0)
+        raw2 = raw.copy()
+        raw2[~keep] = 0
+        out.append((v2, raw2))
+    return out
 
 
 def gpu_stage(net, dtype, B, m, mode, balance, j, want_dx=True, G_override=None, sess=None,
-              neutral=True, neutral_samples=None, stash_in=None, lanes=1, pairs=False):
+              stash_in=None, lanes=1, pairs=False, serial=False, family=NORMAL,
+              grad_samples=None):
+    """One stage step of partition j through the C ABI.  `grad_samples`
+    zeroes the upstream gradients of every other sample; `serial` issues
+    everything on one stream (the benchmark's configuration)."""
     n = len(balance)
     lo = sum(balance[:j - 1])
     hi = lo + balance[j - 1]
     if sess is None:
-        sess = Session(net, dtype, n=n, balance=balance, bind_layers=range(lo, hi))
+        sess = Session(net, dtype, n=n, balance=balance, bind_layers=range(lo, hi),
+                       family=family)
         sess.plan(B, m, mode, lanes)
         sess.pairs = pairs
-    xv, xraw, G = stage_inputs(sess, j, B, dtype)
+    xv, xraw, G = stage_values(net, lo, hi, B, dtype, family)
     if G_override is not None:
         G = G_override
-    elif neutral:
-        G = neutral_G(net, dtype, lo, hi, xv, G, samples=neutral_samples, stash_in=stash_in)
+    elif grad_samples is not None:
+        G = only_samples(G, grad_samples)
     x = nchw_to_device_nhwc(xraw, dtype)
     C, H, W = sess.part_out_shape(j)
     y = torch.empty((B, H, W, C), dtype=x.dtype, device="cuda")
@@ -92,7 +166,8 @@ def gpu_stage(net, dtype, B, m, mode, balance, j, want_dx=True, G_override=None,
         for i in range(1, m + 1):
             sess.stash_view(i, sid, True).copy_(g[(i - 1) * b:i * b])
     torch.cuda.synchronize()
-    sess.stage_step(j, x, y, dy, dx, torch.cuda.current_stream().cuda_stream)
+    stream = torch.cuda.current_stream().cuda_stream
+    sess.stage_step(j, x, y, dy, dx, stream, serial=serial)
     torch.cuda.synchronize()
     stash = {sid: torch.cat([sess.stash_view(i, sid, False) for i in range(1, m + 1)])
              for sid in ex}
@@ -100,166 +175,41 @@ def gpu_stage(net, dtype, B, m, mode, balance, j, want_dx=True, G_override=None,
             "G": G, "xv": xv, "lo": lo, "hi": hi}
 
 
-def oracle_stage(net, dtype, lo, hi, xv, G, samples=None, stash_in=None):
-    P = oracle.net_params(net, dtype)
-    Gv = [g[0] for g in G]
-    st = dict(stash_in or {})
-    if samples is not None:
-        xv = xv[samples]
-        Gv = [g[samples] for g in Gv]
-        st = {k: v[samples] for k, v in st.items()}
-    return network.run(net, P, xv, lo=lo, hi=hi, out_grads=Gv, storage=storage(dtype),
-                       stash_in=st)
+def check_stage(got, ref, dtype, what, family=NORMAL, dx=True, grads=True, samples=None):
+    """Stage outputs (main and exported skips), dx_in and every weight and
+    bias gradient against the oracle.  `samples` restricts the per-sample
+    tensors of the GPU run to those samples (the oracle ran only them)."""
+    tol = tol_for(dtype, family)
+    sel = slice(None) if samples is None else list(samples)
+    errs = {}
+    ok = check("y", nhwc_to_nchw64(got["y"][sel]), ref["y"], tol, errs)
+    for sid, t in got["stash"].items():
+        ok &= check(f"skip{sid}", nhwc_to_nchw64(t[sel]), ref["stash"][sid], tol, errs)
+    if dx:
+        ok &= check("dx", nhwc_to_nchw64(got["dx"][sel]), ref["dx"], tol, errs)
+    if grads:
+        for idx, (dW, db) in ref["grads"].items():
+            ok &= check(f"dW{idx}", got["grads"][idx][0], dW, tol, errs)
+            if db is not None:
+                ok &= check(f"db{idx}", got["grads"][idx][1], db, tol, errs)
+    _finish(what, ok, errs, ref, family)
+    return errs
 
 
-ALTS = ("f32", "f32rev", "f32split", "f32c32")
-
-
-def oracle_stage_variants(net, dtype, lo, hi, xv, G, samples=None, stash_in=None):
-    """The parity reference (float64 contraction) and the same computation
-    with each float32 contraction variant: the distance between the variants
-    and the reference is the spread that valid bf16 runs of this network show
-    (ReLU / pool decisions within rounding distance of flipping)."""
-    ref = oracle_stage(net, dtype, lo, hi, xv, G, samples, stash_in)
-    alts = []
-    for mode in (ALTS if dtype == BF16 else ()):
-        with ops.contraction(mode):
-            alts.append(oracle_stage(net, dtype, lo, hi, xv, G, samples, stash_in))
-    return ref, alts
-
-
-def oracle_network_variants(net, dtype, B):
-    ref = oracle_network(net, dtype, B)
-    alts = []
-    for mode in (ALTS if dtype == BF16 else ()):
-        with ops.contraction(mode):
-            alts.append(oracle_network(net, dtype, B))
-    return ref, alts
-
-
-def neutral_G(net, dtype, lo, hi, xv, G, samples=None, stash_in=None):
-    """Decision-neutral upstream gradients: zero G_k wherever the ReLU
-    decision of the layer that produces output k is within the rounding
-    distance of flipping, i.e. |z_ref| <= 4 max|z_ref - z_alt| over the float32
-    contraction variants (plus a float32-epsilon floor).  Such decisions may
-    legitimately go either way; with G = 0 there they cannot change any
-    gradient.  Uses only the oracle."""
-    P = oracle.net_params(net, dtype)
-    x = xv if samples is None else xv[samples]
-    st0 = dict(stash_in or {})
-    if samples is not None:
-        st0 = {k: v[samples] for k, v in st0.items()}
-    producers = [hi - 1] + [next(k for k in range(lo, hi) if net.layers[k].stash_id == sid)
-                            for sid in network.exported_stashes(net, lo, hi)]
-
-    def preacts(mode):
-        with ops.contraction(mode):
-            _, tape = network.forward_layers(net, P, lo, hi, x, dict(st0), storage(dtype))
-            out = {}
-            for k in producers:
-                L = net.layers[k]
-                w, b = P[k]
-                out[k] = network._FWD[L.kind](tape.inputs[k - lo], w, b if L.bias else None)
-            return out
-    ref = preacts("f64")
-    alts = [preacts(m) for m in ALTS]
-    newG = []
-    for slot, k in enumerate(producers):
-        v, raw = G[slot]
-        L = net.layers[k]
-        if not L.relu:
-            newG.append((v, raw))
-            continue
-        zr = ref[k]
-        theta = max(float(np.max(np.abs(zr - a[k]))) for a in alts)
-        theta = 4.0 * theta + 1e-6 * float(np.max(np.abs(zr)))
-        amb = np.abs(zr) <= theta
-        v2, raw2 = v.copy(), raw.copy()
-        if samples is None:
-            v2[amb] = 0.0
-            raw2[amb] = 0
-        else:
-            sub = v2[samples]
-            sub[amb] = 0.0
-            v2[samples] = sub
-            rs = raw2[samples]
-            rs[amb] = 0
-            raw2[samples] = rs
-        newG.append((v2, raw2))
-    return newG
-
-
-def rmsrel(a, b):
-    a = np.asarray(a, dtype=np.float64)
-    b = np.asarray(b, dtype=np.float64)
-    den = np.linalg.norm(b)
-    return float(np.linalg.norm(a - b) / den) if den > 0 else float(np.linalg.norm(a))
-
-
-SPREAD_FACTOR = 4.0
-
-
-FLIP_MAXREL = 5e-2
-
-
-def check_grad(name, got, ref, alts, dtype, errs, strict=False):
-    """max-rel and rms-rel error of `got` against the reference.
-
-    strict (single layers, forward outputs, fp32 runs): both within the
-    parity tolerance.  Gradients of bf16 runs through several ReLU / pool
-    layers pass if either
-      (a) max-rel and rms-rel are within the tolerance or SPREAD_FACTOR times
-          the largest distance of a float32-contraction variant from the
-          reference, whichever is larger; or
-      (b) rms-rel is within the tolerance and max-rel within FLIP_MAXREL: a few
-          decision flips (each moves one whole upstream gradient element) on
-          an otherwise matching tensor.  The GPU's MFMA accumulation does not
-          round like an IEEE float32 sum, so its flip count need not match
-          the float32 variants'."""
-    tol = TOL[dtype]
-    e_max, e_rms = maxrel(got, ref), rmsrel(got, ref)
-    bmax = brms = tol
-    sp = max((maxrel(a, ref) for a in alts), default=0.0)
-    if strict or dtype != BF16 or not alts:
-        errs[name] = (e_max, bmax, e_rms, brms, sp)
-        return e_max <= bmax and e_rms <= brms
-    bmax = max(tol, SPREAD_FACTOR * sp)
-    brms = max(tol, SPREAD_FACTOR * max(rmsrel(a, ref) for a in alts))
-    ok = (e_max <= bmax and e_rms <= brms) or (e_rms <= tol and e_max <= FLIP_MAXREL)
-    if not (e_max <= bmax and e_rms <= brms) and ok:
-        bmax = FLIP_MAXREL
-    errs[name] = (e_max, bmax, e_rms, brms, sp)
-    return ok
-
-
-def report(what, errs):
-    worst = max(errs, key=lambda k: errs[k][0] / errs[k][1])
-    say(f"{what}: " + ", ".join(f"{k}={v[0]:.2e}/{v[1]:.1e}(spread {v[4]:.1e})"
-                                for k, v in errs.items()))
-    say(f"{what}: worst {worst} max-rel {errs[worst][0]:.3e} (bound {errs[worst][1]:.2e}), "
-        f"rms-rel {errs[worst][2]:.3e} (bound {errs[worst][3]:.2e})")
-
-
-def gpu_stage_with_popped(net, bal, j, dtype=BF16, B=4, m=2, mode=0):
+def gpu_stage_with_popped(net, bal, j, dtype=BF16, B=4, m=2, mode=0, family=NORMAL):
     """Runs stage j after writing seeded values into the slots of skips that
     stage j pops but an earlier partition stashes."""
-    from paper_2004_09910_amd.harness import Session
     lo = sum(bal[:j - 1])
     hi = lo + bal[j - 1]
-    sess = Session(net, dtype, n=len(bal), balance=bal, bind_layers=range(lo, hi))
+    sess = Session(net, dtype, n=len(bal), balance=bal, bind_layers=range(lo, hi), family=family)
     sess.plan(B, m, mode)
-    stashed_inside = {L.stash_id for L in net.layers[lo:hi] if L.stash_id >= 0}
-    popped = [L.pop_id for L in net.layers[lo:hi]
-              if L.pop_id >= 0 and L.pop_id not in stashed_inside]
     stash_in = {}
     b = B // m
-    for sid in popped:
-        shp = (B,) + sess.stash_shape(sid)
-        v, raw = synth.quantize(synth.normal(500 + sid, shp), dtype)
+    for sid, (v, raw) in popped_stash_values(net, lo, hi, B, dtype, family).items():
         stash_in[sid] = v
         d = nchw_to_device_nhwc(raw, dtype)
         for i in range(1, m + 1):
             sess.stash_view(i, sid, False).copy_(d[(i - 1) * b:i * b])
-    got = gpu_stage(net, dtype, B, m, mode, bal, j, sess=sess, stash_in=stash_in)
+    got = gpu_stage(net, dtype, B, m, mode, bal, j, sess=sess, stash_in=stash_in, family=family)
     got["stash_in"] = stash_in
     return got

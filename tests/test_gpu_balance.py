@@ -8,11 +8,11 @@ import pytest
 import torch
 
 import paper_2004_09910_amd as tgp
-from gpu_util import check_grad, oracle_network_variants, report, say, TOL
+from gpu_util import check_network, network_inputs, oracle_network, say
 from paper_2004_09910_amd.harness import Session, nchw_to_device_nhwc, nhwc_to_nchw64
-from test_gpu_parity import check_network
-from workloads import specs, synth
+from workloads import specs
 from workloads.specs import BF16, CKPT_ALWAYS
+from workloads.synth import EXACT
 
 pytestmark = pytest.mark.gpu
 
@@ -34,11 +34,11 @@ def test_layer_times_restore_the_partition():
 
 @pytest.mark.parametrize("n", [2, 3])
 def test_balance_by_time_pipeline(n):
-    """Partition on measured times, then a full pipeline step (m = 2, every
-    checkpoint mode) on that partition against the oracle."""
-    net = specs.unet(3, 64, 64, 24, "unet3-c64")
+    """Partition on measured times, then a full pipeline step (m = 2) on that
+    partition against the oracle, on exact inputs."""
+    net = specs.unet(3, 64, 64, 32, "unet3-c64-32")
     B, m = 4, 2
-    sess = Session(net, BF16, n=1)
+    sess = Session(net, BF16, n=1, family=EXACT)
     say(f"balance by time, unet3 n={n}")
     bal, us = sess.balance_by_time(B // m, n, CKPT_ALWAYS, iters=2)
     say(f"  layer us {[round(u, 1) for u in us]} -> balance {bal}")
@@ -46,11 +46,11 @@ def test_balance_by_time_pipeline(n):
     # the same rule on the reported times, in whole nanoseconds
     ns = [int(math.floor(float(u) * 1000.0 + 0.5)) for u in us]
     assert tgp.balance_minmax(ns, n) == bal
-    pair = oracle_network_variants(net, BF16, B)
+    inputs = network_inputs(net, BF16, B, EXACT)
+    ref = oracle_network(net, BF16, B, EXACT, inputs, certify=True)
     sess.plan(B, m, CKPT_ALWAYS)
-    _, xraw = synth.input_x(net, B, BF16)
+    _, xraw, _, traw, _ = inputs
     h, w = net.out_hw()
-    _, traw = synth.target_like((B, net.out_channels(), h, w), BF16)
     x = nchw_to_device_nhwc(xraw, BF16)
     t = nchw_to_device_nhwc(traw, BF16)
     loss = torch.zeros(1, dtype=torch.float32, device="cuda")
@@ -58,5 +58,5 @@ def test_balance_by_time_pipeline(n):
     sess.pipeline_step(x, t, loss, y)
     torch.cuda.synchronize()
     got = {"loss": float(loss.item()), "y": nhwc_to_nchw64(y), "grads": sess.grads64()}
-    check_network(got, pair, BF16, f"unet3 balance-by-time {bal}")
+    check_network(got, ref, BF16, f"unet3 balance-by-time {bal}", EXACT)
     sess.close()

@@ -1,17 +1,18 @@
 """Single-layer parity: each kernel family through the C ABI, as a one-layer
 stage with an injected upstream gradient.  Both sides start from identical
-bf16 inputs, so no ReLU or pool decision can differ and every output (y, dx,
-dW, db) is held to the parity tolerance directly: 2e-2 max-rel for bf16,
-1e-4 for fp32.  Shapes include ragged pixel tiles and the benchmark's own
-level-0 and deepest layer shapes at its micro-batch size."""
+bf16 inputs, so only the layer's own output ReLU decides anything, and
+every output (y, dx, dW, db) is held to the parity tolerance: 2e-2 max-rel
+for bf16, 1e-4 for fp32, on N(0,1) inputs.  Stages of several layers in one
+partition take the EXACT input family in bf16 (1e-6).  Shapes include
+ragged pixel tiles and the benchmark's own level-0 and deepest layer shapes
+at its micro-batch size."""
 import pytest
 
-from gpu_util import (TOL, check_grad, gpu_stage, gpu_stage_with_popped, maxrel, oracle_stage,
-                      oracle_stage_variants, report, say)
-from paper_2004_09910_amd.harness import nhwc_to_nchw64
+from gpu_util import check_stage, gpu_stage, gpu_stage_with_popped, oracle_stage, say
 from workloads import specs
 from workloads.specs import (BF16, CONV1X1, CONV3X3, DWCONV3X3, FP32, PRO_MAXPOOL2,
                              PRO_UPCAT2, Layer, Net)
+from workloads.synth import EXACT, NORMAL
 
 pytestmark = pytest.mark.gpu
 
@@ -20,32 +21,17 @@ def one_layer(L, h, w, name="one"):
     return Net(name, (L,), L.cin, h, w)
 
 
-def run_and_check(net, bal, j, dtype, B, m, what, popped=False, variants=True):
-    """variants=False skips the float32-contraction oracle runs, which only
-    report a spread here (every check below is strict)."""
+def run_and_check(net, bal, j, dtype, B, m, what, popped=False, family=NORMAL):
     say(what)
     if popped:
-        got = gpu_stage_with_popped(net, bal, j, dtype=dtype, B=B, m=m)
+        got = gpu_stage_with_popped(net, bal, j, dtype=dtype, B=B, m=m, family=family)
     else:
-        got = gpu_stage(net, dtype, B, m, 0, bal, j)
-    if variants:
-        ref, alts = oracle_stage_variants(net, dtype, got["lo"], got["hi"], got["xv"], got["G"],
-                                          stash_in=got.get("stash_in"))
-    else:
-        ref = oracle_stage(net, dtype, got["lo"], got["hi"], got["xv"], got["G"],
-                           stash_in=got.get("stash_in"))
-        alts = []
-    errs = {}
-    ok = check_grad("y", nhwc_to_nchw64(got["y"]), ref["y"], [a["y"] for a in alts], dtype, errs, strict=True)
-    ok &= check_grad("dx", nhwc_to_nchw64(got["dx"]), ref["dx"], [a["dx"] for a in alts], dtype, errs, strict=True)
-    for idx, (dW, db) in ref["grads"].items():
-        ok &= check_grad(f"dW{idx}", got["grads"][idx][0], dW, [a["grads"][idx][0] for a in alts], dtype, errs,
-                         strict=True)
-        if db is not None:
-            ok &= check_grad(f"db{idx}", got["grads"][idx][1], db, [a["grads"][idx][1] for a in alts], dtype,
-                             errs, strict=True)
-    report(what, errs)
-    assert ok, errs
+        got = gpu_stage(net, dtype, B, m, 0, bal, j, family=family)
+    ref = oracle_stage(net, dtype, got["lo"], got["hi"], got["xv"], got["G"],
+                       stash_in=got.get("stash_in"), family=family,
+                       certify=(family == EXACT))
+    check_stage(got, ref, dtype, what, family)
+    got["sess"].close()
 
 
 @pytest.mark.parametrize("cin,cout,h,w,B,m", [
@@ -187,7 +173,8 @@ def test_pool_backward_inside_a_partition(dtype, c, bias):
                          Layer(CONV3X3, c, 2 * c, prologue=PRO_MAXPOOL2),
                          Layer(CONV3X3, 3 * c, c, prologue=PRO_UPCAT2, pop_id=0)), c, 16, 24)
     run_and_check(net, (3,), 1, dtype, 4, 2,
-                  f"pool inside a partition, {'bf16' if dtype == BF16 else 'fp32'} c={c} bias={bias}")
+                  f"pool inside a partition, {'bf16' if dtype == BF16 else 'fp32'} c={c} bias={bias}",
+                  family=EXACT if dtype == BF16 else NORMAL)
 
 
 def test_fp32_direct_conv():
@@ -219,5 +206,4 @@ def test_largest_layers_at_full_shape(cin, cout, h, B):
     at their real per-micro-batch shape: forward, data gradient, weight and
     bias gradient against the float64 oracle."""
     net = one_layer(Layer(CONV3X3, cin, cout), h, h)
-    run_and_check(net, (1,), 1, BF16, B, 1, f"full-shape layer {cin}->{cout} @{h}x{h} b={B}",
-                  variants=False)
+    run_and_check(net, (1,), 1, BF16, B, 1, f"full-shape layer {cin}->{cout} @{h}x{h} b={B}")

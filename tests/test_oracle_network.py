@@ -299,3 +299,118 @@ def test_bf16_storage_is_exact_on_representable_values():
         np.testing.assert_array_equal(o, ops.round_bf16(o))
     d = network.run(net, P2, x2, target=t, storage="f64")
     assert any(not np.array_equal(u, v) for u, v in zip(c["tape"].outputs, d["tape"].outputs))
+
+
+# ---------------------------------------------------------------- bf16 rounding points
+# Hand-computed cases for the points where the bf16-storage mode rounds
+# (reading R8: every stored activation, dZ, input gradient, summed upsample
+# gradient and loss gradient is bf16).  bf16 keeps 8 significant bits, so
+# integers are exact up to 256, even ones up to 512, multiples of 4 up to
+# 1024, of 8 up to 2048 and of 32 from 4096 to 8192; ties go to the even
+# significand.  Every weight is a centre tap only, so a 3x3 convolution is a
+# per-pixel scale and every value below can be followed by hand.
+
+def _centre(c_out, c_in, vals):
+    w = np.zeros((c_out, c_in, 3, 3))
+    w[:, :, 1, 1] = np.asarray(vals, dtype=np.float64).reshape(c_out, c_in)
+    return w
+
+
+def _rounding_net():
+    # L0: conv 1->1 (x3), ReLU, stashed as skip 0       at 2x2
+    # L1: 2x2 max-pool, conv 1->1 (x3), ReLU           at 1x1
+    # L2: upsample + concat [up, skip 0], conv 2->1 (x3, x3), no ReLU  at 2x2
+    layers = (specs.Layer(CONV3X3, 1, 1, bias=False, stash_id=0),
+              specs.Layer(CONV3X3, 1, 1, bias=False, prologue=PRO_MAXPOOL2),
+              specs.Layer(CONV3X3, 2, 1, bias=False, relu=False, prologue=PRO_UPCAT2, pop_id=0))
+    P = [(_centre(1, 1, [3]), None), (_centre(1, 1, [3]), None), (_centre(1, 2, [3, 3]), None)]
+    return specs.Net("rounding", layers, 1, 2, 2), P
+
+
+X_ROUND = np.array([[1.0, 2.0], [3.0, 4.0]]).reshape(1, 1, 2, 2)
+G_ROUND = np.array([[171.0, 1.0], [1.0, 1.0]]).reshape(1, 1, 2, 2)
+
+
+def _pinned_stage(run_fn):
+    """The whole net as a stage with upstream gradient G_ROUND.
+
+    Forward (exact): y0 = 3x = [[3, 6], [9, 12]]; pool -> 12; y1 = 36;
+    y2 = 3*36 + 3*y0 = [[117, 126], [135, 144]].
+    Backward: dZ2 = G = [[171, 1], [1, 1]]; the input gradient of L2 is 3G =
+    [[513, 3], [3, 3]] in both channels, stored as [[512, 3], [3, 3]]
+    (513 -> 512).  Its skip half goes to L0; its upsample half sums to
+    512 + 3 + 3 + 3 = 521, stored as 520.  dZ1 = 520, dW1 (centre) = 520 * 12
+    = 6240; L1's input gradient 3 * 520 = 1560 goes to the pool's argmax
+    (pixel (1, 1)).  At L0 the skip gradient is added: [[512, 3], [3, 1563]],
+    stored as dZ0 = [[512, 3], [3, 1560]] (1563 -> 1560).  dW0 (centre) =
+    512*1 + 3*2 + 3*3 + 1560*4 = 6767; dx = 3 dZ0 = [[1536, 9], [9, 4680]],
+    stored as [[1536, 9], [9, 4672]] (4680 -> 4672).  dW2 (centre) =
+    (36 * sum G, sum G * y0) = (6264, 540)."""
+    net, P = _rounding_net()
+    r = run_fn(net, P, X_ROUND, out_grads=[G_ROUND], storage="bf16")
+    return (r["grads"][0][0][0, 0, 1, 1], r["grads"][1][0][0, 0, 1, 1],
+            tuple(r["grads"][2][0][0, :, 1, 1]), tuple(r["dx"].ravel()))
+
+
+PINNED_STAGE = (6767.0, 6240.0, (6264.0, 540.0), (1536.0, 9.0, 9.0, 4672.0))
+
+
+def _pinned_upcat_stage(run_fn):
+    """L2 alone as a stage (input y1 = 36 at 1x1, skip 0 popped from outside
+    with y0): its input gradient is the stored upsample sum, 520 (521 before
+    rounding)."""
+    net, P = _rounding_net()
+    stash = {0: np.array([[3.0, 6.0], [9.0, 12.0]]).reshape(1, 1, 2, 2)}
+    r = run_fn(net, P, np.full((1, 1, 1, 1), 36.0), lo=2, hi=3, out_grads=[G_ROUND],
+               storage="bf16", stash_in=stash)
+    return float(r["dx"].ravel()[0])
+
+
+def _pinned_loss(run_fn):
+    """One 1x1 convolution 1->1 (weight 1, bias 128, no ReLU) on x = 1:
+    y = 129; target 0.5; numel 1, so dL/dy = 2 (129 - 0.5) = 257, stored (as
+    the layer's dZ) as 256, a tie, to the even significand; dW = db =
+    256 * 1."""
+    net = specs.Net("loss", (specs.Layer(CONV1X1, 1, 1, relu=False),), 1, 1, 1)
+    P = [(np.ones((1, 1, 1, 1)), np.array([128.0]))]
+    r = run_fn(net, P, np.ones((1, 1, 1, 1)), target=np.full((1, 1, 1, 1), 0.5), storage="bf16")
+    return float(r["grads"][0][0].ravel()[0]), float(r["grads"][0][1][0])
+
+
+def test_bf16_rounding_points_hand_values():
+    assert _pinned_stage(network.run) == PINNED_STAGE
+    assert _pinned_upcat_stage(network.run) == 520.0
+    assert _pinned_loss(network.run) == (256.0, 256.0)
+
+
+def _mutants():
+    """Copies of the oracle's backward_layers in which one call of the bf16
+    store no longer rounds, one copy per call site, with run() calling it."""
+    import inspect
+    import textwrap
+    src = {f: textwrap.dedent(inspect.getsource(getattr(network, f)))
+           for f in ("run", "backward_layers")}
+    for fname in ("backward_layers",):
+        text = src[fname]
+        n = text.count("_store(")
+        for k in range(n):
+            parts = text.split("_store(")
+            mutated = "_store(".join(parts[:k + 1]) + "_keep(" + "_store(".join(parts[k + 1:])
+            ns = dict(network.__dict__)
+            ns["_keep"] = lambda a, storage: a
+            for other, t in src.items():
+                exec(compile(mutated if other == fname else t, "<mutant>", "exec"), ns)
+            yield f"{fname} store #{k + 1}", ns["run"]
+
+
+def test_each_bf16_store_is_pinned():
+    """Removing the rounding at any single store of the backward changes a
+    hand-pinned value above."""
+    seen = 0
+    for name, run_fn in _mutants():
+        seen += 1
+        same = (_pinned_stage(run_fn) == PINNED_STAGE and
+                _pinned_upcat_stage(run_fn) == 520.0 and
+                _pinned_loss(run_fn) == (256.0, 256.0))
+        assert not same, name
+    assert seen == 3   # dZ, input gradient, upsample sum
