@@ -54,7 +54,15 @@ PROFILE_COMMANDS = {
                   "-- python3 bench.py --copy-calibration",
     "copy_write": "rocprofv3 --pmc WRITE_SIZE --output-format csv -d rocprof_out/prof_cwrite -o cw "
                   "-- python3 bench.py --copy-calibration",
+    "mfma": "rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_BUSY_CU_CYCLES GRBM_GUI_ACTIVE "
+            "--output-format csv -d rocprof_out/prof_mfma -o m "
+            "-- python3 bench.py --eager --steps 1 --warmup 1 --no-cpu-baseline",
+    "lds": "rocprofv3 --pmc SQ_INSTS_VALU_MFMA_MOPS_BF16 SQ_LDS_BANK_CONFLICT SQ_WAIT_INST_LDS "
+           "SQ_INSTS_LDS SQ_WAVE_CYCLES --output-format csv -d rocprof_out/prof_lds -o l "
+           "-- python3 bench.py --eager --steps 1 --warmup 1 --no-cpu-baseline",
 }
+N_SIMD = 1024           # MI355X: 256 CUs x 4 SIMDs
+CLOCK_GHZ = 2.4         # MI355X peak engine clock
 
 
 KERNEL_FILES = [("conv3x3_rows32", "conv_rows32.hip"), ("conv_wgrad_rows", "wgrad_rows.hip"),
@@ -158,6 +166,10 @@ def summarize_profiles(out_dir, workload):
                      f"{float(r['Percentage']):.2f} | {eager.get(nm, float('nan')):.2f} |")
     with open(os.path.join(PROFILES, f"kernel_trace_{workload}.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
+    if os.path.isdir(os.path.join(out_dir, "prof_mfma")) and os.path.isdir(os.path.join(out_dir, "prof_lds")):
+        summarize_counters(out_dir, workload, eager)
+    if not os.path.isdir(os.path.join(out_dir, "prof_fetch")):
+        return
     top = short_kernel_name(rows[0]["Name"])
     fetch, nf = _counter_means(os.path.join(out_dir, "prof_fetch"))
     write, nw = _counter_means(os.path.join(out_dir, "prof_write"))
@@ -197,6 +209,98 @@ def summarize_profiles(out_dir, workload):
     with open(os.path.join(PROFILES, f"traffic_{safe}_{workload}.md"), "w") as f:
         f.write("\n".join(tl) + "\n")
     print(_json.dumps(info))
+
+
+def _counters_by_kernel(path):
+    """{kernel: {counter: [value per dispatch]}} from a rocprofv3 --pmc run
+    (each value summed over the counter's dimensions), plus the dispatches'
+    durations in ns under '_ns'."""
+    import csv
+    import glob
+    out = {}
+    for f in glob.glob(os.path.join(path, "**", "*counter_collection.csv"), recursive=True):
+        for r in csv.DictReader(open(f)):
+            k = short_kernel_name(r["Kernel_Name"])
+            d = out.setdefault(k, {})
+            d.setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+            if r["Counter_Name"] == "SQ_VALU_MFMA_BUSY_CYCLES":
+                d.setdefault("_ns", []).append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    return out
+
+
+def summarize_counters(out_dir, workload, eager_us=None):
+    """Writes profiles/counters_<workload>.md from the two counter runs
+    (PROFILE_COMMANDS 'mfma' and 'lds') over one eager step.
+
+    Per kernel, means per dispatch of:
+      MFMA GFLOP    512 x SQ_INSTS_VALU_MFMA_MOPS_BF16 (the counter is the
+                    multiply and add operations divided by 512);
+      FLOP / busy   MFMA FLOP per SQ_VALU_MFMA_BUSY_CYCLES summed over SIMDs
+                    (1024 is the full dense bf16 rate of one SIMD);
+      MFMA busy     SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x duration x
+                    2.4 GHz), with the duration of the counter run's own
+                    dispatches and with the eager-pass duration of the kernel
+                    trace;
+      LDS           bank-conflict cycles per LDS instruction, and the share of
+                    wave time spent waiting to issue an LDS instruction
+                    (SQ_WAIT_INST_LDS / SQ_WAVE_CYCLES, both in quad-cycles)."""
+    import math
+    a = _counters_by_kernel(os.path.join(out_dir, "prof_mfma"))
+    b = _counters_by_kernel(os.path.join(out_dir, "prof_lds"))
+
+    def mean(d, k, c):
+        v = d.get(k, {}).get(c)
+        return sum(v) / len(v) if v else float("nan")
+    rows = []
+    for k in a:
+        busy = mean(a, k, "SQ_VALU_MFMA_BUSY_CYCLES")
+        us_c = mean(a, k, "_ns") / 1e3
+        flop = 512.0 * mean(b, k, "SQ_INSTS_VALU_MFMA_MOPS_BF16")
+        lds = mean(b, k, "SQ_INSTS_LDS")
+        conf = mean(b, k, "SQ_LDS_BANK_CONFLICT")
+        wait = mean(b, k, "SQ_WAIT_INST_LDS")
+        wave = mean(b, k, "SQ_WAVE_CYCLES")
+        us = (eager_us or {}).get(k, float("nan"))
+        rows.append({"kernel": k, "dispatches": len(a[k].get("_ns", [])), "us_c": us_c, "us": us,
+                     "busy_c": busy / (N_SIMD * us_c * CLOCK_GHZ * 1e3),
+                     "busy_e": busy / (N_SIMD * us * CLOCK_GHZ * 1e3),
+                     "flop": flop,
+                     "conf_per_lds": conf / lds if lds > 0 else float("nan"),
+                     "lds_wait": wait / wave if wave > 0 else float("nan"),
+                     "flop_per_busy": flop / busy if busy > 0 else float("nan")})
+    rows.sort(key=lambda r: -(r["us_c"] * r["dispatches"]))
+    lines = [f"# MFMA and LDS counters: {workload}", "",
+             "Commands (from the repository root on the GPU host; one counter group per run):", "",
+             "    " + PROFILE_COMMANDS["mfma"], "    " + PROFILE_COMMANDS["lds"], "",
+             "Means per dispatch over one eager step (two micro-batches per launch). "
+             "`MFMA GFLOP` = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16. `FLOP/busy cycle` = those FLOPs "
+             "per SQ_VALU_MFMA_BUSY_CYCLES (summed over SIMDs): 1024 means every busy MFMA cycle "
+             "of a SIMD does the full dense bf16 work (32x32x16: 32768 FLOP in 32 cycles). "
+             "`MFMA busy` = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x duration x 2.4 GHz), with "
+             "the duration of the counter run's own dispatches (`busy, counter run`) and with "
+             f"the eager-pass duration of the kernel trace (`kernel_trace_{workload}.md`; "
+             "`busy, eager`). `LDS wait` = SQ_WAIT_INST_LDS / SQ_WAVE_CYCLES, the share of wave "
+             "time spent waiting to issue an LDS instruction. (GRBM_GUI_ACTIVE and "
+             "SQ_BUSY_CU_CYCLES were collected too but carry a per-dispatch overhead of "
+             "10-30 thousand cycles, so they are not used as denominators.)", "",
+             "| kernel | dispatches | MFMA GFLOP | FLOP/busy cycle | us, counter run | "
+             "MFMA busy, counter run | eager us | MFMA busy, eager | "
+             "LDS conflict cycles/instr | LDS wait |",
+             "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+
+    def f(v, fmt):
+        return "-" if not (isinstance(v, float) and math.isfinite(v)) else format(v, fmt)
+    for r in rows:
+        if not (r["flop"] > 0 or r["us_c"] > 5):
+            continue
+        lines.append(f"| `{r['kernel']}` | {r['dispatches']} | {f(r['flop'] / 1e9, '.2f')} | "
+                     f"{f(r['flop_per_busy'], '.0f')} | {f(r['us_c'], '.2f')} | "
+                     f"{f(100 * r['busy_c'], '.1f')}% | {f(r['us'], '.2f')} | "
+                     f"{f(100 * r['busy_e'], '.1f')}% | {f(r['conf_per_lds'], '.3f')} | "
+                     f"{f(100 * r['lds_wait'], '.1f')}% |")
+    with open(os.path.join(PROFILES, f"counters_{workload}.md"), "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    return rows
 
 
 def recorded_traffic(kernel, workload, pairs):
