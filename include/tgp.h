@@ -256,6 +256,30 @@ tgp_status tgp_grad_accumulate(tgp_net* net, int j, int i, int overwrite, void* 
 tgp_status tgp_pipeline_step(tgp_net* net, const void* x, const void* target, int B, int m,
                              int n, int ckpt_mode, float* loss_dev, void* y_out, void* stream);
 
+/* tgp_pipeline_step without a bound workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The step runs exactly as
+ * tgp_pipeline_step (same kernels, bit-identical results) with the library's
+ * own static device array of TGP_STATIC_SCRATCH_BYTES as its workspace; it
+ * calls no hipMalloc, hipFree or other allocating routine.  The caller still
+ * passes x, target, loss_dev and y_out (same meaning, layout and ownership
+ * as tgp_pipeline_step) and must have called tgp_plan; a workspace bound
+ * with tgp_bind_workspace is left bound and unused by this call.  Each
+ * device holds its own copy of the array from the first call on it until
+ * the process ends; every call on one device shares that copy and leaves
+ * its contents behind, so calls that may run at the same time on one device
+ * (other streams, other threads, other nets) race and must be serialised by
+ * the caller.  Nothing in the array needs to start at zero.
+ * Errors: ENOSPACE when the plan's workspace exceeds TGP_STATIC_SCRATCH_BYTES;
+ * EINVAL with more than one lane (lane streams would have to be created);
+ * EUNSUPPORTED on a device index of TGP_STATIC_MAX_DEVICES or more; all
+ * errors of tgp_pipeline_step otherwise. */
+#define TGP_STATIC_SCRATCH_BYTES ((size_t)64 << 20)
+#define TGP_STATIC_MAX_DEVICES 64
+tgp_status tgp_pipeline_step_static(tgp_net* net, const void* x, const void* target, int B,
+                                    int m, int n, int ckpt_mode, float* loss_dev, void* y_out,
+                                    void* stream);
+
 /* Host-only: the (op, i, j) sequence tgp_pipeline_step issues for (m, n,
  * ckpt_mode), as 3 int32 per op in `ops` (capacity `cap` ops); *count gets
  * the number of ops.  EINVAL if cap is too small (count still set). */

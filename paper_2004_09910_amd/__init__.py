@@ -65,6 +65,7 @@ _SIG = {
     "tgp_stage_backward_recompute": [_P, _I, _I, _P, _P, _P],
     "tgp_grad_accumulate": [_P, _I, _I, _I, _P],
     "tgp_pipeline_step": [_P, _P, _P, _I, _I, _I, _I, _P, _P, _P],
+    "tgp_pipeline_step_static": [_P, _P, _P, _I, _I, _I, _I, _P, _P, _P],
     "tgp_schedule_trace": [_I, _I, _I, ctypes.POINTER(ctypes.c_int32), _I, ctypes.POINTER(_I)],
     "tgp_stage_forward2": [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P],
     "tgp_stage_backward_recompute2": [_P, _I, _I, _I, _P, _P, _P, _P, _P],
@@ -244,6 +245,18 @@ def pipeline_step(net: int, x: int, target: int, B: int, m: int, n: int, ckpt_mo
                   loss_dev: int, y_out: Optional[int] = None, stream: int = 0) -> None:
     _check(_lib.tgp_pipeline_step(net, _vp(x), _vp(target), B, m, n, ckpt_mode, _vp(loss_dev),
                                   _vp(y_out), _vp(stream)), "tgp_pipeline_step")
+
+
+STATIC_SCRATCH_BYTES = 64 << 20   # TGP_STATIC_SCRATCH_BYTES
+
+
+def pipeline_step_static(net: int, x: int, target: int, B: int, m: int, n: int, ckpt_mode: int,
+                         loss_dev: int, y_out: Optional[int] = None, stream: int = 0) -> None:
+    """tgp_pipeline_step on the library's static device scratch (no bound
+    workspace, no allocation; one lane)."""
+    _check(_lib.tgp_pipeline_step_static(net, _vp(x), _vp(target), B, m, n, ckpt_mode,
+                                         _vp(loss_dev), _vp(y_out), _vp(stream)),
+           "tgp_pipeline_step_static")
 
 
 def schedule_trace(m: int, n: int, ckpt_mode: int) -> List[Tuple[int, int, int]]:

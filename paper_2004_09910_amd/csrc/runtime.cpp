@@ -12,6 +12,7 @@
 #include <cstdio>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -1414,6 +1415,61 @@ tgp_status tgp_pipeline_step(tgp_net* N, const void* x, const void* target, int 
                              S(stream)),
          "loss_finalize");
   return TGP_OK;
+}
+
+// ------------------------------------------------------------ static scratch
+// The workspace of tgp_pipeline_step_static: a device array of
+// TGP_STATIC_SCRATCH_BYTES that every device the library runs on holds from
+// load to process end.  Host code never passes `scratch` itself to a kernel
+// or a copy (in host code the name is a host-side stand-in, not a device
+// address): it asks hipGetSymbolAddress for the array's address on each
+// device once, keeps it per device and uses only that.
+static __device__ __align__(256) unsigned char scratch[TGP_STATIC_SCRATCH_BYTES];
+
+static std::mutex g_scratch_mu;
+static void* g_scratch_dev[TGP_STATIC_MAX_DEVICES] = {};
+
+// Device address of the current device's copy of `scratch`.
+static tgp_status scratch_address(void** p) {
+  int dev = 0;
+  HIPCHK(hipGetDevice(&dev), "hipGetDevice");
+  if (dev < 0 || dev >= TGP_STATIC_MAX_DEVICES)
+    return fail(TGP_EUNSUPPORTED, "device %d beyond the %d the static scratch serves", dev,
+                TGP_STATIC_MAX_DEVICES);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* q = nullptr;
+    HIPCHK(hipGetSymbolAddress(&q, HIP_SYMBOL(scratch)), "hipGetSymbolAddress(scratch)");
+    if (!q || ((uintptr_t)q & 255))
+      return fail(TGP_EHIP, "static scratch address %p is not 256-byte aligned", q);
+    g_scratch_dev[dev] = q;
+  }
+  *p = g_scratch_dev[dev];
+  return TGP_OK;
+}
+
+tgp_status tgp_pipeline_step_static(tgp_net* N, const void* x, const void* target, int B, int m,
+                                    int n, int mode, float* loss_dev, void* y_out, void* stream) {
+  if (!N) return fail(TGP_EINVAL, "net is NULL");
+  if (!N->planned) return fail(TGP_ESTATE, "tgp_plan has not been called");
+  if (N->ws_need > TGP_STATIC_SCRATCH_BYTES)
+    return fail(TGP_ENOSPACE,
+                "the plan needs a workspace of %zu bytes; the static scratch holds %zu",
+                N->ws_need, (size_t)TGP_STATIC_SCRATCH_BYTES);
+  if (N->lanes != 1)
+    return fail(TGP_EINVAL, "the static-scratch step runs one lane (lanes = %d): call "
+                "tgp_set_lanes(net, 1) before tgp_plan", N->lanes);
+  void* p = nullptr;
+  tgp_status r = scratch_address(&p);
+  if (r != TGP_OK) return r;
+  char* ws0 = N->ws;
+  const size_t size0 = N->ws_size;
+  N->ws = (char*)p;
+  N->ws_size = TGP_STATIC_SCRATCH_BYTES;
+  r = tgp_pipeline_step(N, x, target, B, m, n, mode, loss_dev, y_out, stream);
+  N->ws = ws0;            // the bound workspace (if any) is the net's again
+  N->ws_size = size0;
+  return r;
 }
 
 tgp_status tgp_schedule_trace(int m, int n, int mode, int32_t* ops, int cap, int* count) {
