@@ -453,6 +453,7 @@ def cpu_baseline(wl, lo, hi, samples, dtype):
         cores = max([d.get("num_threads", 1) for d in threadpool_info()] + [1])
     except Exception:
         cores = os.cpu_count()
+    host = host_cpu_info()
     import oracle
     from oracle import network
     from workloads import synth
@@ -474,7 +475,28 @@ def cpu_baseline(wl, lo, hi, samples, dtype):
     return {"value": samples / dt, "unit": "samples/s", "cores": cores, "kind": "oracle",
             "sample": f"{samples} single-sample forward+backward passes of the stage at full "
                       f"per-sample shape (no recompute, float64 with bf16 storage rounding), "
-                      f"{dt:.1f} s"}
+                      f"{dt:.1f} s",
+            "cores_note": "threads of the BLAS pool the oracle's float64 contractions ran on",
+            **host}
+
+
+def host_cpu_info():
+    """Logical CPUs of the host, those this process may run on, and the CPU
+    model from /proc/cpuinfo."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = None
+    return {"host_logical_cpus": os.cpu_count(), "usable_cpus": usable, "cpu_model": model}
 
 
 def memory_account(net, B, m, mode):

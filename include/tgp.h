@@ -24,6 +24,15 @@
  *     library never allocates device memory: the caller sizes a workspace with
  *     tgp_plan and binds it with tgp_bind_workspace.  Pointers must stay
  *     valid for as long as the calls that use them may run.
+ *   - Alignment (kernels use 16-byte vector accesses along the channel
+ *     dimension): whole tensors -- weights, biases and accumulators given to
+ *     tgp_bind_params, and x, target and y_out of tgp_pipeline_step -- must
+ *     start at a multiple of 16 bytes, loss_dev at a multiple of 4.  The
+ *     micro-batch slices given to the stage calls (x_in, y_out, dy_out,
+ *     dx_in and their paired forms) must start at a multiple of the largest
+ *     power of two up to 16 that divides the tensor's channel row (channels x
+ *     element size): 16 bytes for every tensor of 8 or more bf16 (4 or more
+ *     fp32) channels in multiples of 8 (4).  Violations return TGP_EINVAL.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Calls enqueue work and return without synchronising; kernel faults
  *     surface at the caller's next synchronisation.
@@ -230,7 +239,7 @@ tgp_status tgp_stage_forward2(tgp_net* net, int j, int i0, int i1, int checkpoin
 tgp_status tgp_stage_backward_recompute2(tgp_net* net, int j, int i0, int i1, const void* dy0,
                                          const void* dy1, void* dx0, void* dx1, void* stream);
 
-/* g^j (+)= g_i^j into the bound float32 accumulators of partition j's layers/* g^j (+)= g_i^j into the bound float32 accumulators of partition j's layers
+/* g^j (+)= g_i^j into the bound float32 accumulators of partition j's layers
  * (Sec. 2: the gradient is the sum of g_i^j over i); the partial sums B_{i,j}
  * left are added up here, in an order fixed by the shapes.  overwrite must be 1
  * exactly for i = m (the first backward of a step), else 0.  Requires
@@ -252,7 +261,11 @@ tgp_status tgp_grad_accumulate(tgp_net* net, int j, int i, int overwrite, void* 
  * before the loss; the results are bit-identical to one lane.  The streams
  * are created on first use (on the current device) and destroyed with the
  * net; the fork and join are events, so the step can be captured into a
- * HIP graph from `stream`. */
+ * HIP graph from `stream`.  If a task fails (TGP_EHIP) the step is
+ * abandoned: the lanes are still joined into `stream`, every task returns to
+ * its idle state, and the next tgp_pipeline_step (or stage call) starts a
+ * fresh step; the work already enqueued still runs and the outputs and
+ * accumulators hold partial results. */
 tgp_status tgp_pipeline_step(tgp_net* net, const void* x, const void* target, int B, int m,
                              int n, int ckpt_mode, float* loss_dev, void* y_out, void* stream);
 
@@ -325,6 +338,15 @@ tgp_status tgp_profile_clear(void);
  * layout at every width. */
 int tgp_debug_set_fwd_variant(int v);
 int tgp_debug_set_rowtile_mask(int m);
+
+/* Launch-failure injection, for tests of the error path only (per calling
+ * thread).  tgp_debug_fail_launch(n) with n >= 1 makes the n-th kernel launch
+ * from now on fail as a rejected launch would: that launch and every later
+ * one of the same library call are skipped (nothing reaches the device) and
+ * the call returns TGP_EHIP with tgp_last_error naming the operation.  n = 0
+ * disarms.  Returns the launches that were left before the previous setting
+ * would have fired (0 if disarmed). */
+int tgp_debug_fail_launch(int n);
 
 /* Message of the last failed call on this thread ("" if none). */
 const char* tgp_last_error(void);

@@ -97,6 +97,8 @@ _lib.tgp_debug_set_fwd_variant.argtypes = [_I]
 _lib.tgp_debug_set_fwd_variant.restype = _I
 _lib.tgp_debug_set_rowtile_mask.argtypes = [_I]
 _lib.tgp_debug_set_rowtile_mask.restype = _I
+_lib.tgp_debug_fail_launch.argtypes = [_I]
+_lib.tgp_debug_fail_launch.restype = _I
 _lib.tgp_net_destroy.argtypes = [_P]
 _lib.tgp_net_destroy.restype = None
 _lib.tgp_last_error.argtypes = []
@@ -290,6 +292,13 @@ def debug_set_fwd_variant(v: int) -> int:
     """Forces the convolution kernel configuration (0 = automatic plan);
     returns the previous value.  Testing and tuning only."""
     return _lib.tgp_debug_set_fwd_variant(int(v))
+
+
+def debug_fail_launch(n: int) -> int:
+    """Makes the n-th kernel launch from now on (on this thread) fail, with
+    every later launch of that call skipped; 0 disarms.  Error-path tests
+    only.  Returns the previous countdown."""
+    return _lib.tgp_debug_fail_launch(int(n))
 
 
 def debug_set_rowtile_mask(m: int) -> int:

@@ -42,6 +42,8 @@ def build(verbose=False):
     # --no-undefined: a kernel stub the host pass failed to emit is a link
     # error here instead of a load failure later
     cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,--no-undefined", "-o", tmp] + objs
+    # roctx ranges around the tasks (the rocprofiler-sdk marker library)
+    cmd += ["-L/opt/rocm/lib", "-lrocprofiler-sdk-roctx", "-Wl,-rpath,/opt/rocm/lib"]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stderr)

@@ -1103,7 +1103,7 @@ hipError_t launch_fwd_dma(const char* name9, const char* name1, const bf16_t* X,
   else
     TGP_LAUNCH(ps, (conv_fwd_dma<WCO, WP, TM, TN, 1, NS>), grid, dim3(WCO * WP * 64), 0, st, X,
                        X2, Wt, b, Y, Y2, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major);
-  return hipGetLastError();
+  return launch_status();
 }
 
 #define TGP_FWD_CFG(WCO, WP, TM, TN, NS)                                                        \
@@ -1135,19 +1135,19 @@ hipError_t launch_fwd_rows(const char* name_f, const char* name_t, const bf16_t*
     ProfScope ps(name_f, flops, xbytes + wbytes + 2.0 * P * s.cout, st);
     TGP_LAUNCH(ps, (conv_fwd_rows<WCO, WP, TM, TN, NS, false>), grid, block, 0, st, X, Wt, b,
                        Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, tiles, sps);
-    return hipGetLastError();
+    return launch_status();
   }
   {
     ProfScope ps(name_t, flops, xbytes + wbytes + 4.0 * S * P * s.cout, st);
     TGP_LAUNCH(ps, (conv_fwd_rows<WCO, WP, TM, TN, NS, true>), grid, block, 0, st, X, Wt, b,
                        Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, tiles, sps);
   }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_status();
   if (e != hipSuccess) return e;
   ProfScope ps2("conv_rows_epilogue", 0.0, 4.0 * S * P * s.cout + 2.0 * P * s.cout, st);
   TGP_LAUNCH(ps2, conv_rows_epilogue, dim3(cdiv(P * s.cout, 2048)), dim3(256), 0, st, part, b,
                      Y, P, s.cout, S, relu);
-  return hipGetLastError();
+  return launch_status();
 }
 
 #define TGP_ROWS_CFG(WCO, WP, TM, TN, NS, S)                                                   \
@@ -1195,19 +1195,19 @@ hipError_t launch_rows_pers(const char* name_f, const char* name_t, const bf16_t
     ProfScope ps(name_f, flops, xbytes + wbytes + 2.0 * P * s.cout, st);
     TGP_LAUNCH(ps, (conv_rows_pers<WCO, WP, TM, TN, NS, false>), dim3(G), dim3(NW * 64), 0, st,
                        X, Wt, b, Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, npt, 1);
-    return hipGetLastError();
+    return launch_status();
   }
   {
     ProfScope ps(name_t, flops, xbytes + wbytes + 4.0 * S * P * s.cout, st);
     TGP_LAUNCH(ps, (conv_rows_pers<WCO, WP, TM, TN, NS, true>), dim3(G), dim3(NW * 64), 0, st,
                        X, Wt, b, Y, part, (int)P, s.H, s.W, s.cin, s.cout, relu, co_major, npt, S);
   }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_status();
   if (e != hipSuccess) return e;
   ProfScope ps2("conv_rows_epilogue", 0.0, 4.0 * S * P * s.cout + 2.0 * P * s.cout, st);
   TGP_LAUNCH(ps2, conv_rows_epilogue, dim3(cdiv(P * s.cout, 2048)), dim3(256), 0, st, part, b,
                      Y, P, s.cout, S, relu);
-  return hipGetLastError();
+  return launch_status();
 }
 
 #define TGP_PERS_CFG(WCO, WP, TM, TN, NS, S)                                                    \
@@ -1383,7 +1383,7 @@ hipError_t weight_transform(int dt, const void* w, void* wt, int cout, int cin, 
   else
     TGP_LAUNCH(ps, wtransform_kernel<float>, dim3(cdiv(n, 256)), dim3(256), 0, st,
                        (const float*)w, (float*)wt, cout, cin, taps);
-  return hipGetLastError();
+  return launch_status();
 }
 
 // Bit 2 of g_rowtile_mask selects the row-blocked weight-gradient kernel.
@@ -1444,7 +1444,7 @@ static hipError_t launch_wgrad_mfma(const void* x, const void* x1, const void* d
       TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 1>), grid, dim3(256), 0, st, X, X2, DZ, DZ2,
                  partial, P2, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
   }
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
@@ -1476,7 +1476,7 @@ hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hi
                4.0 * E * (S + 1) + (extra ? 4.0 * extra->E * (extra->S + 1) : 0.0), st);
   if (E % 4) {
     TGP_LAUNCH(ps, splitk_reduce_scalar, dim3(cdiv(E, 256)), dim3(256), 0, st, part, out, E, S);
-    return hipGetLastError();
+    return launch_status();
   }
   // many splits of few columns: 16 columns x 64 split lanes; few splits:
   // 256 columns x 4 lanes (chosen by the first sum's S; the second, if any,
@@ -1497,7 +1497,7 @@ hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hi
   else
     TGP_LAUNCH(ps, splitk_reduce<256>, dim3(nb1 + nb2), dim3(1024), 0, st, part, out, E, S, p2,
                o2, E2, S2, nb1);
-  return hipGetLastError();
+  return launch_status();
 }
 
 // Two micro-batches of one layer: one launch where the planned kernel takes

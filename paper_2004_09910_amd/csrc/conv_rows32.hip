@@ -423,7 +423,7 @@ static hipError_t launch_rows32(const bf16_t* X, const bf16_t* X2, const bf16_t*
                2.0 * ((double)P * s.cin + 9.0 * s.cin * s.cout + (double)P * s.cout), st);
   TGP_LAUNCH(ps, (conv3x3_rows32<W, R, FW, NS, CH, RK>), dim3(G), dim3(CH == 2 ? 256 : 512), 0, st, X,
              X2, Wt, b, Y, Y2, s.nb, s.H, s.cin, s.cout, relu);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, void* y,

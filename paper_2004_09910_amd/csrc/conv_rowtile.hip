@@ -268,7 +268,7 @@ static hipError_t launch_rowtile(const char* name, const bf16_t* X, const bf16_t
                2.0 * ((double)P * s.cin + 9.0 * s.cin * s.cout + (double)P * s.cout), st);
   TGP_LAUNCH(ps, (conv3x3_rowtile<TN, NS, SKB>), dim3(G), dim3(256), 0, st, X, Wt, b, Y, s.nb,
              s.H, s.W, s.cin, s.cout, relu, R);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t conv_forward_rowtile(const void* x, const void* w, const float* b, void* y,

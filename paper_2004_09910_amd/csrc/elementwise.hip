@@ -965,7 +965,7 @@ hipError_t conv_forward(int dt, const void* x, const void* w, const float* b, vo
     else
       TGP_LAUNCH(ps, conv1x1_small_fwd_k<float>, dim3(cdiv(P, 256)), dim3(256), 0, st,
                  (const float*)x, (const float*)w, b, (float*)y, P, s.cin, s.cout, relu);
-    return hipGetLastError();
+    return launch_status();
   }
   long P = s.pixels();
   dim3 g(cdiv(P * s.cout, 256));
@@ -978,7 +978,7 @@ hipError_t conv_forward(int dt, const void* x, const void* w, const float* b, vo
   else
     TGP_LAUNCH(ps, conv_fwd_direct<float>, g, dim3(256), 0, st, (const float*)x,
                        (const float*)w, b, (float*)y, P, s.H, s.W, s.cin, s.cout, s.taps, relu);
-  return hipGetLastError();
+  return launch_status();
 }
 
 bool conv_dgrad_uses_wt(int dt, const ConvShape& s) { return mfma_conv_ok(dt, s.cout, s.cin); }
@@ -1003,7 +1003,7 @@ hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, voi
   else
     TGP_LAUNCH(ps, conv_dgrad_direct<float>, g, dim3(256), 0, st, (const float*)dz,
                        (const float*)w, (float*)dx, P, s.H, s.W, s.cin, s.cout, s.taps);
-  return hipGetLastError();
+  return launch_status();
 }
 
 size_t conv_wgrad_partial_floats(int dt, const ConvShape& s) {
@@ -1037,7 +1037,7 @@ hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* p
         TGP_LAUNCH(ps, wgrad1x1_small_k<float>, dim3(nbk), dim3(256), 0, st, (const float*)x,
                    (const float*)dz, partial, P, s.cin, s.cout, rows);
     }
-    const hipError_t e = hipGetLastError();
+    const hipError_t e = launch_status();
     if (e != hipSuccess) return e;
     if (defer) {
       *defer = ReduceJob{partial, dw, E, nbk};
@@ -1060,7 +1060,7 @@ hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* p
     TGP_LAUNCH(ps, conv_wgrad_direct<float>, g, dim3(256), 0, st, (const float*)x,
                        (const float*)dz, partial, P, s.H, s.W, s.cin, s.cout, s.taps, pps);
   }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_status();
   if (e != hipSuccess) return e;
   if (defer) {
     *defer = ReduceJob{partial, dw, E, S};
@@ -1123,7 +1123,7 @@ hipError_t dw_forward2(const void* x0, const void* x1, const void* w, const floa
   TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, false>), g, dim3(256), 0, st, (const bf16_t*)x0,
              (const bf16_t*)(x1 ? x1 : x0), (const bf16_t*)w, b, (bf16_t*)y0,
              (bf16_t*)(x1 ? y1 : y0), H, W, C, relu);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t dw_dgrad2(const void* dz0, const void* dz1, const void* w, void* dx0, void* dx1,
@@ -1136,7 +1136,7 @@ hipError_t dw_dgrad2(const void* dz0, const void* dz1, const void* w, void* dx0,
   TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, true>), g, dim3(256), 0, st, (const bf16_t*)dz0,
              (const bf16_t*)(dz1 ? dz1 : dz0), (const bf16_t*)w, (const float*)nullptr,
              (bf16_t*)dx0, (bf16_t*)(dz1 ? dx1 : dx0), H, W, C, 0);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t dw_wgrad2(const void* x0, const void* x1, const void* dz0, const void* dz1,
@@ -1154,7 +1154,7 @@ hipError_t dw_wgrad2(const void* x0, const void* x1, const void* dz0, const void
                (const bf16_t*)(x1 ? x1 : x0), (const bf16_t*)dz0,
                (const bf16_t*)(x1 ? dz1 : dz0), part0, x1 ? part1 : part0, H, W, C);
   }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_status();
   if (e != hipSuccess) return e;
   if (n == 1) return splitk_reduce_launch(part0, dw0, E, S, st);
   const ReduceJob second{part1, dw1, E, S};   // both sums in one launch
@@ -1174,7 +1174,7 @@ hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void
   else
     TGP_LAUNCH(ps, dw_fwd<float>, g, dim3(256), 0, st, (const float*)x, (const float*)w, b,
                        (float*)y, P, H, W, C, relu);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int H, int W,
@@ -1190,7 +1190,7 @@ hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int
   else
     TGP_LAUNCH(ps, dw_dgrad_k<float>, g, dim3(256), 0, st, (const float*)dz,
                        (const float*)w, (float*)dx, P, H, W, C);
-  return hipGetLastError();
+  return launch_status();
 }
 
 size_t dw_wgrad_partial_floats(int nb, int H, int W, int C) {
@@ -1220,7 +1220,7 @@ hipError_t dw_wgrad(int dt, const void* x, const void* dz, float* dw, float* par
     TGP_LAUNCH(ps, dw_wgrad_k<float>, g, dim3(256), 0, st, (const float*)x,
                        (const float*)dz, partial, P, H, W, C, pps);
   }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_status();
   if (e != hipSuccess) return e;
   return splitk_reduce_launch(partial, dw, E, S, st);
 }
@@ -1237,7 +1237,7 @@ hipError_t relu_backward(int dt, const void* dy, const void* dskip, const void* 
   else
     TGP_LAUNCH(ps, relu_bwd_k<float>, g, dim3(256), 0, st, (const float*)dy,
                        (const float*)dskip, (const float*)y, (float*)dz, relu, n, vec);
-  return hipGetLastError();
+  return launch_status();
 }
 
 static long colsum_rows(long P) { return P < 1024 ? (P < 1 ? 1 : P) : 1024; }
@@ -1312,7 +1312,7 @@ hipError_t relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, long P
       TGP_LAUNCH(ps, relu_bwd_bias_k<float>, dim3(nb, n), dim3(256), 0, st,
                  rb_ptrs<float>(a[0]), rb_ptrs<float>(b), relu, P, C, rows);
   }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_status();
   if (e != hipSuccess) return e;
   return rb_finish(n, a, C, nb, st);
 }
@@ -1348,7 +1348,7 @@ hipError_t pool_relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, i
       TGP_LAUNCH(ps, pool_relu_bwd_bias_k<float>, dim3(nbk, n), dim3(256), 0, st,
                  rb_ptrs<float>(a[0]), rb_ptrs<float>(b), relu, nb, H, W, C, rows);
   }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_status();
   if (e != hipSuccess) return e;
   return rb_finish(n, a, C, nbk, st);
 }
@@ -1372,7 +1372,7 @@ hipError_t bias_grad(int dt, const void* dz, float* db, float* partial, long P, 
   else
     TGP_LAUNCH(ps, colsum_k<float>, g, dim3(256), 0, st, (const float*)dz, partial, P, C, rows);
   }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_status();
   if (e != hipSuccess) return e;
   return splitk_reduce_launch(partial, db, C, nb, st);
 }
@@ -1391,7 +1391,7 @@ hipError_t maxpool_forward2(int dt, const void* x0, void* y0, const void* x1, vo
   else
     TGP_LAUNCH(ps, maxpool_fwd_k<float>, g, dim3(256), 0, st, (const float*)x0, (float*)y0,
                (const float*)(n == 2 ? x1 : x0), (float*)(n == 2 ? y1 : y0), nb, H, W, C);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t maxpool_forward(int dt, const void* x, void* y, int nb, int H, int W, int C,
@@ -1411,7 +1411,7 @@ hipError_t maxpool_backward(int dt, const void* x, const void* dy, void* dx, int
   else
     TGP_LAUNCH(ps, maxpool_bwd_k<float>, g, dim3(256), 0, st, (const float*)x,
                        (const float*)dy, (float*)dx, nb, H, W, C);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t upcat_forward(int dt, const void* prev, const void* skip, void* out, int nb, int H,
@@ -1426,7 +1426,7 @@ hipError_t upcat_forward(int dt, const void* prev, const void* skip, void* out, 
   else
     TGP_LAUNCH(ps, upcat_fwd_k<float>, g, dim3(256), 0, st, (const float*)prev,
                        (const float*)skip, (float*)out, nb, H, W, C1, C2);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t upcat_backward(int dt, const void* dcat, void* dprev, void* dskip, int nb, int H,
@@ -1446,7 +1446,7 @@ hipError_t upcat_backward(int dt, const void* dcat, void* dprev, void* dskip, in
     TGP_LAUNCH(ps, upcat_bwd_skip_k<float>, dim3(cdiv(P * (C2 / N), 256)), dim3(256), 0, st,
                        (const float*)dcat, (float*)dskip, P, C1, C2);
   }
-  return hipGetLastError();
+  return launch_status();
 }
 
 static long mse_per_block(long n) { return n < 4096 ? 4096 : 16384; }
@@ -1466,17 +1466,17 @@ hipError_t mse_forward_backward(int dt, const void* y, const void* t, void* dy,
     TGP_LAUNCH(ps, mse_k<float>, dim3(nb), dim3(256), 0, st, (const float*)y,
                        (const float*)t, (float*)dy, partial, n, inv_numel, pb);
   }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_status();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(serial_sum_k, dim3(1), dim3(64), 0, st, (const float*)partial, nb, 1.0f,
                      loss_part);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t loss_finalize(const float* parts, int m, float inv_numel, float* loss,
                          hipStream_t st) {
   hipLaunchKernelGGL(serial_sum_k, dim3(1), dim3(64), 0, st, parts, m, inv_numel, loss);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t grad_accumulate_batch(AccBatch b, int overwrite, hipStream_t st) {
@@ -1499,13 +1499,13 @@ hipError_t grad_accumulate_batch(AccBatch b, int overwrite, hipStream_t st) {
   ProfScope ps("reduce_accumulate", 0.0, bytes, st);
   const unsigned grid = (unsigned)(blocks < 512 ? blocks : 512);   // two blocks per CU
   TGP_LAUNCH(ps, reduce_accumulate_k, dim3(grid), dim3(1024), 0, st, b, overwrite, (int)blocks);
-  return hipGetLastError();
+  return launch_status();
 }
 
 hipError_t grad_accumulate(float* acc, const float* g, long n, int overwrite, hipStream_t st) {
   ProfScope ps("grad_accumulate", (double)n, (overwrite ? 8.0 : 12.0) * n, st);
   TGP_LAUNCH(ps, accumulate_k, dim3(cdiv(n, 1024)), dim3(256), 0, st, acc, g, n, overwrite);
-  return hipGetLastError();
+  return launch_status();
 }
 
 }  // namespace tgpk

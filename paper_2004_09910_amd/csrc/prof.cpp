@@ -34,9 +34,32 @@ struct State {
 
 thread_local State g;
 
+// launch-failure injection: launches left before the injected failure
+// (0 = disarmed), and the failure pending collection
+thread_local int g_fail_in = 0;
+thread_local hipError_t g_failed = hipSuccess;
+
 }  // namespace
 
 bool prof_enabled() { return g.on; }
+
+bool launch_skipped() {
+  if (g_failed != hipSuccess) return true;
+  if (g_fail_in > 0 && --g_fail_in == 0) {
+    g_failed = hipErrorLaunchFailure;
+    return true;
+  }
+  return false;
+}
+
+hipError_t launch_status() {
+  if (g_failed != hipSuccess) {
+    const hipError_t e = g_failed;
+    g_failed = hipSuccess;
+    return e;
+  }
+  return hipGetLastError();
+}
 
 ProfScope::ProfScope(const char* name, double flops, double bytes, hipStream_t) {
   if (!g.on) return;
@@ -55,6 +78,13 @@ void ProfScope::mark_launched() {
 }  // namespace tgpk
 
 extern "C" {
+
+int tgp_debug_fail_launch(int n) {
+  const int prev = tgpk::g_fail_in;
+  tgpk::g_fail_in = n > 0 ? n : 0;
+  tgpk::g_failed = hipSuccess;
+  return prev;
+}
 
 tgp_status tgp_profile_enable(int enable) {
   tgpk::g.on = enable != 0;

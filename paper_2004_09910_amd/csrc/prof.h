@@ -11,6 +11,14 @@ namespace tgpk {
 
 bool prof_enabled();
 
+// Launch-failure injection, for tests of the error path only
+// (tgp_debug_fail_launch): once armed for the n-th launch, that launch and
+// every later one on the thread are skipped (nothing reaches the device)
+// until a launcher collects the failure through launch_status(), which the
+// launchers return in place of hipGetLastError().
+bool launch_skipped();
+hipError_t launch_status();
+
 class ProfScope {
  public:
   ProfScope(const char* name, double flops, double bytes, hipStream_t st);
@@ -29,6 +37,7 @@ class ProfScope {
 // queue gaps an event recorded before and after the launch would add.
 #define TGP_LAUNCH(ps, kernel, grid, block, shmem, st, ...)                                   \
   do {                                                                                       \
+    if (::tgpk::launch_skipped()) break;                                                     \
     if ((ps).active()) {                                                                     \
       hipExtLaunchKernelGGL(kernel, grid, block, shmem, st, (ps).start_event(),              \
                             (ps).stop_event(), 0, __VA_ARGS__);                              \

@@ -4,6 +4,7 @@
 // scheduler that issues them (Algorithm 1 and its reverse).  It owns no
 // device memory: every buffer is a slice of caller-owned memory.
 #include <hip/hip_runtime.h>
+#include <rocprofiler-sdk-roctx/roctx.h>
 
 #include <algorithm>
 #include <array>
@@ -34,6 +35,34 @@ tgp_status fail(tgp_status s, const char* fmt, ...) {
 }
 
 inline size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// Kernels read and write caller tensors with 16-byte vector accesses along
+// the innermost (channel) dimension where a row of it spans a multiple of
+// 16 bytes.  A micro-batch slice of a tensor whose channel row is R bytes
+// must start at a multiple of the largest power of two up to 16 dividing R;
+// whole tensors (weights, biases, accumulators, the step's inputs and
+// outputs) at a multiple of 16.
+bool aligned_to(const void* p, size_t a) { return ((uintptr_t)p & (a - 1)) == 0; }
+bool row_aligned(const void* p, long row_bytes) {
+  size_t need = 16;
+  while (need > 1 && row_bytes % (long)need) need >>= 1;
+  return aligned_to(p, need);
+}
+
+// roctx range around one task (F, F', B, ACC, LOSS) or a whole step, for
+// timelines under a tracing tool; a no-op cost without one.
+struct Range {
+  Range(const char* what, int i, int j) {
+    char buf[48];
+    if (j > 0) snprintf(buf, sizeof buf, "%s i=%d j=%d", what, i, j);
+    else snprintf(buf, sizeof buf, "%s i=%d", what, i);
+    roctxRangePushA(buf);
+  }
+  explicit Range(const char* what) { roctxRangePushA(what); }
+  ~Range() { roctxRangePop(); }
+  Range(const Range&) = delete;
+  Range& operator=(const Range&) = delete;
+};
 
 enum CellState : uint8_t { IDLE = 0, FWD = 1, BWD = 2, ACC = 3 };
 
@@ -363,10 +392,12 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
         ++rcn;
       }
     if (rcn) {
+      Range rg("F'", rc[0], j);
       tgp_status r = run_forward_g(N, j, rcn, rc, ph, rx, ry, st);
       if (r != TGP_OK) return r;
     }
   }
+  Range rg("B", iv[0], j);
   BwdMb M[2];
   auto stale = [&](int i) -> char& {
     return N->wt_stale[(size_t)((i - 1) % N->lanes) * N->n + (j - 1)];
@@ -619,6 +650,7 @@ tgp_status run_backward(tgp_net* N, int j, int i, const void* dy_out, void* dx_i
 }
 
 tgp_status run_accumulate(tgp_net* N, int j, int i, int overwrite, hipStream_t st) {
+  Range rg("ACC", i, j);
   tgpk::AccBatch batch;
   batch.count = 0;
   auto flush = [&]() -> tgp_status {
@@ -659,6 +691,20 @@ tgp_status check_ready(const tgp_net* N, int j = 0) {
   if (j >= 1 && j <= N->n) { lo = N->lo[j - 1]; hi = N->hi[j - 1]; }
   for (int l = lo; l < hi; ++l)
     if (!N->L[l].bound) return fail(TGP_ESTATE, "layer %d has no bound parameters", l);
+  return TGP_OK;
+}
+
+// Alignment of the micro-batch slices a stage call gets: the partition's
+// input (or its gradient) and output (or its gradient); either may be NULL.
+tgp_status check_slices(const tgp_net* N, int j, const void* in, const void* out) {
+  const LayerRt& first = N->L[N->lo[j - 1]];
+  const LayerRt& last = N->L[N->hi[j - 1] - 1];
+  if (in && !row_aligned(in, (long)first.inC * N->esz))
+    return fail(TGP_EINVAL, "partition %d input pointer %p is not aligned to its %ld-byte rows",
+                j, in, (long)first.inC * N->esz);
+  if (out && !row_aligned(out, (long)last.d.cout * N->esz))
+    return fail(TGP_EINVAL, "partition %d output pointer %p is not aligned to its %ld-byte rows",
+                j, out, (long)last.d.cout * N->esz);
   return TGP_OK;
 }
 
@@ -747,6 +793,7 @@ struct GpuExec : Exec {
     return tgp_stage_forward(N, j, i, ckpt ? 1 : 0, bnd(i, j - 1), (void*)bnd(i, j), on(i));
   }
   tgp_status loss(int i) override {
+    Range rg("LOSS", i, 0);
     const LayerRt& last = N->L.back();
     long n_mb = (long)N->b * last.H * last.W * last.d.cout;
     long numel = n_mb * N->m;
@@ -949,6 +996,10 @@ tgp_status tgp_bind_params(tgp_net* N, int layer, const void* w, const float* b,
   if (!w || !dw_acc) return fail(TGP_EINVAL, "layer %d: NULL weight or accumulator", layer);
   if (Lr.d.bias && (!b || !db_acc)) return fail(TGP_EINVAL, "layer %d: bias pointers missing", layer);
   if (!Lr.d.bias && (b || db_acc)) return fail(TGP_EINVAL, "layer %d has no bias", layer);
+  if (!aligned_to(w, 16) || !aligned_to(dw_acc, 16) || (b && !aligned_to(b, 16)) ||
+      (db_acc && !aligned_to(db_acc, 16)))
+    return fail(TGP_EINVAL, "layer %d: weight, bias and accumulator pointers must be 16-byte "
+                "aligned", layer);
   Lr.w = w; Lr.b = b; Lr.dw_acc = dw_acc; Lr.db_acc = db_acc; Lr.bound = true;
   return TGP_OK;
 }
@@ -1232,11 +1283,13 @@ tgp_status tgp_stage_forward(tgp_net* N, int j, int i, int checkpoint, const voi
   if (j < 1 || j > N->n) return fail(TGP_EINVAL, "partition %d out of 1..%d", j, N->n);
   if (i < 1 || i > N->m) return fail(TGP_EINVAL, "micro-batch %d out of 1..%d", i, N->m);
   if (!x_in || !y_out) return fail(TGP_EINVAL, "NULL x_in or y_out");
+  if ((r = check_slices(N, j, x_in, y_out)) != TGP_OK) return r;
   if ((checkpoint != 0) != ckpt_of(N->mode, i, N->m))
     return fail(TGP_EINVAL, "checkpoint=%d disagrees with the planned policy for i=%d", checkpoint, i);
   int c = cell(N, i, j);
   if (N->st[c] == FWD || N->st[c] == BWD)
     return fail(TGP_ESTATE, "F_{%d,%d} already ran in this step", i, j);
+  Range rg("F", i, j);
   r = run_forward(N, j, i, checkpoint ? 0 : 1, x_in, y_out, S(stream));
   if (r != TGP_OK) return r;
   N->st[c] = FWD;
@@ -1253,6 +1306,7 @@ tgp_status tgp_stage_backward_recompute(tgp_net* N, int j, int i, const void* dy
   if (j < 1 || j > N->n) return fail(TGP_EINVAL, "partition %d out of 1..%d", j, N->n);
   if (i < 1 || i > N->m) return fail(TGP_EINVAL, "micro-batch %d out of 1..%d", i, N->m);
   if (!dy_out) return fail(TGP_EINVAL, "NULL dy_out");
+  if ((r = check_slices(N, j, dx_in, dy_out)) != TGP_OK) return r;
   int c = cell(N, i, j);
   if (N->st[c] != FWD) return fail(TGP_ESTATE, "B_{%d,%d} needs F_{%d,%d} first", i, j, i, j);
   if (i < N->m && N->st[cell(N, i + 1, j)] != ACC)
@@ -1282,6 +1336,9 @@ tgp_status tgp_stage_forward2(tgp_net* N, int j, int i0, int i1, int checkpoint0
   if (i0 == i1 || (i0 - 1) % N->lanes == (i1 - 1) % N->lanes)
     return fail(TGP_EINVAL, "micro-batches %d and %d share a lane (lanes = %d)", i0, i1, N->lanes);
   if (!x0 || !x1 || !y0 || !y1) return fail(TGP_EINVAL, "NULL x_in or y_out");
+  if ((r = check_slices(N, j, x0, y0)) != TGP_OK || (r = check_slices(N, j, x1, y1)) != TGP_OK)
+    return r;
+  Range rg("F", i0, j);
   const int ph[2] = {checkpoint0 ? 0 : 1, checkpoint1 ? 0 : 1};
   const void* xs[2] = {x0, x1};
   void* ys[2] = {y0, y1};
@@ -1308,6 +1365,8 @@ tgp_status tgp_stage_backward_recompute2(tgp_net* N, int j, int i0, int i1, cons
     return fail(TGP_EINVAL, "two backwards at once need two or more lanes");
   if (!dy0 || !dy1) return fail(TGP_EINVAL, "NULL dy_out");
   if ((dx0 == nullptr) != (dx1 == nullptr)) return fail(TGP_EINVAL, "dx_in: both or neither");
+  if ((r = check_slices(N, j, dx0, dy0)) != TGP_OK || (r = check_slices(N, j, dx1, dy1)) != TGP_OK)
+    return r;
   for (int i : {i0, i1})
     if (N->st[cell(N, i, j)] != FWD) return fail(TGP_ESTATE, "B_{%d,%d} needs F_{%d,%d} first", i, j, i, j);
   if (i0 < N->m && N->st[cell(N, i0 + 1, j)] != ACC)
@@ -1369,12 +1428,16 @@ tgp_status tgp_pipeline_step(tgp_net* N, const void* x, const void* target, int 
   tgp_status r = check_ready(N);
   if (r != TGP_OK) return r;
   if (!x || !target || !loss_dev) return fail(TGP_EINVAL, "NULL x, target or loss");
+  if (!aligned_to(x, 16) || !aligned_to(target, 16) || (y_out && !aligned_to(y_out, 16)) ||
+      !aligned_to(loss_dev, 4))
+    return fail(TGP_EINVAL, "x, target and y_out must be 16-byte aligned, loss_dev 4-byte");
   if (B != N->B || m != N->m || mode != N->mode)
     return fail(TGP_EINVAL, "B/m/mode differ from tgp_plan (%d/%d/%d)", N->B, N->m, N->mode);
   if (n != N->n) return fail(TGP_EINVAL, "n=%d differs from the partition (%d)", n, N->n);
   for (int c = 0; c < m * n; ++c)
     if (N->st[c] == FWD || N->st[c] == BWD)
       return fail(TGP_ESTATE, "a stage step is in progress");
+  Range rg("pipeline_step");
   GpuExec ex;
   ex.N = N;
   ex.x = (const char*)x;
@@ -1400,13 +1463,26 @@ tgp_status tgp_pipeline_step(tgp_net* N, const void* x, const void* target, int 
       HIPCHK(hipStreamWaitEvent(N->lane_streams[k], fork, 0), "hipStreamWaitEvent");
   }
   r = run_schedule(m, n, mode, ex);
+  if (r != TGP_OK) {
+    // a task failed part way: the step is abandoned, so every task of it
+    // returns to idle and the next step (or stage call) starts afresh
+    const std::string msg = g_err;
+    std::fill(N->st.begin(), N->st.end(), (uint8_t)IDLE);
+    std::fill(N->wt_stale.begin(), N->wt_stale.end(), (char)0);
+    g_err = msg;
+  }
   if (ex.K > 1) {
-    // join (also after an error, so that no fork is left open in a capture)
+    // join every lane, also after an error, so that no fork is left open in
+    // a capture; the first failure is the one reported
+    tgp_status rj = TGP_OK;
     for (int k = 0; k <= ex.K; ++k) {
       hipEvent_t e = N->lane_events[ex.K + 1 + k];
-      HIPCHK(hipEventRecord(e, N->lane_streams[k]), "hipEventRecord");
-      HIPCHK(hipStreamWaitEvent(ex.st, e, 0), "hipStreamWaitEvent");
+      hipError_t he = hipEventRecord(e, N->lane_streams[k]);
+      if (he == hipSuccess) he = hipStreamWaitEvent(ex.st, e, 0);
+      if (he != hipSuccess && rj == TGP_OK && r == TGP_OK)
+        rj = fail(TGP_EHIP, "lane join: %s", hipGetErrorString(he));
     }
+    if (r == TGP_OK) r = rj;
   }
   if (r != TGP_OK) return r;
   const LayerRt& last = N->L.back();

@@ -401,7 +401,7 @@ static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* X2, const bf1
   ProfScope ps(name, flops, bytes, st);
   TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, NS, KS>), dim3(G), dim3(256 * KS), 0, st, X, X2, DZ,
              DZ2, out, out2, s.nb, s.H, s.cin, s.cout, p.R);
-  return hipGetLastError();
+  return launch_status();
 }
 
 template <int W, int RPS, int NS>

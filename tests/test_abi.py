@@ -282,3 +282,43 @@ def test_unbound_layers_are_rejected():
     assert tgp.call_status("tgp_stage_forward", h, 1, 1, 1, FAKE, FAKE, None) == tgp.ESTATE
     assert "bound" in tgp.last_error()
     tgp.net_destroy(h)
+
+
+def test_misaligned_pointers_are_rejected():
+    """Whole tensors must be 16-byte aligned (loss 4-byte); micro-batch
+    slices to the largest power of two up to 16 dividing their channel row.
+    The fp32 8-channel stack has 32-byte rows, so its slices need 16."""
+    h, nbytes = _bound_net(mode=0, B=4, m=2, n=2)
+    tgp.bind_workspace(h, FAKE, nbytes)
+    st = lambda name, *a: tgp.call_status(name, h, *a)
+    for args in ((FAKE + 8, FAKE, FAKE, FAKE), (FAKE, FAKE + 4, FAKE, FAKE),
+                 (FAKE, FAKE, FAKE + 8, FAKE), (FAKE, FAKE, FAKE, FAKE + 2)):
+        assert st("tgp_bind_params", 0, *args) == tgp.EINVAL
+        assert "aligned" in tgp.last_error()
+    assert st("tgp_bind_params", 0, FAKE, FAKE, FAKE, FAKE) == tgp.OK
+    assert st("tgp_stage_forward", 1, 1, 1, FAKE + 8, FAKE, None) == tgp.EINVAL
+    assert st("tgp_stage_forward", 1, 1, 1, FAKE, FAKE + 4, None) == tgp.EINVAL
+    assert "aligned" in tgp.last_error()
+    assert st("tgp_stage_backward_recompute", 1, 2, FAKE + 8, None, None) == tgp.EINVAL
+    assert st("tgp_stage_backward_recompute", 1, 2, FAKE, FAKE + 8, None) == tgp.EINVAL
+    assert st("tgp_pipeline_step", FAKE + 8, FAKE, 4, 2, 2, 0, FAKE, None, None) == tgp.EINVAL
+    assert st("tgp_pipeline_step", FAKE, FAKE + 8, 4, 2, 2, 0, FAKE, None, None) == tgp.EINVAL
+    assert st("tgp_pipeline_step", FAKE, FAKE, 4, 2, 2, 0, FAKE + 2, None, None) == tgp.EINVAL
+    assert st("tgp_pipeline_step", FAKE, FAKE, 4, 2, 2, 0, FAKE, FAKE + 8, None) == tgp.EINVAL
+    tgp.net_destroy(h)
+    # a 1-channel output (the U-Net head) has 2-byte bf16 rows: any even
+    # address is a valid slice of it
+    net = specs.Net("head", (specs.Layer(specs.CONV1X1, 64, 1, relu=False),), 64, 4, 4)
+    h = _net(net, dtype=0)
+    tgp.bind_params(h, 0, FAKE, FAKE, FAKE, FAKE)
+    tgp.bind_workspace(h, FAKE, tgp.plan(h, 2, 2, 0))
+    assert tgp.call_status("tgp_stage_forward", h, 1, 1, 1, FAKE + 8, FAKE, None) == tgp.EINVAL
+    assert tgp.call_status("tgp_stage_forward", h, 1, 1, 1, FAKE, FAKE + 1, None) == tgp.EINVAL
+    tgp.net_destroy(h)
+
+
+def test_launch_failure_hook_arms_and_disarms():
+    """tgp_debug_fail_launch returns the previous countdown; 0 disarms."""
+    assert tgp.debug_fail_launch(5) == 0
+    assert tgp.debug_fail_launch(0) == 5
+    assert tgp.debug_fail_launch(0) == 0
