@@ -88,7 +88,9 @@ __device__ __forceinline__ u32x4 make_rsrc(const void* p, int bytes) {
 // and would otherwise wait for every load in flight before the next LDS
 // read, which serialises the ring.  The kernels order their rings
 // themselves (wait_vmcnt / wait_stages, then ring_barrier).  M0 holds the
-// LDS destination only while the load issues and is restored after it.
+// LDS destination only while the load issues and is restored after it; the
+// wait state the hardware needs between writing M0 and a load that reads it
+// is in the block, since the compiler's hazard checks do not look inside.
 __device__ __forceinline__ void dma16(u32x4 rsrc, __attribute__((address_space(3))) void* dst,
                                       int voff, int soff) {
   const unsigned m = __builtin_amdgcn_readfirstlane((unsigned)(unsigned long)dst);
@@ -96,6 +98,7 @@ __device__ __forceinline__ void dma16(u32x4 rsrc, __attribute__((address_space(3
   asm volatile(
       "s_mov_b32 %0, m0\n\t"
       "s_mov_b32 m0, %1\n\t"
+      "s_nop 0\n\t"          // the load reads M0: one wait state after writing it
       "buffer_load_dwordx4 %2, %3, %4 offen lds\n\t"
       "s_mov_b32 m0, %0"
       : "=&s"(saved)

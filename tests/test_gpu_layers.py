@@ -102,6 +102,41 @@ def test_rows32_resident_weights(cfg, r):
         tgp.debug_set_fwd_variant(old)
 
 
+# Configurations of the row-tiled 16x16x32 kernel (widths the nine-tap kernel
+# is not built for): (index, W, rows per tile).  Rows per tile follow from the
+# configuration's sub-tiles per wave and its LDS slot: 4, 2, 1 at width 128
+# and 2, 1 at width 256 (the third does not fit a 256-pixel row).
+ROWTILE = [(0, 128, 4), (1, 128, 2), (2, 128, 1), (0, 256, 2), (1, 256, 1)]
+
+
+@pytest.mark.parametrize("cfg,w,r", ROWTILE)
+def test_rowtile_configurations(cfg, w, r):
+    """Each configuration of the row-tiled kernel, forced, on a layer whose
+    last row block is ragged (H = R + 1), with two 32-channel chunks and two
+    output-channel tiles; the data gradient (64 output channels from 128)
+    runs the same configuration."""
+    import paper_2004_09910_amd as tgp
+    old = tgp.debug_set_fwd_variant(301 + cfg)
+    try:
+        net = one_layer(Layer(CONV3X3, 64, 128), r + 1, w)
+        run_and_check(net, (1,), 1, BF16, 2, 1, f"rowtile cfg {cfg} 64->128 @{r + 1}x{w}")
+    finally:
+        tgp.debug_set_fwd_variant(old)
+
+
+@pytest.mark.parametrize("cfg", [None, 0, 1, 2])
+def test_rowtile_128x128(cfg):
+    """A whole 128 x 128 image (the 6-level U-Net's level 1 at 128 channels):
+    the automatic plan (the row-tiled kernel) and each configuration forced."""
+    import paper_2004_09910_amd as tgp
+    old = tgp.debug_set_fwd_variant(0 if cfg is None else 301 + cfg)
+    try:
+        net = one_layer(Layer(CONV3X3, 128, 128), 128, 128)
+        run_and_check(net, (1,), 1, BF16, 2, 1, f"rowtile 128->128 @128x128 cfg {cfg}")
+    finally:
+        tgp.debug_set_fwd_variant(old)
+
+
 @pytest.mark.parametrize("cin,cout,h,w", [(64, 128, 7, 48), (128, 64, 5, 96), (64, 64, 3, 192),
                                           (128, 128, 5, 24)])
 def test_wgrad_rows_four_wave_layout(cin, cout, h, w):
