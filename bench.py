@@ -525,6 +525,39 @@ def memory_account(net, B, m, mode):
     return w + nb, pbytes, ws, pbytes + ws + io
 
 
+MEM_SHAPE = dict(B=32, hw=192, in_ch=3, levels=6)   # the paper's U-Net memory benchmark
+
+
+def largest_unet(budget, m, mode, channels):
+    """(blocks per level, first-level channels, memory_account) of the
+    six-level U-Net of MEM_SHAPE with the most parameters whose planned
+    memory fits `budget` bytes, over the channel counts given and any
+    number of blocks."""
+    from workloads import specs
+    B, hw, in_ch, levels = (MEM_SHAPE[k] for k in ("B", "hw", "in_ch", "levels"))
+    best = None
+    for C in channels:
+        def fits(blocks):
+            net = specs.unet(levels, C, in_ch, hw, f"unet6-B{blocks}-C{C}", blocks=blocks)
+            a = memory_account(net, B, m, mode)
+            return a if a is not None and a[3] <= budget else None
+        if not fits(1):
+            continue
+        lo, hi = 1, 2
+        while fits(hi) and hi < 512:
+            lo, hi = hi, hi * 2
+        while hi - lo > 1:          # largest blocks count that fits
+            mid = (lo + hi) // 2
+            if fits(mid):
+                lo = mid
+            else:
+                hi = mid
+        a = fits(lo)
+        if best is None or a[0] > best[2][0]:
+            best = (lo, C, a)
+    return best
+
+
 def memory_report():
     """U-Net memory benchmark analog (Sec. 4.2.2 and its table): the largest
     U-Net (B conv blocks per level, C channels at the first level; six levels,
@@ -541,27 +574,7 @@ def memory_report():
     channels = [32, 48, 64, 72, 96, 128, 160, 192, 224, 256, 320, 384]
     rows = []
     for label, m, mode in settings:
-        best = None
-        for C in channels:
-            def fits(blocks):
-                net = specs.unet(levels, C, in_ch, hw, f"unet6-B{blocks}-C{C}", blocks=blocks)
-                a = memory_account(net, B, m, mode)
-                return a if a is not None and a[3] <= HBM else None
-            if not fits(1):
-                continue
-            lo, hi = 1, 2
-            while fits(hi) and hi < 512:
-                lo, hi = hi, hi * 2
-            while hi - lo > 1:          # largest blocks count that fits
-                mid = (lo + hi) // 2
-                if fits(mid):
-                    lo = mid
-                else:
-                    hi = mid
-            a = fits(lo)
-            if best is None or a[0] > best[2][0]:
-                best = (lo, C, a)
-        blocks, C, (params, pbytes, ws, total) = best
+        blocks, C, (params, pbytes, ws, total) = largest_unet(HBM, m, mode, channels)
         log(f"{label}: (B, C) = ({blocks}, {C}), {params / 1e9:.2f}B parameters, {total / 1e9:.1f} GB")
         rows.append({"setting": label, "m": m, "blocks": blocks, "channels": C, "params": params,
                      "param_gb": pbytes / 1e9, "workspace_gb": ws / 1e9, "total_gb": total / 1e9})
@@ -579,6 +592,19 @@ def memory_report():
     for r in rows:
         lines.append(f"| {r['setting']} | ({r['blocks']}, {r['channels']}) | {r['params'] / 1e9:.2f}B | "
                      f"{r['param_gb']:.1f} GB | {r['workspace_gb']:.1f} GB | {r['total_gb']:.1f} GB |")
+    scale = memory_at_scale()
+    if scale:
+        lines += ["", f"The planner's choice under a {scale[0]['budget_gb']:.0f} GB budget, trained "
+                  "for one `tgp_pipeline_step` on the GPU (weights drawn on the device; the "
+                  "3-channel first layer runs the direct kernels); allocated is torch's peak over "
+                  "creation, planning and the step, including the caller's tensors:", "",
+                  "| setting | (B, C) | parameters | planned | allocated peak | workspace | step |",
+                  "|---|---|---:|---:|---:|---:|---:|"]
+        for c in scale:
+            lines.append(f"| {c['setting']} | ({c['blocks']}, {c['channels']}) | "
+                         f"{c['params'] / 1e9:.2f}B | {c['planned_gb']:.3f} GB | "
+                         f"{c['allocated_gb']:.3f} GB | {c['workspace_gb']:.3f} GB | "
+                         f"{c['step_s']:.2f} s |")
     check = memory_check()
     if check:
         lines += ["", "Planned against allocated memory on the GPU for the 5-level, 64-channel network "
@@ -591,7 +617,53 @@ def memory_report():
     os.makedirs(PROFILES, exist_ok=True)
     with open(os.path.join(PROFILES, "memory_unet.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
-    print(json.dumps({"largest": rows, "check": check}), flush=True)
+    print(json.dumps({"largest": rows, "check": check, "at_scale": scale}), flush=True)
+
+
+def memory_at_scale(budget=64e9):
+    """On a GPU: the largest U-Net of MEM_SHAPE that the planner fits in
+    `budget` bytes without checkpointing (m = 1) and with checkpointing at
+    m = 8, each created, planned and trained for one pipeline step; planned
+    bytes against torch's allocated peak."""
+    import torch
+    if not torch.cuda.is_available():
+        return None
+    from paper_2004_09910_amd.harness import Session
+    from workloads import specs
+    from workloads.specs import BF16, CKPT_ALWAYS, CKPT_NEVER
+    B, hw, in_ch, levels = (MEM_SHAPE[k] for k in ("B", "hw", "in_ch", "levels"))
+    out = []
+    for label, m, mode in [("no checkpointing, m = 1", 1, CKPT_NEVER),
+                           ("checkpointing (always), m = 8", 8, CKPT_ALWAYS)]:
+        blocks, C, acct = largest_unet(budget, m, mode, [64, 96, 128, 160, 192, 224, 256])
+        net = specs.unet(levels, C, in_ch, hw, f"unet6-B{blocks}-C{C}", blocks=blocks)
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+        torch.cuda.reset_peak_memory_stats()
+        base = torch.cuda.memory_allocated()
+        log(f"memory at scale: {label}: (B, C) = ({blocks}, {C}), {acct[0] / 1e9:.2f}B parameters")
+        sess = Session(net, BF16, n=1, init="device")
+        ws = sess.plan(B, m, mode)
+        x = torch.randn((B, hw, hw, in_ch), device="cuda").to(torch.bfloat16)
+        oh, ow = net.out_hw()
+        t = torch.randn((B, oh, ow, net.out_channels()), device="cuda").to(torch.bfloat16)
+        loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+        y = torch.empty_like(t)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        sess.pipeline_step(x, t, loss, y)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        peak = torch.cuda.max_memory_allocated() - base
+        log(f"  planned {acct[3] / 1e9:.3f} GB, allocated peak {peak / 1e9:.3f} GB, step {dt:.2f} s, "
+            f"loss {float(loss.item()):.4g}")
+        out.append({"setting": label, "budget_gb": budget / 1e9, "blocks": blocks, "channels": C,
+                    "params": acct[0], "planned_gb": acct[3] / 1e9, "allocated_gb": peak / 1e9,
+                    "workspace_gb": ws / 1e9, "step_s": dt, "loss": float(loss.item())})
+        sess.close()
+        del sess, x, t, y, loss
+        torch.cuda.empty_cache()
+    return out
 
 
 def memory_check():

@@ -59,9 +59,15 @@ class Session:
     def __init__(self, net: specs.Net, dtype: int, n: int = 1,
                  balance: Optional[Sequence[int]] = None, device: str = "cuda",
                  seed_offset: int = 0, bind_layers: Optional[Sequence[int]] = None,
-                 family: str = synth.NORMAL):
+                 family: str = synth.NORMAL, init: str = "seeded"):
+        """init = 'seeded': the seeded parameters of `family` (what the oracle
+        gets); 'device': He-normal weights and zero biases drawn on the device
+        by torch, for memory and throughput runs of models too large to draw
+        on the host (no oracle comparison possible)."""
+        assert init in ("seeded", "device"), init
         self.net, self.dtype, self.device = net, dtype, device
         self.family = family
+        self.init = init
         self.h = tgp.net_create([layer_tuple(L) for L in net.layers], net.in_channels,
                                 net.height, net.width, dtype)
         tgp.set_partition(self.h, n, balance)
@@ -85,16 +91,25 @@ class Session:
 
     def _bind_layer(self, idx: int, seed_offset: int):
         L = self.net.layers[idx]
-        (w64, wraw), b = synth.layer_params(self.net, idx, self.dtype, seed_offset, self.family)
-        wt = raw_to_torch(wraw, self.dtype)
-        if L.kind == DWCONV3X3:
-            wk = wt.reshape(L.cout, 9)
+        if self.init == "device":
+            shape = (L.cout, 9) if L.kind == DWCONV3X3 else (L.cout, 3 if L.taps == 9 else 1,
+                                                             3 if L.taps == 9 else 1, L.cin)
+            wk = (torch.randn(shape, device=self.device) * (2.0 / L.fan_in()) ** 0.5).to(
+                TORCH_DT[self.dtype])
+            bt = torch.zeros(L.cout, dtype=torch.float32, device=self.device) if L.bias else None
+            w64 = b = None
         else:
-            wk = wt.permute(0, 2, 3, 1)   # OIHW -> KRSC
-        wk = wk.contiguous().to(self.device)
-        bt = None if b is None else torch.from_numpy(b[1]).to(self.device)
+            (w64, wraw), b = synth.layer_params(self.net, idx, self.dtype, seed_offset,
+                                                self.family)
+            wt = raw_to_torch(wraw, self.dtype)
+            if L.kind == DWCONV3X3:
+                wk = wt.reshape(L.cout, 9)
+            else:
+                wk = wt.permute(0, 2, 3, 1)   # OIHW -> KRSC
+            wk = wk.contiguous().to(self.device)
+            bt = None if b is None else torch.from_numpy(b[1]).to(self.device)
         dw = torch.zeros(wk.shape, dtype=torch.float32, device=self.device)
-        db = None if b is None else torch.zeros(L.cout, dtype=torch.float32, device=self.device)
+        db = torch.zeros(L.cout, dtype=torch.float32, device=self.device) if L.bias else None
         tgp.bind_params(self.h, idx, wk.data_ptr(), None if bt is None else bt.data_ptr(),
                         dw.data_ptr(), None if db is None else db.data_ptr())
         self.params[idx] = {"w": wk, "b": bt, "dw": dw, "db": db, "w64": w64,
