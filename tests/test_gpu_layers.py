@@ -7,6 +7,7 @@ partition take the EXACT input family in bf16 (1e-6).  Shapes include
 ragged pixel tiles and the benchmark's own level-0 and deepest layer shapes
 at its micro-batch size."""
 import pytest
+import torch
 
 from gpu_util import check_stage, gpu_stage, gpu_stage_with_popped, oracle_stage, say
 from workloads import specs
@@ -86,6 +87,38 @@ def test_rows32_configurations(cfg, w, r):
         run_and_check(net, (1,), 1, BF16, 2, 1, f"rows32 cfg {cfg} 64->128 @{r + 1}x{w}")
     finally:
         tgp.debug_set_fwd_variant(old)
+
+
+@pytest.mark.parametrize("w,h", [(24, 25), (96, 13)])
+def test_rows32_configurations_agree_bitwise(w, h):
+    """Every configuration of the nine-tap kernel at one width sums each
+    output in the same order (16-channel chunk, tap, channel), whatever its
+    tile, fragment layout or wave count: forced one after another on the
+    same layer and inputs (H leaves a ragged last row block in each), they
+    give the same bits for y and dx_in."""
+    import paper_2004_09910_amd as tgp
+    cfgs = [(c, r) for c, cw, r in ROWS32 if cw == w]
+    net = one_layer(Layer(CONV3X3, 64, 128), h, w)
+    ref = None
+    for cfg, r in cfgs:
+        assert r < h and h % r
+        old = tgp.debug_set_fwd_variant(401 + cfg)
+        try:
+            say(f"rows32 cfg {cfg} @{h}x{w}")
+            tgp.profile_enable(True)
+            tgp.profile_read()
+            got = gpu_stage(net, BF16, 2, 1, 0, (1,), 1)
+            ran = {k["name"] for k in tgp.profile_read()}
+        finally:
+            tgp.profile_enable(False)
+            tgp.debug_set_fwd_variant(old)
+        got["sess"].close()
+        assert any(n.startswith(f"conv3x3_rows32<{w},{r},") for n in ran), ran
+        if ref is None:
+            ref = got
+            continue
+        for key in ("y", "dx"):
+            assert torch.equal(got[key], ref[key]), f"cfg {cfg} {key} differs from cfg {cfgs[0][0]}"
 
 
 @pytest.mark.parametrize("cfg,r", [(16, 2), (17, 3)])
