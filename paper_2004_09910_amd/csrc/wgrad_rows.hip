@@ -194,6 +194,10 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
     coords(0, i_kr, i_r, i_co0, i_ci0);
     i_ns = stages_of(i_kr);
   }
+  // A stage's DMA is issued all at once, right after the ring barrier of
+  // the stage NS - 1 before it.  (Spread over the k steps between the
+  // MFMAs, the memory pipeline's issue stalls held up the MFMAs: 25 to 60%
+  // slower.)
   auto issue = [&](int slot) __attribute__((always_inline)) {
     const bool g1 = i_kr >= kpg;                             // second micro-batch (uniform)
     const int krl = g1 ? i_kr - kpg : i_kr;
@@ -254,24 +258,33 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
       // issued after it are pending (epilogue stores only lengthen this wait)
       wait_ring(min(NS - 2, total - 1 - idx));
       ring_barrier();
-      if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);
+      if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);   // the slot freed last stage
       const unsigned char* sp = smem + (idx % NS) * SB;
-#pragma unroll
-      for (int tt = 0; tt < KT / KS; ++tt) {
-        // k step t: stage pixels 16 t .. 16 t + 15 (dZ rows are the pixel
-        // index); with KS = 2 this wave takes every other step
+      // k step t: stage pixels 16 t .. 16 t + 15 (dZ rows are the pixel
+      // index); with KS = 2 this wave takes every other step.  Step tt + 1's
+      // fragments are read while step tt's MFMAs run (left to itself the
+      // compiler waited for each MFMA's own reads right before it).
+      constexpr int NT = KT / KS;                               // this wave's k steps
+      bf16x8_t a[2], b[2][3];
+      auto load = [&](int tt, int buf) __attribute__((always_inline)) {
         const int t = KS * tt + (KS == 1 ? 0 : kh);
         const int ka = 16 * t * 128;
         int kx;
         if constexpr (KS == 1) kx = xoff(t);
         else kx = kh ? xoff(KS * tt + 1) : xoff(KS * tt);
-        const bf16x8_t a = frag2(tr16(sp + fa + ka), tr16(sp + fa + ka + 4 * 128));
-        bf16x8_t b[3];
+        a[buf] = frag2(tr16(sp + fa + ka), tr16(sp + fa + ka + 4 * 128));
 #pragma unroll
         for (int s = 0; s < 3; ++s)
-          b[s] = frag2(tr16(sp + fb[s] + kx), tr16(sp + fb[s] + kx + 4 * 128));
+          b[buf][s] = frag2(tr16(sp + fb[s] + kx), tr16(sp + fb[s] + kx + 4 * 128));
+      };
+      load(0, 0);
 #pragma unroll
-        for (int s = 0; s < 3; ++s) acc[s] = mfma32(a, b[s], acc[s]);
+      for (int tt = 0; tt < NT; ++tt) {
+        if (tt + 1 < NT) load(tt + 1, (tt + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int s = 0; s < 3; ++s) acc[s] = mfma32(a[tt & 1], b[tt & 1][s], acc[s]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
     if constexpr (KS == 2) {

@@ -328,6 +328,34 @@ def test_amoeba_cells_pairs_are_bit_identical():
     assert torch.equal(runs[1]["dx"], runs[0]["dx"])
 
 
+@pytest.mark.timeout(600)
+def test_five_level_unet_network():
+    """The whole benchmark network (5-level, 64-channel U-Net) at 64 x 64 in
+    the 4 partitions of its FLOP balance, trained for one step by
+    tgp_pipeline_step on exact inputs, B = 8: m = 2 and 4 under every
+    checkpoint mode, once on two lanes.  Loss, output and every weight and
+    bias gradient equal the oracle's full-batch run, so g = sum_i g_i holds
+    through all partitions and the runs agree bit for bit."""
+    net = specs.unet(5, 64, 64, 64, "unet5-c64-64")
+    B = 8
+    say("unet5 network oracle inputs (exact family)")
+    inputs = network_inputs(net, BF16, B, EXACT, log=say)
+    say("unet5 network oracle run")
+    ref = oracle_network(net, BF16, B, EXACT, inputs, certify=True, log=say)
+    runs = []
+    for m, mode, lanes in ((2, CKPT_ALWAYS, 1), (4, CKPT_ALWAYS, 2), (4, CKPT_EXCEPT_LAST, 1),
+                           (4, CKPT_NEVER, 1)):
+        what = f"unet5 network m={m} mode={mode} lanes={lanes}"
+        say(what)
+        got = gpu_network(net, BF16, B, m, 4, mode, lanes=lanes, family=EXACT, inputs=inputs)
+        assert tuple(got["sess"].balance) == (7, 5, 3, 4)
+        check_network(got, ref, BF16, what, EXACT)
+        got.pop("sess").close()
+        runs.append(got)
+    for r in runs[1:]:
+        same_bits(runs[0], r)
+
+
 @pytest.mark.timeout(1200)
 def test_six_level_unet_network():
     """The 6-level, 128-channel U-Net (128 -> 4096 channels, 503 M
