@@ -356,10 +356,13 @@ __global__ __launch_bounds__(256) void dw3_rows_k(const bf16_t* __restrict__ x0,
 // Depthwise 3x3 weight-gradient partials over bf16 NHWC (same shape rules
 // as dw3_rows_k).  Thread (column, pack) of block (chunk, strip) sums
 // dz[p] * x[p + tap] over the rows [h0, h0 + RS) of its column for its
-// eight channels and nine taps (x through the sliding window); the block
-// then adds its 256 / CP column groups in order in LDS and writes
-// part[blk][c * 9 + t], blk = strip block * chunks + chunk.  The partials
-// are summed in block order afterwards, so the result is deterministic.
+// eight channels and nine taps (x through the sliding window, the next
+// row's window and dz loaded while the current row's products run); the
+// block then adds its 256 / CP column groups in order in LDS, taps 0-4 and
+// then 5-8 through one buffer of a 41-float row per thread (the odd row
+// length keeps both the writes and the reads free of bank conflicts), and
+// writes part[blk][c * 9 + t], blk = strip block * chunks + chunk.  The partials are summed in block order
+// afterwards, so the result is deterministic.
 // gridDim.z (1 or 2) micro-batches: blockIdx.z selects (x0, dz0, part0) or
 // (x1, dz1, part1).
 template <int RS>
@@ -373,7 +376,9 @@ __global__ __launch_bounds__(256) void dw3_wgrad_rows_k(const bf16_t* __restrict
   const bf16_t* __restrict__ x = blockIdx.z ? x1 : x0;
   const bf16_t* __restrict__ dz = blockIdx.z ? dz1 : dz0;
   float* __restrict__ part = blockIdx.z ? part1 : part0;
-  __shared__ float red[72][256];
+  constexpr int TH = 5;                      // taps per reduction pass
+  constexpr int RW = TH * 8 + 1;             // floats per thread row
+  __shared__ float red[256][RW];
   const int CP = C >> 3;
   const int q = blockIdx.x * 256 + threadIdx.x;
   const int wc = q / CP, cp = q - (q / CP) * CP;
@@ -385,24 +390,39 @@ __global__ __launch_bounds__(256) void dw3_wgrad_rows_k(const bf16_t* __restrict
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[t][i] = 0.f;
   if (wc < W) {
-    const long base = (long)n * H * W * C + cp * 8;
-    const bf16_t* xn = x + base;
+    // buffer loads over the sample's image: an offset outside it reads
+    // zeros, so the halo needs no branches (a branch per load made the
+    // compiler wait for every load in flight, the prefetch included)
+    const int img = H * W * C * 2;                              // bytes per sample image
+    const long sb = (long)n * H * W * C;
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(x + sb), (short)0, img, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rz = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(dz + sb), (short)0, img, 0x00020000);
     auto ld = [&](int hh, int ww) __attribute__((always_inline)) {
-      return ((unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W)
-                 ? ld16(xn + ((long)hh * W + ww) * C)
-                 : make_uint4(0u, 0u, 0u, 0u);
+      const bool ok = (unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W;
+      const int off = ok ? ((hh * W + ww) * C + cp * 8) * 2 : (int)0x80000000;
+      return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0));
     };
-    uint4 win[3][3];
+    auto ldz = [&](int hh) __attribute__((always_inline)) {
+      const int off = hh < H ? ((hh * W + wc) * C + cp * 8) * 2 : (int)0x80000000;
+      return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rz, off, 0, 0));
+    };
+    const int h1 = min(h0 + RS, H);
+    uint4 win[3][3], nxt[3], dzc = ldz(h0);
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
       win[0][s] = ld(h0 - 1, wc + s - 1);
       win[1][s] = ld(h0, wc + s - 1);
+      win[2][s] = ld(h0 + 1, wc + s - 1);
     }
-    for (int h = h0; h < h0 + RS && h < H; ++h) {
+    for (int h = h0; h < h1; ++h) {
+      // next row's loads first: they arrive while this row's products run
 #pragma unroll
-      for (int s = 0; s < 3; ++s) win[2][s] = ld(h + 1, wc + s - 1);
+      for (int s = 0; s < 3; ++s) nxt[s] = ld(h + 2, wc + s - 1);
+      const uint4 dzn = ldz(h + 1);
       float d[8];
-      Pk<bf16_t>::un(ld16(dz + base + ((long)h * W + wc) * C), d);
+      Pk<bf16_t>::un(dzc, d);
 #pragma unroll
       for (int r = 0; r < 3; ++r)
 #pragma unroll
@@ -416,21 +436,29 @@ __global__ __launch_bounds__(256) void dw3_wgrad_rows_k(const bf16_t* __restrict
       for (int s = 0; s < 3; ++s) {
         win[0][s] = win[1][s];
         win[1][s] = win[2][s];
+        win[2][s] = nxt[s];
       }
+      dzc = dzn;
     }
   }
-#pragma unroll
-  for (int t = 0; t < 9; ++t)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) red[t * 8 + i][threadIdx.x] = acc[t][i];
-  __syncthreads();
   const int E = C * 9, NG = 256 / CP;
   float* out = part + ((long)blockIdx.y * gridDim.x + blockIdx.x) * E;
-  for (int e = threadIdx.x; e < E; e += 256) {
-    const int c = e / 9, t = e - (e / 9) * 9, pk = c >> 3, i = c & 7;
-    float s = 0.f;
-    for (int g = 0; g < NG; ++g) s += red[t * 8 + i][g * CP + pk];
-    out[e] = s;
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    const int t0 = pass * TH, nt = pass ? 9 - TH : TH;
+    if (pass) __syncthreads();                 // the first pass's reads are done
+#pragma unroll
+    for (int t = 0; t < TH; ++t)
+      if (t < nt)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) red[threadIdx.x][t * 8 + i] = acc[t0 + t][i];
+    __syncthreads();
+    for (int e = threadIdx.x; e < C * nt; e += 256) {
+      const int c = e / nt, t = e - (e / nt) * nt, pk = c >> 3, i = c & 7;
+      float s = 0.f;
+      for (int g = 0; g < NG; ++g) s += red[g * CP + pk][t * 8 + i];
+      out[c * 9 + t0 + t] = s;
+    }
   }
 }
 
