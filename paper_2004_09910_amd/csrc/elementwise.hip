@@ -312,21 +312,27 @@ __global__ __launch_bounds__(256) void dw3_rows_k(const bf16_t* __restrict__ x0,
   float bias[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) bias[i] = b ? b[cp * 8 + i] : 0.f;
-  const bf16_t* xn = x + (long)n * H * W * C + cp * 8;
+  // buffer loads over the sample's image: an offset outside it reads zeros,
+  // so the halo needs no branches and the next row's loads stay in flight
+  // while this row's products run
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(x + (long)n * H * W * C), (short)0, H * W * C * 2, 0x00020000);
   auto ld = [&](int hh, int ww) __attribute__((always_inline)) {
-    return ((unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W)
-               ? ld16(xn + ((long)hh * W + ww) * C)
-               : make_uint4(0u, 0u, 0u, 0u);
+    const bool ok = (unsigned)hh < (unsigned)H && (unsigned)ww < (unsigned)W;
+    const int off = ok ? ((hh * W + ww) * C + cp * 8) * 2 : (int)0x80000000;
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rx, off, 0, 0));
   };
-  uint4 win[3][3];
+  uint4 win[3][3], nxt[3];
 #pragma unroll
   for (int s = 0; s < 3; ++s) {
     win[0][s] = ld(h0 - 1, wc + s - 1);
     win[1][s] = ld(h0, wc + s - 1);
+    win[2][s] = ld(h0 + 1, wc + s - 1);
   }
-  for (int h = h0; h < h0 + RS && h < H; ++h) {
+  const int h1 = min(h0 + RS, H);
+  for (int h = h0; h < h1; ++h) {
 #pragma unroll
-    for (int s = 0; s < 3; ++s) win[2][s] = ld(h + 1, wc + s - 1);
+    for (int s = 0; s < 3; ++s) nxt[s] = ld(h + 2, wc + s - 1);
     float acc[8];
 #pragma unroll
     for (int i = 0; i < 8; ++i) acc[i] = 0.f;
@@ -349,6 +355,7 @@ __global__ __launch_bounds__(256) void dw3_rows_k(const bf16_t* __restrict__ x0,
     for (int s = 0; s < 3; ++s) {
       win[0][s] = win[1][s];
       win[1][s] = win[2][s];
+      win[2][s] = nxt[s];
     }
   }
 }
@@ -466,12 +473,13 @@ constexpr int kDwRows = 4;       // output rows per thread, forward and data gra
 constexpr int kDwWgradRows = 8;  // rows per thread of the weight gradient
 
 // The row-window depthwise kernels apply: bf16, whole 16-byte packs, a pack
-// count dividing the block, and 16-byte aligned tensors and weights.
-static bool dw3_rows_ok(int dt, int nb, int H, int C, const void* a, const void* b2,
+// count dividing the block, 16-byte aligned tensors and weights, and a
+// sample image under 2 GiB (their buffer loads take 32-bit offsets).
+static bool dw3_rows_ok(int dt, int nb, int H, int W, int C, const void* a, const void* b2,
                         const void* c2) {
   auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
   return dt == 0 && C > 0 && C % 8 == 0 && 256 % (C / 8) == 0 && al(a) && al(b2) && al(c2) &&
-         (long)nb * cdiv(H, kDwRows) <= 65535;
+         (long)nb * cdiv(H, kDwRows) <= 65535 && 2.0 * H * W * C < 2147483648.0;
 }
 
 static int dw3_wgrad_blocks(int nb, int H, int W, int C) {
@@ -1136,9 +1144,9 @@ hipError_t conv_wgrad2(int dt, const void* x0, const void* x1, const void* dz0, 
 
 // The row-window depthwise kernels over one or two micro-batches (x1 null:
 // one); false where they do not apply.
-bool dw_pair_ok(int dt, int nb, int H, int C, const void* a0, const void* a1, const void* b0,
-                const void* b1, const void* c) {
-  return dw3_rows_ok(dt, nb, H, C, a0, b0, c) && dw3_rows_ok(dt, nb, H, C, a1, b1, c);
+bool dw_pair_ok(int dt, int nb, int H, int W, int C, const void* a0, const void* a1,
+                const void* b0, const void* b1, const void* c) {
+  return dw3_rows_ok(dt, nb, H, W, C, a0, b0, c) && dw3_rows_ok(dt, nb, H, W, C, a1, b1, c);
 }
 
 hipError_t dw_forward2(const void* x0, const void* x1, const void* w, const float* b, void* y0,
@@ -1192,7 +1200,7 @@ hipError_t dw_wgrad2(const void* x0, const void* x1, const void* dz0, const void
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
                       int H, int W, int C, int relu, hipStream_t st) {
   long P = (long)nb * H * W;
-  if (dw3_rows_ok(dt, nb, H, C, x, w, y))
+  if (dw3_rows_ok(dt, nb, H, W, C, x, w, y))
     return dw_forward2(x, nullptr, w, b, y, nullptr, nb, H, W, C, relu, st);
   dim3 g(cdiv(P * C, 256));
   ProfScope ps("dw_forward", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
@@ -1208,7 +1216,7 @@ hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void
 hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int H, int W,
                     int C, hipStream_t st) {
   long P = (long)nb * H * W;
-  if (dw3_rows_ok(dt, nb, H, C, dz, w, dx))
+  if (dw3_rows_ok(dt, nb, H, W, C, dz, w, dx))
     return dw_dgrad2(dz, nullptr, w, dx, nullptr, nb, H, W, C, st);
   dim3 g(cdiv(P * C, 256));
   ProfScope ps("dw_dgrad", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
@@ -1234,7 +1242,7 @@ hipError_t dw_wgrad(int dt, const void* x, const void* dz, float* dw, float* par
                     int H, int W, int C, hipStream_t st) {
   long P = (long)nb * H * W;
   long E = (long)C * 9;
-  if (dw3_rows_ok(dt, nb, H, C, x, dz, partial) && P > 0)
+  if (dw3_rows_ok(dt, nb, H, W, C, x, dz, partial) && P > 0)
     return dw_wgrad2(x, nullptr, dz, nullptr, dw, nullptr, partial, nullptr, nb, H, W, C, st);
   long pps = direct_wgrad_pps(P);
   int S = direct_wgrad_splits(P);

@@ -110,8 +110,8 @@ size_t dw_wgrad_partial_floats(int nb, int H, int W, int C);
 // Two micro-batches per launch for the bf16 row-window depthwise kernels,
 // where dw_pair_ok holds for both micro-batches' tensors (a*, b*) and the
 // weights c.
-bool dw_pair_ok(int dt, int nb, int H, int C, const void* a0, const void* a1, const void* b0,
-                const void* b1, const void* c);
+bool dw_pair_ok(int dt, int nb, int H, int W, int C, const void* a0, const void* a1,
+                const void* b0, const void* b1, const void* c);
 hipError_t dw_forward2(const void* x0, const void* x1, const void* w, const float* b, void* y0,
                        void* y1, int nb, int H, int W, int C, int relu, hipStream_t st);
 hipError_t dw_dgrad2(const void* dz0, const void* dz1, const void* w, void* dx0, void* dx1,

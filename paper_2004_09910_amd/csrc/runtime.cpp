@@ -297,7 +297,7 @@ tgp_status run_forward_g(tgp_net* N, int j, int cnt, const int* iv, const int* p
                                     Lr.inC, st),
              "maxpool_forward");
     if (d.kind == TGP_DWCONV3X3 && cnt == 2 &&
-        tgpk::dw_pair_ok(N->dt, N->b, Lr.H, d.cout, cin_ptr[0], cin_ptr[1], out[0], out[1],
+        tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[0], cin_ptr[1], out[0], out[1],
                          Lr.w)) {
       HIPCHK(tgpk::dw_forward2(cin_ptr[0], cin_ptr[1], Lr.w, d.bias ? Lr.b : nullptr, out[0],
                                out[1], N->b, Lr.H, Lr.W, d.cout, d.relu, st),
@@ -567,10 +567,10 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
                                &(*pjs[1])[0]),
              "conv_wgrad2");
     } else if (d.kind == TGP_DWCONV3X3 && cnt == 2 &&
-               tgpk::dw_pair_ok(N->dt, N->b, Lr.H, d.cout, cin_ptr[0], cin_ptr[1], dzk[0], dzk[1],
-                                M[0].part) &&
-               tgpk::dw_pair_ok(N->dt, N->b, Lr.H, d.cout, cin_ptr[0], cin_ptr[1], dzk[0], dzk[1],
-                                M[1].part)) {
+               tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[0], cin_ptr[1], dzk[0],
+                                dzk[1], M[0].part) &&
+               tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[0], cin_ptr[1], dzk[0],
+                                dzk[1], M[1].part)) {
       HIPCHK(tgpk::dw_wgrad2(cin_ptr[0], cin_ptr[1], dzk[0], dzk[1],
                              (float*)G_(N, M[0].i, Lr.o_gw), (float*)G_(N, M[1].i, Lr.o_gw),
                              M[0].part, M[1].part, N->b, Lr.H, Lr.W, d.cout, st),
@@ -600,8 +600,8 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
       dgrad_out[k] = d.prologue == TGP_PRO_NONE ? dest_prev[k] : M[k].dinp;
     }
     if (d.kind == TGP_DWCONV3X3 && cnt == 2 &&
-        tgpk::dw_pair_ok(N->dt, N->b, Lr.H, d.cout, dzk[0], dzk[1], dgrad_out[0], dgrad_out[1],
-                         Lr.w)) {
+        tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, dzk[0], dzk[1], dgrad_out[0],
+                         dgrad_out[1], Lr.w)) {
       HIPCHK(tgpk::dw_dgrad2(dzk[0], dzk[1], Lr.w, dgrad_out[0], dgrad_out[1], N->b, Lr.H, Lr.W,
                              d.cout, st),
              "dw_dgrad");
