@@ -283,6 +283,17 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_dma(
 #pragma unroll
   for (int s = 0; s < NS - 1; ++s)
     if (s < nk) issue(s, s);
+  // this lane's bias values for the epilogue, loaded up front as 16-byte
+  // vectors (channels co0 + wco TM 32 + 32 i + 8 g + 4 (lane / 32) + t);
+  // loaded one by one at the epilogue they held up every store
+  f32x4_t bv[TM][4];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      bv[i][g] = bias ? *(const f32x4_t*)(bias + co0 + wco * TM * 32 + i * 32 + 8 * g +
+                                          4 * (lane >> 5))
+                      : f32x4_t{};
   for (int ks = 0; ks < nk; ++ks) {
     const int ahead = min(NS - 2, nk - 1 - ks);
     wait_stages<NS, LPS>(ahead);
@@ -331,8 +342,7 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_dma(
         float v[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-          v[t] = acc[i][j][4 * g + t];
-          if (bias) v[t] += bias[co + t];
+          v[t] = acc[i][j][4 * g + t] + bv[i][g][t];
           if (relu) v[t] = fmaxf(v[t], 0.0f);
         }
         uint2 o;
@@ -449,6 +459,16 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_rows(
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = f32x16_t{};
+  // this lane's bias values for the epilogue, loaded up front (channels
+  // co0 + wco TM 32 + 32 i + 8 g + 4 (lane / 32) + t)
+  f32x4_t bv[TM][4];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      bv[i][g] = (!SPLIT && bias) ? *(const f32x4_t*)(bias + co0 + wco * TM * 32 + i * 32 +
+                                                     8 * g + 4 * (lane >> 5))
+                                  : f32x4_t{};
 
   const int n = s_end - s_begin;
 #pragma unroll
@@ -523,8 +543,7 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_rows(
           float v[4];
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
-            v[t] = acc[i][j][4 * g + t];
-            if (bias) v[t] += bias[co + t];
+            v[t] = acc[i][j][4 * g + t] + bv[i][g][t];
             if (relu) v[t] = fmaxf(v[t], 0.0f);
           }
           uint2 o;
