@@ -329,26 +329,41 @@ __global__ __launch_bounds__(WCO * WP * 64) void conv_fwd_dma(
     }
   }
 
+  // Epilogue: lanes l and l + 32 hold channels 8 g + 0..3 and 8 g + 4..7
+  // of pixel l % 32.  Swapping the halves of groups 2 h and 2 h + 1 across
+  // the two half-waves leaves lane l with channels 16 h + 0..7 and lane
+  // l + 32 with 16 h + 8..15, so each lane stores 16 contiguous bytes
+  // (scattered 8-byte stores cost a memory-pipeline cycle per lane).
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
       const int p = p0 + wp * TN * 32 + j * 32 + (lane & 31);
-      if (p >= P) continue;
-      bf16_t* yrow = Y + (long)p * Cout;
+      unsigned pk[4][2];
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        const int co = co0 + wco * TM * 32 + i * 32 + 8 * g + 4 * (lane >> 5);
         float v[4];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
           v[t] = acc[i][j][4 * g + t] + bv[i][g][t];
           if (relu) v[t] = fmaxf(v[t], 0.0f);
         }
-        uint2 o;
-        o.x = f2bf(v[0]) | (f2bf(v[1]) << 16);
-        o.y = f2bf(v[2]) | (f2bf(v[3]) << 16);
-        *(uint2*)(yrow + co) = o;
+        pk[g][0] = f2bf(v[0]) | (f2bf(v[1]) << 16);
+        pk[g][1] = f2bf(v[2]) | (f2bf(v[3]) << 16);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const auto sw = __builtin_amdgcn_permlane32_swap(pk[2 * h][r], pk[2 * h + 1][r], false,
+                                                           false);
+          pk[2 * h][r] = sw[0];
+          pk[2 * h + 1][r] = sw[1];
+        }
+        const int co = co0 + wco * TM * 32 + i * 32 + 16 * h + 8 * (lane >> 5);
+        if (p < P)
+          *(u32x4*)(Y + (long)p * Cout + co) =
+              u32x4{pk[2 * h][0], pk[2 * h][1], pk[2 * h + 1][0], pk[2 * h + 1][1]};
       }
     }
   }
