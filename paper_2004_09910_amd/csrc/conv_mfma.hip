@@ -601,6 +601,144 @@ __global__ __launch_bounds__(256) void conv_rows_epilogue(const float* __restric
   *(u32x4*)(Y + e) = o;
 }
 
+// ---------------------------------------------------------------- 1x1, resident weights
+
+// 1x1 convolution y[p][co] = act(sum_ci x[p][ci] w[co][ci] + b[co]) with
+// Cout = 256 and Cin a multiple of 64 up to 256 (the depthwise/pointwise
+// cells): a GEMM whose K is short, so a block with a tile of weights has
+// little work per byte of weights it loads.  Here each block loads the
+// whole weight matrix into LDS once (256 rows of Cin channels, in the
+// 64-channel stage blocks and 16-byte-chunk swizzle of conv_fwd_dma) and
+// then streams tiles of 64 pixels through an NS-deep ring of 64-channel
+// stages.  Wave w computes output channels 32 w .. 32 w + 31 of the tile's
+// 64 pixels (two 32 x 32 MFMA tiles), so every pixel row is read once.
+// The K order (64-channel stages, 16-channel MFMA steps, increasing
+// channel) is conv_fwd_dma's, so both kernels give the same bits.  Blocks
+// are persistent over the tiles of both micro-batches (X2 / Y2: a second
+// micro-batch of P pixels, its tiles after the first's).
+template <int NS>
+__global__ __launch_bounds__(512) void conv1x1_res(
+    const bf16_t* __restrict__ X0, const bf16_t* __restrict__ X2, const bf16_t* __restrict__ Wt,
+    const float* __restrict__ bias, bf16_t* __restrict__ Y0, bf16_t* __restrict__ Y2, int P,
+    int Cin, int relu) {
+  constexpr int COUT = 256, BM = 64, NW = 8;
+  __shared__ u32x4 smem[(4 * COUT + NS * BM) * 8];             // weights, then the ring
+  u32x4* const ring = smem + 4 * COUT * 8;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nks = Cin / 64;                                     // stages per tile
+  const int T1 = (P + BM - 1) / BM;                             // tiles per micro-batch
+  const int T = X2 ? 2 * T1 : T1;
+  const int G = gridDim.x;
+  const int lb = xcd_remap(blockIdx.x, G);
+  const int n_mine = lb < T ? (T - lb + G - 1) / G : 0;
+  const int total = n_mine * nks;
+
+  // DMA: one wave instruction fills 8 rows of 128 bytes; lane l the 16
+  // bytes of physical chunk l & 7 of row l >> 3, holding logical chunk c.
+  const int rsub = lane >> 3;
+  // weights: row R = 256 s + co of stage block s
+  for (int u = 0; u < nks * COUT / 8 / NW; ++u) {
+    const int R = (wave + NW * u) * 8 + rsub;
+    const int sblk = R / COUT, co = R - sblk * COUT;
+    const int c = (lane & 7) ^ ((R ^ (R >> 3)) & 7);
+    __builtin_amdgcn_global_load_lds((const void*)(Wt + (long)co * Cin + sblk * 64 + c * 8),
+                                     TGP_LDS(&smem[(wave + NW * u) * 64]), 16, 0, 0);
+  }
+  // the X ring: stage idx of this block is tile lb + (idx / nks) G, stage
+  // idx % nks; row r = wave * 8 + rsub of the slot is pixel p0 + r
+  const int xr = wave * 8 + rsub;
+  const int xc = (lane & 7) ^ ((xr ^ (xr >> 3)) & 7);
+  auto issue = [&](int idx) __attribute__((always_inline)) {
+    const int tt = lb + (idx / nks) * G, ks = idx - (idx / nks) * nks;
+    const bool g1 = tt >= T1;                                   // uniform
+    const bf16_t* X = g1 ? X2 : X0;
+    const int p = min((g1 ? tt - T1 : tt) * BM + xr, P - 1);    // rows past P: any pixel
+    __builtin_amdgcn_global_load_lds((const void*)(X + (long)p * Cin + ks * 64 + xc * 8),
+                                     TGP_LDS(&ring[(idx % NS) * BM * 8 + wave * 64]), 16, 0, 0);
+  };
+#pragma unroll
+  for (int k = 0; k < NS - 1; ++k)
+    if (k < total) issue(k);
+
+  // this lane's bias values (channels 32 wave + 8 g + 4 (lane / 32) + t)
+  f32x4_t bv[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+    bv[g] = bias ? *(const f32x4_t*)(bias + 32 * wave + 8 * g + 4 * (lane >> 5)) : f32x4_t{};
+
+  int idx = 0;
+  for (int it = 0; it < n_mine; ++it) {
+    const int tt = lb + it * G;
+    const bool g1 = tt >= T1;
+    bf16_t* __restrict__ Y = g1 ? Y2 : Y0;
+    const int p0 = (g1 ? tt - T1 : tt) * BM;
+    f32x16_t acc[2] = {f32x16_t{}, f32x16_t{}};
+    for (int ks = 0; ks < nks; ++ks, ++idx) {
+      // loads complete in order (the weights first); epilogue stores only
+      // lengthen this wait
+      wait_stages<NS, 1>(min(NS - 2, total - 1 - idx));
+      ring_barrier();
+      if (idx + NS - 1 < total) issue(idx + NS - 1);
+      const u32x4* As = smem + ks * COUT * 8;
+      const u32x4* Bs = ring + (idx % NS) * BM * 8;
+      bf16x8_t a[2], b[2][2];
+      auto load = [&](int kk, int buf) __attribute__((always_inline)) {
+        const int qq = 2 * kk + (lane >> 5);
+        const int ra = 32 * wave + (lane & 31);
+        a[buf] = as_bf16x8(As[ra * 8 + swz(ra, qq)]);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int rb = 32 * j + (lane & 31);
+          b[buf][j] = as_bf16x8(Bs[rb * 8 + swz(rb, qq)]);
+        }
+      };
+      load(0, 0);
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        if (kk + 1 < 4) load(kk + 1, (kk + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[j] = mfma32(a[kk & 1], b[kk & 1][j], acc[j]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // Epilogue: lanes l and l + 32 hold channels 8 g + 0..3 and 8 g + 4..7
+    // of pixel l % 32; swapping the halves of groups 2 h and 2 h + 1 across
+    // the half-waves leaves each lane 8 consecutive channels, one 16-byte
+    // store.
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int p = p0 + 32 * j + (lane & 31);
+      unsigned pk[4][2];
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        float v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          v[t] = acc[j][4 * g + t] + bv[g][t];
+          if (relu) v[t] = fmaxf(v[t], 0.0f);
+        }
+        pk[g][0] = f2bf(v[0]) | (f2bf(v[1]) << 16);
+        pk[g][1] = f2bf(v[2]) | (f2bf(v[3]) << 16);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          const auto sw = __builtin_amdgcn_permlane32_swap(pk[2 * h][r], pk[2 * h + 1][r], false,
+                                                           false);
+          pk[2 * h][r] = sw[0];
+          pk[2 * h + 1][r] = sw[1];
+        }
+        if (p < P)
+          *(u32x4*)(Y + (long)p * COUT + 32 * wave + 16 * h + 8 * (lane >> 5)) =
+              u32x4{pk[2 * h][0], pk[2 * h][1], pk[2 * h + 1][0], pk[2 * h + 1][1]};
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- forward, persistent row-stage 3x3
 
 // XOR swizzle of the four 16-byte chunks of a 64-byte LDS row: eight
@@ -1258,9 +1396,32 @@ int g_rowtile_mask = 15;
 thread_local int t_in_dgrad = 0;
 
 struct FwdPlan {
-  int cfg;   // 1..: row-stage configurations; 100+: per-tap; 200+: persistent row-stage
+  int cfg;   // 1..: row-stage configurations; 100+: per-tap (150: 1x1 with resident
+             // weights); 200+: persistent row-stage
   int S;
 };
+
+// The resident-weight 1x1 kernel's shapes (its static LDS holds 256 x 256
+// weights) and its launch.
+static bool conv1x1_res_ok(const ConvShape& s) {
+  return s.taps == 1 && s.cout == 256 && s.cin % 64 == 0 && s.cin <= 256 && s.pixels() > 0;
+}
+
+static hipError_t launch_1x1_res(const bf16_t* X, const bf16_t* X2, const bf16_t* Wt,
+                                 const float* b, bf16_t* Y, bf16_t* Y2, const ConvShape& s,
+                                 int relu, hipStream_t st) {
+  if (!conv1x1_res_ok(s) || (X2 == nullptr) != (Y2 == nullptr)) return hipErrorInvalidValue;
+  const long P = s.pixels();
+  if (P > (1L << 30)) return hipErrorInvalidValue;              // pixel index is an int
+  const int ng = X2 ? 2 : 1;
+  const long T = ng * ((P + 63) / 64);
+  const int G = (int)(T < 256 ? T : 256);
+  ProfScope ps("conv1x1_res", 2.0 * ng * P * s.cout * s.cin,
+               2.0 * ((double)ng * P * (s.cin + s.cout) + (double)s.cout * s.cin), st);
+  TGP_LAUNCH(ps, conv1x1_res<3>, dim3(G), dim3(512), 0, st, X, X2, Wt, b, Y, Y2, (int)P, s.cin,
+             relu);
+  return launch_status();
+}
 
 struct PersTile { int BN, BM; };
 PersTile pers_tile(int cfg) {
@@ -1302,10 +1463,13 @@ FwdPlan fwd_plan(const ConvShape& s) {
     pl.cfg = 203;  // persistent row-stage, 64 x 256
   } else if (k3 && P <= 16384 && s.cin >= 256 && s.cout % 128 == 0) {
     pl.cfg = 207;  // persistent row-stage, 128 x 256, 8 waves
+  } else if (conv1x1_res_ok(s)) {
+    pl.cfg = 150;  // 1x1, all weights resident in LDS
   } else {
     pl.cfg = 100;
   }
   if (g_fwd_variant > 0) pl.cfg = g_fwd_variant;
+  if (pl.cfg == 150 && !conv1x1_res_ok(s)) pl.cfg = 100;
   if (pl.cfg >= 400) {
     g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
     if (!conv_rows32_ok(s)) pl.cfg = 100;
@@ -1366,6 +1530,7 @@ hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void*
   bf16_t* Y2 = nullptr;
   const FwdPlan pl = fwd_plan(s);
   const bool wide = s.cout % 128 == 0;
+  if (pl.cfg == 150) return launch_1x1_res(X, nullptr, Wt, b, Y, nullptr, s, relu, st);
   if (pl.cfg >= 400) {
     g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
     const hipError_t e = conv_forward_rows32(x, w, b, y, s, relu, st);
@@ -1541,6 +1706,9 @@ hipError_t conv_forward_mfma2(const void* x0, const void* x1, const void* w, con
                               void* y0, void* y1, const ConvShape& s, int relu, float* part0,
                               float* part1, size_t part_cap, hipStream_t st) {
   const FwdPlan pl = fwd_plan(s);
+  if (pl.cfg == 150)
+    return launch_1x1_res((const bf16_t*)x0, (const bf16_t*)x1, (const bf16_t*)w, b, (bf16_t*)y0,
+                          (bf16_t*)y1, s, relu, st);
   if (pl.cfg >= 400) {
     g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
     const hipError_t e = conv_forward_rows32(x0, w, b, y0, s, relu, st, x1, y1);

@@ -192,6 +192,33 @@ def test_conv1x1_and_depthwise():
     run_and_check(net, (1,), 1, BF16, 4, 2, "dwconv3x3 256 @14x14")
 
 
+@pytest.mark.parametrize("cin,h,w,B,m", [(256, 20, 20, 2, 1), (128, 9, 7, 4, 2), (64, 56, 56, 4, 2)])
+def test_conv1x1_resident_weights(cin, h, w, B, m):
+    """The 1x1 kernel with all weights resident in LDS (256 output
+    channels): against the oracle on y, dx, dW and db, with a ragged last
+    64-pixel tile; and bit for bit the same y and dx as the per-tap kernel
+    (forced), whose K order it shares."""
+    import paper_2004_09910_amd as tgp
+    net = one_layer(Layer(CONV1X1, cin, 256), h, w)
+    tgp.profile_enable(True)
+    tgp.profile_read()
+    try:
+        run_and_check(net, (1,), 1, BF16, B, m, f"conv1x1_res {cin}->256 @{h}x{w} B={B} m={m}")
+        ran = {k["name"] for k in tgp.profile_read()}
+    finally:
+        tgp.profile_enable(False)
+    assert "conv1x1_res" in ran, ran
+    got = gpu_stage(net, BF16, B, m, 0, (1,), 1)
+    got["sess"].close()
+    old = tgp.debug_set_fwd_variant(101)
+    try:
+        ref = gpu_stage(net, BF16, B, m, 0, (1,), 1)
+    finally:
+        tgp.debug_set_fwd_variant(old)
+    ref["sess"].close()
+    assert torch.equal(got["y"], ref["y"]) and torch.equal(got["dx"], ref["dx"])
+
+
 @pytest.mark.parametrize("c,h,w,relu", [(64, 15, 9, True), (16, 7, 33, False), (2048, 5, 5, True),
                                          (24, 6, 6, True)])
 def test_depthwise_shapes(c, h, w, relu):
