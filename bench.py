@@ -181,11 +181,11 @@ def summarize_profiles(out_dir, workload):
     f_write = gib_kib / cw[copy_k[0]]
     fb = fetch[top] * 1024 * f_fetch
     wb = write[top] * 1024 * f_write
-    pairs = False
+    group = 1
     for line in open(os.path.join(out_dir, "prof_fetch.log")):
         if line.startswith("{"):
-            pairs = bool(_json.loads(line)["config"].get("pairs", False))
-    info = {"kernel": top, "workload": workload, "pairs": pairs, "fetch_bytes": fb, "write_bytes": wb,
+            group = int(_json.loads(line)["config"].get("group", 1))
+    info = {"kernel": top, "workload": workload, "group": group, "fetch_bytes": fb, "write_bytes": wb,
             "bytes_per_launch": fb + wb, "dispatches": nf.get(top, 0),
             "fetch_scale": f_fetch, "write_scale": f_write, "source_hash": kernel_source_hash(top)}
     tl = [f"# HBM traffic of `{top}`: {workload}", "",
@@ -197,7 +197,7 @@ def summarize_profiles(out_dir, workload):
            f"a 1 GiB device copy reads {cf[copy_k[0]]:.1f} KiB, so the scale is {f_fetch:.4f}.",
            f"- WRITE_SIZE, mean per dispatch: {write[top]:.1f} KiB over {nw.get(top, 0)} dispatches; "
            f"the copy writes {cw[copy_k[0]]:.1f} KiB, scale {f_write:.4f}.",
-           f"- Launches: {'two micro-batches' if pairs else 'one micro-batch'} per launch.",
+           f"- Launches: {group} micro-batch{'es' if group > 1 else ''} per launch.",
            f"- HBM bytes per launch: {fb / 1e6:.2f} MB read + {wb / 1e6:.2f} MB written = "
            f"{(fb + wb) / 1e6:.2f} MB.", "",
            "Other kernels of the same runs (mean KiB per dispatch, unscaled):", "",
@@ -303,7 +303,7 @@ def summarize_counters(out_dir, workload, eager_us=None):
     return rows
 
 
-def recorded_traffic(kernel, workload, pairs):
+def recorded_traffic(kernel, workload, group):
     """HBM bytes per launch of `kernel` from a profiles/ summary taken with
     the current kernel sources and the same micro-batches per launch, else
     None."""
@@ -318,7 +318,7 @@ def recorded_traffic(kernel, workload, pairs):
             if line.startswith("traffic_json: "):
                 info = _json.loads(line[len("traffic_json: "):])
                 if info.get("kernel") == kernel and info.get("workload") == workload and \
-                        info.get("source_hash") == cur and info.get("pairs", False) == pairs:
+                        info.get("source_hash") == cur and info.get("group", 1) == group:
                     return info["bytes_per_launch"]
     return None
 
@@ -360,7 +360,7 @@ def network_bench(args, wl, mode):
     from workloads import specs, synth
     from workloads.specs import BF16
     net, B, m = wl.net, wl.batch, wl.m
-    lanes = args.lanes if m > 1 else 1
+    lanes = (args.lanes or 2) if m > 1 else 1
     log("setting up", wl.name)
     sess = Session(net, BF16, n=wl.n)
     sess.plan(B, m, mode, lanes)
@@ -855,14 +855,15 @@ def main():
                          "and the 6-level U-Net network print a line of their own")
     ap.add_argument("--mode", default=None, choices=["always", "except_last", "never"],
                     help="checkpoint mode (default: the workload's own)")
-    ap.add_argument("--lanes", type=int, default=2,
-                    help="concurrency lanes: micro-batch i runs on stream (i - 1) %% lanes")
-    ap.add_argument("--no-pairs", dest="pairs", action="store_false",
-                    help="one micro-batch per launch (default: two per launch when lanes and m "
-                         "are even)")
+    ap.add_argument("--lanes", type=int, default=None,
+                    help="concurrency lanes: micro-batch i runs on stream (i - 1) %% lanes "
+                         "(default: the group size, at least 2)")
+    ap.add_argument("--group", type=int, default=4, choices=[1, 2, 4],
+                    help="micro-batches per stage call and kernel launch (halved until it "
+                         "divides the lanes and m)")
     ap.add_argument("--one-stream", dest="one_stream", action="store_true", default=None,
                     help="issue the whole step on one stream, accumulations included (the "
-                         "default with two micro-batches per launch)")
+                         "default with several micro-batches per launch)")
     ap.add_argument("--lane-streams", dest="one_stream", action="store_false",
                     help="issue micro-batches on lane streams and the accumulations on one more "
                          "stream (the default with one micro-batch per launch)")
@@ -932,14 +933,17 @@ def main():
     log("setting up", wl.name)
     sess = Session(net, BF16, n=wl.n, bind_layers=None)
     lo, hi = sess.bounds[0]
+    if args.lanes is None:
+        args.lanes = max(2, args.group)
+    while args.group > 1 and (min(args.lanes, wl.m) % args.group or wl.m % args.group):
+        args.group //= 2
     sess.plan(wl.batch, wl.m, mode, args.lanes)
-    args.pairs = args.pairs and min(args.lanes, wl.m) % 2 == 0 and wl.m % 2 == 0
-    sess.pairs = args.pairs
+    sess.group = args.group
     if args.one_stream is None:
         # measured: with two micro-batches per launch the accumulations on a
         # stream of their own slow the persistent convolutions they overlap
         # more than they gain; with one per launch, two lane streams win
-        args.one_stream = args.pairs
+        args.one_stream = args.group > 1
     B, m = wl.batch, wl.m
     _, xraw = synth.input_x(net, B, BF16)
     x = nchw_to_device_nhwc(xraw, BF16)
@@ -1027,11 +1031,11 @@ def main():
             f"{(r['bytes'] / (r['ms'] * 1e-3) / 1e9) if r['ms'] > 0 else 0:8.1f} GB/s")
     dom = stats[0]
     roof = roofline_of(dom, per_step_div)
-    roof["traffic"] = recorded_traffic(dom["name"], wl.name, args.pairs)
+    roof["traffic"] = recorded_traffic(dom["name"], wl.name, args.group)
     roof["timed"] = "eager pass of the step on one stream, each launch timed alone" \
         if graph is not None else "the timed eager steps"
-    if args.pairs:
-        roof["timed"] += "; two micro-batches per launch"
+    if args.group > 1:
+        roof["timed"] += f"; {args.group} micro-batches per launch"
     kernel_ms = sum(r["ms"] for r in stats) / per_step_div
 
     out = {
@@ -1043,7 +1047,7 @@ def main():
                    "layers": hi - lo, "global_batch": B, "micro_batches": m,
                    "checkpoint": args.mode, "input": f"{B}x{net.in_channels}x{net.height}x{net.width}",
                    "dx_in": True, "launch": "hip_graph" if graph is not None else "eager",
-                   "lanes": args.lanes, "pairs": args.pairs, "one_stream": args.one_stream},
+                   "lanes": args.lanes, "group": args.group, "one_stream": args.one_stream},
         "mfma_util_pct": 100.0 * step_flops / (ms_step * 1e-3) / BF16_PEAK,
         "step_tflop": step_flops / 1e12,
         "kernel_busy_ms_per_step": kernel_ms,

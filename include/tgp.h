@@ -239,6 +239,24 @@ tgp_status tgp_stage_forward2(tgp_net* net, int j, int i0, int i1, int checkpoin
 tgp_status tgp_stage_backward_recompute2(tgp_net* net, int j, int i0, int i1, const void* dy0,
                                          const void* dy1, void* dx0, void* dx1, void* stream);
 
+/* The same for a group of count (1..4) tasks: tgp_stage_forward_n runs
+ * F_{i,j} for i = i0, i0 + 1, .., i0 + count - 1 (checkpoint[k], x_in[k]
+ * and y_out[k] belong to micro-batch i0 + k), and
+ * tgp_stage_backward_recompute_n runs F'_{i,j} + B_{i,j} for i = i0, i0 - 1,
+ * .., i0 - count + 1 (dy_out[k] and dx_in[k] belong to micro-batch i0 - k),
+ * each layer's convolutions as one launch over the whole group where the
+ * kernel takes that many tensors, else as launches of two and one.  Each
+ * micro-batch's arguments, checks and results are those of the single-task
+ * call (bit-identical values).  The group's micro-batches must be on
+ * different lanes: count <= lanes (EINVAL otherwise); a backward group of
+ * two or more needs per-micro-batch gradient slots (two or more lanes).
+ * dx_in[k] are all NULL or all set.  The arrays hold count entries. */
+tgp_status tgp_stage_forward_n(tgp_net* net, int j, int i0, int count, const int* checkpoint,
+                               const void* const* x_in, void* const* y_out, void* stream);
+tgp_status tgp_stage_backward_recompute_n(tgp_net* net, int j, int i0, int count,
+                                          const void* const* dy_out, void* const* dx_in,
+                                          void* stream);
+
 /* g^j (+)= g_i^j into the bound float32 accumulators of partition j's layers
  * (Sec. 2: the gradient is the sum of g_i^j over i); the partial sums B_{i,j}
  * left are added up here, in an order fixed by the shapes.  overwrite must be 1

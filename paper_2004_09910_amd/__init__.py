@@ -69,6 +69,10 @@ _SIG = {
     "tgp_schedule_trace": [_I, _I, _I, ctypes.POINTER(ctypes.c_int32), _I, ctypes.POINTER(_I)],
     "tgp_stage_forward2": [_P, _I, _I, _I, _I, _I, _P, _P, _P, _P, _P],
     "tgp_stage_backward_recompute2": [_P, _I, _I, _I, _P, _P, _P, _P, _P],
+    "tgp_stage_forward_n": [_P, _I, _I, _I, ctypes.POINTER(_I), ctypes.POINTER(_P),
+                            ctypes.POINTER(_P), _P],
+    "tgp_stage_backward_recompute_n": [_P, _I, _I, _I, ctypes.POINTER(_P), ctypes.POINTER(_P),
+                                       _P],
     "tgp_layer_times_plan": [_P, _I, _I, ctypes.POINTER(ctypes.c_size_t)],
     "tgp_layer_times": [_P, _P, ctypes.c_size_t, _I, ctypes.POINTER(ctypes.c_float), _P],
     "tgp_balance_by_time": [_P, _P, ctypes.c_size_t, _I, _I, ctypes.POINTER(_I),
@@ -236,6 +240,25 @@ def stage_backward_recompute2(net: int, j: int, i0: int, i1: int, dy0: int, dy1:
     _check(_lib.tgp_stage_backward_recompute2(net, j, i0, i1, _vp(dy0), _vp(dy1), _vp(dx0),
                                               _vp(dx1), _vp(stream)),
            "tgp_stage_backward_recompute2")
+
+
+def stage_forward_n(net: int, j: int, i0: int, checkpoints: Sequence[bool], xs: Sequence[int],
+                    ys: Sequence[int], stream: int = 0) -> None:
+    """F_{i,j} for i = i0 .. i0 + len(xs) - 1 (element k: micro-batch i0 + k)."""
+    n = len(xs)
+    _check(_lib.tgp_stage_forward_n(net, j, i0, n, (_I * n)(*[int(c) for c in checkpoints]),
+                                    (_P * n)(*[_vp(x) for x in xs]),
+                                    (_P * n)(*[_vp(y) for y in ys]), _vp(stream)),
+           "tgp_stage_forward_n")
+
+
+def stage_backward_recompute_n(net: int, j: int, i0: int, dys: Sequence[int],
+                               dxs: Sequence[Optional[int]], stream: int = 0) -> None:
+    """F'_{i,j} + B_{i,j} for i = i0, i0 - 1, .. (element k: micro-batch i0 - k)."""
+    n = len(dys)
+    _check(_lib.tgp_stage_backward_recompute_n(net, j, i0, n, (_P * n)(*[_vp(d) for d in dys]),
+                                               (_P * n)(*[_vp(d) for d in dxs]), _vp(stream)),
+           "tgp_stage_backward_recompute_n")
 
 
 def grad_accumulate(net: int, j: int, i: int, overwrite: bool, stream: int = 0) -> None:

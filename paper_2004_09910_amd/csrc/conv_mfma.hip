@@ -1533,7 +1533,7 @@ hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void*
   if (pl.cfg == 150) return launch_1x1_res(X, nullptr, Wt, b, Y, nullptr, s, relu, st);
   if (pl.cfg >= 400) {
     g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
-    const hipError_t e = conv_forward_rows32(x, w, b, y, s, relu, st);
+    const hipError_t e = conv_forward_rows32(1, &x, w, b, &y, s, relu, st);
     g_rows32_cfg = -1;
     return e;
   }
@@ -1699,22 +1699,17 @@ hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hi
   return launch_status();
 }
 
-// Two micro-batches of one layer: one launch where the planned kernel takes
-// two tensors (the nine-tap kernel), else one launch each; the same values
-// as two conv_forward_mfma calls either way.
-hipError_t conv_forward_mfma2(const void* x0, const void* x1, const void* w, const float* b,
-                              void* y0, void* y1, const ConvShape& s, int relu, float* part0,
-                              float* part1, size_t part_cap, hipStream_t st) {
+// Two micro-batches of one layer where the planned kernel takes two tensors
+// (the per-tap and resident-weight kernels), else one launch each; the same
+// values as two conv_forward_mfma calls either way.
+static hipError_t conv_forward_mfma_pair(const void* x0, const void* x1, const void* w,
+                                         const float* b, void* y0, void* y1, const ConvShape& s,
+                                         int relu, float* part0, float* part1, size_t part_cap,
+                                         hipStream_t st) {
   const FwdPlan pl = fwd_plan(s);
   if (pl.cfg == 150)
     return launch_1x1_res((const bf16_t*)x0, (const bf16_t*)x1, (const bf16_t*)w, b, (bf16_t*)y0,
                           (bf16_t*)y1, s, relu, st);
-  if (pl.cfg >= 400) {
-    g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
-    const hipError_t e = conv_forward_rows32(x0, w, b, y0, s, relu, st, x1, y1);
-    g_rows32_cfg = -1;
-    return e;
-  }
   if (pl.cfg >= 100 && pl.cfg < 200) {
     // the per-tap kernel: both micro-batches' tiles in one grid
     const long P = s.pixels();
@@ -1735,21 +1730,50 @@ hipError_t conv_forward_mfma2(const void* x0, const void* x1, const void* w, con
   return conv_forward_mfma(x1, w, b, y1, s, relu, part1, part_cap, st);
 }
 
-// The weight gradients of two micro-batches, both sums left pending: one
-// launch of the row-blocked kernel where it applies, else one each.
-hipError_t conv_wgrad_mfma2(const void* x0, const void* x1, const void* dz0, const void* dz1,
-                            float* dw0, float* dw1, float* part0, float* part1,
-                            const ConvShape& s, hipStream_t st, ReduceJob* defer0,
-                            ReduceJob* defer1) {
-  if (use_wgrad_rows(s))
-    return conv_wgrad_rows_launch2(x0, x1, dz0, dz1, dw0, dw1, part0, part1, s, st, defer0,
-                                   defer1);
-  WgradPlan pl;
-  hipError_t e = launch_wgrad_mfma(x0, x1, dz0, dz1, dw0, dw1, part0, part1, s, pl, st);
-  if (e != hipSuccess) return e;
+// n micro-batches of one layer: one launch of the nine-tap kernel where it
+// is planned, else pairs (and a single for odd n).
+hipError_t conv_forward_mfma_n(int n, const void* const* x, const void* w, const float* b,
+                               void* const* y, const ConvShape& s, int relu, float* const* part,
+                               size_t part_cap, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  const FwdPlan pl = fwd_plan(s);
+  if (pl.cfg >= 400) {
+    g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
+    const hipError_t e = conv_forward_rows32(n, x, w, b, y, s, relu, st);
+    g_rows32_cfg = -1;
+    return e;
+  }
+  for (int k = 0; k < n; k += 2) {
+    const hipError_t e =
+        k + 1 < n ? conv_forward_mfma_pair(x[k], x[k + 1], w, b, y[k], y[k + 1], s, relu, part[k],
+                                           part[k + 1], part_cap, st)
+                  : conv_forward_mfma(x[k], w, b, y[k], s, relu, part[k], part_cap, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// The weight gradients of n micro-batches, every sum left pending: one
+// launch of the row-blocked kernel where it applies, else pairs of the
+// per-tap kernel (and a single for odd n).
+hipError_t conv_wgrad_mfma_n(int n, const void* const* x, const void* const* dz,
+                             float* const* dw, float* const* part, const ConvShape& s,
+                             hipStream_t st, ReduceJob* const* defer) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  if (use_wgrad_rows(s)) return conv_wgrad_rows_launch_n(n, x, dz, dw, part, s, st, defer);
   const long E = (long)s.cout * s.taps * s.cin;
-  *defer0 = ReduceJob{part0, dw0, E, pl.S};   // partial == dw when S == 1
-  *defer1 = ReduceJob{part1, dw1, E, pl.S};
+  for (int k = 0; k < n; k += 2) {
+    const bool two = k + 1 < n;
+    WgradPlan pl;
+    float* p0 = part[k];
+    float* p1 = two ? part[k + 1] : nullptr;
+    hipError_t e = launch_wgrad_mfma(x[k], two ? x[k + 1] : nullptr, dz[k],
+                                     two ? dz[k + 1] : nullptr, dw[k], two ? dw[k + 1] : nullptr,
+                                     p0, p1, s, pl, st);
+    if (e != hipSuccess) return e;
+    *defer[k] = ReduceJob{p0, dw[k], E, pl.S};   // partial == dw when S == 1
+    if (two) *defer[k + 1] = ReduceJob{p1, dw[k + 1], E, pl.S};
+  }
   return hipSuccess;
 }
 

@@ -67,14 +67,18 @@ struct Rows32Geom {
 // pixels, so that one wave's MFMAs run while the other waits on its DMA
 // issue or its LDS reads.
 //
-// X2 / Y2 (both null or both set) are a second micro-batch of nb samples
-// with the same weights: its tiles follow the first's (sample index nb ..
-// 2 nb - 1), so one launch covers both and each block streams a tile of
-// each through its ring.
+// The micro-batches of one launch (ng of them, nb samples each, the same
+// weights): the tiles of micro-batch k follow those of k - 1 (sample index
+// k nb .. k nb + nb - 1), so one launch covers them all and a block streams
+// tiles of several through its ring.
+struct R32Io {
+  const bf16_t* x[kMaxGroup];
+  bf16_t* y[kMaxGroup];
+};
+
 template <int W, int R, int FW, int NS, int CH, int RK>
 __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
-    const bf16_t* __restrict__ X, const bf16_t* __restrict__ X2, const bf16_t* __restrict__ Wt,
-    const float* __restrict__ bias, bf16_t* __restrict__ Y, bf16_t* __restrict__ Y2, int nb,
+    R32Io io, int ng, const bf16_t* __restrict__ Wt, const float* __restrict__ bias, int nb,
     int H, int Cin, int Cout, int relu) {
   typedef Rows32Geom<W, R, RK> G_;
   constexpr int BWP = G_::BWP, SB = G_::SB, F = G_::F, AR = G_::AR, RB = G_::RB;
@@ -93,7 +97,6 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
   const int chf = CH == 2 ? 0 : wave >> 2;                      // channel half (CH = 1)
   const int nrb = (H + R - 1) / R;                              // row blocks per sample
   const int nct = Cout / 64;
-  const int ng = X2 ? 2 : 1;                                     // micro-batches
   const int items = ng * nb * nrb * nct;
   const int G = gridDim.x;
   const int lb = xcd_remap(blockIdx.x, G);
@@ -111,8 +114,7 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
     }
   };
 
-  const u32x4 rx = make_rsrc(X, nb * H * W * Cin * 2);
-  const u32x4 rx2 = make_rsrc(X2 ? X2 : X, nb * H * W * Cin * 2);
+  const int xbytes = nb * H * W * Cin * 2;                      // one micro-batch's input
   const u32x4 rw = make_rsrc(Wt, Cout * 9 * Cin * 2);
 
   // DMA: instruction u of this wave fills stage chunk k = NW u + wave
@@ -159,11 +161,14 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
     }
   }
 
-  auto coords = [&](int it, int& n, int& h0, int& co0) __attribute__((always_inline)) {
+  // item -> micro-batch gi, its sample n, first row h0, output channels co0
+  auto coords = [&](int it, int& gi, int& n, int& h0, int& co0) __attribute__((always_inline)) {
     const int item = lb + it * G;
     const int ct = item % nct, rest = item / nct;
     const int rb = rest % nrb;
     n = rest / nrb;
+    gi = n / nb;
+    n -= gi * nb;
     h0 = rb * R;
     co0 = ct * 64;
   };
@@ -172,16 +177,14 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
   // inside the stage loop it is spread over the nine taps; the instruction
   // issue stalls while the memory pipeline is full, and spread out those
   // stalls overlap the MFMAs already queued
-  int i_it = 0, i_ks = 0, i_n = 0, i_h0 = 0, i_co0 = 0;
-  if (total > 0) coords(0, i_n, i_h0, i_co0);
+  int i_it = 0, i_ks = 0, i_gi = 0, i_n = 0, i_h0 = 0, i_co0 = 0;
+  if (total > 0) coords(0, i_gi, i_n, i_h0, i_co0);
+  u32x4 rxg = make_rsrc(pick4(io.x, i_gi), xbytes);            // the issuing item's input
   auto issue_part = [&](int slot, int u0, int u1) __attribute__((always_inline)) {
     const int c0 = i_ks * 16;
     const int soff_a = (i_co0 * 9 * Cin + c0) * 2;
     const int hb = i_h0 - 1;                                    // input row of block row 0
-    const bool g1 = i_n >= nb;                                  // second micro-batch (uniform)
-    const int nn = g1 ? i_n - nb : i_n;
-    const u32x4 rxg = g1 ? rx2 : rx;
-    const int base_b = ((nn * H + hb) * W * Cin + c0) * 2;     // negative for hb = -1
+    const int base_b = ((i_n * H + hb) * W * Cin + c0) * 2;    // negative for hb = -1
     const bool interior = hb >= 0 && hb + R + 2 <= H;
 #pragma unroll
     for (int u = 0; u < LW; ++u) {
@@ -200,7 +203,10 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
   auto issue_done = [&]() __attribute__((always_inline)) {
     if (++i_ks == nk) {
       i_ks = 0;
-      if (++i_it < n_items) coords(i_it, i_n, i_h0, i_co0);
+      if (++i_it < n_items) {
+        coords(i_it, i_gi, i_n, i_h0, i_co0);
+        rxg = make_rsrc(pick4(io.x, i_gi), xbytes);
+      }
     }
   };
 
@@ -230,8 +236,8 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
 
   int idx = 0;
   for (int c_it = 0; c_it < n_items; ++c_it) {
-    int n, h0, co0;
-    coords(c_it, n, h0, co0);
+    int gi, n, h0, co0;
+    coords(c_it, gi, n, h0, co0);
     // this lane's bias values for the epilogue, loaded up front: channel
     // co0 + 32 (half) + 8 g + 4 (l / 32) + e is bv[i][g][e], half = i (CH = 2)
     // or chf (CH = 1)
@@ -306,9 +312,8 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
     constexpr int NCK = 4 * CH;                                 // 16-byte chunks per pixel
     unsigned char* ep = ring + ((idx - 1) % NS) * SB + wave * 32 * ROWB;
     static_assert(NW * 32 * ROWB <= SB, "epilogue staging fits a slot");
-    const bool g1 = n >= nb;
-    bf16_t* const Yg = g1 ? Y2 : Y;
-    const long pix0 = (long)((g1 ? n - nb : n) * H + h0) * W;
+    bf16_t* const Yg = pick4(io.y, gi);
+    const long pix0 = (long)(n * H + h0) * W;
     const int pw = lane & 31, hw = lane >> 5;
 #pragma unroll
     for (int j = 0; j < FW; ++j) {
@@ -403,9 +408,8 @@ bool conv_rows32_ok(const ConvShape& s) {
 }
 
 template <int W, int R, int FW, int NS, int CH, int RK>
-static hipError_t launch_rows32(const bf16_t* X, const bf16_t* X2, const bf16_t* Wt,
-                                const float* b, bf16_t* Y, bf16_t* Y2, const ConvShape& s,
-                                int relu, hipStream_t st) {
+static hipError_t launch_rows32(const R32Io& io, int ng, const bf16_t* Wt, const float* b,
+                                const ConvShape& s, int relu, hipStream_t st) {
   static const char* name = nullptr;
   static char buf[64];
   if (!name) {
@@ -414,34 +418,34 @@ static hipError_t launch_rows32(const bf16_t* X, const bf16_t* X2, const bf16_t*
     name = buf;
   }
   if (RK && (s.cin != 16 * RK || s.cout != 64)) return hipErrorInvalidValue;
-  const int ng = X2 ? 2 : 1;
   const long items = (long)ng * s.nb * ((s.H + R - 1) / R) * (s.cout / 64);
   const int G = (int)(items < 256 ? items : 256);
   if (G == 0) return hipSuccess;
   const long P = (long)ng * s.pixels();
   ProfScope ps(name, 2.0 * P * s.cout * 9 * s.cin,
                2.0 * ((double)P * s.cin + 9.0 * s.cin * s.cout + (double)P * s.cout), st);
-  TGP_LAUNCH(ps, (conv3x3_rows32<W, R, FW, NS, CH, RK>), dim3(G), dim3(CH == 2 ? 256 : 512), 0, st, X,
-             X2, Wt, b, Y, Y2, s.nb, s.H, s.cin, s.cout, relu);
+  TGP_LAUNCH(ps, (conv3x3_rows32<W, R, FW, NS, CH, RK>), dim3(G), dim3(CH == 2 ? 256 : 512), 0, st,
+             io, ng, Wt, b, s.nb, s.H, s.cin, s.cout, relu);
   return launch_status();
 }
 
-hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, void* y,
-                               const ConvShape& s, int relu, hipStream_t st, const void* x2,
-                               void* y2) {
-  const int c = rows32_pick(s, x2 ? 2 : 1);
-  if (c < 0 || !conv_rows32_ok(s) || (x2 == nullptr) != (y2 == nullptr))
-    return hipErrorInvalidValue;
-  const bf16_t* X = (const bf16_t*)x;
-  const bf16_t* X2 = (const bf16_t*)x2;
+hipError_t conv_forward_rows32(int n, const void* const* x, const void* w, const float* b,
+                               void* const* y, const ConvShape& s, int relu, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  const int c = rows32_pick(s, n);
+  if (c < 0 || !conv_rows32_ok(s)) return hipErrorInvalidValue;
+  R32Io io{};
+  for (int k = 0; k < kMaxGroup; ++k) {   // unused entries repeat micro-batch 0
+    io.x[k] = (const bf16_t*)x[k < n ? k : 0];
+    io.y[k] = (bf16_t*)y[k < n ? k : 0];
+    if (!io.x[k] || !io.y[k]) return hipErrorInvalidValue;
+  }
   const bf16_t* Wt = (const bf16_t*)w;
-  bf16_t* Y = (bf16_t*)y;
-  bf16_t* Y2 = (bf16_t*)y2;
   switch (c) {
 #define R32_CASE(i)                                                                      \
   case i:                                                                                \
     return launch_rows32<kR32Cfgs[i].W, kR32Cfgs[i].R, kR32Cfgs[i].FW, kR32Cfgs[i].NS,   \
-                         kR32Cfgs[i].CH, kR32Cfgs[i].RK>(X, X2, Wt, b, Y, Y2, s, relu, st);
+                         kR32Cfgs[i].CH, kR32Cfgs[i].RK>(io, n, Wt, b, s, relu, st);
     R32_CASE(0) R32_CASE(1) R32_CASE(2) R32_CASE(3) R32_CASE(4) R32_CASE(5)
     R32_CASE(6) R32_CASE(7) R32_CASE(8) R32_CASE(9) R32_CASE(10) R32_CASE(11)
     R32_CASE(12) R32_CASE(13) R32_CASE(14) R32_CASE(15) R32_CASE(16) R32_CASE(17)

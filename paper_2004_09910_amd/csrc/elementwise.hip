@@ -17,13 +17,12 @@ size_t wgrad_mfma_partial_floats(const ConvShape& s);
 hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* partial,
                            const ConvShape& s, hipStream_t st, const ReduceJob* extra,
                            ReduceJob* defer);
-hipError_t conv_forward_mfma2(const void* x0, const void* x1, const void* w, const float* b,
-                              void* y0, void* y1, const ConvShape& s, int relu, float* part0,
-                              float* part1, size_t part_cap, hipStream_t st);
-hipError_t conv_wgrad_mfma2(const void* x0, const void* x1, const void* dz0, const void* dz1,
-                            float* dw0, float* dw1, float* part0, float* part1,
-                            const ConvShape& s, hipStream_t st, ReduceJob* defer0,
-                            ReduceJob* defer1);
+hipError_t conv_forward_mfma_n(int n, const void* const* x, const void* w, const float* b,
+                               void* const* y, const ConvShape& s, int relu, float* const* part,
+                               size_t part_cap, hipStream_t st);
+hipError_t conv_wgrad_mfma_n(int n, const void* const* x, const void* const* dz,
+                             float* const* dw, float* const* part, const ConvShape& s,
+                             hipStream_t st, ReduceJob* const* defer);
 
 namespace {
 
@@ -524,8 +523,8 @@ __global__ __launch_bounds__(256) void relu_bwd_k(const T* __restrict__ dy, cons
 // 16-byte channel pack t % CP for rows t / CP, t / CP + 256 / CP, ...
 // (serial, fixed order); row lanes are then added in order in LDS and
 // part[b][c] is written.  Needs 256 % CP == 0 (CP = C / pack).  A launch
-// covers gridDim.y (1 or 2) micro-batches of the same shape; blockIdx.y
-// selects the pointer set.
+// covers gridDim.y (1 .. kMaxGroup) micro-batches of the same shape;
+// blockIdx.y selects the pointer set.
 template <typename T>
 struct RbPtrs {
   const T* dy;   // the incoming gradient (the pool gradient for the pooled kernel)
@@ -534,11 +533,32 @@ struct RbPtrs {
   T* dz;
   float* part;
 };
+template <typename T>
+struct RbGroup {   // pointer set k of each field is micro-batch k's
+  const T* dy[kMaxGroup];
+  const T* ds[kMaxGroup];
+  const T* y[kMaxGroup];
+  T* dz[kMaxGroup];
+  float* part[kMaxGroup];
+};
+// Element k (uniform, below 4) of a kernel-argument array, read at constant
+// indices so that the array stays in the argument segment instead of being
+// copied to private memory for a dynamic index.
+template <typename P>
+__device__ __forceinline__ P sel4(const P (&a)[4], int k) {
+  return k == 0 ? a[0] : k == 1 ? a[1] : k == 2 ? a[2] : a[3];
+}
+// The pointer set of group entry blockIdx.y.
+template <typename T>
+__device__ __forceinline__ RbPtrs<T> rb_pick(const RbGroup<T>& a) {
+  const int k = blockIdx.y;
+  return RbPtrs<T>{sel4(a.dy, k), sel4(a.ds, k), sel4(a.y, k), sel4(a.dz, k), sel4(a.part, k)};
+}
 
 template <typename T>
-__global__ __launch_bounds__(256) void relu_bwd_bias_k(RbPtrs<T> g0, RbPtrs<T> g1, int relu,
-                                                       long P, int C, long rows) {
-  const RbPtrs<T> g = blockIdx.y ? g1 : g0;
+__global__ __launch_bounds__(256) void relu_bwd_bias_k(RbGroup<T> ga, int relu, long P, int C,
+                                                       long rows) {
+  const RbPtrs<T> g = rb_pick(ga);
   const T* __restrict__ dy = g.dy;
   const T* __restrict__ ds = g.ds;
   const T* __restrict__ y = g.y;
@@ -591,10 +611,9 @@ __global__ __launch_bounds__(256) void relu_bwd_bias_k(RbPtrs<T> g0, RbPtrs<T> g
 // pixels of a window in row-major order), then row lanes are added in order
 // in LDS and part[b][c] is written.
 template <typename T>
-__global__ __launch_bounds__(256) void pool_relu_bwd_bias_k(RbPtrs<T> g0, RbPtrs<T> g1, int relu,
-                                                            int nb, int H, int W, int C,
-                                                            long rows) {
-  const RbPtrs<T> gp = blockIdx.y ? g1 : g0;
+__global__ __launch_bounds__(256) void pool_relu_bwd_bias_k(RbGroup<T> ga, int relu, int nb,
+                                                            int H, int W, int C, long rows) {
+  const RbPtrs<T> gp = rb_pick(ga);
   const T* __restrict__ dp = gp.dy;
   const T* __restrict__ ds = gp.ds;
   const T* __restrict__ y = gp.y;
@@ -708,14 +727,17 @@ __global__ __launch_bounds__(256) void dw_wgrad_k(const T* __restrict__ x, const
 
 // ---------------------------------------------------------------- pool
 
-// 2x2/2 max pool of gridDim.y (1 or 2) micro-batches (blockIdx.y selects
-// x0 / y0 or x1 / y1).
+// 2x2/2 max pool of gridDim.y (1 .. kMaxGroup) micro-batches (blockIdx.y
+// selects x[k] / y[k]).
 template <typename T>
-__global__ __launch_bounds__(256) void maxpool_fwd_k(const T* __restrict__ x0, T* __restrict__ y0,
-                                                     const T* __restrict__ x1, T* __restrict__ y1,
-                                                     int nb, int H, int W, int C) {
-  const T* __restrict__ x = blockIdx.y ? x1 : x0;
-  T* __restrict__ y = blockIdx.y ? y1 : y0;
+struct PoolGroup {
+  const T* x[kMaxGroup];
+  T* y[kMaxGroup];
+};
+template <typename T>
+__global__ __launch_bounds__(256) void maxpool_fwd_k(PoolGroup<T> pg, int nb, int H, int W, int C) {
+  const T* __restrict__ x = sel4(pg.x, blockIdx.y);
+  T* __restrict__ y = sel4(pg.y, blockIdx.y);
   constexpr int N = Pk<T>::N;
   int CP = C / N, H2 = H / 2, W2 = W / 2;
   long e = (long)blockIdx.x * 256 + threadIdx.x;
@@ -1105,41 +1127,49 @@ hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* p
   return splitk_reduce_launch(partial, dw, E, S, st, extra);
 }
 
-hipError_t conv_forward2(int dt, const void* x0, const void* x1, const void* w, const float* b,
-                         void* y0, void* y1, const ConvShape& s, int relu, float* part0,
-                         float* part1, size_t part_cap, hipStream_t st) {
+hipError_t conv_forward_n(int dt, int n, const void* const* x, const void* w, const float* b,
+                          void* const* y, const ConvShape& s, int relu, float* const* part,
+                          size_t part_cap, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
   if (mfma_conv_ok(dt, s.cin, s.cout))
-    return conv_forward_mfma2(x0, x1, w, b, y0, y1, s, relu, part0, part1, part_cap, st);
-  hipError_t e = conv_forward(dt, x0, w, b, y0, s, relu, part0, part_cap, st);
-  if (e != hipSuccess) return e;
-  return conv_forward(dt, x1, w, b, y1, s, relu, part1, part_cap, st);
+    return conv_forward_mfma_n(n, x, w, b, y, s, relu, part, part_cap, st);
+  for (int k = 0; k < n; ++k) {
+    const hipError_t e = conv_forward(dt, x[k], w, b, y[k], s, relu, part[k], part_cap, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
-hipError_t conv_dgrad2(int dt, const void* dz0, const void* dz1, const void* w, const void* wt,
-                       void* dx0, void* dx1, const ConvShape& s, float* part0, float* part1,
-                       size_t part_cap, hipStream_t st) {
+hipError_t conv_dgrad_n(int dt, int n, const void* const* dz, const void* w, const void* wt,
+                        void* const* dx, const ConvShape& s, float* const* part,
+                        size_t part_cap, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
   if (conv_dgrad_uses_wt(dt, s)) {
     ConvShape t{s.nb, s.H, s.W, s.cout, s.cin, s.taps};
     t_in_dgrad = 1;
-    const hipError_t e = conv_forward_mfma2(dz0, dz1, wt, nullptr, dx0, dx1, t, 0, part0, part1,
-                                            part_cap, st);
+    const hipError_t e = conv_forward_mfma_n(n, dz, wt, nullptr, dx, t, 0, part, part_cap, st);
     t_in_dgrad = 0;
     return e;
   }
-  hipError_t e = conv_dgrad(dt, dz0, w, wt, dx0, s, part0, part_cap, st);
-  if (e != hipSuccess) return e;
-  return conv_dgrad(dt, dz1, w, wt, dx1, s, part1, part_cap, st);
+  for (int k = 0; k < n; ++k) {
+    const hipError_t e = conv_dgrad(dt, dz[k], w, wt, dx[k], s, part[k], part_cap, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
-hipError_t conv_wgrad2(int dt, const void* x0, const void* x1, const void* dz0, const void* dz1,
-                       float* dw0, float* dw1, float* part0, float* part1, const ConvShape& s,
-                       hipStream_t st, ReduceJob* defer0, ReduceJob* defer1) {
-  if (!defer0 || !defer1) return hipErrorInvalidValue;
-  if (mfma_conv_ok(dt, s.cin, s.cout))
-    return conv_wgrad_mfma2(x0, x1, dz0, dz1, dw0, dw1, part0, part1, s, st, defer0, defer1);
-  hipError_t e = conv_wgrad(dt, x0, dz0, dw0, part0, s, st, nullptr, defer0);
-  if (e != hipSuccess) return e;
-  return conv_wgrad(dt, x1, dz1, dw1, part1, s, st, nullptr, defer1);
+hipError_t conv_wgrad_n(int dt, int n, const void* const* x, const void* const* dz,
+                        float* const* dw, float* const* part, const ConvShape& s, hipStream_t st,
+                        ReduceJob* const* defer) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  for (int k = 0; k < n; ++k)
+    if (!defer[k]) return hipErrorInvalidValue;
+  if (mfma_conv_ok(dt, s.cin, s.cout)) return conv_wgrad_mfma_n(n, x, dz, dw, part, s, st, defer);
+  for (int k = 0; k < n; ++k) {
+    const hipError_t e = conv_wgrad(dt, x[k], dz[k], dw[k], part[k], s, st, nullptr, defer[k]);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // The row-window depthwise kernels over one or two micro-batches (x1 null:
@@ -1315,6 +1345,27 @@ template <typename T>
 static RbPtrs<T> rb_ptrs(const RbArgs& a) {
   return RbPtrs<T>{(const T*)a.dy, (const T*)a.dskip, (const T*)a.y, (T*)a.dz, a.partial};
 }
+// The group's pointer sets; unused entries repeat the first.
+template <typename T>
+static RbGroup<T> rb_group(int n, const RbArgs* a) {
+  RbGroup<T> g;
+  for (int k = 0; k < kMaxGroup; ++k) {
+    const RbPtrs<T> p = rb_ptrs<T>(a[k < n ? k : 0]);
+    g.dy[k] = p.dy;
+    g.ds[k] = p.ds;
+    g.y[k] = p.y;
+    g.dz[k] = p.dz;
+    g.part[k] = p.part;
+  }
+  return g;
+}
+// n within 1 .. kMaxGroup, all with or all without a skip gradient.
+static bool rb_group_ok(int n, const RbArgs* a) {
+  if (n < 1 || n > kMaxGroup) return false;
+  for (int k = 1; k < n; ++k)
+    if ((a[k].dskip == nullptr) != (a[0].dskip == nullptr)) return false;
+  return true;
+}
 
 // The bias sums of n launched micro-batches: left pending (defer) or reduced.
 static hipError_t rb_finish(int n, const RbArgs* a, long C, int nblk, hipStream_t st) {
@@ -1331,11 +1382,9 @@ static hipError_t rb_finish(int n, const RbArgs* a, long C, int nblk, hipStream_
 
 hipError_t relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, long P, int C,
                                 hipStream_t st) {
-  if (n < 1 || n > 2 || (n == 2 && ((a[0].dskip == nullptr) != (a[1].dskip == nullptr))))
-    return hipErrorInvalidValue;
+  if (!rb_group_ok(n, a)) return hipErrorInvalidValue;
   long rows = relu_bias_rows(P, C, dt == 0 ? 8 : 4);
   int nb = cdiv(P, rows);
-  const RbArgs& b = a[n - 1];
   {
     ProfScope ps("relu_backward_bias", 0.0,
                  n * ((dt == 0 ? 2.0 : 4.0) * P * C * (3 + (a[0].dskip ? 1 : 0) - (relu ? 0 : 1)) +
@@ -1343,10 +1392,10 @@ hipError_t relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, long P
                  st);
     if (dt == 0)
       TGP_LAUNCH(ps, relu_bwd_bias_k<bf16_t>, dim3(nb, n), dim3(256), 0, st,
-                 rb_ptrs<bf16_t>(a[0]), rb_ptrs<bf16_t>(b), relu, P, C, rows);
+                 rb_group<bf16_t>(n, a), relu, P, C, rows);
     else
       TGP_LAUNCH(ps, relu_bwd_bias_k<float>, dim3(nb, n), dim3(256), 0, st,
-                 rb_ptrs<float>(a[0]), rb_ptrs<float>(b), relu, P, C, rows);
+                 rb_group<float>(n, a), relu, P, C, rows);
   }
   hipError_t e = launch_status();
   if (e != hipSuccess) return e;
@@ -1362,15 +1411,13 @@ hipError_t relu_backward_bias(int dt, const void* dy, const void* dskip, const v
 
 hipError_t pool_relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, int nb, int H,
                                      int W, int C, hipStream_t st) {
-  if (n < 1 || n > 2 || (n == 2 && ((a[0].dskip == nullptr) != (a[1].dskip == nullptr))))
-    return hipErrorInvalidValue;
+  if (!rb_group_ok(n, a)) return hipErrorInvalidValue;
   for (int k = 0; k < n; ++k)
     if (!pool_relu_bias_fusable(dt, C, H, W, a[k].dy, a[k].dskip, a[k].y, a[k].dz))
       return hipErrorInvalidValue;
   const long P2 = (long)nb * (H / 2) * (W / 2);
   const long rows = relu_bias_rows(P2, C, dt == 0 ? 8 : 4);
   const int nbk = cdiv(P2, rows);
-  const RbArgs& b = a[n - 1];
   {
     const double esz = dt == 0 ? 2.0 : 4.0;
     ProfScope ps("pool_relu_backward_bias", 0.0,
@@ -1379,10 +1426,10 @@ hipError_t pool_relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, i
                  st);
     if (dt == 0)
       TGP_LAUNCH(ps, pool_relu_bwd_bias_k<bf16_t>, dim3(nbk, n), dim3(256), 0, st,
-                 rb_ptrs<bf16_t>(a[0]), rb_ptrs<bf16_t>(b), relu, nb, H, W, C, rows);
+                 rb_group<bf16_t>(n, a), relu, nb, H, W, C, rows);
     else
       TGP_LAUNCH(ps, pool_relu_bwd_bias_k<float>, dim3(nbk, n), dim3(256), 0, st,
-                 rb_ptrs<float>(a[0]), rb_ptrs<float>(b), relu, nb, H, W, C, rows);
+                 rb_group<float>(n, a), relu, nb, H, W, C, rows);
   }
   hipError_t e = launch_status();
   if (e != hipSuccess) return e;
@@ -1413,26 +1460,37 @@ hipError_t bias_grad(int dt, const void* dz, float* db, float* partial, long P, 
   return splitk_reduce_launch(partial, db, C, nb, st);
 }
 
-hipError_t maxpool_forward2(int dt, const void* x0, void* y0, const void* x1, void* y1, int nb,
-                            int H, int W, int C, hipStream_t st) {
-  const int n = x1 ? 2 : 1;
-  if ((x1 == nullptr) != (y1 == nullptr)) return hipErrorInvalidValue;
+template <typename T>
+static PoolGroup<T> pool_group(int n, const void* const* x, void* const* y) {
+  PoolGroup<T> g;
+  for (int k = 0; k < kMaxGroup; ++k) {   // unused entries repeat the first
+    g.x[k] = (const T*)x[k < n ? k : 0];
+    g.y[k] = (T*)y[k < n ? k : 0];
+  }
+  return g;
+}
+
+hipError_t maxpool_forward_n(int dt, int n, const void* const* x, void* const* y, int nb, int H,
+                             int W, int C, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  for (int k = 0; k < n; ++k)
+    if (!x[k] || !y[k]) return hipErrorInvalidValue;
   int N = dt == 0 ? 8 : 4;
   long total = (long)nb * (H / 2) * (W / 2) * (C / N);
   dim3 g(cdiv(total, 256), n);
   ProfScope ps("maxpool_forward", 0.0, n * (dt == 0 ? 2.0 : 4.0) * nb * H * W * C * 1.25, st);
   if (dt == 0)
-    TGP_LAUNCH(ps, maxpool_fwd_k<bf16_t>, g, dim3(256), 0, st, (const bf16_t*)x0, (bf16_t*)y0,
-               (const bf16_t*)(n == 2 ? x1 : x0), (bf16_t*)(n == 2 ? y1 : y0), nb, H, W, C);
+    TGP_LAUNCH(ps, maxpool_fwd_k<bf16_t>, g, dim3(256), 0, st, pool_group<bf16_t>(n, x, y), nb, H,
+               W, C);
   else
-    TGP_LAUNCH(ps, maxpool_fwd_k<float>, g, dim3(256), 0, st, (const float*)x0, (float*)y0,
-               (const float*)(n == 2 ? x1 : x0), (float*)(n == 2 ? y1 : y0), nb, H, W, C);
+    TGP_LAUNCH(ps, maxpool_fwd_k<float>, g, dim3(256), 0, st, pool_group<float>(n, x, y), nb, H,
+               W, C);
   return launch_status();
 }
 
 hipError_t maxpool_forward(int dt, const void* x, void* y, int nb, int H, int W, int C,
                            hipStream_t st) {
-  return maxpool_forward2(dt, x, y, nullptr, nullptr, nb, H, W, C, st);
+  return maxpool_forward_n(dt, 1, &x, &y, nb, H, W, C, st);
 }
 
 hipError_t maxpool_backward(int dt, const void* x, const void* dy, void* dx, int nb, int H,

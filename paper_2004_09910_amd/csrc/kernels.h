@@ -8,6 +8,10 @@
 
 namespace tgpk {
 
+// Micro-batches of one layer that one launch may cover (the same shape and
+// weights, separate tensors).
+constexpr int kMaxGroup = 4;
+
 // One convolution at one micro-batch: nb samples of H x W, NHWC.
 struct ConvShape {
   int nb, H, W, cin, cout, taps;  // taps = 9 (3x3, pad 1) or 1 (1x1)
@@ -31,13 +35,13 @@ hipError_t conv_forward_rowtile(const void* x, const void* w, const float* b, vo
 extern int g_rowtile_cfg;
 // 32x32x16-MFMA 3x3 convolution on whole-row tiles with all nine taps per
 // 16-channel stage (bf16; W in {24, 48, 96, 192}, Cin % 16 == 0, Cout % 64
-// == 0): whether it supports a shape, and the launch (same contract as
-// conv_forward_rowtile).
+// == 0): whether it supports a shape, and the launch over n (1 ..
+// kMaxGroup) micro-batches x[k] -> y[k] (same contract as
+// conv_forward_rowtile for each).
 int conv_rows32_tiles(const ConvShape& s);
 bool conv_rows32_ok(const ConvShape& s);
-hipError_t conv_forward_rows32(const void* x, const void* w, const float* b, void* y,
-                               const ConvShape& s, int relu, hipStream_t st,
-                               const void* x2 = nullptr, void* y2 = nullptr);
+hipError_t conv_forward_rows32(int n, const void* const* x, const void* w, const float* b,
+                               void* const* y, const ConvShape& s, int relu, hipStream_t st);
 extern int g_rows32_cfg;
 extern int g_rows32_ch;
 extern int g_wgrad_ks;
@@ -63,10 +67,11 @@ size_t wgrad_rows_partial_floats(const ConvShape& s);
 hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, float* partial,
                                   const ConvShape& s, hipStream_t st,
                                   const ReduceJob* extra = nullptr, ReduceJob* defer = nullptr);
-hipError_t conv_wgrad_rows_launch2(const void* x0, const void* x1, const void* dz0,
-                                   const void* dz1, float* dw0, float* dw1, float* partial0,
-                                   float* partial1, const ConvShape& s, hipStream_t st,
-                                   ReduceJob* defer0, ReduceJob* defer1);
+// n (1 .. kMaxGroup) micro-batches in one launch, each sum left pending in
+// *defer[k].
+hipError_t conv_wgrad_rows_launch_n(int n, const void* const* x, const void* const* dz,
+                                    float* const* dw, float* const* partial, const ConvShape& s,
+                                    hipStream_t st, ReduceJob* const* defer);
 
 // Whether the data-gradient kernel for this shape reads the transformed
 // weight wt = [cin][taps][cout] (taps rotated by 180 degrees).
@@ -87,19 +92,20 @@ hipError_t conv_wgrad(int dt, const void* x, const void* dz, float* dw, float* p
                       const ConvShape& s, hipStream_t st, const ReduceJob* extra = nullptr,
                       ReduceJob* defer = nullptr);
 
-// The same three operations for two micro-batches of one layer (the same
-// weights, separate tensors): one launch where the chosen kernel takes two
-// tensors, else one launch each, with the same values as two single calls.
-// conv_wgrad2 always leaves both sums pending.
-hipError_t conv_forward2(int dt, const void* x0, const void* x1, const void* w, const float* b,
-                         void* y0, void* y1, const ConvShape& s, int relu, float* part0,
-                         float* part1, size_t part_cap, hipStream_t st);
-hipError_t conv_dgrad2(int dt, const void* dz0, const void* dz1, const void* w, const void* wt,
-                       void* dx0, void* dx1, const ConvShape& s, float* part0, float* part1,
-                       size_t part_cap, hipStream_t st);
-hipError_t conv_wgrad2(int dt, const void* x0, const void* x1, const void* dz0, const void* dz1,
-                       float* dw0, float* dw1, float* part0, float* part1, const ConvShape& s,
-                       hipStream_t st, ReduceJob* defer0, ReduceJob* defer1);
+// The same three operations for n (1 .. kMaxGroup) micro-batches of one
+// layer (the same weights, separate tensors; array element k is micro-batch
+// k's): one launch where the chosen kernel takes them all, else launches of
+// two and one, with the same values as n single calls.  conv_wgrad_n always
+// leaves every sum pending (*defer[k]).
+hipError_t conv_forward_n(int dt, int n, const void* const* x, const void* w, const float* b,
+                          void* const* y, const ConvShape& s, int relu, float* const* part,
+                          size_t part_cap, hipStream_t st);
+hipError_t conv_dgrad_n(int dt, int n, const void* const* dz, const void* w, const void* wt,
+                        void* const* dx, const ConvShape& s, float* const* part,
+                        size_t part_cap, hipStream_t st);
+hipError_t conv_wgrad_n(int dt, int n, const void* const* x, const void* const* dz,
+                        float* const* dw, float* const* part, const ConvShape& s, hipStream_t st,
+                        ReduceJob* const* defer);
 
 // Depthwise 3x3 (pad 1), w = [c][9].
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
@@ -132,9 +138,9 @@ hipError_t bias_grad(int dt, const void* dz, float* db, float* partial, long P, 
 
 // 2x2/2 max-pool of x (nb x H x W x C) into y; backward routes dy to the first
 // maximal element of each window (row-major).
-// Two micro-batches in one launch (x1 / y1 null: one).
-hipError_t maxpool_forward2(int dt, const void* x0, void* y0, const void* x1, void* y1, int nb,
-                            int H, int W, int C, hipStream_t st);
+// n (1 .. kMaxGroup) micro-batches x[k] -> y[k] in one launch.
+hipError_t maxpool_forward_n(int dt, int n, const void* const* x, void* const* y, int nb, int H,
+                             int W, int C, hipStream_t st);
 hipError_t maxpool_forward(int dt, const void* x, void* y, int nb, int H, int W, int C,
                            hipStream_t st);
 hipError_t maxpool_backward(int dt, const void* x, const void* dy, void* dx, int nb, int H,
@@ -193,8 +199,8 @@ struct RbArgs {
   float* partial;
   ReduceJob* defer;
 };
-// n (1 or 2) micro-batches of the same shape in one launch; both with or
-// both without a skip gradient.
+// n (1 .. kMaxGroup) micro-batches of the same shape in one launch; all
+// with or all without a skip gradient.
 hipError_t relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, long P, int C,
                                 hipStream_t st);
 hipError_t pool_relu_backward_bias_n(int dt, int n, const RbArgs* a, int relu, int nb, int H,

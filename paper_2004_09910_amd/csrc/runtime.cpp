@@ -254,15 +254,18 @@ size_t stash_off(const tgp_net* N, int i, int sid, bool grad) {
   return m.at(sid) + (size_t)(i - 1) * N->stash_stride;
 }
 
-// Forward over partition j for a group of cnt (1 or 2) micro-batches
+constexpr int MG = tgpk::kMaxGroup;
+
+// Forward over partition j for a group of cnt (1 .. MG) micro-batches
 // iv[k], layer by layer; phase[k]: 0 = checkpointed forward, 1 = storing
-// forward, 2 = recompute.  A group of two runs each convolution as one
-// launch where the kernel takes two tensors (same values as one at a time).
+// forward, 2 = recompute.  A group runs each convolution as one launch where
+// the kernel takes all its tensors, else as launches of two and one (same
+// values as one at a time).
 tgp_status run_forward_g(tgp_net* N, int j, int cnt, const int* iv, const int* phase,
                          const void* const* x_in, void* const* y_out, hipStream_t st) {
   const int lo = N->lo[j - 1], hi = N->hi[j - 1];
-  int set[2];
-  const void* src[2];
+  int set[MG];
+  const void* src[MG];
   for (int k = 0; k < cnt; ++k) {
     set[k] = (phase[k] == 1) ? (N->mode == TGP_CKPT_NEVER ? iv[k] - 1 : 0) : -1;
     src[k] = x_in[k];
@@ -270,8 +273,10 @@ tgp_status run_forward_g(tgp_net* N, int j, int cnt, const int* iv, const int* p
   for (int l = lo; l < hi; ++l) {
     LayerRt& Lr = N->L[l];
     const tgp_layer& d = Lr.d;
-    void* out[2];
-    const void* cin_ptr[2];
+    void* out[MG];
+    const void* cin_ptr[MG];
+    void* pro_ptr[MG];
+    float* fpart[MG];
     for (int k = 0; k < cnt; ++k) {
       const int i = iv[k];
       if (phase[k] == 2) out[k] = T_(N, i, Lr.o_scr_out);
@@ -289,31 +294,34 @@ tgp_status run_forward_g(tgp_net* N, int j, int cnt, const int* iv, const int* p
                  "upcat_forward");
         }
         cin_ptr[k] = pro;
+        pro_ptr[k] = pro;
       }
+      fpart[k] = (float*)T_(N, i, N->o_fpart);
     }
-    if (d.prologue == TGP_PRO_MAXPOOL2)   // both micro-batches' pools in one launch
-      HIPCHK(tgpk::maxpool_forward2(N->dt, src[0], (void*)cin_ptr[0], cnt == 2 ? src[1] : nullptr,
-                                    cnt == 2 ? (void*)cin_ptr[1] : nullptr, N->b, Lr.inH, Lr.inW,
-                                    Lr.inC, st),
+    if (d.prologue == TGP_PRO_MAXPOOL2)   // the group's pools in one launch
+      HIPCHK(tgpk::maxpool_forward_n(N->dt, cnt, src, pro_ptr, N->b, Lr.inH, Lr.inW, Lr.inC, st),
              "maxpool_forward");
-    if (d.kind == TGP_DWCONV3X3 && cnt == 2 &&
-        tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[0], cin_ptr[1], out[0], out[1],
-                         Lr.w)) {
-      HIPCHK(tgpk::dw_forward2(cin_ptr[0], cin_ptr[1], Lr.w, d.bias ? Lr.b : nullptr, out[0],
-                               out[1], N->b, Lr.H, Lr.W, d.cout, d.relu, st),
-             "dw_forward");
-    } else if (d.kind == TGP_DWCONV3X3) {
-      for (int k = 0; k < cnt; ++k)
-        HIPCHK(tgpk::dw_forward(N->dt, cin_ptr[k], Lr.w, d.bias ? Lr.b : nullptr, out[k], N->b,
-                                Lr.H, Lr.W, d.cout, d.relu, st),
-               "dw_forward");
+    if (d.kind == TGP_DWCONV3X3) {
+      // the row-window depthwise kernels take two micro-batches per launch
+      for (int k = 0; k < cnt; ++k) {
+        if (k + 1 < cnt && tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[k],
+                                            cin_ptr[k + 1], out[k], out[k + 1], Lr.w)) {
+          HIPCHK(tgpk::dw_forward2(cin_ptr[k], cin_ptr[k + 1], Lr.w, d.bias ? Lr.b : nullptr,
+                                   out[k], out[k + 1], N->b, Lr.H, Lr.W, d.cout, d.relu, st),
+                 "dw_forward");
+          ++k;
+        } else {
+          HIPCHK(tgpk::dw_forward(N->dt, cin_ptr[k], Lr.w, d.bias ? Lr.b : nullptr, out[k], N->b,
+                                  Lr.H, Lr.W, d.cout, d.relu, st),
+                 "dw_forward");
+        }
+      }
     } else {
       tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
-      if (cnt == 2)
-        HIPCHK(tgpk::conv_forward2(N->dt, cin_ptr[0], cin_ptr[1], Lr.w, d.bias ? Lr.b : nullptr,
-                                   out[0], out[1], s, d.relu, (float*)T_(N, iv[0], N->o_fpart),
-                                   (float*)T_(N, iv[1], N->o_fpart), N->fpart_floats, st),
-               "conv_forward2");
+      if (cnt > 1)
+        HIPCHK(tgpk::conv_forward_n(N->dt, cnt, cin_ptr, Lr.w, d.bias ? Lr.b : nullptr, out, s,
+                                    d.relu, fpart, N->fpart_floats, st),
+               "conv_forward_n");
       else
         HIPCHK(tgpk::conv_forward(N->dt, cin_ptr[0], Lr.w, d.bias ? Lr.b : nullptr, out[0], s,
                                   d.relu, (float*)T_(N, iv[0], N->o_fpart), N->fpart_floats, st),
@@ -373,18 +381,19 @@ struct BwdMb {
   const void* dy_pool = nullptr;
 };
 
-// F' (where checkpointed) and B for a group of cnt (1 or 2) micro-batches
-// iv[k] of partition j, layer by layer; a group of two runs the weight and
-// data gradients of each convolution as one launch where the kernel takes
-// two tensors (same values as one at a time).  dx_in[k] are all null or all
-// set.
+// F' (where checkpointed) and B for a group of cnt (1 .. MG) micro-batches
+// iv[k] of partition j, layer by layer; a group runs the weight and data
+// gradients of each convolution as one launch where the kernel takes all its
+// tensors, else as launches of two and one (same values as one at a time).
+// dx_in[k] are all null or all set.
 tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
                           const void* const* dy_out, void* const* dx_in, hipStream_t st) {
   const int lo = N->lo[j - 1], hi = N->hi[j - 1];
   {
-    int rc[2], ph[2] = {2, 2}, rcn = 0;
-    const void* rx[2];
-    void* ry[2] = {nullptr, nullptr};
+    int rc[MG], ph[MG], rcn = 0;
+    const void* rx[MG];
+    void* ry[MG] = {};
+    for (int k = 0; k < MG; ++k) ph[k] = 2;
     for (int k = 0; k < cnt; ++k)
       if (N->saved_ckpt[cell(N, iv[k], j)]) {
         rc[rcn] = iv[k];
@@ -398,7 +407,7 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     }
   }
   Range rg("B", iv[0], j);
-  BwdMb M[2];
+  BwdMb M[MG];
   auto stale = [&](int i) -> char& {
     return N->wt_stale[(size_t)((i - 1) % N->lanes) * N->n + (j - 1)];
   };
@@ -417,10 +426,10 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     const int i = iv[k];
     if (i > N->m - N->lanes) {
       // first backward of partition j on this lane in this step: refresh the
-      // lane's transformed weights used by the data-gradient kernels (the
-      // second of a pair reads the first's, so its lane is refreshed when
-      // a later backward of this step reads it)
-      if (cnt == 2 && k == 1) {
+      // lane's transformed weights used by the data-gradient kernels (a
+      // group reads its first micro-batch's, so the other lanes are
+      // refreshed when a later backward of this step reads them)
+      if (k > 0) {
         stale(i) = 1;
       } else {
         tgp_status r = refresh_wt(i);
@@ -448,15 +457,15 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
   for (int l = hi - 1; l >= lo; --l) {
     LayerRt& Lr = N->L[l];
     const tgp_layer& d = Lr.d;
-    const void* src[2];
-    const void* cin_ptr[2];
-    const void* dzk[2];   // the layer's dz: B.dz, or the incoming dy itself
-    std::array<tgpk::ReduceJob, 2>* pjs[2];
-    const void* yk[2];
-    const void* dskipk[2];
-    float* gbk[2];
-    float* bpartk[2];
-    tgpk::ReduceJob* bdeferk[2];
+    const void* src[MG];
+    const void* cin_ptr[MG];
+    const void* dzk[MG];   // the layer's dz: B.dz, or the incoming dy itself
+    std::array<tgpk::ReduceJob, 2>* pjs[MG];
+    const void* yk[MG];
+    const void* dskipk[MG];
+    float* gbk[MG];
+    float* bpartk[MG];
+    tgpk::ReduceJob* bdeferk[MG];
     const long nout = out_elems_mb(N, Lr);
     const long P = (long)N->b * Lr.H * Lr.W;
     for (int k = 0; k < cnt; ++k) {
@@ -478,10 +487,10 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
       bpartk[k] = Lr.defer_b ? (float*)G_(N, i, Lr.o_gcol) : B.colpart;
       bdeferk[k] = Lr.defer_b ? &pj[1] : nullptr;
     }
-    // The fused kernels take both micro-batches of a pair in one launch when
-    // both qualify (they always do together: same shape and flags, buffers
-    // of the same alignment).
-    tgpk::RbArgs ra[2];
+    // The fused kernels take the whole group in one launch when every
+    // micro-batch qualifies (they always do together: same shape and flags,
+    // buffers of the same alignment).
+    tgpk::RbArgs ra[MG];
     auto fill_ra = [&](const void* const* dyv) {
       for (int k = 0; k < cnt; ++k)
         ra[k] = tgpk::RbArgs{dyv[k], dskipk[k], yk[k], M[k].dz, gbk[k], bpartk[k], bdeferk[k]};
@@ -495,7 +504,8 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
                  tgpk::pool_relu_bias_fusable(N->dt, d.cout, Lr.H, Lr.W, M[k].dy_pool, dskipk[k],
                                               yk[k], M[k].dz);
     if (all_pool) {
-      const void* dps[2] = {M[0].dy_pool, cnt == 2 ? M[1].dy_pool : nullptr};
+      const void* dps[MG];
+      for (int k = 0; k < cnt; ++k) dps[k] = M[k].dy_pool;
       fill_ra(dps);
       HIPCHK(tgpk::pool_relu_backward_bias_n(N->dt, cnt, ra, d.relu, N->b, Lr.H, Lr.W, d.cout, st),
              "pool_relu_backward_bias");
@@ -527,7 +537,8 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
       all_rb = all_rb && (*pjs[k])[1].S == 0 && d.bias && Lr.o_gcol_floats &&
                tgpk::relu_bias_fusable(N->dt, d.cout, M[k].dy, dskipk[k], yk[k], M[k].dz);
     if (all_rb) {
-      const void* dys[2] = {M[0].dy, cnt == 2 ? M[1].dy : nullptr};
+      const void* dys[MG];
+      for (int k = 0; k < cnt; ++k) dys[k] = M[k].dy;
       fill_ra(dys);
       HIPCHK(tgpk::relu_backward_bias_n(N->dt, cnt, ra, d.relu, P, d.cout, st),
              "relu_backward_bias");
@@ -559,27 +570,32 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     }
     // weight gradient
     tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
-    if (d.kind != TGP_DWCONV3X3 && cnt == 2 && Lr.defer_w) {
-      HIPCHK(tgpk::conv_wgrad2(N->dt, cin_ptr[0], cin_ptr[1], dzk[0], dzk[1],
-                               (float*)G_(N, M[0].i, Lr.o_gw), (float*)G_(N, M[1].i, Lr.o_gw),
-                               (float*)G_(N, M[0].i, Lr.o_gpart),
-                               (float*)G_(N, M[1].i, Lr.o_gpart), s, st, &(*pjs[0])[0],
-                               &(*pjs[1])[0]),
-             "conv_wgrad2");
-    } else if (d.kind == TGP_DWCONV3X3 && cnt == 2 &&
-               tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[0], cin_ptr[1], dzk[0],
-                                dzk[1], M[0].part) &&
-               tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[0], cin_ptr[1], dzk[0],
-                                dzk[1], M[1].part)) {
-      HIPCHK(tgpk::dw_wgrad2(cin_ptr[0], cin_ptr[1], dzk[0], dzk[1],
-                             (float*)G_(N, M[0].i, Lr.o_gw), (float*)G_(N, M[1].i, Lr.o_gw),
-                             M[0].part, M[1].part, N->b, Lr.H, Lr.W, d.cout, st),
-             "dw_wgrad");
+    if (d.kind != TGP_DWCONV3X3 && cnt > 1 && Lr.defer_w) {
+      float* gws[MG];
+      float* gps[MG];
+      tgpk::ReduceJob* dfs[MG];
+      for (int k = 0; k < cnt; ++k) {
+        gws[k] = (float*)G_(N, M[k].i, Lr.o_gw);
+        gps[k] = (float*)G_(N, M[k].i, Lr.o_gpart);
+        dfs[k] = &(*pjs[k])[0];
+      }
+      HIPCHK(tgpk::conv_wgrad_n(N->dt, cnt, cin_ptr, dzk, gws, gps, s, st, dfs), "conv_wgrad_n");
     } else {
       for (int k = 0; k < cnt; ++k) {
         BwdMb& B = M[k];
         float* gw = (float*)G_(N, B.i, Lr.o_gw);
-        if (d.kind == TGP_DWCONV3X3) {
+        if (d.kind == TGP_DWCONV3X3 && k + 1 < cnt &&
+            tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[k], cin_ptr[k + 1], dzk[k],
+                             dzk[k + 1], M[k].part) &&
+            tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[k], cin_ptr[k + 1], dzk[k],
+                             dzk[k + 1], M[k + 1].part)) {
+          // the row-window depthwise kernels take two micro-batches per launch
+          HIPCHK(tgpk::dw_wgrad2(cin_ptr[k], cin_ptr[k + 1], dzk[k], dzk[k + 1], gw,
+                                 (float*)G_(N, M[k + 1].i, Lr.o_gw), M[k].part, M[k + 1].part,
+                                 N->b, Lr.H, Lr.W, d.cout, st),
+                 "dw_wgrad");
+          ++k;
+        } else if (d.kind == TGP_DWCONV3X3) {
           HIPCHK(tgpk::dw_wgrad(N->dt, cin_ptr[k], dzk[k], gw, B.part, N->b, Lr.H, Lr.W, d.cout,
                                 st),
                  "dw_wgrad");
@@ -593,29 +609,33 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     }
     if (l == lo && dx_in[0] == nullptr) break;
     // data gradient, into the gradient of the pre-prologue input
-    void* dest_prev[2];
-    void* dgrad_out[2];
+    void* dest_prev[MG];
+    void* dgrad_out[MG];
     for (int k = 0; k < cnt; ++k) {
       dest_prev[k] = (l == lo) ? dx_in[k] : M[k].gnext;
       dgrad_out[k] = d.prologue == TGP_PRO_NONE ? dest_prev[k] : M[k].dinp;
     }
-    if (d.kind == TGP_DWCONV3X3 && cnt == 2 &&
-        tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, dzk[0], dzk[1], dgrad_out[0],
-                         dgrad_out[1], Lr.w)) {
-      HIPCHK(tgpk::dw_dgrad2(dzk[0], dzk[1], Lr.w, dgrad_out[0], dgrad_out[1], N->b, Lr.H, Lr.W,
-                             d.cout, st),
-             "dw_dgrad");
-    } else if (d.kind == TGP_DWCONV3X3) {
-      for (int k = 0; k < cnt; ++k)
-        HIPCHK(tgpk::dw_dgrad(N->dt, dzk[k], Lr.w, dgrad_out[k], N->b, Lr.H, Lr.W, d.cout, st),
-               "dw_dgrad");
-    } else if (cnt == 2) {
-      // the lanes' transformed weights are equal copies; the first's serves both
-      HIPCHK(tgpk::conv_dgrad2(N->dt, dzk[0], dzk[1], Lr.w,
-                               Lr.has_wt ? T_(N, M[0].i, Lr.o_wt) : nullptr, dgrad_out[0],
-                               dgrad_out[1], s, (float*)T_(N, M[0].i, N->o_fpart),
-                               (float*)T_(N, M[1].i, N->o_fpart), N->fpart_floats, st),
-             "conv_dgrad2");
+    if (d.kind == TGP_DWCONV3X3) {
+      for (int k = 0; k < cnt; ++k) {
+        if (k + 1 < cnt && tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, dzk[k], dzk[k + 1],
+                                            dgrad_out[k], dgrad_out[k + 1], Lr.w)) {
+          HIPCHK(tgpk::dw_dgrad2(dzk[k], dzk[k + 1], Lr.w, dgrad_out[k], dgrad_out[k + 1], N->b,
+                                 Lr.H, Lr.W, d.cout, st),
+                 "dw_dgrad");
+          ++k;
+        } else {
+          HIPCHK(tgpk::dw_dgrad(N->dt, dzk[k], Lr.w, dgrad_out[k], N->b, Lr.H, Lr.W, d.cout, st),
+                 "dw_dgrad");
+        }
+      }
+    } else if (cnt > 1) {
+      // the lanes' transformed weights are equal copies; the first's serves all
+      float* fps[MG];
+      for (int k = 0; k < cnt; ++k) fps[k] = (float*)T_(N, M[k].i, N->o_fpart);
+      HIPCHK(tgpk::conv_dgrad_n(N->dt, cnt, dzk, Lr.w,
+                                Lr.has_wt ? T_(N, M[0].i, Lr.o_wt) : nullptr, dgrad_out, s, fps,
+                                N->fpart_floats, st),
+             "conv_dgrad_n");
     } else {
       HIPCHK(tgpk::conv_dgrad(N->dt, dzk[0], Lr.w, Lr.has_wt ? T_(N, M[0].i, Lr.o_wt) : nullptr,
                               dgrad_out[0], s, (float*)T_(N, M[0].i, N->o_fpart),
@@ -1317,34 +1337,35 @@ tgp_status tgp_stage_backward_recompute(tgp_net* N, int j, int i, const void* dy
   return TGP_OK;
 }
 
-tgp_status tgp_stage_forward2(tgp_net* N, int j, int i0, int i1, int checkpoint0,
-                              int checkpoint1, const void* x0, const void* x1, void* y0,
-                              void* y1, void* stream) {
+// F_{iv[k],j} for a group of cnt micro-batches on distinct lanes, in one
+// pass of the partition's layers.
+static tgp_status stage_forward_group(tgp_net* N, int j, int cnt, const int* iv, const int* ck,
+                                      const void* const* xs, void* const* ys, void* stream) {
   tgp_status r = check_ready(N, j);
   if (r != TGP_OK) return r;
   if (j < 1 || j > N->n) return fail(TGP_EINVAL, "partition %d out of 1..%d", j, N->n);
-  const int iv[2] = {i0, i1};
-  const int ck[2] = {checkpoint0, checkpoint1};
-  for (int k = 0; k < 2; ++k) {
+  if (cnt < 1 || cnt > MG) return fail(TGP_EINVAL, "count %d out of 1..%d", cnt, MG);
+  if (!ck || !xs || !ys) return fail(TGP_EINVAL, "NULL checkpoint, x_in or y_out array");
+  for (int k = 0; k < cnt; ++k) {
     if (iv[k] < 1 || iv[k] > N->m) return fail(TGP_EINVAL, "micro-batch %d out of 1..%d", iv[k], N->m);
     if ((ck[k] != 0) != ckpt_of(N->mode, iv[k], N->m))
       return fail(TGP_EINVAL, "checkpoint=%d disagrees with the planned policy for i=%d", ck[k], iv[k]);
     const int c = cell(N, iv[k], j);
     if (N->st[c] == FWD || N->st[c] == BWD)
       return fail(TGP_ESTATE, "F_{%d,%d} already ran in this step", iv[k], j);
+    for (int q = 0; q < k; ++q)
+      if ((iv[q] - 1) % N->lanes == (iv[k] - 1) % N->lanes)
+        return fail(TGP_EINVAL, "micro-batches %d and %d share a lane (lanes = %d)", iv[q], iv[k],
+                    N->lanes);
+    if (!xs[k] || !ys[k]) return fail(TGP_EINVAL, "NULL x_in or y_out");
+    if ((r = check_slices(N, j, xs[k], ys[k])) != TGP_OK) return r;
   }
-  if (i0 == i1 || (i0 - 1) % N->lanes == (i1 - 1) % N->lanes)
-    return fail(TGP_EINVAL, "micro-batches %d and %d share a lane (lanes = %d)", i0, i1, N->lanes);
-  if (!x0 || !x1 || !y0 || !y1) return fail(TGP_EINVAL, "NULL x_in or y_out");
-  if ((r = check_slices(N, j, x0, y0)) != TGP_OK || (r = check_slices(N, j, x1, y1)) != TGP_OK)
-    return r;
-  Range rg("F", i0, j);
-  const int ph[2] = {checkpoint0 ? 0 : 1, checkpoint1 ? 0 : 1};
-  const void* xs[2] = {x0, x1};
-  void* ys[2] = {y0, y1};
-  r = run_forward_g(N, j, 2, iv, ph, xs, ys, S(stream));
+  Range rg("F", iv[0], j);
+  int ph[MG];
+  for (int k = 0; k < cnt; ++k) ph[k] = ck[k] ? 0 : 1;
+  r = run_forward_g(N, j, cnt, iv, ph, xs, ys, S(stream));
   if (r != TGP_OK) return r;
-  for (int k = 0; k < 2; ++k) {
+  for (int k = 0; k < cnt; ++k) {
     const int c = cell(N, iv[k], j);
     N->st[c] = FWD;
     N->saved_x[c] = xs[k];
@@ -1354,31 +1375,66 @@ tgp_status tgp_stage_forward2(tgp_net* N, int j, int i0, int i1, int checkpoint0
   return TGP_OK;
 }
 
-tgp_status tgp_stage_backward_recompute2(tgp_net* N, int j, int i0, int i1, const void* dy0,
-                                         const void* dy1, void* dx0, void* dx1, void* stream) {
+tgp_status tgp_stage_forward2(tgp_net* N, int j, int i0, int i1, int checkpoint0,
+                              int checkpoint1, const void* x0, const void* x1, void* y0,
+                              void* y1, void* stream) {
+  const int iv[2] = {i0, i1};
+  const int ck[2] = {checkpoint0, checkpoint1};
+  const void* xs[2] = {x0, x1};
+  void* ys[2] = {y0, y1};
+  return stage_forward_group(N, j, 2, iv, ck, xs, ys, stream);
+}
+
+tgp_status tgp_stage_forward_n(tgp_net* N, int j, int i0, int count, const int* checkpoint,
+                               const void* const* x_in, void* const* y_out, void* stream) {
+  if (count < 1 || count > MG) return fail(TGP_EINVAL, "count %d out of 1..%d", count, MG);
+  int iv[MG];
+  for (int k = 0; k < count; ++k) iv[k] = i0 + k;
+  return stage_forward_group(N, j, count, iv, checkpoint, x_in, y_out, stream);
+}
+
+tgp_status tgp_stage_backward_recompute_n(tgp_net* N, int j, int i0, int count,
+                                          const void* const* dy_out, void* const* dx_in,
+                                          void* stream) {
   tgp_status r = check_ready(N, j);
   if (r != TGP_OK) return r;
   if (j < 1 || j > N->n) return fail(TGP_EINVAL, "partition %d out of 1..%d", j, N->n);
-  if (i0 < 2 || i0 > N->m || i1 != i0 - 1)
-    return fail(TGP_EINVAL, "need i1 = i0 - 1 within 1..%d (got %d, %d)", N->m, i0, i1);
-  if (N->gslots < N->m || (i0 - 1) % N->lanes == (i1 - 1) % N->lanes)
-    return fail(TGP_EINVAL, "two backwards at once need two or more lanes");
-  if (!dy0 || !dy1) return fail(TGP_EINVAL, "NULL dy_out");
-  if ((dx0 == nullptr) != (dx1 == nullptr)) return fail(TGP_EINVAL, "dx_in: both or neither");
-  if ((r = check_slices(N, j, dx0, dy0)) != TGP_OK || (r = check_slices(N, j, dx1, dy1)) != TGP_OK)
-    return r;
-  for (int i : {i0, i1})
-    if (N->st[cell(N, i, j)] != FWD) return fail(TGP_ESTATE, "B_{%d,%d} needs F_{%d,%d} first", i, j, i, j);
+  if (count < 1 || count > MG) return fail(TGP_EINVAL, "count %d out of 1..%d", count, MG);
+  if (i0 - count + 1 < 1 || i0 > N->m)
+    return fail(TGP_EINVAL, "micro-batches %d down to %d out of 1..%d", i0, i0 - count + 1, N->m);
+  if (count > 1 && (N->gslots < N->m || count > N->lanes))
+    return fail(TGP_EINVAL, "%d backwards at once need %d or more lanes (lanes = %d)", count, count,
+                N->lanes);
+  if (!dy_out || !dx_in) return fail(TGP_EINVAL, "NULL dy_out or dx_in array");
+  int iv[MG];
+  for (int k = 0; k < count; ++k) {
+    iv[k] = i0 - k;
+    if (!dy_out[k]) return fail(TGP_EINVAL, "NULL dy_out");
+    if ((dx_in[k] == nullptr) != (dx_in[0] == nullptr))
+      return fail(TGP_EINVAL, "dx_in: all or none");
+    if ((r = check_slices(N, j, dx_in[k], dy_out[k])) != TGP_OK) return r;
+  }
+  for (int k = 0; k < count; ++k)
+    if (N->st[cell(N, iv[k], j)] != FWD)
+      return fail(TGP_ESTATE, "B_{%d,%d} needs F_{%d,%d} first", iv[k], j, iv[k], j);
   if (i0 < N->m && N->st[cell(N, i0 + 1, j)] != ACC)
     return fail(TGP_ESTATE, "B_{%d,%d} must follow B_{%d,%d} and its accumulation", i0, j, i0 + 1, j);
-  const int iv[2] = {i0, i1};
+  r = run_backward_g(N, j, count, iv, dy_out, dx_in, S(stream));
+  if (r != TGP_OK) return r;
+  for (int k = 0; k < count; ++k) N->st[cell(N, iv[k], j)] = BWD;
+  return TGP_OK;
+}
+
+tgp_status tgp_stage_backward_recompute2(tgp_net* N, int j, int i0, int i1, const void* dy0,
+                                         const void* dy1, void* dx0, void* dx1, void* stream) {
+  if (i1 != i0 - 1) {
+    tgp_status r = check_ready(N, j);
+    if (r != TGP_OK) return r;
+    return fail(TGP_EINVAL, "need i1 = i0 - 1 within 1..%d (got %d, %d)", N->m, i0, i1);
+  }
   const void* dys[2] = {dy0, dy1};
   void* dxs[2] = {dx0, dx1};
-  r = run_backward_g(N, j, 2, iv, dys, dxs, S(stream));
-  if (r != TGP_OK) return r;
-  N->st[cell(N, i0, j)] = BWD;
-  N->st[cell(N, i1, j)] = BWD;
-  return TGP_OK;
+  return tgp_stage_backward_recompute_n(N, j, i0, 2, dys, dxs, stream);
 }
 
 tgp_status tgp_grad_accumulate(tgp_net* N, int j, int i, int overwrite, void* stream) {

@@ -63,19 +63,22 @@ __device__ __forceinline__ void lds_handoff_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// X2 / dZ2 / out2 (all null or all set) are a second micro-batch: its K
-// ranges follow the first's (sample index nb .. 2 nb - 1) and its slices go
-// to out2, so one launch covers both.
+// The micro-batches of one launch (ng of them, nb samples each): the K
+// ranges of micro-batch k follow those of k - 1 and its slices go to
+// out[k], so one launch covers them all.
+struct WgIo {
+  const bf16_t* x[kMaxGroup];
+  const bf16_t* dz[kMaxGroup];
+  float* out[kMaxGroup];
+};
 //
 // KS is the number of waves per SIMD: with KS = 2 the two waves of a SIMD
 // own the same 32 x 32 quarter and take alternate k steps, and the second's
 // sums are added to the first's through LDS before the store, so one wave's
 // MFMAs run while the other waits on its DMA issue or LDS reads.
 template <int W, int RPS, int NS, int KS>
-__global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
-    const bf16_t* __restrict__ X, const bf16_t* __restrict__ X2, const bf16_t* __restrict__ dZ,
-    const bf16_t* __restrict__ dZ2, float* __restrict__ out, float* __restrict__ out2, int nb,
-    int H, int Cin, int Cout, int R) {
+__global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int nb, int H,
+                                                            int Cin, int Cout, int R) {
   constexpr int AR = round32(RPS * W);          // dZ rows per stage
   constexpr int BW = W + 4;                     // LDS rows per padded input row
   constexpr int BR = round32(RPS * BW);         // padded X rows per stage
@@ -102,17 +105,13 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
   const int kpg = merged ? 1 : nb * nrb;          // K ranges per micro-batch
   const int sps = (H + RPS - 1) / RPS;            // stages per sample image (merged)
   const int per_k = 3 * nct * ncit;             // items per K range
-  const int ng = X2 ? 2 : 1;                    // micro-batches
   const int items = ng * kpg * per_k;
   const int G = gridDim.x;
   const int lb = xcd_remap(blockIdx.x, G);
   const int n_items = lb < items ? (items - lb + G - 1) / G : 0;
   const long E = (long)Cout * 9 * Cin;
 
-  const u32x4 rz = make_rsrc(dZ, nb * H * W * Cout * 2);
-  const u32x4 rx = make_rsrc(X, nb * H * W * Cin * 2);
-  const u32x4 rz2 = make_rsrc(X2 ? dZ2 : dZ, nb * H * W * Cout * 2);
-  const u32x4 rx2 = make_rsrc(X2 ? X2 : X, nb * H * W * Cin * 2);
+  const int zbytes = nb * H * W * Cout * 2, xbytes = nb * H * W * Cin * 2;
 
   // DMA lane constants: instruction u of this wave fills chunk c = NW u +
   // wave of the A (dZ) or B (padded X) region, rows 8 c + lane / 8, physical
@@ -188,23 +187,29 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
     return (rows + RPS - 1) / RPS;
   };
 
-  // issue side
-  int i_it = 0, i_st = 0, i_kr = 0, i_r = 0, i_co0 = 0, i_ci0 = 0, i_ns = 0;
+  // issue side; the issuing item's micro-batch gi (K range krl within it)
+  int i_it = 0, i_st = 0, i_kr = 0, i_r = 0, i_co0 = 0, i_ci0 = 0, i_ns = 0, i_krl = 0;
+  u32x4 rzg = {}, rxg = {};
+  auto issue_item = [&]() __attribute__((always_inline)) {
+    i_ns = stages_of(i_kr);
+    const int gi = i_kr / kpg;
+    i_krl = i_kr - gi * kpg;
+    rzg = make_rsrc(pick4(io.dz, gi), zbytes);
+    rxg = make_rsrc(pick4(io.x, gi), xbytes);
+  };
   if (n_items > 0) {
     coords(0, i_kr, i_r, i_co0, i_ci0);
-    i_ns = stages_of(i_kr);
+    issue_item();
   }
   // A stage's DMA is issued all at once, right after the ring barrier of
   // the stage NS - 1 before it.  (Spread over the k steps between the
   // MFMAs, the memory pipeline's issue stalls held up the MFMAs: 25 to 60%
   // slower.)
   auto issue = [&](int slot) __attribute__((always_inline)) {
-    const bool g1 = i_kr >= kpg;                             // second micro-batch (uniform)
-    const int krl = g1 ? i_kr - kpg : i_kr;
+    const int krl = i_krl;
     const int n = merged ? i_st / sps : krl / nrb;
     const int h = merged ? (i_st - (i_st / sps) * sps) * RPS
                          : (krl - (krl / nrb) * nrb) * R + i_st * RPS;   // first image row
-    const u32x4 rzg = g1 ? rz2 : rz, rxg = g1 ? rx2 : rx;
     const int zsoff = (((n * H + h) * W) * Cout + i_co0) * 2;
     const int hb = h + i_r - 1;                              // input row of stage row 0
     const int xsoff = (((n * H + hb) * W) * Cin + i_ci0) * 2;
@@ -230,7 +235,7 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
       i_st = 0;
       if (++i_it < n_items) {
         coords(i_it, i_kr, i_r, i_co0, i_ci0);
-        i_ns = stages_of(i_kr);
+        issue_item();
       }
     }
   };
@@ -328,8 +333,8 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(
     // epilogue: element v of lane l is co 8 (v / 4) + 4 (l / 32) + v % 4, ci
     // l % 32 of this wave's quarter; with KS = 2 wave kh stores v = 8 kh ..
     // 8 kh + 7
-    const bool g1 = kr >= kpg;
-    float* o = (g1 ? out2 : out) + (long)(g1 ? kr - kpg : kr) * E;
+    const int gi = kr / kpg;
+    float* o = pick4(io.out, gi) + (long)(kr - gi * kpg) * E;
     const int ci = ci0 + nw * 32 + (lane & 31);
     auto store = [&](int v0, int v1) __attribute__((always_inline)) {
 #pragma unroll
@@ -400,10 +405,8 @@ size_t wgrad_rows_partial_floats(const ConvShape& s) {
 }
 
 template <int W, int RPS, int NS, int KS>
-static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* X2, const bf16_t* DZ,
-                                    const bf16_t* DZ2, float* out, float* out2,
-                                    const ConvShape& s, const WgPlan& p, hipStream_t st) {
-  const int ng = X2 ? 2 : 1;
+static hipError_t launch_wgrad_rows(const WgIo& io, int ng, const ConvShape& s, const WgPlan& p,
+                                    hipStream_t st) {
   const long items = (long)ng * p.nK * 3 * (s.cout / 64) * (s.cin / 64);
   const int G = (int)(items < 256 ? items : 256);
   const double flops = 2.0 * ng * s.pixels() * s.cout * 9 * s.cin;
@@ -412,30 +415,27 @@ static hipError_t launch_wgrad_rows(const bf16_t* X, const bf16_t* X2, const bf1
   if (!name[0])
     snprintf(name, sizeof name, "conv_wgrad_rows<%d,%d,%d%s>", W, RPS, NS, KS == 2 ? ",8w" : "");
   ProfScope ps(name, flops, bytes, st);
-  TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, NS, KS>), dim3(G), dim3(256 * KS), 0, st, X, X2, DZ,
-             DZ2, out, out2, s.nb, s.H, s.cin, s.cout, p.R);
+  TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, NS, KS>), dim3(G), dim3(256 * KS), 0, st, io, ng, s.nb,
+             s.H, s.cin, s.cout, p.R);
   return launch_status();
 }
 
 template <int W, int RPS, int NS>
-static hipError_t launch_wgrad_rows_ks(const bf16_t* X, const bf16_t* X2, const bf16_t* DZ,
-                                       const bf16_t* DZ2, float* out, float* out2,
-                                       const ConvShape& s, const WgPlan& p, hipStream_t st) {
+static hipError_t launch_wgrad_rows_ks(const WgIo& io, int ng, const ConvShape& s,
+                                       const WgPlan& p, hipStream_t st) {
   // two waves per SIMD pay off where a stage has many k steps (widths 192
   // and 48 measured 1-3 % faster; 96 about even, 24 slower)
   const int ks = g_wgrad_ks ? g_wgrad_ks : ((W == 192 || W == 48) ? 2 : 1);
-  return ks == 2 ? launch_wgrad_rows<W, RPS, NS, 2>(X, X2, DZ, DZ2, out, out2, s, p, st)
-                 : launch_wgrad_rows<W, RPS, NS, 1>(X, X2, DZ, DZ2, out, out2, s, p, st);
+  return ks == 2 ? launch_wgrad_rows<W, RPS, NS, 2>(io, ng, s, p, st)
+                 : launch_wgrad_rows<W, RPS, NS, 1>(io, ng, s, p, st);
 }
 
-static hipError_t launch_wgrad_rows_w(const bf16_t* X, const bf16_t* X2, const bf16_t* DZ,
-                                      const bf16_t* DZ2, float* out, float* out2,
-                                      const ConvShape& s, const WgPlan& p, hipStream_t st) {
+static hipError_t launch_wgrad_rows_w(const WgIo& io, int ng, const ConvShape& s,
+                                      const WgPlan& p, hipStream_t st) {
   switch (s.W) {
 #define WG_CASE(i)                                                                           \
   case kWgCfgs[i].W:                                                                         \
-    return launch_wgrad_rows_ks<kWgCfgs[i].W, kWgCfgs[i].RPS, kWgCfgs[i].NS>(X, X2, DZ, DZ2,  \
-                                                                             out, out2, s, p, st);
+    return launch_wgrad_rows_ks<kWgCfgs[i].W, kWgCfgs[i].RPS, kWgCfgs[i].NS>(io, ng, s, p, st);
     WG_CASE(0) WG_CASE(1) WG_CASE(2) WG_CASE(3) WG_CASE(4)
     WG_CASE(5) WG_CASE(6) WG_CASE(7) WG_CASE(8) WG_CASE(9)
 #undef WG_CASE
@@ -449,9 +449,13 @@ hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, floa
   if (!wgrad_rows_ok(s)) return hipErrorInvalidValue;
   const WgPlan p = wgrad_rows_plan(s);
   float* out = p.nK > 1 ? partial : dw;
-  const bf16_t* X = (const bf16_t*)x;
-  const bf16_t* DZ = (const bf16_t*)dz;
-  hipError_t e = launch_wgrad_rows_w(X, nullptr, DZ, nullptr, out, nullptr, s, p, st);
+  WgIo io{};
+  for (int k = 0; k < kMaxGroup; ++k) {
+    io.x[k] = (const bf16_t*)x;
+    io.dz[k] = (const bf16_t*)dz;
+    io.out[k] = out;
+  }
+  hipError_t e = launch_wgrad_rows_w(io, 1, s, p, st);
   if (e != hipSuccess) return e;
   if (defer) {
     *defer = ReduceJob{out, dw, (long)s.cout * 9 * s.cin, p.nK};
@@ -462,23 +466,25 @@ hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, floa
   return splitk_reduce_launch(partial, dw, (long)s.cout * 9 * s.cin, p.nK, st, extra);
 }
 
-// Two micro-batches in one launch, each sum left pending (*defer0, *defer1):
-// the same slices as two conv_wgrad_rows_launch calls with `defer`.
-hipError_t conv_wgrad_rows_launch2(const void* x0, const void* x1, const void* dz0,
-                                   const void* dz1, float* dw0, float* dw1, float* partial0,
-                                   float* partial1, const ConvShape& s, hipStream_t st,
-                                   ReduceJob* defer0, ReduceJob* defer1) {
-  if (!wgrad_rows_ok(s) || !defer0 || !defer1) return hipErrorInvalidValue;
+// n micro-batches in one launch, each sum left pending (*defer[k]): the
+// same slices as n conv_wgrad_rows_launch calls with `defer`.
+hipError_t conv_wgrad_rows_launch_n(int n, const void* const* x, const void* const* dz,
+                                    float* const* dw, float* const* partial, const ConvShape& s,
+                                    hipStream_t st, ReduceJob* const* defer) {
+  if (n < 1 || n > kMaxGroup || !wgrad_rows_ok(s)) return hipErrorInvalidValue;
   const WgPlan p = wgrad_rows_plan(s);
-  float* o0 = p.nK > 1 ? partial0 : dw0;
-  float* o1 = p.nK > 1 ? partial1 : dw1;
-  const bf16_t *X0 = (const bf16_t*)x0, *X1 = (const bf16_t*)x1;
-  const bf16_t *D0 = (const bf16_t*)dz0, *D1 = (const bf16_t*)dz1;
-  hipError_t e = launch_wgrad_rows_w(X0, X1, D0, D1, o0, o1, s, p, st);
+  WgIo io{};
+  for (int k = 0; k < kMaxGroup; ++k) {   // unused entries repeat micro-batch 0
+    const int q = k < n ? k : 0;
+    io.x[k] = (const bf16_t*)x[q];
+    io.dz[k] = (const bf16_t*)dz[q];
+    io.out[k] = p.nK > 1 ? partial[q] : dw[q];
+    if (!io.x[k] || !io.dz[k] || !io.out[k] || !defer[q]) return hipErrorInvalidValue;
+  }
+  hipError_t e = launch_wgrad_rows_w(io, n, s, p, st);
   if (e != hipSuccess) return e;
   const long E = (long)s.cout * 9 * s.cin;
-  *defer0 = ReduceJob{o0, dw0, E, p.nK};
-  *defer1 = ReduceJob{o1, dw1, E, p.nK};
+  for (int k = 0; k < n; ++k) *defer[k] = ReduceJob{io.out[k], dw[k], E, p.nK};
   return hipSuccess;
 }
 

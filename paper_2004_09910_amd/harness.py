@@ -86,7 +86,7 @@ class Session:
         self.ws = None
         self.B = self.m = self.b = self.mode = None
         self.lanes = 1
-        self.pairs = False
+        self.group = 1          # micro-batches per stage call (1, 2 or 4)
         self._lane_streams = None
 
     def _bind_layer(self, idx: int, seed_offset: int):
@@ -214,11 +214,11 @@ class Session:
         NHWC; micro-batch slices are pointer offsets.  With several lanes the
         micro-batches run on lane streams forked from torch's current stream
         (`stream` is then unused) unless `serial`, which issues everything on
-        `stream` in order (two micro-batches per call with `pairs`)."""
+        `stream` in order (`group` micro-batches per call when above 1)."""
         def sl(t, i):
             return t.data_ptr() + (i - 1) * (t.numel() // self.m) * t.element_size()
-        if self.pairs:
-            return self._stage_step_pairs(j, x, y, dy, dx, sl, stream if serial else None)
+        if self.group > 1:
+            return self._stage_step_groups(j, x, y, dy, dx, sl, stream if serial else None)
         if self.lanes > 1 and not serial:
             return self._stage_step_lanes(j, x, y, dy, dx, sl)
         for i in range(1, self.m + 1):
@@ -258,53 +258,59 @@ class Session:
         for s in self._lane_streams:
             cur.wait_stream(s)
 
-    def _stage_step_pairs(self, j, x, y, dy, dx, sl, serial_stream=None):
-        """stage_step with two micro-batches per launch: forwards (1, 2),
-        (3, 4), ..., backwards (m, m - 1), (m - 2, m - 3), ..., each pair on
-        one stream per lane pair, and the accumulations, in the order m..1,
-        on one more stream that waits for each pair's backward (all on
-        `serial_stream`, in that order, when given).  Needs an even number of
-        lanes and an even m."""
+    def _stage_step_groups(self, j, x, y, dy, dx, sl, serial_stream=None):
+        """stage_step with G = `group` micro-batches per call: forwards
+        (1..G), (G+1..2G), ..., backwards (m..m-G+1), ..., each group on the
+        stream of its lanes, and the accumulations, in the order m..1, on
+        one more stream that waits for each group's backward (all on
+        `serial_stream`, in that order, when given).  Needs G to divide the
+        lanes and m."""
+        G = self.group
         K = min(self.lanes, self.m)
-        if K % 2 or self.m % 2:
-            raise ValueError(f"pairs need even lanes and m (lanes={self.lanes}, m={self.m})")
+        if K % G or self.m % G:
+            raise ValueError(f"groups of {G} need lanes and m divisible by {G} "
+                             f"(lanes={self.lanes}, m={self.m})")
+        h = self.h
+
+        def fwd(i, s):
+            ks = range(G)
+            tgp.stage_forward_n(h, j, i, [self.checkpointed(i + k) for k in ks],
+                                [sl(x, i + k) for k in ks], [sl(y, i + k) for k in ks], s)
+
+        def bwd(i, s):
+            ks = range(G)
+            tgp.stage_backward_recompute_n(h, j, i, [sl(dy, i - k) for k in ks],
+                                           [None if dx is None else sl(dx, i - k) for k in ks], s)
+
         if serial_stream is not None:
-            for i in range(1, self.m + 1, 2):
-                tgp.stage_forward2(self.h, j, i, i + 1, self.checkpointed(i),
-                                   self.checkpointed(i + 1), sl(x, i), sl(x, i + 1), sl(y, i),
-                                   sl(y, i + 1), serial_stream)
-            for i in range(self.m, 0, -2):
-                tgp.stage_backward_recompute2(self.h, j, i, i - 1, sl(dy, i), sl(dy, i - 1),
-                                              None if dx is None else sl(dx, i),
-                                              None if dx is None else sl(dx, i - 1), serial_stream)
-                tgp.grad_accumulate(self.h, j, i, i == self.m, serial_stream)
-                tgp.grad_accumulate(self.h, j, i - 1, False, serial_stream)
+            for i in range(1, self.m + 1, G):
+                fwd(i, serial_stream)
+            for i in range(self.m, 0, -G):
+                bwd(i, serial_stream)
+                for k in range(G):
+                    tgp.grad_accumulate(h, j, i - k, i - k == self.m, serial_stream)
             return
         cur = torch.cuda.current_stream()
         if self._lane_streams is None:
-            self._lane_streams = [torch.cuda.Stream() for _ in range(K // 2 + 1)]
-        streams, acc = self._lane_streams[:K // 2], self._lane_streams[K // 2]
+            self._lane_streams = [torch.cuda.Stream() for _ in range(K // G + 1)]
+        streams, acc = self._lane_streams[:K // G], self._lane_streams[K // G]
         for s in self._lane_streams:
             s.wait_stream(cur)
 
-        def pair_stream(i0, i1):
-            return streams[min((i0 - 1) % K, (i1 - 1) % K) // 2]
-        for i in range(1, self.m + 1, 2):
-            s = pair_stream(i, i + 1)
-            tgp.stage_forward2(self.h, j, i, i + 1, self.checkpointed(i), self.checkpointed(i + 1),
-                               sl(x, i), sl(x, i + 1), sl(y, i), sl(y, i + 1), s.cuda_stream)
+        def group_stream(i_lo):            # the group of micro-batches i_lo .. i_lo + G - 1
+            return streams[((i_lo - 1) % K) // G]
+        for i in range(1, self.m + 1, G):
+            fwd(i, group_stream(i).cuda_stream)
         self._events = []
-        for i in range(self.m, 0, -2):
-            s = pair_stream(i, i - 1)
-            tgp.stage_backward_recompute2(self.h, j, i, i - 1, sl(dy, i), sl(dy, i - 1),
-                                          None if dx is None else sl(dx, i),
-                                          None if dx is None else sl(dx, i - 1), s.cuda_stream)
+        for i in range(self.m, 0, -G):
+            s = group_stream(i - G + 1)
+            bwd(i, s.cuda_stream)
             ev = torch.cuda.Event()
             ev.record(s)
             self._events.append(ev)
             acc.wait_event(ev)
-            tgp.grad_accumulate(self.h, j, i, i == self.m, acc.cuda_stream)
-            tgp.grad_accumulate(self.h, j, i - 1, False, acc.cuda_stream)
+            for k in range(G):
+                tgp.grad_accumulate(h, j, i - k, i - k == self.m, acc.cuda_stream)
         for s in self._lane_streams:
             cur.wait_stream(s)
 

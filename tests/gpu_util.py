@@ -136,7 +136,7 @@ def only_samples(G, samples):
 
 
 def gpu_stage(net, dtype, B, m, mode, balance, j, want_dx=True, G_override=None, sess=None,
-              stash_in=None, lanes=1, pairs=False, serial=False, family=NORMAL,
+              stash_in=None, lanes=1, group=1, serial=False, family=NORMAL,
               grad_samples=None):
     """One stage step of partition j through the C ABI.  `grad_samples`
     zeroes the upstream gradients of every other sample; `serial` issues
@@ -148,7 +148,7 @@ def gpu_stage(net, dtype, B, m, mode, balance, j, want_dx=True, G_override=None,
         sess = Session(net, dtype, n=n, balance=balance, bind_layers=range(lo, hi),
                        family=family)
         sess.plan(B, m, mode, lanes)
-        sess.pairs = pairs
+        sess.group = group
     xv, xraw, G = stage_values(net, lo, hi, B, dtype, family)
     if G_override is not None:
         G = G_override

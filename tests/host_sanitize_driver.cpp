@@ -114,6 +114,17 @@ int main() {
                                      nullptr) == TGP_EINVAL);
             EXPECT(tgp_pipeline_step(N, FAKE, FAKE, 8, m, n, mode, (float*)((char*)FAKE + 2),
                                      nullptr, nullptr) == TGP_EINVAL);
+            {   // group calls that fail a host check (count, order, lanes, state)
+              const int ckv[4] = {ck, ck, ck, ck};
+              const void* xs[4] = {FAKE, FAKE, FAKE, FAKE};
+              void* ys[4] = {FAKE, FAKE, FAKE, FAKE};
+              EXPECT(tgp_stage_forward_n(N, 1, 1, 0, ckv, xs, ys, nullptr) == TGP_EINVAL);
+              EXPECT(tgp_stage_forward_n(N, 1, 1, 5, ckv, xs, ys, nullptr) == TGP_EINVAL);
+              EXPECT(tgp_stage_forward_n(N, 1, m, 2, ckv, xs, ys, nullptr) == TGP_EINVAL);
+              EXPECT(tgp_stage_backward_recompute_n(N, 1, 1, 2, xs, ys, nullptr) == TGP_EINVAL);
+              const tgp_status sb = tgp_stage_backward_recompute_n(N, 1, m, 1, xs, ys, nullptr);
+              EXPECT(sb == TGP_ESTATE);
+            }
             if (lanes > 1) {   // refused for its size or for its lanes
               const tgp_status st = tgp_pipeline_step_static(N, FAKE, FAKE, 8, m, n, mode,
                                                              (float*)FAKE, nullptr, nullptr);

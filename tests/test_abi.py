@@ -264,12 +264,52 @@ def test_paired_stage_calls_check_lanes_and_order():
     assert st("tgp_stage_backward_recompute2", 1, 1, 0, F, F, None, None, None) == tgp.EINVAL
     assert st("tgp_stage_backward_recompute2", 1, 4, 3, F, None, None, None, None) == tgp.EINVAL
     assert st("tgp_stage_backward_recompute2", 1, 4, 3, F, F, F, None, None) == tgp.EINVAL
-    assert "both" in tgp.last_error()
+    assert "all or none" in tgp.last_error()
     # one lane: a single gradient slot, so no backward pair
     tgp.set_lanes(h, 1)
     tgp.bind_workspace(h, FAKE, tgp.plan(h, 8, 4, 1))
     assert st("tgp_stage_forward2", 1, 1, 2, 1, 1, F, F, F, F, None) == tgp.EINVAL
     assert st("tgp_stage_backward_recompute2", 1, 4, 3, F, F, None, None, None) == tgp.EINVAL
+    assert "lanes" in tgp.last_error()
+    tgp.net_destroy(h)
+
+
+def test_group_stage_calls_check_count_lanes_and_order():
+    """tgp_stage_forward_n / tgp_stage_backward_recompute_n: 1..4 tasks on
+    distinct lanes, consecutive micro-batches (i0 upwards for the forward,
+    downwards for the backward), each passing the single call's checks.
+    Every call here fails a host check, so nothing is enqueued."""
+    import ctypes
+    h, _ = _bound_net(mode=1, B=8, m=4, n=2)
+    tgp.set_lanes(h, 4)
+    tgp.bind_workspace(h, FAKE, tgp.plan(h, 8, 4, 1))
+    st = lambda name, *a: tgp.call_status(name, h, *a)
+    F = FAKE
+    I4 = lambda *v: (ctypes.c_int * 4)(*v)
+    P4 = lambda *v: (ctypes.c_void_p * 4)(*v)
+    ck = I4(1, 1, 1, 0)                       # except-last: only i = 4 keeps its activations
+    xs, none = P4(F, F, F, F), P4(None, None, None, None)
+    assert st("tgp_stage_forward_n", 1, 1, 0, ck, xs, xs, None) == tgp.EINVAL      # count 0
+    assert st("tgp_stage_forward_n", 1, 1, 5, ck, xs, xs, None) == tgp.EINVAL      # count 5
+    assert st("tgp_stage_forward_n", 1, 2, 4, ck, xs, xs, None) == tgp.EINVAL      # i = 5
+    assert st("tgp_stage_forward_n", 1, 1, 4, I4(1, 1, 1, 1), xs, xs, None) == tgp.EINVAL
+    assert "checkpoint" in tgp.last_error()
+    assert st("tgp_stage_forward_n", 1, 1, 4, ck, P4(F, None, F, F), xs, None) == tgp.EINVAL
+    assert st("tgp_stage_forward_n", 3, 1, 2, ck, xs, xs, None) == tgp.EINVAL      # j = 3
+    assert st("tgp_stage_backward_recompute_n", 1, 4, 4, xs, none, None) == tgp.ESTATE
+    assert st("tgp_stage_backward_recompute_n", 1, 3, 4, xs, none, None) == tgp.EINVAL   # 3..0
+    assert st("tgp_stage_backward_recompute_n", 1, 4, 4, xs, P4(F, None, None, None),
+              None) == tgp.EINVAL
+    assert "all or none" in tgp.last_error()
+    assert st("tgp_stage_backward_recompute_n", 1, 4, 4, P4(F, F, None, F), none,
+              None) == tgp.EINVAL
+    # two lanes: micro-batches 1 and 3 share one, and a backward of four
+    # needs four
+    tgp.set_lanes(h, 2)
+    tgp.bind_workspace(h, FAKE, tgp.plan(h, 8, 4, 1))
+    assert st("tgp_stage_forward_n", 1, 1, 4, ck, xs, xs, None) == tgp.EINVAL
+    assert "share a lane" in tgp.last_error()
+    assert st("tgp_stage_backward_recompute_n", 1, 4, 4, xs, none, None) == tgp.EINVAL
     assert "lanes" in tgp.last_error()
     tgp.net_destroy(h)
 

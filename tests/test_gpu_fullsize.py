@@ -23,7 +23,7 @@ from workloads.synth import EXACT
 pytestmark = pytest.mark.gpu
 
 SAMPLES = [0, 31]   # first sample of micro-batch 1 and last of micro-batch 8
-BENCH = dict(lanes=2, pairs=True, serial=True)
+BENCH = dict(lanes=4, group=4, serial=True)
 
 
 @pytest.fixture(scope="module")

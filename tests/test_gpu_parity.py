@@ -52,23 +52,24 @@ def test_lanes_are_bit_identical(mode):
 
 
 @pytest.mark.parametrize("mode", MODES)
-def test_micro_batch_pairs_are_bit_identical(mode):
-    """Two micro-batches per launch (tgp_stage_forward2 /
-    tgp_stage_backward_recompute2 on two lanes) give the same bits as one
-    micro-batch per launch on one stream, on a stage that holds both
+def test_micro_batch_groups_are_bit_identical(mode):
+    """Two and four micro-batches per launch (tgp_stage_forward_n /
+    tgp_stage_backward_recompute_n on as many lanes) give the same bits as
+    one micro-batch per launch on one stream, on a stage that holds both
     nine-tap kernel widths, pooling, an exported skip and a ragged mix of
     layer shapes."""
     net = specs.unet(5, 64, 64, 48, "unet5-c64-48")
     bal = (7, 5, 3, 4)
     runs = []
-    for k, pairs in ((1, False), (2, True)):
-        say(f"pairs={pairs} mode={mode}")
-        runs.append(gpu_stage(net, BF16, 8, 4, mode, bal, 1, lanes=k, pairs=pairs))
-    same_bits(runs[0], runs[1])
-    assert torch.equal(runs[1]["y"], runs[0]["y"])
-    assert torch.equal(runs[1]["dx"], runs[0]["dx"])
-    for sid in runs[0]["stash"]:
-        assert torch.equal(runs[1]["stash"][sid], runs[0]["stash"][sid])
+    for k in (1, 2, 4):
+        say(f"group={k} mode={mode}")
+        runs.append(gpu_stage(net, BF16, 8, 4, mode, bal, 1, lanes=k, group=k))
+    for r in runs[1:]:
+        same_bits(runs[0], r)
+        assert torch.equal(r["y"], runs[0]["y"])
+        assert torch.equal(r["dx"], runs[0]["dx"])
+        for sid in runs[0]["stash"]:
+            assert torch.equal(r["stash"][sid], runs[0]["stash"][sid])
 
 
 def test_pair_then_single_calls_in_one_step():
@@ -108,19 +109,20 @@ def test_pair_then_single_calls_in_one_step():
     assert torch.equal(got["dx"], ref["dx"])
 
 
-def test_micro_batch_pairs_bench_stage():
-    """The pair path on the benchmark's own stage (U-Net level-0 layers at
-    192 x 192, micro-batch 4), m = 2, against one micro-batch per launch."""
+def test_micro_batch_groups_bench_stage():
+    """The group path on the benchmark's own stage (U-Net level-0 layers at
+    192 x 192, micro-batch 4), m = 4, in groups of two and four against one
+    micro-batch per launch."""
     net = specs.unet(5, 64, 64, 192, "unet5-c64")
     bal = (7, 5, 3, 4)
     runs = []
-    for k, pairs in ((1, False), (2, True)):
-        say(f"bench stage pairs={pairs}")
-        runs.append(gpu_stage(net, BF16, 8, 2, CKPT_EXCEPT_LAST, bal, 1, lanes=k,
-                              pairs=pairs))
-    same_bits(runs[0], runs[1])
-    assert torch.equal(runs[1]["y"], runs[0]["y"])
-    assert torch.equal(runs[1]["dx"], runs[0]["dx"])
+    for k in (1, 2, 4):
+        say(f"bench stage group={k}")
+        runs.append(gpu_stage(net, BF16, 16, 4, CKPT_EXCEPT_LAST, bal, 1, lanes=k, group=k))
+    for r in runs[1:]:
+        same_bits(runs[0], r)
+        assert torch.equal(r["y"], runs[0]["y"])
+        assert torch.equal(r["dx"], runs[0]["dx"])
 
 
 def test_tiny_fp32_pipeline_all_modes():
@@ -313,19 +315,20 @@ def test_amoeba_cells_stage_except_last():
     check_stage(got, ref, BF16, "cells outputs", dx=False, grads=False)
 
 
-def test_amoeba_cells_pairs_are_bit_identical():
-    """Two micro-batches per launch on the depthwise / pointwise cells (the
-    depthwise kernels run once per micro-batch inside the pair) against one
-    per launch, except-last."""
+def test_amoeba_cells_groups_are_bit_identical():
+    """Two and four micro-batches per call on the depthwise / pointwise cells
+    (the depthwise and 1x1 kernels take two micro-batches per launch, so a
+    group of four runs as two launches each) against one per launch,
+    except-last."""
     net = specs.amoeba_cells(4, 256, 14, "cells4-c256")
     runs = []
-    for k, pairs in ((1, False), (2, True)):
-        say(f"cells pairs={pairs}")
-        runs.append(gpu_stage(net, BF16, 8, 4, CKPT_EXCEPT_LAST, (8,), 1, lanes=k,
-                              pairs=pairs))
-    same_bits(runs[0], runs[1])
-    assert torch.equal(runs[1]["y"], runs[0]["y"])
-    assert torch.equal(runs[1]["dx"], runs[0]["dx"])
+    for k in (1, 2, 4):
+        say(f"cells group={k}")
+        runs.append(gpu_stage(net, BF16, 8, 4, CKPT_EXCEPT_LAST, (8,), 1, lanes=k, group=k))
+    for r in runs[1:]:
+        same_bits(runs[0], r)
+        assert torch.equal(r["y"], runs[0]["y"])
+        assert torch.equal(r["dx"], runs[0]["dx"])
 
 
 @pytest.mark.timeout(600)
