@@ -614,13 +614,17 @@ __global__ __launch_bounds__(256) void conv_rows_epilogue(const float* __restric
 // 64 pixels (two 32 x 32 MFMA tiles), so every pixel row is read once.
 // The K order (64-channel stages, 16-channel MFMA steps, increasing
 // channel) is conv_fwd_dma's, so both kernels give the same bits.  Blocks
-// are persistent over the tiles of both micro-batches (X2 / Y2: a second
-// micro-batch of P pixels, its tiles after the first's).
+// are persistent over the tiles of all ng micro-batches of the launch (each
+// of P pixels, micro-batch k's tiles after those of k - 1).
+struct Mb1x1 {
+  const bf16_t* x[kMaxGroup];
+  bf16_t* y[kMaxGroup];
+};
 template <int NS>
-__global__ __launch_bounds__(512) void conv1x1_res(
-    const bf16_t* __restrict__ X0, const bf16_t* __restrict__ X2, const bf16_t* __restrict__ Wt,
-    const float* __restrict__ bias, bf16_t* __restrict__ Y0, bf16_t* __restrict__ Y2, int P,
-    int Cin, int relu) {
+__global__ __launch_bounds__(512) void conv1x1_res(Mb1x1 io, int ng,
+                                                   const bf16_t* __restrict__ Wt,
+                                                   const float* __restrict__ bias, int P, int Cin,
+                                                   int relu) {
   constexpr int COUT = 256, BM = 64, NW = 8;
   __shared__ u32x4 smem[(4 * COUT + NS * BM) * 8];             // weights, then the ring
   u32x4* const ring = smem + 4 * COUT * 8;
@@ -628,7 +632,7 @@ __global__ __launch_bounds__(512) void conv1x1_res(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nks = Cin / 64;                                     // stages per tile
   const int T1 = (P + BM - 1) / BM;                             // tiles per micro-batch
-  const int T = X2 ? 2 * T1 : T1;
+  const int T = ng * T1;
   const int G = gridDim.x;
   const int lb = xcd_remap(blockIdx.x, G);
   const int n_mine = lb < T ? (T - lb + G - 1) / G : 0;
@@ -651,9 +655,9 @@ __global__ __launch_bounds__(512) void conv1x1_res(
   const int xc = (lane & 7) ^ ((xr ^ (xr >> 3)) & 7);
   auto issue = [&](int idx) __attribute__((always_inline)) {
     const int tt = lb + (idx / nks) * G, ks = idx - (idx / nks) * nks;
-    const bool g1 = tt >= T1;                                   // uniform
-    const bf16_t* X = g1 ? X2 : X0;
-    const int p = min((g1 ? tt - T1 : tt) * BM + xr, P - 1);    // rows past P: any pixel
+    const int gi = tt / T1;                                     // micro-batch (uniform)
+    const bf16_t* X = pick4(io.x, gi);
+    const int p = min((tt - gi * T1) * BM + xr, P - 1);         // rows past P: any pixel
     __builtin_amdgcn_global_load_lds((const void*)(X + (long)p * Cin + ks * 64 + xc * 8),
                                      TGP_LDS(&ring[(idx % NS) * BM * 8 + wave * 64]), 16, 0, 0);
   };
@@ -670,9 +674,9 @@ __global__ __launch_bounds__(512) void conv1x1_res(
   int idx = 0;
   for (int it = 0; it < n_mine; ++it) {
     const int tt = lb + it * G;
-    const bool g1 = tt >= T1;
-    bf16_t* __restrict__ Y = g1 ? Y2 : Y0;
-    const int p0 = (g1 ? tt - T1 : tt) * BM;
+    const int gi = tt / T1;
+    bf16_t* __restrict__ Y = pick4(io.y, gi);
+    const int p0 = (tt - gi * T1) * BM;
     f32x16_t acc[2] = {f32x16_t{}, f32x16_t{}};
     for (int ks = 0; ks < nks; ++ks, ++idx) {
       // loads complete in order (the weights first); epilogue stores only
@@ -993,13 +997,16 @@ __device__ __forceinline__ void transpose8x8(const u32x4 (&in)[8], u32x4 (&out)[
   }
 }
 
-// X2 / dZ2 / part2 (all null or all set): a second micro-batch, whose blocks
-// form the second half of the grid.
+// The ng micro-batches of one launch: micro-batch k's blocks form the k-th
+// of ng equal parts of the grid.
+struct MbWg {
+  const bf16_t* x[kMaxGroup];
+  const bf16_t* dz[kMaxGroup];
+  float* part[kMaxGroup];
+};
 template <int WM, int WN, int TM, int TN, int TAPS>
-__global__ __launch_bounds__(256) void conv_wgrad_mfma(
-    const bf16_t* __restrict__ X0, const bf16_t* __restrict__ X2, const bf16_t* __restrict__ dZ0,
-    const bf16_t* __restrict__ dZ2, float* __restrict__ part0, float* __restrict__ part2, int P,
-    int H, int W, int Cin, int Cout, int pix_per_split) {
+__global__ __launch_bounds__(256) void conv_wgrad_mfma(MbWg io, int ng, int P, int H, int W,
+                                                       int Cin, int Cout, int pix_per_split) {
   static_assert(WM * WN == 4, "4 waves");
   constexpr int BMc = WM * TM * 32;  // output channels (co) per block
   constexpr int BNc = WN * TN * 32;  // input channels (ci) per block
@@ -1015,13 +1022,13 @@ __global__ __launch_bounds__(256) void conv_wgrad_mfma(
   // runs a contiguous range of splits with all their tiles, so the pixel rows
   // of X and dZ a split reads are fetched into one L2 only.
   const int T = TAPS * ncb * (Cout / BMc);
-  const int per = X2 ? gridDim.x / 2 : gridDim.x;               // blocks per micro-batch
+  const int per = gridDim.x / ng;                               // blocks per micro-batch
   const int lb0 = xcd_remap(blockIdx.x, gridDim.x);
-  const bool g1 = lb0 >= per;                                   // second micro-batch (uniform)
-  const int lb = g1 ? lb0 - per : lb0;
-  const bf16_t* __restrict__ X = g1 ? X2 : X0;
-  const bf16_t* __restrict__ dZ = g1 ? dZ2 : dZ0;
-  float* __restrict__ part = g1 ? part2 : part0;
+  const int gi = lb0 / per;                                     // micro-batch (uniform)
+  const int lb = lb0 - gi * per;
+  const bf16_t* __restrict__ X = pick4(io.x, gi);
+  const bf16_t* __restrict__ dZ = pick4(io.dz, gi);
+  float* __restrict__ part = pick4(io.part, gi);
   const int split = lb / T;
   const int t = lb - split * T;
   const int tx = t % (TAPS * ncb);
@@ -1407,19 +1414,22 @@ static bool conv1x1_res_ok(const ConvShape& s) {
   return s.taps == 1 && s.cout == 256 && s.cin % 64 == 0 && s.cin <= 256 && s.pixels() > 0;
 }
 
-static hipError_t launch_1x1_res(const bf16_t* X, const bf16_t* X2, const bf16_t* Wt,
-                                 const float* b, bf16_t* Y, bf16_t* Y2, const ConvShape& s,
-                                 int relu, hipStream_t st) {
-  if (!conv1x1_res_ok(s) || (X2 == nullptr) != (Y2 == nullptr)) return hipErrorInvalidValue;
+// n micro-batches x[k] -> y[k] in one launch.
+static hipError_t launch_1x1_res(int n, const void* const* x, const bf16_t* Wt, const float* b,
+                                 void* const* y, const ConvShape& s, int relu, hipStream_t st) {
+  if (!conv1x1_res_ok(s) || n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
   const long P = s.pixels();
   if (P > (1L << 30)) return hipErrorInvalidValue;              // pixel index is an int
-  const int ng = X2 ? 2 : 1;
-  const long T = ng * ((P + 63) / 64);
+  Mb1x1 io;
+  for (int k = 0; k < kMaxGroup; ++k) {   // unused entries repeat the first
+    io.x[k] = (const bf16_t*)x[k < n ? k : 0];
+    io.y[k] = (bf16_t*)y[k < n ? k : 0];
+  }
+  const long T = n * ((P + 63) / 64);
   const int G = (int)(T < 256 ? T : 256);
-  ProfScope ps("conv1x1_res", 2.0 * ng * P * s.cout * s.cin,
-               2.0 * ((double)ng * P * (s.cin + s.cout) + (double)s.cout * s.cin), st);
-  TGP_LAUNCH(ps, conv1x1_res<3>, dim3(G), dim3(512), 0, st, X, X2, Wt, b, Y, Y2, (int)P, s.cin,
-             relu);
+  ProfScope ps("conv1x1_res", 2.0 * n * P * s.cout * s.cin,
+               2.0 * ((double)n * P * (s.cin + s.cout) + (double)s.cout * s.cin), st);
+  TGP_LAUNCH(ps, conv1x1_res<3>, dim3(G), dim3(512), 0, st, io, n, Wt, b, (int)P, s.cin, relu);
   return launch_status();
 }
 
@@ -1530,7 +1540,7 @@ hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void*
   bf16_t* Y2 = nullptr;
   const FwdPlan pl = fwd_plan(s);
   const bool wide = s.cout % 128 == 0;
-  if (pl.cfg == 150) return launch_1x1_res(X, nullptr, Wt, b, Y, nullptr, s, relu, st);
+  if (pl.cfg == 150) return launch_1x1_res(1, &x, Wt, b, &y, s, relu, st);
   if (pl.cfg >= 400) {
     g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
     const hipError_t e = conv_forward_rows32(1, &x, w, b, &y, s, relu, st);
@@ -1599,49 +1609,48 @@ size_t wgrad_mfma_partial_floats(const ConvShape& s) {
   return (size_t)pl.S * E;
 }
 
-// The per-tap weight gradient of one micro-batch, or of two in one grid
-// (x1 / dz1 / partial1 set; dw1 their sum's target); the split plan is the
-// single micro-batch's either way.
-static hipError_t launch_wgrad_mfma(const void* x, const void* x1, const void* dz,
-                                    const void* dz1, float* dw, float* dw1, float*& partial,
-                                    float*& partial1, const ConvShape& s, WgradPlan& pl,
-                                    hipStream_t st) {
+// The per-tap weight gradient of n micro-batches in one grid; the split plan
+// is the single micro-batch's either way.  Where the plan has one split,
+// part[k] is set to dw[k] (the kernel writes the gradient itself).
+static hipError_t launch_wgrad_mfma(int n, const void* const* x, const void* const* dz,
+                                    float* const* dw, float** part, const ConvShape& s,
+                                    WgradPlan& pl, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
   long P = s.pixels();
-  const bf16_t* X = (const bf16_t*)x;
-  const bf16_t* DZ = (const bf16_t*)dz;
-  const bf16_t* X2 = (const bf16_t*)x1;
-  const bf16_t* DZ2 = (const bf16_t*)dz1;
-  const int ng = x1 ? 2 : 1;
   bool big = s.cin % 128 == 0 && s.cout % 128 == 0;
   int bm = big ? 128 : 64, bn = big ? 128 : 64;
   int tiles = s.taps * (s.cin / bn) * (s.cout / bm);
   long E = (long)s.cout * s.taps * s.cin;
   pl = wgrad_plan<2, 2>(P, tiles, E);
-  dim3 grid(ng * s.taps * (s.cin / bn) * (s.cout / bm) * pl.S);
-  double flops = 2.0 * ng * P * E;
-  double bytes = ng * (2.0 * ((double)P * s.cin + (double)P * s.cout) + 4.0 * pl.S * E);
+  if (pl.S == 1)   // a single split writes the gradient itself
+    for (int k = 0; k < n; ++k) part[k] = dw[k];
+  MbWg io;
+  for (int k = 0; k < kMaxGroup; ++k) {   // unused entries repeat the first
+    const int q = k < n ? k : 0;
+    io.x[k] = (const bf16_t*)x[q];
+    io.dz[k] = (const bf16_t*)dz[q];
+    io.part[k] = part[q];
+  }
+  dim3 grid(n * s.taps * (s.cin / bn) * (s.cout / bm) * pl.S);
+  double flops = 2.0 * n * P * E;
+  double bytes = n * (2.0 * ((double)P * s.cin + (double)P * s.cout) + 4.0 * pl.S * E);
   const char* nm = big ? (s.taps == 9 ? "conv_wgrad_mfma<2,2,2,2,9>" : "conv_wgrad_mfma<2,2,2,2,1>")
                        : (s.taps == 9 ? "conv_wgrad_mfma<2,2,1,1,9>" : "conv_wgrad_mfma<2,2,1,1,1>");
   ProfScope ps(nm, flops, bytes, st);
-  if (pl.S == 1) {   // a single split writes the gradient itself
-    partial = dw;
-    partial1 = dw1;
-  }
-  float* P2 = x1 ? partial1 : nullptr;
   if (big) {
     if (s.taps == 9)
-      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 2, 2, 9>), grid, dim3(256), 0, st, X, X2, DZ, DZ2,
-                 partial, P2, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 2, 2, 9>), grid, dim3(256), 0, st, io, n, (int)P, s.H,
+                 s.W, s.cin, s.cout, pl.pix_per_split);
     else
-      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 2, 2, 1>), grid, dim3(256), 0, st, X, X2, DZ, DZ2,
-                 partial, P2, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 2, 2, 1>), grid, dim3(256), 0, st, io, n, (int)P, s.H,
+                 s.W, s.cin, s.cout, pl.pix_per_split);
   } else {
     if (s.taps == 9)
-      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 9>), grid, dim3(256), 0, st, X, X2, DZ, DZ2,
-                 partial, P2, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 9>), grid, dim3(256), 0, st, io, n, (int)P, s.H,
+                 s.W, s.cin, s.cout, pl.pix_per_split);
     else
-      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 1>), grid, dim3(256), 0, st, X, X2, DZ, DZ2,
-                 partial, P2, (int)P, s.H, s.W, s.cin, s.cout, pl.pix_per_split);
+      TGP_LAUNCH(ps, (conv_wgrad_mfma<2, 2, 1, 1, 1>), grid, dim3(256), 0, st, io, n, (int)P, s.H,
+                 s.W, s.cin, s.cout, pl.pix_per_split);
   }
   return launch_status();
 }
@@ -1652,8 +1661,7 @@ hipError_t conv_wgrad_mfma(const void* x, const void* dz, float* dw, float* part
   if (use_wgrad_rows(s)) return conv_wgrad_rows_launch(x, dz, dw, partial, s, st, extra, defer);
   long E = (long)s.cout * s.taps * s.cin;
   WgradPlan pl;
-  float* unused = nullptr;
-  hipError_t e = launch_wgrad_mfma(x, nullptr, dz, nullptr, dw, nullptr, partial, unused, s, pl, st);
+  hipError_t e = launch_wgrad_mfma(1, &x, &dz, &dw, &partial, s, pl, st);
   if (e != hipSuccess) return e;
   if (defer) {
     *defer = ReduceJob{partial, dw, E, pl.S};   // partial == dw when S == 1
@@ -1700,16 +1708,13 @@ hipError_t splitk_reduce_launch(const float* part, float* out, long E, int S, hi
 }
 
 // Two micro-batches of one layer where the planned kernel takes two tensors
-// (the per-tap and resident-weight kernels), else one launch each; the same
-// values as two conv_forward_mfma calls either way.
+// (the per-tap kernel), else one launch each; the same values as two
+// conv_forward_mfma calls either way.
 static hipError_t conv_forward_mfma_pair(const void* x0, const void* x1, const void* w,
                                          const float* b, void* y0, void* y1, const ConvShape& s,
                                          int relu, float* part0, float* part1, size_t part_cap,
                                          hipStream_t st) {
   const FwdPlan pl = fwd_plan(s);
-  if (pl.cfg == 150)
-    return launch_1x1_res((const bf16_t*)x0, (const bf16_t*)x1, (const bf16_t*)w, b, (bf16_t*)y0,
-                          (bf16_t*)y1, s, relu, st);
   if (pl.cfg >= 100 && pl.cfg < 200) {
     // the per-tap kernel: both micro-batches' tiles in one grid
     const long P = s.pixels();
@@ -1730,13 +1735,14 @@ static hipError_t conv_forward_mfma_pair(const void* x0, const void* x1, const v
   return conv_forward_mfma(x1, w, b, y1, s, relu, part1, part_cap, st);
 }
 
-// n micro-batches of one layer: one launch of the nine-tap kernel where it
-// is planned, else pairs (and a single for odd n).
+// n micro-batches of one layer: one launch of the nine-tap or resident-
+// weight 1x1 kernel where it is planned, else pairs (and a single for odd n).
 hipError_t conv_forward_mfma_n(int n, const void* const* x, const void* w, const float* b,
                                void* const* y, const ConvShape& s, int relu, float* const* part,
                                size_t part_cap, hipStream_t st) {
   if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
   const FwdPlan pl = fwd_plan(s);
+  if (pl.cfg == 150) return launch_1x1_res(n, x, (const bf16_t*)w, b, y, s, relu, st);
   if (pl.cfg >= 400) {
     g_rows32_cfg = pl.cfg >= 401 ? pl.cfg - 401 : -1;
     const hipError_t e = conv_forward_rows32(n, x, w, b, y, s, relu, st);
@@ -1753,27 +1759,20 @@ hipError_t conv_forward_mfma_n(int n, const void* const* x, const void* w, const
   return hipSuccess;
 }
 
-// The weight gradients of n micro-batches, every sum left pending: one
-// launch of the row-blocked kernel where it applies, else pairs of the
-// per-tap kernel (and a single for odd n).
+// The weight gradients of n micro-batches in one launch, every sum left
+// pending: the row-blocked kernel where it applies, else the per-tap one.
 hipError_t conv_wgrad_mfma_n(int n, const void* const* x, const void* const* dz,
                              float* const* dw, float* const* part, const ConvShape& s,
                              hipStream_t st, ReduceJob* const* defer) {
   if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
   if (use_wgrad_rows(s)) return conv_wgrad_rows_launch_n(n, x, dz, dw, part, s, st, defer);
   const long E = (long)s.cout * s.taps * s.cin;
-  for (int k = 0; k < n; k += 2) {
-    const bool two = k + 1 < n;
-    WgradPlan pl;
-    float* p0 = part[k];
-    float* p1 = two ? part[k + 1] : nullptr;
-    hipError_t e = launch_wgrad_mfma(x[k], two ? x[k + 1] : nullptr, dz[k],
-                                     two ? dz[k + 1] : nullptr, dw[k], two ? dw[k + 1] : nullptr,
-                                     p0, p1, s, pl, st);
-    if (e != hipSuccess) return e;
-    *defer[k] = ReduceJob{p0, dw[k], E, pl.S};   // partial == dw when S == 1
-    if (two) *defer[k + 1] = ReduceJob{p1, dw[k + 1], E, pl.S};
-  }
+  WgradPlan pl;
+  float* pp[kMaxGroup];
+  for (int k = 0; k < n; ++k) pp[k] = part[k];
+  hipError_t e = launch_wgrad_mfma(n, x, dz, dw, pp, s, pl, st);
+  if (e != hipSuccess) return e;
+  for (int k = 0; k < n; ++k) *defer[k] = ReduceJob{pp[k], dw[k], E, pl.S};   // pp == dw when S == 1
   return hipSuccess;
 }
 

@@ -26,6 +26,14 @@ hipError_t conv_wgrad_mfma_n(int n, const void* const* x, const void* const* dz,
 
 namespace {
 
+// Element k (uniform, below 4) of a kernel-argument array, read at constant
+// indices so that the array stays in the argument segment instead of being
+// copied to private memory for a dynamic index.
+template <typename P>
+__device__ __forceinline__ P sel4(const P (&a)[4], int k) {
+  return k == 0 ? a[0] : k == 1 ? a[1] : k == 2 ? a[2] : a[3];
+}
+
 // ---------------------------------------------------------------- 16-byte packs
 
 template <typename T> struct Pk;
@@ -278,16 +286,17 @@ __global__ __launch_bounds__(256) void dw_dgrad_k(const T* __restrict__ dz, cons
 // FLIP applies the filter rotated by 180 degrees, which is the data
 // gradient (dx = dz correlated with the flipped filter); the sum runs over
 // the window in row-major order.
-// gridDim.z (1 or 2) micro-batches: blockIdx.z selects x0 / y0 or x1 / y1.
+// gridDim.z (1 .. kMaxGroup) micro-batches: blockIdx.z selects x[k] / y[k].
+struct DwIo {
+  const bf16_t* x[kMaxGroup];
+  bf16_t* y[kMaxGroup];
+};
 template <int RS, bool FLIP>
-__global__ __launch_bounds__(256) void dw3_rows_k(const bf16_t* __restrict__ x0,
-                                                  const bf16_t* __restrict__ x1,
-                                                  const bf16_t* __restrict__ w,
-                                                  const float* __restrict__ b,
-                                                  bf16_t* __restrict__ y0, bf16_t* __restrict__ y1,
-                                                  int H, int W, int C, int relu) {
-  const bf16_t* __restrict__ x = blockIdx.z ? x1 : x0;
-  bf16_t* __restrict__ y = blockIdx.z ? y1 : y0;
+__global__ __launch_bounds__(256) void dw3_rows_k(DwIo io, const bf16_t* __restrict__ w,
+                                                  const float* __restrict__ b, int H, int W, int C,
+                                                  int relu) {
+  const bf16_t* __restrict__ x = sel4(io.x, blockIdx.z);
+  bf16_t* __restrict__ y = sel4(io.y, blockIdx.z);
   const int CP = C >> 3;
   const int q = blockIdx.x * 256 + threadIdx.x;
   const int wc = q / CP, cp = q - (q / CP) * CP;
@@ -369,19 +378,18 @@ __global__ __launch_bounds__(256) void dw3_rows_k(const bf16_t* __restrict__ x0,
 // length keeps both the writes and the reads free of bank conflicts), and
 // writes part[blk][c * 9 + t], blk = strip block * chunks + chunk.  The partials are summed in block order
 // afterwards, so the result is deterministic.
-// gridDim.z (1 or 2) micro-batches: blockIdx.z selects (x0, dz0, part0) or
-// (x1, dz1, part1).
+// gridDim.z (1 .. kMaxGroup) micro-batches: blockIdx.z selects (x[k],
+// dz[k], part[k]).
+struct DwWgIo {
+  const bf16_t* x[kMaxGroup];
+  const bf16_t* dz[kMaxGroup];
+  float* part[kMaxGroup];
+};
 template <int RS>
-__global__ __launch_bounds__(256) void dw3_wgrad_rows_k(const bf16_t* __restrict__ x0,
-                                                        const bf16_t* __restrict__ x1,
-                                                        const bf16_t* __restrict__ dz0,
-                                                        const bf16_t* __restrict__ dz1,
-                                                        float* __restrict__ part0,
-                                                        float* __restrict__ part1, int H, int W,
-                                                        int C) {
-  const bf16_t* __restrict__ x = blockIdx.z ? x1 : x0;
-  const bf16_t* __restrict__ dz = blockIdx.z ? dz1 : dz0;
-  float* __restrict__ part = blockIdx.z ? part1 : part0;
+__global__ __launch_bounds__(256) void dw3_wgrad_rows_k(DwWgIo io, int H, int W, int C) {
+  const bf16_t* __restrict__ x = sel4(io.x, blockIdx.z);
+  const bf16_t* __restrict__ dz = sel4(io.dz, blockIdx.z);
+  float* __restrict__ part = sel4(io.part, blockIdx.z);
   constexpr int TH = 5;                      // taps per reduction pass
   constexpr int RW = TH * 8 + 1;             // floats per thread row
   __shared__ float red[256][RW];
@@ -541,13 +549,6 @@ struct RbGroup {   // pointer set k of each field is micro-batch k's
   T* dz[kMaxGroup];
   float* part[kMaxGroup];
 };
-// Element k (uniform, below 4) of a kernel-argument array, read at constant
-// indices so that the array stays in the argument segment instead of being
-// copied to private memory for a dynamic index.
-template <typename P>
-__device__ __forceinline__ P sel4(const P (&a)[4], int k) {
-  return k == 0 ? a[0] : k == 1 ? a[1] : k == 2 ? a[2] : a[3];
-}
 // The pointer set of group entry blockIdx.y.
 template <typename T>
 __device__ __forceinline__ RbPtrs<T> rb_pick(const RbGroup<T>& a) {
@@ -1172,66 +1173,81 @@ hipError_t conv_wgrad_n(int dt, int n, const void* const* x, const void* const* 
   return hipSuccess;
 }
 
-// The row-window depthwise kernels over one or two micro-batches (x1 null:
-// one); false where they do not apply.
-bool dw_pair_ok(int dt, int nb, int H, int W, int C, const void* a0, const void* a1,
-                const void* b0, const void* b1, const void* c) {
-  return dw3_rows_ok(dt, nb, H, W, C, a0, b0, c) && dw3_rows_ok(dt, nb, H, W, C, a1, b1, c);
+bool dw_rows_ok(int dt, int nb, int H, int W, int C, const void* a, const void* b,
+                const void* c) {
+  return dw3_rows_ok(dt, nb, H, W, C, a, b, c);
 }
 
-hipError_t dw_forward2(const void* x0, const void* x1, const void* w, const float* b, void* y0,
-                       void* y1, int nb, int H, int W, int C, int relu, hipStream_t st) {
+hipError_t dw_forward_n(int n, const void* const* x, const void* w, const float* b,
+                        void* const* y, int nb, int H, int W, int C, int relu, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
   const long P = (long)nb * H * W;
-  const int n = x1 ? 2 : 1;
   if (P == 0) return hipSuccess;
+  DwIo io;
+  for (int k = 0; k < kMaxGroup; ++k) {   // unused entries repeat the first
+    io.x[k] = (const bf16_t*)x[k < n ? k : 0];
+    io.y[k] = (bf16_t*)y[k < n ? k : 0];
+  }
   const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwRows)), n);
   ProfScope ps("dw3_rows_fwd", n * 18.0 * P * C, n * 4.0 * P * C, st);
-  TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, false>), g, dim3(256), 0, st, (const bf16_t*)x0,
-             (const bf16_t*)(x1 ? x1 : x0), (const bf16_t*)w, b, (bf16_t*)y0,
-             (bf16_t*)(x1 ? y1 : y0), H, W, C, relu);
+  TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, false>), g, dim3(256), 0, st, io, (const bf16_t*)w, b, H,
+             W, C, relu);
   return launch_status();
 }
 
-hipError_t dw_dgrad2(const void* dz0, const void* dz1, const void* w, void* dx0, void* dx1,
-                     int nb, int H, int W, int C, hipStream_t st) {
+hipError_t dw_dgrad_n(int n, const void* const* dz, const void* w, void* const* dx, int nb,
+                      int H, int W, int C, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
   const long P = (long)nb * H * W;
-  const int n = dz1 ? 2 : 1;
   if (P == 0) return hipSuccess;
+  DwIo io;
+  for (int k = 0; k < kMaxGroup; ++k) {
+    io.x[k] = (const bf16_t*)dz[k < n ? k : 0];
+    io.y[k] = (bf16_t*)dx[k < n ? k : 0];
+  }
   const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwRows)), n);
   ProfScope ps("dw3_rows_dgrad", n * 18.0 * P * C, n * 4.0 * P * C, st);
-  TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, true>), g, dim3(256), 0, st, (const bf16_t*)dz0,
-             (const bf16_t*)(dz1 ? dz1 : dz0), (const bf16_t*)w, (const float*)nullptr,
-             (bf16_t*)dx0, (bf16_t*)(dz1 ? dx1 : dx0), H, W, C, 0);
+  TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, true>), g, dim3(256), 0, st, io, (const bf16_t*)w,
+             (const float*)nullptr, H, W, C, 0);
   return launch_status();
 }
 
-hipError_t dw_wgrad2(const void* x0, const void* x1, const void* dz0, const void* dz1,
-                     float* dw0, float* dw1, float* part0, float* part1, int nb, int H, int W,
-                     int C, hipStream_t st) {
+hipError_t dw_wgrad_n(int n, const void* const* x, const void* const* dz, float* const* dw,
+                      float* const* part, int nb, int H, int W, int C, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
   const long P = (long)nb * H * W;
   const long E = (long)C * 9;
-  const int n = x1 ? 2 : 1;
   if (P == 0) return hipSuccess;
   const int S = dw3_wgrad_blocks(nb, H, W, C);
+  DwWgIo io;
+  for (int k = 0; k < kMaxGroup; ++k) {
+    io.x[k] = (const bf16_t*)x[k < n ? k : 0];
+    io.dz[k] = (const bf16_t*)dz[k < n ? k : 0];
+    io.part[k] = part[k < n ? k : 0];
+  }
   const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwWgradRows)), n);
   {
     ProfScope ps("dw3_wgrad_rows", n * 18.0 * P * C, n * (4.0 * P * C + 4.0 * S * E), st);
-    TGP_LAUNCH(ps, (dw3_wgrad_rows_k<kDwWgradRows>), g, dim3(256), 0, st, (const bf16_t*)x0,
-               (const bf16_t*)(x1 ? x1 : x0), (const bf16_t*)dz0,
-               (const bf16_t*)(x1 ? dz1 : dz0), part0, x1 ? part1 : part0, H, W, C);
+    TGP_LAUNCH(ps, (dw3_wgrad_rows_k<kDwWgradRows>), g, dim3(256), 0, st, io, H, W, C);
   }
   hipError_t e = launch_status();
-  if (e != hipSuccess) return e;
-  if (n == 1) return splitk_reduce_launch(part0, dw0, E, S, st);
-  const ReduceJob second{part1, dw1, E, S};   // both sums in one launch
-  return splitk_reduce_launch(part0, dw0, E, S, st, &second);
+  // the sums, two per reduction launch
+  for (int k = 0; k < n && e == hipSuccess; k += 2) {
+    if (k + 1 < n) {
+      const ReduceJob second{part[k + 1], dw[k + 1], E, S};
+      e = splitk_reduce_launch(part[k], dw[k], E, S, st, &second);
+    } else {
+      e = splitk_reduce_launch(part[k], dw[k], E, S, st);
+    }
+  }
+  return e;
 }
 
 hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void* y, int nb,
                       int H, int W, int C, int relu, hipStream_t st) {
   long P = (long)nb * H * W;
   if (dw3_rows_ok(dt, nb, H, W, C, x, w, y))
-    return dw_forward2(x, nullptr, w, b, y, nullptr, nb, H, W, C, relu, st);
+    return dw_forward_n(1, &x, w, b, &y, nb, H, W, C, relu, st);
   dim3 g(cdiv(P * C, 256));
   ProfScope ps("dw_forward", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
   if (dt == 0)
@@ -1247,7 +1263,7 @@ hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int
                     int C, hipStream_t st) {
   long P = (long)nb * H * W;
   if (dw3_rows_ok(dt, nb, H, W, C, dz, w, dx))
-    return dw_dgrad2(dz, nullptr, w, dx, nullptr, nb, H, W, C, st);
+    return dw_dgrad_n(1, &dz, w, &dx, nb, H, W, C, st);
   dim3 g(cdiv(P * C, 256));
   ProfScope ps("dw_dgrad", 18.0 * P * C, (dt == 0 ? 4.0 : 8.0) * P * C, st);
   if (dt == 0)
@@ -1273,7 +1289,7 @@ hipError_t dw_wgrad(int dt, const void* x, const void* dz, float* dw, float* par
   long P = (long)nb * H * W;
   long E = (long)C * 9;
   if (dw3_rows_ok(dt, nb, H, W, C, x, dz, partial) && P > 0)
-    return dw_wgrad2(x, nullptr, dz, nullptr, dw, nullptr, partial, nullptr, nb, H, W, C, st);
+    return dw_wgrad_n(1, &x, &dz, &dw, &partial, nb, H, W, C, st);
   long pps = direct_wgrad_pps(P);
   int S = direct_wgrad_splits(P);
   dim3 g(cdiv(E, 256), S);

@@ -113,18 +113,18 @@ hipError_t dw_forward(int dt, const void* x, const void* w, const float* b, void
 hipError_t dw_dgrad(int dt, const void* dz, const void* w, void* dx, int nb, int H, int W,
                     int C, hipStream_t st);
 size_t dw_wgrad_partial_floats(int nb, int H, int W, int C);
-// Two micro-batches per launch for the bf16 row-window depthwise kernels,
-// where dw_pair_ok holds for both micro-batches' tensors (a*, b*) and the
-// weights c.
-bool dw_pair_ok(int dt, int nb, int H, int W, int C, const void* a0, const void* a1,
-                const void* b0, const void* b1, const void* c);
-hipError_t dw_forward2(const void* x0, const void* x1, const void* w, const float* b, void* y0,
-                       void* y1, int nb, int H, int W, int C, int relu, hipStream_t st);
-hipError_t dw_dgrad2(const void* dz0, const void* dz1, const void* w, void* dx0, void* dx1,
-                     int nb, int H, int W, int C, hipStream_t st);
-hipError_t dw_wgrad2(const void* x0, const void* x1, const void* dz0, const void* dz1,
-                     float* dw0, float* dw1, float* part0, float* part1, int nb, int H, int W,
-                     int C, hipStream_t st);
+// n (1 .. kMaxGroup) micro-batches per launch for the bf16 row-window
+// depthwise kernels, where dw_rows_ok holds for each micro-batch's tensors
+// (a, b) and the weights or partial buffer c.  dw_wgrad_n reduces each sum
+// at once (two per reduction launch).
+bool dw_rows_ok(int dt, int nb, int H, int W, int C, const void* a, const void* b,
+                const void* c);
+hipError_t dw_forward_n(int n, const void* const* x, const void* w, const float* b,
+                        void* const* y, int nb, int H, int W, int C, int relu, hipStream_t st);
+hipError_t dw_dgrad_n(int n, const void* const* dz, const void* w, void* const* dx, int nb,
+                      int H, int W, int C, hipStream_t st);
+hipError_t dw_wgrad_n(int n, const void* const* x, const void* const* dz, float* const* dw,
+                      float* const* part, int nb, int H, int W, int C, hipStream_t st);
 hipError_t dw_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial, int nb,
                     int H, int W, int C, hipStream_t st);
 

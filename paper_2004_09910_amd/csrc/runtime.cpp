@@ -302,19 +302,19 @@ tgp_status run_forward_g(tgp_net* N, int j, int cnt, const int* iv, const int* p
       HIPCHK(tgpk::maxpool_forward_n(N->dt, cnt, src, pro_ptr, N->b, Lr.inH, Lr.inW, Lr.inC, st),
              "maxpool_forward");
     if (d.kind == TGP_DWCONV3X3) {
-      // the row-window depthwise kernels take two micro-batches per launch
-      for (int k = 0; k < cnt; ++k) {
-        if (k + 1 < cnt && tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[k],
-                                            cin_ptr[k + 1], out[k], out[k + 1], Lr.w)) {
-          HIPCHK(tgpk::dw_forward2(cin_ptr[k], cin_ptr[k + 1], Lr.w, d.bias ? Lr.b : nullptr,
-                                   out[k], out[k + 1], N->b, Lr.H, Lr.W, d.cout, d.relu, st),
-                 "dw_forward");
-          ++k;
-        } else {
+      // the row-window depthwise kernel takes the whole group in one launch
+      bool rows = cnt > 1;
+      for (int k = 0; k < cnt; ++k)
+        rows = rows && tgpk::dw_rows_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[k], out[k], Lr.w);
+      if (rows) {
+        HIPCHK(tgpk::dw_forward_n(cnt, cin_ptr, Lr.w, d.bias ? Lr.b : nullptr, out, N->b, Lr.H,
+                                  Lr.W, d.cout, d.relu, st),
+               "dw_forward");
+      } else {
+        for (int k = 0; k < cnt; ++k)
           HIPCHK(tgpk::dw_forward(N->dt, cin_ptr[k], Lr.w, d.bias ? Lr.b : nullptr, out[k], N->b,
                                   Lr.H, Lr.W, d.cout, d.relu, st),
                  "dw_forward");
-        }
       }
     } else {
       tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
@@ -570,6 +570,10 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     }
     // weight gradient
     tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
+    bool dw_wrows = d.kind == TGP_DWCONV3X3 && cnt > 1;   // one depthwise launch for the group
+    for (int k = 0; k < cnt; ++k)
+      dw_wrows = dw_wrows && tgpk::dw_rows_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[k], dzk[k],
+                                              M[k].part);
     if (d.kind != TGP_DWCONV3X3 && cnt > 1 && Lr.defer_w) {
       float* gws[MG];
       float* gps[MG];
@@ -580,22 +584,20 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
         dfs[k] = &(*pjs[k])[0];
       }
       HIPCHK(tgpk::conv_wgrad_n(N->dt, cnt, cin_ptr, dzk, gws, gps, s, st, dfs), "conv_wgrad_n");
+    } else if (dw_wrows) {
+      float* gws[MG];
+      float* pts[MG];
+      for (int k = 0; k < cnt; ++k) {
+        gws[k] = (float*)G_(N, M[k].i, Lr.o_gw);
+        pts[k] = M[k].part;
+      }
+      HIPCHK(tgpk::dw_wgrad_n(cnt, cin_ptr, dzk, gws, pts, N->b, Lr.H, Lr.W, d.cout, st),
+             "dw_wgrad");
     } else {
       for (int k = 0; k < cnt; ++k) {
         BwdMb& B = M[k];
         float* gw = (float*)G_(N, B.i, Lr.o_gw);
-        if (d.kind == TGP_DWCONV3X3 && k + 1 < cnt &&
-            tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[k], cin_ptr[k + 1], dzk[k],
-                             dzk[k + 1], M[k].part) &&
-            tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[k], cin_ptr[k + 1], dzk[k],
-                             dzk[k + 1], M[k + 1].part)) {
-          // the row-window depthwise kernels take two micro-batches per launch
-          HIPCHK(tgpk::dw_wgrad2(cin_ptr[k], cin_ptr[k + 1], dzk[k], dzk[k + 1], gw,
-                                 (float*)G_(N, M[k + 1].i, Lr.o_gw), M[k].part, M[k + 1].part,
-                                 N->b, Lr.H, Lr.W, d.cout, st),
-                 "dw_wgrad");
-          ++k;
-        } else if (d.kind == TGP_DWCONV3X3) {
+        if (d.kind == TGP_DWCONV3X3) {
           HIPCHK(tgpk::dw_wgrad(N->dt, cin_ptr[k], dzk[k], gw, B.part, N->b, Lr.H, Lr.W, d.cout,
                                 st),
                  "dw_wgrad");
@@ -615,19 +617,16 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
       dest_prev[k] = (l == lo) ? dx_in[k] : M[k].gnext;
       dgrad_out[k] = d.prologue == TGP_PRO_NONE ? dest_prev[k] : M[k].dinp;
     }
-    if (d.kind == TGP_DWCONV3X3) {
-      for (int k = 0; k < cnt; ++k) {
-        if (k + 1 < cnt && tgpk::dw_pair_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, dzk[k], dzk[k + 1],
-                                            dgrad_out[k], dgrad_out[k + 1], Lr.w)) {
-          HIPCHK(tgpk::dw_dgrad2(dzk[k], dzk[k + 1], Lr.w, dgrad_out[k], dgrad_out[k + 1], N->b,
-                                 Lr.H, Lr.W, d.cout, st),
-                 "dw_dgrad");
-          ++k;
-        } else {
-          HIPCHK(tgpk::dw_dgrad(N->dt, dzk[k], Lr.w, dgrad_out[k], N->b, Lr.H, Lr.W, d.cout, st),
-                 "dw_dgrad");
-        }
-      }
+    bool dw_drows = d.kind == TGP_DWCONV3X3 && cnt > 1;
+    for (int k = 0; k < cnt; ++k)
+      dw_drows = dw_drows && tgpk::dw_rows_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, dzk[k],
+                                              dgrad_out[k], Lr.w);
+    if (dw_drows) {
+      HIPCHK(tgpk::dw_dgrad_n(cnt, dzk, Lr.w, dgrad_out, N->b, Lr.H, Lr.W, d.cout, st), "dw_dgrad");
+    } else if (d.kind == TGP_DWCONV3X3) {
+      for (int k = 0; k < cnt; ++k)
+        HIPCHK(tgpk::dw_dgrad(N->dt, dzk[k], Lr.w, dgrad_out[k], N->b, Lr.H, Lr.W, d.cout, st),
+               "dw_dgrad");
     } else if (cnt > 1) {
       // the lanes' transformed weights are equal copies; the first's serves all
       float* fps[MG];
