@@ -85,7 +85,11 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
   constexpr int SB = (AR + BR) * 128;           // stage bytes
   constexpr int NW = 4 * KS;                    // waves
   constexpr int AC = AR / 8, BC = BR / 8;       // DMA chunks (8 rows, 1 KiB) per region
-  constexpr int LA = (AC + NW - 1) / NW, LB = (BC + NW - 1) / NW;   // per wave, at most
+  // With KS = 2 only the four waves of phase 1 issue the DMA (each twice
+  // its share): an issuing wave stalls while the memory pipeline is full,
+  // and meanwhile its SIMD's phase-0 wave keeps the MFMAs busy.
+  constexpr int ND = KS == 2 ? 4 : NW;          // waves that issue the DMA
+  constexpr int LA = (AC + ND - 1) / ND, LB = (BC + ND - 1) / ND;   // per issuing wave, at most
   constexpr int KT = RPS * W / 16;               // k steps per stage
   static_assert(RPS * W % 16 == 0 && W % 8 == 0, "k steps of 16 pixels, halves within a row");
   static_assert(KT % KS == 0, "k steps shared evenly");
@@ -113,14 +117,16 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
 
   const int zbytes = nb * H * W * Cout * 2, xbytes = nb * H * W * Cin * 2;
 
-  // DMA lane constants: instruction u of this wave fills chunk c = NW u +
-  // wave of the A (dZ) or B (padded X) region, rows 8 c + lane / 8, physical
+  // DMA lane constants: instruction u of issuing wave d fills chunk c = ND u
+  // + d of the A (dZ) or B (padded X) region, rows 8 c + lane / 8, physical
   // chunk lane % 8, which holds logical chunk (lane % 8) ^ (2 (row & 3)).
   // Chunks past a region's end are not issued (wave-uniform).
+  const int dwi = KS == 2 ? qw : wave;          // index among the issuing waves
+  const bool issuer = KS == 1 || kh == 1;
   int aoff[LA], arow[LA], boff[LB], brow[LB];
 #pragma unroll
   for (int u = 0; u < LA; ++u) {
-    const int row = (NW * u + wave) * 8 + (lane >> 3);
+    const int row = (ND * u + dwi) * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ (2 * (row & 3));
     const int rr = row / W, w = row - rr * W;
     const bool ok = row < RPS * W;
@@ -129,18 +135,21 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
   }
 #pragma unroll
   for (int u = 0; u < LB; ++u) {
-    const int row = (NW * u + wave) * 8 + (lane >> 3);
+    const int row = (ND * u + dwi) * 8 + (lane >> 3);
     const int lc = (lane & 7) ^ (2 * (row & 3));
     const int rr = row / BW, q = row - rr * BW;
     const bool ok = rr < RPS && q >= 1 && q <= W;
     boff[u] = ok ? ((rr * W + q - 1) * Cin + 8 * lc) * 2 : WG_OOB;
     brow[u] = ok ? rr : -1;
   }
-  // DMA instructions this wave issues per stage (the waits count them)
-  const int na = (AC - wave + NW - 1) / NW, nbq = (BC - wave + NW - 1) / NW;
+  // DMA instructions an issuing wave issues per stage (the waits count
+  // them); the other waves find the stage complete after the ring barrier,
+  // which the issuers reach only once their loads have landed
+  const int na = (AC - dwi + ND - 1) / ND, nbq = (BC - dwi + ND - 1) / ND;
   const int mine = na + nbq;
   auto wait_ring = [&](int ahead) __attribute__((always_inline)) {
-    if constexpr (AC % NW == 0 && BC % NW == 0) {
+    if (!issuer) return;
+    if constexpr (AC % ND == 0 && BC % ND == 0) {
       wait_stages<NS, LA + LB>(ahead);
     } else {
       if (mine == LA + LB) wait_stages<NS, LA + LB>(ahead);
@@ -215,16 +224,16 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
     const int xsoff = (((n * H + hb) * W) * Cin + i_ci0) * 2;
 #pragma unroll
     for (int u = 0; u < LA; ++u) {
-      const int c = NW * u + wave;
-      if (AC % NW != 0 && c >= AC) continue;                 // wave-uniform
+      const int c = ND * u + dwi;
+      if (!issuer || (AC % ND != 0 && c >= AC)) continue;   // wave-uniform
       auto* dst = TGP_LDS(smem + slot * SB + c * 1024);
       const bool ok = arow[u] >= 0 && h + arow[u] < H;
       dma16(rzg, dst, ok ? aoff[u] + zsoff : WG_OOB, 0);
     }
 #pragma unroll
     for (int u = 0; u < LB; ++u) {
-      const int c = NW * u + wave;
-      if (BC % NW != 0 && c >= BC) continue;                 // wave-uniform
+      const int c = ND * u + dwi;
+      if (!issuer || (BC % ND != 0 && c >= BC)) continue;   // wave-uniform
       auto* dst = TGP_LDS(smem + slot * SB + AR * 128 + c * 1024);
       const bool ok = brow[u] >= 0 && (unsigned)(hb + brow[u]) < (unsigned)H && h + brow[u] < H;
       // the row offset can be negative for filter row 0 (rows above are out
@@ -423,9 +432,11 @@ static hipError_t launch_wgrad_rows(const WgIo& io, int ng, const ConvShape& s, 
 template <int W, int RPS, int NS>
 static hipError_t launch_wgrad_rows_ks(const WgIo& io, int ng, const ConvShape& s,
                                        const WgPlan& p, hipStream_t st) {
-  // two waves per SIMD pay off where a stage has many k steps (widths 192
-  // and 48 measured 1-3 % faster; 96 about even, 24 slower)
-  const int ks = g_wgrad_ks ? g_wgrad_ks : ((W == 192 || W == 48) ? 2 : 1);
+  // two waves per SIMD, the phase-1 waves issuing the DMA, pay off where a
+  // stage has many k steps (on the U-Net stage: 192 and 48 7-11% faster
+  // than with every wave issuing, 96 7% faster than one wave per SIMD; 24
+  // 14% slower)
+  const int ks = g_wgrad_ks ? g_wgrad_ks : ((W == 192 || W == 96 || W == 48) ? 2 : 1);
   return ks == 2 ? launch_wgrad_rows<W, RPS, NS, 2>(io, ng, s, p, st)
                  : launch_wgrad_rows<W, RPS, NS, 1>(io, ng, s, p, st);
 }
