@@ -1213,7 +1213,8 @@ hipError_t dw_dgrad_n(int n, const void* const* dz, const void* w, void* const* 
 }
 
 hipError_t dw_wgrad_n(int n, const void* const* x, const void* const* dz, float* const* dw,
-                      float* const* part, int nb, int H, int W, int C, hipStream_t st) {
+                      float* const* part, int nb, int H, int W, int C, hipStream_t st,
+                      ReduceJob* const* defer) {
   if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
   const long P = (long)nb * H * W;
   const long E = (long)C * 9;
@@ -1231,6 +1232,10 @@ hipError_t dw_wgrad_n(int n, const void* const* x, const void* const* dz, float*
     TGP_LAUNCH(ps, (dw3_wgrad_rows_k<kDwWgradRows>), g, dim3(256), 0, st, io, H, W, C);
   }
   hipError_t e = launch_status();
+  if (defer) {   // left to the caller's accumulation, in the same order
+    for (int k = 0; k < n; ++k) *defer[k] = ReduceJob{part[k], dw[k], E, S};
+    return e;
+  }
   // the sums, two per reduction launch
   for (int k = 0; k < n && e == hipSuccess; k += 2) {
     if (k + 1 < n) {

@@ -116,7 +116,8 @@ size_t dw_wgrad_partial_floats(int nb, int H, int W, int C);
 // n (1 .. kMaxGroup) micro-batches per launch for the bf16 row-window
 // depthwise kernels, where dw_rows_ok holds for each micro-batch's tensors
 // (a, b) and the weights or partial buffer c.  dw_wgrad_n reduces each sum
-// at once (two per reduction launch).
+// at once (two per reduction launch), or with `defer` leaves sum k pending
+// in *defer[k].
 bool dw_rows_ok(int dt, int nb, int H, int W, int C, const void* a, const void* b,
                 const void* c);
 hipError_t dw_forward_n(int n, const void* const* x, const void* w, const float* b,
@@ -124,7 +125,8 @@ hipError_t dw_forward_n(int n, const void* const* x, const void* w, const float*
 hipError_t dw_dgrad_n(int n, const void* const* dz, const void* w, void* const* dx, int nb,
                       int H, int W, int C, hipStream_t st);
 hipError_t dw_wgrad_n(int n, const void* const* x, const void* const* dz, float* const* dw,
-                      float* const* part, int nb, int H, int W, int C, hipStream_t st);
+                      float* const* part, int nb, int H, int W, int C, hipStream_t st,
+                      ReduceJob* const* defer = nullptr);
 hipError_t dw_wgrad(int dt, const void* x, const void* dz, float* dw, float* partial, int nb,
                     int H, int W, int C, hipStream_t st);
 
@@ -168,8 +170,10 @@ hipError_t grad_accumulate(float* acc, const float* g, long n, int overwrite, hi
 
 // acc_k = r_k (overwrite) or acc_k + r_k, r_k = sum_{s < S_k} g_k[s n_k ..]
 // (the pending split-K sums of one micro-batch's gradients), for up to
-// kMaxAcc tensors in one launch (passed by value).  Each r_k is summed in
-// the order splitk_reduce_launch uses for (n_k, S_k).
+// kMaxAcc tensors in one launch (passed by value).  Each r_k is summed in a
+// fixed order that depends on (n_k, S_k) only; it is not always the order
+// of splitk_reduce_launch, so a layer's sums are either always left to the
+// accumulation or always reduced at once.
 constexpr int kMaxAcc = 48;
 struct AccBatch {
   int count;

@@ -570,10 +570,16 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     }
     // weight gradient
     tgpk::ConvShape s{N->b, Lr.H, Lr.W, d.cin, d.cout, Lr.taps};
-    bool dw_wrows = d.kind == TGP_DWCONV3X3 && cnt > 1;   // one depthwise launch for the group
-    for (int k = 0; k < cnt; ++k)
+    // one depthwise launch for the group, its sums left to the accumulation
+    // when the layer keeps its partials in the slots
+    bool dw_wrows = d.kind == TGP_DWCONV3X3;
+    float* dw_parts[MG];
+    for (int k = 0; k < cnt; ++k) {
+      dw_parts[k] = d.kind == TGP_DWCONV3X3 && Lr.defer_w ? (float*)G_(N, M[k].i, Lr.o_gpart)
+                                                          : M[k].part;
       dw_wrows = dw_wrows && tgpk::dw_rows_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, cin_ptr[k], dzk[k],
-                                              M[k].part);
+                                              dw_parts[k]);
+    }
     if (d.kind != TGP_DWCONV3X3 && cnt > 1 && Lr.defer_w) {
       float* gws[MG];
       float* gps[MG];
@@ -584,14 +590,15 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
         dfs[k] = &(*pjs[k])[0];
       }
       HIPCHK(tgpk::conv_wgrad_n(N->dt, cnt, cin_ptr, dzk, gws, gps, s, st, dfs), "conv_wgrad_n");
-    } else if (dw_wrows) {
+    } else if (dw_wrows && (cnt > 1 || Lr.defer_w)) {
       float* gws[MG];
-      float* pts[MG];
+      tgpk::ReduceJob* dfs[MG];
       for (int k = 0; k < cnt; ++k) {
         gws[k] = (float*)G_(N, M[k].i, Lr.o_gw);
-        pts[k] = M[k].part;
+        dfs[k] = &(*pjs[k])[0];
       }
-      HIPCHK(tgpk::dw_wgrad_n(cnt, cin_ptr, dzk, gws, pts, N->b, Lr.H, Lr.W, d.cout, st),
+      HIPCHK(tgpk::dw_wgrad_n(cnt, cin_ptr, dzk, gws, dw_parts, N->b, Lr.H, Lr.W, d.cout, st,
+                              Lr.defer_w ? dfs : nullptr),
              "dw_wgrad");
     } else {
       for (int k = 0; k < cnt; ++k) {
@@ -1098,7 +1105,13 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
     Lr.defer_w = false;
     Lr.o_gpart = 0;
     if (Lr.d.kind == TGP_DWCONV3X3) {
-      max_part = std::max(max_part, tgpk::dw_wgrad_partial_floats(N->b, Lr.H, Lr.W, Lr.d.cout));
+      // the row-window kernel's partials stay in the slot for the
+      // accumulation (its sum order differs from the immediate reduction's,
+      // so the choice is made here, for every call of the plan)
+      const size_t pf = tgpk::dw_wgrad_partial_floats(N->b, Lr.H, Lr.W, Lr.d.cout);
+      max_part = std::max(max_part, pf);
+      Lr.defer_w = N->dt == TGP_BF16 && pf * 4 <= kDeferBytes;
+      if (Lr.defer_w) Lr.o_gpart = takeG(std::max<size_t>(pf, 1) * 4);
     } else {
       const size_t pf = tgpk::conv_wgrad_partial_floats(N->dt, s);
       Lr.defer_w = pf * 4 <= kDeferBytes;
