@@ -109,6 +109,42 @@ def test_pair_then_single_calls_in_one_step():
     assert torch.equal(got["dx"], ref["dx"])
 
 
+def test_group_then_pair_then_single_calls_in_one_step():
+    """Forwards as one group of four, then a backward group of two (4, 3)
+    and single backwards of 2 and 1, on four lanes and one stream: each
+    later call on a lane whose transformed weights the group did not refresh
+    must refresh them first.  Bits equal one micro-batch per launch."""
+    import paper_2004_09910_amd as tgp
+    from paper_2004_09910_amd.harness import Session
+
+    class Mixed(Session):
+        def stage_step(self, j, x, y, dy, dx, stream=0, serial=False):
+            def sl(t, i):
+                return t.data_ptr() + (i - 1) * (t.numel() // self.m) * t.element_size()
+            tgp.stage_forward_n(self.h, j, 1, [self.checkpointed(i) for i in range(1, 5)],
+                                [sl(x, i) for i in range(1, 5)], [sl(y, i) for i in range(1, 5)],
+                                stream)
+            tgp.stage_backward_recompute_n(self.h, j, 4, [sl(dy, 4), sl(dy, 3)],
+                                           [sl(dx, 4), sl(dx, 3)], stream)
+            tgp.grad_accumulate(self.h, j, 4, True, stream)
+            tgp.grad_accumulate(self.h, j, 3, False, stream)
+            for i in (2, 1):
+                tgp.stage_backward_recompute(self.h, j, i, sl(dy, i), sl(dx, i), stream)
+                tgp.grad_accumulate(self.h, j, i, False, stream)
+
+    net = specs.unet(5, 64, 64, 48, "unet5-c64-48")
+    bal = (7, 5, 3, 4)
+    say("mixed group: reference, one per launch")
+    ref = gpu_stage(net, BF16, 8, 4, CKPT_ALWAYS, bal, 1)
+    say("mixed group: group of four, pair, singles")
+    sess = Mixed(net, BF16, n=len(bal), balance=bal, bind_layers=range(0, 7))
+    sess.plan(8, 4, CKPT_ALWAYS, 4)
+    got = gpu_stage(net, BF16, 8, 4, CKPT_ALWAYS, bal, 1, sess=sess)
+    same_bits(ref, got)
+    assert torch.equal(got["y"], ref["y"])
+    assert torch.equal(got["dx"], ref["dx"])
+
+
 def test_micro_batch_groups_bench_stage():
     """The group path on the benchmark's own stage (U-Net level-0 layers at
     192 x 192, micro-batch 4), m = 4, in groups of two and four against one
