@@ -145,6 +145,46 @@ def test_group_then_pair_then_single_calls_in_one_step():
     assert torch.equal(got["dx"], ref["dx"])
 
 
+def test_groups_of_three_in_one_step():
+    """A forward group of three (1, 2, 3) and a single forward of 4, then a
+    backward group of three (4, 3, 2) and a single backward of 1: every
+    group kernel runs with an unused fourth pointer set, the per-tap and
+    depthwise paths as a pair and a single.  Bits equal one micro-batch per
+    launch, on the reduced U-Net stage and on the cells."""
+    import paper_2004_09910_amd as tgp
+    from paper_2004_09910_amd.harness import Session
+
+    class Threes(Session):
+        def stage_step(self, j, x, y, dy, dx, stream=0, serial=False):
+            def sl(t, i):
+                return t.data_ptr() + (i - 1) * (t.numel() // self.m) * t.element_size()
+            tgp.stage_forward_n(self.h, j, 1, [self.checkpointed(i) for i in (1, 2, 3)],
+                                [sl(x, i) for i in (1, 2, 3)], [sl(y, i) for i in (1, 2, 3)],
+                                stream)
+            tgp.stage_forward(self.h, j, 4, self.checkpointed(4), sl(x, 4), sl(y, 4), stream)
+            tgp.stage_backward_recompute_n(self.h, j, 4, [sl(dy, i) for i in (4, 3, 2)],
+                                           [None if dx is None else sl(dx, i) for i in (4, 3, 2)],
+                                           stream)
+            for i in (4, 3, 2):
+                tgp.grad_accumulate(self.h, j, i, i == 4, stream)
+            tgp.stage_backward_recompute(self.h, j, 1, sl(dy, 1), None if dx is None else sl(dx, 1),
+                                         stream)
+            tgp.grad_accumulate(self.h, j, 1, False, stream)
+
+    cases = [(specs.unet(5, 64, 64, 48, "unet5-c64-48"), (7, 5, 3, 4), CKPT_EXCEPT_LAST, 7),
+             (specs.amoeba_cells(4, 256, 14, "cells4-c256"), (8,), CKPT_EXCEPT_LAST, 8)]
+    for net, bal, mode, nl in cases:
+        say(f"threes {net.name}: reference")
+        ref = gpu_stage(net, BF16, 8, 4, mode, bal, 1)
+        say(f"threes {net.name}: groups of three")
+        sess = Threes(net, BF16, n=len(bal), balance=bal, bind_layers=range(0, nl))
+        sess.plan(8, 4, mode, 4)
+        got = gpu_stage(net, BF16, 8, 4, mode, bal, 1, sess=sess)
+        same_bits(ref, got)
+        assert torch.equal(got["y"], ref["y"])
+        assert torch.equal(got["dx"], ref["dx"])
+
+
 def test_micro_batch_groups_bench_stage():
     """The group path on the benchmark's own stage (U-Net level-0 layers at
     192 x 192, micro-batch 4), m = 4, in groups of two and four against one
