@@ -858,7 +858,7 @@ def main():
     ap.add_argument("--lanes", type=int, default=None,
                     help="concurrency lanes: micro-batch i runs on stream (i - 1) %% lanes "
                          "(default: the group size, at least 2)")
-    ap.add_argument("--group", type=int, default=4, choices=[1, 2, 4],
+    ap.add_argument("--group", type=int, default=8, choices=[1, 2, 4, 8],
                     help="micro-batches per stage call and kernel launch (halved until it "
                          "divides the lanes and m)")
     ap.add_argument("--one-stream", dest="one_stream", action="store_true", default=None,

@@ -28,3 +28,14 @@ template <> struct Elt<bf16_t> {
 };
 
 __host__ __device__ __forceinline__ int cdiv(long a, long b) { return (int)((a + b - 1) / b); }
+
+// Element k (wave-uniform, 0 <= k < N) of a kernel-argument array, read at
+// constant indices so that the array stays in the argument segment rather
+// than being copied to private memory for a dynamic index.
+template <typename T, int N>
+__device__ __forceinline__ T pickg(const T (&a)[N], int k) {
+  T r = a[0];
+#pragma unroll
+  for (int i = 1; i < N; ++i) r = k == i ? a[i] : r;
+  return r;
+}

@@ -656,7 +656,7 @@ __global__ __launch_bounds__(512) void conv1x1_res(Mb1x1 io, int ng,
   auto issue = [&](int idx) __attribute__((always_inline)) {
     const int tt = lb + (idx / nks) * G, ks = idx - (idx / nks) * nks;
     const int gi = tt / T1;                                     // micro-batch (uniform)
-    const bf16_t* X = pick4(io.x, gi);
+    const bf16_t* X = pickg(io.x, gi);
     const int p = min((tt - gi * T1) * BM + xr, P - 1);         // rows past P: any pixel
     __builtin_amdgcn_global_load_lds((const void*)(X + (long)p * Cin + ks * 64 + xc * 8),
                                      TGP_LDS(&ring[(idx % NS) * BM * 8 + wave * 64]), 16, 0, 0);
@@ -675,7 +675,7 @@ __global__ __launch_bounds__(512) void conv1x1_res(Mb1x1 io, int ng,
   for (int it = 0; it < n_mine; ++it) {
     const int tt = lb + it * G;
     const int gi = tt / T1;
-    bf16_t* __restrict__ Y = pick4(io.y, gi);
+    bf16_t* __restrict__ Y = pickg(io.y, gi);
     const int p0 = (tt - gi * T1) * BM;
     f32x16_t acc[2] = {f32x16_t{}, f32x16_t{}};
     for (int ks = 0; ks < nks; ++ks, ++idx) {
@@ -1026,9 +1026,9 @@ __global__ __launch_bounds__(256) void conv_wgrad_mfma(MbWg io, int ng, int P, i
   const int lb0 = xcd_remap(blockIdx.x, gridDim.x);
   const int gi = lb0 / per;                                     // micro-batch (uniform)
   const int lb = lb0 - gi * per;
-  const bf16_t* __restrict__ X = pick4(io.x, gi);
-  const bf16_t* __restrict__ dZ = pick4(io.dz, gi);
-  float* __restrict__ part = pick4(io.part, gi);
+  const bf16_t* __restrict__ X = pickg(io.x, gi);
+  const bf16_t* __restrict__ dZ = pickg(io.dz, gi);
+  float* __restrict__ part = pickg(io.part, gi);
   const int split = lb / T;
   const int t = lb - split * T;
   const int tx = t % (TAPS * ncb);

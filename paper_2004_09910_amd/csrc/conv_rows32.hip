@@ -179,7 +179,7 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
   // stalls overlap the MFMAs already queued
   int i_it = 0, i_ks = 0, i_gi = 0, i_n = 0, i_h0 = 0, i_co0 = 0;
   if (total > 0) coords(0, i_gi, i_n, i_h0, i_co0);
-  u32x4 rxg = make_rsrc(pick4(io.x, i_gi), xbytes);            // the issuing item's input
+  u32x4 rxg = make_rsrc(pickg(io.x, i_gi), xbytes);            // the issuing item's input
   auto issue_part = [&](int slot, int u0, int u1) __attribute__((always_inline)) {
     const int c0 = i_ks * 16;
     const int soff_a = (i_co0 * 9 * Cin + c0) * 2;
@@ -205,7 +205,7 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
       i_ks = 0;
       if (++i_it < n_items) {
         coords(i_it, i_gi, i_n, i_h0, i_co0);
-        rxg = make_rsrc(pick4(io.x, i_gi), xbytes);
+        rxg = make_rsrc(pickg(io.x, i_gi), xbytes);
       }
     }
   };
@@ -312,7 +312,7 @@ __global__ __launch_bounds__(CH == 2 ? 256 : 512) void conv3x3_rows32(
     constexpr int NCK = 4 * CH;                                 // 16-byte chunks per pixel
     unsigned char* ep = ring + ((idx - 1) % NS) * SB + wave * 32 * ROWB;
     static_assert(NW * 32 * ROWB <= SB, "epilogue staging fits a slot");
-    bf16_t* const Yg = pick4(io.y, gi);
+    bf16_t* const Yg = pickg(io.y, gi);
     const long pix0 = (long)(n * H + h0) * W;
     const int pw = lane & 31, hw = lane >> 5;
 #pragma unroll

@@ -26,13 +26,6 @@ hipError_t conv_wgrad_mfma_n(int n, const void* const* x, const void* const* dz,
 
 namespace {
 
-// Element k (uniform, below 4) of a kernel-argument array, read at constant
-// indices so that the array stays in the argument segment instead of being
-// copied to private memory for a dynamic index.
-template <typename P>
-__device__ __forceinline__ P sel4(const P (&a)[4], int k) {
-  return k == 0 ? a[0] : k == 1 ? a[1] : k == 2 ? a[2] : a[3];
-}
 
 // ---------------------------------------------------------------- 16-byte packs
 
@@ -295,8 +288,8 @@ template <int RS, bool FLIP>
 __global__ __launch_bounds__(256) void dw3_rows_k(DwIo io, const bf16_t* __restrict__ w,
                                                   const float* __restrict__ b, int H, int W, int C,
                                                   int relu) {
-  const bf16_t* __restrict__ x = sel4(io.x, blockIdx.z);
-  bf16_t* __restrict__ y = sel4(io.y, blockIdx.z);
+  const bf16_t* __restrict__ x = pickg(io.x, blockIdx.z);
+  bf16_t* __restrict__ y = pickg(io.y, blockIdx.z);
   const int CP = C >> 3;
   const int q = blockIdx.x * 256 + threadIdx.x;
   const int wc = q / CP, cp = q - (q / CP) * CP;
@@ -387,9 +380,9 @@ struct DwWgIo {
 };
 template <int RS>
 __global__ __launch_bounds__(256) void dw3_wgrad_rows_k(DwWgIo io, int H, int W, int C) {
-  const bf16_t* __restrict__ x = sel4(io.x, blockIdx.z);
-  const bf16_t* __restrict__ dz = sel4(io.dz, blockIdx.z);
-  float* __restrict__ part = sel4(io.part, blockIdx.z);
+  const bf16_t* __restrict__ x = pickg(io.x, blockIdx.z);
+  const bf16_t* __restrict__ dz = pickg(io.dz, blockIdx.z);
+  float* __restrict__ part = pickg(io.part, blockIdx.z);
   constexpr int TH = 5;                      // taps per reduction pass
   constexpr int RW = TH * 8 + 1;             // floats per thread row
   __shared__ float red[256][RW];
@@ -553,7 +546,7 @@ struct RbGroup {   // pointer set k of each field is micro-batch k's
 template <typename T>
 __device__ __forceinline__ RbPtrs<T> rb_pick(const RbGroup<T>& a) {
   const int k = blockIdx.y;
-  return RbPtrs<T>{sel4(a.dy, k), sel4(a.ds, k), sel4(a.y, k), sel4(a.dz, k), sel4(a.part, k)};
+  return RbPtrs<T>{pickg(a.dy, k), pickg(a.ds, k), pickg(a.y, k), pickg(a.dz, k), pickg(a.part, k)};
 }
 
 template <typename T>
@@ -737,8 +730,8 @@ struct PoolGroup {
 };
 template <typename T>
 __global__ __launch_bounds__(256) void maxpool_fwd_k(PoolGroup<T> pg, int nb, int H, int W, int C) {
-  const T* __restrict__ x = sel4(pg.x, blockIdx.y);
-  T* __restrict__ y = sel4(pg.y, blockIdx.y);
+  const T* __restrict__ x = pickg(pg.x, blockIdx.y);
+  T* __restrict__ y = pickg(pg.y, blockIdx.y);
   constexpr int N = Pk<T>::N;
   int CP = C / N, H2 = H / 2, W2 = W / 2;
   long e = (long)blockIdx.x * 256 + threadIdx.x;

@@ -65,14 +65,6 @@ __device__ __forceinline__ void wait_stages(int ahead) {
   wait_vmcnt<0>();
 }
 
-// Element k (wave-uniform, 0 <= k < 4) of a kernel-argument array, read at
-// constant indices so that the array stays in the argument segment rather
-// than being copied to private memory for a dynamic index.
-template <typename T>
-__device__ __forceinline__ T pick4(const T (&a)[4], int k) {
-  return k == 0 ? a[0] : k == 1 ? a[1] : k == 2 ? a[2] : a[3];
-}
-
 // The dispatcher deals workgroups round-robin over the 8 XCDs (each with its
 // own L2); this maps dispatch index bid of nb to a logical index so that each
 // XCD runs one contiguous range of logical indices.

@@ -203,8 +203,8 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
     i_ns = stages_of(i_kr);
     const int gi = i_kr / kpg;
     i_krl = i_kr - gi * kpg;
-    rzg = make_rsrc(pick4(io.dz, gi), zbytes);
-    rxg = make_rsrc(pick4(io.x, gi), xbytes);
+    rzg = make_rsrc(pickg(io.dz, gi), zbytes);
+    rxg = make_rsrc(pickg(io.x, gi), xbytes);
   };
   if (n_items > 0) {
     coords(0, i_kr, i_r, i_co0, i_ci0);
@@ -343,7 +343,7 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
     // l % 32 of this wave's quarter; with KS = 2 wave kh stores v = 8 kh ..
     // 8 kh + 7
     const int gi = kr / kpg;
-    float* o = pick4(io.out, gi) + (long)(kr - gi * kpg) * E;
+    float* o = pickg(io.out, gi) + (long)(kr - gi * kpg) * E;
     const int ci = ci0 + nw * 32 + (lane & 31);
     auto store = [&](int v0, int v1) __attribute__((always_inline)) {
 #pragma unroll

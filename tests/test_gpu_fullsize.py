@@ -1,7 +1,8 @@
 """Parity at the benchmark's full size and launch configuration: the U-Net
 stage (partition 1 of 4, input 32x64x192x192 bf16, m = 8, checkpoint
-always), run as the benchmark runs it (two micro-batches per launch on the
-buffers of two lanes, everything on one stream), checked on sampled
+always), run as the benchmark runs it (all eight micro-batches in one
+launch per layer, on the buffers of eight lanes, everything on one stream),
+checked on sampled
 outputs the oracle computes one sample at a time, and bit-exact against the
 same run without checkpointing.
 
@@ -23,7 +24,7 @@ from workloads.synth import EXACT
 pytestmark = pytest.mark.gpu
 
 SAMPLES = [0, 31]   # first sample of micro-batch 1 and last of micro-batch 8
-BENCH = dict(lanes=4, group=4, serial=True)
+BENCH = dict(lanes=8, group=8, serial=True)
 
 
 @pytest.fixture(scope="module")

@@ -201,6 +201,26 @@ def test_micro_batch_groups_bench_stage():
         assert torch.equal(r["dx"], runs[0]["dx"])
 
 
+def test_groups_of_eight_are_bit_identical():
+    """Eight micro-batches per call and launch (m = 8, eight lanes) against
+    one per launch: the ragged stage (both nine-tap widths, pooling, an
+    exported skip), the benchmark stage's 192 x 192 layers and the
+    depthwise / pointwise cells, except-last."""
+    cases = [
+        ("unet5-c64-48", specs.unet(5, 64, 64, 48, "unet5-c64-48"), 8, (7, 5, 3, 4)),
+        ("unet5-c64", specs.unet(5, 64, 64, 192, "unet5-c64"), 16, (7, 5, 3, 4)),
+        ("cells4-c256", specs.amoeba_cells(4, 256, 14, "cells4-c256"), 8, (8,)),
+    ]
+    for name, net, B, bal in cases:
+        runs = []
+        for k in (1, 8):
+            say(f"eights {name} group={k}")
+            runs.append(gpu_stage(net, BF16, B, 8, CKPT_EXCEPT_LAST, bal, 1, lanes=k, group=k))
+        same_bits(runs[0], runs[1])
+        assert torch.equal(runs[1]["y"], runs[0]["y"])
+        assert torch.equal(runs[1]["dx"], runs[0]["dx"])
+
+
 def test_tiny_fp32_pipeline_all_modes():
     """4-layer conv3x3+bias+ReLU stack, C=16, 8x16x32x32 fp32, m=4, n=2."""
     wl = specs.tiny()
