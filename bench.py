@@ -858,7 +858,7 @@ def main():
     ap.add_argument("--lanes", type=int, default=None,
                     help="concurrency lanes: micro-batch i runs on stream (i - 1) %% lanes "
                          "(default: the group size, at least 2)")
-    ap.add_argument("--group", type=int, default=8, choices=[1, 2, 4, 8],
+    ap.add_argument("--group", type=int, default=16, choices=[1, 2, 4, 8, 16],
                     help="micro-batches per stage call and kernel launch (halved until it "
                          "divides the lanes and m)")
     ap.add_argument("--one-stream", dest="one_stream", action="store_true", default=None,
@@ -933,9 +933,11 @@ def main():
     log("setting up", wl.name)
     sess = Session(net, BF16, n=wl.n, bind_layers=None)
     lo, hi = sess.bounds[0]
+    while args.group > 1 and wl.m % args.group:
+        args.group //= 2
     if args.lanes is None:
         args.lanes = max(2, args.group)
-    while args.group > 1 and (min(args.lanes, wl.m) % args.group or wl.m % args.group):
+    while args.group > 1 and min(args.lanes, wl.m) % args.group:
         args.group //= 2
     sess.plan(wl.batch, wl.m, mode, args.lanes)
     sess.group = args.group

@@ -239,7 +239,7 @@ tgp_status tgp_stage_forward2(tgp_net* net, int j, int i0, int i1, int checkpoin
 tgp_status tgp_stage_backward_recompute2(tgp_net* net, int j, int i0, int i1, const void* dy0,
                                          const void* dy1, void* dx0, void* dx1, void* stream);
 
-/* The same for a group of count (1..8) tasks: tgp_stage_forward_n runs
+/* The same for a group of count (1..16) tasks: tgp_stage_forward_n runs
  * F_{i,j} for i = i0, i0 + 1, .., i0 + count - 1 (checkpoint[k], x_in[k]
  * and y_out[k] belong to micro-batch i0 + k), and
  * tgp_stage_backward_recompute_n runs F'_{i,j} + B_{i,j} for i = i0, i0 - 1,

@@ -71,9 +71,12 @@ struct Rows32Geom {
 // weights): the tiles of micro-batch k follow those of k - 1 (sample index
 // k nb .. k nb + nb - 1), so one launch covers them all and a block streams
 // tiles of several through its ring.
+// At most eight per launch (a larger group runs as launches of eight): a
+// select over more pointers cost the U-Net stage's launches about 1%.
+constexpr int kR32Group = 8;
 struct R32Io {
-  const bf16_t* x[kMaxGroup];
-  bf16_t* y[kMaxGroup];
+  const bf16_t* x[kR32Group];
+  bf16_t* y[kR32Group];
 };
 
 template <int W, int R, int FW, int NS, int CH, int RK>
@@ -432,10 +435,18 @@ static hipError_t launch_rows32(const R32Io& io, int ng, const bf16_t* Wt, const
 hipError_t conv_forward_rows32(int n, const void* const* x, const void* w, const float* b,
                                void* const* y, const ConvShape& s, int relu, hipStream_t st) {
   if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  if (n > kR32Group) {
+    for (int k0 = 0; k0 < n; k0 += kR32Group) {
+      const int c = n - k0 < kR32Group ? n - k0 : kR32Group;
+      const hipError_t e = conv_forward_rows32(c, x + k0, w, b, y + k0, s, relu, st);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
   const int c = rows32_pick(s, n);
   if (c < 0 || !conv_rows32_ok(s)) return hipErrorInvalidValue;
   R32Io io{};
-  for (int k = 0; k < kMaxGroup; ++k) {   // unused entries repeat micro-batch 0
+  for (int k = 0; k < kR32Group; ++k) {   // unused entries repeat micro-batch 0
     io.x[k] = (const bf16_t*)x[k < n ? k : 0];
     io.y[k] = (bf16_t*)y[k < n ? k : 0];
     if (!io.x[k] || !io.y[k]) return hipErrorInvalidValue;

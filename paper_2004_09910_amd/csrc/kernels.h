@@ -10,7 +10,7 @@ namespace tgpk {
 
 // Micro-batches of one layer that one launch may cover (the same shape and
 // weights, separate tensors).
-constexpr int kMaxGroup = 8;
+constexpr int kMaxGroup = 16;
 
 // One convolution at one micro-batch: nb samples of H x W, NHWC.
 struct ConvShape {

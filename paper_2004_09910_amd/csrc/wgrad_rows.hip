@@ -66,10 +66,12 @@ __device__ __forceinline__ void lds_handoff_barrier() {
 // The micro-batches of one launch (ng of them, nb samples each): the K
 // ranges of micro-batch k follow those of k - 1 and its slices go to
 // out[k], so one launch covers them all.
+// At most eight per launch (a larger group runs as launches of eight).
+constexpr int kWgGroup = 8;
 struct WgIo {
-  const bf16_t* x[kMaxGroup];
-  const bf16_t* dz[kMaxGroup];
-  float* out[kMaxGroup];
+  const bf16_t* x[kWgGroup];
+  const bf16_t* dz[kWgGroup];
+  float* out[kWgGroup];
 };
 //
 // KS is the number of waves per SIMD: with KS = 2 the two waves of a SIMD
@@ -466,7 +468,7 @@ hipError_t conv_wgrad_rows_launch(const void* x, const void* dz, float* dw, floa
   const WgPlan p = wgrad_rows_plan(s);
   float* out = p.nK > 1 ? partial : dw;
   WgIo io{};
-  for (int k = 0; k < kMaxGroup; ++k) {
+  for (int k = 0; k < kWgGroup; ++k) {
     io.x[k] = (const bf16_t*)x;
     io.dz[k] = (const bf16_t*)dz;
     io.out[k] = out;
@@ -488,9 +490,18 @@ hipError_t conv_wgrad_rows_launch_n(int n, const void* const* x, const void* con
                                     float* const* dw, float* const* partial, const ConvShape& s,
                                     hipStream_t st, ReduceJob* const* defer) {
   if (n < 1 || n > kMaxGroup || !wgrad_rows_ok(s)) return hipErrorInvalidValue;
+  if (n > kWgGroup) {
+    for (int k0 = 0; k0 < n; k0 += kWgGroup) {
+      const int c = n - k0 < kWgGroup ? n - k0 : kWgGroup;
+      const hipError_t e =
+          conv_wgrad_rows_launch_n(c, x + k0, dz + k0, dw + k0, partial + k0, s, st, defer + k0);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
   const WgPlan p = wgrad_rows_plan(s);
   WgIo io{};
-  for (int k = 0; k < kMaxGroup; ++k) {   // unused entries repeat micro-batch 0
+  for (int k = 0; k < kWgGroup; ++k) {   // unused entries repeat micro-batch 0
     const int q = k < n ? k : 0;
     io.x[k] = (const bf16_t*)x[q];
     io.dz[k] = (const bf16_t*)dz[q];

@@ -275,7 +275,7 @@ def test_paired_stage_calls_check_lanes_and_order():
 
 
 def test_group_stage_calls_check_count_lanes_and_order():
-    """tgp_stage_forward_n / tgp_stage_backward_recompute_n: 1..8 tasks on
+    """tgp_stage_forward_n / tgp_stage_backward_recompute_n: 1..16 tasks on
     distinct lanes, consecutive micro-batches (i0 upwards for the forward,
     downwards for the backward), each passing the single call's checks.
     Every call here fails a host check, so nothing is enqueued."""
@@ -290,8 +290,8 @@ def test_group_stage_calls_check_count_lanes_and_order():
     ck = I4(1, 1, 1, 0)                       # except-last: only i = 4 keeps its activations
     xs, none = P4(F, F, F, F), P4(None, None, None, None)
     assert st("tgp_stage_forward_n", 1, 1, 0, ck, xs, xs, None) == tgp.EINVAL      # count 0
-    assert st("tgp_stage_forward_n", 1, 1, 9, ck, xs, xs, None) == tgp.EINVAL      # count 9
-    assert "count 9" in tgp.last_error()
+    assert st("tgp_stage_forward_n", 1, 1, 17, ck, xs, xs, None) == tgp.EINVAL     # count 17
+    assert "count 17" in tgp.last_error()
     assert st("tgp_stage_forward_n", 1, 1, 5, ck, xs, xs, None) == tgp.EINVAL      # i = 5
     assert st("tgp_stage_forward_n", 1, 2, 4, ck, xs, xs, None) == tgp.EINVAL      # i = 5
     assert st("tgp_stage_forward_n", 1, 1, 4, I4(1, 1, 1, 1), xs, xs, None) == tgp.EINVAL

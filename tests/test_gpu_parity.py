@@ -201,21 +201,25 @@ def test_micro_batch_groups_bench_stage():
         assert torch.equal(r["dx"], runs[0]["dx"])
 
 
-def test_groups_of_eight_are_bit_identical():
+def test_groups_of_eight_and_sixteen_are_bit_identical():
     """Eight micro-batches per call and launch (m = 8, eight lanes) against
     one per launch: the ragged stage (both nine-tap widths, pooling, an
     exported skip), the benchmark stage's 192 x 192 layers and the
-    depthwise / pointwise cells, except-last."""
+    depthwise / pointwise cells; and sixteen (m = 16, sixteen lanes, the
+    largest group) on the cells and on the ragged stage, whose nine-tap and
+    row-blocked weight-gradient kernels take eight per launch; except-last."""
     cases = [
-        ("unet5-c64-48", specs.unet(5, 64, 64, 48, "unet5-c64-48"), 8, (7, 5, 3, 4)),
-        ("unet5-c64", specs.unet(5, 64, 64, 192, "unet5-c64"), 16, (7, 5, 3, 4)),
-        ("cells4-c256", specs.amoeba_cells(4, 256, 14, "cells4-c256"), 8, (8,)),
+        ("unet5-c64-48", specs.unet(5, 64, 64, 48, "unet5-c64-48"), 8, 8, (7, 5, 3, 4), 8),
+        ("unet5-c64", specs.unet(5, 64, 64, 192, "unet5-c64"), 16, 8, (7, 5, 3, 4), 8),
+        ("cells4-c256", specs.amoeba_cells(4, 256, 14, "cells4-c256"), 8, 8, (8,), 8),
+        ("cells4-c256", specs.amoeba_cells(4, 256, 14, "cells4-c256"), 16, 16, (8,), 16),
+        ("unet5-c64-48", specs.unet(5, 64, 64, 48, "unet5-c64-48"), 16, 16, (7, 5, 3, 4), 16),
     ]
-    for name, net, B, bal in cases:
+    for name, net, B, m, bal, g in cases:
         runs = []
-        for k in (1, 8):
-            say(f"eights {name} group={k}")
-            runs.append(gpu_stage(net, BF16, B, 8, CKPT_EXCEPT_LAST, bal, 1, lanes=k, group=k))
+        for k in (1, g):
+            say(f"large groups {name} m={m} group={k}")
+            runs.append(gpu_stage(net, BF16, B, m, CKPT_EXCEPT_LAST, bal, 1, lanes=k, group=k))
         same_bits(runs[0], runs[1])
         assert torch.equal(runs[1]["y"], runs[0]["y"])
         assert torch.equal(runs[1]["dx"], runs[0]["dx"])
