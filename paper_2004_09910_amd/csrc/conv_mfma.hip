@@ -1429,7 +1429,7 @@ static hipError_t launch_1x1_res(int n, const void* const* x, const bf16_t* Wt, 
   const int G = (int)(T < 256 ? T : 256);
   ProfScope ps("conv1x1_res", 2.0 * n * P * s.cout * s.cin,
                2.0 * ((double)n * P * (s.cin + s.cout) + (double)s.cout * s.cin), st);
-  TGP_LAUNCH(ps, conv1x1_res<3>, dim3(G), dim3(512), 0, st, io, n, Wt, b, (int)P, s.cin, relu);
+  TGP_LAUNCH(ps, conv1x1_res<4>, dim3(G), dim3(512), 0, st, io, n, Wt, b, (int)P, s.cin, relu);
   return launch_status();
 }
 

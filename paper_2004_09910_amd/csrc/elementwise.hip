@@ -469,7 +469,7 @@ __global__ __launch_bounds__(256) void dw3_wgrad_rows_k(DwWgIo io, int H, int W,
   }
 }
 
-constexpr int kDwRows = 4;       // output rows per thread, forward and data gradient
+constexpr int kDwRows = 8;       // output rows per thread, forward and data gradient
 constexpr int kDwWgradRows = 8;  // rows per thread of the weight gradient
 
 // The row-window depthwise kernels apply: bf16, whole 16-byte packs, a pack
