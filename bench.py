@@ -269,10 +269,18 @@ def summarize_counters(out_dir, workload, eager_us=None):
                      "lds_wait": wait / wave if wave > 0 else float("nan"),
                      "flop_per_busy": flop / busy if busy > 0 else float("nan")})
     rows.sort(key=lambda r: -(r["us_c"] * r["dispatches"]))
+    import json as _json
+    group = 1
+    log = os.path.join(out_dir, "mfma.log")
+    if os.path.exists(log):
+        for line in open(log):
+            if line.startswith("{"):
+                group = int(_json.loads(line)["config"].get("group", 1))
+    per_launch = f"{group} micro-batch{'es' if group > 1 else ''} per launch"
     lines = [f"# MFMA and LDS counters: {workload}", "",
              "Commands (from the repository root on the GPU host; one counter group per run):", "",
              "    " + PROFILE_COMMANDS["mfma"], "    " + PROFILE_COMMANDS["lds"], "",
-             "Means per dispatch over one eager step (two micro-batches per launch). "
+             f"Means per dispatch over one eager step ({per_launch}). "
              "`MFMA GFLOP` = 512 x SQ_INSTS_VALU_MFMA_MOPS_BF16. `FLOP/busy cycle` = those FLOPs "
              "per SQ_VALU_MFMA_BUSY_CYCLES (summed over SIMDs): 1024 means every busy MFMA cycle "
              "of a SIMD does the full dense bf16 work (32x32x16: 32768 FLOP in 32 cycles). "
