@@ -264,6 +264,16 @@ tgp_status tgp_stage_backward_recompute_n(tgp_net* net, int j, int i0, int count
  * B_{i,j} and, for i < m, the accumulation of i + 1; ESTATE otherwise. */
 tgp_status tgp_grad_accumulate(tgp_net* net, int j, int i, int overwrite, void* stream);
 
+/* The accumulations of count (1..16) micro-batches i0, i0 - 1, ..,
+ * i0 - count + 1, in that order, as one launch where their pending sums lie
+ * at one stride from each other (else one launch per micro-batch): the same
+ * values as count tgp_grad_accumulate calls, each g_i^j added to g^j in
+ * turn (Sec. 2).  overwrite must be 1 exactly for i0 = m.  Requires B_{i,j}
+ * of every micro-batch of the group and, for i0 < m, the accumulation of
+ * i0 + 1 (ESTATE otherwise); EINVAL for a count or a range outside 1..m. */
+tgp_status tgp_grad_accumulate_n(tgp_net* net, int j, int i0, int count, int overwrite,
+                                 void* stream);
+
 /* One training step over the whole network: scatter x (B samples) into m
  * micro-batches; forward clocks k = 1..m+n-1 running F_{i,j} for i+j-1 = k
  * with j ascending (Algorithm 1); MSE loss sum (y-t)^2 / numel(target) of

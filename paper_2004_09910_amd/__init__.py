@@ -64,6 +64,7 @@ _SIG = {
     "tgp_stage_forward": [_P, _I, _I, _I, _P, _P, _P],
     "tgp_stage_backward_recompute": [_P, _I, _I, _P, _P, _P],
     "tgp_grad_accumulate": [_P, _I, _I, _I, _P],
+    "tgp_grad_accumulate_n": [_P, _I, _I, _I, _I, _P],
     "tgp_pipeline_step": [_P, _P, _P, _I, _I, _I, _I, _P, _P, _P],
     "tgp_pipeline_step_static": [_P, _P, _P, _I, _I, _I, _I, _P, _P, _P],
     "tgp_schedule_trace": [_I, _I, _I, ctypes.POINTER(ctypes.c_int32), _I, ctypes.POINTER(_I)],
@@ -264,6 +265,13 @@ def stage_backward_recompute_n(net: int, j: int, i0: int, dys: Sequence[int],
 def grad_accumulate(net: int, j: int, i: int, overwrite: bool, stream: int = 0) -> None:
     _check(_lib.tgp_grad_accumulate(net, j, i, int(overwrite), _vp(stream)),
            "tgp_grad_accumulate")
+
+
+def grad_accumulate_n(net: int, j: int, i0: int, count: int, overwrite: bool,
+                      stream: int = 0) -> None:
+    """The accumulations of micro-batches i0, i0 - 1, .., i0 - count + 1."""
+    _check(_lib.tgp_grad_accumulate_n(net, j, i0, count, int(overwrite), _vp(stream)),
+           "tgp_grad_accumulate_n")
 
 
 def pipeline_step(net: int, x: int, target: int, B: int, m: int, n: int, ckpt_mode: int,

@@ -918,71 +918,82 @@ __host__ __device__ __forceinline__ int acc_c4(int S) {
   return c;
 }
 
+// NG: micro-batches per entry as a template constant (1) or b.ng (0).
+template <int NG>
 __global__ __launch_bounds__(1024) void reduce_accumulate_k(AccBatch b, int overwrite,
                                                             int ntiles) {
   // blocks are persistent over tiles (tile = the block of the layout above),
   // so the entry lookup and the block start are paid once per block
   __shared__ float4 red[1024];
+  const int ng = NG ? NG : b.ng;
   int k = 0;   // entry of the current tile (tiles only increase)
   for (int tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     while (k + 1 < b.count && tile >= b.blk0[k + 1]) ++k;
     const long bx = (long)tile - b.blk0[k];
     const long E = b.n[k];
     const int S = b.S[k];
-    const float* __restrict__ part = b.g[k];
     float* __restrict__ acc = b.acc[k];
     if (E % 4) {   // tile-uniform
       const long e = bx * 1024 + threadIdx.x;
       if (e < E) {
-        float r = 0.f;
-        for (int s = 0; s < S; ++s) r += part[(long)s * E + e];
-        acc[e] = overwrite ? r : acc[e] + r;
+        float cur = 0.f;
+        for (int q = 0; q < ng; ++q) {
+          const float* __restrict__ part = b.g[k] + q * b.gstride[k];
+          float r = 0.f;
+          for (int s = 0; s < S; ++s) r += part[(long)s * E + e];
+          cur = q > 0 ? cur + r : overwrite ? r : acc[e] + r;
+        }
+        acc[e] = cur;
       }
       continue;
     }
     const int C4 = acc_c4(S), LANES = 1024 / C4;
     const int col = threadIdx.x % C4, lane = threadIdx.x / C4;
     const long e4 = (bx * C4 + col) * 4;
-    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (e4 < E) {
-      // up to eight loads in flight per step; slices past S add zeros
-      for (int s = lane; s < S; s += 8 * LANES) {
-        float4 t[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u)
-          t[u] = s + u * LANES < S ? *(const float4*)(part + (long)(s + u * LANES) * E + e4)
-                                   : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          a.x += t[u].x; a.y += t[u].y; a.z += t[u].z; a.w += t[u].w;
-        }
-      }
-    }
-    if (LANES == 1) {   // tile-uniform
+    float4 cur = make_float4(0.f, 0.f, 0.f, 0.f);   // the running sum (lane 0)
+    for (int q = 0; q < ng; ++q) {
+      const float* __restrict__ part = b.g[k] + q * b.gstride[k];
+      float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
       if (e4 < E) {
-        if (!overwrite) {
-          const float4 o = *(const float4*)(acc + e4);
-          a.x = o.x + a.x; a.y = o.y + a.y; a.z = o.z + a.z; a.w = o.w + a.w;
+        // up to eight loads in flight per step; slices past S add zeros
+        for (int s = lane; s < S; s += 8 * LANES) {
+          float4 t[8];
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            t[u] = s + u * LANES < S ? *(const float4*)(part + (long)(s + u * LANES) * E + e4)
+                                     : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            a.x += t[u].x; a.y += t[u].y; a.z += t[u].z; a.w += t[u].w;
+          }
         }
-        *(float4*)(acc + e4) = a;
       }
-      continue;
+      float4 r = a;
+      if (LANES > 1) {   // tile-uniform
+        red[lane * C4 + col] = a;
+        __syncthreads();
+        if (lane == 0) {
+          r = red[col];
+          for (int l = 1; l < LANES; ++l) {
+            const float4 t = red[l * C4 + col];
+            r.x += t.x; r.y += t.y; r.z += t.z; r.w += t.w;
+          }
+        }
+        if (NG != 1) __syncthreads();   // red is rewritten by the next micro-batch
+      }
+      if (lane == 0 && e4 < E) {
+        if (q > 0) {
+          cur.x = cur.x + r.x; cur.y = cur.y + r.y; cur.z = cur.z + r.z; cur.w = cur.w + r.w;
+        } else if (overwrite) {
+          cur = r;
+        } else {
+          const float4 o = *(const float4*)(acc + e4);
+          cur.x = o.x + r.x; cur.y = o.y + r.y; cur.z = o.z + r.z; cur.w = o.w + r.w;
+        }
+      }
     }
-    red[lane * C4 + col] = a;
-    __syncthreads();
-    if (lane == 0 && e4 < E) {
-      float4 r = red[col];
-      for (int l = 1; l < LANES; ++l) {
-        const float4 t = red[l * C4 + col];
-        r.x += t.x; r.y += t.y; r.z += t.z; r.w += t.w;
-      }
-      if (!overwrite) {
-        const float4 o = *(const float4*)(acc + e4);
-        r.x = o.x + r.x; r.y = o.y + r.y; r.z = o.z + r.z; r.w = o.w + r.w;
-      }
-      *(float4*)(acc + e4) = r;
-    }
-    __syncthreads();   // red is rewritten by the next tile
+    if (lane == 0 && e4 < E) *(float4*)(acc + e4) = cur;
+    if (NG == 1 && LANES > 1) __syncthreads();   // red is rewritten by the next tile
   }
 }
 
@@ -1588,17 +1599,18 @@ hipError_t loss_finalize(const float* parts, int m, float inv_numel, float* loss
 }
 
 hipError_t grad_accumulate_batch(AccBatch b, int overwrite, hipStream_t st) {
-  if (b.count < 0 || b.count > kMaxAcc) return hipErrorInvalidValue;
+  if (b.count < 0 || b.count > kMaxAcc || b.ng < 1 || b.ng > kMaxGroup) return hipErrorInvalidValue;
   long blocks = 0;
   double bytes = 0;
   int used = 0;
   for (int k = 0; k < b.count; ++k) {
     if (b.n[k] <= 0 || b.S[k] < 1) continue;
-    b.acc[used] = b.acc[k]; b.g[used] = b.g[k]; b.n[used] = b.n[k]; b.S[used] = b.S[k];
+    b.acc[used] = b.acc[k]; b.g[used] = b.g[k]; b.gstride[used] = b.gstride[k];
+    b.n[used] = b.n[k]; b.S[used] = b.S[k];
     b.blk0[used] = (int)blocks;
     const int C4 = acc_c4(b.S[k]);
     blocks += b.n[k] % 4 ? cdiv(b.n[k], 1024L) : cdiv(b.n[k], 4L * C4);
-    bytes += 4.0 * b.n[k] * (b.S[k] + (overwrite ? 1 : 2));
+    bytes += 4.0 * b.n[k] * ((double)b.S[k] * b.ng + (overwrite ? 1 : 2));
     ++used;
   }
   b.count = used;
@@ -1606,7 +1618,12 @@ hipError_t grad_accumulate_batch(AccBatch b, int overwrite, hipStream_t st) {
   if (blocks >= (1L << 31)) return hipErrorInvalidValue;
   ProfScope ps("reduce_accumulate", 0.0, bytes, st);
   const unsigned grid = (unsigned)(blocks < 512 ? blocks : 512);   // two blocks per CU
-  TGP_LAUNCH(ps, reduce_accumulate_k, dim3(grid), dim3(1024), 0, st, b, overwrite, (int)blocks);
+  if (b.ng == 1)
+    TGP_LAUNCH(ps, reduce_accumulate_k<1>, dim3(grid), dim3(1024), 0, st, b, overwrite,
+               (int)blocks);
+  else
+    TGP_LAUNCH(ps, reduce_accumulate_k<0>, dim3(grid), dim3(1024), 0, st, b, overwrite,
+               (int)blocks);
   return launch_status();
 }
 

@@ -173,12 +173,17 @@ hipError_t grad_accumulate(float* acc, const float* g, long n, int overwrite, hi
 // kMaxAcc tensors in one launch (passed by value).  Each r_k is summed in a
 // fixed order that depends on (n_k, S_k) only; it is not always the order
 // of splitk_reduce_launch, so a layer's sums are either always left to the
-// accumulation or always reduced at once.
-constexpr int kMaxAcc = 48;
+// accumulation or always reduced at once.  With ng > 1 the launch does ng
+// such accumulations in a row, micro-batch q's slices at g_k + q gstride_k:
+// acc_k (+)= r_k(0), then acc_k += r_k(1), .., the same values as ng
+// launches (overwrite applies to the first).
+constexpr int kMaxAcc = 64;
 struct AccBatch {
   int count;
+  int ng;              // micro-batches per entry, 1 .. kMaxGroup
   float* acc[kMaxAcc];
   const float* g[kMaxAcc];
+  long gstride[kMaxAcc];   // floats from one micro-batch's slices to the next's
   long n[kMaxAcc];
   int S[kMaxAcc];
   int blk0[kMaxAcc];   // first block of each entry (filled by the launcher)

@@ -679,6 +679,7 @@ tgp_status run_accumulate(tgp_net* N, int j, int i, int overwrite, hipStream_t s
   Range rg("ACC", i, j);
   tgpk::AccBatch batch;
   batch.count = 0;
+  batch.ng = 1;
   auto flush = [&]() -> tgp_status {
     if (batch.count == 0) return TGP_OK;
     HIPCHK(tgpk::grad_accumulate_batch(batch, overwrite, st), "grad_accumulate");
@@ -692,6 +693,7 @@ tgp_status run_accumulate(tgp_net* N, int j, int i, int overwrite, hipStream_t s
     }
     batch.acc[batch.count] = acc;
     batch.g[batch.count] = job.part;
+    batch.gstride[batch.count] = 0;
     batch.n[batch.count] = job.E;
     batch.S[batch.count] = job.S;
     ++batch.count;
@@ -705,6 +707,54 @@ tgp_status run_accumulate(tgp_net* N, int j, int i, int overwrite, hipStream_t s
     if (r != TGP_OK) return r;
   }
   return flush();
+}
+
+// The accumulations of micro-batches i0, i0 - 1, .., i0 - cnt + 1 (in that
+// order) for partition j, as one launch when every tensor's pending sums of
+// the cnt micro-batches have one shape and lie at one stride from each
+// other (the per-micro-batch gradient slots), else one launch per
+// micro-batch.  The values are those of cnt run_accumulate calls.
+tgp_status run_accumulate_g(tgp_net* N, int j, int i0, int cnt, int overwrite, hipStream_t st) {
+  const size_t L = N->L.size();
+  auto job = [&](int q, int l, int w) -> const tgpk::ReduceJob& {
+    return N->pend[(size_t)(i0 - q - 1) * L + l][w];
+  };
+  tgpk::AccBatch batch;
+  batch.count = 0;
+  batch.ng = cnt;
+  bool one = cnt > 1;
+  std::vector<std::pair<float*, std::pair<int, int>>> ents;   // (acc, (layer, which))
+  for (int l = N->lo[j - 1]; l < N->hi[j - 1] && one; ++l) {
+    LayerRt& Lr = N->L[l];
+    for (int w = 0; w < (Lr.d.bias ? 2 : 1) && one; ++w) {
+      const tgpk::ReduceJob& j0 = job(0, l, w);
+      const long stride = cnt > 1 ? (long)(job(1, l, w).part - j0.part) : 0;
+      for (int q = 1; q < cnt && one; ++q) {
+        const tgpk::ReduceJob& jq = job(q, l, w);
+        one = jq.E == j0.E && jq.S == j0.S && jq.part - j0.part == (long)q * stride;
+      }
+      ents.push_back({w ? Lr.db_acc : Lr.dw_acc, {l, w}});
+    }
+  }
+  if (!one || ents.size() > (size_t)tgpk::kMaxAcc) {
+    for (int q = 0; q < cnt; ++q) {
+      tgp_status r = run_accumulate(N, j, i0 - q, q == 0 ? overwrite : 0, st);
+      if (r != TGP_OK) return r;
+    }
+    return TGP_OK;
+  }
+  Range rg("ACC", i0, j);
+  for (auto& e : ents) {
+    const tgpk::ReduceJob& j0 = job(0, e.second.first, e.second.second);
+    const int k = batch.count++;
+    batch.acc[k] = e.first;
+    batch.g[k] = j0.part;
+    batch.gstride[k] = (long)(job(1, e.second.first, e.second.second).part - j0.part);
+    batch.n[k] = j0.E;
+    batch.S[k] = j0.S;
+  }
+  HIPCHK(tgpk::grad_accumulate_batch(batch, overwrite, st), "grad_accumulate");
+  return TGP_OK;
 }
 
 // Plan and workspace present, and the layers of partition j (all partitions
@@ -1463,6 +1513,27 @@ tgp_status tgp_grad_accumulate(tgp_net* N, int j, int i, int overwrite, void* st
   r = run_accumulate(N, j, i, overwrite, S(stream));
   if (r != TGP_OK) return r;
   N->st[c] = ACC;
+  return TGP_OK;
+}
+
+tgp_status tgp_grad_accumulate_n(tgp_net* N, int j, int i0, int count, int overwrite,
+                                 void* stream) {
+  tgp_status r = check_ready(N, j);
+  if (r != TGP_OK) return r;
+  if (j < 1 || j > N->n) return fail(TGP_EINVAL, "partition %d out of 1..%d", j, N->n);
+  if (count < 1 || count > MG) return fail(TGP_EINVAL, "count %d out of 1..%d", count, MG);
+  if (i0 - count + 1 < 1 || i0 > N->m)
+    return fail(TGP_EINVAL, "micro-batches %d down to %d out of 1..%d", i0, i0 - count + 1, N->m);
+  if ((overwrite != 0) != (i0 == N->m))
+    return fail(TGP_EINVAL, "overwrite must be 1 exactly for i0 = m");
+  for (int q = 0; q < count; ++q)
+    if (N->st[cell(N, i0 - q, j)] != BWD)
+      return fail(TGP_ESTATE, "accumulate (%d,%d) needs B_{%d,%d} first", i0 - q, j, i0 - q, j);
+  if (i0 < N->m && N->st[cell(N, i0 + 1, j)] != ACC)
+    return fail(TGP_ESTATE, "accumulate (%d,%d) must follow accumulate (%d,%d)", i0, j, i0 + 1, j);
+  r = run_accumulate_g(N, j, i0, count, overwrite, S(stream));
+  if (r != TGP_OK) return r;
+  for (int q = 0; q < count; ++q) N->st[cell(N, i0 - q, j)] = ACC;
   return TGP_OK;
 }
 

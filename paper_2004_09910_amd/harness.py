@@ -261,10 +261,10 @@ class Session:
     def _stage_step_groups(self, j, x, y, dy, dx, sl, serial_stream=None):
         """stage_step with G = `group` micro-batches per call: forwards
         (1..G), (G+1..2G), ..., backwards (m..m-G+1), ..., each group on the
-        stream of its lanes, and the accumulations, in the order m..1, on
-        one more stream that waits for each group's backward (all on
-        `serial_stream`, in that order, when given).  Needs G to divide the
-        lanes and m."""
+        stream of its lanes, and each group's accumulations (one call, in
+        the order m..1) on one more stream that waits for the group's
+        backward (all on `serial_stream`, in that order, when given).  Needs
+        G to divide the lanes and m."""
         G = self.group
         K = min(self.lanes, self.m)
         if K % G or self.m % G:
@@ -287,8 +287,7 @@ class Session:
                 fwd(i, serial_stream)
             for i in range(self.m, 0, -G):
                 bwd(i, serial_stream)
-                for k in range(G):
-                    tgp.grad_accumulate(h, j, i - k, i - k == self.m, serial_stream)
+                tgp.grad_accumulate_n(h, j, i, G, i == self.m, serial_stream)
             return
         cur = torch.cuda.current_stream()
         if self._lane_streams is None:
@@ -309,8 +308,7 @@ class Session:
             ev.record(s)
             self._events.append(ev)
             acc.wait_event(ev)
-            for k in range(G):
-                tgp.grad_accumulate(h, j, i - k, i - k == self.m, acc.cuda_stream)
+            tgp.grad_accumulate_n(h, j, i, G, i == self.m, acc.cuda_stream)
         for s in self._lane_streams:
             cur.wait_stream(s)
 

@@ -119,7 +119,11 @@ int main() {
               const void* xs[4] = {FAKE, FAKE, FAKE, FAKE};
               void* ys[4] = {FAKE, FAKE, FAKE, FAKE};
               EXPECT(tgp_stage_forward_n(N, 1, 1, 0, ckv, xs, ys, nullptr) == TGP_EINVAL);
-              EXPECT(tgp_stage_forward_n(N, 1, 1, 5, ckv, xs, ys, nullptr) == TGP_EINVAL);
+              EXPECT(tgp_stage_forward_n(N, 1, 1, 17, ckv, xs, ys, nullptr) == TGP_EINVAL);
+              EXPECT(tgp_grad_accumulate_n(N, 1, m, 0, 1, nullptr) == TGP_EINVAL);
+              EXPECT(tgp_grad_accumulate_n(N, 1, m, m + 1, 1, nullptr) == TGP_EINVAL);
+              EXPECT(tgp_grad_accumulate_n(N, 1, m, 1, 0, nullptr) == TGP_EINVAL);
+              EXPECT(tgp_grad_accumulate_n(N, 1, m, m, 1, nullptr) == TGP_ESTATE);
               EXPECT(tgp_stage_forward_n(N, 1, m, 2, ckv, xs, ys, nullptr) == TGP_EINVAL);
               EXPECT(tgp_stage_backward_recompute_n(N, 1, 1, 2, xs, ys, nullptr) == TGP_EINVAL);
               const tgp_status sb = tgp_stage_backward_recompute_n(N, 1, m, 1, xs, ys, nullptr);

@@ -305,6 +305,17 @@ def test_group_stage_calls_check_count_lanes_and_order():
     assert "all or none" in tgp.last_error()
     assert st("tgp_stage_backward_recompute_n", 1, 4, 4, P4(F, F, None, F), none,
               None) == tgp.EINVAL
+    # grouped accumulation: count and range, overwrite exactly for i0 = m,
+    # and every micro-batch's backward first
+    assert st("tgp_grad_accumulate_n", 1, 4, 0, 1, None) == tgp.EINVAL        # count 0
+    assert st("tgp_grad_accumulate_n", 1, 4, 17, 1, None) == tgp.EINVAL       # count 17
+    assert st("tgp_grad_accumulate_n", 1, 4, 5, 1, None) == tgp.EINVAL        # 4..0
+    assert st("tgp_grad_accumulate_n", 1, 4, 4, 0, None) == tgp.EINVAL        # overwrite
+    assert "overwrite" in tgp.last_error()
+    assert st("tgp_grad_accumulate_n", 1, 3, 2, 1, None) == tgp.EINVAL        # overwrite
+    assert st("tgp_grad_accumulate_n", 3, 4, 4, 1, None) == tgp.EINVAL        # j = 3
+    assert st("tgp_grad_accumulate_n", 1, 4, 4, 1, None) == tgp.ESTATE        # no B yet
+    assert "needs B" in tgp.last_error()
     # two lanes: micro-batches 1 and 3 share one, and a backward of four
     # needs four
     tgp.set_lanes(h, 2)
