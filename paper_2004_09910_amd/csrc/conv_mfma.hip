@@ -1211,18 +1211,20 @@ __global__ __launch_bounds__(256) void splitk_reduce_scalar(const float* __restr
 
 // wt[ci][tap'][co] = w[co][taps-1-tap'][ci]: the data gradient of a
 // cross-correlation is a cross-correlation with the 180-degree rotated,
-// channel-transposed filter.
+// channel-transposed filter.  A batch of tensors in one launch: blocks
+// blk0[k] .. blk0[k + 1] - 1 serve tensor k.
 template <typename T>
-__global__ void wtransform_kernel(const T* __restrict__ w, T* __restrict__ wt, int cout, int cin,
-                                  int taps) {
-  long e = (long)blockIdx.x * 256 + threadIdx.x;
-  long n = (long)cout * cin * taps;
-  if (e >= n) return;
-  int co = e % cout;
-  long r = e / cout;
-  int tp = r % taps;
-  int ci = r / taps;
-  wt[e] = w[((long)co * taps + (taps - 1 - tp)) * cin + ci];
+__global__ void wtransform_batch_kernel(WtBatch b) {
+  int k = 0;
+  while (k + 1 < b.count && (int)blockIdx.x >= b.blk0[k + 1]) ++k;
+  const long e = (long)(blockIdx.x - b.blk0[k]) * 256 + threadIdx.x;
+  const int cout = b.cout[k], cin = b.cin[k], taps = b.taps[k];
+  if (e >= (long)cout * cin * taps) return;
+  const int co = e % cout;
+  const long r = e / cout;
+  const int tp = r % taps;
+  const int ci = r / taps;
+  ((T*)b.wt[k])[e] = ((const T*)b.w[k])[((long)co * taps + (taps - 1 - tp)) * cin + ci];
 }
 
 struct WgradPlan {
@@ -1582,16 +1584,24 @@ hipError_t conv_forward_mfma(const void* x, const void* w, const float* b, void*
   }
 }
 
-hipError_t weight_transform(int dt, const void* w, void* wt, int cout, int cin, int taps,
-                            hipStream_t st) {
-  long n = (long)cout * cin * taps;
-  ProfScope ps("wtransform", 0.0, 2.0 * n * (dt == 0 ? 2 : 4), st);
+hipError_t weight_transform_batch(int dt, WtBatch b, hipStream_t st) {
+  if (b.count < 0 || b.count > kMaxWt) return hipErrorInvalidValue;
+  long blocks = 0;
+  double bytes = 0;
+  for (int k = 0; k < b.count; ++k) {
+    const long n = (long)b.cout[k] * b.cin[k] * b.taps[k];
+    if (n <= 0) return hipErrorInvalidValue;
+    b.blk0[k] = (int)blocks;
+    blocks += cdiv(n, 256);
+    bytes += 2.0 * n * (dt == 0 ? 2 : 4);
+  }
+  if (b.count == 0) return hipSuccess;
+  if (blocks >= (1L << 31)) return hipErrorInvalidValue;
+  ProfScope ps("wtransform", 0.0, bytes, st);
   if (dt == 0)
-    TGP_LAUNCH(ps, wtransform_kernel<bf16_t>, dim3(cdiv(n, 256)), dim3(256), 0, st,
-                       (const bf16_t*)w, (bf16_t*)wt, cout, cin, taps);
+    TGP_LAUNCH(ps, wtransform_batch_kernel<bf16_t>, dim3((unsigned)blocks), dim3(256), 0, st, b);
   else
-    TGP_LAUNCH(ps, wtransform_kernel<float>, dim3(cdiv(n, 256)), dim3(256), 0, st,
-                       (const float*)w, (float*)wt, cout, cin, taps);
+    TGP_LAUNCH(ps, wtransform_batch_kernel<float>, dim3((unsigned)blocks), dim3(256), 0, st, b);
   return launch_status();
 }
 

@@ -76,8 +76,17 @@ hipError_t conv_wgrad_rows_launch_n(int n, const void* const* x, const void* con
 // Whether the data-gradient kernel for this shape reads the transformed
 // weight wt = [cin][taps][cout] (taps rotated by 180 degrees).
 bool conv_dgrad_uses_wt(int dt, const ConvShape& s);
-hipError_t weight_transform(int dt, const void* w, void* wt, int cout, int cin, int taps,
-                            hipStream_t st);
+// Builds those transformed weights, wt[ci][tap'][co] = w[co][taps-1-tap'][ci],
+// for up to kMaxWt tensors in one launch (passed by value).
+constexpr int kMaxWt = 32;
+struct WtBatch {
+  int count;
+  const void* w[kMaxWt];
+  void* wt[kMaxWt];
+  int cout[kMaxWt], cin[kMaxWt], taps[kMaxWt];
+  int blk0[kMaxWt];   // first block of each tensor (filled by the launcher)
+};
+hipError_t weight_transform_batch(int dt, WtBatch b, hipStream_t st);
 // dx[p][ci] = sum_{co,tap} dz[p - off(tap)][co] w[co][tap][ci]
 hipError_t conv_dgrad(int dt, const void* dz, const void* w, const void* wt, void* dx,
                       const ConvShape& s, float* part, size_t part_cap, hipStream_t st);

@@ -412,13 +412,24 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     return N->wt_stale[(size_t)((i - 1) % N->lanes) * N->n + (j - 1)];
   };
   auto refresh_wt = [&](int i) -> tgp_status {
+    // one launch for the partition's layers (several when more than kMaxWt)
+    tgpk::WtBatch wb;
+    wb.count = 0;
     for (int l = lo; l < hi; ++l) {
       LayerRt& Lr = N->L[l];
-      if (Lr.has_wt)
-        HIPCHK(tgpk::weight_transform(N->dt, Lr.w, T_(N, i, Lr.o_wt), Lr.d.cout, Lr.d.cin,
-                                      Lr.taps, st),
-               "weight_transform");
+      if (!Lr.has_wt) continue;
+      const int k = wb.count++;
+      wb.w[k] = Lr.w;
+      wb.wt[k] = T_(N, i, Lr.o_wt);
+      wb.cout[k] = Lr.d.cout;
+      wb.cin[k] = Lr.d.cin;
+      wb.taps[k] = Lr.taps;
+      if (wb.count == tgpk::kMaxWt || l == hi - 1) {
+        HIPCHK(tgpk::weight_transform_batch(N->dt, wb, st), "weight_transform");
+        wb.count = 0;
+      }
     }
+    if (wb.count > 0) HIPCHK(tgpk::weight_transform_batch(N->dt, wb, st), "weight_transform");
     stale(i) = 0;
     return TGP_OK;
   };
