@@ -363,7 +363,9 @@ tgp_status tgp_profile_clear(void);
  * kernel (default: bits 0-3 set); bit 4 restricts the nine-tap kernel to
  * its four-wave layouts (by default it picks among four- and eight-wave
  * ones), bit 5 makes the row-blocked weight gradient use its four-wave
- * layout at every width. */
+ * layout at every width, bit 6 keeps it at one filter row per work item
+ * (by default micro-batches of four or more samples at widths 96 and 48
+ * take all three filter rows per item). */
 int tgp_debug_set_fwd_variant(int v);
 int tgp_debug_set_rowtile_mask(int m);
 

@@ -917,6 +917,7 @@ extern int g_fwd_split;
 extern int g_rowtile_mask;
 extern int g_rows32_ch;
 extern int g_wgrad_ks;
+extern int g_wgrad_rows3;
 }
 
 extern "C" {
@@ -940,6 +941,7 @@ int tgp_debug_set_rowtile_mask(int v) {
   tgpk::g_rowtile_mask = v;
   tgpk::g_rows32_ch = (v >> 4 & 1) ? 2 : 0;
   tgpk::g_wgrad_ks = (v >> 5 & 1) ? 1 : 0;
+  tgpk::g_wgrad_rows3 = (v >> 6 & 1) ? 0 : 1;
   return old;
 }
 int tgp_debug_set_fwd_order(int v) {

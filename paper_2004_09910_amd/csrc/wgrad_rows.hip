@@ -362,6 +362,219 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
   }
 }
 
+// The same weight gradient with all three filter rows in one item.  The
+// twelve waves of a block are (filter row fr = w / 4, quarter w % 4), three
+// per SIMD, so a stage holds the RPS dZ rows once and the RPS + 2 input rows
+// h - 1 .. h + RPS that the three filter rows read (filter row fr of stage
+// row t reads input block t + fr, an immediate offset).  A stage moves
+// RPS W + (RPS + 2)(W + 4) LDS rows for three filter rows, where the kernel
+// above moves RPS W + RPS (W + 4) for one, and every wave issues its share
+// of the DMA while the two others on its SIMD run MFMAs.  Each wave sums
+// its k steps in order, as the kernel above does with one wave per SIMD.
+template <int W, int RPS, int NS>
+__global__ __launch_bounds__(768) void conv_wgrad_rows3(WgIo io, int ng, int nb, int H, int Cin,
+                                                        int Cout, int R) {
+  constexpr int AR = round32(RPS * W);          // dZ rows per stage
+  constexpr int BW = W + 4;                     // LDS rows per padded input row
+  constexpr int BR = round32((RPS + 2) * BW);   // padded X rows per stage
+  constexpr int SB = (AR + BR) * 128;           // stage bytes
+  constexpr int NW = 12;                        // waves
+  constexpr int AC = AR / 8, BC = BR / 8;       // DMA chunks (8 rows, 1 KiB) per region
+  constexpr int LA = (AC + NW - 1) / NW, LB = (BC + NW - 1) / NW;   // per wave, at most
+  constexpr int KT = RPS * W / 16;              // k steps per stage
+  static_assert(RPS * W % 16 == 0 && W % 8 == 0, "k steps of 16 pixels, halves within a row");
+  static_assert(NS * SB <= 160 * 1024, "LDS ring");
+  static_assert((NS - 2) * (LA + LB) < 64, "vmcnt range");
+  __shared__ __attribute__((aligned(16))) unsigned char smem[NS * SB];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int qw = wave & 3, fr = wave >> 2;      // quarter of the item, filter row
+  const int cw = qw >> 1, nw = qw & 1;          // this wave's co / ci halves
+  const int nct = Cout / 64, ncit = Cin / 64;
+  const bool merged = R == 0;
+  const int nrb = merged ? 1 : (H + R - 1) / R;
+  const int kpg = merged ? 1 : nb * nrb;          // K ranges per micro-batch
+  const int sps = (H + RPS - 1) / RPS;            // stages per sample image (merged)
+  const int per_k = nct * ncit;                   // items per K range
+  const int items = ng * kpg * per_k;
+  const int G = gridDim.x;
+  const int lb = xcd_remap(blockIdx.x, G);
+  const int n_items = lb < items ? (items - lb + G - 1) / G : 0;
+  const long E = (long)Cout * 9 * Cin;
+
+  const int zbytes = nb * H * W * Cout * 2, xbytes = nb * H * W * Cin * 2;
+
+  // DMA lane constants: instruction u of wave w fills chunk c = NW u + w of
+  // the A (dZ) or B (padded X) region, as in the kernel above.  B block rr
+  // of a stage is input row h - 1 + rr.
+  int aoff[LA], arow[LA], boff[LB], brow[LB];
+#pragma unroll
+  for (int u = 0; u < LA; ++u) {
+    const int row = (NW * u + wave) * 8 + (lane >> 3);
+    const int lc = (lane & 7) ^ (2 * (row & 3));
+    const int rr = row / W, w = row - rr * W;
+    const bool ok = row < RPS * W;
+    aoff[u] = ok ? ((rr * W + w) * Cout + 8 * lc) * 2 : WG_OOB;
+    arow[u] = ok ? rr : -1;
+  }
+#pragma unroll
+  for (int u = 0; u < LB; ++u) {
+    const int row = (NW * u + wave) * 8 + (lane >> 3);
+    const int lc = (lane & 7) ^ (2 * (row & 3));
+    const int rr = row / BW, q = row - rr * BW;
+    const bool ok = rr < RPS + 2 && q >= 1 && q <= W;
+    boff[u] = ok ? ((rr * W + q - 1) * Cin + 8 * lc) * 2 : WG_OOB;
+    brow[u] = ok ? rr : -1;
+  }
+  // DMA instructions this wave issues per stage (the waits count them)
+  const int na = (AC - wave + NW - 1) / NW, nbq = (BC - wave + NW - 1) / NW;
+  const int mine = na + nbq;
+  auto wait_ring = [&](int ahead) __attribute__((always_inline)) {
+    if constexpr (AC % NW == 0 && BC % NW == 0) {
+      wait_stages<NS, LA + LB>(ahead);
+    } else {
+      if (mine == LA + LB) wait_stages<NS, LA + LB>(ahead);
+      else if (mine == LA + LB - 1) wait_stages<NS, LA + LB - 1>(ahead);
+      else wait_stages<NS, LA + LB - 2>(ahead);
+    }
+  };
+
+  // Fragment lane constants, as in the kernel above; filter row fr's input
+  // blocks start fr blocks further on.
+  const int g = lane >> 4, j = lane & 15;
+  const int kb = 8 * (g >> 1) + (j >> 2);
+  const int cha = (cw * 32 + 16 * (g & 1) + 4 * (j & 3)) * 2;
+  const int chb = (nw * 32 + 16 * (g & 1) + 4 * (j & 3)) * 2;
+  const int fa = kb * 128 + (((cha >> 4) ^ (2 * (kb & 3))) << 4) + (cha & 15);
+  int fb[3];
+#pragma unroll
+  for (int s = 0; s < 3; ++s)
+    fb[s] = AR * 128 + fr * BW * 128 + (kb + s) * 128 +
+            (((chb >> 4) ^ (2 * ((kb + s) & 3))) << 4) + (chb & 15);
+  auto xoff = [&](int t) __attribute__((always_inline)) {
+    if constexpr (W % 16 == 0) return (16 * t + 4 * ((16 * t) / W)) * 128;
+    else return (16 * t + 4 * ((16 * t + 8 * (g >> 1)) / W)) * 128;
+  };
+
+  auto coords = [&](int it, int& kr, int& co0, int& ci0) __attribute__((always_inline)) {
+    const int item = lb + it * G;
+    kr = item / per_k;
+    const int t = item - kr * per_k;
+    co0 = (t / ncit) * 64;
+    ci0 = (t % ncit) * 64;
+  };
+  auto stages_of = [&](int kr) __attribute__((always_inline)) {
+    if (merged) return nb * sps;
+    const int rb = kr % nrb;
+    const int rows = min(R, H - rb * R);
+    return (rows + RPS - 1) / RPS;
+  };
+
+  int i_it = 0, i_st = 0, i_kr = 0, i_co0 = 0, i_ci0 = 0, i_ns = 0, i_krl = 0;
+  u32x4 rzg = {}, rxg = {};
+  auto issue_item = [&]() __attribute__((always_inline)) {
+    i_ns = stages_of(i_kr);
+    const int gi = i_kr / kpg;
+    i_krl = i_kr - gi * kpg;
+    rzg = make_rsrc(pickg(io.dz, gi), zbytes);
+    rxg = make_rsrc(pickg(io.x, gi), xbytes);
+  };
+  if (n_items > 0) {
+    coords(0, i_kr, i_co0, i_ci0);
+    issue_item();
+  }
+  auto issue = [&](int slot) __attribute__((always_inline)) {
+    const int krl = i_krl;
+    const int n = merged ? i_st / sps : krl / nrb;
+    const int h = merged ? (i_st - (i_st / sps) * sps) * RPS
+                         : (krl - (krl / nrb) * nrb) * R + i_st * RPS;   // first image row
+    const int zsoff = (((n * H + h) * W) * Cout + i_co0) * 2;
+    const int hb = h - 1;                                    // input row of B block 0
+    const int xsoff = (((n * H + hb) * W) * Cin + i_ci0) * 2;
+#pragma unroll
+    for (int u = 0; u < LA; ++u) {
+      const int c = NW * u + wave;
+      if (AC % NW != 0 && c >= AC) continue;                 // wave-uniform
+      auto* dst = TGP_LDS(smem + slot * SB + c * 1024);
+      const bool ok = arow[u] >= 0 && h + arow[u] < H;
+      dma16(rzg, dst, ok ? aoff[u] + zsoff : WG_OOB, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < LB; ++u) {
+      const int c = NW * u + wave;
+      if (BC % NW != 0 && c >= BC) continue;                 // wave-uniform
+      auto* dst = TGP_LDS(smem + slot * SB + AR * 128 + c * 1024);
+      // rows outside the sample's image (above it for h = 0) read zeros; the
+      // row offset can be negative, so it goes into the per-lane offset
+      const bool ok = brow[u] >= 0 && (unsigned)(hb + brow[u]) < (unsigned)H;
+      dma16(rxg, dst, ok ? boff[u] + xsoff : WG_OOB, 0);
+    }
+    if (++i_st == i_ns) {
+      i_st = 0;
+      if (++i_it < n_items) {
+        coords(i_it, i_kr, i_co0, i_ci0);
+        issue_item();
+      }
+    }
+  };
+
+  int total = 0;
+  for (int it = 0; it < n_items; ++it) {
+    int kr, co0, ci0;
+    coords(it, kr, co0, ci0);
+    total += stages_of(kr);
+  }
+
+#pragma unroll
+  for (int k = 0; k < NS - 1; ++k)
+    if (k < total) issue(k);
+
+  int idx = 0;
+  for (int c_it = 0; c_it < n_items; ++c_it) {
+    int kr, co0, ci0;
+    coords(c_it, kr, co0, ci0);
+    const int ns = stages_of(kr);
+    f32x16_t acc[3] = {f32x16_t{}, f32x16_t{}, f32x16_t{}};
+    for (int st = 0; st < ns; ++st, ++idx) {
+      wait_ring(min(NS - 2, total - 1 - idx));
+      ring_barrier();
+      if (idx + NS - 1 < total) issue((idx + NS - 1) % NS);   // the slot freed last stage
+      const unsigned char* sp = smem + (idx % NS) * SB;
+      bf16x8_t a[2], b[2][3];
+      auto load = [&](int t, int buf) __attribute__((always_inline)) {
+        const int ka = 16 * t * 128;
+        const int kx = xoff(t);
+        a[buf] = frag2(tr16(sp + fa + ka), tr16(sp + fa + ka + 4 * 128));
+#pragma unroll
+        for (int s = 0; s < 3; ++s)
+          b[buf][s] = frag2(tr16(sp + fb[s] + kx), tr16(sp + fb[s] + kx + 4 * 128));
+      };
+      load(0, 0);
+#pragma unroll
+      for (int tt = 0; tt < KT; ++tt) {
+        if (tt + 1 < KT) load(tt + 1, (tt + 1) & 1);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int s = 0; s < 3; ++s) acc[s] = mfma32(a[tt & 1], b[tt & 1][s], acc[s]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // epilogue: element v of lane l is co 8 (v / 4) + 4 (l / 32) + v % 4, ci
+    // l % 32 of this wave's quarter, tap (fr, s)
+    const int gi = kr / kpg;
+    float* o = pickg(io.out, gi) + (long)(kr - gi * kpg) * E;
+    const int ci = ci0 + nw * 32 + (lane & 31);
+#pragma unroll
+    for (int s = 0; s < 3; ++s)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int co = co0 + cw * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        o[((long)co * 9 + 3 * fr + s) * Cin + ci] = acc[s][v];
+      }
+  }
+}
+
 struct WgPlan { int R, nK; };   // image rows per K range (0: whole micro-batch), K ranges
 
 }  // namespace
@@ -448,8 +661,36 @@ static hipError_t launch_wgrad_rows_ks(const WgIo& io, int ng, const ConvShape& 
                  : launch_wgrad_rows<W, RPS, NS, 1>(io, ng, s, p, st);
 }
 
+// The three-filter-row kernel, at the widths and micro-batch sizes where it
+// runs (1: where measured faster; 0: never, for measurement and tests).
+int g_wgrad_rows3 = 1;
+static bool use_rows3(const ConvShape& s) {
+  return g_wgrad_rows3 && s.nb >= 4 && (s.W == 96 || s.W == 48);
+}
+
+template <int W, int RPS, int NS>
+static hipError_t launch_wgrad_rows3(const WgIo& io, int ng, const ConvShape& s, const WgPlan& p,
+                                     hipStream_t st) {
+  static_assert(RPS == (W == 96 ? 2 : 4), "the plan's rows per stage");
+  const long items = (long)ng * p.nK * (s.cout / 64) * (s.cin / 64);
+  const int G = (int)(items < 256 ? items : 256);
+  const double flops = 2.0 * ng * s.pixels() * s.cout * 9 * s.cin;
+  const double bytes = ng * (2.0 * s.pixels() * (s.cin + s.cout) + 4.0 * p.nK * s.cout * 9 * s.cin);
+  static char name[48];
+  if (!name[0]) snprintf(name, sizeof name, "conv_wgrad_rows3<%d,%d,%d>", W, RPS, NS);
+  ProfScope ps(name, flops, bytes, st);
+  TGP_LAUNCH(ps, (conv_wgrad_rows3<W, RPS, NS>), dim3(G), dim3(768), 0, st, io, ng, s.nb, s.H,
+             s.cin, s.cout, p.R);
+  return launch_status();
+}
+
 static hipError_t launch_wgrad_rows_w(const WgIo& io, int ng, const ConvShape& s,
                                       const WgPlan& p, hipStream_t st) {
+  if (use_rows3(s)) {
+    if (wgrad_rows_rps(s.W) != (s.W == 96 ? 2 : 4)) return hipErrorInvalidValue;
+    return s.W == 96 ? launch_wgrad_rows3<96, 2, 2>(io, ng, s, p, st)
+                     : launch_wgrad_rows3<48, 4, 2>(io, ng, s, p, st);
+  }
   switch (s.W) {
 #define WG_CASE(i)                                                                           \
   case kWgCfgs[i].W:                                                                         \

@@ -185,6 +185,39 @@ def test_wgrad_rows_four_wave_layout(cin, cout, h, w):
         tgp.debug_set_rowtile_mask(old)
 
 
+@pytest.mark.parametrize("cin,cout,h,w", [(64, 128, 5, 96), (128, 128, 3, 96), (128, 256, 7, 48),
+                                          (256, 256, 4, 48), (512, 256, 2, 48)])
+def test_wgrad_three_filter_rows(cin, cout, h, w):
+    """The weight gradient with all three filter rows per work item (micro-
+    batches of four samples at widths 96 and 48; the last shape takes one K
+    range over the whole micro-batch): against the oracle, and bit for bit
+    the same weight gradient as the one-filter-row kernel in its four-wave
+    layout (forced), which sums each K range in the same order."""
+    import numpy as np
+    import paper_2004_09910_amd as tgp
+    net = one_layer(Layer(CONV3X3, cin, cout), h, w)
+    tgp.profile_enable(True)
+    tgp.profile_read()
+    try:
+        run_and_check(net, (1,), 1, BF16, 8, 2, f"wgrad three rows {cin}->{cout} @{h}x{w}")
+        ran = {k["name"] for k in tgp.profile_read()}
+    finally:
+        tgp.profile_enable(False)
+    assert any(n.startswith("conv_wgrad_rows3<") for n in ran), ran
+    got = gpu_stage(net, BF16, 8, 2, 0, (1,), 1)
+    got["sess"].close()
+    old = tgp.debug_set_rowtile_mask(15 | 32 | 64)
+    try:
+        ref = gpu_stage(net, BF16, 8, 2, 0, (1,), 1)
+    finally:
+        tgp.debug_set_rowtile_mask(old)
+    ref["sess"].close()
+    for idx in got["grads"]:
+        np.testing.assert_array_equal(got["grads"][idx][0], ref["grads"][idx][0])
+        np.testing.assert_array_equal(got["grads"][idx][1], ref["grads"][idx][1])
+    assert torch.equal(got["dx"], ref["dx"])
+
+
 def test_conv1x1_and_depthwise():
     net = one_layer(Layer(CONV1X1, 256, 256), 14, 14)
     run_and_check(net, (1,), 1, BF16, 4, 2, "conv1x1 256->256 @14x14")
