@@ -661,17 +661,24 @@ static hipError_t launch_wgrad_rows_ks(const WgIo& io, int ng, const ConvShape& 
                  : launch_wgrad_rows<W, RPS, NS, 1>(io, ng, s, p, st);
 }
 
-// The three-filter-row kernel, at the widths and micro-batch sizes where it
-// runs (1: where measured faster; 0: never, for measurement and tests).
+// The three-filter-row kernel: its widths with the ring depth that fits
+// (rows per stage as in kWgCfgs), and where it runs: micro-batches of at
+// least kWg3MinNb samples at the widths in kWg3Use (measured faster there).
+// g_wgrad_rows3 = 0 turns it off (measurement and tests).
+struct Wg3Cfg { int W, RPS, NS; };
+constexpr Wg3Cfg kWg3Cfgs[] = {{128, 1, 2}, {96, 2, 2}, {64, 3, 2}, {48, 4, 2},
+                               {32, 6, 2},  {24, 4, 4}, {16, 8, 3}, {8, 8, 4}};
+constexpr int kWg3MinNb = 4;
+constexpr bool wg3_use_width(int W) { return W == 96 || W == 48 || W == 24; }
 int g_wgrad_rows3 = 1;
 static bool use_rows3(const ConvShape& s) {
-  return g_wgrad_rows3 && s.nb >= 4 && (s.W == 96 || s.W == 48);
+  return g_wgrad_rows3 && s.nb >= kWg3MinNb && wg3_use_width(s.W);
 }
 
 template <int W, int RPS, int NS>
 static hipError_t launch_wgrad_rows3(const WgIo& io, int ng, const ConvShape& s, const WgPlan& p,
                                      hipStream_t st) {
-  static_assert(RPS == (W == 96 ? 2 : 4), "the plan's rows per stage");
+  if (wgrad_rows_rps(W) != RPS) return hipErrorInvalidValue;   // the plan's rows per stage
   const long items = (long)ng * p.nK * (s.cout / 64) * (s.cin / 64);
   const int G = (int)(items < 256 ? items : 256);
   const double flops = 2.0 * ng * s.pixels() * s.cout * 9 * s.cin;
@@ -687,9 +694,15 @@ static hipError_t launch_wgrad_rows3(const WgIo& io, int ng, const ConvShape& s,
 static hipError_t launch_wgrad_rows_w(const WgIo& io, int ng, const ConvShape& s,
                                       const WgPlan& p, hipStream_t st) {
   if (use_rows3(s)) {
-    if (wgrad_rows_rps(s.W) != (s.W == 96 ? 2 : 4)) return hipErrorInvalidValue;
-    return s.W == 96 ? launch_wgrad_rows3<96, 2, 2>(io, ng, s, p, st)
-                     : launch_wgrad_rows3<48, 4, 2>(io, ng, s, p, st);
+    switch (s.W) {
+#define WG3_CASE(i)                                                                          \
+  case kWg3Cfgs[i].W:                                                                        \
+    return launch_wgrad_rows3<kWg3Cfgs[i].W, kWg3Cfgs[i].RPS, kWg3Cfgs[i].NS>(io, ng, s, p, st);
+      WG3_CASE(0) WG3_CASE(1) WG3_CASE(2) WG3_CASE(3) WG3_CASE(4) WG3_CASE(5) WG3_CASE(6)
+      WG3_CASE(7)
+#undef WG3_CASE
+      default: return hipErrorInvalidValue;
+    }
   }
   switch (s.W) {
 #define WG_CASE(i)                                                                           \

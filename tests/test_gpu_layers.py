@@ -186,11 +186,13 @@ def test_wgrad_rows_four_wave_layout(cin, cout, h, w):
 
 
 @pytest.mark.parametrize("cin,cout,h,w", [(64, 128, 5, 96), (128, 128, 3, 96), (128, 256, 7, 48),
-                                          (256, 256, 4, 48), (512, 256, 2, 48)])
+                                          (256, 256, 4, 48), (512, 256, 2, 48), (128, 128, 5, 24),
+                                          (256, 512, 3, 24)])
 def test_wgrad_three_filter_rows(cin, cout, h, w):
     """The weight gradient with all three filter rows per work item (micro-
-    batches of four samples at widths 96 and 48; the last shape takes one K
-    range over the whole micro-batch): against the oracle, and bit for bit
+    batches of four samples at widths 96, 48 and 24; 512 -> 256 at 48 and
+    256 -> 512 at 24 take one K range over the whole micro-batch): against
+    the oracle, and bit for bit
     the same weight gradient as the one-filter-row kernel in its four-wave
     layout (forced), which sums each K range in the same order."""
     import numpy as np
