@@ -651,24 +651,30 @@ static hipError_t launch_wgrad_rows(const WgIo& io, int ng, const ConvShape& s, 
 
 template <int W, int RPS, int NS>
 static hipError_t launch_wgrad_rows_ks(const WgIo& io, int ng, const ConvShape& s,
-                                       const WgPlan& p, hipStream_t st) {
+                                       const WgPlan& p, hipStream_t st, bool one_wave) {
   // two waves per SIMD, the phase-1 waves issuing the DMA, pay off where a
   // stage has many k steps (on the U-Net stage: 192 and 48 7-11% faster
   // than with every wave issuing, 96 7% faster than one wave per SIMD; 24
   // 14% slower)
-  const int ks = g_wgrad_ks ? g_wgrad_ks : ((W == 192 || W == 96 || W == 48) ? 2 : 1);
+  const int ks = one_wave ? 1 : g_wgrad_ks ? g_wgrad_ks
+                                           : ((W == 192 || W == 96 || W == 48) ? 2 : 1);
   return ks == 2 ? launch_wgrad_rows<W, RPS, NS, 2>(io, ng, s, p, st)
                  : launch_wgrad_rows<W, RPS, NS, 1>(io, ng, s, p, st);
 }
 
 // The three-filter-row kernel: its widths with the ring depth that fits
-// (rows per stage as in kWgCfgs), and where it runs: micro-batches of at
-// least kWg3MinNb samples at the widths in kWg3Use (measured faster there).
-// g_wgrad_rows3 = 0 turns it off (measurement and tests).
+// (rows per stage as in kWgCfgs), and the shapes it serves: micro-batches
+// of at least kWg3MinNb samples at the widths wg3_use_width names (measured
+// faster there).  It has a third of the one-row kernel's items, so a launch
+// of few micro-batches would leave CUs idle: such a launch runs the one-row
+// kernel with one wave per SIMD instead, which sums every K range in the
+// same order (the same bits).  g_wgrad_rows3 = 0 turns it off (measurement
+// and tests).
 struct Wg3Cfg { int W, RPS, NS; };
 constexpr Wg3Cfg kWg3Cfgs[] = {{128, 1, 2}, {96, 2, 2}, {64, 3, 2}, {48, 4, 2},
                                {32, 6, 2},  {24, 4, 4}, {16, 8, 3}, {8, 8, 4}};
 constexpr int kWg3MinNb = 4;
+constexpr long kWg3MinItems = 128;   // items of a launch below which it runs the one-row kernel
 constexpr bool wg3_use_width(int W) { return W == 96 || W == 48 || W == 24; }
 int g_wgrad_rows3 = 1;
 static bool use_rows3(const ConvShape& s) {
@@ -693,7 +699,8 @@ static hipError_t launch_wgrad_rows3(const WgIo& io, int ng, const ConvShape& s,
 
 static hipError_t launch_wgrad_rows_w(const WgIo& io, int ng, const ConvShape& s,
                                       const WgPlan& p, hipStream_t st) {
-  if (use_rows3(s)) {
+  const bool rows3 = use_rows3(s);
+  if (rows3 && (long)ng * p.nK * (s.cout / 64) * (s.cin / 64) >= kWg3MinItems) {
     switch (s.W) {
 #define WG3_CASE(i)                                                                          \
   case kWg3Cfgs[i].W:                                                                        \
@@ -707,7 +714,8 @@ static hipError_t launch_wgrad_rows_w(const WgIo& io, int ng, const ConvShape& s
   switch (s.W) {
 #define WG_CASE(i)                                                                           \
   case kWgCfgs[i].W:                                                                         \
-    return launch_wgrad_rows_ks<kWgCfgs[i].W, kWgCfgs[i].RPS, kWgCfgs[i].NS>(io, ng, s, p, st);
+    return launch_wgrad_rows_ks<kWgCfgs[i].W, kWgCfgs[i].RPS, kWgCfgs[i].NS>(io, ng, s, p, st, \
+                                                                             rows3);
     WG_CASE(0) WG_CASE(1) WG_CASE(2) WG_CASE(3) WG_CASE(4)
     WG_CASE(5) WG_CASE(6) WG_CASE(7) WG_CASE(8) WG_CASE(9)
 #undef WG_CASE

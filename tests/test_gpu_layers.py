@@ -190,34 +190,41 @@ def test_wgrad_rows_four_wave_layout(cin, cout, h, w):
                                           (256, 512, 3, 24)])
 def test_wgrad_three_filter_rows(cin, cout, h, w):
     """The weight gradient with all three filter rows per work item (micro-
-    batches of four samples at widths 96, 48 and 24; 512 -> 256 at 48 and
-    256 -> 512 at 24 take one K range over the whole micro-batch): against
-    the oracle, and bit for bit
-    the same weight gradient as the one-filter-row kernel in its four-wave
-    layout (forced), which sums each K range in the same order."""
+    batches of four samples at widths 96, 48 and 24, in launches of eight
+    micro-batches; 512 -> 256 at 48 and 256 -> 512 at 24 take one K range
+    over the whole micro-batch): against the oracle, and bit for bit the
+    same weight gradient as the one-filter-row kernel in its four-wave layout
+    (forced), which sums each K range in the same order, and as one
+    micro-batch per launch, which runs that layout by itself."""
     import numpy as np
     import paper_2004_09910_amd as tgp
     net = one_layer(Layer(CONV3X3, cin, cout), h, w)
+    what = f"wgrad three rows {cin}->{cout} @{h}x{w}"
+    say(what)
     tgp.profile_enable(True)
     tgp.profile_read()
     try:
-        run_and_check(net, (1,), 1, BF16, 8, 2, f"wgrad three rows {cin}->{cout} @{h}x{w}")
+        got = gpu_stage(net, BF16, 32, 8, 0, (1,), 1, lanes=8, group=8)
         ran = {k["name"] for k in tgp.profile_read()}
     finally:
         tgp.profile_enable(False)
     assert any(n.startswith("conv_wgrad_rows3<") for n in ran), ran
-    got = gpu_stage(net, BF16, 8, 2, 0, (1,), 1)
+    ref = oracle_stage(net, BF16, got["lo"], got["hi"], got["xv"], got["G"])
+    check_stage(got, ref, BF16, what)
     got["sess"].close()
     old = tgp.debug_set_rowtile_mask(15 | 32 | 64)
     try:
-        ref = gpu_stage(net, BF16, 8, 2, 0, (1,), 1)
+        forced = gpu_stage(net, BF16, 32, 8, 0, (1,), 1, lanes=8, group=8)
     finally:
         tgp.debug_set_rowtile_mask(old)
-    ref["sess"].close()
-    for idx in got["grads"]:
-        np.testing.assert_array_equal(got["grads"][idx][0], ref["grads"][idx][0])
-        np.testing.assert_array_equal(got["grads"][idx][1], ref["grads"][idx][1])
-    assert torch.equal(got["dx"], ref["dx"])
+    forced["sess"].close()
+    single = gpu_stage(net, BF16, 32, 8, 0, (1,), 1)
+    single["sess"].close()
+    for other in (forced, single):
+        for idx in got["grads"]:
+            np.testing.assert_array_equal(got["grads"][idx][0], other["grads"][idx][0])
+            np.testing.assert_array_equal(got["grads"][idx][1], other["grads"][idx][1])
+        assert torch.equal(got["dx"], other["dx"])
 
 
 def test_conv1x1_and_depthwise():
