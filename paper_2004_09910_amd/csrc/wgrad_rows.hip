@@ -95,7 +95,7 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
   constexpr int KT = RPS * W / 16;               // k steps per stage
   static_assert(RPS * W % 16 == 0 && W % 8 == 0, "k steps of 16 pixels, halves within a row");
   static_assert(KT % KS == 0, "k steps shared evenly");
-  static_assert(NW * 2048 <= SB, "exchange of the sums fits a slot");
+  static_assert(NW * 2048 <= SB && (KS != 3 || 8 * 4096 <= SB), "exchange of the sums fits a slot");
   __shared__ __attribute__((aligned(16))) unsigned char smem[NS * SB];
 
   // the wave index is uniform: readfirstlane lets the compiler branch on it
@@ -124,7 +124,7 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
   // chunk lane % 8, which holds logical chunk (lane % 8) ^ (2 (row & 3)).
   // Chunks past a region's end are not issued (wave-uniform).
   const int dwi = KS == 2 ? qw : wave;          // index among the issuing waves
-  const bool issuer = KS == 1 || kh == 1;
+  const bool issuer = KS != 2 || kh == 1;
   int aoff[LA], arow[LA], boff[LB], brow[LB];
 #pragma unroll
   for (int u = 0; u < LA; ++u) {
@@ -287,7 +287,8 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
         const int ka = 16 * t * 128;
         int kx;
         if constexpr (KS == 1) kx = xoff(t);
-        else kx = kh ? xoff(KS * tt + 1) : xoff(KS * tt);
+        else if constexpr (KS == 2) kx = kh ? xoff(KS * tt + 1) : xoff(KS * tt);
+        else kx = xoff(KS * tt + kh);
         a[buf] = frag2(tr16(sp + fa + ka), tr16(sp + fa + ka + 4 * 128));
 #pragma unroll
         for (int s = 0; s < 3; ++s)
@@ -341,6 +342,34 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
       // the exchange reads are done before the slot's refill is issued
       asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     }
+    if constexpr (KS == 3) {
+      // waves kh = 1, 2 of a quarter pass their sums to wave 0 through the
+      // slot just consumed (4 KiB per wave and tap), which adds them in the
+      // order kh = 1, 2
+      f32x4_t* xs = (f32x4_t*)(smem + ((idx - 1) % NS) * SB);
+#pragma unroll
+      for (int s = 0; s < 3; ++s) {
+        lds_handoff_barrier();
+        if (kh) {
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            xs[((kh - 1) * 4 + qw) * 256 + c * 64 + lane] =
+                f32x4_t{acc[s][4 * c], acc[s][4 * c + 1], acc[s][4 * c + 2], acc[s][4 * c + 3]};
+        }
+        lds_handoff_barrier();
+        if (!kh) {
+#pragma unroll
+          for (int p2 = 0; p2 < 2; ++p2)
+#pragma unroll
+            for (int c = 0; c < 4; ++c) {
+              const f32x4_t v = xs[(p2 * 4 + qw) * 256 + c * 64 + lane];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) acc[s][4 * c + e] += v[e];
+            }
+        }
+      }
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    }
     // epilogue: element v of lane l is co 8 (v / 4) + 4 (l / 32) + v % 4, ci
     // l % 32 of this wave's quarter; with KS = 2 wave kh stores v = 8 kh ..
     // 8 kh + 7
@@ -356,9 +385,9 @@ __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int
           o[((long)co * 9 + 3 * r + s) * Cin + ci] = acc[s][v];
         }
     };
-    if (KS == 1) store(0, 16);
-    else if (kh) store(8, 16);
-    else store(0, 8);
+    if (KS == 1 || (KS == 3 && kh == 0)) store(0, 16);
+    else if (KS == 2 && kh) store(8, 16);
+    else if (KS == 2) store(0, 8);
   }
 }
 
@@ -642,7 +671,8 @@ static hipError_t launch_wgrad_rows(const WgIo& io, int ng, const ConvShape& s, 
   const double bytes = ng * (2.0 * s.pixels() * (s.cin + s.cout) + 4.0 * p.nK * s.cout * 9 * s.cin);
   static char name[48];
   if (!name[0])
-    snprintf(name, sizeof name, "conv_wgrad_rows<%d,%d,%d%s>", W, RPS, NS, KS == 2 ? ",8w" : "");
+    snprintf(name, sizeof name, "conv_wgrad_rows<%d,%d,%d%s>", W, RPS, NS,
+             KS == 2 ? ",8w" : KS == 3 ? ",12w" : "");
   ProfScope ps(name, flops, bytes, st);
   TGP_LAUNCH(ps, (conv_wgrad_rows<W, RPS, NS, KS>), dim3(G), dim3(256 * KS), 0, st, io, ng, s.nb,
              s.H, s.cin, s.cout, p.R);
@@ -657,7 +687,9 @@ static hipError_t launch_wgrad_rows_ks(const WgIo& io, int ng, const ConvShape& 
   // than with every wave issuing, 96 7% faster than one wave per SIMD; 24
   // 14% slower)
   const int ks = one_wave ? 1 : g_wgrad_ks ? g_wgrad_ks
-                                           : ((W == 192 || W == 96 || W == 48) ? 2 : 1);
+                                           : W == 192 ? 3 : ((W == 96 || W == 48) ? 2 : 1);
+  if constexpr (W == 192)
+    if (ks == 3) return launch_wgrad_rows<W, RPS, NS, 3>(io, ng, s, p, st);
   return ks == 2 ? launch_wgrad_rows<W, RPS, NS, 2>(io, ng, s, p, st)
                  : launch_wgrad_rows<W, RPS, NS, 1>(io, ng, s, p, st);
 }
