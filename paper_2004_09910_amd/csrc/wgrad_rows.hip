@@ -77,7 +77,9 @@ struct WgIo {
 // KS is the number of waves per SIMD: with KS = 2 the two waves of a SIMD
 // own the same 32 x 32 quarter and take alternate k steps, and the second's
 // sums are added to the first's through LDS before the store, so one wave's
-// MFMAs run while the other waits on its DMA issue or LDS reads.
+// MFMAs run while the other waits on its DMA issue or LDS reads.  With
+// KS = 3 the three take every third k step, all of them issue DMA, and the
+// first adds the second's and then the third's sums before storing.
 template <int W, int RPS, int NS, int KS>
 __global__ __launch_bounds__(256 * KS) void conv_wgrad_rows(WgIo io, int ng, int nb, int H,
                                                             int Cin, int Cout, int R) {
@@ -685,7 +687,7 @@ static hipError_t launch_wgrad_rows_ks(const WgIo& io, int ng, const ConvShape& 
   // two waves per SIMD, the phase-1 waves issuing the DMA, pay off where a
   // stage has many k steps (on the U-Net stage: 192 and 48 7-11% faster
   // than with every wave issuing, 96 7% faster than one wave per SIMD; 24
-  // 14% slower)
+  // 14% slower); at 192 three waves per SIMD are 5% faster again
   const int ks = one_wave ? 1 : g_wgrad_ks ? g_wgrad_ks
                                            : W == 192 ? 3 : ((W == 96 || W == 48) ? 2 : 1);
   if constexpr (W == 192)
