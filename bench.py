@@ -105,13 +105,14 @@ def short_kernel_name(full):
     head = head.split("::")[-1]
     n = (head + sep + tail).replace(" ", "")
     # the wave-layout template argument is named the way the launchers name
-    # their profiling scopes: ",8w" for the eight-wave layouts, else nothing
+    # their profiling scopes: ",8w" / ",12w" for the eight- and twelve-wave
+    # layouts, else nothing
     args = tail.rstrip(">").replace(" ", "").split(",") if sep else []
     if head == "conv3x3_rows32" and len(args) == 6:
         n = (f"{head}<{','.join(args[:4])}{',8w' if args[4] == '1' else ''}"
              f"{',rk' if args[5] != '0' else ''}>")
     elif head == "conv_wgrad_rows" and len(args) == 4:
-        n = f"{head}<{','.join(args[:3])}{',8w' if args[3] == '2' else ''}>"
+        n = f"{head}<{','.join(args[:3])}{ {'2': ',8w', '3': ',12w'}.get(args[3], '')}>"
     return n
 
 
