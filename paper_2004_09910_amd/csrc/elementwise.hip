@@ -280,11 +280,18 @@ __global__ __launch_bounds__(256) void dw_dgrad_k(const T* __restrict__ dz, cons
 // gradient (dx = dz correlated with the flipped filter); the sum runs over
 // the window in row-major order.
 // gridDim.z (1 .. kMaxGroup) micro-batches: blockIdx.z selects x[k] / y[k].
+// MASK (data gradient only): the result stored is the ReLU backward of the
+// layer below, whose output m[k] masks it (its dz), and the block's column
+// sums of the stored values go to part[k] (row blockIdx.y gridDim.x +
+// blockIdx.x, C floats): that layer's bias-gradient partials.  It needs every
+// thread of a block inside the image (W C / 8 a multiple of 256).
 struct DwIo {
   const bf16_t* x[kMaxGroup];
   bf16_t* y[kMaxGroup];
+  const bf16_t* m[kMaxGroup];
+  float* part[kMaxGroup];
 };
-template <int RS, bool FLIP>
+template <int RS, bool FLIP, bool MASK = false>
 __global__ __launch_bounds__(256) void dw3_rows_k(DwIo io, const bf16_t* __restrict__ w,
                                                   const float* __restrict__ b, int H, int W, int C,
                                                   int relu) {
@@ -331,6 +338,7 @@ __global__ __launch_bounds__(256) void dw3_rows_k(DwIo io, const bf16_t* __restr
     win[2][s] = ld(h0 + 1, wc + s - 1);
   }
   const int h1 = min(h0 + RS, H);
+  float bsum[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};   // MASK: this thread's column sums
   for (int h = h0; h < h1; ++h) {
 #pragma unroll
     for (int s = 0; s < 3; ++s) nxt[s] = ld(h + 2, wc + s - 1);
@@ -351,12 +359,45 @@ __global__ __launch_bounds__(256) void dw3_rows_k(DwIo io, const bf16_t* __restr
       acc[i] += bias[i];
       if (relu) acc[i] = fmaxf(acc[i], 0.f);
     }
-    st16(y + (long)n * H * W * C + ((long)h * W + wc) * C + cp * 8, Pk<bf16_t>::pk(acc));
+    const long eo = (long)n * H * W * C + ((long)h * W + wc) * C + cp * 8;
+    if constexpr (MASK) {
+      float mv[8];
+      Pk<bf16_t>::un(ld16(pickg(io.m, blockIdx.z) + eo), mv);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) acc[i] = mv[i] > 0.f ? acc[i] : 0.f;
+      const uint4 o = Pk<bf16_t>::pk(acc);
+      st16(y + eo, o);
+      Pk<bf16_t>::un(o, acc);   // the bias gradient sums the stored (rounded) dz
+#pragma unroll
+      for (int i = 0; i < 8; ++i) bsum[i] += acc[i];
+    } else {
+      st16(y + eo, Pk<bf16_t>::pk(acc));
+    }
 #pragma unroll
     for (int s = 0; s < 3; ++s) {
       win[0][s] = win[1][s];
       win[1][s] = win[2][s];
       win[2][s] = nxt[s];
+    }
+  }
+  if constexpr (MASK) {
+    // the block's column sums: lanes of one channel pack added in order of
+    // their column
+    __shared__ float red[256 * 8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) red[threadIdx.x * 8 + i] = bsum[i];
+    __syncthreads();
+    if ((int)threadIdx.x < CP) {
+      float s8[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) s8[i] = red[threadIdx.x * 8 + i];
+      for (int l = 1; l < 256 / CP; ++l)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) s8[i] += red[(l * CP + threadIdx.x) * 8 + i];
+      float* pr = pickg(io.part, blockIdx.z) + ((long)blockIdx.y * gridDim.x + blockIdx.x) * C +
+                  cp * 8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) pr[i] = s8[i];
     }
   }
 }
@@ -1212,6 +1253,37 @@ hipError_t dw_dgrad_n(int n, const void* const* dz, const void* w, void* const* 
   const dim3 g((unsigned)cdiv((long)W * (C / 8), 256), (unsigned)(nb * cdiv(H, kDwRows)), n);
   ProfScope ps("dw3_rows_dgrad", n * 18.0 * P * C, n * 4.0 * P * C, st);
   TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, true>), g, dim3(256), 0, st, io, (const bf16_t*)w,
+             (const float*)nullptr, H, W, C, 0);
+  return launch_status();
+}
+
+bool dw_dgrad_mask_ok(int nb, int H, int W, int C) {
+  return C % 8 == 0 && 256 % (C / 8) == 0 && (long)W * (C / 8) % 256 == 0 &&
+         (long)nb * cdiv(H, kDwRows) <= 65535 && 2.0 * nb * H * W * C < 2147483648.0;
+}
+
+int dw_dgrad_mask_rows(int nb, int H, int W, int C) {
+  return (int)((long)W * (C / 8) / 256 * nb * cdiv(H, kDwRows));
+}
+
+hipError_t dw_dgrad_mask_n(int n, const void* const* dz, const void* w, void* const* dx,
+                           const void* const* y, float* const* part, int nb, int H, int W, int C,
+                           hipStream_t st) {
+  if (n < 1 || n > kMaxGroup || !dw_dgrad_mask_ok(nb, H, W, C)) return hipErrorInvalidValue;
+  const long P = (long)nb * H * W;
+  if (P == 0) return hipSuccess;
+  DwIo io;
+  for (int k = 0; k < kMaxGroup; ++k) {
+    const int q = k < n ? k : 0;
+    io.x[k] = (const bf16_t*)dz[q];
+    io.y[k] = (bf16_t*)dx[q];
+    io.m[k] = (const bf16_t*)y[q];
+    io.part[k] = part[q];
+    if (!io.x[k] || !io.y[k] || !io.m[k] || !io.part[k]) return hipErrorInvalidValue;
+  }
+  const dim3 g((unsigned)((long)W * (C / 8) / 256), (unsigned)(nb * cdiv(H, kDwRows)), n);
+  ProfScope ps("dw3_rows_dgrad_mask", n * 18.0 * P * C, n * 6.0 * P * C, st);
+  TGP_LAUNCH(ps, (dw3_rows_k<kDwRows, true, true>), g, dim3(256), 0, st, io, (const bf16_t*)w,
              (const float*)nullptr, H, W, C, 0);
   return launch_status();
 }

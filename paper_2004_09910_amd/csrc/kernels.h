@@ -133,6 +133,15 @@ hipError_t dw_forward_n(int n, const void* const* x, const void* w, const float*
                         void* const* y, int nb, int H, int W, int C, int relu, hipStream_t st);
 hipError_t dw_dgrad_n(int n, const void* const* dz, const void* w, void* const* dx, int nb,
                       int H, int W, int C, hipStream_t st);
+// dw_dgrad_n whose stored result is the ReLU backward of the layer below
+// (dz = dx where its output y > 0, else 0) and whose blocks leave that
+// layer's bias-gradient column sums in part[k] (dw_dgrad_mask_rows rows of
+// C floats, summed later in a fixed order); where dw_dgrad_mask_ok holds.
+bool dw_dgrad_mask_ok(int nb, int H, int W, int C);
+int dw_dgrad_mask_rows(int nb, int H, int W, int C);
+hipError_t dw_dgrad_mask_n(int n, const void* const* dz, const void* w, void* const* dx,
+                           const void* const* y, float* const* part, int nb, int H, int W, int C,
+                           hipStream_t st);
 hipError_t dw_wgrad_n(int n, const void* const* x, const void* const* dz, float* const* dw,
                       float* const* part, int nb, int H, int W, int C, hipStream_t st,
                       ReduceJob* const* defer = nullptr);

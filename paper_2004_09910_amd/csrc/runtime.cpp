@@ -88,6 +88,9 @@ struct LayerRt {
   bool defer_w = false, defer_b = false;   // partials kept for the accumulation
   std::vector<size_t> o_sto_out, o_sto_pro;  // per stored set
   bool has_wt = false;
+  // mask_below: this (depthwise) layer's data gradient is stored as the ReLU
+  // backward of the layer below, with that layer's bias column sums
+  bool mask_below = false;
 };
 
 }  // namespace
@@ -379,6 +382,10 @@ struct BwdMb {
   // is left to layer l's ReLU backward (dy then names the buffer it would
   // have filled)
   const void* dy_pool = nullptr;
+  // dy is already this layer's dz, and its bias column sums (dz_rows rows)
+  // are in its column slot (layer l + 1's masked data gradient)
+  bool dz_ready = false;
+  int dz_rows = 0;
 };
 
 // F' (where checkpointed) and B for a group of cnt (1 .. MG) micro-batches
@@ -497,6 +504,13 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
       // column partials: kept in the slot, or (too large to keep) reduced at once
       bpartk[k] = Lr.defer_b ? (float*)G_(N, i, Lr.o_gcol) : B.colpart;
       bdeferk[k] = Lr.defer_b ? &pj[1] : nullptr;
+      if (B.dz_ready) {
+        // layer l + 1's data gradient stored this layer's dz and its bias
+        // column sums: no ReLU backward here
+        dzk[k] = B.dy;
+        pj[1] = tgpk::ReduceJob{bpartk[k], gbk[k], (long)d.cout, B.dz_rows};
+        B.dz_ready = false;
+      }
     }
     // The fused kernels take the whole group in one launch when every
     // micro-batch qualifies (they always do together: same shape and flags,
@@ -639,7 +653,26 @@ tgp_status run_backward_g(tgp_net* N, int j, int cnt, const int* iv,
     for (int k = 0; k < cnt; ++k)
       dw_drows = dw_drows && tgpk::dw_rows_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, dzk[k],
                                               dgrad_out[k], Lr.w);
-    if (dw_drows) {
+    // the ReLU backward of layer l - 1 folded into this data gradient (planned
+    // when it applies; the tensors' alignment is checked here)
+    bool masked = Lr.mask_below && l > lo && d.prologue == TGP_PRO_NONE;
+    const void* masks[MG];
+    float* mparts[MG];
+    for (int k = 0; k < cnt && masked; ++k) {
+      masks[k] = M[k].v.out[l - 1 - lo];
+      mparts[k] = (float*)G_(N, M[k].i, N->L[l - 1].o_gcol);
+      masked = tgpk::dw_rows_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, dzk[k], dgrad_out[k], Lr.w) &&
+               tgpk::dw_rows_ok(N->dt, N->b, Lr.H, Lr.W, d.cout, masks[k], dgrad_out[k], Lr.w);
+    }
+    if (masked) {
+      HIPCHK(tgpk::dw_dgrad_mask_n(cnt, dzk, Lr.w, dgrad_out, masks, mparts, N->b, Lr.H, Lr.W,
+                                   d.cout, st),
+             "dw_dgrad_mask");
+      for (int k = 0; k < cnt; ++k) {
+        M[k].dz_ready = true;
+        M[k].dz_rows = tgpk::dw_dgrad_mask_rows(N->b, Lr.H, Lr.W, d.cout);
+      }
+    } else if (dw_drows) {
       HIPCHK(tgpk::dw_dgrad_n(cnt, dzk, Lr.w, dgrad_out, N->b, Lr.H, Lr.W, d.cout, st), "dw_dgrad");
     } else if (d.kind == TGP_DWCONV3X3) {
       for (int k = 0; k < cnt; ++k)
@@ -1182,7 +1215,30 @@ tgp_status tgp_plan(tgp_net* N, int B, int m, int mode, size_t* bytes) {
       else max_part = std::max(max_part, pf);
     }
     Lr.o_gcol_floats = Lr.d.bias ? tgpk::relu_bias_partial_floats(N->dt, P, Lr.d.cout) : 0;
+    {
+      // this layer's ReLU backward folded into the data gradient of a
+      // depthwise layer above it in the partition (bf16, no prologue there,
+      // no skip here); its column slot then holds that kernel's sums too
+      const int li = (int)(&Lr - &N->L[0]);
+      if (li + 1 < (int)N->L.size()) {
+        LayerRt& U = N->L[li + 1];
+        U.mask_below = N->dt == TGP_BF16 && U.part == Lr.part &&
+                       U.d.kind == TGP_DWCONV3X3 && U.d.prologue == TGP_PRO_NONE &&
+                       Lr.d.relu && Lr.d.bias && Lr.d.stash_id < 0 && Lr.o_gcol_floats &&
+                       U.H == Lr.H && U.W == Lr.W && U.d.cin == Lr.d.cout &&
+                       tgpk::dw_dgrad_mask_ok(N->b, U.H, U.W, U.d.cout);
+        if (U.mask_below)
+          Lr.o_gcol_floats = std::max<size_t>(
+              Lr.o_gcol_floats,
+              (size_t)tgpk::dw_dgrad_mask_rows(N->b, U.H, U.W, U.d.cout) * Lr.d.cout);
+      }
+    }
     Lr.defer_b = Lr.o_gcol_floats && Lr.o_gcol_floats * 4 <= kDeferBytes;
+    {
+      const size_t li = (size_t)(&Lr - &N->L[0]);
+      if (li + 1 < N->L.size() && N->L[li + 1].mask_below && !Lr.defer_b)
+        N->L[li + 1].mask_below = false;   // its sums need the slot
+    }
     Lr.o_gcol = Lr.defer_b ? takeG(Lr.o_gcol_floats * 4) : 0;
     if (Lr.o_gcol_floats && !Lr.defer_b) max_col = std::max(max_col, Lr.o_gcol_floats);
     max_col = std::max(max_col, tgpk::colsum_partial_floats(P, Lr.d.cout));
