@@ -364,8 +364,9 @@ tgp_status tgp_profile_clear(void);
  * its four-wave layouts (by default it picks among four- and eight-wave
  * ones), bit 5 makes the row-blocked weight gradient use its four-wave
  * layout at every width, bit 6 keeps it at one filter row per work item
- * (by default micro-batches of four or more samples at widths 96 and 48
- * take all three filter rows per item). */
+ * (by default launches of several micro-batches of four or more samples at
+ * widths 96, 48 and 24 take all three filter rows per item; the values are
+ * the same either way). */
 int tgp_debug_set_fwd_variant(int v);
 int tgp_debug_set_rowtile_mask(int m);
 
