@@ -365,8 +365,8 @@ tgp_status tgp_profile_clear(void);
  * ones), bit 5 makes the row-blocked weight gradient use its four-wave
  * layout at every width, bit 6 keeps it at one filter row per work item
  * (by default launches of several micro-batches of four or more samples at
- * widths 96, 48 and 24 take all three filter rows per item; the values are
- * the same either way). */
+ * widths 96, 48 and 24 take all three filter rows per item, with the values
+ * of the four-wave layout). */
 int tgp_debug_set_fwd_variant(int v);
 int tgp_debug_set_rowtile_mask(int m);
 
