@@ -218,7 +218,9 @@ tgp_status tgp_stage_forward(tgp_net* net, int j, int i, int checkpoint, const v
  * gradient found in theirs.  The weight gradient g_i^j is left for
  * tgp_grad_accumulate, as partial sums over pixel ranges in the workspace.
  * Order (Sec. 2.1): for a given j, i = m, m-1, .., 1, each after F_{i,j}
- * and after tgp_grad_accumulate(j, i+1); ESTATE otherwise. */
+ * and after B_{i+1,j}; with one shared gradient slot (one lane, or a plan
+ * without per-micro-batch slots) also after tgp_grad_accumulate(j, i+1);
+ * ESTATE otherwise.  The accumulations still run in the order i = m..1. */
 tgp_status tgp_stage_backward_recompute(tgp_net* net, int j, int i, const void* dy_out,
                                         void* dx_in, void* stream);
 

@@ -801,6 +801,14 @@ tgp_status run_accumulate_g(tgp_net* N, int j, int i0, int cnt, int overwrite, h
   return TGP_OK;
 }
 
+// B_{i,j} may run once B_{i+1,j} has: with one gradient slot per
+// micro-batch its accumulation may come later (the slots are distinct),
+// with a shared slot it must have run (B_{i,j} overwrites the slot).
+bool follows_ok(const tgp_net* N, int i, int j) {
+  const int s = N->st[cell(N, i + 1, j)];
+  return s == ACC || (s == BWD && N->gslots >= N->m);
+}
+
 // Plan and workspace present, and the layers of partition j (all partitions
 // for j = 0) bound.
 tgp_status check_ready(const tgp_net* N, int j = 0) {
@@ -934,8 +942,25 @@ struct GpuExec : Exec {
     HIPCHK(hipStreamWaitEvent(acc, lane_ev[k], 0), "hipStreamWaitEvent");
     return TGP_OK;
   }
+  // With a gradient slot per micro-batch (K > 1), the accumulations of
+  // partition j are issued in groups of up to kAccGroup consecutive
+  // micro-batches (i0 down to i0 - count + 1, the schedule's order), one
+  // launch each: every g^j is read and written once per group, with the
+  // values of one accumulation per micro-batch.
+  static constexpr int kAccGroup = 8;
+  std::vector<int> acc_top, acc_cnt;
   tgp_status accumulate(int i, int j, bool ow) override {
-    return tgp_grad_accumulate(N, j, i, ow ? 1 : 0, K > 1 ? acc : st);
+    if (K == 1 || N->gslots < N->m) return tgp_grad_accumulate(N, j, i, ow ? 1 : 0, K > 1 ? acc : st);
+    if (acc_cnt.size() < (size_t)N->n + 1) {
+      acc_top.assign(N->n + 1, 0);
+      acc_cnt.assign(N->n + 1, 0);
+    }
+    if (acc_cnt[j] == 0) acc_top[j] = i;
+    ++acc_cnt[j];
+    if (acc_cnt[j] < kAccGroup && i > 1) return TGP_OK;
+    const int top = acc_top[j], cnt = acc_cnt[j];
+    acc_cnt[j] = 0;
+    return tgp_grad_accumulate_n(N, j, top, cnt, top == N->m ? 1 : 0, acc);
   }
 };
 
@@ -1460,8 +1485,9 @@ tgp_status tgp_stage_backward_recompute(tgp_net* N, int j, int i, const void* dy
   if ((r = check_slices(N, j, dx_in, dy_out)) != TGP_OK) return r;
   int c = cell(N, i, j);
   if (N->st[c] != FWD) return fail(TGP_ESTATE, "B_{%d,%d} needs F_{%d,%d} first", i, j, i, j);
-  if (i < N->m && N->st[cell(N, i + 1, j)] != ACC)
-    return fail(TGP_ESTATE, "B_{%d,%d} must follow B_{%d,%d} and its accumulation", i, j, i + 1, j);
+  if (i < N->m && !follows_ok(N, i, j))
+    return fail(TGP_ESTATE, "B_{%d,%d} must follow B_{%d,%d}%s", i, j, i + 1, j,
+                N->gslots < N->m ? " and its accumulation" : "");
   r = run_backward(N, j, i, dy_out, dx_in, S(stream));
   if (r != TGP_OK) return r;
   N->st[c] = BWD;
@@ -1548,8 +1574,9 @@ tgp_status tgp_stage_backward_recompute_n(tgp_net* N, int j, int i0, int count,
   for (int k = 0; k < count; ++k)
     if (N->st[cell(N, iv[k], j)] != FWD)
       return fail(TGP_ESTATE, "B_{%d,%d} needs F_{%d,%d} first", iv[k], j, iv[k], j);
-  if (i0 < N->m && N->st[cell(N, i0 + 1, j)] != ACC)
-    return fail(TGP_ESTATE, "B_{%d,%d} must follow B_{%d,%d} and its accumulation", i0, j, i0 + 1, j);
+  if (i0 < N->m && !follows_ok(N, i0, j))
+    return fail(TGP_ESTATE, "B_{%d,%d} must follow B_{%d,%d}%s", i0, j, i0 + 1, j,
+                N->gslots < N->m ? " and its accumulation" : "");
   r = run_backward_g(N, j, count, iv, dy_out, dx_in, S(stream));
   if (r != TGP_OK) return r;
   for (int k = 0; k < count; ++k) N->st[cell(N, iv[k], j)] = BWD;
