@@ -948,14 +948,16 @@ __global__ __launch_bounds__(256) void accumulate_k(float* __restrict__ acc, con
 // entry in one launch.  Tiles blk0[k] .. blk0[k + 1] - 1 serve entry k.  A
 // tile of 1024 threads covers C4 float4 columns with LANES = 1024 / C4
 // split lanes; lane l sums s = l, l + LANES, .. in ascending order, then the
-// lanes are added in order 0 .. LANES - 1, with (C4, LANES) a function of S
-// only, so the sum is fixed by the shape.  An entry with n not a multiple of
-// 4 takes one element per thread, s ascending.
+// lanes are added pairwise in LDS (lane l takes lane l + h for h = LANES / 2,
+// .., 1), with (C4, LANES) a function of S only, so the sum is fixed by the
+// shape.  An entry with n not a multiple of 4 takes one element per thread,
+// s ascending.
 __host__ __device__ __forceinline__ int acc_c4(int S) {
   // about four slices per split lane: C4 = 4096 / S rounded down to a power
-  // of two, within 16 .. 1024
+  // of two, within 1 .. 1024 (a bias gradient's hundreds of block sums then
+  // spread over several tiles instead of one long one)
   int c = 1024;
-  while (c > 16 && (long)c * S > 4096) c >>= 1;
+  while (c > 1 && (long)c * S > 4096) c >>= 1;
   return c;
 }
 
@@ -1013,12 +1015,13 @@ __global__ __launch_bounds__(1024) void reduce_accumulate_k(AccBatch b, int over
       if (LANES > 1) {   // tile-uniform
         red[lane * C4 + col] = a;
         __syncthreads();
-        if (lane == 0) {
-          r = red[col];
-          for (int l = 1; l < LANES; ++l) {
-            const float4 t = red[l * C4 + col];
+        for (int h = LANES >> 1; h > 0; h >>= 1) {
+          if (lane < h) {
+            const float4 t = red[(lane + h) * C4 + col];
             r.x += t.x; r.y += t.y; r.z += t.z; r.w += t.w;
+            red[lane * C4 + col] = r;
           }
+          __syncthreads();
         }
         if (NG != 1) __syncthreads();   // red is rewritten by the next micro-batch
       }
