@@ -961,15 +961,6 @@ __host__ __device__ __forceinline__ int acc_c4(int S) {
   return c;
 }
 
-// Barrier for LDS hand-offs only: this wave's LDS accesses have completed
-// when it arrives, global loads in flight stay in flight, and the compiler
-// moves no memory access across it.
-__device__ __forceinline__ void acc_lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
-
 // NG: micro-batches per entry as a template constant (1) or b.ng (0).
 template <int NG>
 __global__ __launch_bounds__(1024) void reduce_accumulate_k(AccBatch b, int overwrite,
@@ -1002,49 +993,39 @@ __global__ __launch_bounds__(1024) void reduce_accumulate_k(AccBatch b, int over
     const int C4 = acc_c4(S), LANES = 1024 / C4;
     const int col = threadIdx.x % C4, lane = threadIdx.x / C4;
     const long e4 = (bx * C4 + col) * 4;
-    const bool live = e4 < E;
     float4 cur = make_float4(0.f, 0.f, 0.f, 0.f);   // the running sum (lane 0)
-    // slices lane + u LANES, u < 8, of micro-batch q (past S: zeros); the
-    // next micro-batch's are issued before this one's lanes meet in LDS
-    float4 t[8];
-    auto first = [&](int q) {
-      const float* __restrict__ part = b.g[k] + q * b.gstride[k];
-#pragma unroll
-      for (int u = 0; u < 8; ++u)
-        t[u] = live && lane + u * LANES < S
-                   ? *(const float4*)(part + (long)(lane + u * LANES) * E + e4)
-                   : make_float4(0.f, 0.f, 0.f, 0.f);
-    };
-    first(0);
     for (int q = 0; q < ng; ++q) {
       const float* __restrict__ part = b.g[k] + q * b.gstride[k];
       float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (e4 < E) {
+        // up to eight loads in flight per step; slices past S add zeros
+        for (int s = lane; s < S; s += 8 * LANES) {
+          float4 t[8];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        a.x += t[u].x; a.y += t[u].y; a.z += t[u].z; a.w += t[u].w;
-      }
-      if (live) {   // slices past 8 LANES (S above 8192 only: C4 * S <= 4096 for C4 > 1)
-        for (int s = lane + 8 * LANES; s < S; s += LANES) {
-          const float4 v = *(const float4*)(part + (long)s * E + e4);
-          a.x += v.x; a.y += v.y; a.z += v.z; a.w += v.w;
+          for (int u = 0; u < 8; ++u)
+            t[u] = s + u * LANES < S ? *(const float4*)(part + (long)(s + u * LANES) * E + e4)
+                                     : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            a.x += t[u].x; a.y += t[u].y; a.z += t[u].z; a.w += t[u].w;
+          }
         }
       }
-      if (q + 1 < ng) first(q + 1);
       float4 r = a;
-      if (LANES > 1) {   // tile-uniform; LDS-only barriers keep the loads above in flight
+      if (LANES > 1) {   // tile-uniform
         red[lane * C4 + col] = a;
-        acc_lds_barrier();
+        __syncthreads();
         for (int h = LANES >> 1; h > 0; h >>= 1) {
           if (lane < h) {
-            const float4 w = red[(lane + h) * C4 + col];
-            r.x += w.x; r.y += w.y; r.z += w.z; r.w += w.w;
+            const float4 t = red[(lane + h) * C4 + col];
+            r.x += t.x; r.y += t.y; r.z += t.z; r.w += t.w;
             red[lane * C4 + col] = r;
           }
-          acc_lds_barrier();
+          __syncthreads();
         }
-        if (NG != 1) acc_lds_barrier();   // red is rewritten by the next micro-batch
+        if (NG != 1) __syncthreads();   // red is rewritten by the next micro-batch
       }
-      if (lane == 0 && live) {
+      if (lane == 0 && e4 < E) {
         if (q > 0) {
           cur.x = cur.x + r.x; cur.y = cur.y + r.y; cur.z = cur.z + r.z; cur.w = cur.w + r.w;
         } else if (overwrite) {
@@ -1056,7 +1037,7 @@ __global__ __launch_bounds__(1024) void reduce_accumulate_k(AccBatch b, int over
       }
     }
     if (lane == 0 && e4 < E) *(float4*)(acc + e4) = cur;
-    if (NG == 1 && LANES > 1) acc_lds_barrier();   // red is rewritten by the next tile
+    if (NG == 1 && LANES > 1) __syncthreads();   // red is rewritten by the next tile
   }
 }
 
